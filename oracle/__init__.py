@@ -1,0 +1,12 @@
+"""CPU oracle (float64 NumPy) of the decoder forward pass.
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()``
+and the ``cpu_baseline`` leg of ``bench.py``; never by the product path.
+"""
+from .decoder import (OracleDecoder, apply_rope, causal_gqa_attention, generate_greedy,
+                      greedy, rms_norm, rope_cos_sin, rope_inv_freq, round_to_bf16,
+                      round_to_f32, silu, softmax, swiglu_mlp, teacher_forced)
+
+__all__ = ["OracleDecoder", "apply_rope", "causal_gqa_attention", "generate_greedy", "greedy",
+           "rms_norm", "rope_cos_sin", "rope_inv_freq", "round_to_bf16", "round_to_f32",
+           "silu", "softmax", "swiglu_mlp", "teacher_forced"]

@@ -1,0 +1,330 @@
+"""Pins of the CPU oracle to facts outside itself.
+
+Each test checks the oracle against a closed form, an invariant of the model
+family, brute force on tiny inputs, or an independent library routine (torch's
+RMSNorm/SiLU/SDPA, HF transformers' Llama and Qwen2 causal LMs in float64), so
+that a dropped term, a wrong sign or index, or a transposed operand anywhere in
+the oracle fails at least one of them.  CPU only.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.decoder import OracleDecoder, generate_greedy, teacher_forced
+from synthetic import model_weights, small_shape
+
+RNG = np.random.default_rng(1234)
+
+
+# ----------------------------------------------------------------- RMSNorm
+
+def test_rmsnorm_constant_row_closed_form():
+    c, eps = 0.37, 1e-5
+    g = RNG.standard_normal(8)
+    x = np.full((3, 8), c)
+    np.testing.assert_allclose(oracle.rms_norm(x, g, eps), np.broadcast_to(g * c / math.sqrt(c * c + eps), (3, 8)),
+                               rtol=1e-14)
+
+
+def test_rmsnorm_matches_torch_and_is_scale_invariant():
+    x = RNG.standard_normal((5, 64))
+    g = 1 + 0.1 * RNG.standard_normal(64)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (64,), weight=torch.from_numpy(g), eps=1e-6)
+    np.testing.assert_allclose(oracle.rms_norm(x, g, 1e-6), ref.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.rms_norm(7.5 * x, g, 0.0), oracle.rms_norm(x, g, 0.0), rtol=1e-12)
+    # eps matters: a tiny-magnitude row is not blown up to unit RMS
+    tiny = 1e-4 * x[:1]
+    assert np.sqrt(np.mean(oracle.rms_norm(tiny, np.ones(64), 1e-5) ** 2)) < 0.1
+
+
+# ----------------------------------------------------------------- RoPE
+
+def _rot(x, pos, hd, theta=10000.0):
+    c, s = oracle.rope_cos_sin(np.asarray(pos), hd, theta)
+    return oracle.apply_rope(x, c, s)
+
+
+def test_rope_identities():
+    hd = 16
+    q = RNG.standard_normal((1, 1, hd))
+    k = RNG.standard_normal((1, 1, hd))
+    np.testing.assert_allclose(_rot(q, [0], hd), q, rtol=0, atol=0)
+    for m in (1, 5, 123, 4000):
+        np.testing.assert_allclose(np.linalg.norm(_rot(q, [m], hd)), np.linalg.norm(q), rtol=1e-13)
+    # R(m) R(n) = R(m + n)
+    np.testing.assert_allclose(_rot(_rot(q, [7], hd), [11], hd), _rot(q, [18], hd), atol=1e-13)
+    # <R(m) q, R(n) k> = <R(m - n) q, k>
+    for m, n in ((9, 4), (100, 37), (4096, 17)):
+        lhs = np.sum(_rot(q, [m], hd) * _rot(k, [n], hd))
+        rhs = np.sum(_rot(q, [m - n], hd) * k)
+        assert abs(lhs - rhs) < 1e-11 * max(1.0, abs(lhs))
+
+
+def test_rope_matches_transformers_rotate_half():
+    """Pairing (i, i + HD/2) and inv_freq = theta^(-2i/HD), as HF's Llama."""
+    from transformers.models.llama.modeling_llama import apply_rotary_pos_emb
+    hd, theta = 32, 500000.0
+    S = 9
+    pos = np.arange(3, 3 + S)
+    q = RNG.standard_normal((S, 2, hd))
+    k = RNG.standard_normal((S, 1, hd))
+    inv = theta ** (-np.arange(0, hd, 2, dtype=np.float64) / hd)
+    ang = np.outer(pos, inv)
+    emb = np.concatenate([ang, ang], axis=-1)
+    cos, sin = torch.from_numpy(np.cos(emb))[None], torch.from_numpy(np.sin(emb))[None]
+    qt = torch.from_numpy(q).permute(1, 0, 2)[None]
+    kt = torch.from_numpy(k).permute(1, 0, 2)[None]
+    qr, kr = apply_rotary_pos_emb(qt, kt, cos, sin)
+    np.testing.assert_allclose(_rot(q, pos, hd, theta), qr[0].permute(1, 0, 2).numpy(), atol=1e-13)
+    np.testing.assert_allclose(_rot(k, pos, hd, theta), kr[0].permute(1, 0, 2).numpy(), atol=1e-13)
+
+
+# ----------------------------------------------------------------- attention
+
+def _brute_attention(q, k, v, q_pos):
+    """Explicit loops, one query and head at a time (MHA/GQA by index math)."""
+    sq, H, hd = q.shape
+    KV = k.shape[1]
+    out = np.zeros_like(q)
+    for i in range(sq):
+        for h in range(H):
+            kvh = h * KV // H
+            scores = []
+            for j in range(q_pos[i] + 1):
+                scores.append(sum(q[i, h, d] * k[j, kvh, d] for d in range(hd)) / math.sqrt(hd))
+            m = max(scores)
+            e = [math.exp(s - m) for s in scores]
+            z = sum(e)
+            for d in range(hd):
+                out[i, h, d] = sum(e[j] / z * v[j, kvh, d] for j in range(len(e)))
+    return out
+
+
+@pytest.mark.parametrize("H,KV,sq,sk", [(4, 2, 5, 9), (3, 3, 4, 4), (6, 2, 1, 7), (2, 1, 9, 9)])
+def test_attention_brute_force(H, KV, sq, sk):
+    hd = 8
+    q = RNG.standard_normal((sq, H, hd))
+    k = RNG.standard_normal((sk, KV, hd))
+    v = RNG.standard_normal((sk, KV, hd))
+    q_pos = np.arange(sk - sq, sk)
+    np.testing.assert_allclose(oracle.causal_gqa_attention(q, k, v, q_pos),
+                               _brute_attention(q, k, v, q_pos), atol=1e-12)
+
+
+def test_softmax_rows_sum_to_one_and_special_cases():
+    s = RNG.standard_normal((6, 11)) * 30
+    s[:, 7:] = -np.inf
+    p = oracle.softmax(s)
+    assert np.all(np.abs(p.sum(-1) - 1) < 1e-12)
+    assert np.all(p[:, 7:] == 0)
+    H, KV, S, hd = 4, 2, 7, 8
+    q = RNG.standard_normal((S, H, hd))
+    k = RNG.standard_normal((S, KV, hd))
+    v = RNG.standard_normal((S, KV, hd))
+    pos = np.arange(S)
+    o = oracle.causal_gqa_attention(q, k, v, pos)
+    # the first query sees only key 0: o = v_0 exactly
+    np.testing.assert_array_equal(o[0], v[0][np.arange(H) * KV // H])
+    # v == 1 everywhere gives 1 (probabilities sum to one)
+    np.testing.assert_allclose(oracle.causal_gqa_attention(q, k, np.ones_like(v), pos), 1.0, atol=1e-13)
+    # q == 0 gives uniform weights: the running mean of v
+    o0 = oracle.causal_gqa_attention(np.zeros_like(q), k, v, pos)
+    cm = np.cumsum(v, axis=0) / np.arange(1, S + 1)[:, None, None]
+    np.testing.assert_allclose(o0, cm[:, np.arange(H) * KV // H], atol=1e-13)
+
+
+def test_attention_matches_torch_sdpa_gqa():
+    H, KV, S, hd = 6, 2, 13, 16
+    q = RNG.standard_normal((S, H, hd))
+    k = RNG.standard_normal((S, KV, hd))
+    v = RNG.standard_normal((S, KV, hd))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q).transpose(0, 1)[None], torch.from_numpy(k).transpose(0, 1)[None],
+        torch.from_numpy(v).transpose(0, 1)[None], is_causal=True, enable_gqa=True)
+    np.testing.assert_allclose(oracle.causal_gqa_attention(q, k, v, np.arange(S)),
+                               ref[0].transpose(0, 1).numpy(), atol=1e-12)
+
+
+def _mha(q, k, v):
+    """Separate multi-head routine: one kv head per query head."""
+    S, H, hd = q.shape
+    out = np.zeros_like(q)
+    for h in range(H):
+        s = q[:, h] @ k[:, h].T / np.sqrt(hd)
+        s[np.triu_indices(S, 1)] = -np.inf
+        p = np.exp(s - s.max(-1, keepdims=True))
+        out[:, h] = (p / p.sum(-1, keepdims=True)) @ v[:, h]
+    return out
+
+
+def test_gqa_with_kv_equal_heads_is_mha():
+    S, H, hd = 10, 5, 8
+    q, k, v = (RNG.standard_normal((S, H, hd)) for _ in range(3))
+    np.testing.assert_allclose(oracle.causal_gqa_attention(q, k, v, np.arange(S)), _mha(q, k, v),
+                               atol=1e-12)
+
+
+# ----------------------------------------------------------------- MLP
+
+def test_silu_and_swiglu():
+    z = np.linspace(-20, 20, 401)
+    np.testing.assert_allclose(oracle.silu(z), torch.nn.functional.silu(torch.from_numpy(z)).numpy(),
+                               rtol=1e-14, atol=1e-300)
+    assert oracle.silu(np.zeros(1))[0] == 0.0
+    D, I = 6, 10
+    h = RNG.standard_normal((3, D))
+    wg, wu, wd = RNG.standard_normal((I, D)), RNG.standard_normal((I, D)), RNG.standard_normal((D, I))
+    np.testing.assert_allclose(oracle.swiglu_mlp(h, wg, np.zeros_like(wu), wd), 0.0)
+    ref = ((h @ wg.T) / (1 + np.exp(-(h @ wg.T))) * (h @ wu.T)) @ wd.T
+    np.testing.assert_allclose(oracle.swiglu_mlp(h, wg, wu, wd), ref, rtol=1e-13)
+
+
+def test_bf16_rounding_matches_torch():
+    x = np.concatenate([RNG.standard_normal(10000) * 10.0 ** RNG.integers(-8, 8, 10000),
+                        [0.0, -0.0, 1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -9]])
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(oracle.round_to_bf16(x), ref)
+
+
+def test_greedy_ties_go_to_lowest_index():
+    lg = np.array([[0.0, 3.0, 1.0, 3.0], [5.0, 5.0, 5.0, 5.0]])
+    np.testing.assert_array_equal(oracle.greedy(lg), [1, 0])
+
+
+# ----------------------------------------------------------------- whole model
+
+def _tiny(kind: str, dtype="f32", layers=2):
+    base = {"llama": "1b", "qwen": "7b"}[kind]
+    shp = small_shape(base, layers=layers, vocab=97, intermediate=48, hidden=48, dtype=dtype)
+    shp.update(num_attention_heads=6, num_key_value_heads=2, head_dim=8)
+    return shp
+
+
+def _np_weights(shp, seed=0):
+    return {k: v.float().numpy().astype(np.float64) for k, v in model_weights(shp, seed).items()}
+
+
+@pytest.mark.parametrize("kind", ["llama", "qwen"])
+def test_incremental_decode_equals_full_recompute(kind):
+    shp = _tiny(kind)
+    w = _np_weights(shp)
+    seq = RNG.integers(0, shp["vocab_size"], 12)
+    full = OracleDecoder(shp, w).prefill([seq], all_logits=True)[0]
+    m = OracleDecoder(shp, w)
+    first = m.prefill([seq[:5]], all_logits=True)[0]
+    rest = [m.decode([t])[0] for t in seq[5:]]
+    np.testing.assert_allclose(np.concatenate([first, np.stack(rest)]), full, atol=1e-10)
+    # chunked extension of a cache gives the same logits as well
+    m2 = OracleDecoder(shp, w)
+    m2.prefill([seq[:3]])
+    np.testing.assert_allclose(m2.extend(0, seq[3:]), full[3:], atol=1e-10)
+
+
+@pytest.mark.parametrize("kind", ["llama", "qwen"])
+def test_causal_prefix_invariance_and_batch_independence(kind):
+    shp = _tiny(kind)
+    w = _np_weights(shp)
+    a = RNG.integers(0, shp["vocab_size"], 9)
+    b = RNG.integers(0, shp["vocab_size"], 4)
+    long = OracleDecoder(shp, w).prefill([np.concatenate([a, b])], all_logits=True)[0]
+    short = OracleDecoder(shp, w).prefill([a], all_logits=True)[0]
+    np.testing.assert_allclose(long[:9], short, atol=1e-12)
+    # a sequence's logits do not depend on the other sequences of the batch
+    both = OracleDecoder(shp, w).prefill([a, b], all_logits=True)
+    np.testing.assert_allclose(both[0], short, atol=1e-12)
+
+
+def test_gqa_model_equals_mha_model_with_repeated_kv_weights():
+    """Pins the kv-head mapping h -> h // (H/KV) at the model level."""
+    shp = _tiny("qwen")
+    w = _np_weights(shp)
+    H, KV, hd = shp["num_attention_heads"], shp["num_key_value_heads"], shp["head_dim"]
+    g = H // KV
+    mha = dict(shp, num_key_value_heads=H)
+    w2 = dict(w)
+    for n in list(w):
+        if n.endswith(("k_proj.weight", "v_proj.weight")):
+            w2[n] = np.repeat(w[n].reshape(KV, hd, -1), g, axis=0).reshape(H * hd, -1)
+        if n.endswith(("k_proj.bias", "v_proj.bias")):
+            w2[n] = np.repeat(w[n].reshape(KV, hd), g, axis=0).reshape(H * hd)
+    seq = RNG.integers(0, shp["vocab_size"], 7)
+    np.testing.assert_allclose(OracleDecoder(mha, w2).prefill([seq], all_logits=True)[0],
+                               OracleDecoder(shp, w).prefill([seq], all_logits=True)[0], atol=1e-11)
+
+
+def _hf_model(kind, shp, w):
+    import transformers
+    common = dict(hidden_size=shp["hidden_size"], num_hidden_layers=shp["num_hidden_layers"],
+                  num_attention_heads=shp["num_attention_heads"],
+                  num_key_value_heads=shp["num_key_value_heads"],
+                  intermediate_size=shp["intermediate_size"], vocab_size=shp["vocab_size"],
+                  rms_norm_eps=shp["rms_norm_eps"], max_position_embeddings=256,
+                  tie_word_embeddings=shp["tie_word_embeddings"], hidden_act="silu")
+    if kind == "llama":
+        cfg = transformers.LlamaConfig(head_dim=shp["head_dim"], attention_bias=False,
+                                       rope_parameters={"rope_type": "default",
+                                                        "rope_theta": shp["rope_theta"]},
+                                       **common)
+        model = transformers.LlamaForCausalLM(cfg)
+    else:
+        cfg = transformers.Qwen2Config(rope_parameters={"rope_type": "default",
+                                                        "rope_theta": shp["rope_theta"]},
+                                       **common)
+        model = transformers.Qwen2ForCausalLM(cfg)
+    model = model.to(torch.float64).eval()
+    sd = {k: torch.from_numpy(v) for k, v in w.items()}
+    if shp["tie_word_embeddings"]:
+        sd["lm_head.weight"] = sd["model.embed_tokens.weight"]
+    missing, unexpected = model.load_state_dict(sd, strict=False)
+    assert not unexpected, unexpected
+    assert all("rotary" in m for m in missing), missing
+    assert model.config.rope_parameters["rope_theta"] == shp["rope_theta"]
+    return model
+
+
+@pytest.mark.parametrize("kind", ["llama", "qwen"])
+def test_whole_model_matches_transformers_fp64(kind):
+    """The paper's baseline library (Results, Experimental Setup) runs the same
+    state dict in float64: prefill logits at every position, then greedy decode
+    with its KV cache."""
+    shp = _tiny(kind, layers=3)
+    assert shp["hidden_size"] == shp["num_attention_heads"] * shp["head_dim"]
+    w = _np_weights(shp, seed=3)
+    model = _hf_model(kind, shp, w)
+    ids = RNG.integers(0, shp["vocab_size"], (2, 11))
+    with torch.no_grad():
+        ref = model(torch.from_numpy(ids)).logits.numpy()
+    orc = OracleDecoder(shp, w).prefill(list(ids), all_logits=True)
+    # HF evaluates the rotary angles in float32 even for a float64 model, so
+    # agreement is ~1e-7; a wrong pairing, sign, head map or operand order
+    # gives differences of order 0.1.
+    for b in range(2):
+        np.testing.assert_allclose(orc[b], ref[b], atol=1e-6, rtol=0)
+    # greedy generation with the KV cache
+    steps = 6
+    toks, _ = generate_greedy(OracleDecoder(shp, w), list(ids), steps)
+    with torch.no_grad():
+        out = model.generate(torch.from_numpy(ids), max_new_tokens=steps + 1, do_sample=False,
+                             pad_token_id=0, eos_token_id=None)
+    np.testing.assert_array_equal(toks, out[:, ids.shape[1]:].numpy())
+
+
+def test_teacher_forced_equals_free_running_on_own_tokens():
+    shp = _tiny("llama")
+    w = _np_weights(shp)
+    seqs = [RNG.integers(0, shp["vocab_size"], 6) for _ in range(3)]
+    toks, lg = generate_greedy(OracleDecoder(shp, w), seqs, 4)
+    lg2 = teacher_forced(OracleDecoder(shp, w), seqs, toks[:, :4])
+    np.testing.assert_array_equal(lg, lg2)
+
+
+def test_io_round_mode_stays_close_to_exact():
+    shp = _tiny("qwen", dtype="bf16")
+    w = _np_weights(shp)
+    seq = RNG.integers(0, shp["vocab_size"], 8)
+    a = OracleDecoder(shp, w).prefill([seq], all_logits=True)[0]
+    b = OracleDecoder(shp, w, io_round="bf16").prefill([seq], all_logits=True)[0]
+    assert 0 < np.max(np.abs(a - b)) < 2e-2
