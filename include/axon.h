@@ -1,0 +1,181 @@
+/*
+ * axon.h - C ABI of the MI355X decoder forward pass (prefill + greedy decode).
+ *
+ * The library runs the inference hot path of the decoder-only Llama/Qwen-style
+ * models that the Axon compiler emits and benchmarks (Results section,
+ * Experimental Setup; Technical Supplement, "Python Overhead"): RMSNorm,
+ * QKV/O projections with rotary positions, causal grouped-query attention over
+ * a KV cache, and the SwiGLU MLP, followed by the final norm, the output head
+ * and a greedy argmax.
+ *
+ * The calls follow the paper's framing of a model: a definition (here the
+ * typed configuration struct, the analogue of the ``Config.dim @@hidden_size``
+ * lookups of the built-in Config module) plus a flat, path-keyed weight map as
+ * found in a safetensors checkpoint (Introduction; ``_param("layers.0.
+ * self_attn.q_proj.weight")`` in the Python-overhead study).  As with the
+ * paper's typechecker, every shape is checked before anything executes.
+ *
+ * Conventions for every call
+ *   - Every int-returning call returns AXON_OK (0) or a negative axon_status;
+ *     nothing aborts.  axon_last_error() returns a thread-local message for the
+ *     last failing call on the calling thread.
+ *   - All argument checks run on the host before any work is enqueued; a call
+ *     that fails validation enqueues nothing and leaves the model unchanged.
+ *   - GPU work is enqueued asynchronously on the caller's hipStream_t (passed as
+ *     void*; NULL means the default stream).  Only axon_init_model
+ *     synchronizes.  The caller must not use one model from two streams at once.
+ *   - "device pointer" means memory allocated with hipMalloc (or by a framework
+ *     on the same device); "host pointer" means ordinary CPU memory.
+ */
+#ifndef AXON_H
+#define AXON_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct axon_model axon_model; /* opaque; owned by the library */
+
+enum axon_status {
+  AXON_OK = 0,
+  AXON_E_INVALID = -1,  /* bad argument: NULL pointer, bad config value, bad count */
+  AXON_E_SHAPE = -2,    /* a weight's shape does not match the configuration */
+  AXON_E_MISSING = -3,  /* a required weight is absent, or an unknown/duplicate name is given */
+  AXON_E_DTYPE = -4,    /* a weight's dtype differs from the model dtype */
+  AXON_E_CAPACITY = -5, /* batch, sequence length, token count or page table beyond capacity */
+  AXON_E_OOM = -6,      /* device allocation failed */
+  AXON_E_HIP = -7       /* a HIP runtime call failed (message carries hipGetErrorString) */
+};
+
+enum axon_dtype { AXON_BF16 = 1, AXON_F32 = 2 };
+
+/* Model definition and capacities.  Field meanings follow the HF config keys
+ * that the generated code reads (hidden_size, num_hidden_layers, ...). */
+typedef struct {
+  int32_t hidden;         /* D; multiple of 64 */
+  int32_t n_layers;       /* L >= 1 */
+  int32_t n_heads;        /* H; a multiple of n_kv_heads */
+  int32_t n_kv_heads;     /* KV; H / KV <= 16 */
+  int32_t head_dim;       /* hd; 64 or 128 */
+  int32_t intermediate;   /* I; multiple of 64 */
+  int32_t vocab;          /* V >= 1 */
+  float rms_eps;          /* RMSNorm epsilon (inside the square root), > 0 */
+  double rope_theta;      /* RoPE base, > 1 */
+  int32_t qkv_bias;       /* 1: q/k/v projections carry a bias (Qwen-style) */
+  int32_t tie_embeddings; /* 1: the output head reuses model.embed_tokens.weight */
+  int32_t dtype;          /* AXON_BF16 or AXON_F32 (weights, KV cache, activations) */
+  int32_t max_batch;      /* sequence slots, 1..1024 */
+  int32_t max_seq;        /* tokens per sequence (prompt + generated), >= 1 */
+  int32_t max_tokens;     /* largest prefill token count per call; 0 = max_batch*max_seq */
+  int32_t kv_page_size;   /* 0: contiguous cache; else tokens per page, a multiple of 16 */
+  int32_t kv_num_pages;   /* page-pool size when kv_page_size > 0 */
+} axon_config;
+
+/* One entry of the flat weight map.  Names follow the HF Llama/Qwen2 layout:
+ *   model.embed_tokens.weight                 [V, D]
+ *   model.layers.{i}.input_layernorm.weight   [D]
+ *   model.layers.{i}.self_attn.q_proj.weight  [H*hd, D]   (.bias [H*hd] iff qkv_bias)
+ *   model.layers.{i}.self_attn.k_proj.weight  [KV*hd, D]  (.bias [KV*hd] iff qkv_bias)
+ *   model.layers.{i}.self_attn.v_proj.weight  [KV*hd, D]  (.bias [KV*hd] iff qkv_bias)
+ *   model.layers.{i}.self_attn.o_proj.weight  [D, H*hd]
+ *   model.layers.{i}.post_attention_layernorm.weight [D]
+ *   model.layers.{i}.mlp.gate_proj.weight     [I, D]
+ *   model.layers.{i}.mlp.up_proj.weight       [I, D]
+ *   model.layers.{i}.mlp.down_proj.weight     [D, I]
+ *   model.norm.weight                         [D]
+ *   lm_head.weight                            [V, D]  (present iff tie_embeddings == 0)
+ * Linear weights are [out, in] row-major.  Every tensor is contiguous,
+ * row-major, in the model dtype.  ``data`` is a host pointer if on_device == 0,
+ * else a device pointer on the current device. */
+typedef struct {
+  const char* name;
+  int32_t dtype;     /* AXON_BF16 or AXON_F32 */
+  int32_t ndim;      /* 1 or 2 */
+  int64_t shape[2];  /* shape[1] ignored when ndim == 1 */
+  const void* data;
+  int32_t on_device;
+} axon_weight;
+
+/* Validate the configuration and the weight map, allocate device memory on
+ * the current HIP device, copy and repack the weights (the caller keeps
+ * ownership of its buffers and may free them once the call returns), allocate
+ * the KV cache (contiguous or a page pool) and the work buffers, and build the
+ * rotary cos/sin table.  Synchronizes ``stream`` before returning.
+ * On success *out receives the handle; on failure *out is set to NULL and no
+ * device memory stays allocated. */
+int axon_init_model(const axon_config* cfg, const axon_weight* weights, int32_t n_weights,
+                    void* stream, axon_model** out);
+
+/* Prefill: start ``batch`` fresh sequences in slots 0..batch-1 (every earlier
+ * sequence is dropped) and run the forward pass over their prompts.
+ *   d_tokens      device int32 [sum S_b], the prompts packed back to back;
+ *   d_cu_seqlens  device int32 [batch+1], prefix sums of the prompt lengths;
+ *   h_cu_seqlens  host copy of the same array (checked on the host, so no
+ *                 device-to-host copy is needed);
+ *   h_block_table host int32 [batch, block_table_stride] page ids, required iff
+ *                 the cache is paged (else NULL).  Row b lists the pages of
+ *                 slot b in logical order; it must cover the prompt and any
+ *                 later decode positions (unused entries may be -1).  Page ids
+ *                 are in [0, kv_num_pages) and no page appears twice.  The
+ *                 table is copied; the caller keeps ownership;
+ *   all_logits    0: logits of the last position of each sequence, d_logits is
+ *                 device float [batch, V]; 1: logits of every position,
+ *                 d_logits is device float [sum S_b, V];  d_logits may be NULL;
+ *   d_next_tokens device int32 [batch]: greedy argmax of each sequence's last
+ *                 logits (lowest index on ties).
+ * Positions are 0..S_b-1 (a fresh cache).  Each S_b must be in [1, max_seq]
+ * and sum S_b <= max_tokens. */
+int axon_prefill(axon_model* m, int32_t batch, const int32_t* d_tokens,
+                 const int32_t* d_cu_seqlens, const int32_t* h_cu_seqlens,
+                 const int32_t* h_block_table, int32_t block_table_stride, int32_t all_logits,
+                 float* d_logits, int32_t* d_next_tokens, void* stream);
+
+/* One greedy decode step for slots 0..batch-1 (batch <= the batch of the last
+ * prefill).  Slot b consumes d_tokens[b] (device int32 [batch]) at position
+ * len_b (its current length), appends its key/value to the cache, writes the
+ * logits (device float [batch, V], or NULL to skip) and the argmax token
+ * (device int32 [batch]), and increments len_b.  Fails with AXON_E_CAPACITY if
+ * some len_b + 1 > max_seq or (paged) the slot's page table has no page for
+ * position len_b.  The step is recorded once per (batch, pointer triple) as a
+ * HIP graph and replayed; d_tokens and d_next_tokens may be the same buffer
+ * only if the caller does not need the input afterwards. */
+int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_tokens, float* d_logits,
+                     int32_t* d_next_tokens, void* stream);
+
+/* Current length of every slot (host copy kept by the library, no device
+ * access).  Writes min(n, max_batch) entries to ``lens``; returns the number of
+ * active slots (the batch of the last prefill), or a negative status. */
+int axon_slot_lengths(const axon_model* m, int32_t* lens, int32_t n);
+
+/* Measurement support.  While enabled, every launch of the kernel classes
+ *   0 = few-token projection GEMM (decode, weight streaming),
+ *   1 = many-token projection GEMM (prefill, MFMA tiles),
+ *   2 = decode attention (split over key chunks, with its combine kernel),
+ *   3 = prefill attention
+ * is bracketed by two HIP events recorded on the stream it is launched on, and
+ * decode steps run eagerly instead of as a recorded graph (kernel durations
+ * are unchanged; only launch gaps differ).  Enabling (1) or disabling (0)
+ * drops earlier records.  Returns AXON_OK or AXON_E_INVALID. */
+int axon_timing_enable(axon_model* m, int32_t enable);
+
+/* Copy out up to ``cap`` timing records: cls[i] is the kernel class,
+ * dims[3*i..3*i+2] = (N output features, M tokens, K reduction length) of a
+ * projection, or (heads, sequences, summed context/query tokens) of an
+ * attention launch, ms[i] the event-measured duration in milliseconds.
+ * Synchronizes on the recorded events.  Returns the number of records (which
+ * may exceed cap), or a negative status. */
+int axon_timing_records(axon_model* m, int32_t* cls, int32_t* dims, float* ms, int32_t cap);
+
+/* Release every device buffer and recorded graph of the model.  NULL is a
+ * no-op.  The caller must have synchronized the streams it used. */
+void axon_free(axon_model* m);
+
+/* Message describing the last failure on this thread ("" if none). */
+const char* axon_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AXON_H */

@@ -1,0 +1,733 @@
+// C ABI and runtime of the decoder forward pass: configuration and weight-map
+// validation (all on the host, before any HIP call), weight repacking, KV
+// cache, work buffers, the prefill and decode kernel sequences, and the
+// per-(batch, pointers) HIP graph of the decode step.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <string>
+#include <tuple>
+#include <unordered_map>
+#include <vector>
+
+#include "axon.h"
+#include "kernels.h"
+
+using namespace axon;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                      \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess) return fail(AXON_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+std::string shape_str(int ndim, const int64_t* s) {
+  if (ndim == 1) return "[" + std::to_string(s[0]) + "]";
+  return "[" + std::to_string(s[0]) + ", " + std::to_string(s[1]) + "]";
+}
+
+struct Expected {
+  int ndim;
+  int64_t shape[2];
+};
+
+// The weight names and shapes implied by a configuration.
+std::vector<std::pair<std::string, Expected>> expected_weights(const axon_config& c) {
+  const int64_t D = c.hidden, H = c.n_heads, KV = c.n_kv_heads, hd = c.head_dim, I = c.intermediate,
+                V = c.vocab;
+  std::vector<std::pair<std::string, Expected>> w;
+  w.push_back({"model.embed_tokens.weight", {2, {V, D}}});
+  for (int i = 0; i < c.n_layers; ++i) {
+    const std::string p = "model.layers." + std::to_string(i) + ".";
+    w.push_back({p + "input_layernorm.weight", {1, {D, 0}}});
+    w.push_back({p + "self_attn.q_proj.weight", {2, {H * hd, D}}});
+    w.push_back({p + "self_attn.k_proj.weight", {2, {KV * hd, D}}});
+    w.push_back({p + "self_attn.v_proj.weight", {2, {KV * hd, D}}});
+    if (c.qkv_bias) {
+      w.push_back({p + "self_attn.q_proj.bias", {1, {H * hd, 0}}});
+      w.push_back({p + "self_attn.k_proj.bias", {1, {KV * hd, 0}}});
+      w.push_back({p + "self_attn.v_proj.bias", {1, {KV * hd, 0}}});
+    }
+    w.push_back({p + "self_attn.o_proj.weight", {2, {D, H * hd}}});
+    w.push_back({p + "post_attention_layernorm.weight", {1, {D, 0}}});
+    w.push_back({p + "mlp.gate_proj.weight", {2, {I, D}}});
+    w.push_back({p + "mlp.up_proj.weight", {2, {I, D}}});
+    w.push_back({p + "mlp.down_proj.weight", {2, {D, I}}});
+  }
+  w.push_back({"model.norm.weight", {1, {D, 0}}});
+  if (!c.tie_embeddings) w.push_back({"lm_head.weight", {2, {V, D}}});
+  return w;
+}
+
+int validate_config(const axon_config& c) {
+  auto bad = [](const std::string& m) { return fail(AXON_E_INVALID, "invalid config: " + m); };
+  if (c.hidden <= 0 || c.hidden % 64) return bad("hidden must be a positive multiple of 64");
+  if (c.n_layers <= 0) return bad("n_layers must be >= 1");
+  if (c.n_heads <= 0 || c.n_kv_heads <= 0) return bad("n_heads and n_kv_heads must be >= 1");
+  if (c.n_heads % c.n_kv_heads) return bad("n_heads must be a multiple of n_kv_heads");
+  if (c.n_heads / c.n_kv_heads > 16) return bad("n_heads / n_kv_heads must be <= 16");
+  if (c.head_dim != 64 && c.head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (c.intermediate <= 0 || c.intermediate % 64) return bad("intermediate must be a positive multiple of 64");
+  if (c.vocab <= 0) return bad("vocab must be >= 1");
+  if (!(c.rms_eps > 0.f) || !std::isfinite(c.rms_eps)) return bad("rms_eps must be finite and > 0");
+  if (!(c.rope_theta > 1.0) || !std::isfinite(c.rope_theta)) return bad("rope_theta must be finite and > 1");
+  if (c.qkv_bias != 0 && c.qkv_bias != 1) return bad("qkv_bias must be 0 or 1");
+  if (c.tie_embeddings != 0 && c.tie_embeddings != 1) return bad("tie_embeddings must be 0 or 1");
+  if (c.dtype != AXON_BF16 && c.dtype != AXON_F32) return bad("dtype must be AXON_BF16 or AXON_F32");
+  if (c.max_batch < 1 || c.max_batch > 1024) return bad("max_batch must be in [1, 1024]");
+  if (c.max_seq < 1 || c.max_seq > (1 << 20)) return bad("max_seq must be in [1, 2^20]");
+  if (c.max_tokens < 0) return bad("max_tokens must be >= 0");
+  if (c.kv_page_size < 0 || c.kv_page_size % 16) return bad("kv_page_size must be 0 or a multiple of 16");
+  if (c.kv_page_size > 0 && c.kv_num_pages < 1) return bad("kv_num_pages must be >= 1 for a paged cache");
+  return AXON_OK;
+}
+
+struct LayerW {
+  void* wqkv;   // [(H+2KV)hd, D]
+  void* bqkv;   // [(H+2KV)hd] or null
+  void* wo;     // [D, H hd]
+  void* wgu;    // [2I, D], 16 gate rows then the 16 matching up rows, repeated
+  void* wd;     // [D, I]
+  void* gin;    // [D]
+  void* gpost;  // [D]
+};
+
+struct TimingRec {
+  int cls, d0, d1, d2;
+  hipEvent_t a, b;
+};
+
+struct GraphKey {
+  int batch;
+  const void* tok;
+  const void* logits;
+  const void* next;
+  bool operator<(const GraphKey& o) const {
+    return std::tie(batch, tok, logits, next) < std::tie(o.batch, o.tok, o.logits, o.next);
+  }
+};
+
+}  // namespace
+
+struct axon_model {
+  axon_config cfg{};
+  int esz = 2;
+  bool bf = true;
+  std::vector<void*> dev_allocs;
+  void* embed = nullptr;
+  void* lm_head = nullptr;
+  void* gfinal = nullptr;
+  std::vector<LayerW> layers;
+  // KV cache
+  void* kcache = nullptr;
+  void* vcache = nullptr;
+  int64_t kv_layer_elems = 0;
+  int ps = 0;
+  int bt_stride = 0;
+  int32_t* d_bt = nullptr;
+  int32_t* h_bt = nullptr;  // pinned host copy of the page table
+  hipEvent_t bt_copied = nullptr;
+  float* rope_cos = nullptr;
+  float* rope_sin = nullptr;
+  // work buffers
+  int rows = 0;
+  float* x = nullptr;
+  void* h = nullptr;
+  float* qkv = nullptr;
+  void* q = nullptr;
+  void* o = nullptr;
+  void* a = nullptr;
+  void* hlast = nullptr;
+  float* gu_f32 = nullptr;
+  float* logits_int = nullptr;
+  float* parts = nullptr;
+  float* attn_part = nullptr;
+  int32_t* d_len = nullptr;
+  std::vector<int> h_len;
+  int active = 0;
+  hipStream_t cap_stream = nullptr;
+  std::map<GraphKey, hipGraphExec_t> graphs;
+  bool use_graphs = true;
+  // kernel timing (measurement mode)
+  bool timing = false;
+  std::vector<TimingRec> trecs;
+  std::vector<hipEvent_t> tpool;
+  size_t tnext = 0;
+
+  hipEvent_t tevent() {
+    if (tnext == tpool.size()) {
+      hipEvent_t e = nullptr;
+      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      tpool.push_back(e);
+    }
+    return tpool[tnext++];
+  }
+  // Run ``launch`` between two events on s when timing is on.
+  template <typename F>
+  void timed(int cls, int d0, int d1, int d2, hipStream_t s, F&& launch) {
+    if (!timing) {
+      launch();
+      return;
+    }
+    TimingRec r{cls, d0, d1, d2, tevent(), tevent()};
+    if (r.a) (void)hipEventRecord(r.a, s);
+    launch();
+    if (r.b) (void)hipEventRecord(r.b, s);
+    if (r.a && r.b) trecs.push_back(r);
+  }
+
+  int D() const { return cfg.hidden; }
+  int H() const { return cfg.n_heads; }
+  int KVh() const { return cfg.n_kv_heads; }
+  int hd() const { return cfg.head_dim; }
+  int I() const { return cfg.intermediate; }
+  int V() const { return cfg.vocab; }
+  int nqkv() const { return (cfg.n_heads + 2 * cfg.n_kv_heads) * cfg.head_dim; }
+
+  KVView kv(int l, bool paged_table) const {
+    KVView v;
+    v.k = (char*)kcache + (int64_t)l * kv_layer_elems * esz;
+    v.v = (char*)vcache + (int64_t)l * kv_layer_elems * esz;
+    v.bt = paged_table ? d_bt : nullptr;
+    v.bt_stride = bt_stride;
+    v.ps = ps;
+    v.kv_heads = cfg.n_kv_heads;
+    v.hd = cfg.head_dim;
+    return v;
+  }
+  bool paged() const { return cfg.kv_page_size > 0; }
+};
+
+namespace {
+
+int dev_alloc(axon_model* m, void** p, size_t bytes) {
+  if (bytes == 0) bytes = 256;
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return fail(e == hipErrorOutOfMemory ? AXON_E_OOM : AXON_E_HIP,
+                "device allocation of " + std::to_string(bytes) + " bytes failed: " + hipGetErrorString(e));
+  }
+  m->dev_allocs.push_back(*p);
+  return AXON_OK;
+}
+
+void release(axon_model* m) {
+  for (hipEvent_t e : m->tpool) (void)hipEventDestroy(e);
+  for (auto& kv : m->graphs) (void)hipGraphExecDestroy(kv.second);
+  m->graphs.clear();
+  for (void* p : m->dev_allocs) (void)hipFree(p);
+  m->dev_allocs.clear();
+  if (m->h_bt) (void)hipHostFree(m->h_bt);
+  if (m->bt_copied) (void)hipEventDestroy(m->bt_copied);
+  if (m->cap_stream) (void)hipStreamDestroy(m->cap_stream);
+  delete m;
+}
+
+// ------------------------------------------------------------------ forward
+template <typename T>
+void gemm_many(axon_model* m, const void* W, const void* X, int N, int M, int K, int epi, float* out_f32,
+               void* out_t, int ldo, hipStream_t s) {
+  EpiArgs ep{out_f32, out_t, ldo, 0};
+  m->timed(1, N, M, K, s, [&] {
+    if constexpr (sizeof(T) == 2)
+      launch_gemm_bf16((const bf16*)W, (const bf16*)X, N, M, K, epi, ep, s);
+    else
+      launch_gemm_f32((const float*)W, (const float*)X, N, M, K, epi, ep, s);
+  });
+}
+
+// Few-token projection; returns the number of float partials written (1 when
+// the epilogue was applied in place).
+template <typename T>
+int gemm_few(axon_model* m, const void* W, const void* X, int N, int M, int K, int epi, float* out_f32,
+             void* out_t, int ldo, hipStream_t s, int64_t* part_stride) {
+  if constexpr (sizeof(T) == 2) {
+    const int splits = plan_gemv_splits(N, M, K);
+    if (splits > 1) {
+      EpiArgs ep{m->parts, nullptr, N, (int64_t)M * N};
+      m->timed(0, N, M, K, s,
+               [&] { launch_gemv_bf16((const bf16*)W, (const bf16*)X, N, M, K, splits, EPI_PART, ep, s); });
+      *part_stride = (int64_t)M * N;
+      return splits;
+    }
+    EpiArgs ep{out_f32, out_t, ldo, 0};
+    m->timed(0, N, M, K, s, [&] { launch_gemv_bf16((const bf16*)W, (const bf16*)X, N, M, K, 1, epi, ep, s); });
+    *part_stride = 0;
+    return 0;
+  } else {
+    EpiArgs ep{out_f32, out_t, ldo, 0};
+    m->timed(0, N, M, K, s, [&] { launch_gemm_f32((const float*)W, (const float*)X, N, M, K, epi, ep, s); });
+    *part_stride = 0;
+    return 0;
+  }
+}
+
+template <typename T>
+void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, const int32_t* d_cu,
+                     const int32_t* h_cu, int all_logits, float* d_logits, int32_t* d_next, hipStream_t s) {
+  const int D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V(), nq = m->nqkv();
+  const float eps = m->cfg.rms_eps;
+  T* h = (T*)m->h;
+  launch_set_lengths(d_cu, m->d_len, B, s);
+  launch_embed_rmsnorm<T>(d_tokens, (const T*)m->embed, (const T*)m->layers[0].gin, m->x, h, Ttok, D, V, eps, s);
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    const LayerW& w = m->layers[l];
+    KVView kv = m->kv(l, m->paged());
+    gemm_many<T>(m, w.wqkv, h, nq, Ttok, D, EPI_F32, m->qkv, nullptr, nq, s);
+    launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, Ttok, B, d_cu,
+                      nullptr, H, s);
+    m->timed(3, H, B, Ttok, s, [&] { launch_attn_prefill<T>((const T*)m->q, kv, (T*)m->o, Ttok, B, d_cu, h_cu, H, s); });
+    gemm_many<T>(m, w.wo, m->o, D, Ttok, H * hd, EPI_RESID, m->x, nullptr, D, s);
+    launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, Ttok, D, eps, nullptr, s);
+    if constexpr (sizeof(T) == 2) {
+      gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_SILU, nullptr, m->a, I, s);
+    } else {
+      gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_F32, m->gu_f32, nullptr, 2 * I, s);
+      launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, Ttok, I, s);
+    }
+    gemm_many<T>(m, w.wd, m->a, D, Ttok, I, EPI_RESID, m->x, nullptr, D, s);
+    const bool last = l + 1 == m->cfg.n_layers;
+    const T* gnext = (const T*)(last ? m->gfinal : m->layers[l + 1].gin);
+    if (!last || all_logits)
+      launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, gnext, h, Ttok, D, eps, nullptr, s);
+    else
+      launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, gnext, (T*)m->hlast, B, D, eps, d_cu, s);
+  }
+  if (all_logits) {
+    gemm_many<T>(m, m->lm_head, h, V, Ttok, D, EPI_F32, d_logits, nullptr, V, s);
+    launch_argmax_rows(d_logits, B, V, d_next, d_cu, s);
+  } else {
+    float* dst = d_logits ? d_logits : m->logits_int;
+    int64_t ps = 0;
+    const int np = gemm_few<T>(m, m->lm_head, m->hlast, V, B, D, EPI_F32, dst, nullptr, V, s, &ps);
+    if (np > 1) launch_sum_reduce(m->parts, np, ps, dst, B, V, s);
+    launch_argmax(dst, B, V, d_next, nullptr, s);
+  }
+}
+
+template <typename T>
+void enqueue_decode(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next, hipStream_t s) {
+  const int D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V(), nq = m->nqkv();
+  const float eps = m->cfg.rms_eps;
+  T* h = (T*)m->h;
+  int64_t ps = 0;
+  launch_embed_rmsnorm<T>(d_tokens, (const T*)m->embed, (const T*)m->layers[0].gin, m->x, h, B, D, V, eps, s);
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    const LayerW& w = m->layers[l];
+    KVView kv = m->kv(l, m->paged());
+    int np = gemm_few<T>(m, w.wqkv, h, nq, B, D, EPI_F32, m->qkv, nullptr, nq, s, &ps);
+    if (np > 1)
+      launch_rope_kv<T>(m->parts, np, ps, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, B, 0,
+                        nullptr, m->d_len, H, s);
+    else
+      launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, B, 0, nullptr,
+                        m->d_len, H, s);
+    int ctx_sum = 0;
+    for (int b = 0; b < B; ++b) ctx_sum += m->h_len[b] + 1;
+    m->timed(2, H, B, ctx_sum, s, [&] {
+      launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
+    });
+    np = gemm_few<T>(m, w.wo, m->o, D, B, H * hd, EPI_RESID, m->x, nullptr, D, s, &ps);
+    launch_resid_rmsnorm<T>(m->x, np > 1 ? m->parts : nullptr, np > 1 ? np : 0, ps, (const T*)w.gpost, h, B, D,
+                            eps, nullptr, s);
+    if constexpr (sizeof(T) == 2) {
+      np = gemm_few<T>(m, w.wgu, h, 2 * I, B, D, EPI_SILU, nullptr, m->a, I, s, &ps);
+      if (np > 1) launch_silu_reduce<T>(m->parts, np, ps, (T*)m->a, B, I, s);
+    } else {
+      gemm_few<T>(m, w.wgu, h, 2 * I, B, D, EPI_F32, m->gu_f32, nullptr, 2 * I, s, &ps);
+      launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, B, I, s);
+    }
+    np = gemm_few<T>(m, w.wd, m->a, D, B, I, EPI_RESID, m->x, nullptr, D, s, &ps);
+    const bool last = l + 1 == m->cfg.n_layers;
+    const T* gnext = (const T*)(last ? m->gfinal : m->layers[l + 1].gin);
+    launch_resid_rmsnorm<T>(m->x, np > 1 ? m->parts : nullptr, np > 1 ? np : 0, ps, gnext, h, B, D, eps, nullptr,
+                            s);
+  }
+  float* dst = d_logits ? d_logits : m->logits_int;
+  const int np = gemm_few<T>(m, m->lm_head, h, V, B, D, EPI_F32, dst, nullptr, V, s, &ps);
+  if (np > 1) launch_sum_reduce(m->parts, np, ps, dst, B, V, s);
+  launch_argmax(dst, B, V, d_next, m->d_len, s);
+}
+
+int check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(AXON_E_HIP, std::string(what) + ": kernel launch failed: " + hipGetErrorString(e));
+  return AXON_OK;
+}
+
+}  // namespace
+
+// ====================================================================== ABI
+
+extern "C" const char* axon_last_error(void) { return g_err.c_str(); }
+
+extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weights, int32_t n_weights, void* stream,
+                               axon_model** out) {
+  g_err.clear();
+  if (!out) return fail(AXON_E_INVALID, "out is NULL");
+  *out = nullptr;
+  if (!cfg) return fail(AXON_E_INVALID, "cfg is NULL");
+  if (n_weights < 0 || (n_weights > 0 && !weights)) return fail(AXON_E_INVALID, "weights is NULL or n_weights < 0");
+  int rc = validate_config(*cfg);
+  if (rc) return rc;
+  const axon_config& c = *cfg;
+
+  // ---- weight map (host only)
+  auto expected = expected_weights(c);
+  std::unordered_map<std::string, size_t> index;
+  for (size_t i = 0; i < expected.size(); ++i) index[expected[i].first] = i;
+  std::vector<const axon_weight*> found(expected.size(), nullptr);
+  for (int i = 0; i < n_weights; ++i) {
+    const axon_weight& w = weights[i];
+    if (!w.name) return fail(AXON_E_INVALID, "weight " + std::to_string(i) + " has a NULL name");
+    auto it = index.find(w.name);
+    if (it == index.end()) {
+      std::string why = std::string(w.name) == "lm_head.weight" ? " (tie_embeddings is set)" : "";
+      return fail(AXON_E_MISSING, std::string("unknown weight '") + w.name + "'" + why);
+    }
+    if (found[it->second]) return fail(AXON_E_MISSING, std::string("duplicate weight '") + w.name + "'");
+    const Expected& e = expected[it->second].second;
+    if (w.dtype != c.dtype)
+      return fail(AXON_E_DTYPE, std::string("weight '") + w.name + "' has dtype " + std::to_string(w.dtype) +
+                                    ", the model dtype is " + std::to_string(c.dtype));
+    if (w.ndim != e.ndim || w.shape[0] != e.shape[0] || (e.ndim == 2 && w.shape[1] != e.shape[1]))
+      return fail(AXON_E_SHAPE, std::string("weight '") + w.name + "' has shape " +
+                                    (w.ndim == 1 || w.ndim == 2 ? shape_str(w.ndim, w.shape) : "ndim=" + std::to_string(w.ndim)) +
+                                    ", expected " + shape_str(e.ndim, e.shape));
+    if (!w.data) return fail(AXON_E_INVALID, std::string("weight '") + w.name + "' has NULL data");
+    found[it->second] = &w;
+  }
+  for (size_t i = 0; i < expected.size(); ++i)
+    if (!found[i]) return fail(AXON_E_MISSING, "missing weight '" + expected[i].first + "'");
+
+  // ---- device state
+  axon_model* m = new axon_model();
+  m->cfg = c;
+  m->bf = c.dtype == AXON_BF16;
+  m->esz = m->bf ? 2 : 4;
+  if (const char* e = std::getenv("AXON_NO_GRAPH")) m->use_graphs = std::atoi(e) == 0;
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t D = c.hidden, H = c.n_heads, KV = c.n_kv_heads, hd = c.head_dim, I = c.intermediate, V = c.vocab;
+  const int64_t esz = m->esz, nq = (H + 2 * KV) * hd;
+  auto get = [&](const std::string& n) -> const axon_weight* { return found[index.at(n)]; };
+  auto kind = [](const axon_weight* w) { return w->on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice; };
+
+#define TRY(expr)          \
+  do {                     \
+    int r_ = (expr);       \
+    if (r_) {              \
+      (void)hipStreamSynchronize(s); \
+      release(m);          \
+      return r_;           \
+    }                      \
+  } while (0)
+#define HTRY(expr)                                                                                 \
+  do {                                                                                             \
+    hipError_t e_ = (expr);                                                                        \
+    if (e_ != hipSuccess) {                                                                        \
+      std::string msg_ = std::string(#expr) + ": " + hipGetErrorString(e_);                        \
+      (void)hipStreamSynchronize(s);                                                               \
+      release(m);                                                                                  \
+      return fail(AXON_E_HIP, msg_);                                                               \
+    }                                                                                              \
+  } while (0)
+
+  auto copy_in = [&](void** dst, const axon_weight* w) -> int {
+    const size_t bytes = (size_t)w->shape[0] * (w->ndim == 2 ? (size_t)w->shape[1] : 1) * esz;
+    int r = dev_alloc(m, dst, bytes);
+    if (r) return r;
+    hipError_t e = hipMemcpyAsync(*dst, w->data, bytes, kind(w), s);
+    if (e != hipSuccess) return fail(AXON_E_HIP, std::string("copy of '") + w->name + "': " + hipGetErrorString(e));
+    return AXON_OK;
+  };
+
+  TRY(copy_in(&m->embed, get("model.embed_tokens.weight")));
+  TRY(copy_in(&m->gfinal, get("model.norm.weight")));
+  if (c.tie_embeddings) m->lm_head = m->embed;
+  else TRY(copy_in(&m->lm_head, get("lm_head.weight")));
+  m->layers.resize(c.n_layers);
+  for (int l = 0; l < c.n_layers; ++l) {
+    const std::string p = "model.layers." + std::to_string(l) + ".";
+    LayerW& w = m->layers[l];
+    TRY(copy_in(&w.gin, get(p + "input_layernorm.weight")));
+    TRY(copy_in(&w.gpost, get(p + "post_attention_layernorm.weight")));
+    TRY(copy_in(&w.wo, get(p + "self_attn.o_proj.weight")));
+    TRY(copy_in(&w.wd, get(p + "mlp.down_proj.weight")));
+    // fused QKV: rows q, then k, then v
+    TRY(dev_alloc(m, &w.wqkv, (size_t)nq * D * esz));
+    const axon_weight* wq = get(p + "self_attn.q_proj.weight");
+    const axon_weight* wk = get(p + "self_attn.k_proj.weight");
+    const axon_weight* wv = get(p + "self_attn.v_proj.weight");
+    HTRY(hipMemcpyAsync(w.wqkv, wq->data, H * hd * D * esz, kind(wq), s));
+    HTRY(hipMemcpyAsync((char*)w.wqkv + H * hd * D * esz, wk->data, KV * hd * D * esz, kind(wk), s));
+    HTRY(hipMemcpyAsync((char*)w.wqkv + (H + KV) * hd * D * esz, wv->data, KV * hd * D * esz, kind(wv), s));
+    w.bqkv = nullptr;
+    if (c.qkv_bias) {
+      TRY(dev_alloc(m, &w.bqkv, (size_t)nq * esz));
+      const axon_weight* bq = get(p + "self_attn.q_proj.bias");
+      const axon_weight* bk = get(p + "self_attn.k_proj.bias");
+      const axon_weight* bv = get(p + "self_attn.v_proj.bias");
+      HTRY(hipMemcpyAsync(w.bqkv, bq->data, H * hd * esz, kind(bq), s));
+      HTRY(hipMemcpyAsync((char*)w.bqkv + H * hd * esz, bk->data, KV * hd * esz, kind(bk), s));
+      HTRY(hipMemcpyAsync((char*)w.bqkv + (H + KV) * hd * esz, bv->data, KV * hd * esz, kind(bv), s));
+    }
+    // gate/up interleaved in blocks of 16 rows: [g0..g15, u0..u15, g16..g31, u16..u31, ...]
+    TRY(dev_alloc(m, &w.wgu, (size_t)2 * I * D * esz));
+    const axon_weight* wg = get(p + "mlp.gate_proj.weight");
+    const axon_weight* wu = get(p + "mlp.up_proj.weight");
+    const size_t blk = 16 * D * esz;
+    HTRY(hipMemcpy2DAsync(w.wgu, 2 * blk, wg->data, blk, blk, I / 16, kind(wg), s));
+    HTRY(hipMemcpy2DAsync((char*)w.wgu + blk, 2 * blk, wu->data, blk, blk, I / 16, kind(wu), s));
+  }
+
+  // ---- KV cache
+  if (m->paged()) {
+    m->ps = c.kv_page_size;
+    const int64_t pages = c.kv_num_pages;
+    m->kv_layer_elems = pages * KV * m->ps * hd;
+    m->bt_stride = (c.max_seq + m->ps - 1) / m->ps;
+    TRY(dev_alloc(m, (void**)&m->d_bt, (size_t)c.max_batch * m->bt_stride * sizeof(int32_t)));
+    HTRY(hipHostMalloc((void**)&m->h_bt, (size_t)c.max_batch * m->bt_stride * sizeof(int32_t), hipHostMallocDefault));
+    for (int64_t i = 0; i < (int64_t)c.max_batch * m->bt_stride; ++i) m->h_bt[i] = -1;
+    HTRY(hipEventCreateWithFlags(&m->bt_copied, hipEventDisableTiming));
+  } else {
+    m->ps = (c.max_seq + 15) / 16 * 16;
+    m->kv_layer_elems = (int64_t)c.max_batch * KV * m->ps * hd;
+  }
+  const size_t kv_bytes = (size_t)c.n_layers * m->kv_layer_elems * esz;
+  TRY(dev_alloc(m, &m->kcache, kv_bytes));
+  TRY(dev_alloc(m, &m->vcache, kv_bytes));
+  HTRY(hipMemsetAsync(m->kcache, 0, kv_bytes, s));
+  HTRY(hipMemsetAsync(m->vcache, 0, kv_bytes, s));
+
+  // ---- rotary table, computed in double precision, stored as float
+  {
+    const int half = (int)hd / 2;
+    std::vector<float> cs((size_t)c.max_seq * half), sn((size_t)c.max_seq * half);
+    for (int p = 0; p < c.max_seq; ++p)
+      for (int i = 0; i < half; ++i) {
+        const double ang = (double)p * std::pow(c.rope_theta, -2.0 * i / (double)hd);
+        cs[(size_t)p * half + i] = (float)std::cos(ang);
+        sn[(size_t)p * half + i] = (float)std::sin(ang);
+      }
+    TRY(dev_alloc(m, (void**)&m->rope_cos, cs.size() * sizeof(float)));
+    TRY(dev_alloc(m, (void**)&m->rope_sin, sn.size() * sizeof(float)));
+    HTRY(hipMemcpy(m->rope_cos, cs.data(), cs.size() * sizeof(float), hipMemcpyHostToDevice));
+    HTRY(hipMemcpy(m->rope_sin, sn.data(), sn.size() * sizeof(float), hipMemcpyHostToDevice));
+  }
+
+  // ---- work buffers
+  {
+    int64_t tmax = c.max_tokens > 0 ? c.max_tokens : (int64_t)c.max_batch * c.max_seq;
+    tmax = std::max<int64_t>(tmax, c.max_batch);
+    m->rows = (int)tmax;
+    TRY(dev_alloc(m, (void**)&m->x, tmax * D * 4));
+    TRY(dev_alloc(m, &m->h, tmax * D * esz));
+    TRY(dev_alloc(m, (void**)&m->qkv, tmax * nq * 4));
+    TRY(dev_alloc(m, &m->q, tmax * H * hd * esz));
+    TRY(dev_alloc(m, &m->o, tmax * H * hd * esz));
+    TRY(dev_alloc(m, &m->a, tmax * I * esz));
+    TRY(dev_alloc(m, &m->hlast, (int64_t)c.max_batch * D * esz));
+    TRY(dev_alloc(m, (void**)&m->logits_int, (int64_t)c.max_batch * V * 4));
+    if (!m->bf) TRY(dev_alloc(m, (void**)&m->gu_f32, tmax * 2 * I * 4));
+    int64_t pmax = 1;
+    if (m->bf) {
+      const int64_t shapes[5][2] = {{nq, D}, {D, H * hd}, {2 * I, D}, {D, I}, {V, D}};
+      for (auto& sh : shapes) {
+        const int sp = plan_gemv_splits((int)sh[0], c.max_batch, (int)sh[1]);
+        if (sp > 1) pmax = std::max<int64_t>(pmax, sp * sh[0]);
+      }
+    }
+    TRY(dev_alloc(m, (void**)&m->parts, pmax * c.max_batch * 4));
+    const int64_t nch = plan_decode_chunks(c.max_seq);
+    TRY(dev_alloc(m, (void**)&m->attn_part, (int64_t)c.max_batch * H * nch * (hd + 2) * 4));
+    TRY(dev_alloc(m, (void**)&m->d_len, (size_t)c.max_batch * sizeof(int32_t)));
+    HTRY(hipMemsetAsync(m->d_len, 0, (size_t)c.max_batch * sizeof(int32_t), s));
+  }
+  m->h_len.assign(c.max_batch, 0);
+  HTRY(hipStreamCreateWithFlags(&m->cap_stream, hipStreamNonBlocking));
+  HTRY(hipStreamSynchronize(s));
+#undef TRY
+#undef HTRY
+  *out = m;
+  return AXON_OK;
+}
+
+extern "C" int axon_prefill(axon_model* m, int32_t batch, const int32_t* d_tokens, const int32_t* d_cu_seqlens,
+                            const int32_t* h_cu_seqlens, const int32_t* h_block_table, int32_t block_table_stride,
+                            int32_t all_logits, float* d_logits, int32_t* d_next_tokens, void* stream) {
+  g_err.clear();
+  if (!m) return fail(AXON_E_INVALID, "model is NULL");
+  const axon_config& c = m->cfg;
+  if (batch < 1) return fail(AXON_E_INVALID, "batch must be >= 1");
+  if (batch > c.max_batch)
+    return fail(AXON_E_CAPACITY, "batch " + std::to_string(batch) + " exceeds max_batch " + std::to_string(c.max_batch));
+  if (!d_tokens || !d_cu_seqlens || !h_cu_seqlens || !d_next_tokens)
+    return fail(AXON_E_INVALID, "d_tokens, d_cu_seqlens, h_cu_seqlens and d_next_tokens must be non-NULL");
+  if (all_logits != 0 && all_logits != 1) return fail(AXON_E_INVALID, "all_logits must be 0 or 1");
+  if (all_logits && !d_logits) return fail(AXON_E_INVALID, "all_logits requires d_logits");
+  if (h_cu_seqlens[0] != 0) return fail(AXON_E_INVALID, "cu_seqlens[0] must be 0");
+  int64_t total = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int64_t sb = (int64_t)h_cu_seqlens[b + 1] - h_cu_seqlens[b];
+    if (sb < 1) return fail(AXON_E_INVALID, "sequence " + std::to_string(b) + " has length " + std::to_string(sb) + " (must be >= 1)");
+    if (sb > c.max_seq)
+      return fail(AXON_E_CAPACITY, "sequence " + std::to_string(b) + " has length " + std::to_string(sb) +
+                                       " > max_seq " + std::to_string(c.max_seq));
+    total += sb;
+  }
+  if (total > m->rows)
+    return fail(AXON_E_CAPACITY, "prefill of " + std::to_string(total) + " tokens exceeds max_tokens " + std::to_string(m->rows));
+  hipStream_t s = (hipStream_t)stream;
+  if (m->paged()) {
+    if (!h_block_table) return fail(AXON_E_INVALID, "a paged cache needs h_block_table");
+    if (block_table_stride < 1) return fail(AXON_E_INVALID, "block_table_stride must be >= 1");
+    const int cols = std::min(block_table_stride, m->bt_stride);
+    std::vector<char> used(c.kv_num_pages, 0);
+    for (int b = 0; b < batch; ++b) {
+      const int sb = h_cu_seqlens[b + 1] - h_cu_seqlens[b];
+      const int need = (sb + m->ps - 1) / m->ps;
+      if (need > cols)
+        return fail(AXON_E_CAPACITY, "page table row " + std::to_string(b) + " has " + std::to_string(cols) +
+                                         " columns, the prompt needs " + std::to_string(need));
+      for (int j = 0; j < cols; ++j) {
+        const int p = h_block_table[(int64_t)b * block_table_stride + j];
+        if (p < 0) {
+          if (j < need)
+            return fail(AXON_E_CAPACITY, "page table row " + std::to_string(b) + " has no page for block " + std::to_string(j));
+          continue;
+        }
+        if (p >= c.kv_num_pages)
+          return fail(AXON_E_CAPACITY, "page id " + std::to_string(p) + " out of range [0, " + std::to_string(c.kv_num_pages) + ")");
+        if (used[p]) return fail(AXON_E_INVALID, "page id " + std::to_string(p) + " appears twice");
+        used[p] = 1;
+      }
+    }
+    // the previous upload must have left the pinned staging copy
+    HIP_TRY(hipEventSynchronize(m->bt_copied));
+    for (int b = 0; b < c.max_batch; ++b)
+      for (int j = 0; j < m->bt_stride; ++j)
+        m->h_bt[(int64_t)b * m->bt_stride + j] =
+            (b < batch && j < cols) ? h_block_table[(int64_t)b * block_table_stride + j] : -1;
+    HIP_TRY(hipMemcpyAsync(m->d_bt, m->h_bt, (size_t)c.max_batch * m->bt_stride * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s));
+    HIP_TRY(hipEventRecord(m->bt_copied, s));
+  } else if (h_block_table) {
+    return fail(AXON_E_INVALID, "h_block_table given for a contiguous cache");
+  }
+  if (m->bf)
+    enqueue_prefill<bf16>(m, batch, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, all_logits, d_logits,
+                          d_next_tokens, s);
+  else
+    enqueue_prefill<float>(m, batch, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, all_logits, d_logits,
+                           d_next_tokens, s);
+  int rc = check_launch("prefill");
+  if (rc) return rc;
+  for (int b = 0; b < c.max_batch; ++b) m->h_len[b] = b < batch ? h_cu_seqlens[b + 1] - h_cu_seqlens[b] : 0;
+  m->active = batch;
+  return AXON_OK;
+}
+
+extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_tokens, float* d_logits,
+                                int32_t* d_next_tokens, void* stream) {
+  g_err.clear();
+  if (!m) return fail(AXON_E_INVALID, "model is NULL");
+  if (!d_tokens || !d_next_tokens) return fail(AXON_E_INVALID, "d_tokens and d_next_tokens must be non-NULL");
+  if (batch < 1) return fail(AXON_E_INVALID, "batch must be >= 1");
+  if (batch > m->active)
+    return fail(AXON_E_CAPACITY, "batch " + std::to_string(batch) + " exceeds the " + std::to_string(m->active) +
+                                     " active slots of the last prefill");
+  for (int b = 0; b < batch; ++b) {
+    const int pos = m->h_len[b];
+    if (pos + 1 > m->cfg.max_seq)
+      return fail(AXON_E_CAPACITY, "slot " + std::to_string(b) + " is full (max_seq " + std::to_string(m->cfg.max_seq) + ")");
+    if (m->paged() && m->h_bt[(int64_t)b * m->bt_stride + pos / m->ps] < 0)
+      return fail(AXON_E_CAPACITY, "slot " + std::to_string(b) + " has no page for position " + std::to_string(pos));
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (m->use_graphs && !m->timing) {
+    GraphKey key{batch, d_tokens, d_logits, d_next_tokens};
+    auto it = m->graphs.find(key);
+    if (it == m->graphs.end()) {
+      hipGraph_t g = nullptr;
+      HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
+      if (m->bf) enqueue_decode<bf16>(m, batch, d_tokens, d_logits, d_next_tokens, m->cap_stream);
+      else enqueue_decode<float>(m, batch, d_tokens, d_logits, d_next_tokens, m->cap_stream);
+      hipError_t le = hipGetLastError();
+      hipError_t ce = hipStreamEndCapture(m->cap_stream, &g);
+      if (le != hipSuccess || ce != hipSuccess) {
+        if (g) (void)hipGraphDestroy(g);
+        return fail(AXON_E_HIP, std::string("decode graph capture failed: ") +
+                                    hipGetErrorString(le != hipSuccess ? le : ce));
+      }
+      hipGraphExec_t ex = nullptr;
+      hipError_t ie = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(g);
+      if (ie != hipSuccess) return fail(AXON_E_HIP, std::string("decode graph instantiate: ") + hipGetErrorString(ie));
+      it = m->graphs.emplace(key, ex).first;
+    }
+    HIP_TRY(hipGraphLaunch(it->second, s));
+  } else {
+    if (m->bf) enqueue_decode<bf16>(m, batch, d_tokens, d_logits, d_next_tokens, s);
+    else enqueue_decode<float>(m, batch, d_tokens, d_logits, d_next_tokens, s);
+    int rc = check_launch("decode");
+    if (rc) return rc;
+  }
+  for (int b = 0; b < batch; ++b) m->h_len[b] += 1;
+  return AXON_OK;
+}
+
+extern "C" int axon_slot_lengths(const axon_model* m, int32_t* lens, int32_t n) {
+  g_err.clear();
+  if (!m) return fail(AXON_E_INVALID, "model is NULL");
+  if (n > 0 && !lens) return fail(AXON_E_INVALID, "lens is NULL");
+  for (int i = 0; i < n && i < m->cfg.max_batch; ++i) lens[i] = m->h_len[i];
+  return m->active;
+}
+
+extern "C" int axon_timing_enable(axon_model* m, int32_t enable) {
+  g_err.clear();
+  if (!m) return fail(AXON_E_INVALID, "model is NULL");
+  if (enable != 0 && enable != 1) return fail(AXON_E_INVALID, "enable must be 0 or 1");
+  m->timing = enable == 1;
+  m->trecs.clear();
+  m->tnext = 0;
+  return AXON_OK;
+}
+
+extern "C" int axon_timing_records(axon_model* m, int32_t* cls, int32_t* dims, float* ms, int32_t cap) {
+  g_err.clear();
+  if (!m) return fail(AXON_E_INVALID, "model is NULL");
+  if (cap > 0 && (!cls || !dims || !ms)) return fail(AXON_E_INVALID, "output arrays are NULL");
+  for (int i = 0; i < (int)m->trecs.size() && i < cap; ++i) {
+    const TimingRec& r = m->trecs[i];
+    HIP_TRY(hipEventSynchronize(r.b));
+    float t = 0.f;
+    HIP_TRY(hipEventElapsedTime(&t, r.a, r.b));
+    cls[i] = r.cls;
+    dims[3 * i] = r.d0;
+    dims[3 * i + 1] = r.d1;
+    dims[3 * i + 2] = r.d2;
+    ms[i] = t;
+  }
+  return (int)m->trecs.size();
+}
+
+extern "C" void axon_free(axon_model* m) {
+  if (m) release(m);
+}

@@ -1,0 +1,81 @@
+// Shared device-side types and helpers for the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+
+#define AXON_DEV __device__ __forceinline__
+
+AXON_DEV float to_f32(float v) { return v; }
+AXON_DEV float to_f32(bf16 v) { return (float)v; }
+template <typename T> AXON_DEV T from_f32(float v);
+template <> AXON_DEV float from_f32<float>(float v) { return v; }
+template <> AXON_DEV bf16 from_f32<bf16>(float v) { return (bf16)v; }  // round to nearest even
+
+// Sum over the 64 lanes of a wavefront.
+AXON_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+AXON_DEV float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  return v;
+}
+
+// Block-wide sum for blockDim.x a multiple of 64 (<= 1024); every thread gets the result.
+AXON_DEV float block_sum(float v, float* red /* >= 16 floats of shared memory */) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nw = blockDim.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float s = 0.f;
+  for (int i = 0; i < nw; ++i) s += red[i];
+  return s;
+}
+
+// Sequence index of packed token t given prefix sums cu[0..nseq] (cu[0] = 0).
+AXON_DEV int seq_of_token(const int32_t* __restrict__ cu, int nseq, int t) {
+  int lo = 0, hi = nseq - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (cu[mid] <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// KV-cache addressing.  One layout serves the contiguous and the paged cache:
+// a "page" holds ``ps`` consecutive positions of one sequence for every kv head.
+//   K  page: [KV][ps][hd]      (row per position, head_dim contiguous)
+//   V^T page: [KV][hd][ps]     (row per head-dim index, positions contiguous)
+// Contiguous cache: page = slot, ps = per-slot capacity.  Paged cache: page =
+// block_table[slot * bt_stride + pos / ps].
+struct KVView {
+  void* k;            // this layer's K pages
+  void* v;            // this layer's V^T pages
+  const int32_t* bt;  // block table or nullptr (contiguous)
+  int bt_stride;
+  int ps;             // positions per page
+  int kv_heads;
+  int hd;
+};
+
+AXON_DEV int64_t kv_page(const KVView& c, int slot, int pos) {
+  return c.bt ? (int64_t)c.bt[(int64_t)slot * c.bt_stride + pos / c.ps] : (int64_t)slot;
+}
+// element offset of K[pos][d=0] for (slot, kv head)
+AXON_DEV int64_t k_off(const KVView& c, int slot, int kvh, int pos) {
+  return ((kv_page(c, slot, pos) * c.kv_heads + kvh) * c.ps + pos % c.ps) * (int64_t)c.hd;
+}
+// element offset of V^T[d][pos] for (slot, kv head)
+AXON_DEV int64_t vt_off(const KVView& c, int slot, int kvh, int d, int pos) {
+  return ((kv_page(c, slot, pos) * c.kv_heads + kvh) * (int64_t)c.hd + d) * c.ps + pos % c.ps;
+}

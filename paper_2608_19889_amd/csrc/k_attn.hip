@@ -1,0 +1,407 @@
+// Causal grouped-query attention over the KV cache.
+//
+// softmax(q k^T / sqrt(hd)) v per query head, keys 0..pos of the query's own
+// sequence, kv head = query head / (H / KV).  Softmax runs online in base 2
+// with float statistics.
+//
+// Both bf16 kernels compute S^T = K Q^T (keys as MFMA rows, queries as
+// columns), so that a lane owns one query column: the row maximum and sum of a
+// query are then in-lane reductions plus one or two cross-lane exchanges, and
+// the probabilities already sit in the lane layout of the B operand of the
+// following O^T = V^T P^T product (the k index of that product is permuted to
+// match, and V^T is read with the same permutation from the transposed V pages).
+#include "common.h"
+#include "kernels.h"
+
+namespace axon {
+
+constexpr float LOG2E = 1.4426950408889634f;
+
+// ============================================================================
+// Prefill (bf16): a workgroup = 128 queries of one head of one sequence, four
+// wavefronts of 32 queries; key tiles of 64 staged in LDS (K row-major, V
+// transposed), v_mfma_f32_32x32x16_bf16 for both products.
+// ============================================================================
+constexpr int PQ = 128, PK = 64;
+
+template <int HD>
+__global__ void __launch_bounds__(256) attn_prefill_bf16_kernel(const bf16* __restrict__ q, KVView kv,
+                                                                bf16* __restrict__ o, int nseq,
+                                                                const int32_t* __restrict__ cu, int H) {
+  constexpr int KST = HD + 8;  // padded K row (elements)
+  constexpr int VST = PK + 8;  // padded V^T row (elements)
+  __shared__ __attribute__((aligned(16))) bf16 ks[PK * KST];
+  __shared__ __attribute__((aligned(16))) bf16 vs[HD * VST];
+
+  // locate (sequence, query tile) of this workgroup
+  int seq = 0, tile = blockIdx.x;
+  for (; seq < nseq; ++seq) {
+    const int nt = (cu[seq + 1] - cu[seq] + PQ - 1) / PQ;
+    if (tile < nt) break;
+    tile -= nt;
+  }
+  const int head = blockIdx.y;
+  const int group = H / kv.kv_heads;
+  const int kvh = head / group;
+  const int S = cu[seq + 1] - cu[seq];
+  const int tok0 = cu[seq];
+  const int q0 = tile * PQ;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int qw0 = q0 + wave * 32;
+  const int myq = qw0 + (lane & 31);
+  const int hl = lane >> 5;
+
+  // Q^T fragments (B operand): column = query, k = head-dim
+  bf16x8 qf[HD / 16];
+  {
+    const bf16x8 z = {};
+    const bf16* qp = q + ((int64_t)(tok0 + myq) * H + head) * HD + hl * 8;
+#pragma unroll
+    for (int k = 0; k < HD / 16; ++k) qf[k] = myq < S ? *(const bf16x8*)(qp + k * 16) : z;
+  }
+
+  f32x16 acc_o[HD / 32];
+#pragma unroll
+  for (int d = 0; d < HD / 32; ++d) acc_o[d] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;
+  const float sc = LOG2E / sqrtf((float)HD);
+
+  const int kend = min(S, q0 + PQ);  // keys needed by the workgroup
+  const int ntiles = (kend + PK - 1) / PK;
+  for (int kt = 0; kt < ntiles; ++kt) {
+    const int j0 = kt * PK;
+    // ---- stage K [64][HD] and V^T [HD][64]
+    {
+      constexpr int KCH = HD / 8;
+      for (int idx = tid; idx < PK * KCH; idx += 256) {
+        const int r = idx / KCH, c = idx % KCH;
+        const int j = j0 + r;
+        bf16x8 v = {};
+        if (j < S) v = *(const bf16x8*)((const bf16*)kv.k + k_off(kv, seq, kvh, j) + c * 8);
+        *(bf16x8*)(ks + r * KST + c * 8) = v;
+      }
+      for (int idx = tid; idx < HD * (PK / 8); idx += 256) {
+        const int d = idx / (PK / 8), c = idx % (PK / 8);
+        const int j = j0 + c * 8;
+        bf16x8 v = {};
+        if (j < S) v = *(const bf16x8*)((const bf16*)kv.v + vt_off(kv, seq, kvh, d, j));
+        *(bf16x8*)(vs + d * VST + c * 8) = v;
+      }
+    }
+    __syncthreads();
+    if (j0 <= qw0 + 31 && qw0 < S) {
+      // ---- S^T = K Q^T for 2 blocks of 32 keys
+      f32x16 s[2];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        s[r] = f32x16{};
+        const bf16* kr = ks + (r * 32 + (lane & 31)) * KST + hl * 8;
+#pragma unroll
+        for (int k = 0; k < HD / 16; ++k)
+          s[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(kr + k * 16), qf[k], s[r], 0, 0, 0);
+      }
+      // ---- mask, scale, online softmax (lane = query column)
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = j0 + r * 32 + (i / 4) * 8 + hl * 4 + (i % 4);
+          const float v = (key <= myq && key < S) ? s[r][i] * sc : -INFINITY;
+          s[r][i] = v;
+          mloc = fmaxf(mloc, v);
+        }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      const float m_new = fmaxf(m_run, mloc);
+      const float m_ref = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = exp2f(m_run - m_ref);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int d = 0; d < HD / 32; ++d) acc_o[d] *= alpha;
+      bf16x8 pb[2][2];
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float p = exp2f(s[r][i] - m_ref);
+          l_run += p;
+          pb[r][i / 8][i % 8] = (bf16)p;
+        }
+      // ---- O^T += V^T P^T; the k index of block (r, h) covers keys
+      //      r*32 + h*16 + {hl*4 + 0..3, 8 + hl*4 + 0..3}
+#pragma unroll
+      for (int d = 0; d < HD / 32; ++d) {
+        const bf16* vr = vs + (d * 32 + (lane & 31)) * VST + hl * 4;
+#pragma unroll
+        for (int r = 0; r < 2; ++r)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const bf16x4 lo = *(const bf16x4*)(vr + r * 32 + h * 16);
+            const bf16x4 hi = *(const bf16x4*)(vr + r * 32 + h * 16 + 8);
+            const bf16x8 va = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            acc_o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[r][h], acc_o[d], 0, 0, 0);
+          }
+      }
+    }
+    __syncthreads();
+  }
+  if (myq >= S) return;
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = 1.f / l_tot;
+  bf16* op = o + ((int64_t)(tok0 + myq) * H + head) * HD;
+#pragma unroll
+  for (int d = 0; d < HD / 32; ++d)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int dd = d * 32 + g * 8 + hl * 4;
+      *(bf16x4*)(op + dd) = bf16x4{(bf16)(acc_o[d][g * 4 + 0] * inv), (bf16)(acc_o[d][g * 4 + 1] * inv),
+                                   (bf16)(acc_o[d][g * 4 + 2] * inv), (bf16)(acc_o[d][g * 4 + 3] * inv)};
+    }
+}
+
+// ============================================================================
+// Decode (bf16): one query per slot.  Workgroup = (key chunk, kv head, slot),
+// four wavefronts; each wavefront takes 32-key steps with the group's query
+// heads as the columns of v_mfma_f32_16x16x32_bf16 (up to 16 heads per group).
+// K and V^T fragments are loaded straight from HBM.  Each workgroup writes an
+// unnormalized partial (o, max, sum) per head; a combine kernel merges chunks.
+// ============================================================================
+constexpr int DCH = 256;  // keys per chunk (4 wavefronts x 2 steps x 32)
+
+template <int HD>
+__global__ void __launch_bounds__(256) attn_decode_bf16_kernel(const bf16* __restrict__ q, KVView kv,
+                                                               float* __restrict__ part, int H,
+                                                               const int32_t* __restrict__ len,
+                                                               int max_chunks) {
+  __shared__ float sm[4][16], sl[4][16];
+  __shared__ float so[4][HD][17];
+  const int chunk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int ctx = len[b] + 1;
+  const int c0 = chunk * DCH;
+  if (c0 >= ctx) return;
+  const int group = H / kv.kv_heads;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = lane & 15, gq = lane >> 4;
+  const float sc = LOG2E / sqrtf((float)HD);
+
+  bf16x8 qf[HD / 32];
+  {
+    const bf16x8 z = {};
+    const bf16* qp = q + ((int64_t)b * H + kvh * group + col) * HD + gq * 8;
+#pragma unroll
+    for (int k = 0; k < HD / 32; ++k) qf[k] = col < group ? *(const bf16x8*)(qp + k * 32) : z;
+  }
+  f32x4 acc[HD / 16];
+#pragma unroll
+  for (int d = 0; d < HD / 16; ++d) acc[d] = f32x4{};
+  float m_run = -INFINITY, l_run = 0.f;
+  const bf16* kb = (const bf16*)kv.k;
+  const bf16* vb = (const bf16*)kv.v;
+
+  for (int step = wave; step * 32 < DCH; step += 4) {
+    const int j0 = c0 + step * 32;
+    if (j0 >= ctx) break;
+    f32x4 s[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+      const int key = j0 + blk * 16 + col;
+      const bool ok = key < ctx;  // keys past the context may have no page: never dereferenced
+      const bf16* kp = kb + (ok ? k_off(kv, b, kvh, key) : 0) + gq * 8;
+      bf16x8 kf[HD / 32];
+      const bf16x8 z = {};
+#pragma unroll
+      for (int k = 0; k < HD / 32; ++k) kf[k] = ok ? *(const bf16x8*)(kp + k * 32) : z;
+      s[blk] = f32x4{};
+#pragma unroll
+      for (int k = 0; k < HD / 32; ++k) s[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[k], qf[k], s[blk], 0, 0, 0);
+    }
+    // s[blk][i]: key j0 + blk*16 + gq*4 + i, head column ``col``
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = j0 + blk * 16 + gq * 4 + i;
+        const float v = key < ctx ? s[blk][i] * sc : -INFINITY;
+        s[blk][i] = v;
+        mloc = fmaxf(mloc, v);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float m_new = fmaxf(m_run, mloc);  // finite: key j0 < ctx is in this step
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d) acc[d] *= alpha;
+    bf16x8 pb;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = exp2f(s[blk][i] - m_new);
+        l_run += p;
+        pb[blk * 4 + i] = (bf16)p;
+      }
+    // V^T fragments: row d, keys {j0 + gq*4 + 0..3, j0 + 16 + gq*4 + 0..3}
+    const int ja = j0 + gq * 4, jb = j0 + 16 + gq * 4;
+    const bool oka = ja < ctx, okb = jb < ctx;
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d) {
+      const int dd = d * 16 + col;
+      const bf16x4 z4 = {};
+      const bf16x4 lo = oka ? *(const bf16x4*)(vb + vt_off(kv, b, kvh, dd, ja)) : z4;
+      const bf16x4 hi = okb ? *(const bf16x4*)(vb + vt_off(kv, b, kvh, dd, jb)) : z4;
+      const bf16x8 va = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, acc[d], 0, 0, 0);
+    }
+  }
+  // per-wave statistics: m uniform over the 4 lane groups of a column; l summed
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+  if (gq == 0) {
+    sm[wave][col] = m_run;
+    sl[wave][col] = l_run;
+  }
+  // acc[d][i]: head-dim d*16 + gq*4 + i, column ``col``
+#pragma unroll
+  for (int d = 0; d < HD / 16; ++d)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) so[wave][d * 16 + gq * 4 + i][col] = acc[d][i];
+  __syncthreads();
+  // merge the four wavefronts; thread -> (head column, head-dim slice)
+  for (int idx = threadIdx.x; idx < group * HD; idx += 256) {
+    const int c = idx / HD, d = idx % HD;
+    float M = -INFINITY;
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, sm[w][c]);
+    float L = 0.f, O = 0.f;
+    for (int w = 0; w < 4; ++w) {
+      const float f = sm[w][c] == -INFINITY ? 0.f : exp2f(sm[w][c] - M);
+      L += f * sl[w][c];
+      O += f * so[w][d][c];
+    }
+    float* pp = part + (((int64_t)b * H + kvh * group + c) * max_chunks + chunk) * (HD + 2);
+    pp[d] = O;
+    if (d == 0) {
+      pp[HD] = M;
+      pp[HD + 1] = L;
+    }
+  }
+}
+
+// merge chunk partials of one (slot, head): o = sum_c 2^(m_c - M) o_c / sum_c 2^(m_c - M) l_c
+template <typename T, int HD>
+__global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restrict__ part, T* __restrict__ o, int H,
+                                                          const int32_t* __restrict__ len, int max_chunks) {
+  const int b = blockIdx.y, h = blockIdx.x, d = threadIdx.x;
+  const int ctx = len[b] + 1;
+  const int nch = (ctx + DCH - 1) / DCH;
+  const float* pp = part + ((int64_t)b * H + h) * max_chunks * (HD + 2);
+  float M = -INFINITY;
+  for (int c = 0; c < nch; ++c) M = fmaxf(M, pp[c * (HD + 2) + HD]);
+  float L = 0.f, O = 0.f;
+  for (int c = 0; c < nch; ++c) {
+    const float f = exp2f(pp[c * (HD + 2) + HD] - M);
+    L += f * pp[c * (HD + 2) + HD + 1];
+    O += f * pp[c * (HD + 2) + d];
+  }
+  o[((int64_t)b * H + h) * HD + d] = from_f32<T>(O / L);
+}
+
+// ============================================================================
+// float32 check mode: one thread per (query token, head), online softmax over
+// the keys of its sequence read from the cache.  Serves prefill (cu) and
+// decode (len).
+// ============================================================================
+template <int HD>
+__global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ q, KVView kv, float* __restrict__ o,
+                                                      int T_tokens, int nseq, const int32_t* __restrict__ cu,
+                                                      const int32_t* __restrict__ len, int H) {
+  const int t = blockIdx.x * 64 + threadIdx.x;
+  const int head = blockIdx.y;
+  if (t >= T_tokens) return;
+  int slot, pos;
+  if (len) {
+    slot = t;
+    pos = len[t];
+  } else {
+    slot = seq_of_token(cu, nseq, t);
+    pos = t - cu[slot];
+  }
+  const int kvh = head / (H / kv.kv_heads);
+  float qv[HD], acc[HD];
+  const float* qp = q + ((int64_t)t * H + head) * HD;
+  for (int d = 0; d < HD; ++d) { qv[d] = qp[d]; acc[d] = 0.f; }
+  const float sc = LOG2E / sqrtf((float)HD);
+  float m = -INFINITY, l = 0.f;
+  const float* kb = (const float*)kv.k;
+  const float* vb = (const float*)kv.v;
+  for (int j = 0; j <= pos; ++j) {
+    const float* kp = kb + k_off(kv, slot, kvh, j);
+    float s = 0.f;
+    for (int d = 0; d < HD; ++d) s = fmaf(qv[d], kp[d], s);
+    s *= sc;
+    const float m_new = fmaxf(m, s);
+    const float alpha = exp2f(m - m_new), p = exp2f(s - m_new);
+    l = l * alpha + p;
+    for (int d = 0; d < HD; ++d) acc[d] = acc[d] * alpha + p * vb[vt_off(kv, slot, kvh, d, j)];
+    m = m_new;
+  }
+  float* op = o + ((int64_t)t * H + head) * HD;
+  for (int d = 0; d < HD; ++d) op[d] = acc[d] / l;
+}
+
+// ---------------------------------------------------------------- launchers
+
+template <typename T>
+void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, const int32_t* cu,
+                         const int32_t* h_cu, int H, hipStream_t s) {
+  if (T_tokens <= 0) return;
+  if constexpr (sizeof(T) == 4) {
+    dim3 grid((T_tokens + 63) / 64, H);
+    if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H);
+    else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H);
+  } else {
+    int tiles = 0;
+    for (int b = 0; b < nseq; ++b) tiles += (h_cu[b + 1] - h_cu[b] + PQ - 1) / PQ;
+    dim3 grid(tiles, H);
+    if (kv.hd == 64) attn_prefill_bf16_kernel<64><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H);
+    else attn_prefill_bf16_kernel<128><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H);
+  }
+}
+
+int plan_decode_chunks(int max_ctx) { return (max_ctx + DCH - 1) / DCH; }
+
+template <typename T>
+void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len, int max_ctx,
+                        hipStream_t s) {
+  if (B <= 0) return;
+  if constexpr (sizeof(T) == 4) {
+    dim3 grid((B + 63) / 64, H);
+    if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H);
+    else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H);
+  } else {
+    const int nch = plan_decode_chunks(max_ctx);
+    dim3 grid(nch, kv.kv_heads, B);
+    dim3 cgrid(H, B);
+    if (kv.hd == 64) {
+      attn_decode_bf16_kernel<64><<<grid, 256, 0, s>>>(q, kv, part, H, len, nch);
+      attn_combine_kernel<T, 64><<<cgrid, 64, 0, s>>>(part, o, H, len, nch);
+    } else {
+      attn_decode_bf16_kernel<128><<<grid, 256, 0, s>>>(q, kv, part, H, len, nch);
+      attn_combine_kernel<T, 128><<<cgrid, 128, 0, s>>>(part, o, H, len, nch);
+    }
+  }
+}
+
+template void launch_attn_prefill<float>(const float*, KVView, float*, int, int, const int32_t*, const int32_t*, int,
+                                         hipStream_t);
+template void launch_attn_prefill<bf16>(const bf16*, KVView, bf16*, int, int, const int32_t*, const int32_t*, int,
+                                        hipStream_t);
+template void launch_attn_decode<float>(const float*, KVView, float*, float*, int, int, const int32_t*, int,
+                                        hipStream_t);
+template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int, int, const int32_t*, int,
+                                       hipStream_t);
+
+}  // namespace axon

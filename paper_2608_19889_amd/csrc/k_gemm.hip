@@ -1,0 +1,389 @@
+// Projection GEMMs: out[t][n] = sum_k X[t][k] * W[n][k] (the F.linear
+// convention: W is [out, in] row-major, X is tokens x in).
+//
+// Both operands are K-contiguous, so the kernels compute C^T = W X^T with W as
+// the MFMA A operand (rows = output features) and X as the B operand (columns
+// = tokens): every lane's operand fragment is 8 consecutive k values, one
+// 16-byte load, from either operand.
+#include "common.h"
+#include "kernels.h"
+
+namespace axon {
+
+AXON_DEV float silu_f(float z) { return z / (1.f + __expf(-z)); }
+
+// Store (or add, for the residual stream) four consecutive output columns of
+// which ``left`` are inside the matrix.
+template <bool ADD>
+AXON_DEV void store_cols(float* p, f32x4 v, int left) {
+  if (left >= 4) {
+    if constexpr (ADD) v += *(const f32x4*)p;
+    *(f32x4*)p = v;
+  } else {
+    for (int j = 0; j < left; ++j) p[j] = ADD ? p[j] + v[j] : v[j];
+  }
+}
+
+// ============================================================================
+// Prefill GEMM: 128 (W rows) x 128 (tokens) x 64 (k) tiles, 4 wavefronts in a
+// 2 x 2 arrangement, each owning a 64 x 64 sub-tile = 2 x 2 blocks of
+// v_mfma_f32_32x32x16_bf16.  Tiles are staged through LDS, double-buffered;
+// a row of 64 k values is 8 chunks of 16 bytes, stored at chunk ^ (row & 7)
+// so that the 16-byte fragment reads of 8 consecutive rows hit distinct banks.
+// ============================================================================
+namespace pf {
+constexpr int BN = 128, BM = 128, BK = 64, CH = BK / 8;
+}
+
+template <int EPI>
+__global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__ W, const bf16* __restrict__ X,
+                                                        int N, int M, int K, EpiArgs ep) {
+  using namespace pf;
+  __shared__ bf16x8 lds[2][2][BN * CH];  // [buffer][0 = W, 1 = X][row * 8 + swizzled chunk]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+
+  // global -> register staging: 4 chunks of W and 4 of X per thread
+  bf16x8 ra[4], rb[4];
+  const bf16x8 zero8 = {};
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = tid + i * 256, row = idx >> 3, ch = idx & 7;
+      const int n = n0 + row, m = m0 + row;
+      ra[i] = n < N ? *(const bf16x8*)(W + (int64_t)n * K + k0 + ch * 8) : zero8;
+      rb[i] = m < M ? *(const bf16x8*)(X + (int64_t)m * K + k0 + ch * 8) : zero8;
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = tid + i * 256, row = idx >> 3, ch = idx & 7;
+      lds[buf][0][row * CH + (ch ^ (row & 7))] = ra[i];
+      lds[buf][1][row * CH + (ch ^ (row & 7))] = rb[i];
+    }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+
+  const int nk = K / BK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * BK);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int ch = ks * 2 + (lane >> 5);
+      bf16x8 fa[2], fb[2];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const int ra_row = wr * 64 + r * 32 + (lane & 31);
+        const int rb_row = wc * 64 + r * 32 + (lane & 31);
+        fa[r] = lds[buf][0][ra_row * CH + (ch ^ (ra_row & 7))];
+        fb[r] = lds[buf][1][rb_row * CH + (ch ^ (rb_row & 7))];
+      }
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+    }
+    if (kt + 1 < nk) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // epilogue: acc[a][b][i] = C[n][t] with
+  //   n = n0 + wr*64 + a*32 + (i/4)*8 + (lane/32)*4 + i%4,  t = m0 + wc*64 + b*32 + lane%32
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int t = m0 + wc * 64 + b * 32 + (lane & 31);
+    if (t >= M) continue;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int nb = n0 + wr * 64 + a * 32;  // 32-aligned row block
+      if (nb >= N) continue;
+      if constexpr (EPI == EPI_SILU) {
+        // rows nb..nb+15 are gate rows, nb+16..nb+31 the matching up rows
+        bf16* out = (bf16*)ep.out_t + (int64_t)t * ep.ldo + (nb / 32) * 16;
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          const int f = g * 8 + (lane >> 5) * 4;
+          bf16x4 v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = (bf16)(silu_f(acc[a][b][g * 4 + j]) * acc[a][b][8 + g * 4 + j]);
+          *(bf16x4*)(out + f) = v;
+        }
+      } else {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = nb + g * 8 + (lane >> 5) * 4;
+          if (n >= N) continue;
+          float* p = ep.out_f32 + (int64_t)t * ep.ldo + n;
+          f32x4 v = {acc[a][b][g * 4 + 0], acc[a][b][g * 4 + 1], acc[a][b][g * 4 + 2], acc[a][b][g * 4 + 3]};
+          store_cols<EPI == EPI_RESID>(p, v, N - n);
+        }
+      }
+    }
+  }
+}
+
+void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi, const EpiArgs& ep,
+                      hipStream_t s) {
+  if (M <= 0) return;
+  dim3 grid((N + pf::BN - 1) / pf::BN, (M + pf::BM - 1) / pf::BM);
+  switch (epi) {
+    case EPI_F32: gemm_bf16_kernel<EPI_F32><<<grid, 256, 0, s>>>(W, X, N, M, K, ep); break;
+    case EPI_RESID: gemm_bf16_kernel<EPI_RESID><<<grid, 256, 0, s>>>(W, X, N, M, K, ep); break;
+    case EPI_SILU: gemm_bf16_kernel<EPI_SILU><<<grid, 256, 0, s>>>(W, X, N, M, K, ep); break;
+    default: break;
+  }
+}
+
+// ============================================================================
+// Decode GEMM (M = batch <= 64 tokens): HBM-bound on the weight stream.
+// Each wavefront owns 32 W rows (two 16-row blocks of
+// v_mfma_f32_16x16x32_bf16) and up to 64 token columns (NB blocks of 16); a
+// workgroup of 4 wavefronts covers 128 rows; the K range is split across
+// gridDim.y workgroups when there are too few row blocks to fill the chip.
+// W fragments are loaded straight from HBM (16 bytes per lane), four k-steps
+// in flight per wavefront.
+// ============================================================================
+template <int EPI, int NB>
+__global__ void __launch_bounds__(256) gemv_bf16_kernel(const bf16* __restrict__ W, const bf16* __restrict__ X,
+                                                        int N, int M, int K, int kchunk, EpiArgs ep) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nb = blockIdx.x * 128 + wave * 32;  // first of this wave's 32 rows
+  const int k_begin = blockIdx.y * kchunk;
+  const int k_end = min(K, k_begin + kchunk);
+  const int r16 = lane & 15, kq = (lane >> 4) * 8;
+  const bf16x8 zero8 = {};
+
+  const bf16* wrow[2];
+  bool wok[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int n = nb + r * 16 + r16;
+    wok[r] = n < N;
+    wrow[r] = W + (int64_t)(wok[r] ? n : 0) * K + kq;
+  }
+  const bf16* xrow[NB];
+  bool xok[NB];
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    const int t = c * 16 + r16;
+    xok[c] = t < M;
+    xrow[c] = X + (int64_t)(xok[c] ? t : 0) * K + kq;
+  }
+
+  f32x4 acc[2][NB];
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int c = 0; c < NB; ++c) acc[r][c] = f32x4{};
+
+  constexpr int U = 4;
+  int k = k_begin;
+  for (; k + 32 * U <= k_end; k += 32 * U) {
+    bf16x8 a[U][2], b[U][NB];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int r = 0; r < 2; ++r) a[u][r] = wok[r] ? *(const bf16x8*)(wrow[r] + k + u * 32) : zero8;
+#pragma unroll
+      for (int c = 0; c < NB; ++c) b[u][c] = xok[c] ? *(const bf16x8*)(xrow[c] + k + u * 32) : zero8;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int c = 0; c < NB; ++c)
+          acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][r], b[u][c], acc[r][c], 0, 0, 0);
+  }
+  for (; k < k_end; k += 32) {
+    bf16x8 a[2], b[NB];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) a[r] = wok[r] ? *(const bf16x8*)(wrow[r] + k) : zero8;
+#pragma unroll
+    for (int c = 0; c < NB; ++c) b[c] = xok[c] ? *(const bf16x8*)(xrow[c] + k) : zero8;
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+      for (int c = 0; c < NB; ++c)
+        acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[r], b[c], acc[r][c], 0, 0, 0);
+  }
+
+  // acc[r][c][i] = C[n][t], n = nb + r*16 + (lane/16)*4 + i, t = c*16 + lane%16
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    const int t = c * 16 + r16;
+    if (t >= M) continue;
+    if constexpr (EPI == EPI_SILU) {
+      if (nb >= N) continue;
+      bf16* out = (bf16*)ep.out_t + (int64_t)t * ep.ldo + (nb / 32) * 16 + (lane >> 4) * 4;
+      bf16x4 v;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = (bf16)(silu_f(acc[0][c][j]) * acc[1][c][j]);
+      *(bf16x4*)out = v;
+    } else {
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const int n = nb + r * 16 + (lane >> 4) * 4;
+        if (n >= N) continue;
+        float* p;
+        if constexpr (EPI == EPI_PART)
+          p = ep.out_f32 + blockIdx.y * ep.part_stride + (int64_t)t * ep.ldo + n;
+        else
+          p = ep.out_f32 + (int64_t)t * ep.ldo + n;
+        store_cols<EPI == EPI_RESID>(p, acc[r][c], N - n);
+      }
+    }
+  }
+}
+
+int plan_gemv_splits(int N, int M, int K) {
+  (void)M;
+  const int row_blocks = (N + 127) / 128;
+  const int kblocks = K / 128;  // at least 128 k per split
+  int s = 1;
+  while (row_blocks * s < 1024 && s * 2 <= kblocks && s < 16) s *= 2;
+  return s;
+}
+
+template <int EPI>
+static void gemv_dispatch(const bf16* W, const bf16* X, int N, int M, int K, int splits, const EpiArgs& ep,
+                          hipStream_t s) {
+  const int kchunk = ((K / splits) + 31) / 32 * 32;
+  dim3 grid((N + 127) / 128, splits);
+  const int nb = (M + 15) / 16;
+  switch (nb) {
+    case 1: gemv_bf16_kernel<EPI, 1><<<grid, 256, 0, s>>>(W, X, N, M, K, kchunk, ep); break;
+    case 2: gemv_bf16_kernel<EPI, 2><<<grid, 256, 0, s>>>(W, X, N, M, K, kchunk, ep); break;
+    case 3: gemv_bf16_kernel<EPI, 3><<<grid, 256, 0, s>>>(W, X, N, M, K, kchunk, ep); break;
+    default: gemv_bf16_kernel<EPI, 4><<<grid, 256, 0, s>>>(W, X, N, M, K, kchunk, ep); break;
+  }
+}
+
+void launch_gemv_bf16(const bf16* W, const bf16* X, int N, int M, int K, int splits, int epi,
+                      const EpiArgs& ep, hipStream_t s) {
+  if (M <= 0) return;
+  if (splits > 1) {
+    gemv_dispatch<EPI_PART>(W, X, N, M, K, splits, ep, s);
+    return;
+  }
+  switch (epi) {
+    case EPI_F32: gemv_dispatch<EPI_F32>(W, X, N, M, K, 1, ep, s); break;
+    case EPI_RESID: gemv_dispatch<EPI_RESID>(W, X, N, M, K, 1, ep, s); break;
+    case EPI_SILU: gemv_dispatch<EPI_SILU>(W, X, N, M, K, 1, ep, s); break;
+    default: gemv_dispatch<EPI_PART>(W, X, N, M, K, 1, ep, s); break;
+  }
+}
+
+// ============================================================================
+// float32 check-mode GEMM: 64 x 64 tiles, k-step 16, 256 threads with a 4 x 4
+// register block each, operands staged k-major in LDS.
+// ============================================================================
+template <int EPI>
+__global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__ W, const float* __restrict__ X,
+                                                       int N, int M, int K, EpiArgs ep) {
+  __shared__ float ws[16][68], xs[16][68];
+  const int tid = threadIdx.x;
+  const int n0 = blockIdx.x * 64, m0 = blockIdx.y * 64;
+  const int lr = tid >> 2, lk = (tid & 3) * 4;
+  const int tf = tid & 15, tt = tid >> 4;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    {
+      const int n = n0 + lr, m = m0 + lr;
+      f32x4 wv = {}, xv = {};
+      if (n < N) {
+        for (int j = 0; j < 4; ++j) wv[j] = (k0 + lk + j < K) ? W[(int64_t)n * K + k0 + lk + j] : 0.f;
+      }
+      if (m < M) {
+        for (int j = 0; j < 4; ++j) xv[j] = (k0 + lk + j < K) ? X[(int64_t)m * K + k0 + lk + j] : 0.f;
+      }
+      for (int j = 0; j < 4; ++j) { ws[lk + j][lr] = wv[j]; xs[lk + j][lr] = xv[j]; }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+      for (int i = 0; i < 4; ++i) { a[i] = ws[kk][tf * 4 + i]; b[i] = xs[kk][tt * 4 + i]; }
+      for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+  for (int j = 0; j < 4; ++j) {
+    const int t = m0 + tt * 4 + j;
+    if (t >= M) continue;
+    for (int i = 0; i < 4; ++i) {
+      const int n = n0 + tf * 4 + i;
+      if (n >= N) continue;
+      float* p = ep.out_f32 + (int64_t)t * ep.ldo + n;
+      if constexpr (EPI == EPI_RESID) *p += acc[i][j];
+      else *p = acc[i][j];
+    }
+  }
+}
+
+void launch_gemm_f32(const float* W, const float* X, int N, int M, int K, int epi, const EpiArgs& ep,
+                     hipStream_t s) {
+  if (M <= 0) return;
+  dim3 grid((N + 63) / 64, (M + 63) / 64);
+  if (epi == EPI_RESID) gemm_f32_kernel<EPI_RESID><<<grid, 256, 0, s>>>(W, X, N, M, K, ep);
+  else gemm_f32_kernel<EPI_F32><<<grid, 256, 0, s>>>(W, X, N, M, K, ep);
+}
+
+// ============================================================================
+// split-K reductions
+// ============================================================================
+template <typename T>
+__global__ void silu_reduce_kernel(const float* __restrict__ parts, int nparts, int64_t part_stride,
+                                   T* __restrict__ a, int M, int I) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)M * I) return;
+  const int t = (int)(idx / I), f = (int)(idx % I);
+  const int rg = (f / 16) * 32 + (f % 16);  // gate row in the interleaved layout; up row = rg + 16
+  const float* p = parts + (int64_t)t * 2 * I;
+  float g = 0.f, u = 0.f;
+  for (int s = 0; s < nparts; ++s) {
+    g += p[s * part_stride + rg];
+    u += p[s * part_stride + rg + 16];
+  }
+  a[idx] = from_f32<T>(silu_f(g) * u);
+}
+
+template <typename T>
+void launch_silu_reduce(const float* parts, int nparts, int64_t part_stride, T* a, int M, int I, hipStream_t s) {
+  const int64_t n = (int64_t)M * I;
+  if (n <= 0) return;
+  silu_reduce_kernel<T><<<(unsigned)((n + 255) / 256), 256, 0, s>>>(parts, nparts, part_stride, a, M, I);
+}
+template void launch_silu_reduce<float>(const float*, int, int64_t, float*, int, int, hipStream_t);
+template void launch_silu_reduce<bf16>(const float*, int, int64_t, bf16*, int, int, hipStream_t);
+
+__global__ void sum_reduce_kernel(const float* __restrict__ parts, int nparts, int64_t part_stride,
+                                  float* __restrict__ out, int64_t n) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n) return;
+  float v = 0.f;
+  for (int s = 0; s < nparts; ++s) v += parts[s * part_stride + idx];
+  out[idx] = v;
+}
+
+void launch_sum_reduce(const float* parts, int nparts, int64_t part_stride, float* out, int M, int N,
+                       hipStream_t s) {
+  const int64_t n = (int64_t)M * N;
+  if (n <= 0) return;
+  sum_reduce_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(parts, nparts, part_stride, out, n);
+}
+
+}  // namespace axon
