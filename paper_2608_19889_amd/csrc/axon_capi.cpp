@@ -4,6 +4,7 @@
 // per-(batch, pointers) HIP graph of the decode step.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -79,6 +80,7 @@ int validate_config(const axon_config& c) {
   if (c.n_heads <= 0 || c.n_kv_heads <= 0) return bad("n_heads and n_kv_heads must be >= 1");
   if (c.n_heads % c.n_kv_heads) return bad("n_heads must be a multiple of n_kv_heads");
   if (c.n_heads / c.n_kv_heads > 16) return bad("n_heads / n_kv_heads must be <= 16");
+  if (c.n_heads / c.n_kv_heads * c.head_dim > 1536) return bad("(n_heads / n_kv_heads) * head_dim must be <= 1536");
   if (c.head_dim != 64 && c.head_dim != 128) return bad("head_dim must be 64 or 128");
   if (c.intermediate <= 0 || c.intermediate % 64) return bad("intermediate must be a positive multiple of 64");
   if (c.vocab <= 0) return bad("vocab must be >= 1");
@@ -153,8 +155,12 @@ struct axon_model {
   void* hlast = nullptr;
   float* gu_f32 = nullptr;
   float* logits_int = nullptr;
-  float* parts = nullptr;
   float* attn_part = nullptr;
+  float* ss = nullptr;       // per-workgroup sums of squares of x rows
+  void* xg = nullptr;        // bf16(x * g) for the next normalized projection
+  int ss_n = 0;              // number of partials currently in ss
+  float* am_val = nullptr;   // per-workgroup argmax partials of the head
+  int32_t* am_idx = nullptr;
   int32_t* d_len = nullptr;
   std::vector<int> h_len;
   int active = 0;
@@ -251,30 +257,11 @@ void gemm_many(axon_model* m, const void* W, const void* X, int N, int M, int K,
   });
 }
 
-// Few-token projection; returns the number of float partials written (1 when
-// the epilogue was applied in place).
-template <typename T>
-int gemm_few(axon_model* m, const void* W, const void* X, int N, int M, int K, int epi, float* out_f32,
-             void* out_t, int ldo, hipStream_t s, int64_t* part_stride) {
-  if constexpr (sizeof(T) == 2) {
-    const int splits = plan_gemv_splits(N, M, K);
-    if (splits > 1) {
-      EpiArgs ep{m->parts, nullptr, N, (int64_t)M * N};
-      m->timed(0, N, M, K, s,
-               [&] { launch_gemv_bf16((const bf16*)W, (const bf16*)X, N, M, K, splits, EPI_PART, ep, s); });
-      *part_stride = (int64_t)M * N;
-      return splits;
-    }
-    EpiArgs ep{out_f32, out_t, ldo, 0};
-    m->timed(0, N, M, K, s, [&] { launch_gemv_bf16((const bf16*)W, (const bf16*)X, N, M, K, 1, epi, ep, s); });
-    *part_stride = 0;
-    return 0;
-  } else {
-    EpiArgs ep{out_f32, out_t, ldo, 0};
-    m->timed(0, N, M, K, s, [&] { launch_gemm_f32((const float*)W, (const float*)X, N, M, K, epi, ep, s); });
-    *part_stride = 0;
-    return 0;
-  }
+// Few-token projection in float32 check mode.
+void gemm_few_f32(axon_model* m, const void* W, const void* X, int N, int M, int K, int epi, float* out,
+                  int ldo, hipStream_t s) {
+  EpiArgs ep{out, nullptr, ldo, 0};
+  m->timed(0, N, M, K, s, [&] { launch_gemm_f32((const float*)W, (const float*)X, N, M, K, epi, ep, s); });
 }
 
 template <typename T>
@@ -311,57 +298,111 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
   if (all_logits) {
     gemm_many<T>(m, m->lm_head, h, V, Ttok, D, EPI_F32, d_logits, nullptr, V, s);
     launch_argmax_rows(d_logits, B, V, d_next, d_cu, s);
+  } else if constexpr (sizeof(T) == 2) {
+    GemvArgs ha{};
+    ha.W = (const bf16*)m->lm_head; ha.N = V; ha.K = D; ha.M = B; ha.X = (const bf16*)m->hlast;
+    ha.out_f32 = d_logits; ha.ldo = V; ha.am_val = m->am_val; ha.am_idx = m->am_idx;
+    m->timed(0, V, B, D, s, [&] { launch_gemv_fused(ha, GV_HEAD, s); });
+    const int hr = gemv_rows(V, D, B, GV_HEAD);
+    launch_argmax_final(m->am_val, m->am_idx, (V + hr - 1) / hr, B, d_next, nullptr, s);
   } else {
     float* dst = d_logits ? d_logits : m->logits_int;
-    int64_t ps = 0;
-    const int np = gemm_few<T>(m, m->lm_head, m->hlast, V, B, D, EPI_F32, dst, nullptr, V, s, &ps);
-    if (np > 1) launch_sum_reduce(m->parts, np, ps, dst, B, V, s);
+    gemm_few_f32(m, m->lm_head, m->hlast, V, B, D, EPI_F32, dst, V, s);
     launch_argmax(dst, B, V, d_next, nullptr, s);
   }
 }
 
-template <typename T>
-void enqueue_decode(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next, hipStream_t s) {
+// Decode step, float32 check mode: GEMM + separate normalization kernels.
+void enqueue_decode_f32(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
+                        hipStream_t s) {
+  using T = float;
   const int D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V(), nq = m->nqkv();
   const float eps = m->cfg.rms_eps;
   T* h = (T*)m->h;
-  int64_t ps = 0;
   launch_embed_rmsnorm<T>(d_tokens, (const T*)m->embed, (const T*)m->layers[0].gin, m->x, h, B, D, V, eps, s);
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const LayerW& w = m->layers[l];
     KVView kv = m->kv(l, m->paged());
-    int np = gemm_few<T>(m, w.wqkv, h, nq, B, D, EPI_F32, m->qkv, nullptr, nq, s, &ps);
-    if (np > 1)
-      launch_rope_kv<T>(m->parts, np, ps, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, B, 0,
-                        nullptr, m->d_len, H, s);
-    else
-      launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, B, 0, nullptr,
-                        m->d_len, H, s);
+    gemm_few_f32(m, w.wqkv, h, nq, B, D, EPI_F32, m->qkv, nq, s);
+    launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, B, 0, nullptr,
+                      m->d_len, H, s);
+    launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
+    gemm_few_f32(m, w.wo, m->o, D, B, H * hd, EPI_RESID, m->x, D, s);
+    launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, B, D, eps, nullptr, s);
+    gemm_few_f32(m, w.wgu, h, 2 * I, B, D, EPI_F32, m->gu_f32, 2 * I, s);
+    launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, B, I, s);
+    gemm_few_f32(m, w.wd, m->a, D, B, I, EPI_RESID, m->x, D, s);
+    const bool last = l + 1 == m->cfg.n_layers;
+    const T* gnext = (const T*)(last ? m->gfinal : m->layers[l + 1].gin);
+    launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, gnext, h, B, D, eps, nullptr, s);
+  }
+  float* dst = d_logits ? d_logits : m->logits_int;
+  gemm_few_f32(m, m->lm_head, h, V, B, D, EPI_F32, dst, V, s);
+  launch_argmax(dst, B, V, d_next, m->d_len, s);
+}
+
+// Decode step, bf16: five fused weight-streaming projections per layer.
+//   embed: x = E[tok], sum of squares
+//   per layer: QKV (RMSNorm on load; bias + RoPE + KV write) -> attention ->
+//              O (x += ; sums of squares) -> gate/up (RMSNorm on load; SiLU) ->
+//              down (x += ; sums of squares)
+//   head (RMSNorm on load; logits + argmax partials) -> argmax
+void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
+                         hipStream_t s) {
+  const int D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V(), nq = m->nqkv();
+  const float eps = m->cfg.rms_eps;
+  bf16* xg = (bf16*)m->xg;
+  launch_embed_ss(d_tokens, (const bf16*)m->embed, (const bf16*)m->layers[0].gin, m->x, xg, m->ss, B, D, V, s);
+  int ss_n = 1;
+  auto gemv = [&](GemvArgs& a, int epi) { m->timed(0, a.N, a.M, a.K, s, [&] { launch_gemv_fused(a, epi, s); }); };
+  auto ss_count = [&](int K) {
+    const int rr = gemv_rows(D, K, B, GV_RESID);
+    return (D + rr - 1) / rr;
+  };
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    const LayerW& w = m->layers[l];
+    KVView kv = m->kv(l, m->paged());
+    const bool last = l + 1 == m->cfg.n_layers;
+    GemvArgs qa{};
+    qa.W = (const bf16*)w.wqkv; qa.N = nq; qa.K = D; qa.M = B;
+    qa.X = xg; qa.ss_in = m->ss; qa.ss_n = ss_n; qa.eps = eps;
+    qa.bias = (const bf16*)w.bqkv; qa.cos_t = m->rope_cos; qa.sin_t = m->rope_sin; qa.q_out = (bf16*)m->q;
+    qa.kv = kv; qa.len = m->d_len; qa.H = H;
+    gemv(qa, GV_ROPE);
     int ctx_sum = 0;
     for (int b = 0; b < B; ++b) ctx_sum += m->h_len[b] + 1;
     m->timed(2, H, B, ctx_sum, s, [&] {
-      launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
+      launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
     });
-    np = gemm_few<T>(m, w.wo, m->o, D, B, H * hd, EPI_RESID, m->x, nullptr, D, s, &ps);
-    launch_resid_rmsnorm<T>(m->x, np > 1 ? m->parts : nullptr, np > 1 ? np : 0, ps, (const T*)w.gpost, h, B, D,
-                            eps, nullptr, s);
-    if constexpr (sizeof(T) == 2) {
-      np = gemm_few<T>(m, w.wgu, h, 2 * I, B, D, EPI_SILU, nullptr, m->a, I, s, &ps);
-      if (np > 1) launch_silu_reduce<T>(m->parts, np, ps, (T*)m->a, B, I, s);
-    } else {
-      gemm_few<T>(m, w.wgu, h, 2 * I, B, D, EPI_F32, m->gu_f32, nullptr, 2 * I, s, &ps);
-      launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, B, I, s);
-    }
-    np = gemm_few<T>(m, w.wd, m->a, D, B, I, EPI_RESID, m->x, nullptr, D, s, &ps);
-    const bool last = l + 1 == m->cfg.n_layers;
-    const T* gnext = (const T*)(last ? m->gfinal : m->layers[l + 1].gin);
-    launch_resid_rmsnorm<T>(m->x, np > 1 ? m->parts : nullptr, np > 1 ? np : 0, ps, gnext, h, B, D, eps, nullptr,
-                            s);
+    GemvArgs oa{};
+    oa.W = (const bf16*)w.wo; oa.N = D; oa.K = H * hd; oa.M = B; oa.X = (const bf16*)m->o;
+    oa.out_f32 = m->x; oa.ldo = D; oa.ss_out = m->ss; oa.xg_out = xg; oa.gain_next = (const bf16*)w.gpost;
+    gemv(oa, GV_RESID);
+    ss_n = ss_count(H * hd);
+    GemvArgs ga{};
+    ga.W = (const bf16*)w.wgu; ga.N = 2 * I; ga.K = D; ga.M = B;
+    ga.X = xg; ga.ss_in = m->ss; ga.ss_n = ss_n; ga.eps = eps;
+    ga.out_t = (bf16*)m->a; ga.ldo = I;
+    gemv(ga, GV_SILU);
+    GemvArgs da{};
+    da.W = (const bf16*)w.wd; da.N = D; da.K = I; da.M = B; da.X = (const bf16*)m->a;
+    da.out_f32 = m->x; da.ldo = D; da.ss_out = m->ss; da.xg_out = xg;
+    da.gain_next = (const bf16*)(last ? m->gfinal : m->layers[l + 1].gin);
+    gemv(da, GV_RESID);
+    ss_n = ss_count(I);
   }
-  float* dst = d_logits ? d_logits : m->logits_int;
-  const int np = gemm_few<T>(m, m->lm_head, h, V, B, D, EPI_F32, dst, nullptr, V, s, &ps);
-  if (np > 1) launch_sum_reduce(m->parts, np, ps, dst, B, V, s);
-  launch_argmax(dst, B, V, d_next, m->d_len, s);
+  GemvArgs ha{};
+  ha.W = (const bf16*)m->lm_head; ha.N = V; ha.K = D; ha.M = B;
+  ha.X = xg; ha.ss_in = m->ss; ha.ss_n = ss_n; ha.eps = eps;
+  ha.out_f32 = d_logits; ha.ldo = V; ha.am_val = m->am_val; ha.am_idx = m->am_idx;
+  gemv(ha, GV_HEAD);
+  const int hr = gemv_rows(V, D, B, GV_HEAD);
+  launch_argmax_final(m->am_val, m->am_idx, (V + hr - 1) / hr, B, d_next, m->d_len, s);
+}
+
+void enqueue_decode(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next, hipStream_t s) {
+  if (m->bf) enqueue_decode_bf16(m, B, d_tokens, d_logits, d_next, s);
+  else enqueue_decode_f32(m, B, d_tokens, d_logits, d_next, s);
 }
 
 int check_launch(const char* what) {
@@ -468,14 +509,22 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     TRY(copy_in(&w.gpost, get(p + "post_attention_layernorm.weight")));
     TRY(copy_in(&w.wo, get(p + "self_attn.o_proj.weight")));
     TRY(copy_in(&w.wd, get(p + "mlp.down_proj.weight")));
-    // fused QKV: rows q, then k, then v
+    // fused QKV: heads q, then k, then v; within each head, rows in groups of
+    // 8 = 4 first-half rows i and their rotation partners i + hd/2
     TRY(dev_alloc(m, &w.wqkv, (size_t)nq * D * esz));
     const axon_weight* wq = get(p + "self_attn.q_proj.weight");
     const axon_weight* wk = get(p + "self_attn.k_proj.weight");
     const axon_weight* wv = get(p + "self_attn.v_proj.weight");
-    HTRY(hipMemcpyAsync(w.wqkv, wq->data, H * hd * D * esz, kind(wq), s));
-    HTRY(hipMemcpyAsync((char*)w.wqkv + H * hd * D * esz, wk->data, KV * hd * D * esz, kind(wk), s));
-    HTRY(hipMemcpyAsync((char*)w.wqkv + (H + KV) * hd * D * esz, wv->data, KV * hd * D * esz, kind(wv), s));
+    const size_t row = (size_t)D * esz;
+    for (int64_t hh = 0; hh < H + 2 * KV; ++hh) {
+      const axon_weight* src = hh < H ? wq : (hh < H + KV ? wk : wv);
+      const int64_t hs = hh < H ? hh : (hh < H + KV ? hh - H : hh - H - KV);
+      const char* sbase = (const char*)src->data + hs * hd * row;
+      char* dbase = (char*)w.wqkv + hh * hd * row;
+      HTRY(hipMemcpy2DAsync(dbase, 8 * row, sbase, 4 * row, 4 * row, hd / 8, kind(src), s));
+      HTRY(hipMemcpy2DAsync(dbase + 4 * row, 8 * row, sbase + (hd / 2) * row, 4 * row, 4 * row, hd / 8,
+                            kind(src), s));
+    }
     w.bqkv = nullptr;
     if (c.qkv_bias) {
       TRY(dev_alloc(m, &w.bqkv, (size_t)nq * esz));
@@ -545,17 +594,15 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     TRY(dev_alloc(m, &m->hlast, (int64_t)c.max_batch * D * esz));
     TRY(dev_alloc(m, (void**)&m->logits_int, (int64_t)c.max_batch * V * 4));
     if (!m->bf) TRY(dev_alloc(m, (void**)&m->gu_f32, tmax * 2 * I * 4));
-    int64_t pmax = 1;
-    if (m->bf) {
-      const int64_t shapes[5][2] = {{nq, D}, {D, H * hd}, {2 * I, D}, {D, I}, {V, D}};
-      for (auto& sh : shapes) {
-        const int sp = plan_gemv_splits((int)sh[0], c.max_batch, (int)sh[1]);
-        if (sp > 1) pmax = std::max<int64_t>(pmax, sp * sh[0]);
-      }
-    }
-    TRY(dev_alloc(m, (void**)&m->parts, pmax * c.max_batch * 4));
-    const int64_t nch = plan_decode_chunks(c.max_seq);
-    TRY(dev_alloc(m, (void**)&m->attn_part, (int64_t)c.max_batch * H * nch * (hd + 2) * 4));
+    int64_t bsplits = 1;
+    for (int b = 1; b <= c.max_batch; ++b)
+      bsplits = std::max<int64_t>(bsplits, (int64_t)b * plan_decode_splits(b, c.n_kv_heads, c.max_seq));
+    TRY(dev_alloc(m, (void**)&m->attn_part, bsplits * H * (hd + 2) * 4));
+    TRY(dev_alloc(m, (void**)&m->ss, (int64_t)std::max<int64_t>(D / 8, 1) * c.max_batch * 4));
+    TRY(dev_alloc(m, &m->xg, (int64_t)c.max_batch * D * 2));
+    const int64_t nam = (V + 15) / 16;
+    TRY(dev_alloc(m, (void**)&m->am_val, nam * c.max_batch * 4));
+    TRY(dev_alloc(m, (void**)&m->am_idx, nam * c.max_batch * 4));
     TRY(dev_alloc(m, (void**)&m->d_len, (size_t)c.max_batch * sizeof(int32_t)));
     HTRY(hipMemsetAsync(m->d_len, 0, (size_t)c.max_batch * sizeof(int32_t), s));
   }
@@ -666,8 +713,7 @@ extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_t
     if (it == m->graphs.end()) {
       hipGraph_t g = nullptr;
       HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
-      if (m->bf) enqueue_decode<bf16>(m, batch, d_tokens, d_logits, d_next_tokens, m->cap_stream);
-      else enqueue_decode<float>(m, batch, d_tokens, d_logits, d_next_tokens, m->cap_stream);
+      enqueue_decode(m, batch, d_tokens, d_logits, d_next_tokens, m->cap_stream);
       hipError_t le = hipGetLastError();
       hipError_t ce = hipStreamEndCapture(m->cap_stream, &g);
       if (le != hipSuccess || ce != hipSuccess) {
@@ -683,8 +729,7 @@ extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_t
     }
     HIP_TRY(hipGraphLaunch(it->second, s));
   } else {
-    if (m->bf) enqueue_decode<bf16>(m, batch, d_tokens, d_logits, d_next_tokens, s);
-    else enqueue_decode<float>(m, batch, d_tokens, d_logits, d_next_tokens, s);
+    enqueue_decode(m, batch, d_tokens, d_logits, d_next_tokens, s);
     int rc = check_launch("decode");
     if (rc) return rc;
   }

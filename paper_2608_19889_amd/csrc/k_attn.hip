@@ -10,6 +10,8 @@
 // the probabilities already sit in the lane layout of the B operand of the
 // following O^T = V^T P^T product (the k index of that product is permuted to
 // match, and V^T is read with the same permutation from the transposed V pages).
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -161,29 +163,33 @@ __global__ void __launch_bounds__(256) attn_prefill_bf16_kernel(const bf16* __re
 }
 
 // ============================================================================
-// Decode (bf16): one query per slot.  Workgroup = (key chunk, kv head, slot),
-// four wavefronts; each wavefront takes 32-key steps with the group's query
-// heads as the columns of v_mfma_f32_16x16x32_bf16 (up to 16 heads per group).
-// K and V^T fragments are loaded straight from HBM.  Each workgroup writes an
-// unnormalized partial (o, max, sum) per head; a combine kernel merges chunks.
+// Decode (bf16): one query per slot.  Workgroup = (key split, kv head, slot)
+// with DNW wavefronts; the group's query heads are the columns of
+// v_mfma_f32_16x16x32_bf16 (up to 16 heads per group); each wavefront takes 64
+// keys per iteration and issues the K and V^T loads of both 32-key halves,
+// straight from HBM, before computing either.  The wavefronts' (max, sum, o) are merged in LDS; with one split
+// the normalized output is written directly, otherwise an unnormalized
+// partial per split is merged by the combine kernel.
 // ============================================================================
-constexpr int DCH = 256;  // keys per chunk (4 wavefronts x 2 steps x 32)
-
-template <int HD>
-__global__ void __launch_bounds__(256) attn_decode_bf16_kernel(const bf16* __restrict__ q, KVView kv,
-                                                               float* __restrict__ part, int H,
-                                                               const int32_t* __restrict__ len,
-                                                               int max_chunks) {
-  __shared__ float sm[4][16], sl[4][16];
-  __shared__ float so[4][HD][17];
-  const int chunk = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+template <int HD, int DNW>
+__global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* __restrict__ q, KVView kv,
+                                                                    bf16* __restrict__ o, float* __restrict__ part,
+                                                                    int H, const int32_t* __restrict__ len,
+                                                                    int split_len) {
+  extern __shared__ float dyn[];
+  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int nsplit = gridDim.x;
   const int ctx = len[b] + 1;
-  const int c0 = chunk * DCH;
-  if (c0 >= ctx) return;
+  const int s0 = split * split_len;
+  const int s1 = min(ctx, s0 + split_len);
+  if (s0 >= ctx) return;
   const int group = H / kv.kv_heads;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, gq = lane >> 4;
   const float sc = LOG2E / sqrtf((float)HD);
+  float* sm = dyn;                 // [DNW][16]
+  float* sl = dyn + DNW * 16;      // [DNW][16]
+  float* so = dyn + 2 * DNW * 16;  // [DNW][group][HD]
 
   bf16x8 qf[HD / 32];
   {
@@ -198,23 +204,42 @@ __global__ void __launch_bounds__(256) attn_decode_bf16_kernel(const bf16* __res
   float m_run = -INFINITY, l_run = 0.f;
   const bf16* kb = (const bf16*)kv.k;
   const bf16* vb = (const bf16*)kv.v;
-
-  for (int step = wave; step * 32 < DCH; step += 4) {
-    const int j0 = c0 + step * 32;
-    if (j0 >= ctx) break;
-    f32x4 s[2];
+  const bf16x8 z8 = {};
+  const bf16x4 z4 = {};
+  struct Frag {
+    bf16x8 k[2][HD / 32];
+    bf16x4 vlo[HD / 16], vhi[HD / 16];
+  };
+  // issue the K and V^T loads of the 32 keys starting at j0
+  auto load = [&](Frag& f, int j0) {
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
       const int key = j0 + blk * 16 + col;
-      const bool ok = key < ctx;  // keys past the context may have no page: never dereferenced
+      const bool ok = key < s1;  // keys past the context may have no page: never dereferenced
       const bf16* kp = kb + (ok ? k_off(kv, b, kvh, key) : 0) + gq * 8;
-      bf16x8 kf[HD / 32];
-      const bf16x8 z = {};
 #pragma unroll
-      for (int k = 0; k < HD / 32; ++k) kf[k] = ok ? *(const bf16x8*)(kp + k * 32) : z;
+      for (int k = 0; k < HD / 32; ++k) f.k[blk][k] = ok ? *(const bf16x8*)(kp + k * 32) : z8;
+    }
+    const int ja = j0 + gq * 4, jb = j0 + 16 + gq * 4;
+    const bool oka = ja < s1, okb = jb < s1;
+    const int64_t va = oka ? vt_off(kv, b, kvh, 0, ja) : 0;
+    const int64_t vbo = okb ? vt_off(kv, b, kvh, 0, jb) : 0;
+    const int64_t vrow = kv.ps;  // V^T row stride (positions per page)
+#pragma unroll
+    for (int d = 0; d < HD / 16; ++d) {
+      const int dd = d * 16 + col;
+      f.vlo[d] = oka ? *(const bf16x4*)(vb + va + dd * vrow) : z4;
+      f.vhi[d] = okb ? *(const bf16x4*)(vb + vbo + dd * vrow) : z4;
+    }
+  };
+  // scores, online softmax update and P V for the 32 keys starting at j0
+  auto step = [&](const Frag& f, int j0) {
+    f32x4 s[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
       s[blk] = f32x4{};
 #pragma unroll
-      for (int k = 0; k < HD / 32; ++k) s[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[k], qf[k], s[blk], 0, 0, 0);
+      for (int k = 0; k < HD / 32; ++k) s[blk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[blk][k], qf[k], s[blk], 0, 0, 0);
     }
     // s[blk][i]: key j0 + blk*16 + gq*4 + i, head column ``col``
     float mloc = -INFINITY;
@@ -223,13 +248,13 @@ __global__ void __launch_bounds__(256) attn_decode_bf16_kernel(const bf16* __res
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int key = j0 + blk * 16 + gq * 4 + i;
-        const float v = key < ctx ? s[blk][i] * sc : -INFINITY;
+        const float v = key < s1 ? s[blk][i] * sc : -INFINITY;
         s[blk][i] = v;
         mloc = fmaxf(mloc, v);
       }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_run, mloc);  // finite: key j0 < ctx is in this step
+    const float m_new = fmaxf(m_run, mloc);  // finite: key j0 < s1 is in this step
     const float alpha = exp2f(m_run - m_new);
     m_run = m_new;
     l_run *= alpha;
@@ -244,60 +269,73 @@ __global__ void __launch_bounds__(256) attn_decode_bf16_kernel(const bf16* __res
         l_run += p;
         pb[blk * 4 + i] = (bf16)p;
       }
-    // V^T fragments: row d, keys {j0 + gq*4 + 0..3, j0 + 16 + gq*4 + 0..3}
-    const int ja = j0 + gq * 4, jb = j0 + 16 + gq * 4;
-    const bool oka = ja < ctx, okb = jb < ctx;
+    // O^T += V^T P^T; k index = {gq*4 + 0..3} of block 0, then of block 1
 #pragma unroll
     for (int d = 0; d < HD / 16; ++d) {
-      const int dd = d * 16 + col;
-      const bf16x4 z4 = {};
-      const bf16x4 lo = oka ? *(const bf16x4*)(vb + vt_off(kv, b, kvh, dd, ja)) : z4;
-      const bf16x4 hi = okb ? *(const bf16x4*)(vb + vt_off(kv, b, kvh, dd, jb)) : z4;
-      const bf16x8 va = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-      acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, acc[d], 0, 0, 0);
+      const bf16x8 vv = {f.vlo[d][0], f.vlo[d][1], f.vlo[d][2], f.vlo[d][3],
+                         f.vhi[d][0], f.vhi[d][1], f.vhi[d][2], f.vhi[d][3]};
+      acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vv, pb, acc[d], 0, 0, 0);
     }
+  };
+  // wavefront w takes 64 keys at s0 + w*64, s0 + (w + DNW)*64, ...; both
+  // halves' loads are issued before either is consumed
+  for (int j0 = s0 + wave * 64; j0 < s1; j0 += DNW * 64) {
+    Frag f0, f1;
+    load(f0, j0);
+    const bool two = j0 + 32 < s1;
+    if (two) load(f1, j0 + 32);
+    step(f0, j0);
+    if (two) step(f1, j0 + 32);
   }
   // per-wave statistics: m uniform over the 4 lane groups of a column; l summed
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
   if (gq == 0) {
-    sm[wave][col] = m_run;
-    sl[wave][col] = l_run;
+    sm[wave * 16 + col] = m_run;
+    sl[wave * 16 + col] = l_run;
   }
   // acc[d][i]: head-dim d*16 + gq*4 + i, column ``col``
+  if (col < group) {
 #pragma unroll
-  for (int d = 0; d < HD / 16; ++d)
+    for (int d = 0; d < HD / 16; ++d)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) so[wave][d * 16 + gq * 4 + i][col] = acc[d][i];
+      for (int i = 0; i < 4; ++i) so[(wave * group + col) * HD + d * 16 + gq * 4 + i] = acc[d][i];
+  }
   __syncthreads();
-  // merge the four wavefronts; thread -> (head column, head-dim slice)
-  for (int idx = threadIdx.x; idx < group * HD; idx += 256) {
+  for (int idx = threadIdx.x; idx < group * HD; idx += DNW * 64) {
     const int c = idx / HD, d = idx % HD;
     float M = -INFINITY;
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, sm[w][c]);
+    for (int w = 0; w < DNW; ++w) M = fmaxf(M, sm[w * 16 + c]);
     float L = 0.f, O = 0.f;
-    for (int w = 0; w < 4; ++w) {
-      const float f = sm[w][c] == -INFINITY ? 0.f : exp2f(sm[w][c] - M);
-      L += f * sl[w][c];
-      O += f * so[w][d][c];
+    for (int w = 0; w < DNW; ++w) {
+      const float mw = sm[w * 16 + c];
+      const float f = mw == -INFINITY ? 0.f : exp2f(mw - M);
+      L += f * sl[w * 16 + c];
+      O += f * so[(w * group + c) * HD + d];
     }
-    float* pp = part + (((int64_t)b * H + kvh * group + c) * max_chunks + chunk) * (HD + 2);
-    pp[d] = O;
-    if (d == 0) {
-      pp[HD] = M;
-      pp[HD + 1] = L;
+    const int h = kvh * group + c;
+    if (nsplit == 1) {
+      o[((int64_t)b * H + h) * HD + d] = (bf16)(O / L);
+    } else {
+      float* pp = part + (((int64_t)b * H + h) * nsplit + split) * (HD + 2);
+      pp[d] = O;
+      if (d == 0) {
+        pp[HD] = M;
+        pp[HD + 1] = L;
+      }
     }
   }
 }
 
-// merge chunk partials of one (slot, head): o = sum_c 2^(m_c - M) o_c / sum_c 2^(m_c - M) l_c
+// merge split partials of one (slot, head): o = sum_c 2^(m_c - M) o_c / sum_c 2^(m_c - M) l_c
 template <typename T, int HD>
 __global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restrict__ part, T* __restrict__ o, int H,
-                                                          const int32_t* __restrict__ len, int max_chunks) {
+                                                          const int32_t* __restrict__ len, int nsplit,
+                                                          int split_len) {
   const int b = blockIdx.y, h = blockIdx.x, d = threadIdx.x;
   const int ctx = len[b] + 1;
-  const int nch = (ctx + DCH - 1) / DCH;
-  const float* pp = part + ((int64_t)b * H + h) * max_chunks * (HD + 2);
+  const int nch = min(nsplit, (ctx + split_len - 1) / split_len);
+  const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
   float M = -INFINITY;
   for (int c = 0; c < nch; ++c) M = fmaxf(M, pp[c * (HD + 2) + HD]);
   float L = 0.f, O = 0.f;
@@ -371,7 +409,27 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
   }
 }
 
-int plan_decode_chunks(int max_ctx) { return (max_ctx + DCH - 1) / DCH; }
+// wavefronts per decode workgroup: 16 for head_dim 64 when their partial
+// outputs fit in 64 KB of LDS (head_dim 128 needs > 128 registers per lane)
+static int decode_waves(int group, int hd) { return (hd == 64 && group * hd <= 1024) ? 16 : 8; }
+
+int plan_decode_splits(int B, int kv_heads, int max_ctx) {
+  // one workgroup per (slot, kv head) when that already fills the chip,
+  // otherwise split the keys (each split keeps >= 2 iterations per wavefront)
+  const int pairs = B * kv_heads;
+  const int want = pairs >= 64 ? 1 : (256 + pairs - 1) / pairs;
+  const int cap = (max_ctx + 8 * 128 - 1) / (8 * 128);
+  return std::max(1, std::min(want, cap));
+}
+
+template <int HD, int NW>
+static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int B, int H, const int32_t* len,
+                          int nsplit, int split_len, hipStream_t s) {
+  const int group = H / kv.kv_heads;
+  const size_t lds = (size_t)(2 * NW * 16 + NW * group * HD) * sizeof(float);
+  attn_decode_bf16_kernel<HD, NW><<<dim3(nsplit, kv.kv_heads, B), NW * 64, lds, s>>>(q, kv, o, part, H, len,
+                                                                                      split_len);
+}
 
 template <typename T>
 void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len, int max_ctx,
@@ -382,15 +440,17 @@ void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, 
     if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H);
     else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H);
   } else {
-    const int nch = plan_decode_chunks(max_ctx);
-    dim3 grid(nch, kv.kv_heads, B);
+    const int nsplit = plan_decode_splits(B, kv.kv_heads, max_ctx);
+    const int split_len = ((max_ctx + nsplit - 1) / nsplit + 31) / 32 * 32;
+    const int nw = decode_waves(H / kv.kv_heads, kv.hd);
     dim3 cgrid(H, B);
     if (kv.hd == 64) {
-      attn_decode_bf16_kernel<64><<<grid, 256, 0, s>>>(q, kv, part, H, len, nch);
-      attn_combine_kernel<T, 64><<<cgrid, 64, 0, s>>>(part, o, H, len, nch);
+      if (nw == 16) decode_launch<64, 16>(q, kv, o, part, B, H, len, nsplit, split_len, s);
+      else decode_launch<64, 8>(q, kv, o, part, B, H, len, nsplit, split_len, s);
+      if (nsplit > 1) attn_combine_kernel<T, 64><<<cgrid, 64, 0, s>>>(part, o, H, len, nsplit, split_len);
     } else {
-      attn_decode_bf16_kernel<128><<<grid, 256, 0, s>>>(q, kv, part, H, len, nch);
-      attn_combine_kernel<T, 128><<<cgrid, 128, 0, s>>>(part, o, H, len, nch);
+      decode_launch<128, 8>(q, kv, o, part, B, H, len, nsplit, split_len, s);
+      if (nsplit > 1) attn_combine_kernel<T, 128><<<cgrid, 128, 0, s>>>(part, o, H, len, nsplit, split_len);
     }
   }
 }

@@ -147,146 +147,6 @@ void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi
 }
 
 // ============================================================================
-// Decode GEMM (M = batch <= 64 tokens): HBM-bound on the weight stream.
-// Each wavefront owns 32 W rows (two 16-row blocks of
-// v_mfma_f32_16x16x32_bf16) and up to 64 token columns (NB blocks of 16); a
-// workgroup of 4 wavefronts covers 128 rows; the K range is split across
-// gridDim.y workgroups when there are too few row blocks to fill the chip.
-// W fragments are loaded straight from HBM (16 bytes per lane), four k-steps
-// in flight per wavefront.
-// ============================================================================
-template <int EPI, int NB>
-__global__ void __launch_bounds__(256) gemv_bf16_kernel(const bf16* __restrict__ W, const bf16* __restrict__ X,
-                                                        int N, int M, int K, int kchunk, EpiArgs ep) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nb = blockIdx.x * 128 + wave * 32;  // first of this wave's 32 rows
-  const int k_begin = blockIdx.y * kchunk;
-  const int k_end = min(K, k_begin + kchunk);
-  const int r16 = lane & 15, kq = (lane >> 4) * 8;
-  const bf16x8 zero8 = {};
-
-  const bf16* wrow[2];
-  bool wok[2];
-#pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int n = nb + r * 16 + r16;
-    wok[r] = n < N;
-    wrow[r] = W + (int64_t)(wok[r] ? n : 0) * K + kq;
-  }
-  const bf16* xrow[NB];
-  bool xok[NB];
-#pragma unroll
-  for (int c = 0; c < NB; ++c) {
-    const int t = c * 16 + r16;
-    xok[c] = t < M;
-    xrow[c] = X + (int64_t)(xok[c] ? t : 0) * K + kq;
-  }
-
-  f32x4 acc[2][NB];
-#pragma unroll
-  for (int r = 0; r < 2; ++r)
-#pragma unroll
-    for (int c = 0; c < NB; ++c) acc[r][c] = f32x4{};
-
-  constexpr int U = 4;
-  int k = k_begin;
-  for (; k + 32 * U <= k_end; k += 32 * U) {
-    bf16x8 a[U][2], b[U][NB];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-#pragma unroll
-      for (int r = 0; r < 2; ++r) a[u][r] = wok[r] ? *(const bf16x8*)(wrow[r] + k + u * 32) : zero8;
-#pragma unroll
-      for (int c = 0; c < NB; ++c) b[u][c] = xok[c] ? *(const bf16x8*)(xrow[c] + k + u * 32) : zero8;
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int r = 0; r < 2; ++r)
-#pragma unroll
-        for (int c = 0; c < NB; ++c)
-          acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][r], b[u][c], acc[r][c], 0, 0, 0);
-  }
-  for (; k < k_end; k += 32) {
-    bf16x8 a[2], b[NB];
-#pragma unroll
-    for (int r = 0; r < 2; ++r) a[r] = wok[r] ? *(const bf16x8*)(wrow[r] + k) : zero8;
-#pragma unroll
-    for (int c = 0; c < NB; ++c) b[c] = xok[c] ? *(const bf16x8*)(xrow[c] + k) : zero8;
-#pragma unroll
-    for (int r = 0; r < 2; ++r)
-#pragma unroll
-      for (int c = 0; c < NB; ++c)
-        acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[r], b[c], acc[r][c], 0, 0, 0);
-  }
-
-  // acc[r][c][i] = C[n][t], n = nb + r*16 + (lane/16)*4 + i, t = c*16 + lane%16
-#pragma unroll
-  for (int c = 0; c < NB; ++c) {
-    const int t = c * 16 + r16;
-    if (t >= M) continue;
-    if constexpr (EPI == EPI_SILU) {
-      if (nb >= N) continue;
-      bf16* out = (bf16*)ep.out_t + (int64_t)t * ep.ldo + (nb / 32) * 16 + (lane >> 4) * 4;
-      bf16x4 v;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) v[j] = (bf16)(silu_f(acc[0][c][j]) * acc[1][c][j]);
-      *(bf16x4*)out = v;
-    } else {
-#pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        const int n = nb + r * 16 + (lane >> 4) * 4;
-        if (n >= N) continue;
-        float* p;
-        if constexpr (EPI == EPI_PART)
-          p = ep.out_f32 + blockIdx.y * ep.part_stride + (int64_t)t * ep.ldo + n;
-        else
-          p = ep.out_f32 + (int64_t)t * ep.ldo + n;
-        store_cols<EPI == EPI_RESID>(p, acc[r][c], N - n);
-      }
-    }
-  }
-}
-
-int plan_gemv_splits(int N, int M, int K) {
-  (void)M;
-  const int row_blocks = (N + 127) / 128;
-  const int kblocks = K / 128;  // at least 128 k per split
-  int s = 1;
-  while (row_blocks * s < 1024 && s * 2 <= kblocks && s < 16) s *= 2;
-  return s;
-}
-
-template <int EPI>
-static void gemv_dispatch(const bf16* W, const bf16* X, int N, int M, int K, int splits, const EpiArgs& ep,
-                          hipStream_t s) {
-  const int kchunk = ((K / splits) + 31) / 32 * 32;
-  dim3 grid((N + 127) / 128, splits);
-  const int nb = (M + 15) / 16;
-  switch (nb) {
-    case 1: gemv_bf16_kernel<EPI, 1><<<grid, 256, 0, s>>>(W, X, N, M, K, kchunk, ep); break;
-    case 2: gemv_bf16_kernel<EPI, 2><<<grid, 256, 0, s>>>(W, X, N, M, K, kchunk, ep); break;
-    case 3: gemv_bf16_kernel<EPI, 3><<<grid, 256, 0, s>>>(W, X, N, M, K, kchunk, ep); break;
-    default: gemv_bf16_kernel<EPI, 4><<<grid, 256, 0, s>>>(W, X, N, M, K, kchunk, ep); break;
-  }
-}
-
-void launch_gemv_bf16(const bf16* W, const bf16* X, int N, int M, int K, int splits, int epi,
-                      const EpiArgs& ep, hipStream_t s) {
-  if (M <= 0) return;
-  if (splits > 1) {
-    gemv_dispatch<EPI_PART>(W, X, N, M, K, splits, ep, s);
-    return;
-  }
-  switch (epi) {
-    case EPI_F32: gemv_dispatch<EPI_F32>(W, X, N, M, K, 1, ep, s); break;
-    case EPI_RESID: gemv_dispatch<EPI_RESID>(W, X, N, M, K, 1, ep, s); break;
-    case EPI_SILU: gemv_dispatch<EPI_SILU>(W, X, N, M, K, 1, ep, s); break;
-    default: gemv_dispatch<EPI_PART>(W, X, N, M, K, 1, ep, s); break;
-  }
-}
-
-// ============================================================================
 // float32 check-mode GEMM: 64 x 64 tiles, k-step 16, 256 threads with a 4 x 4
 // register block each, operands staged k-major in LDS.
 // ============================================================================
@@ -369,21 +229,5 @@ void launch_silu_reduce(const float* parts, int nparts, int64_t part_stride, T* 
 }
 template void launch_silu_reduce<float>(const float*, int, int64_t, float*, int, int, hipStream_t);
 template void launch_silu_reduce<bf16>(const float*, int, int64_t, bf16*, int, int, hipStream_t);
-
-__global__ void sum_reduce_kernel(const float* __restrict__ parts, int nparts, int64_t part_stride,
-                                  float* __restrict__ out, int64_t n) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= n) return;
-  float v = 0.f;
-  for (int s = 0; s < nparts; ++s) v += parts[s * part_stride + idx];
-  out[idx] = v;
-}
-
-void launch_sum_reduce(const float* parts, int nparts, int64_t part_stride, float* out, int M, int N,
-                       hipStream_t s) {
-  const int64_t n = (int64_t)M * N;
-  if (n <= 0) return;
-  sum_reduce_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(parts, nparts, part_stride, out, n);
-}
 
 }  // namespace axon

@@ -1,0 +1,386 @@
+// Few-token projections for the decode step (M <= 64 tokens), fused with
+// their neighbours.  HBM-bound on the weight stream.
+//
+// A workgroup owns 16*RB output features of W [N][K] and the whole K range;
+// its KS wavefronts split K into contiguous chunks, run
+// v_mfma_f32_16x16x32_bf16 with W as the A operand (16 rows per block) and the
+// tokens as the B operand (16 columns per block, NB blocks), and reduce their
+// partial tiles through LDS in a fixed order (deterministic, no split-K
+// partials in HBM).
+//
+// Normalized operand (NORM): RMSNorm(x) g enters as bf16(x[t][k] * g[k]),
+// written by the producer of x together with per-workgroup partial sums of
+// squares of x; the accumulator is scaled by inv[t] = rsqrt(sum of squares /
+// K + eps) in the epilogue.  This replaces a separate normalization kernel.
+//
+// Epilogues:
+//   GV_HEAD  logits (optional) + per-workgroup (max, first index) per token
+//   GV_RESID x[t][n] += acc; writes bf16(x * g_next) for the next normalized
+//            projection and per-workgroup sums of squares of the new x
+//   GV_SILU  rows come in blocks of 16 gate rows + the 16 matching up rows:
+//            a[t][f] = bf16(silu(gate) * up)
+//   GV_ROPE  rows of the fused QKV projection are permuted so that an 8-row
+//            group holds 4 rotation-pair first halves and their partners:
+//            bias + rotary embedding at position len[t], then q -> q_out,
+//            k -> K pages, v -> transposed V pages.
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace axon {
+
+AXON_DEV float silu_g(float z) { return z / (1.f + __expf(-z)); }
+
+constexpr int GV_U = 4;  // k-steps of 32 per pipeline stage
+
+template <int ROWS, int KS, int NB, bool NORM, int EPI>
+__global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
+  constexpr int RB = ROWS < 16 ? 1 : ROWS / 16;  // 16-row MFMA blocks (an 8-row tile leaves 8 rows idle)
+  constexpr int COLS = NB * 16;
+  constexpr int NT = KS * 64;
+  constexpr int U = GV_U;
+  __shared__ float red[KS][RB * 16][COLS + 1];
+  __shared__ float s_ss[NT];
+  __shared__ float s_inv[64];
+  __shared__ float s_aux[RB * 16][COLS + 1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n0 = blockIdx.x * ROWS;
+  const int K = a.K, M = a.M;
+  const int kc = ((K + KS - 1) / KS + 32 * U - 1) / (32 * U) * (32 * U);
+  const int k0 = min(K, wave * kc), k1 = min(K, k0 + kc);
+  const int r16 = lane & 15, kq = (lane >> 4) * 8;
+  const bf16x8 z8 = {};
+
+  const bf16* wrow[RB];
+  bool wok[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    const int n = n0 + r * 16 + r16;
+    wok[r] = n < a.N && (ROWS >= 16 || r16 < ROWS);
+    wrow[r] = a.W + (int64_t)(wok[r] ? n : 0) * K + kq;
+  }
+  const bf16* xrow[NB];
+  bool tok[NB];
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    const int t = c * 16 + r16;
+    tok[c] = t < M;
+    xrow[c] = a.X + (int64_t)(tok[c] ? t : 0) * K + kq;
+  }
+
+  // sums of squares of the normalized rows: the first SSR partials of this
+  // thread are loaded into registers now and consumed after the stream
+  constexpr int SSR = 8;
+  float ss_reg[SSR];
+  const int ss_slices = NT / M, ss_t = tid % M, ss_sl = tid / M;
+  if constexpr (NORM) {
+#pragma unroll
+    for (int i = 0; i < SSR; ++i) {
+      const int j = ss_sl + i * ss_slices;
+      ss_reg[i] = (ss_sl < ss_slices && j < a.ss_n) ? a.ss_in[(int64_t)j * M + ss_t] : 0.f;
+    }
+  }
+
+  // B operand: token rows of X (for a normalized operand X = bf16(x * g) was
+  // written by the producer of x; 1/rms is applied to the accumulator)
+  auto load_b = [&](int c, int k) -> bf16x8 { return tok[c] ? *(const bf16x8*)(xrow[c] + k) : z8; };
+
+  f32x4 acc[RB][NB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int c = 0; c < NB; ++c) acc[r][c] = f32x4{};
+
+  // software-pipelined stream over [k0, k1): stage s+1 is loaded while stage s
+  // feeds the MFMAs; k1 - k0 is a multiple of 32 (K % 64 == 0)
+  bf16x8 wa[U][RB], xb[U][NB];
+  auto load_stage = [&](int k) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool in = k + u * 32 < k1;
+#pragma unroll
+      for (int r = 0; r < RB; ++r) wa[u][r] = (in && wok[r]) ? *(const bf16x8*)(wrow[r] + k + u * 32) : z8;
+#pragma unroll
+      for (int c = 0; c < NB; ++c) xb[u][c] = in ? load_b(c, k + u * 32) : z8;
+    }
+  };
+  if (k0 < k1) load_stage(k0);
+  for (int k = k0; k < k1; k += 32 * U) {
+    bf16x8 ca[U][RB], cb[U][NB];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int r = 0; r < RB; ++r) ca[u][r] = wa[u][r];
+#pragma unroll
+      for (int c = 0; c < NB; ++c) cb[u][c] = xb[u][c];
+    }
+    if (k + 32 * U < k1) load_stage(k + 32 * U);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int r = 0; r < RB; ++r)
+#pragma unroll
+        for (int c = 0; c < NB; ++c)
+          acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ca[u][r], cb[u][c], acc[r][c], 0, 0, 0);
+  }
+
+  // ---- cross-wavefront reduction: acc[r][c][i] = C[n0 + r*16 + (lane/16)*4 + i][c*16 + lane%16]
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[wave][r * 16 + (lane >> 4) * 4 + i][c * 16 + r16] = acc[r][c][i];
+  if constexpr (NORM) {
+    float ss_part = 0.f;
+#pragma unroll
+    for (int i = 0; i < SSR; ++i) ss_part += ss_reg[i];
+    if (ss_sl < ss_slices)
+      for (int j = ss_sl + SSR * ss_slices; j < a.ss_n; j += ss_slices) ss_part += a.ss_in[(int64_t)j * M + ss_t];
+    s_ss[tid] = ss_part;
+  }
+  __syncthreads();
+  if constexpr (NORM) {
+    if (tid < M) {
+      float tot = 0.f;
+      for (int sl = 0; sl < ss_slices; ++sl) tot += s_ss[sl * M + tid];
+      s_inv[tid] = rsqrtf(tot / (float)K + a.eps);
+    }
+    __syncthreads();
+  }
+  auto total = [&](int row, int col) {
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < KS; ++w) s += red[w][row][col];
+    if constexpr (NORM) s *= s_inv[col];
+    return s;
+  };
+
+  if constexpr (EPI == GV_RESID) {
+    for (int it = tid; it < ROWS * COLS; it += NT) {
+      const int row = it / COLS, col = it % COLS, n = n0 + row;
+      float sq = 0.f;
+      if (col < M && n < a.N) {
+        float* p = a.out_f32 + (int64_t)col * a.ldo + n;
+        const float v = *p + total(row, col);
+        *p = v;
+        sq = v * v;
+        a.xg_out[(int64_t)col * a.ldo + n] = (bf16)(v * (float)a.gain_next[n]);
+      }
+      s_aux[row][col] = sq;
+    }
+    __syncthreads();
+    if (tid < M) {
+      float s = 0.f;
+      for (int row = 0; row < ROWS; ++row) s += s_aux[row][tid];
+      a.ss_out[(int64_t)blockIdx.x * M + tid] = s;
+    }
+  } else if constexpr (EPI == GV_SILU) {
+    // rows 0..15 gate, 16..31 the matching up rows (RB == 2)
+    for (int it = tid; it < 16 * COLS; it += NT) {
+      const int f = it / COLS, col = it % COLS;
+      if (col >= M) continue;
+      const float g = total(f, col), u = total(16 + f, col);
+      a.out_t[(int64_t)col * a.ldo + n0 / 2 + f] = (bf16)(silu_g(g) * u);
+    }
+  } else if constexpr (EPI == GV_ROPE) {
+    // an 8-row group of a head = first halves i = 4g..4g+3 and their partners
+    const int hd = a.kv.hd, half = hd / 2;
+    const int head = n0 / hd, g0 = (n0 % hd) / 8;
+    const int KVh = a.kv.kv_heads;
+    for (int it = tid; it < (ROWS / 2) * COLS; it += NT) {
+      const int pr = it / COLS, t = it % COLS;
+      if (t >= M) continue;
+      const int gl = pr / 4, i4 = pr % 4;
+      const int i = (g0 + gl) * 4 + i4;  // rotation pair (i, i + hd/2) of this head
+      float x1 = total(gl * 8 + i4, t), x2 = total(gl * 8 + 4 + i4, t);
+      if (a.bias) {
+        x1 += (float)a.bias[head * hd + i];
+        x2 += (float)a.bias[head * hd + half + i];
+      }
+      const int pos = a.len[t];
+      if (head < a.H + KVh) {
+        const float cs = a.cos_t[(int64_t)pos * half + i], sn = a.sin_t[(int64_t)pos * half + i];
+        const float y1 = x1 * cs - x2 * sn, y2 = x2 * cs + x1 * sn;
+        bf16* dst = head < a.H ? a.q_out + ((int64_t)t * a.H + head) * hd
+                               : (bf16*)a.kv.k + k_off(a.kv, t, head - a.H, pos);
+        dst[i] = (bf16)y1;
+        dst[i + half] = (bf16)y2;
+      } else {
+        const int kvh = head - a.H - KVh;
+        bf16* vt = (bf16*)a.kv.v;
+        vt[vt_off(a.kv, t, kvh, i, pos)] = (bf16)x1;
+        vt[vt_off(a.kv, t, kvh, i + half, pos)] = (bf16)x2;
+      }
+    }
+  } else {  // GV_HEAD
+    for (int it = tid; it < ROWS * COLS; it += NT) {
+      const int row = it / COLS, col = it % COLS, n = n0 + row;
+      float v = -INFINITY;
+      if (col < M && n < a.N) {
+        v = total(row, col);
+        if (a.out_f32) a.out_f32[(int64_t)col * a.ldo + n] = v;
+      }
+      s_aux[row][col] = v;
+    }
+    __syncthreads();
+    if (tid < M) {
+      float best = -INFINITY;
+      int bi = 0x7fffffff;
+      for (int row = 0; row < ROWS; ++row) {
+        const float v = s_aux[row][tid];
+        if (v > best) { best = v; bi = n0 + row; }
+      }
+      a.am_val[(int64_t)tid * gridDim.x + blockIdx.x] = best;
+      a.am_idx[(int64_t)tid * gridDim.x + blockIdx.x] = bi;
+    }
+  }
+}
+
+// next[t] = index of the largest partial maximum (lowest index on ties);
+// len[t] += 1 when ``len`` is set.
+__global__ void __launch_bounds__(256) argmax_final_kernel(const float* __restrict__ val,
+                                                           const int32_t* __restrict__ idx, int nparts,
+                                                           int32_t* __restrict__ next, int32_t* __restrict__ len) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int t = blockIdx.x;
+  float best = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int j = threadIdx.x; j < nparts; j += blockDim.x) {
+    const float v = val[(int64_t)t * nparts + j];
+    const int i = idx[(int64_t)t * nparts + j];
+    if (v > best || (v == best && i < bi)) { best = v; bi = i; }
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float ov = __shfl_xor(best, m, 64);
+    const int oi = __shfl_xor(bi, m, 64);
+    if (ov > best || (ov == best && oi < bi)) { best = ov; bi = oi; }
+  }
+  if ((threadIdx.x & 63) == 0) { sv[threadIdx.x >> 6] = best; si[threadIdx.x >> 6] = bi; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w)
+      if (sv[w] > best || (sv[w] == best && si[w] < bi)) { best = sv[w]; bi = si[w]; }
+    next[t] = bi == 0x7fffffff ? 0 : bi;
+    if (len) len[t] += 1;
+  }
+}
+
+// x[t] = E[tok[t]] as float, xg[t] = bf16(x[t] * g), ss_out[t] = sum of
+// squares of the row (a single partial for the first projection's normalization)
+__global__ void __launch_bounds__(256) embed_ss_kernel(const int32_t* __restrict__ tok, const bf16* __restrict__ emb,
+                                                       const bf16* __restrict__ g, float* __restrict__ x,
+                                                       bf16* __restrict__ xg, float* __restrict__ ss_out, int D,
+                                                       int V) {
+  __shared__ float red[16];
+  const int t = blockIdx.x;
+  const int id = min(max(tok[t], 0), V - 1);
+  const bf16* e = emb + (int64_t)id * D;
+  float* xr = x + (int64_t)t * D;
+  float ss = 0.f;
+  for (int i = threadIdx.x * 8; i < D; i += blockDim.x * 8) {
+    const bf16x8 v = *(const bf16x8*)(e + i);
+    f32x4 lo, hi;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      lo[j] = (float)v[j];
+      hi[j] = (float)v[j + 4];
+      ss += lo[j] * lo[j] + hi[j] * hi[j];
+    }
+    *(f32x4*)(xr + i) = lo;
+    *(f32x4*)(xr + i + 4) = hi;
+    const bf16x8 gv = *(const bf16x8*)(g + i);
+    bf16x8 o;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = (bf16)((float)v[j] * (float)gv[j]);
+    *(bf16x8*)(xg + (int64_t)t * D + i) = o;
+  }
+  ss = block_sum(ss, red);
+  if (threadIdx.x == 0) ss_out[t] = ss;
+}
+
+// ---------------------------------------------------------------- launchers
+
+// more token columns -> fewer wavefronts (registers and LDS of the reduction)
+constexpr int ks_for(int ks, int nb) { return nb == 1 ? ks : (nb == 2 ? (ks < 8 ? ks : 8) : 4); }
+
+// Workgroup shape per epilogue and token count: ROWS output features, KS
+// wavefronts splitting K.  Wide projections take 32..64 rows with 4
+// wavefronts; narrow ones 8 or 16 rows with up to 16 wavefronts, so that the
+// grid still spreads over all CUs (one CU streams only ~25 GB/s).
+struct GvShape {
+  int rows, ks;
+};
+
+GvShape gemv_shape(int N, int K, int M, int epi) {
+  const int nb = (M + 15) / 16;
+  if (epi == GV_SILU) return {32, 4};
+  if (epi == GV_HEAD) return {nb <= 2 ? 64 : 32, 4};
+  const int rows = N / 16 >= 512 ? 16 : 8;
+  int ks = 16;
+  while (ks > 4 && K / ks < 256) ks /= 2;
+  return {rows, ks_for(ks, nb)};
+}
+
+int gemv_rows(int N, int K, int M, int epi) { return gemv_shape(N, K, M, epi).rows; }
+
+template <int ROWS, int KS, bool NORM, int EPI>
+static void gv_nb(const GemvArgs& a, hipStream_t s) {
+  const dim3 grid((a.N + ROWS - 1) / ROWS);
+  switch ((a.M + 15) / 16) {
+    case 1: gemv_fused_kernel<ROWS, ks_for(KS, 1), 1, NORM, EPI><<<grid, ks_for(KS, 1) * 64, 0, s>>>(a); break;
+    case 2: gemv_fused_kernel<ROWS, ks_for(KS, 2), 2, NORM, EPI><<<grid, ks_for(KS, 2) * 64, 0, s>>>(a); break;
+    case 3: gemv_fused_kernel<ROWS, ks_for(KS, 3), 3, NORM, EPI><<<grid, ks_for(KS, 3) * 64, 0, s>>>(a); break;
+    default: gemv_fused_kernel<ROWS, ks_for(KS, 4), 4, NORM, EPI><<<grid, ks_for(KS, 4) * 64, 0, s>>>(a); break;
+  }
+}
+
+template <int ROWS, bool NORM, int EPI>
+static void gv_narrow(const GemvArgs& a, int ks, hipStream_t s) {
+  if (ks >= 16) gv_nb<ROWS, 16, NORM, EPI>(a, s);
+  else if (ks >= 8) gv_nb<ROWS, 8, NORM, EPI>(a, s);
+  else gv_nb<ROWS, 4, NORM, EPI>(a, s);
+}
+
+void launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return;
+  const GvShape sh = gemv_shape(a.N, a.K, a.M, epi);
+  const bool norm = a.ss_in != nullptr;
+  switch (epi) {
+    case GV_RESID:
+      if (sh.rows == 8) gv_narrow<8, false, GV_RESID>(a, sh.ks, s);
+      else gv_narrow<16, false, GV_RESID>(a, sh.ks, s);
+      break;
+    case GV_ROPE:
+      if (sh.rows == 8) gv_narrow<8, true, GV_ROPE>(a, sh.ks, s);
+      else gv_narrow<16, true, GV_ROPE>(a, sh.ks, s);
+      break;
+    case GV_SILU: gv_nb<32, 4, true, GV_SILU>(a, s); break;
+    default:
+      if (sh.rows == 64) {
+        if (norm) gv_nb<64, 4, true, GV_HEAD>(a, s);
+        else gv_nb<64, 4, false, GV_HEAD>(a, s);
+      } else {
+        if (norm) gv_nb<32, 4, true, GV_HEAD>(a, s);
+        else gv_nb<32, 4, false, GV_HEAD>(a, s);
+      }
+      break;
+  }
+}
+
+void launch_argmax_final(const float* val, const int32_t* idx, int nparts, int M, int32_t* next, int32_t* len,
+                         hipStream_t s) {
+  if (M <= 0) return;
+  argmax_final_kernel<<<M, 256, 0, s>>>(val, idx, nparts, next, len);
+}
+
+void launch_embed_ss(const int32_t* tok, const bf16* emb, const bf16* g, float* x, bf16* xg, float* ss_out, int M,
+                     int D, int V, hipStream_t s) {
+  if (M <= 0) return;
+  embed_ss_kernel<<<M, 256, 0, s>>>(tok, emb, g, x, xg, ss_out, D, V);
+}
+
+}  // namespace axon

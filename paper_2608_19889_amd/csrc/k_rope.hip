@@ -1,7 +1,9 @@
 // Bias + rotary position embedding + KV-cache write.
 //
 // The projection output row of a token holds H query heads, then KV key
-// heads, then KV value heads (head_dim each).  Queries and keys are rotated by
+// heads, then KV value heads (head_dim each); within a head the columns come
+// in groups of 8 = 4 first-half elements i and their rotation partners
+// i + hd/2 (qkv_col below), the row order the fused decode projection needs.  Queries and keys are rotated by
 // their absolute position with rotate-half pairing (element i with i + hd/2,
 // angle pos * theta^(-2i/hd), cos/sin read from a float table built in double
 // precision on the host); queries go to q_out [T][H][hd], keys to the K pages,
@@ -24,6 +26,14 @@ AXON_DEV void token_slot_pos(int t, int nseq, const int32_t* __restrict__ cu, co
   }
 }
 
+// column of element j of head h in the permuted projection output
+template <int HD>
+AXON_DEV int qkv_col(int h, int j) {
+  constexpr int HALF = HD / 2;
+  const int jj = j < HALF ? j : j - HALF;
+  return h * HD + (jj / 4) * 8 + (j < HALF ? 0 : 4) + jj % 4;
+}
+
 template <typename T, int HD>
 __global__ void __launch_bounds__(256) rope_kv_kernel(const float* __restrict__ parts, int nparts, int64_t pstride,
                                                       const T* __restrict__ bias, const float* __restrict__ cos_t,
@@ -37,11 +47,12 @@ __global__ void __launch_bounds__(256) rope_kv_kernel(const float* __restrict__ 
   const int t0 = blockIdx.x * ROPE_TT;
   const int head = blockIdx.y;
   const int off = head * HD;
-  auto val = [&](int t, int c) {
-    const float* p = parts + (int64_t)t * nqkv + c;
+  // element j of this head for token t (bias indexed in the original order)
+  auto val = [&](int t, int j) {
+    const float* p = parts + (int64_t)t * nqkv + qkv_col<HD>(head, j);
     float v = 0.f;
     for (int s = 0; s < nparts; ++s) v += p[s * pstride];
-    if (bias) v += to_f32(bias[c]);
+    if (bias) v += to_f32(bias[off + j]);
     return v;
   };
   if (head < H + KVh) {
@@ -51,7 +62,7 @@ __global__ void __launch_bounds__(256) rope_kv_kernel(const float* __restrict__ 
       if (t >= T_tokens) continue;
       int slot, pos;
       token_slot_pos(t, nseq, cu, len, slot, pos);
-      const float x1 = val(t, off + i), x2 = val(t, off + i + HALF);
+      const float x1 = val(t, i), x2 = val(t, i + HALF);
       const float c = cos_t[(int64_t)pos * HALF + i], s = sin_t[(int64_t)pos * HALF + i];
       const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
       T* dst;
@@ -66,7 +77,7 @@ __global__ void __launch_bounds__(256) rope_kv_kernel(const float* __restrict__ 
     const int kvh = head - H - KVh;
     for (int idx = threadIdx.x; idx < ROPE_TT * HD; idx += blockDim.x) {
       const int tt = idx / HD, d = idx % HD;
-      if (t0 + tt < T_tokens) vt[tt][d] = val(t0 + tt, off + d);
+      if (t0 + tt < T_tokens) vt[tt][d] = val(t0 + tt, d);
     }
     __syncthreads();
     for (int idx = threadIdx.x; idx < ROPE_TT * HD; idx += blockDim.x) {

@@ -14,7 +14,7 @@ enum Epi : int {
   EPI_RESID = 1,  // out_f32[t * ldo + n] += acc   (residual stream, float)
   EPI_SILU = 2,   // W rows interleaved in blocks of 16 gate rows then 16 up rows;
                   // out_t[t * ldo + f] = silu(gate_f) * up_f
-  EPI_PART = 3    // out_f32[split * part_stride + t * ldo + n] = acc (split-K partial)
+  EPI_PART = 3    // (reserved)
 };
 
 struct EpiArgs {
@@ -40,12 +40,6 @@ void launch_set_lengths(const int32_t* cu, int32_t* len, int n, hipStream_t s);
 // Many-token GEMM (prefill): bf16 MFMA tiles.  Requires K % 64 == 0, N % 32 == 0.
 void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi, const EpiArgs& ep,
                       hipStream_t s);
-// Few-token GEMM (decode, M <= 64): streams W once.  Returns the number of
-// K splits used (> 1 means EPI_PART partials were written to ep.out_f32 with
-// stride ep.part_stride, and the caller's reduction applies the epilogue).
-int plan_gemv_splits(int N, int M, int K);
-void launch_gemv_bf16(const bf16* W, const bf16* X, int N, int M, int K, int splits, int epi,
-                      const EpiArgs& ep, hipStream_t s);
 // float32 check-mode GEMM (any M): EPI_F32 / EPI_RESID / EPI_PART(split 0 only).
 void launch_gemm_f32(const float* W, const float* X, int N, int M, int K, int epi, const EpiArgs& ep,
                      hipStream_t s);
@@ -54,9 +48,42 @@ void launch_gemm_f32(const float* W, const float* X, int N, int M, int K, int ep
 template <typename T>
 void launch_silu_reduce(const float* parts, int nparts, int64_t part_stride, T* a, int M, int I,
                         hipStream_t s);
-// out[t][n] = sum_s parts[s][t][n]
-void launch_sum_reduce(const float* parts, int nparts, int64_t part_stride, float* out, int M, int N,
-                       hipStream_t s);
+// ---- fused decode projections (k_gemv.hip)
+enum GvEpi : int { GV_HEAD = 0, GV_RESID = 1, GV_SILU = 2, GV_ROPE = 3 };
+
+struct GemvArgs {
+  const bf16* W;  // [N][K]
+  int N, K, M;
+  // B operand X [M][K] bf16.  Normalized operand (ss_in != nullptr): X holds
+  // bf16(x * g) and the result is scaled by rsqrt(sum of squares / K + eps)
+  const bf16* X;
+  const float* ss_in;  // [ss_n][M] partial sums of squares of the rows of x
+  int ss_n;
+  float eps;
+  // epilogue outputs
+  float* out_f32;  // GV_HEAD logits [M][ldo] (may be null) / GV_RESID x [M][ldo]
+  int ldo;
+  bf16* out_t;     // GV_SILU a [M][ldo]
+  float* ss_out;   // GV_RESID: [N / gemv_rows][M]
+  bf16* xg_out;    // GV_RESID: bf16(x * gain_next) [M][ldo]
+  const bf16* gain_next;
+  float* am_val;   // GV_HEAD: [M][N / gemv_rows] partial maxima
+  int32_t* am_idx;
+  // GV_ROPE
+  const bf16* bias;  // [(H+2KV)hd] in the original (unpermuted) order, or null
+  const float* cos_t;
+  const float* sin_t;
+  bf16* q_out;  // [M][H][hd]
+  KVView kv;
+  const int32_t* len;
+  int H;
+};
+int gemv_rows(int N, int K, int M, int epi);  // output rows per workgroup (ss partial count = N / rows)
+void launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s);
+void launch_argmax_final(const float* val, const int32_t* idx, int nparts, int M, int32_t* next, int32_t* len,
+                         hipStream_t s);
+void launch_embed_ss(const int32_t* tok, const bf16* emb, const bf16* g, float* x, bf16* xg, float* ss_out, int M,
+                     int D, int V, hipStream_t s);
 
 // ---- bias + rotary + KV-cache write (k_rope.hip)
 // qkv rows are sum_s parts[s][t][:] (+ bias): q heads, then k heads, then v heads.
@@ -74,8 +101,10 @@ template <typename T>
 void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, const int32_t* cu,
                          const int32_t* h_cu, int H, hipStream_t s);
 // Decode attention: one query per slot at position len[b] (after the step's
-// key/value were written), context len[b] + 1; split over key chunks.
-int plan_decode_chunks(int max_ctx);
+// key/value were written), context len[b] + 1; keys split over
+// plan_decode_splits() workgroups per (slot, kv head).  ``part`` holds
+// B * H * splits * (hd + 2) floats.
+int plan_decode_splits(int B, int kv_heads, int max_ctx);
 template <typename T>
 void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len,
                         int max_ctx, hipStream_t s);
