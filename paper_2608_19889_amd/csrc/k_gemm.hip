@@ -134,9 +134,204 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
   }
 }
 
+// ============================================================================
+// Large prefill GEMM: 256 (W rows) x 256 (tokens) tiles, k-tiles of BK, 8
+// wavefronts in a 2 x 4 arrangement, each owning 128 x 64 = 4 x 2 blocks of
+// v_mfma_f32_32x32x16_bf16.  Operands go straight from global memory to LDS
+// (global_load_lds_dwordx4: lane L of an instruction writes 16 bytes at LDS
+// offset 16 L) into a ring of STAGES k-tiles in 128 KB of LDS, loads running
+// STAGES-1 k-tiles ahead; the bank swizzle of the panels is produced by
+// choosing which global chunk each lane loads.
+// Workgroups are renumbered so that each XCD (workgroup id mod 8) receives a
+// contiguous range of tiles, walked in groups of 8 token tiles so that
+// neighbouring tiles share operand panels in that XCD's L2.
+// ============================================================================
+namespace pf2 {
+constexpr int BN = 256, BM = 256;
+}
+
+AXON_DEV void tile_order(int bid, int gx, int gy, int& pn, int& pm) {
+  const int G = gx * gy;
+  int logical = bid;
+  const int full = G / 8 * 8;
+  if (bid < full) logical = (bid % 8) * (full / 8) + bid / 8;
+  constexpr int GROUP = 8;
+  const int per_group = GROUP * gx;
+  const int gid = logical / per_group;
+  const int first_m = gid * GROUP;
+  const int gsize = min(gy - first_m, GROUP);
+  pm = first_m + (logical % per_group) % gsize;
+  pn = (logical % per_group) / gsize;
+}
+
+// physical 16-byte chunk of logical chunk c in row r of an LDS panel with CH
+// chunks per row: 8 consecutive rows reading the same logical chunk hit
+// distinct bank groups
+template <int CH>
+AXON_DEV int swz(int r, int c) {
+  if constexpr (CH == 8) return c ^ (r & 7);
+  else return c ^ ((r >> 1) & 3);
+}
+
+template <int STAGES>
+AXON_DEV void wait_stage(int after) {
+  // allow the loads of ``after`` later stages (4 per stage per thread at BK 32,
+  // 8 at BK 64) to stay in flight
+  if constexpr (STAGES == 2) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  } else {
+    if (after >= 2) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else if (after == 1) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+}
+
+template <int EPI, int BK, int STAGES, int NWV>
+__global__ void __launch_bounds__(NWV * 64, 1) gemm_bf16_256_kernel(const bf16* __restrict__ W,
+                                                                    const bf16* __restrict__ X, int N, int M, int K,
+                                                                    EpiArgs ep) {
+  using namespace pf2;
+  constexpr int CH = BK / 8;                 // 16-byte chunks per panel row
+  constexpr int PANEL = BN * CH;             // chunks per operand panel
+  constexpr int STAGE = 2 * PANEL;           // W panel + X panel
+  constexpr int NT = NWV * 64;
+  constexpr int LPT = PANEL / NT;            // chunks per thread per operand per stage
+  constexpr int WCOLS = NWV / 2;             // wavefront columns (token direction)
+  constexpr int TB = 256 / WCOLS / 32;       // 32-token blocks per wavefront
+  extern __shared__ bf16x8 lds2[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave / WCOLS, wc = wave % WCOLS;
+  const int gx = (N + BN - 1) / BN, gy = (M + BM - 1) / BM;
+  int pn, pm;
+  tile_order(blockIdx.x, gx, gy, pn, pm);
+  const int n0 = pn * BN, m0 = pm * BM;
+
+  // this thread's chunks of each operand per stage: q = (i*NWV + wave)*64 + lane
+  const bf16* wsrc[LPT];
+  const bf16* xsrc[LPT];
+#pragma unroll
+  for (int i = 0; i < LPT; ++i) {
+    const int q = (i * NWV + wave) * 64 + lane;
+    const int row = q / CH, c = swz<CH>(row, q % CH);  // swz is its own inverse
+    const int n = min(n0 + row, N - 1), m = min(m0 + row, M - 1);  // rows past the edge: any valid row
+    wsrc[i] = W + (int64_t)n * K + c * 8;
+    xsrc[i] = X + (int64_t)m * K + c * 8;
+  }
+  auto issue = [&](int stage, int k0) {
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+      bf16x8* base = lds2 + stage * STAGE + (i * NWV + wave) * 64;
+      __builtin_amdgcn_global_load_lds((const void*)(wsrc[i] + k0), (__attribute__((address_space(3))) void*)base,
+                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)(xsrc[i] + k0),
+                                       (__attribute__((address_space(3))) void*)(base + PANEL), 16, 0, 0);
+    }
+  };
+
+  f32x16 acc[4][TB];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < TB; ++b) acc[a][b] = f32x16{};
+
+  const int nk = K / BK;
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < nk) issue(st, st * BK);
+  for (int kt = 0; kt < nk; ++kt) {
+    wait_stage<STAGES>(min(STAGES - 2, nk - 1 - kt));
+    __syncthreads();  // stage kt landed for every wavefront; stage kt-1 is free
+    if (kt + STAGES - 1 < nk) issue((kt + STAGES - 1) % STAGES, (kt + STAGES - 1) * BK);
+    const bf16x8* la = lds2 + (kt % STAGES) * STAGE;
+    const bf16x8* lb = la + PANEL;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int ch = ks * 2 + (lane >> 5);
+      bf16x8 fa[4], fb[TB];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const int r = wr * 128 + a * 32 + (lane & 31);
+        fa[a] = la[r * CH + swz<CH>(r, ch)];
+      }
+#pragma unroll
+      for (int b = 0; b < TB; ++b) {
+        const int r = wc * (32 * TB) + b * 32 + (lane & 31);
+        fb[b] = lb[r * CH + swz<CH>(r, ch)];
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < TB; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+    }
+  }
+  // epilogue: acc[a][b][i] = C[n][t],
+  //   n = n0 + wr*128 + a*32 + (i/4)*8 + (lane/32)*4 + i%4,  t = m0 + wc*32*TB + b*32 + lane%32
+#pragma unroll
+  for (int b = 0; b < TB; ++b) {
+    const int t = m0 + wc * (32 * TB) + b * 32 + (lane & 31);
+    if (t >= M) continue;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const int nb = n0 + wr * 128 + a * 32;
+      if (nb >= N) continue;
+      if constexpr (EPI == EPI_SILU) {
+        bf16* out = (bf16*)ep.out_t + (int64_t)t * ep.ldo + (nb / 32) * 16;
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          const int f = g * 8 + (lane >> 5) * 4;
+          bf16x4 v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = (bf16)(silu_f(acc[a][b][g * 4 + j]) * acc[a][b][8 + g * 4 + j]);
+          *(bf16x4*)(out + f) = v;
+        }
+      } else {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = nb + g * 8 + (lane >> 5) * 4;
+          if (n >= N) continue;
+          float* p = ep.out_f32 + (int64_t)t * ep.ldo + n;
+          f32x4 v = {acc[a][b][g * 4 + 0], acc[a][b][g * 4 + 1], acc[a][b][g * 4 + 2], acc[a][b][g * 4 + 3]};
+          store_cols<EPI == EPI_RESID>(p, v, N - n);
+        }
+      }
+    }
+  }
+}
+
+#ifndef AXON_G256_BK
+#define AXON_G256_BK 64
+#define AXON_G256_STAGES 2
+#define AXON_G256_WAVES 8
+#endif
+constexpr int G256_BK = AXON_G256_BK, G256_STAGES = AXON_G256_STAGES, G256_WAVES = AXON_G256_WAVES;
+constexpr int G256_LDS = G256_STAGES * 2 * pf2::BN * (G256_BK / 8) * 16;
+
+template <int EPI>
+static void launch_256(const bf16* W, const bf16* X, int N, int M, int K, const EpiArgs& ep, hipStream_t s) {
+  static bool attr = false;
+  auto kern = gemm_bf16_256_kernel<EPI, G256_BK, G256_STAGES, G256_WAVES>;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, G256_LDS);
+    attr = true;
+  }
+  const int tiles = ((N + pf2::BN - 1) / pf2::BN) * ((M + pf2::BM - 1) / pf2::BM);
+  kern<<<tiles, G256_WAVES * 64, G256_LDS, s>>>(W, X, N, M, K, ep);
+}
+
 void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi, const EpiArgs& ep,
                       hipStream_t s) {
   if (M <= 0) return;
+  // 256 x 256 tiles unless that leaves most CUs idle (fewer than 160 tiles)
+  const int64_t tiles256 = (int64_t)((N + 255) / 256) * ((M + 255) / 256);
+  if (M >= 256 && N >= 256 && tiles256 >= 160) {
+    switch (epi) {
+      case EPI_F32: launch_256<EPI_F32>(W, X, N, M, K, ep, s); return;
+      case EPI_RESID: launch_256<EPI_RESID>(W, X, N, M, K, ep, s); return;
+      case EPI_SILU: launch_256<EPI_SILU>(W, X, N, M, K, ep, s); return;
+      default: break;
+    }
+  }
   dim3 grid((N + pf::BN - 1) / pf::BN, (M + pf::BM - 1) / pf::BM);
   switch (epi) {
     case EPI_F32: gemm_bf16_kernel<EPI_F32><<<grid, 256, 0, s>>>(W, X, N, M, K, ep); break;
