@@ -52,7 +52,17 @@ def main():
     ap.add_argument("--workload", default="1b", choices=["1b", "7b", "135m", "7b_paged", "32b"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--decode-steps", type=int, default=None,
+                    help="override the workload's decode step count (hardware-counter runs only)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="finish with one 1 GiB device-to-device copy (a known-size reference for HBM counters)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) of a "
+                         "--copy-calibration run into profiles/decode_gemv_<workload>_traffic.json and exit")
     args = ap.parse_args()
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters[0], args.summarize_counters[1], args.workload)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(this build has no multi-GPU path)", file=sys.stderr)
@@ -70,7 +80,7 @@ def main():
     wl = dict(WORKLOADS[args.workload])
     shape = MODEL_SHAPES[wl["model"]]
     esz = 2 if shape["dtype"] == "bf16" else 4
-    B, steps = wl["batch"], wl["steps"]
+    B, steps = wl["batch"], wl["steps"] if args.decode_steps is None else args.decode_steps
     L, D, V = shape["num_hidden_layers"], shape["hidden_size"], shape["vocab_size"]
     KV, hd = shape["num_key_value_heads"], shape["head_dim"]
     dev = "cuda"
@@ -181,7 +191,16 @@ def main():
 
     if not args.no_roofline:
         out.update(roofline_pass(m, generate, shape, esz, lens))
+        out["roofline"]["traffic"] = measured_traffic(out["roofline"], args.workload)
     m.close()
+    if args.copy_calibration:
+        src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] calibration copy: 1 GiB read + 1 GiB written")
+        del src, dst
     del w
     torch.cuda.empty_cache()
 
@@ -242,14 +261,89 @@ def roofline_pass(m, generate, shape, esz, lens):
     return {"roofline": r, "kernels": kernels}
 
 
-def cpu_baseline(shape, wl, lens, steps, B):
-    """The float64 oracle on the host cores, on a bounded sample: one sequence,
-    a short prefill and a few decode steps; its per-token costs are scaled to
-    the workload's generated tokens/s."""
+def kernel_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("k_gemv.hip", "kernels.h", "common.h"):
+        h.update(open(os.path.join(ROOT, "paper_2608_19889_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(roof, workload):
+    """HBM bytes per launch of the decode projection kernels from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE runs (scaled by the counters' reading of
+    a 1 GiB copy), or None when those counters were taken on other kernel
+    sources or another workload."""
+    path = os.path.join(ROOT, "profiles", f"decode_gemv_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_source_digest") != kernel_source_digest():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def summarize_counters(fetch_csv, write_csv, workload):
+    """HBM bytes per decode-projection launch from FETCH_SIZE / WRITE_SIZE
+    (KiB per dispatch).  Each counter is scaled by what it reads for the 1 GiB
+    calibration copy (the largest __amd_rocclr_copyBuffer dispatch); per-kernel
+    averages are then weighted by the launch mix of one generate on the
+    workload (per decode step: QKV, O, gate/up and down projections of every
+    layer plus the head; plus the prefill's head)."""
+    import csv
+    from synthetic import MODEL_SHAPES, WORKLOADS
+    wl = WORKLOADS[workload]
+    L, steps = MODEL_SHAPES[wl["model"]]["num_hidden_layers"], wl["steps"]
+
+    def per_kernel(path):
+        rows = list(csv.DictReader(open(path)))
+        cal = max(float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"])
+        scale = (1 << 30) / (cal * 1024.0)
+        agg = {}
+        for r in rows:
+            name = r["Kernel_Name"]
+            if "gemv_fused_kernel" not in name:
+                continue
+            key = name[name.index("gemv_fused_kernel"):name.index(">") + 1]
+            a = agg.setdefault(key, [0, 0.0])
+            a[0] += 1
+            a[1] += float(r["Counter_Value"]) * 1024.0 * scale
+        return scale, {k: v[1] / v[0] for k, v in agg.items()}
+
+    fs, fetch = per_kernel(fetch_csv)
+    ws, write = per_kernel(write_csv)
+    per = {k: fetch[k] + write.get(k, 0.0) for k in fetch}
+    # classify: the head kernels have 64 or 32 rows and the GV_HEAD epilogue (last template argument 0)
+    head_dec = [k for k in per if k.endswith(", true, 0>")]
+    head_pre = [k for k in per if k.endswith(", false, 0>")]
+    layer = [k for k in per if not k.endswith(", 0>")]
+    step_bytes = L * sum(per[k] for k in layer) + sum(per[k] for k in head_dec)
+    launches = steps * (4 * L + 1) + 1
+    total = steps * step_bytes + sum(per[k] for k in head_pre)
+    rec = {"workload": workload, "kernel_source_digest": kernel_source_digest(),
+           "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
+           "hbm_bytes_per_kernel": {k: round(v) for k, v in sorted(per.items())},
+           "hbm_bytes_per_launch": round(total / launches),
+           "launch_mix": f"{steps} decode steps x ({L} layers x 4 projections + head) + prefill head = {launches}",
+           "commands": [f"rocprofv3 --pmc {c} --kernel-include-regex 'gemv_fused|copyBuffer|elementwise_kernel' "
+                        f"-f csv -d <dir> -o run -- python3 bench.py --workload {workload} --steps 1 --warmup 0 "
+                        f"--decode-steps 4 --no-cpu-baseline --no-roofline --copy-calibration"
+                        for c in ("FETCH_SIZE", "WRITE_SIZE")]}
+    out = os.path.join(ROOT, "profiles", f"decode_gemv_{workload}_traffic.json")
+    with open(out, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec, indent=1))
+
+
+def cpu_baseline(shape, wl, lens, steps, B, seqs_sample=2):
+    """The float64 oracle on the host cores, on a bounded sample of the same
+    workload: the first ``seqs_sample`` sequences run in full (prefill of the
+    real prompt, then every greedy decode step).  The oracle processes one
+    sequence at a time, so generated tokens / wall time over the sample is its
+    throughput on the whole batch."""
     import numpy as np
-    import torch
     import oracle
-    from synthetic import model_weights, prompts
+    from synthetic import model_weights, paged_workload, prompts
     try:
         from threadpoolctl import threadpool_info
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [os.cpu_count()])
@@ -260,27 +354,21 @@ def cpu_baseline(shape, wl, lens, steps, B):
     orc = oracle.OracleDecoder(shape, w)
     del w
     log(f"[bench] oracle weights ready in {time.time() - t0:.1f}s")
-    P_s, S_s = 64, 3
-    ids = prompts(1, P_s, shape["vocab_size"], seed=0)[0].numpy()
+    if wl["paged"]:
+        seqs, _, _ = paged_workload(B, wl["len_range"][0], wl["len_range"][1], steps, shape["vocab_size"],
+                                    wl["page_size"], seed=0)
+        seqs = [s.numpy() for s in seqs[:seqs_sample]]
+    else:
+        seqs = list(prompts(B, wl["prompt_len"], shape["vocab_size"], seed=0).numpy()[:seqs_sample])
     t1 = time.perf_counter()
-    lg = orc.prefill([ids])
+    toks, _ = oracle.generate_greedy(orc, seqs, steps)
     t2 = time.perf_counter()
-    tok = [int(np.argmax(lg[0]))]
-    for _ in range(S_s):
-        tok = [int(np.argmax(orc.decode(tok)[0]))]
-    t3 = time.perf_counter()
-    pre_tok_s = P_s / (t2 - t1)
-    dec_step_s = (t3 - t2) / S_s
-    # workload time on the oracle: prefill all prompt tokens, then every
-    # sequence's decode steps one at a time (the oracle has no batching)
-    total_s = sum(lens) / pre_tok_s + B * steps * dec_step_s
-    value = B * (steps + 1) / total_s
-    log(f"[bench] oracle sample: prefill {pre_tok_s:.1f} tok/s, decode {dec_step_s:.3f} s/token")
+    gen = toks.size
+    value = gen / (t2 - t1)
+    log(f"[bench] oracle sample: {gen} tokens in {t2 - t1:.1f}s")
     return {"value": round(value, 4), "unit": "generated tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"1 sequence: {P_s}-token prefill ({t2 - t1:.1f}s) + {S_s} decode steps "
-                      f"({t3 - t2:.1f}s) of the same model in float64; scaled to the workload "
-                      f"({sum(lens)} prompt tokens, {B}x{steps} decode tokens)",
-            "prefill_tok_s": round(pre_tok_s, 2), "decode_s_per_token": round(dec_step_s, 4)}
+            "sample": f"{len(seqs)} of the {B} sequences, complete (prefill of {[len(x) for x in seqs]} prompt "
+                      f"tokens + {steps} greedy decode steps each), float64, {t2 - t1:.1f}s"}
 
 
 if __name__ == "__main__":

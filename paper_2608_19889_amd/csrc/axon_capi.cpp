@@ -20,6 +20,8 @@
 
 using namespace axon;
 
+thread_local axon::TimingSlot axon::g_timing_slot;
+
 namespace {
 
 thread_local std::string g_err;
@@ -181,7 +183,9 @@ struct axon_model {
     }
     return tpool[tnext++];
   }
-  // Run ``launch`` between two events on s when timing is on.
+  // Time ``launch`` when timing is on.  Single-kernel classes (projections)
+  // carry the events in their own dispatch; multi-kernel ones are bracketed
+  // by event records on s.
   template <typename F>
   void timed(int cls, int d0, int d1, int d2, hipStream_t s, F&& launch) {
     if (!timing) {
@@ -189,10 +193,22 @@ struct axon_model {
       return;
     }
     TimingRec r{cls, d0, d1, d2, tevent(), tevent()};
-    if (r.a) (void)hipEventRecord(r.a, s);
+    if (!r.a || !r.b) {
+      launch();
+      return;
+    }
+    if (cls == 0 || cls == 1) {
+      axon::g_timing_slot = axon::TimingSlot{r.a, r.b};
+      launch();
+      const bool used = axon::g_timing_slot.start == nullptr;
+      axon::g_timing_slot = axon::TimingSlot{};
+      if (used) trecs.push_back(r);
+      return;
+    }
+    (void)hipEventRecord(r.a, s);
     launch();
-    if (r.b) (void)hipEventRecord(r.b, s);
-    if (r.a && r.b) trecs.push_back(r);
+    (void)hipEventRecord(r.b, s);
+    trecs.push_back(r);
   }
 
   int D() const { return cfg.hidden; }

@@ -316,7 +316,7 @@ static void launch_256(const bf16* W, const bf16* X, int N, int M, int K, const 
     attr = true;
   }
   const int tiles = ((N + pf2::BN - 1) / pf2::BN) * ((M + pf2::BM - 1) / pf2::BM);
-  kern<<<tiles, G256_WAVES * 64, G256_LDS, s>>>(W, X, N, M, K, ep);
+  klaunch(kern, dim3(tiles), dim3(G256_WAVES * 64), G256_LDS, s, W, X, N, M, K, ep);
 }
 
 void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi, const EpiArgs& ep,
@@ -334,9 +334,9 @@ void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi
   }
   dim3 grid((N + pf::BN - 1) / pf::BN, (M + pf::BM - 1) / pf::BM);
   switch (epi) {
-    case EPI_F32: gemm_bf16_kernel<EPI_F32><<<grid, 256, 0, s>>>(W, X, N, M, K, ep); break;
-    case EPI_RESID: gemm_bf16_kernel<EPI_RESID><<<grid, 256, 0, s>>>(W, X, N, M, K, ep); break;
-    case EPI_SILU: gemm_bf16_kernel<EPI_SILU><<<grid, 256, 0, s>>>(W, X, N, M, K, ep); break;
+    case EPI_F32: klaunch(gemm_bf16_kernel<EPI_F32>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
+    case EPI_RESID: klaunch(gemm_bf16_kernel<EPI_RESID>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
+    case EPI_SILU: klaunch(gemm_bf16_kernel<EPI_SILU>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
     default: break;
   }
 }
@@ -393,8 +393,8 @@ void launch_gemm_f32(const float* W, const float* X, int N, int M, int K, int ep
                      hipStream_t s) {
   if (M <= 0) return;
   dim3 grid((N + 63) / 64, (M + 63) / 64);
-  if (epi == EPI_RESID) gemm_f32_kernel<EPI_RESID><<<grid, 256, 0, s>>>(W, X, N, M, K, ep);
-  else gemm_f32_kernel<EPI_F32><<<grid, 256, 0, s>>>(W, X, N, M, K, ep);
+  if (epi == EPI_RESID) klaunch(gemm_f32_kernel<EPI_RESID>, grid, dim3(256), 0, s, W, X, N, M, K, ep);
+  else klaunch(gemm_f32_kernel<EPI_F32>, grid, dim3(256), 0, s, W, X, N, M, K, ep);
 }
 
 // ============================================================================

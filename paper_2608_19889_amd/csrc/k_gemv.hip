@@ -331,10 +331,10 @@ template <int ROWS, int KS, bool NORM, int EPI>
 static void gv_nb(const GemvArgs& a, hipStream_t s) {
   const dim3 grid((a.N + ROWS - 1) / ROWS);
   switch ((a.M + 15) / 16) {
-    case 1: gemv_fused_kernel<ROWS, ks_for(KS, 1), 1, NORM, EPI><<<grid, ks_for(KS, 1) * 64, 0, s>>>(a); break;
-    case 2: gemv_fused_kernel<ROWS, ks_for(KS, 2), 2, NORM, EPI><<<grid, ks_for(KS, 2) * 64, 0, s>>>(a); break;
-    case 3: gemv_fused_kernel<ROWS, ks_for(KS, 3), 3, NORM, EPI><<<grid, ks_for(KS, 3) * 64, 0, s>>>(a); break;
-    default: gemv_fused_kernel<ROWS, ks_for(KS, 4), 4, NORM, EPI><<<grid, ks_for(KS, 4) * 64, 0, s>>>(a); break;
+    case 1: klaunch(gemv_fused_kernel<ROWS, ks_for(KS, 1), 1, NORM, EPI>, grid, dim3(ks_for(KS, 1) * 64), 0, s, a); break;
+    case 2: klaunch(gemv_fused_kernel<ROWS, ks_for(KS, 2), 2, NORM, EPI>, grid, dim3(ks_for(KS, 2) * 64), 0, s, a); break;
+    case 3: klaunch(gemv_fused_kernel<ROWS, ks_for(KS, 3), 3, NORM, EPI>, grid, dim3(ks_for(KS, 3) * 64), 0, s, a); break;
+    default: klaunch(gemv_fused_kernel<ROWS, ks_for(KS, 4), 4, NORM, EPI>, grid, dim3(ks_for(KS, 4) * 64), 0, s, a); break;
   }
 }
 

@@ -1,12 +1,32 @@
 // Host-side launchers of the gfx950 kernels.  Every launcher enqueues on the
 // given stream and returns immediately; shapes are validated by the caller.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "common.h"
 
 namespace axon {
+
+// Measurement hook: when the runtime arms this slot, the next kernel launched
+// through klaunch() carries the two events in its own dispatch
+// (hipExtLaunchKernelGGL), so their elapsed time is that kernel's execution.
+struct TimingSlot {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local TimingSlot g_timing_slot;
+
+template <typename Kern, typename... Args>
+void klaunch(Kern kern, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
+  if (g_timing_slot.start) {
+    const TimingSlot t = g_timing_slot;
+    g_timing_slot = TimingSlot{};
+    hipExtLaunchKernelGGL(kern, grid, block, shmem, s, t.start, t.stop, 0, args...);
+  } else {
+    kern<<<grid, block, shmem, s>>>(args...);
+  }
+}
 
 // Epilogues of the projection GEMMs (out[t][n] = sum_k X[t][k] * W[n][k]).
 enum Epi : int {
