@@ -5,8 +5,8 @@ and the ``cpu_baseline`` leg of ``bench.py``; never by the product path.
 """
 from .decoder import (OracleDecoder, apply_rope, causal_gqa_attention, generate_greedy,
                       greedy, rms_norm, rope_cos_sin, rope_inv_freq, round_to_bf16,
-                      round_to_f32, silu, softmax, swiglu_mlp, teacher_forced)
+                      round_to_f32, silu, softmax, swiglu_mlp, teacher_forced, weights_f64)
 
 __all__ = ["OracleDecoder", "apply_rope", "causal_gqa_attention", "generate_greedy", "greedy",
            "rms_norm", "rope_cos_sin", "rope_inv_freq", "round_to_bf16", "round_to_f32",
-           "silu", "softmax", "swiglu_mlp", "teacher_forced"]
+           "silu", "softmax", "swiglu_mlp", "teacher_forced", "weights_f64"]

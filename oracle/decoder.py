@@ -273,8 +273,15 @@ def teacher_forced(model: OracleDecoder, seqs, forced: np.ndarray):
 
 
 def _to_f64(t) -> np.ndarray:
+    """float64 view of a weight; float64 arrays are used as given (no copy), so
+    several oracle instances can share one converted weight map."""
     if hasattr(t, "detach"):
         t = t.detach().to("cpu")
         import torch  # local: only to read torch inputs
         return t.to(torch.float64).numpy()
     return np.asarray(t, dtype=np.float64)
+
+
+def weights_f64(weights: dict) -> dict:
+    """Convert a weight map once, for sharing between oracle instances."""
+    return {k: _to_f64(v) for k, v in weights.items()}

@@ -343,7 +343,8 @@ void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi
 
 // ============================================================================
 // float32 check-mode GEMM: 64 x 64 tiles, k-step 16, 256 threads with a 4 x 4
-// register block each, operands staged k-major in LDS.
+// register block each, operands staged k-major in LDS.  Dot products use
+// compensated (Kahan) float32 summation, so their error does not grow with K.
 // ============================================================================
 template <int EPI>
 __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__ W, const float* __restrict__ X,
@@ -353,7 +354,7 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
   const int n0 = blockIdx.x * 64, m0 = blockIdx.y * 64;
   const int lr = tid >> 2, lk = (tid & 3) * 4;
   const int tf = tid & 15, tt = tid >> 4;
-  float acc[4][4] = {};
+  float acc[4][4] = {}, comp[4][4] = {};
   for (int k0 = 0; k0 < K; k0 += 16) {
     {
       const int n = n0 + lr, m = m0 + lr;
@@ -372,7 +373,12 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
       float a[4], b[4];
       for (int i = 0; i < 4; ++i) { a[i] = ws[kk][tf * 4 + i]; b[i] = xs[kk][tt * 4 + i]; }
       for (int i = 0; i < 4; ++i)
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < 4; ++j) {
+          const float y = fmaf(a[i], b[j], -comp[i][j]);
+          const float t = acc[i][j] + y;
+          comp[i][j] = (t - acc[i][j]) - y;
+          acc[i][j] = t;
+        }
     }
     __syncthreads();
   }
