@@ -9,6 +9,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <functional>
 #include <map>
 #include <string>
 #include <tuple>
@@ -169,6 +170,7 @@ struct axon_model {
   hipStream_t cap_stream = nullptr;
   std::map<GraphKey, hipGraphExec_t> graphs;
   bool use_graphs = true;
+  std::string enqueue_err;  // set while enqueueing a step when a launch had no kernel
   // kernel timing (measurement mode)
   bool timing = false;
   std::vector<TimingRec> trecs;
@@ -280,6 +282,16 @@ void gemm_few_f32(axon_model* m, const void* W, const void* X, int N, int M, int
   m->timed(0, N, M, K, s, [&] { launch_gemm_f32((const float*)W, (const float*)X, N, M, K, epi, ep, s); });
 }
 
+// Fused few-token projection; a shape with no kernel is recorded in
+// m->enqueue_err (checked by the caller once the step is enqueued).
+void gemv_step(axon_model* m, const GemvArgs& a, int epi, hipStream_t s) {
+  bool ok = true;
+  m->timed(0, a.N, a.M, a.K, s, [&] { ok = launch_gemv_fused(a, epi, s); });
+  if (!ok && m->enqueue_err.empty())
+    m->enqueue_err = "no fused projection kernel for N=" + std::to_string(a.N) + " K=" + std::to_string(a.K) +
+                     " M=" + std::to_string(a.M) + " epilogue " + std::to_string(epi);
+}
+
 template <typename T>
 void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, const int32_t* d_cu,
                      const int32_t* h_cu, int all_logits, float* d_logits, int32_t* d_next, hipStream_t s) {
@@ -314,46 +326,57 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
   if (all_logits) {
     gemm_many<T>(m, m->lm_head, h, V, Ttok, D, EPI_F32, d_logits, nullptr, V, s);
     launch_argmax_rows(d_logits, B, V, d_next, d_cu, s);
-  } else if constexpr (sizeof(T) == 2) {
+  } else if (sizeof(T) == 2 && B <= GEMV_MAX_M) {
     GemvArgs ha{};
     ha.W = (const bf16*)m->lm_head; ha.N = V; ha.K = D; ha.M = B; ha.X = (const bf16*)m->hlast;
     ha.out_f32 = d_logits; ha.ldo = V; ha.am_val = m->am_val; ha.am_idx = m->am_idx;
-    m->timed(0, V, B, D, s, [&] { launch_gemv_fused(ha, GV_HEAD, s); });
+    gemv_step(m, ha, GV_HEAD, s);
     const int hr = gemv_rows(V, D, B, GV_HEAD);
     launch_argmax_final(m->am_val, m->am_idx, (V + hr - 1) / hr, B, d_next, nullptr, s);
   } else {
     float* dst = d_logits ? d_logits : m->logits_int;
-    gemm_few_f32(m, m->lm_head, m->hlast, V, B, D, EPI_F32, dst, V, s);
+    if constexpr (sizeof(T) == 2) gemm_many<T>(m, m->lm_head, m->hlast, V, B, D, EPI_F32, dst, nullptr, V, s);
+    else gemm_few_f32(m, m->lm_head, m->hlast, V, B, D, EPI_F32, dst, V, s);
     launch_argmax(dst, B, V, d_next, nullptr, s);
   }
 }
 
-// Decode step, float32 check mode: GEMM + separate normalization kernels.
-void enqueue_decode_f32(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
-                        hipStream_t s) {
-  using T = float;
+// Decode step as separate GEMM, RoPE/KV, attention and normalization kernels:
+// the float32 check mode, and bf16 batches wider than one fused projection.
+template <typename T>
+void enqueue_decode_many(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
+                         hipStream_t s) {
   const int D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V(), nq = m->nqkv();
   const float eps = m->cfg.rms_eps;
   T* h = (T*)m->h;
   launch_embed_rmsnorm<T>(d_tokens, (const T*)m->embed, (const T*)m->layers[0].gin, m->x, h, B, D, V, eps, s);
+  // projection: bf16 prefill GEMM, or the float32 GEMM of the check mode
+  auto proj = [&](const void* W, const void* X, int N, int K, int epi, float* out_f32, void* out_t, int ldo) {
+    if constexpr (sizeof(T) == 2) gemm_many<T>(m, W, X, N, B, K, epi, out_f32, out_t, ldo, s);
+    else gemm_few_f32(m, W, X, N, B, K, epi, out_f32, ldo, s);
+  };
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const LayerW& w = m->layers[l];
     KVView kv = m->kv(l, m->paged());
-    gemm_few_f32(m, w.wqkv, h, nq, B, D, EPI_F32, m->qkv, nq, s);
+    proj(w.wqkv, h, nq, D, EPI_F32, m->qkv, nullptr, nq);
     launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, B, 0, nullptr,
                       m->d_len, H, s);
     launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
-    gemm_few_f32(m, w.wo, m->o, D, B, H * hd, EPI_RESID, m->x, D, s);
+    proj(w.wo, m->o, D, H * hd, EPI_RESID, m->x, nullptr, D);
     launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, B, D, eps, nullptr, s);
-    gemm_few_f32(m, w.wgu, h, 2 * I, B, D, EPI_F32, m->gu_f32, 2 * I, s);
-    launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, B, I, s);
-    gemm_few_f32(m, w.wd, m->a, D, B, I, EPI_RESID, m->x, D, s);
+    if constexpr (sizeof(T) == 2) {
+      proj(w.wgu, h, 2 * I, D, EPI_SILU, nullptr, m->a, I);
+    } else {
+      proj(w.wgu, h, 2 * I, D, EPI_F32, m->gu_f32, nullptr, 2 * I);
+      launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, B, I, s);
+    }
+    proj(w.wd, m->a, D, I, EPI_RESID, m->x, nullptr, D);
     const bool last = l + 1 == m->cfg.n_layers;
     const T* gnext = (const T*)(last ? m->gfinal : m->layers[l + 1].gin);
     launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, gnext, h, B, D, eps, nullptr, s);
   }
   float* dst = d_logits ? d_logits : m->logits_int;
-  gemm_few_f32(m, m->lm_head, h, V, B, D, EPI_F32, dst, V, s);
+  proj(m->lm_head, h, V, D, EPI_F32, dst, nullptr, V);
   launch_argmax(dst, B, V, d_next, m->d_len, s);
 }
 
@@ -370,7 +393,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
   bf16* xg = (bf16*)m->xg;
   launch_embed_ss(d_tokens, (const bf16*)m->embed, (const bf16*)m->layers[0].gin, m->x, xg, m->ss, B, D, V, s);
   int ss_n = 1;
-  auto gemv = [&](GemvArgs& a, int epi) { m->timed(0, a.N, a.M, a.K, s, [&] { launch_gemv_fused(a, epi, s); }); };
+  auto gemv = [&](GemvArgs& a, int epi) { gemv_step(m, a, epi, s); };
   auto ss_count = [&](int K) {
     const int rr = gemv_rows(D, K, B, GV_RESID);
     return (D + rr - 1) / rr;
@@ -417,14 +440,24 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
 }
 
 void enqueue_decode(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next, hipStream_t s) {
-  if (m->bf) enqueue_decode_bf16(m, B, d_tokens, d_logits, d_next, s);
-  else enqueue_decode_f32(m, B, d_tokens, d_logits, d_next, s);
+  if (m->bf && B <= GEMV_MAX_M) enqueue_decode_bf16(m, B, d_tokens, d_logits, d_next, s);
+  else if (m->bf) enqueue_decode_many<bf16>(m, B, d_tokens, d_logits, d_next, s);
+  else enqueue_decode_many<float>(m, B, d_tokens, d_logits, d_next, s);
 }
 
 int check_launch(const char* what) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(AXON_E_HIP, std::string(what) + ": kernel launch failed: " + hipGetErrorString(e));
   return AXON_OK;
+}
+
+// A projection shape without a kernel (never produced by a validated model):
+// reported, and cleared for the next call.
+int take_enqueue_err(axon_model* m, const char* what) {
+  if (m->enqueue_err.empty()) return AXON_OK;
+  std::string e;
+  e.swap(m->enqueue_err);
+  return fail(AXON_E_INVALID, std::string(what) + ": " + e);
 }
 
 }  // namespace
@@ -513,34 +546,80 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     return AXON_OK;
   };
 
-  TRY(copy_in(&m->embed, get("model.embed_tokens.weight")));
+  // Weight matrices.  ``fill`` writes the row-major (permuted) matrix; float
+  // models keep it as is, bf16 models stage it in ``stage`` and store it
+  // fragment-tiled (every bf16 projection kernel and the embedding gather
+  // read that layout).
+  struct StageBuf {
+    void* p = nullptr;
+    ~StageBuf() {
+      if (p) (void)hipFree(p);  // waits for the tiling kernels that read it
+    }
+  } stage;
+  if (m->bf) {
+    const int64_t most = std::max({V * D, nq * D, D * H * hd, 2 * I * D});
+    hipError_t e = hipMalloc(&stage.p, (size_t)most * esz);
+    if (e != hipSuccess) {
+      stage.p = nullptr;
+      (void)hipGetLastError();
+      release(m);
+      return fail(e == hipErrorOutOfMemory ? AXON_E_OOM : AXON_E_HIP,
+                  std::string("staging allocation failed: ") + hipGetErrorString(e));
+    }
+  }
+  auto matrix = [&](void** dst, int64_t N, int64_t K, const std::function<int(void*)>& fill) -> int {
+    if (!m->bf) {
+      int r = dev_alloc(m, dst, (size_t)N * K * esz);
+      return r ? r : fill(*dst);
+    }
+    int r = dev_alloc(m, dst, (size_t)(N + 15) / 16 * 16 * K * esz);
+    if (!r) r = fill(stage.p);
+    if (r) return r;
+    launch_tile_weight((const bf16*)stage.p, (bf16*)*dst, N, (int)K, s);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? AXON_OK : fail(AXON_E_HIP, std::string("weight tiling: ") + hipGetErrorString(e));
+  };
+  auto copy_to = [&](const axon_weight* w) {
+    return [&, w](void* dst) -> int {
+      const size_t bytes = (size_t)w->shape[0] * (size_t)w->shape[1] * esz;
+      hipError_t e = hipMemcpyAsync(dst, w->data, bytes, kind(w), s);
+      return e == hipSuccess ? AXON_OK
+                             : fail(AXON_E_HIP, std::string("copy of '") + w->name + "': " + hipGetErrorString(e));
+    };
+  };
+
+  TRY(matrix(&m->embed, V, D, copy_to(get("model.embed_tokens.weight"))));
   TRY(copy_in(&m->gfinal, get("model.norm.weight")));
   if (c.tie_embeddings) m->lm_head = m->embed;
-  else TRY(copy_in(&m->lm_head, get("lm_head.weight")));
+  else TRY(matrix(&m->lm_head, V, D, copy_to(get("lm_head.weight"))));
   m->layers.resize(c.n_layers);
   for (int l = 0; l < c.n_layers; ++l) {
     const std::string p = "model.layers." + std::to_string(l) + ".";
     LayerW& w = m->layers[l];
     TRY(copy_in(&w.gin, get(p + "input_layernorm.weight")));
     TRY(copy_in(&w.gpost, get(p + "post_attention_layernorm.weight")));
-    TRY(copy_in(&w.wo, get(p + "self_attn.o_proj.weight")));
-    TRY(copy_in(&w.wd, get(p + "mlp.down_proj.weight")));
+    TRY(matrix(&w.wo, D, H * hd, copy_to(get(p + "self_attn.o_proj.weight"))));
+    TRY(matrix(&w.wd, D, I, copy_to(get(p + "mlp.down_proj.weight"))));
     // fused QKV: heads q, then k, then v; within each head, rows in groups of
     // 8 = 4 first-half rows i and their rotation partners i + hd/2
-    TRY(dev_alloc(m, &w.wqkv, (size_t)nq * D * esz));
     const axon_weight* wq = get(p + "self_attn.q_proj.weight");
     const axon_weight* wk = get(p + "self_attn.k_proj.weight");
     const axon_weight* wv = get(p + "self_attn.v_proj.weight");
-    const size_t row = (size_t)D * esz;
-    for (int64_t hh = 0; hh < H + 2 * KV; ++hh) {
-      const axon_weight* src = hh < H ? wq : (hh < H + KV ? wk : wv);
-      const int64_t hs = hh < H ? hh : (hh < H + KV ? hh - H : hh - H - KV);
-      const char* sbase = (const char*)src->data + hs * hd * row;
-      char* dbase = (char*)w.wqkv + hh * hd * row;
-      HTRY(hipMemcpy2DAsync(dbase, 8 * row, sbase, 4 * row, 4 * row, hd / 8, kind(src), s));
-      HTRY(hipMemcpy2DAsync(dbase + 4 * row, 8 * row, sbase + (hd / 2) * row, 4 * row, 4 * row, hd / 8,
-                            kind(src), s));
-    }
+    TRY(matrix(&w.wqkv, nq, D, [&](void* dst) -> int {
+      const size_t row = (size_t)D * esz;
+      for (int64_t hh = 0; hh < H + 2 * KV; ++hh) {
+        const axon_weight* src = hh < H ? wq : (hh < H + KV ? wk : wv);
+        const int64_t hs = hh < H ? hh : (hh < H + KV ? hh - H : hh - H - KV);
+        const char* sbase = (const char*)src->data + hs * hd * row;
+        char* dbase = (char*)dst + hh * hd * row;
+        hipError_t e = hipMemcpy2DAsync(dbase, 8 * row, sbase, 4 * row, 4 * row, hd / 8, kind(src), s);
+        if (e == hipSuccess)
+          e = hipMemcpy2DAsync(dbase + 4 * row, 8 * row, sbase + (hd / 2) * row, 4 * row, 4 * row, hd / 8,
+                               kind(src), s);
+        if (e != hipSuccess) return fail(AXON_E_HIP, std::string("QKV repack: ") + hipGetErrorString(e));
+      }
+      return AXON_OK;
+    }));
     w.bqkv = nullptr;
     if (c.qkv_bias) {
       TRY(dev_alloc(m, &w.bqkv, (size_t)nq * esz));
@@ -552,12 +631,14 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
       HTRY(hipMemcpyAsync((char*)w.bqkv + (H + KV) * hd * esz, bv->data, KV * hd * esz, kind(bv), s));
     }
     // gate/up interleaved in blocks of 16 rows: [g0..g15, u0..u15, g16..g31, u16..u31, ...]
-    TRY(dev_alloc(m, &w.wgu, (size_t)2 * I * D * esz));
     const axon_weight* wg = get(p + "mlp.gate_proj.weight");
     const axon_weight* wu = get(p + "mlp.up_proj.weight");
-    const size_t blk = 16 * D * esz;
-    HTRY(hipMemcpy2DAsync(w.wgu, 2 * blk, wg->data, blk, blk, I / 16, kind(wg), s));
-    HTRY(hipMemcpy2DAsync((char*)w.wgu + blk, 2 * blk, wu->data, blk, blk, I / 16, kind(wu), s));
+    TRY(matrix(&w.wgu, 2 * I, D, [&](void* dst) -> int {
+      const size_t blk = 16 * D * esz;
+      hipError_t e = hipMemcpy2DAsync(dst, 2 * blk, wg->data, blk, blk, I / 16, kind(wg), s);
+      if (e == hipSuccess) e = hipMemcpy2DAsync((char*)dst + blk, 2 * blk, wu->data, blk, blk, I / 16, kind(wu), s);
+      return e == hipSuccess ? AXON_OK : fail(AXON_E_HIP, std::string("gate/up repack: ") + hipGetErrorString(e));
+    }));
   }
 
   // ---- KV cache
@@ -700,6 +781,7 @@ extern "C" int axon_prefill(axon_model* m, int32_t batch, const int32_t* d_token
     enqueue_prefill<float>(m, batch, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, all_logits, d_logits,
                            d_next_tokens, s);
   int rc = check_launch("prefill");
+  if (!rc) rc = take_enqueue_err(m, "prefill");
   if (rc) return rc;
   for (int b = 0; b < c.max_batch; ++b) m->h_len[b] = b < batch ? h_cu_seqlens[b + 1] - h_cu_seqlens[b] : 0;
   m->active = batch;
@@ -734,8 +816,13 @@ extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_t
       hipError_t ce = hipStreamEndCapture(m->cap_stream, &g);
       if (le != hipSuccess || ce != hipSuccess) {
         if (g) (void)hipGraphDestroy(g);
+        m->enqueue_err.clear();
         return fail(AXON_E_HIP, std::string("decode graph capture failed: ") +
                                     hipGetErrorString(le != hipSuccess ? le : ce));
+      }
+      if (int rc = take_enqueue_err(m, "decode")) {
+        (void)hipGraphDestroy(g);
+        return rc;
       }
       hipGraphExec_t ex = nullptr;
       hipError_t ie = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
@@ -747,6 +834,7 @@ extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_t
   } else {
     enqueue_decode(m, batch, d_tokens, d_logits, d_next_tokens, s);
     int rc = check_launch("decode");
+    if (!rc) rc = take_enqueue_err(m, "decode");
     if (rc) return rc;
   }
   for (int b = 0; b < batch; ++b) m->h_len[b] += 1;

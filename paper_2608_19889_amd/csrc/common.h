@@ -79,3 +79,15 @@ AXON_DEV int64_t k_off(const KVView& c, int slot, int kvh, int pos) {
 AXON_DEV int64_t vt_off(const KVView& c, int slot, int kvh, int d, int pos) {
   return ((kv_page(c, slot, pos) * c.kv_heads + kvh) * (int64_t)c.hd + d) * c.ps + pos % c.ps;
 }
+
+// Fragment-tiled storage of a bf16 weight matrix W [N][K] (K % 32 == 0).  Rows
+// come in blocks of 16 (the last block zero-padded); each block is cut along k
+// into 16 x 32 tiles of 1 KB, stored one after another, and a tile holds its
+// 64 16-byte chunks in the lane order of a v_mfma 16x16x32 A operand: chunk
+// (r, s) = row r of the block, k values 8s..8s+7 of the tile, at position
+// r + 16 s.  A wavefront's fragment load is one contiguous 1 KB read, and a
+// row block is one contiguous stream along k.
+// Element offset of W[n][8c .. 8c+7] (c = k-chunk index, k = 8c):
+AXON_DEV int64_t wt_chunk(int64_t n, int c, int K) {
+  return (((n >> 4) * (K >> 5) + (c >> 2)) * 64 + (n & 15) + 16 * (c & 3)) * 8;
+}

@@ -1,5 +1,6 @@
 // Projection GEMMs: out[t][n] = sum_k X[t][k] * W[n][k] (the F.linear
-// convention: W is [out, in] row-major, X is tokens x in).
+// convention: W is [out, in], X is tokens x in).  bf16 W is fragment-tiled
+// (wt_chunk), float W and both X row-major.
 //
 // Both operands are K-contiguous, so the kernels compute C^T = W X^T with W as
 // the MFMA A operand (rows = output features) and X as the B operand (columns
@@ -52,7 +53,7 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
     for (int i = 0; i < 4; ++i) {
       const int idx = tid + i * 256, row = idx >> 3, ch = idx & 7;
       const int n = n0 + row, m = m0 + row;
-      ra[i] = n < N ? *(const bf16x8*)(W + (int64_t)n * K + k0 + ch * 8) : zero8;
+      ra[i] = n < N ? *(const bf16x8*)(W + wt_chunk(n, (k0 >> 3) + ch, K)) : zero8;
       rb[i] = m < M ? *(const bf16x8*)(X + (int64_t)m * K + k0 + ch * 8) : zero8;
     }
   };
@@ -214,15 +215,17 @@ __global__ void __launch_bounds__(NWV * 64, 1) gemm_bf16_256_kernel(const bf16* 
     const int q = (i * NWV + wave) * 64 + lane;
     const int row = q / CH, c = swz<CH>(row, q % CH);  // swz is its own inverse
     const int n = min(n0 + row, N - 1), m = min(m0 + row, M - 1);  // rows past the edge: any valid row
-    wsrc[i] = W + (int64_t)n * K + c * 8;
+    wsrc[i] = W + wt_chunk(n, c, K);
     xsrc[i] = X + (int64_t)m * K + c * 8;
   }
+  // k-tile k0 (a multiple of 32) of a fragment-tiled row block starts k0 / 32
+  // tiles of 512 elements further on
   auto issue = [&](int stage, int k0) {
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
       bf16x8* base = lds2 + stage * STAGE + (i * NWV + wave) * 64;
-      __builtin_amdgcn_global_load_lds((const void*)(wsrc[i] + k0), (__attribute__((address_space(3))) void*)base,
-                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)(wsrc[i] + (int64_t)k0 * 16),
+                                       (__attribute__((address_space(3))) void*)base, 16, 0, 0);
       __builtin_amdgcn_global_load_lds((const void*)(xsrc[i] + k0),
                                        (__attribute__((address_space(3))) void*)(base + PANEL), 16, 0, 0);
     }

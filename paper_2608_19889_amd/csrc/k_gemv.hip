@@ -34,12 +34,11 @@ AXON_DEV float silu_g(float z) { return z / (1.f + __expf(-z)); }
 
 constexpr int GV_U = 4;  // k-steps of 32 per pipeline stage
 
-template <int ROWS, int KS, int NB, bool NORM, int EPI>
+template <int ROWS, int KS, int NB, bool NORM, int EPI, int U = GV_U>
 __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
   constexpr int RB = ROWS < 16 ? 1 : ROWS / 16;  // 16-row MFMA blocks (an 8-row tile leaves 8 rows idle)
   constexpr int COLS = NB * 16;
   constexpr int NT = KS * 64;
-  constexpr int U = GV_U;
   __shared__ float red[KS][RB * 16][COLS + 1];
   __shared__ float s_ss[NT];
   __shared__ float s_inv[64];
@@ -52,14 +51,18 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
   const int r16 = lane & 15, kq = (lane >> 4) * 8;
   const bf16x8 z8 = {};
 
+  // W is fragment-tiled: the A fragment of row block r at k (a multiple of 32)
+  // is the 16-byte chunk of this lane in the 1 KB tile (row block, k / 32); an
+  // 8-row workgroup uses rows n0 % 16 .. +7 of its block
   const bf16* wrow[RB];
   bool wok[RB];
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
     const int n = n0 + r * 16 + r16;
     wok[r] = n < a.N && (ROWS >= 16 || r16 < ROWS);
-    wrow[r] = a.W + (int64_t)(wok[r] ? n : 0) * K + kq;
+    wrow[r] = a.W + wt_chunk(wok[r] ? n : 0, (lane >> 4), K);
   }
+  auto woff = [](int k) -> int64_t { return (int64_t)(k >> 5) * 512; };
   const bf16* xrow[NB];
   bool tok[NB];
 #pragma unroll
@@ -100,7 +103,7 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
     for (int u = 0; u < U; ++u) {
       const bool in = k + u * 32 < k1;
 #pragma unroll
-      for (int r = 0; r < RB; ++r) wa[u][r] = (in && wok[r]) ? *(const bf16x8*)(wrow[r] + k + u * 32) : z8;
+      for (int r = 0; r < RB; ++r) wa[u][r] = (in && wok[r]) ? *(const bf16x8*)(wrow[r] + woff(k + u * 32)) : z8;
 #pragma unroll
       for (int c = 0; c < NB; ++c) xb[u][c] = in ? load_b(c, k + u * 32) : z8;
     }
@@ -177,12 +180,13 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
       a.ss_out[(int64_t)blockIdx.x * M + tid] = s;
     }
   } else if constexpr (EPI == GV_SILU) {
-    // rows 0..15 gate, 16..31 the matching up rows (RB == 2)
-    for (int it = tid; it < 16 * COLS; it += NT) {
-      const int f = it / COLS, col = it % COLS;
+    // each 32-row block: rows 0..15 gate, 16..31 the matching up rows
+    for (int it = tid; it < (ROWS / 2) * COLS; it += NT) {
+      const int fl = it / COLS, col = it % COLS;
       if (col >= M) continue;
-      const float g = total(f, col), u = total(16 + f, col);
-      a.out_t[(int64_t)col * a.ldo + n0 / 2 + f] = (bf16)(silu_g(g) * u);
+      const int blk = fl / 16, f = fl % 16;
+      const float g = total(blk * 32 + f, col), u = total(blk * 32 + 16 + f, col);
+      a.out_t[(int64_t)col * a.ldo + n0 / 2 + fl] = (bf16)(silu_g(g) * u);
     }
   } else if constexpr (EPI == GV_ROPE) {
     // an 8-row group of a head = first halves i = 4g..4g+3 and their partners
@@ -278,11 +282,10 @@ __global__ void __launch_bounds__(256) embed_ss_kernel(const int32_t* __restrict
   __shared__ float red[16];
   const int t = blockIdx.x;
   const int id = min(max(tok[t], 0), V - 1);
-  const bf16* e = emb + (int64_t)id * D;
   float* xr = x + (int64_t)t * D;
   float ss = 0.f;
   for (int i = threadIdx.x * 8; i < D; i += blockDim.x * 8) {
-    const bf16x8 v = *(const bf16x8*)(e + i);
+    const bf16x8 v = *(const bf16x8*)(emb + wt_chunk(id, i >> 3, D));  // fragment-tiled table
     f32x4 lo, hi;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -304,70 +307,70 @@ __global__ void __launch_bounds__(256) embed_ss_kernel(const int32_t* __restrict
 
 // ---------------------------------------------------------------- launchers
 
-// more token columns -> fewer wavefronts (registers and LDS of the reduction)
-constexpr int ks_for(int ks, int nb) { return nb == 1 ? ks : (nb == 2 ? (ks < 8 ? ks : 8) : 4); }
-
 // Workgroup shape per epilogue and token count: ROWS output features, KS
-// wavefronts splitting K.  Wide projections take 32..64 rows with 4
-// wavefronts; narrow ones 8 or 16 rows with up to 16 wavefronts, so that the
-// grid still spreads over all CUs (one CU streams only ~25 GB/s).
-struct GvShape {
-  int rows, ks;
-};
-
+// wavefronts splitting K, U k-steps of 32 per pipeline stage.  Chosen by
+// timing every candidate on weights streamed from HBM (not from the 256 MB
+// last-level cache): narrow projections need enough row blocks to occupy all
+// 256 CUs (one CU streams only ~25 GB/s); more token columns favour more rows
+// per workgroup (each token fragment is reused across them) and a shallower
+// pipeline (register pressure).
 GvShape gemv_shape(int N, int K, int M, int epi) {
   const int nb = (M + 15) / 16;
-  if (epi == GV_SILU) return {32, 4};
-  if (epi == GV_HEAD) return {nb <= 2 ? 64 : 32, 4};
-  const int rows = N / 16 >= 512 ? 16 : 8;
-  int ks = 16;
-  while (ks > 4 && K / ks < 256) ks /= 2;
-  return {rows, ks_for(ks, nb)};
+  if (nb == 1) {
+    if (epi == GV_SILU) return {32, 4, 4};
+    if (epi == GV_HEAD) return {K <= 2048 ? 32 : 64, 8, 2};
+    if (N / 16 < 192) return {8, 16, 2};
+    return K >= 8192 ? GvShape{16, 8, 4} : GvShape{16, 16, 2};
+  }
+  if (nb == 2) {
+    if (epi == GV_SILU || epi == GV_HEAD) return {64, 2, 2};
+    return epi == GV_ROPE ? GvShape{16, 4, 2} : GvShape{32, 8, 2};
+  }
+  if (epi == GV_SILU) return {64, 4, 2};
+  if (epi == GV_HEAD) return {32, 4, 2};
+  return epi == GV_ROPE ? GvShape{16, 4, 2} : GvShape{16, 4, 4};
 }
 
 int gemv_rows(int N, int K, int M, int epi) { return gemv_shape(N, K, M, epi).rows; }
 
-template <int ROWS, int KS, bool NORM, int EPI>
-static void gv_nb(const GemvArgs& a, hipStream_t s) {
-  const dim3 grid((a.N + ROWS - 1) / ROWS);
-  switch ((a.M + 15) / 16) {
-    case 1: klaunch(gemv_fused_kernel<ROWS, ks_for(KS, 1), 1, NORM, EPI>, grid, dim3(ks_for(KS, 1) * 64), 0, s, a); break;
-    case 2: klaunch(gemv_fused_kernel<ROWS, ks_for(KS, 2), 2, NORM, EPI>, grid, dim3(ks_for(KS, 2) * 64), 0, s, a); break;
-    case 3: klaunch(gemv_fused_kernel<ROWS, ks_for(KS, 3), 3, NORM, EPI>, grid, dim3(ks_for(KS, 3) * 64), 0, s, a); break;
-    default: klaunch(gemv_fused_kernel<ROWS, ks_for(KS, 4), 4, NORM, EPI>, grid, dim3(ks_for(KS, 4) * 64), 0, s, a); break;
+template <int ROWS, int KS, int U, int NB, bool NORM, int EPI>
+static bool gv(const GemvArgs& a, hipStream_t s) {
+  klaunch(gemv_fused_kernel<ROWS, KS, NB, NORM, EPI, U>, dim3((a.N + ROWS - 1) / ROWS), dim3(KS * 64), 0, s, a);
+  return true;
+}
+
+// every shape gemv_shape can return, per (epilogue, normalization, token blocks)
+template <int EPI, bool NORM>
+static bool gv_dispatch(const GemvArgs& a, const GvShape& sh, int nb, hipStream_t s) {
+#define AXON_GV(R, KS_, U_, NB_) \
+  if (sh.rows == R && sh.ks == KS_ && sh.u == U_ && nb == NB_) return gv<R, KS_, U_, NB_, NORM, EPI>(a, s);
+  if constexpr (EPI == GV_SILU) {
+    AXON_GV(32, 4, 4, 1) AXON_GV(64, 2, 2, 2) AXON_GV(64, 4, 2, 3) AXON_GV(64, 4, 2, 4)
+  } else if constexpr (EPI == GV_HEAD) {
+    AXON_GV(32, 8, 2, 1) AXON_GV(64, 8, 2, 1) AXON_GV(64, 2, 2, 2) AXON_GV(32, 4, 2, 3) AXON_GV(32, 4, 2, 4)
+  } else if constexpr (EPI == GV_ROPE) {
+    AXON_GV(8, 16, 2, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 2, 1) AXON_GV(16, 4, 2, 2) AXON_GV(16, 4, 2, 3)
+    AXON_GV(16, 4, 2, 4)
+  } else {
+    AXON_GV(8, 16, 2, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 2, 1) AXON_GV(32, 8, 2, 2) AXON_GV(16, 4, 4, 3)
+    AXON_GV(16, 4, 4, 4)
   }
+#undef AXON_GV
+  return false;
 }
 
-template <int ROWS, bool NORM, int EPI>
-static void gv_narrow(const GemvArgs& a, int ks, hipStream_t s) {
-  if (ks >= 16) gv_nb<ROWS, 16, NORM, EPI>(a, s);
-  else if (ks >= 8) gv_nb<ROWS, 8, NORM, EPI>(a, s);
-  else gv_nb<ROWS, 4, NORM, EPI>(a, s);
-}
-
-void launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s) {
-  if (a.M <= 0 || a.N <= 0) return;
+bool launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return true;
+  if (a.M > 64) return false;
   const GvShape sh = gemv_shape(a.N, a.K, a.M, epi);
+  const int nb = (a.M + 15) / 16;
   const bool norm = a.ss_in != nullptr;
   switch (epi) {
-    case GV_RESID:
-      if (sh.rows == 8) gv_narrow<8, false, GV_RESID>(a, sh.ks, s);
-      else gv_narrow<16, false, GV_RESID>(a, sh.ks, s);
-      break;
-    case GV_ROPE:
-      if (sh.rows == 8) gv_narrow<8, true, GV_ROPE>(a, sh.ks, s);
-      else gv_narrow<16, true, GV_ROPE>(a, sh.ks, s);
-      break;
-    case GV_SILU: gv_nb<32, 4, true, GV_SILU>(a, s); break;
-    default:
-      if (sh.rows == 64) {
-        if (norm) gv_nb<64, 4, true, GV_HEAD>(a, s);
-        else gv_nb<64, 4, false, GV_HEAD>(a, s);
-      } else {
-        if (norm) gv_nb<32, 4, true, GV_HEAD>(a, s);
-        else gv_nb<32, 4, false, GV_HEAD>(a, s);
-      }
-      break;
+    case GV_SILU: return norm && gv_dispatch<GV_SILU, true>(a, sh, nb, s);
+    case GV_ROPE: return norm && gv_dispatch<GV_ROPE, true>(a, sh, nb, s);
+    case GV_RESID: return !norm && gv_dispatch<GV_RESID, false>(a, sh, nb, s);
+    case GV_HEAD: return norm ? gv_dispatch<GV_HEAD, true>(a, sh, nb, s) : gv_dispatch<GV_HEAD, false>(a, sh, nb, s);
+    default: return false;
   }
 }
 

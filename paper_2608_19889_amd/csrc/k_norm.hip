@@ -17,6 +17,11 @@ AXON_DEV void store4(bf16* p, f32x4 v) {
   *(bf16x4*)p = bf16x4{(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
 }
 
+// element i of embedding row id: bf16 tables are fragment-tiled (they double
+// as the tied output head), float tables are row-major
+AXON_DEV const float* emb_at(const float* e, int id, int i, int D) { return e + (int64_t)id * D + i; }
+AXON_DEV const bf16* emb_at(const bf16* e, int id, int i, int D) { return e + wt_chunk(id, i >> 3, D) + (i & 7); }
+
 // x[r,:] = E[tok[r],:] (as float); h[r,:] = x * rsqrt(mean(x^2) + eps) * g
 template <typename T>
 __global__ void __launch_bounds__(256) embed_rmsnorm_kernel(const int32_t* __restrict__ tok,
@@ -27,11 +32,10 @@ __global__ void __launch_bounds__(256) embed_rmsnorm_kernel(const int32_t* __res
   __shared__ float red[16];
   const int r = blockIdx.x;
   const int id = min(max(tok[r], 0), V - 1);  // ids outside [0, V) are clamped, never dereferenced
-  const T* e = emb + (int64_t)id * D;
   float* xr = x + (int64_t)r * D;
   float ss = 0.f;
   for (int i = threadIdx.x * 4; i < D; i += blockDim.x * 4) {
-    f32x4 v = load4(e + i);
+    f32x4 v = load4(emb_at(emb, id, i, D));
     store4(xr + i, v);
     ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
   }
@@ -39,7 +43,7 @@ __global__ void __launch_bounds__(256) embed_rmsnorm_kernel(const int32_t* __res
   const float inv = rsqrtf(ss / (float)D + eps);
   T* hr = h + (int64_t)r * D;
   for (int i = threadIdx.x * 4; i < D; i += blockDim.x * 4) {
-    f32x4 v = load4(e + i), gv = load4(g + i);
+    f32x4 v = load4(emb_at(emb, id, i, D)), gv = load4(g + i);
     store4(hr + i, f32x4{v[0] * inv * gv[0], v[1] * inv * gv[1], v[2] * inv * gv[2], v[3] * inv * gv[3]});
   }
 }

@@ -44,7 +44,11 @@ struct EpiArgs {
   int64_t part_stride;
 };
 
-// ---- row kernels (k_norm.hip)
+// ---- weight layout (k_layout.hip): fragment-tiled copy of row-major bf16
+// W [N][K] (K % 32 == 0) into dst of round_up(N, 16) * K elements
+void launch_tile_weight(const bf16* src, bf16* dst, int64_t N, int K, hipStream_t s);
+
+// ---- row kernels (k_norm.hip); a bf16 embedding table is fragment-tiled
 template <typename T>
 void launch_embed_rmsnorm(const int32_t* tok, const T* emb, const T* g, float* x, T* h, int rows, int D, int V,
                           float eps, hipStream_t s);
@@ -98,8 +102,15 @@ struct GemvArgs {
   const int32_t* len;
   int H;
 };
+constexpr int GEMV_MAX_M = 64;  // token columns one fused projection handles
+struct GvShape {
+  int rows, ks, u;  // output rows per workgroup, wavefronts splitting K, k-steps of 32 per stage
+};
+GvShape gemv_shape(int N, int K, int M, int epi);
 int gemv_rows(int N, int K, int M, int epi);  // output rows per workgroup (ss partial count = N / rows)
-void launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s);
+// false (nothing launched) when M > GEMV_MAX_M or the normalization does not
+// match the epilogue (GV_SILU and GV_ROPE need ss_in, GV_RESID must not have it)
+bool launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s);
 void launch_argmax_final(const float* val, const int32_t* idx, int nparts, int M, int32_t* next, int32_t* len,
                          hipStream_t s);
 void launch_embed_ss(const int32_t* tok, const bf16* emb, const bf16* g, float* x, bf16* xg, float* ss_out, int M,
