@@ -166,15 +166,17 @@ __global__ void __launch_bounds__(256) attn_prefill_bf16_kernel(const bf16* __re
 // Decode (bf16): one query per slot.  Workgroup = (key split, kv head, slot)
 // with DNW wavefronts; the group's query heads are the columns of
 // v_mfma_f32_16x16x32_bf16 (up to 16 heads per group); each wavefront takes 64
-// keys per iteration and issues the K and V^T loads of both 32-key halves,
-// straight from HBM, before computing either.  The wavefronts' (max, sum, o) are merged in LDS; with one split
-// the normalized output is written directly, otherwise an unnormalized
-// partial per split is merged by the combine kernel.
+// keys per iteration as two 32-key chunks whose K and V^T loads go straight
+// from HBM to registers, one chunk ahead of the one being computed.  The
+// wavefronts' (max, sum, o) are merged in LDS; with one split the normalized
+// output is written directly, otherwise every split stores an unnormalized
+// partial and the last split to finish merges them.
 // ============================================================================
 template <int HD, int DNW>
 __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* __restrict__ q, KVView kv,
                                                                     bf16* __restrict__ o, float* __restrict__ part,
-                                                                    int H, const int32_t* __restrict__ len,
+                                                                    int32_t* __restrict__ arrivals, int H,
+                                                                    const int32_t* __restrict__ len,
                                                                     int split_len) {
   extern __shared__ float dyn[];
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
@@ -277,15 +279,23 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
       acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vv, pb, acc[d], 0, 0, 0);
     }
   };
-  // wavefront w takes 64 keys at s0 + w*64, s0 + (w + DNW)*64, ...; both
-  // halves' loads are issued before either is consumed
-  for (int j0 = s0 + wave * 64; j0 < s1; j0 += DNW * 64) {
-    Frag f0, f1;
-    load(f0, j0);
-    const bool two = j0 + 32 < s1;
-    if (two) load(f1, j0 + 32);
-    step(f0, j0);
-    if (two) step(f1, j0 + 32);
+  // wavefront w takes the 32-key chunks of the 64 keys at s0 + w*64, s0 + (w +
+  // DNW)*64, ...; two chunks are in flight: the next but one is loaded into
+  // a chunk's registers as soon as that chunk has been consumed
+  auto chunk = [&](int i) { return s0 + wave * 64 + (i >> 1) * (DNW * 64) + (i & 1) * 32; };
+  {
+    Frag fa, fb;
+    int i = 0;
+    if (chunk(0) < s1) load(fa, chunk(0));
+    if (chunk(1) < s1) load(fb, chunk(1));
+    while (chunk(i) < s1) {
+      step(fa, chunk(i));
+      if (chunk(i + 2) < s1) load(fa, chunk(i + 2));
+      if (chunk(i + 1) >= s1) break;
+      step(fb, chunk(i + 1));
+      if (chunk(i + 3) < s1) load(fb, chunk(i + 3));
+      i += 2;
+    }
   }
   // per-wave statistics: m uniform over the 4 lane groups of a column; l summed
   l_run += __shfl_xor(l_run, 16, 64);
@@ -325,26 +335,45 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
       }
     }
   }
-}
+  if (nsplit == 1) return;
 
-// merge split partials of one (slot, head): o = sum_c 2^(m_c - M) o_c / sum_c 2^(m_c - M) l_c
-template <typename T, int HD>
-__global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restrict__ part, T* __restrict__ o, int H,
-                                                          const int32_t* __restrict__ len, int nsplit,
-                                                          int split_len) {
-  const int b = blockIdx.y, h = blockIdx.x, d = threadIdx.x;
-  const int ctx = len[b] + 1;
-  const int nch = min(nsplit, (ctx + split_len - 1) / split_len);
-  const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
-  float M = -INFINITY;
-  for (int c = 0; c < nch; ++c) M = fmaxf(M, pp[c * (HD + 2) + HD]);
-  float L = 0.f, O = 0.f;
-  for (int c = 0; c < nch; ++c) {
-    const float f = exp2f(pp[c * (HD + 2) + HD] - M);
-    L += f * pp[c * (HD + 2) + HD + 1];
-    O += f * pp[c * (HD + 2) + d];
+  // The last of the nact active splits of this (slot, kv head) to arrive
+  // merges all partials, in split order (the result does not depend on which
+  // workgroup arrives last), and resets the arrival count for the next launch.
+  // One thread per workgroup publishes: the barrier orders every wavefront's
+  // partial stores before its device-scope release fence (a device-scope fence
+  // writes back the whole L2 of the XCD, so it is issued once, not per thread),
+  // and the merging workgroup's acquire fence precedes the barrier its other
+  // threads pass.
+  __shared__ int s_last;
+  const int nact = min(nsplit, (ctx + split_len - 1) / split_len);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    int32_t* cnt = arrivals + (int64_t)b * kv.kv_heads + kvh;
+    const int last = atomicAdd(cnt, 1) == nact - 1;
+    if (last) {
+      atomicExch(cnt, 0);
+      __threadfence();
+    }
+    s_last = last;
   }
-  o[((int64_t)b * H + h) * HD + d] = from_f32<T>(O / L);
+  __syncthreads();
+  if (!s_last) return;
+  for (int idx = threadIdx.x; idx < group * HD; idx += DNW * 64) {
+    const int c = idx / HD, d = idx % HD;
+    const int h = kvh * group + c;
+    const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
+    float M = -INFINITY;
+    for (int sp = 0; sp < nact; ++sp) M = fmaxf(M, pp[sp * (HD + 2) + HD]);
+    float L = 0.f, O = 0.f;
+    for (int sp = 0; sp < nact; ++sp) {
+      const float f = exp2f(pp[sp * (HD + 2) + HD] - M);
+      L += f * pp[sp * (HD + 2) + HD + 1];
+      O += f * pp[sp * (HD + 2) + d];
+    }
+    o[((int64_t)b * H + h) * HD + d] = (bf16)(O / L);
+  }
 }
 
 // ============================================================================
@@ -409,31 +438,32 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
   }
 }
 
-// wavefronts per decode workgroup: 16 for head_dim 64 when their partial
-// outputs fit in 64 KB of LDS (head_dim 128 needs > 128 registers per lane)
-static int decode_waves(int group, int hd) { return (hd == 64 && group * hd <= 1024) ? 16 : 8; }
+// Decode workgroups have DECODE_WAVES wavefronts of 64 keys per iteration.
+// Few (slot, kv head) pairs leave most CUs idle, so their keys are split
+// towards ~192 workgroups, keeping >= 768 keys per split; every split costs
+// a device-scope release fence (an L2 write-back of its XCD), so pairs >= 128
+// are not split.
+constexpr int DECODE_WAVES = 8;
 
 int plan_decode_splits(int B, int kv_heads, int max_ctx) {
-  // one workgroup per (slot, kv head) when that already fills the chip,
-  // otherwise split the keys (each split keeps >= 2 iterations per wavefront)
-  const int pairs = B * kv_heads;
-  const int want = pairs >= 64 ? 1 : (256 + pairs - 1) / pairs;
-  const int cap = (max_ctx + 8 * 128 - 1) / (8 * 128);
-  return std::max(1, std::min(want, cap));
+  const int pairs = std::max(1, B * kv_heads);
+  if (pairs >= 128) return 1;
+  const int want = (192 + pairs - 1) / pairs;
+  return std::max(1, std::min(want, max_ctx / 768));
 }
 
 template <int HD, int NW>
-static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int B, int H, const int32_t* len,
-                          int nsplit, int split_len, hipStream_t s) {
+static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int32_t* arrivals, int B, int H,
+                          const int32_t* len, int nsplit, int split_len, hipStream_t s) {
   const int group = H / kv.kv_heads;
   const size_t lds = (size_t)(2 * NW * 16 + NW * group * HD) * sizeof(float);
-  attn_decode_bf16_kernel<HD, NW><<<dim3(nsplit, kv.kv_heads, B), NW * 64, lds, s>>>(q, kv, o, part, H, len,
-                                                                                      split_len);
+  attn_decode_bf16_kernel<HD, NW><<<dim3(nsplit, kv.kv_heads, B), NW * 64, lds, s>>>(q, kv, o, part, arrivals, H,
+                                                                                      len, split_len);
 }
 
 template <typename T>
-void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len, int max_ctx,
-                        hipStream_t s) {
+void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* arrivals, int B, int H,
+                        const int32_t* len, int max_ctx, hipStream_t s) {
   if (B <= 0) return;
   if constexpr (sizeof(T) == 4) {
     dim3 grid((B + 63) / 64, H);
@@ -441,17 +471,9 @@ void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, 
     else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H);
   } else {
     const int nsplit = plan_decode_splits(B, kv.kv_heads, max_ctx);
-    const int split_len = ((max_ctx + nsplit - 1) / nsplit + 31) / 32 * 32;
-    const int nw = decode_waves(H / kv.kv_heads, kv.hd);
-    dim3 cgrid(H, B);
-    if (kv.hd == 64) {
-      if (nw == 16) decode_launch<64, 16>(q, kv, o, part, B, H, len, nsplit, split_len, s);
-      else decode_launch<64, 8>(q, kv, o, part, B, H, len, nsplit, split_len, s);
-      if (nsplit > 1) attn_combine_kernel<T, 64><<<cgrid, 64, 0, s>>>(part, o, H, len, nsplit, split_len);
-    } else {
-      decode_launch<128, 8>(q, kv, o, part, B, H, len, nsplit, split_len, s);
-      if (nsplit > 1) attn_combine_kernel<T, 128><<<cgrid, 128, 0, s>>>(part, o, H, len, nsplit, split_len);
-    }
+    const int split_len = ((max_ctx + nsplit - 1) / nsplit + 63) / 64 * 64;
+    if (kv.hd == 64) decode_launch<64, DECODE_WAVES>(q, kv, o, part, arrivals, B, H, len, nsplit, split_len, s);
+    else decode_launch<128, DECODE_WAVES>(q, kv, o, part, arrivals, B, H, len, nsplit, split_len, s);
   }
 }
 
@@ -459,9 +481,9 @@ template void launch_attn_prefill<float>(const float*, KVView, float*, int, int,
                                          hipStream_t);
 template void launch_attn_prefill<bf16>(const bf16*, KVView, bf16*, int, int, const int32_t*, const int32_t*, int,
                                         hipStream_t);
-template void launch_attn_decode<float>(const float*, KVView, float*, float*, int, int, const int32_t*, int,
-                                        hipStream_t);
-template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int, int, const int32_t*, int,
+template void launch_attn_decode<float>(const float*, KVView, float*, float*, int32_t*, int, int, const int32_t*,
+                                        int, hipStream_t);
+template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int32_t*, int, int, const int32_t*, int,
                                        hipStream_t);
 
 }  // namespace axon

@@ -43,51 +43,46 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
   __shared__ float s_ss[NT];
   __shared__ float s_inv[64];
   __shared__ float s_aux[RB * 16][COLS + 1];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = blockIdx.x * ROWS;
   const int K = a.K, M = a.M;
   const int kc = ((K + KS - 1) / KS + 32 * U - 1) / (32 * U) * (32 * U);
   const int k0 = min(K, wave * kc), k1 = min(K, k0 + kc);
-  const int r16 = lane & 15, kq = (lane >> 4) * 8;
-  const bf16x8 z8 = {};
+  const int r16 = lane & 15;
 
-  // W is fragment-tiled: the A fragment of row block r at k (a multiple of 32)
-  // is the 16-byte chunk of this lane in the 1 KB tile (row block, k / 32); an
-  // 8-row workgroup uses rows n0 % 16 .. +7 of its block
+  // Every load below is unconditional (a load under a lane condition makes
+  // the compiler wait for all outstanding loads where the branches join).
+  // W is fragment-tiled: the A fragment of row block r at k (a multiple of
+  // 32) is this lane's 16-byte chunk of the 1 KB tile (row block, k / 32).
+  // Rows past N read row N-1 and token columns past M read token M-1: those
+  // MFMA rows / columns only reach outputs that are never stored.  In an
+  // 8-row workgroup lanes 8..15 repeat rows 0..7 (same addresses, no extra
+  // traffic).
   const bf16* wrow[RB];
-  bool wok[RB];
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
-    const int n = n0 + r * 16 + r16;
-    wok[r] = n < a.N && (ROWS >= 16 || r16 < ROWS);
-    wrow[r] = a.W + wt_chunk(wok[r] ? n : 0, (lane >> 4), K);
+    const int n = n0 + r * 16 + (ROWS >= 16 ? r16 : (r16 & 7));
+    wrow[r] = a.W + wt_chunk(min(n, a.N - 1), lane >> 4, K);
   }
   auto woff = [](int k) -> int64_t { return (int64_t)(k >> 5) * 512; };
   const bf16* xrow[NB];
-  bool tok[NB];
 #pragma unroll
-  for (int c = 0; c < NB; ++c) {
-    const int t = c * 16 + r16;
-    tok[c] = t < M;
-    xrow[c] = a.X + (int64_t)(tok[c] ? t : 0) * K + kq;
-  }
+  for (int c = 0; c < NB; ++c) xrow[c] = a.X + (int64_t)min(c * 16 + r16, M - 1) * K + (lane >> 4) * 8;
 
   // sums of squares of the normalized rows: the first SSR partials of this
-  // thread are loaded into registers now and consumed after the stream
+  // thread are loaded into registers now (index clamped, excluded in the sum)
+  // and consumed after the stream
   constexpr int SSR = 8;
   float ss_reg[SSR];
   const int ss_slices = NT / M, ss_t = tid % M, ss_sl = tid / M;
   if constexpr (NORM) {
 #pragma unroll
     for (int i = 0; i < SSR; ++i) {
-      const int j = ss_sl + i * ss_slices;
-      ss_reg[i] = (ss_sl < ss_slices && j < a.ss_n) ? a.ss_in[(int64_t)j * M + ss_t] : 0.f;
+      const int j = min(ss_sl + i * ss_slices, a.ss_n - 1);
+      ss_reg[i] = a.ss_in[(int64_t)j * M + ss_t];
     }
   }
-
-  // B operand: token rows of X (for a normalized operand X = bf16(x * g) was
-  // written by the producer of x; 1/rms is applied to the accumulator)
-  auto load_b = [&](int c, int k) -> bf16x8 { return tok[c] ? *(const bf16x8*)(xrow[c] + k) : z8; };
 
   f32x4 acc[RB][NB];
 #pragma unroll
@@ -95,37 +90,55 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
 #pragma unroll
     for (int c = 0; c < NB; ++c) acc[r][c] = f32x4{};
 
-  // software-pipelined stream over [k0, k1): stage s+1 is loaded while stage s
-  // feeds the MFMAs; k1 - k0 is a multiple of 32 (K % 64 == 0)
+  // software-pipelined stream over the full stages of [k0, k1): stage s+1 is
+  // loaded while stage s feeds the MFMAs; the rest (k1 - k0 is a multiple of
+  // 32) in single k-steps
   bf16x8 wa[U][RB], xb[U][NB];
   auto load_stage = [&](int k) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const bool in = k + u * 32 < k1;
 #pragma unroll
-      for (int r = 0; r < RB; ++r) wa[u][r] = (in && wok[r]) ? *(const bf16x8*)(wrow[r] + woff(k + u * 32)) : z8;
+      for (int r = 0; r < RB; ++r) wa[u][r] = *(const bf16x8*)(wrow[r] + woff(k + u * 32));
 #pragma unroll
-      for (int c = 0; c < NB; ++c) xb[u][c] = in ? load_b(c, k + u * 32) : z8;
+      for (int c = 0; c < NB; ++c) xb[u][c] = *(const bf16x8*)(xrow[c] + k + u * 32);
     }
   };
-  if (k0 < k1) load_stage(k0);
-  for (int k = k0; k < k1; k += 32 * U) {
-    bf16x8 ca[U][RB], cb[U][NB];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-#pragma unroll
-      for (int r = 0; r < RB; ++r) ca[u][r] = wa[u][r];
-#pragma unroll
-      for (int c = 0; c < NB; ++c) cb[u][c] = xb[u][c];
-    }
-    if (k + 32 * U < k1) load_stage(k + 32 * U);
+  auto mfma_stage = [&](const bf16x8 (&wv)[U][RB], const bf16x8 (&xv)[U][NB]) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int r = 0; r < RB; ++r)
 #pragma unroll
         for (int c = 0; c < NB; ++c)
-          acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ca[u][r], cb[u][c], acc[r][c], 0, 0, 0);
+          acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wv[u][r], xv[u][c], acc[r][c], 0, 0, 0);
+  };
+  const int nst = (k1 - k0) / (32 * U);
+  if (nst > 0) {
+    load_stage(k0);
+    for (int st = 1; st < nst; ++st) {
+      bf16x8 ca[U][RB], cb[U][NB];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+#pragma unroll
+        for (int r = 0; r < RB; ++r) ca[u][r] = wa[u][r];
+#pragma unroll
+        for (int c = 0; c < NB; ++c) cb[u][c] = xb[u][c];
+      }
+      load_stage(k0 + st * 32 * U);
+      mfma_stage(ca, cb);
+    }
+    mfma_stage(wa, xb);
+  }
+  for (int k = k0 + nst * 32 * U; k < k1; k += 32) {
+    bf16x8 w1[RB], x1[NB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) w1[r] = *(const bf16x8*)(wrow[r] + woff(k));
+#pragma unroll
+    for (int c = 0; c < NB; ++c) x1[c] = *(const bf16x8*)(xrow[c] + k);
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+#pragma unroll
+      for (int c = 0; c < NB; ++c) acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1[r], x1[c], acc[r][c], 0, 0, 0);
   }
 
   // ---- cross-wavefront reduction: acc[r][c][i] = C[n0 + r*16 + (lane/16)*4 + i][c*16 + lane%16]
@@ -138,7 +151,8 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
   if constexpr (NORM) {
     float ss_part = 0.f;
 #pragma unroll
-    for (int i = 0; i < SSR; ++i) ss_part += ss_reg[i];
+    for (int i = 0; i < SSR; ++i)
+      if (ss_sl < ss_slices && ss_sl + i * ss_slices < a.ss_n) ss_part += ss_reg[i];
     if (ss_sl < ss_slices)
       for (int j = ss_sl + SSR * ss_slices; j < a.ss_n; j += ss_slices) ss_part += a.ss_in[(int64_t)j * M + ss_t];
     s_ss[tid] = ss_part;
