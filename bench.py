@@ -224,7 +224,7 @@ def roofline_pass(m, generate, shape, esz, lens):
     sq = sum(n * (n + 1) / 2 for n in lens)
     cls_name = {ax.T_GEMV: "decode projection GEMM (weight streaming)",
                 ax.T_GEMM: "prefill projection GEMM (MFMA)",
-                ax.T_ATTN_DECODE: "decode attention (split-K + combine)",
+                ax.T_ATTN_DECODE: "decode attention (+ split merge)",
                 ax.T_ATTN_PREFILL: "prefill flash attention"}
     agg = {}
     for c, (d0, d1, d2), ms in recs:

@@ -159,7 +159,6 @@ struct axon_model {
   float* gu_f32 = nullptr;
   float* logits_int = nullptr;
   float* attn_part = nullptr;
-  int32_t* attn_arrivals = nullptr;  // per (slot, kv head) split arrival counts, zero between launches
   float* ss = nullptr;       // per-workgroup sums of squares of x rows
   void* xg = nullptr;        // bf16(x * g) for the next normalized projection
   int ss_n = 0;              // number of partials currently in ss
@@ -362,8 +361,7 @@ void enqueue_decode_many(axon_model* m, int B, const int32_t* d_tokens, float* d
     proj(w.wqkv, h, nq, D, EPI_F32, m->qkv, nullptr, nq);
     launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, B, 0, nullptr,
                       m->d_len, H, s);
-    launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, m->attn_arrivals, B, H, m->d_len,
-                          m->cfg.max_seq, s);
+    launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
     proj(w.wo, m->o, D, H * hd, EPI_RESID, m->x, nullptr, D);
     launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, B, D, eps, nullptr, s);
     if constexpr (sizeof(T) == 2) {
@@ -413,8 +411,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
     int ctx_sum = 0;
     for (int b = 0; b < B; ++b) ctx_sum += m->h_len[b] + 1;
     m->timed(2, H, B, ctx_sum, s, [&] {
-      launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, m->attn_arrivals, B, H, m->d_len,
-                               m->cfg.max_seq, s);
+      launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
     });
     GemvArgs oa{};
     oa.W = (const bf16*)w.wo; oa.N = D; oa.K = H * hd; oa.M = B; oa.X = (const bf16*)m->o;
@@ -698,8 +695,6 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     for (int b = 1; b <= c.max_batch; ++b)
       bsplits = std::max<int64_t>(bsplits, (int64_t)b * plan_decode_splits(b, c.n_kv_heads, c.max_seq));
     TRY(dev_alloc(m, (void**)&m->attn_part, bsplits * H * (hd + 2) * 4));
-    TRY(dev_alloc(m, (void**)&m->attn_arrivals, (size_t)c.max_batch * KV * 4));
-    HTRY(hipMemsetAsync(m->attn_arrivals, 0, (size_t)c.max_batch * KV * 4, s));
     TRY(dev_alloc(m, (void**)&m->ss, (int64_t)std::max<int64_t>(D / 8, 1) * c.max_batch * 4));
     TRY(dev_alloc(m, &m->xg, (int64_t)c.max_batch * D * 2));
     const int64_t nam = (V + 15) / 16;

@@ -170,13 +170,23 @@ __global__ void __launch_bounds__(256) attn_prefill_bf16_kernel(const bf16* __re
 // from HBM to registers, one chunk ahead of the one being computed.  The
 // wavefronts' (max, sum, o) are merged in LDS; with one split the normalized
 // output is written directly, otherwise every split stores an unnormalized
-// partial and the last split to finish merges them.
+// partial and the combine kernel merges them.
 // ============================================================================
+// Page of position ``pos`` of ``slot`` for a wave-uniform (slot, pos): read
+// through the constant address space, so that it is a scalar load whose
+// wait does not hold up the wavefront's outstanding vector loads.  The page
+// table is not written while a kernel runs.
+AXON_DEV int64_t kv_page_uniform(const KVView& c, int slot, int pos) {
+  if (!c.bt) return slot;
+  typedef const __attribute__((address_space(4))) int32_t* cptr;
+  const cptr bt = (cptr)(uintptr_t)c.bt;
+  return bt[__builtin_amdgcn_readfirstlane(slot * c.bt_stride + pos / c.ps)];
+}
+
 template <int HD, int DNW>
 __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* __restrict__ q, KVView kv,
                                                                     bf16* __restrict__ o, float* __restrict__ part,
-                                                                    int32_t* __restrict__ arrivals, int H,
-                                                                    const int32_t* __restrict__ len,
+                                                                    int H, const int32_t* __restrict__ len,
                                                                     int split_len) {
   extern __shared__ float dyn[];
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
@@ -186,7 +196,7 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
   const int s1 = min(ctx, s0 + split_len);
   if (s0 >= ctx) return;
   const int group = H / kv.kv_heads;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, gq = lane >> 4;
   const float sc = LOG2E / sqrtf((float)HD);
   float* sm = dyn;                 // [DNW][16]
@@ -213,25 +223,35 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
     bf16x4 vlo[HD / 16], vhi[HD / 16];
   };
   // issue the K and V^T loads of the 32 keys starting at j0
+  // A 16-key half lies in one page (page sizes are multiples of 16, chunks
+  // start at multiples of 32): its page is looked up once, with a scalar load
+  // (a per-lane load of the page table, on which the K/V addresses depend,
+  // would wait for every load in flight).  Keys past the context may have no
+  // page: never dereferenced.
+  const int64_t vrow = kv.ps;  // V^T row stride (positions per page)
   auto load = [&](Frag& f, int j0) {
+    int64_t kbase[2], vbase[2];
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
-      const int key = j0 + blk * 16 + col;
-      const bool ok = key < s1;  // keys past the context may have no page: never dereferenced
-      const bf16* kp = kb + (ok ? k_off(kv, b, kvh, key) : 0) + gq * 8;
+      const int hs = min(j0 + blk * 16, (s1 - 1) & ~15);  // a valid 16-key group
+      const int64_t pg = kv_page_uniform(kv, b, hs);
+      const int off = (j0 + blk * 16) - hs + hs % kv.ps;  // in-page position of key j0 + blk*16
+      kbase[blk] = ((pg * kv.kv_heads + kvh) * kv.ps + off) * HD;
+      vbase[blk] = (pg * kv.kv_heads + kvh) * (int64_t)HD * kv.ps + off;
+    }
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+      const bool ok = j0 + blk * 16 + col < s1;
+      const bf16* kp = kb + kbase[blk] + col * HD + gq * 8;
 #pragma unroll
       for (int k = 0; k < HD / 32; ++k) f.k[blk][k] = ok ? *(const bf16x8*)(kp + k * 32) : z8;
     }
-    const int ja = j0 + gq * 4, jb = j0 + 16 + gq * 4;
-    const bool oka = ja < s1, okb = jb < s1;
-    const int64_t va = oka ? vt_off(kv, b, kvh, 0, ja) : 0;
-    const int64_t vbo = okb ? vt_off(kv, b, kvh, 0, jb) : 0;
-    const int64_t vrow = kv.ps;  // V^T row stride (positions per page)
+    const bool oka = j0 + gq * 4 < s1, okb = j0 + 16 + gq * 4 < s1;
 #pragma unroll
     for (int d = 0; d < HD / 16; ++d) {
       const int dd = d * 16 + col;
-      f.vlo[d] = oka ? *(const bf16x4*)(vb + va + dd * vrow) : z4;
-      f.vhi[d] = okb ? *(const bf16x4*)(vb + vbo + dd * vrow) : z4;
+      f.vlo[d] = oka ? *(const bf16x4*)(vb + vbase[0] + gq * 4 + dd * vrow) : z4;
+      f.vhi[d] = okb ? *(const bf16x4*)(vb + vbase[1] + gq * 4 + dd * vrow) : z4;
     }
   };
   // scores, online softmax update and P V for the 32 keys starting at j0
@@ -335,45 +355,27 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
       }
     }
   }
-  if (nsplit == 1) return;
+}
 
-  // The last of the nact active splits of this (slot, kv head) to arrive
-  // merges all partials, in split order (the result does not depend on which
-  // workgroup arrives last), and resets the arrival count for the next launch.
-  // One thread per workgroup publishes: the barrier orders every wavefront's
-  // partial stores before its device-scope release fence (a device-scope fence
-  // writes back the whole L2 of the XCD, so it is issued once, not per thread),
-  // and the merging workgroup's acquire fence precedes the barrier its other
-  // threads pass.
-  __shared__ int s_last;
+// Merge the split partials of one (slot, head), in split order:
+// o = sum_c 2^(m_c - M) o_c / sum_c 2^(m_c - M) l_c.
+template <int HD>
+__global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restrict__ part, bf16* __restrict__ o, int H,
+                                                          const int32_t* __restrict__ len, int nsplit,
+                                                          int split_len) {
+  const int b = blockIdx.y, h = blockIdx.x, d = threadIdx.x;
+  const int ctx = len[b] + 1;
   const int nact = min(nsplit, (ctx + split_len - 1) / split_len);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    int32_t* cnt = arrivals + (int64_t)b * kv.kv_heads + kvh;
-    const int last = atomicAdd(cnt, 1) == nact - 1;
-    if (last) {
-      atomicExch(cnt, 0);
-      __threadfence();
-    }
-    s_last = last;
+  const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
+  float M = -INFINITY;
+  for (int sp = 0; sp < nact; ++sp) M = fmaxf(M, pp[sp * (HD + 2) + HD]);
+  float L = 0.f, O = 0.f;
+  for (int sp = 0; sp < nact; ++sp) {
+    const float f = exp2f(pp[sp * (HD + 2) + HD] - M);
+    L += f * pp[sp * (HD + 2) + HD + 1];
+    O += f * pp[sp * (HD + 2) + d];
   }
-  __syncthreads();
-  if (!s_last) return;
-  for (int idx = threadIdx.x; idx < group * HD; idx += DNW * 64) {
-    const int c = idx / HD, d = idx % HD;
-    const int h = kvh * group + c;
-    const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
-    float M = -INFINITY;
-    for (int sp = 0; sp < nact; ++sp) M = fmaxf(M, pp[sp * (HD + 2) + HD]);
-    float L = 0.f, O = 0.f;
-    for (int sp = 0; sp < nact; ++sp) {
-      const float f = exp2f(pp[sp * (HD + 2) + HD] - M);
-      L += f * pp[sp * (HD + 2) + HD + 1];
-      O += f * pp[sp * (HD + 2) + d];
-    }
-    o[((int64_t)b * H + h) * HD + d] = (bf16)(O / L);
-  }
+  o[((int64_t)b * H + h) * HD + d] = (bf16)(O / L);
 }
 
 // ============================================================================
@@ -440,30 +442,33 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
 
 // Decode workgroups have DECODE_WAVES wavefronts of 64 keys per iteration.
 // Few (slot, kv head) pairs leave most CUs idle, so their keys are split
-// towards ~192 workgroups, keeping >= 768 keys per split; every split costs
-// a device-scope release fence (an L2 write-back of its XCD), so pairs >= 128
-// are not split.
+// towards ~256 workgroups with >= 512 keys per split; many pairs are split
+// only for long contexts (<= 1536 keys per split), which bounds the time of the
+// longest sequences of a ragged batch.  Split partials are merged by a second
+// kernel (merging inside the first would take a device-scope release fence
+// per workgroup, an L2 write-back, which costs more).
 constexpr int DECODE_WAVES = 8;
 
 int plan_decode_splits(int B, int kv_heads, int max_ctx) {
   const int pairs = std::max(1, B * kv_heads);
-  if (pairs >= 128) return 1;
-  const int want = (192 + pairs - 1) / pairs;
-  return std::max(1, std::min(want, max_ctx / 768));
+  if (pairs >= 128) return std::max(1, std::min(16, (max_ctx + 1535) / 1536));  // <= 16 bounds the partials
+  const int want = (256 + pairs - 1) / pairs;
+  return std::max(1, std::min(want, max_ctx / 512));
 }
 
 template <int HD, int NW>
-static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int32_t* arrivals, int B, int H,
-                          const int32_t* len, int nsplit, int split_len, hipStream_t s) {
+static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int B, int H, const int32_t* len,
+                          int nsplit, int split_len, hipStream_t s) {
   const int group = H / kv.kv_heads;
   const size_t lds = (size_t)(2 * NW * 16 + NW * group * HD) * sizeof(float);
-  attn_decode_bf16_kernel<HD, NW><<<dim3(nsplit, kv.kv_heads, B), NW * 64, lds, s>>>(q, kv, o, part, arrivals, H,
-                                                                                      len, split_len);
+  attn_decode_bf16_kernel<HD, NW><<<dim3(nsplit, kv.kv_heads, B), NW * 64, lds, s>>>(q, kv, o, part, H, len,
+                                                                                      split_len);
+  if (nsplit > 1) attn_combine_kernel<HD><<<dim3(H, B), HD, 0, s>>>(part, o, H, len, nsplit, split_len);
 }
 
 template <typename T>
-void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* arrivals, int B, int H,
-                        const int32_t* len, int max_ctx, hipStream_t s) {
+void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len, int max_ctx,
+                        hipStream_t s) {
   if (B <= 0) return;
   if constexpr (sizeof(T) == 4) {
     dim3 grid((B + 63) / 64, H);
@@ -472,8 +477,8 @@ void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* arriv
   } else {
     const int nsplit = plan_decode_splits(B, kv.kv_heads, max_ctx);
     const int split_len = ((max_ctx + nsplit - 1) / nsplit + 63) / 64 * 64;
-    if (kv.hd == 64) decode_launch<64, DECODE_WAVES>(q, kv, o, part, arrivals, B, H, len, nsplit, split_len, s);
-    else decode_launch<128, DECODE_WAVES>(q, kv, o, part, arrivals, B, H, len, nsplit, split_len, s);
+    if (kv.hd == 64) decode_launch<64, DECODE_WAVES>(q, kv, o, part, B, H, len, nsplit, split_len, s);
+    else decode_launch<128, DECODE_WAVES>(q, kv, o, part, B, H, len, nsplit, split_len, s);
   }
 }
 
@@ -481,9 +486,9 @@ template void launch_attn_prefill<float>(const float*, KVView, float*, int, int,
                                          hipStream_t);
 template void launch_attn_prefill<bf16>(const bf16*, KVView, bf16*, int, int, const int32_t*, const int32_t*, int,
                                         hipStream_t);
-template void launch_attn_decode<float>(const float*, KVView, float*, float*, int32_t*, int, int, const int32_t*,
-                                        int, hipStream_t);
-template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int32_t*, int, int, const int32_t*, int,
+template void launch_attn_decode<float>(const float*, KVView, float*, float*, int, int, const int32_t*, int,
+                                        hipStream_t);
+template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int, int, const int32_t*, int,
                                        hipStream_t);
 
 }  // namespace axon

@@ -134,11 +134,10 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
 // Decode attention: one query per slot at position len[b] (after the step's
 // key/value were written), context len[b] + 1; keys split over
 // plan_decode_splits() workgroups per (slot, kv head).  ``part`` holds
-// B * H * splits * (hd + 2) floats; ``arrivals`` B * kv_heads int32 counters
-// that must be zero before the first launch (each launch leaves them zero).
+// B * H * splits * (hd + 2) floats.
 int plan_decode_splits(int B, int kv_heads, int max_ctx);
 template <typename T>
-void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* arrivals, int B, int H,
-                        const int32_t* len, int max_ctx, hipStream_t s);
+void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len,
+                        int max_ctx, hipStream_t s);
 
 }  // namespace axon
