@@ -286,43 +286,52 @@ def measured_traffic(roof, workload):
 def summarize_counters(fetch_csv, write_csv, workload):
     """HBM bytes per decode-projection launch from FETCH_SIZE / WRITE_SIZE
     (KiB per dispatch).  Each counter is scaled by what it reads for the 1 GiB
-    calibration copy (the largest __amd_rocclr_copyBuffer dispatch); per-kernel
-    averages are then weighted by the launch mix of one generate on the
-    workload (per decode step: QKV, O, gate/up and down projections of every
-    layer plus the head; plus the prefill's head)."""
+    calibration copy (the largest __amd_rocclr_copyBuffer dispatch).  Every
+    fused-projection dispatch gets a role from its epilogue template argument
+    and its place in dispatch order (the residual projection after QKV is O,
+    the one after gate/up is down); per-role averages are then weighted by the
+    launch mix of one generate on the workload (per decode step: QKV, O,
+    gate/up and down of every layer plus the head; plus the prefill's head)."""
     import csv
     from synthetic import MODEL_SHAPES, WORKLOADS
     wl = WORKLOADS[workload]
     L, steps = MODEL_SHAPES[wl["model"]]["num_hidden_layers"], wl["steps"]
 
-    def per_kernel(path):
-        rows = list(csv.DictReader(open(path)))
+    def per_role(path):
+        rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
         cal = max(float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"])
         scale = (1 << 30) / (cal * 1024.0)
-        agg = {}
+        agg, names, after = {}, {}, None
         for r in rows:
             name = r["Kernel_Name"]
             if "gemv_fused_kernel" not in name:
                 continue
-            key = name[name.index("gemv_fused_kernel"):name.index(">") + 1]
-            a = agg.setdefault(key, [0, 0.0])
+            targs = name[name.index("gemv_fused_kernel<") + 18:name.index(">")].split(",")
+            norm, epi = targs[3].strip() == "true", int(targs[4])
+            if epi == 3:
+                role = after = "qkv"
+            elif epi == 2:
+                role = after = "gate/up"
+            elif epi == 1:
+                role = "o" if after == "qkv" else "down"
+            else:
+                role = "head (decode)" if norm else "head (prefill)"
+            a = agg.setdefault(role, [0, 0.0])
             a[0] += 1
             a[1] += float(r["Counter_Value"]) * 1024.0 * scale
-        return scale, {k: v[1] / v[0] for k, v in agg.items()}
+            names.setdefault(role, name[name.index("gemv_fused_kernel"):name.index(">") + 1])
+        return scale, {k: v[1] / v[0] for k, v in agg.items()}, names
 
-    fs, fetch = per_kernel(fetch_csv)
-    ws, write = per_kernel(write_csv)
+    fs, fetch, names = per_role(fetch_csv)
+    ws, write, _ = per_role(write_csv)
     per = {k: fetch[k] + write.get(k, 0.0) for k in fetch}
-    # classify: the head kernels have 64 or 32 rows and the GV_HEAD epilogue (last template argument 0)
-    head_dec = [k for k in per if k.endswith(", true, 0>")]
-    head_pre = [k for k in per if k.endswith(", false, 0>")]
-    layer = [k for k in per if not k.endswith(", 0>")]
-    step_bytes = L * sum(per[k] for k in layer) + sum(per[k] for k in head_dec)
+    step_bytes = L * sum(per[k] for k in ("qkv", "o", "gate/up", "down")) + per["head (decode)"]
     launches = steps * (4 * L + 1) + 1
-    total = steps * step_bytes + sum(per[k] for k in head_pre)
+    total = steps * step_bytes + per["head (prefill)"]
     rec = {"workload": workload, "kernel_source_digest": kernel_source_digest(),
            "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
-           "hbm_bytes_per_kernel": {k: round(v) for k, v in sorted(per.items())},
+           "hbm_bytes_per_launch_by_role": {k: round(v) for k, v in per.items()},
+           "kernel_by_role": names,
            "hbm_bytes_per_launch": round(total / launches),
            "launch_mix": f"{steps} decode steps x ({L} layers x 4 projections + head) + prefill head = {launches}",
            "commands": [f"rocprofv3 --pmc {c} --kernel-include-regex 'gemv_fused|copyBuffer|elementwise_kernel' "
