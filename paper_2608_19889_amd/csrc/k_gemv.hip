@@ -73,14 +73,23 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
   // sums of squares of the normalized rows: the first SSR partials of this
   // thread are loaded into registers now (index clamped, excluded in the sum)
   // and consumed after the stream
-  constexpr int SSR = 8;
+  // (tokens x slices threads; no more slices than the partials need, which
+  // keeps the per-token sum over slices short)
+  constexpr int SSR = 16;
   float ss_reg[SSR];
-  const int ss_slices = NT / M, ss_t = tid % M, ss_sl = tid / M;
+  const int ss_slices = NORM ? min(NT / M, max(1, (a.ss_n + SSR - 1) / SSR)) : 1;
+  const int ss_t = tid % M, ss_sl = tid / M;
   if constexpr (NORM) {
+    // only the wavefronts holding slices load (a wave-uniform branch)
+    if (wave * 64 < ss_slices * M) {
 #pragma unroll
-    for (int i = 0; i < SSR; ++i) {
-      const int j = min(ss_sl + i * ss_slices, a.ss_n - 1);
-      ss_reg[i] = a.ss_in[(int64_t)j * M + ss_t];
+      for (int i = 0; i < SSR; ++i) {
+        const int j = min(ss_sl + i * ss_slices, a.ss_n - 1);
+        ss_reg[i] = a.ss_in[(int64_t)j * M + ss_t];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < SSR; ++i) ss_reg[i] = 0.f;
     }
   }
 
@@ -189,9 +198,9 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
     }
     __syncthreads();
     if (tid < M) {
-      float s = 0.f;
-      for (int row = 0; row < ROWS; ++row) s += s_aux[row][tid];
-      a.ss_out[(int64_t)blockIdx.x * M + tid] = s;
+      float sq = 0.f;
+      for (int row = 0; row < ROWS; ++row) sq += s_aux[row][tid];
+      a.ss_out[(int64_t)blockIdx.x * M + tid] = sq;
     }
   } else if constexpr (EPI == GV_SILU) {
     // each 32-row block: rows 0..15 gate, 16..31 the matching up rows
@@ -243,15 +252,25 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
       s_aux[row][col] = v;
     }
     __syncthreads();
-    if (tid < M) {
+    // per token, the largest logit of the tile and its lowest index (a
+    // wavefront per token)
+    for (int t = wave; t < M; t += KS) {
       float best = -INFINITY;
       int bi = 0x7fffffff;
-      for (int row = 0; row < ROWS; ++row) {
-        const float v = s_aux[row][tid];
+      for (int row = lane; row < ROWS; row += 64) {
+        const float v = s_aux[row][t];
         if (v > best) { best = v; bi = n0 + row; }
       }
-      a.am_val[(int64_t)tid * gridDim.x + blockIdx.x] = best;
-      a.am_idx[(int64_t)tid * gridDim.x + blockIdx.x] = bi;
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const float ov = __shfl_xor(best, m, 64);
+        const int oi = __shfl_xor(bi, m, 64);
+        if (ov > best || (ov == best && oi < bi)) { best = ov; bi = oi; }
+      }
+      if (lane == 0) {
+        a.am_val[(int64_t)t * gridDim.x + blockIdx.x] = best;
+        a.am_idx[(int64_t)t * gridDim.x + blockIdx.x] = bi;
+      }
     }
   }
 }
