@@ -19,21 +19,48 @@ namespace axon {
 
 constexpr float LOG2E = 1.4426950408889634f;
 
+// Page of position ``pos`` of ``slot`` for a wave-uniform (slot, pos): read
+// through the constant address space, so that it is a scalar load whose
+// wait does not hold up the wavefront's outstanding vector loads.  The page
+// table is not written while a kernel runs.
+AXON_DEV int64_t kv_page_uniform(const KVView& c, int slot, int pos) {
+  if (!c.bt) return slot;
+  typedef const __attribute__((address_space(4))) int32_t* cptr;
+  const cptr bt = (cptr)(uintptr_t)c.bt;
+  return bt[__builtin_amdgcn_readfirstlane(slot * c.bt_stride + pos / c.ps)];
+}
+
 // ============================================================================
 // Prefill (bf16): a workgroup = 128 queries of one head of one sequence, four
-// wavefronts of 32 queries; key tiles of 64 staged in LDS (K row-major, V
-// transposed), v_mfma_f32_32x32x16_bf16 for both products.
+// wavefronts of 32 queries; key tiles of 64, K [64][hd] and V^T [hd][64]
+// moved straight from global memory into LDS (global_load_lds_dwordx4: lane L
+// writes 16 bytes at offset 16 L) one tile ahead of the tile being computed,
+// in two LDS buffers; v_mfma_f32_32x32x16_bf16 for both products.  The bank
+// swizzle of a tile (16-byte chunk c of row r stored at c ^ swz(r)) is made by
+// choosing which global chunk each lane loads.  Keys past the sequence load
+// its last key (finite; their scores are masked).
 // ============================================================================
 constexpr int PQ = 128, PK = 64;
 
+// physical 16-byte chunk of logical chunk c in row r of an LDS tile whose
+// rows hold CH chunks: the 16 lanes of a read phase (16 consecutive rows,
+// one logical chunk) hit distinct banks
+template <int CH>
+AXON_DEV int pswz(int r, int c) {
+  if constexpr (CH == 16) return c ^ (r & 15);
+  else return c ^ ((r >> 1) & 7);  // 8 chunks: rows r and r+1 share a 256-byte bank line
+}
+
 template <int HD>
-__global__ void __launch_bounds__(256) attn_prefill_bf16_kernel(const bf16* __restrict__ q, KVView kv,
-                                                                bf16* __restrict__ o, int nseq,
-                                                                const int32_t* __restrict__ cu, int H) {
-  constexpr int KST = HD + 8;  // padded K row (elements)
-  constexpr int VST = PK + 8;  // padded V^T row (elements)
-  __shared__ __attribute__((aligned(16))) bf16 ks[PK * KST];
-  __shared__ __attribute__((aligned(16))) bf16 vs[HD * VST];
+__global__ void __launch_bounds__(256, 2) attn_prefill_bf16_kernel(const bf16* __restrict__ q, KVView kv,
+                                                                   bf16* __restrict__ o, int nseq,
+                                                                   const int32_t* __restrict__ cu, int H) {
+  constexpr int KCH = HD / 8;            // 16-byte chunks per K row
+  constexpr int VCH = PK / 8;            // chunks per V^T row (8)
+  constexpr int KT = PK * KCH;           // chunks per K tile
+  constexpr int VT = HD * VCH;           // chunks per V^T tile
+  constexpr int BUF = KT + VT;           // chunks per buffer
+  __shared__ bf16x8 lds[2 * BUF];
 
   // locate (sequence, query tile) of this workgroup
   int seq = 0, tile = blockIdx.x;
@@ -48,19 +75,52 @@ __global__ void __launch_bounds__(256) attn_prefill_bf16_kernel(const bf16* __re
   const int S = cu[seq + 1] - cu[seq];
   const int tok0 = cu[seq];
   const int q0 = tile * PQ;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qw0 = q0 + wave * 32;
   const int myq = qw0 + (lane & 31);
   const int hl = lane >> 5;
 
-  // Q^T fragments (B operand): column = query, k = head-dim
+  // Q^T fragments (B operand): column = query, k = head-dim (queries past S
+  // read the last query; their outputs are not stored)
   bf16x8 qf[HD / 16];
   {
-    const bf16x8 z = {};
-    const bf16* qp = q + ((int64_t)(tok0 + myq) * H + head) * HD + hl * 8;
+    const bf16* qp = q + ((int64_t)(tok0 + min(myq, S - 1)) * H + head) * HD + hl * 8;
 #pragma unroll
-    for (int k = 0; k < HD / 16; ++k) qf[k] = myq < S ? *(const bf16x8*)(qp + k * 16) : z;
+    for (int k = 0; k < HD / 16; ++k) qf[k] = *(const bf16x8*)(qp + k * 16);
   }
+
+  // issue the loads of key tile kt into buffer b: thread chunk slots
+  // p = (i*4 + wave)*64 + lane of the K tile, then of the V^T tile
+  const bf16* kb = (const bf16*)kv.k;
+  const bf16* vb = (const bf16*)kv.v;
+  auto issue = [&](int kt, int b) {
+    const int j0 = kt * PK;
+    int64_t pg[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) pg[g] = kv_page_uniform(kv, seq, min(j0 + g * 16, S - 1) & ~15);
+#pragma unroll
+    for (int i = 0; i < KT / 256; ++i) {
+      const int p = (i * 4 + wave) * 64 + lane;
+      const int r = p / KCH, c = pswz<KCH>(r, p % KCH);  // pswz is its own inverse
+      const int key = min(j0 + r, S - 1);  // in [j0, j0 + 64): j0 < S
+      const int64_t page = pg[(key - j0) >> 4];
+      const bf16* src = kb + ((page * kv.kv_heads + kvh) * kv.ps + key % kv.ps) * HD + c * 8;
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)(lds + b * BUF + (i * 4 + wave) * 64),
+                                       16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < VT / 256; ++i) {
+      const int p = (i * 4 + wave) * 64 + lane;
+      const int d = p / VCH, c = pswz<VCH>(d, p % VCH);
+      const int key = min(j0 + c * 8, (S - 1) & ~7);  // 8 keys of one 16-key group, in [j0, j0 + 64)
+      const int64_t page = pg[(key - j0) >> 4];
+      const bf16* src = vb + ((page * kv.kv_heads + kvh) * HD + d) * (int64_t)kv.ps + key % kv.ps;
+      __builtin_amdgcn_global_load_lds(
+          (const void*)src, (__attribute__((address_space(3))) void*)(lds + b * BUF + KT + (i * 4 + wave) * 64), 16,
+          0, 0);
+    }
+  };
 
   f32x16 acc_o[HD / 32];
 #pragma unroll
@@ -70,37 +130,25 @@ __global__ void __launch_bounds__(256) attn_prefill_bf16_kernel(const bf16* __re
 
   const int kend = min(S, q0 + PQ);  // keys needed by the workgroup
   const int ntiles = (kend + PK - 1) / PK;
+  issue(0, 0);
   for (int kt = 0; kt < ntiles; ++kt) {
-    const int j0 = kt * PK;
-    // ---- stage K [64][HD] and V^T [HD][64]
-    {
-      constexpr int KCH = HD / 8;
-      for (int idx = tid; idx < PK * KCH; idx += 256) {
-        const int r = idx / KCH, c = idx % KCH;
-        const int j = j0 + r;
-        bf16x8 v = {};
-        if (j < S) v = *(const bf16x8*)((const bf16*)kv.k + k_off(kv, seq, kvh, j) + c * 8);
-        *(bf16x8*)(ks + r * KST + c * 8) = v;
-      }
-      for (int idx = tid; idx < HD * (PK / 8); idx += 256) {
-        const int d = idx / (PK / 8), c = idx % (PK / 8);
-        const int j = j0 + c * 8;
-        bf16x8 v = {};
-        if (j < S) v = *(const bf16x8*)((const bf16*)kv.v + vt_off(kv, seq, kvh, d, j));
-        *(bf16x8*)(vs + d * VST + c * 8) = v;
-      }
-    }
-    __syncthreads();
+    const int j0 = kt * PK, b = kt & 1;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();  // tile kt landed for every wavefront; buffer b^1 is free
+    if (kt + 1 < ntiles) issue(kt + 1, b ^ 1);
+    const bf16x8* ks = lds + b * BUF;
+    const bf16x8* vs = ks + KT;
     if (j0 <= qw0 + 31 && qw0 < S) {
       // ---- S^T = K Q^T for 2 blocks of 32 keys
       f32x16 s[2];
 #pragma unroll
       for (int r = 0; r < 2; ++r) {
         s[r] = f32x16{};
-        const bf16* kr = ks + (r * 32 + (lane & 31)) * KST + hl * 8;
+        const int row = r * 32 + (lane & 31);
 #pragma unroll
         for (int k = 0; k < HD / 16; ++k)
-          s[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(kr + k * 16), qf[k], s[r], 0, 0, 0);
+          s[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks[row * KCH + pswz<KCH>(row, k * 2 + hl)], qf[k], s[r], 0, 0,
+                                                         0);
       }
       // ---- mask, scale, online softmax (lane = query column)
       float mloc = -INFINITY;
@@ -132,21 +180,23 @@ __global__ void __launch_bounds__(256) attn_prefill_bf16_kernel(const bf16* __re
         }
       // ---- O^T += V^T P^T; the k index of block (r, h) covers keys
       //      r*32 + h*16 + {hl*4 + 0..3, 8 + hl*4 + 0..3}
+      const bf16* vsb = (const bf16*)vs;
 #pragma unroll
       for (int d = 0; d < HD / 32; ++d) {
-        const bf16* vr = vs + (d * 32 + (lane & 31)) * VST + hl * 4;
+        const int dd = d * 32 + (lane & 31);
+        const bf16* vr = vsb + dd * PK + hl * 4;
 #pragma unroll
         for (int r = 0; r < 2; ++r)
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
-            const bf16x4 lo = *(const bf16x4*)(vr + r * 32 + h * 16);
-            const bf16x4 hi = *(const bf16x4*)(vr + r * 32 + h * 16 + 8);
-            const bf16x8 va = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            const int c0 = r * 4 + h * 2;  // logical chunks c0, c0 + 1 of the row
+            const bf16x4 lo = *(const bf16x4*)(vr + pswz<VCH>(dd, c0) * 8);
+            const bf16x4 hi = *(const bf16x4*)(vr + pswz<VCH>(dd, c0 + 1) * 8);
+            const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
             acc_o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[r][h], acc_o[d], 0, 0, 0);
           }
       }
     }
-    __syncthreads();
   }
   if (myq >= S) return;
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -172,16 +222,6 @@ __global__ void __launch_bounds__(256) attn_prefill_bf16_kernel(const bf16* __re
 // output is written directly, otherwise every split stores an unnormalized
 // partial and the combine kernel merges them.
 // ============================================================================
-// Page of position ``pos`` of ``slot`` for a wave-uniform (slot, pos): read
-// through the constant address space, so that it is a scalar load whose
-// wait does not hold up the wavefront's outstanding vector loads.  The page
-// table is not written while a kernel runs.
-AXON_DEV int64_t kv_page_uniform(const KVView& c, int slot, int pos) {
-  if (!c.bt) return slot;
-  typedef const __attribute__((address_space(4))) int32_t* cptr;
-  const cptr bt = (cptr)(uintptr_t)c.bt;
-  return bt[__builtin_amdgcn_readfirstlane(slot * c.bt_stride + pos / c.ps)];
-}
 
 template <int HD, int DNW>
 __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* __restrict__ q, KVView kv,
