@@ -31,8 +31,10 @@ AXON_DEV int64_t kv_page_uniform(const KVView& c, int slot, int pos) {
 }
 
 // ============================================================================
-// Prefill (bf16): a workgroup = 128 queries of one head of one sequence, four
-// wavefronts of 32 queries; key tiles of 64, K [64][hd] and V^T [hd][64]
+// Prefill (bf16): a workgroup = 4 wavefronts x QB blocks of 32 queries of one
+// head of one sequence (each K / V^T fragment read from LDS feeds QB MFMAs:
+// with one block per wavefront the LDS reads alone would need ~128 B/clk
+// per CU at full MFMA rate); key tiles of 64, K [64][hd] and V^T [hd][64]
 // moved straight from global memory into LDS (global_load_lds_dwordx4: lane L
 // writes 16 bytes at offset 16 L) one tile ahead of the tile being computed,
 // in two LDS buffers; v_mfma_f32_32x32x16_bf16 for both products.  The bank
@@ -40,7 +42,11 @@ AXON_DEV int64_t kv_page_uniform(const KVView& c, int slot, int pos) {
 // choosing which global chunk each lane loads.  Keys past the sequence load
 // its last key (finite; their scores are masked).
 // ============================================================================
-constexpr int PQ = 128, PK = 64;
+constexpr int PK = 64;
+#ifndef AXON_PREFILL_QB
+#define AXON_PREFILL_QB 1
+#endif
+constexpr int PREFILL_QB = AXON_PREFILL_QB;  // 32-query blocks per wavefront
 
 // physical 16-byte chunk of logical chunk c in row r of an LDS tile whose
 // rows hold CH chunks: the 16 lanes of a read phase (16 consecutive rows,
@@ -51,8 +57,8 @@ AXON_DEV int pswz(int r, int c) {
   else return c ^ ((r >> 1) & 7);  // 8 chunks: rows r and r+1 share a 256-byte bank line
 }
 
-template <int HD>
-__global__ void __launch_bounds__(256, 2) attn_prefill_bf16_kernel(const bf16* __restrict__ q, KVView kv,
+template <int HD, int QB>
+__global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel(const bf16* __restrict__ q, KVView kv,
                                                                    bf16* __restrict__ o, int nseq,
                                                                    const int32_t* __restrict__ cu, int H) {
   constexpr int KCH = HD / 8;            // 16-byte chunks per K row
@@ -60,12 +66,14 @@ __global__ void __launch_bounds__(256, 2) attn_prefill_bf16_kernel(const bf16* _
   constexpr int KT = PK * KCH;           // chunks per K tile
   constexpr int VT = HD * VCH;           // chunks per V^T tile
   constexpr int BUF = KT + VT;           // chunks per buffer
+  constexpr int WQ = 32 * QB;            // queries per wavefront
+  constexpr int TQ = 4 * WQ;             // queries per workgroup
   __shared__ bf16x8 lds[2 * BUF];
 
   // locate (sequence, query tile) of this workgroup
   int seq = 0, tile = blockIdx.x;
   for (; seq < nseq; ++seq) {
-    const int nt = (cu[seq + 1] - cu[seq] + PQ - 1) / PQ;
+    const int nt = (cu[seq + 1] - cu[seq] + TQ - 1) / TQ;
     if (tile < nt) break;
     tile -= nt;
   }
@@ -74,19 +82,20 @@ __global__ void __launch_bounds__(256, 2) attn_prefill_bf16_kernel(const bf16* _
   const int kvh = head / group;
   const int S = cu[seq + 1] - cu[seq];
   const int tok0 = cu[seq];
-  const int q0 = tile * PQ;
+  const int q0 = tile * TQ;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qw0 = q0 + wave * 32;
-  const int myq = qw0 + (lane & 31);
+  const int qw0 = q0 + wave * WQ;  // this wavefront's queries: QB blocks of 32
   const int hl = lane >> 5;
 
   // Q^T fragments (B operand): column = query, k = head-dim (queries past S
   // read the last query; their outputs are not stored)
-  bf16x8 qf[HD / 16];
-  {
+  bf16x8 qf[QB][HD / 16];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int myq = qw0 + qb * 32 + (lane & 31);
     const bf16* qp = q + ((int64_t)(tok0 + min(myq, S - 1)) * H + head) * HD + hl * 8;
 #pragma unroll
-    for (int k = 0; k < HD / 16; ++k) qf[k] = *(const bf16x8*)(qp + k * 16);
+    for (int k = 0; k < HD / 16; ++k) qf[qb][k] = *(const bf16x8*)(qp + k * 16);
   }
 
   // issue the loads of key tile kt into buffer b: thread chunk slots
@@ -102,7 +111,7 @@ __global__ void __launch_bounds__(256, 2) attn_prefill_bf16_kernel(const bf16* _
     for (int i = 0; i < KT / 256; ++i) {
       const int p = (i * 4 + wave) * 64 + lane;
       const int r = p / KCH, c = pswz<KCH>(r, p % KCH);  // pswz is its own inverse
-      const int key = min(j0 + r, S - 1);  // in [j0, j0 + 64): j0 < S
+      const int key = min(j0 + r, S - 1);                 // in [j0, j0 + 64): j0 < S
       const int64_t page = pg[(key - j0) >> 4];
       const bf16* src = kb + ((page * kv.kv_heads + kvh) * kv.ps + key % kv.ps) * HD + c * 8;
       __builtin_amdgcn_global_load_lds((const void*)src,
@@ -122,13 +131,18 @@ __global__ void __launch_bounds__(256, 2) attn_prefill_bf16_kernel(const bf16* _
     }
   };
 
-  f32x16 acc_o[HD / 32];
+  f32x16 acc_o[QB][HD / 32];
+  float m_run[QB], l_run[QB];
 #pragma unroll
-  for (int d = 0; d < HD / 32; ++d) acc_o[d] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.f;
+  for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+    for (int d = 0; d < HD / 32; ++d) acc_o[qb][d] = f32x16{};
+    m_run[qb] = -INFINITY;
+    l_run[qb] = 0.f;
+  }
   const float sc = LOG2E / sqrtf((float)HD);
 
-  const int kend = min(S, q0 + PQ);  // keys needed by the workgroup
+  const int kend = min(S, q0 + TQ);  // keys needed by the workgroup
   const int ntiles = (kend + PK - 1) / PK;
   issue(0, 0);
   for (int kt = 0; kt < ntiles; ++kt) {
@@ -137,79 +151,111 @@ __global__ void __launch_bounds__(256, 2) attn_prefill_bf16_kernel(const bf16* _
     __syncthreads();  // tile kt landed for every wavefront; buffer b^1 is free
     if (kt + 1 < ntiles) issue(kt + 1, b ^ 1);
     const bf16x8* ks = lds + b * BUF;
-    const bf16x8* vs = ks + KT;
-    if (j0 <= qw0 + 31 && qw0 < S) {
-      // ---- S^T = K Q^T for 2 blocks of 32 keys
-      f32x16 s[2];
+    const bf16* vsb = (const bf16*)(ks + KT);
+    if (j0 > qw0 + WQ - 1 || qw0 >= S) continue;  // every key of the tile is after this wavefront's queries
+    // ---- S^T = K Q^T: each K fragment serves the QB query blocks
+    f32x16 s[QB][2];
 #pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        s[r] = f32x16{};
-        const int row = r * 32 + (lane & 31);
+    for (int r = 0; r < 2; ++r) {
 #pragma unroll
-        for (int k = 0; k < HD / 16; ++k)
-          s[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ks[row * KCH + pswz<KCH>(row, k * 2 + hl)], qf[k], s[r], 0, 0,
-                                                         0);
+      for (int qb = 0; qb < QB; ++qb) s[qb][r] = f32x16{};
+      const int row = r * 32 + (lane & 31);
+#pragma unroll
+      for (int k = 0; k < HD / 16; ++k) {
+        const bf16x8 kf = ks[row * KCH + pswz<KCH>(row, k * 2 + hl)];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          s[qb][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][k], s[qb][r], 0, 0, 0);
       }
-      // ---- mask, scale, online softmax (lane = query column)
+    }
+    // ---- online softmax (lane = query column), on unscaled scores: the
+    //      1/sqrt(hd) scale (log2 e folded in) enters the exponent's FMA.
+    //      Masking only where the tile crosses the diagonal or the sequence
+    //      end.  The reference maximum m_run[qb] is raised only when a score
+    //      exceeds it by more than 8 (in log2 units): probabilities stay <= 2^8
+    //      and the accumulator is rescaled rarely, not every tile (the sum and
+    //      the accumulator always share the reference, so the result is exact).
+    const bool masked = j0 + PK - 1 > qw0 || j0 + PK > S;
+    bf16x8 pb[QB][2][2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const int myq = qw0 + qb * 32 + (lane & 31);
       float mloc = -INFINITY;
-#pragma unroll
-      for (int r = 0; r < 2; ++r)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = j0 + r * 32 + (i / 4) * 8 + hl * 4 + (i % 4);
-          const float v = (key <= myq && key < S) ? s[r][i] * sc : -INFINITY;
-          s[r][i] = v;
-          mloc = fmaxf(mloc, v);
-        }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float m_new = fmaxf(m_run, mloc);
-      const float m_ref = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = exp2f(m_run - m_ref);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int d = 0; d < HD / 32; ++d) acc_o[d] *= alpha;
-      bf16x8 pb[2][2];
-#pragma unroll
-      for (int r = 0; r < 2; ++r)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float p = exp2f(s[r][i] - m_ref);
-          l_run += p;
-          pb[r][i / 8][i % 8] = (bf16)p;
-        }
-      // ---- O^T += V^T P^T; the k index of block (r, h) covers keys
-      //      r*32 + h*16 + {hl*4 + 0..3, 8 + hl*4 + 0..3}
-      const bf16* vsb = (const bf16*)vs;
-#pragma unroll
-      for (int d = 0; d < HD / 32; ++d) {
-        const int dd = d * 32 + (lane & 31);
-        const bf16* vr = vsb + dd * PK + hl * 4;
+      if (masked) {
 #pragma unroll
         for (int r = 0; r < 2; ++r)
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int c0 = r * 4 + h * 2;  // logical chunks c0, c0 + 1 of the row
-            const bf16x4 lo = *(const bf16x4*)(vr + pswz<VCH>(dd, c0) * 8);
-            const bf16x4 hi = *(const bf16x4*)(vr + pswz<VCH>(dd, c0 + 1) * 8);
-            const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-            acc_o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[r][h], acc_o[d], 0, 0, 0);
+          for (int i = 0; i < 16; ++i) {
+            const int key = j0 + r * 32 + (i / 4) * 8 + hl * 4 + (i % 4);
+            const float v = (key <= myq && key < S) ? s[qb][r][i] : -INFINITY;
+            s[qb][r][i] = v;
+            mloc = fmaxf(mloc, v);
           }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 2; ++r)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) mloc = fmaxf(mloc, s[qb][r][i]);
       }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * sc;  // scaled maximum of the tile
+      // raise the reference when the tile's maximum exceeds it by > 8
+      const bool raise = mloc > m_run[qb] + 8.f;
+      if (__builtin_amdgcn_ballot_w64(raise) != 0) {  // wave-uniform: rare after the first tiles
+        const float m_new = raise ? mloc : m_run[qb];
+        const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+        m_run[qb] = m_new;
+        l_run[qb] *= alpha;
+#pragma unroll
+        for (int d = 0; d < HD / 32; ++d) acc_o[qb][d] *= alpha;
+      }
+      const float m_ref = m_run[qb] == -INFINITY ? 0.f : m_run[qb];
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r][i], sc, -m_ref));
+          l_run[qb] += p;
+          pb[qb][r][i / 8][i % 8] = (bf16)p;
+        }
+    }
+    // ---- O^T += V^T P^T; the k index of block (r, h) covers keys
+    //      r*32 + h*16 + {hl*4 + 0..3, 8 + hl*4 + 0..3}; each V fragment
+    //      serves the QB query blocks
+#pragma unroll
+    for (int d = 0; d < HD / 32; ++d) {
+      const int dd = d * 32 + (lane & 31);
+      const bf16* vr = vsb + dd * PK + hl * 4;
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int c0 = r * 4 + h * 2;  // logical chunks c0, c0 + 1 of the row
+          const bf16x4 lo = *(const bf16x4*)(vr + pswz<VCH>(dd, c0) * 8);
+          const bf16x4 hi = *(const bf16x4*)(vr + pswz<VCH>(dd, c0 + 1) * 8);
+          const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            acc_o[qb][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[qb][r][h], acc_o[qb][d], 0, 0, 0);
+        }
     }
   }
-  if (myq >= S) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  const float inv = 1.f / l_tot;
-  bf16* op = o + ((int64_t)(tok0 + myq) * H + head) * HD;
 #pragma unroll
-  for (int d = 0; d < HD / 32; ++d)
+  for (int qb = 0; qb < QB; ++qb) {
+    const int myq = qw0 + qb * 32 + (lane & 31);
+    if (myq >= S) continue;
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32, 64);
+    const float inv = 1.f / l_tot;
+    bf16* op = o + ((int64_t)(tok0 + myq) * H + head) * HD;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int dd = d * 32 + g * 8 + hl * 4;
-      *(bf16x4*)(op + dd) = bf16x4{(bf16)(acc_o[d][g * 4 + 0] * inv), (bf16)(acc_o[d][g * 4 + 1] * inv),
-                                   (bf16)(acc_o[d][g * 4 + 2] * inv), (bf16)(acc_o[d][g * 4 + 3] * inv)};
-    }
+    for (int d = 0; d < HD / 32; ++d)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int dd = d * 32 + g * 8 + hl * 4;
+        *(bf16x4*)(op + dd) =
+            bf16x4{(bf16)(acc_o[qb][d][g * 4 + 0] * inv), (bf16)(acc_o[qb][d][g * 4 + 1] * inv),
+                   (bf16)(acc_o[qb][d][g * 4 + 2] * inv), (bf16)(acc_o[qb][d][g * 4 + 3] * inv)};
+      }
+  }
 }
 
 // ============================================================================
@@ -472,11 +518,12 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
     if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H);
     else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H);
   } else {
+    constexpr int QB = PREFILL_QB, TQ = 4 * 32 * QB;
     int tiles = 0;
-    for (int b = 0; b < nseq; ++b) tiles += (h_cu[b + 1] - h_cu[b] + PQ - 1) / PQ;
+    for (int b = 0; b < nseq; ++b) tiles += (h_cu[b + 1] - h_cu[b] + TQ - 1) / TQ;
     dim3 grid(tiles, H);
-    if (kv.hd == 64) attn_prefill_bf16_kernel<64><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H);
-    else attn_prefill_bf16_kernel<128><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H);
+    if (kv.hd == 64) attn_prefill_bf16_kernel<64, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H);
+    else attn_prefill_bf16_kernel<128, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H);
   }
 }
 
