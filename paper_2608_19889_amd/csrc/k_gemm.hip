@@ -25,12 +25,23 @@ AXON_DEV void store_cols(float* p, f32x4 v, int left) {
   }
 }
 
+// physical 16-byte chunk of logical chunk c in row r of an LDS panel with CH
+// chunks per row.  The LDS serves 256 bytes (64 banks) per cycle, so the 16
+// lanes of a ds_read_b128 phase (16 consecutive rows, one logical chunk) must
+// land in 16 distinct 16-byte bank groups: with 128-byte rows two rows share
+// a 256-byte bank line, so the XOR key is row / 2 (row / 4 for 64-byte rows).
+template <int CH>
+AXON_DEV int swz(int r, int c) {
+  if constexpr (CH == 8) return c ^ ((r >> 1) & 7);
+  else return c ^ ((r >> 2) & 3);
+}
+
 // ============================================================================
 // Prefill GEMM: 128 (W rows) x 128 (tokens) x 64 (k) tiles, 4 wavefronts in a
 // 2 x 2 arrangement, each owning a 64 x 64 sub-tile = 2 x 2 blocks of
 // v_mfma_f32_32x32x16_bf16.  Tiles are staged through LDS, double-buffered;
-// a row of 64 k values is 8 chunks of 16 bytes, stored at chunk ^ (row & 7)
-// so that the 16-byte fragment reads of 8 consecutive rows hit distinct banks.
+// a row of 64 k values is 8 chunks of 16 bytes, stored swizzled (swz)
+// so that the 16-byte fragment reads of 16 consecutive rows hit distinct banks.
 // ============================================================================
 namespace pf {
 constexpr int BN = 128, BM = 128, BK = 64, CH = BK / 8;
@@ -61,8 +72,8 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int idx = tid + i * 256, row = idx >> 3, ch = idx & 7;
-      lds[buf][0][row * CH + (ch ^ (row & 7))] = ra[i];
-      lds[buf][1][row * CH + (ch ^ (row & 7))] = rb[i];
+      lds[buf][0][row * CH + swz<8>(row, ch)] = ra[i];
+      lds[buf][1][row * CH + swz<8>(row, ch)] = rb[i];
     }
   };
 
@@ -87,8 +98,8 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
       for (int r = 0; r < 2; ++r) {
         const int ra_row = wr * 64 + r * 32 + (lane & 31);
         const int rb_row = wc * 64 + r * 32 + (lane & 31);
-        fa[r] = lds[buf][0][ra_row * CH + (ch ^ (ra_row & 7))];
-        fb[r] = lds[buf][1][rb_row * CH + (ch ^ (rb_row & 7))];
+        fa[r] = lds[buf][0][ra_row * CH + swz<8>(ra_row, ch)];
+        fb[r] = lds[buf][1][rb_row * CH + swz<8>(rb_row, ch)];
       }
 #pragma unroll
       for (int a = 0; a < 2; ++a)
@@ -165,14 +176,6 @@ AXON_DEV void tile_order(int bid, int gx, int gy, int& pn, int& pm) {
   pn = (logical % per_group) / gsize;
 }
 
-// physical 16-byte chunk of logical chunk c in row r of an LDS panel with CH
-// chunks per row: 8 consecutive rows reading the same logical chunk hit
-// distinct bank groups
-template <int CH>
-AXON_DEV int swz(int r, int c) {
-  if constexpr (CH == 8) return c ^ (r & 7);
-  else return c ^ ((r >> 1) & 3);
-}
 
 template <int STAGES>
 AXON_DEV void wait_stage(int after) {
@@ -247,26 +250,44 @@ __global__ void __launch_bounds__(NWV * 64, 1) gemm_bf16_256_kernel(const bf16* 
     if (kt + STAGES - 1 < nk) issue((kt + STAGES - 1) % STAGES, (kt + STAGES - 1) * BK);
     const bf16x8* la = lds2 + (kt % STAGES) * STAGE;
     const bf16x8* lb = la + PANEL;
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
+    // operand fragments double-buffered in registers: the LDS reads of k-step
+    // ks+1 are issued before the MFMAs of k-step ks
+    bf16x8 fa[2][4], fb[2][TB];
+    auto frags = [&](int ks, int f) {
       const int ch = ks * 2 + (lane >> 5);
-      bf16x8 fa[4], fb[TB];
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
         const int r = wr * 128 + a * 32 + (lane & 31);
-        fa[a] = la[r * CH + swz<CH>(r, ch)];
+        fa[f][a] = la[r * CH + swz<CH>(r, ch)];
       }
 #pragma unroll
       for (int b = 0; b < TB; ++b) {
         const int r = wc * (32 * TB) + b * 32 + (lane & 31);
-        fb[b] = lb[r * CH + swz<CH>(r, ch)];
+        fb[f][b] = lb[r * CH + swz<CH>(r, ch)];
       }
+    };
+    frags(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      if (ks + 1 < BK / 16) frags(ks + 1, (ks + 1) & 1);
 #pragma unroll
       for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int b = 0; b < TB; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks & 1][a], fb[ks & 1][b], acc[a][b], 0, 0, 0);
+#if AXON_G256_SCHED == 1
+      // interleave: one LDS read after each of the first 4 + TB MFMAs
+#pragma unroll
+      for (int i = 0; i < 4 + TB; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 4 * TB - (4 + TB), 0);
+#endif
     }
+#if AXON_G256_SCHED == 2
+    __builtin_amdgcn_iglp_opt(0);
+#endif
   }
   // epilogue: acc[a][b][i] = C[n][t],
   //   n = n0 + wr*128 + a*32 + (i/4)*8 + (lane/32)*4 + i%4,  t = m0 + wc*32*TB + b*32 + lane%32
@@ -302,6 +323,9 @@ __global__ void __launch_bounds__(NWV * 64, 1) gemm_bf16_256_kernel(const bf16* 
   }
 }
 
+#ifndef AXON_G256_SCHED
+#define AXON_G256_SCHED 0
+#endif
 #ifndef AXON_G256_BK
 #define AXON_G256_BK 64
 #define AXON_G256_STAGES 2
