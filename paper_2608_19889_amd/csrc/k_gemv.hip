@@ -162,8 +162,18 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
 #pragma unroll
     for (int i = 0; i < SSR; ++i)
       if (ss_sl < ss_slices && ss_sl + i * ss_slices < a.ss_n) ss_part += ss_reg[i];
-    if (ss_sl < ss_slices)
-      for (int j = ss_sl + SSR * ss_slices; j < a.ss_n; j += ss_slices) ss_part += a.ss_in[(int64_t)j * M + ss_t];
+    // partials beyond the prefetched ones: 16 independent loads per round
+    // (a load-add loop would wait for every load in turn)
+    if (ss_sl < ss_slices) {
+      for (int j0 = ss_sl + SSR * ss_slices; j0 < a.ss_n; j0 += SSR * ss_slices) {
+        float v[SSR];
+#pragma unroll
+        for (int i = 0; i < SSR; ++i) v[i] = a.ss_in[(int64_t)min(j0 + i * ss_slices, a.ss_n - 1) * M + ss_t];
+#pragma unroll
+        for (int i = 0; i < SSR; ++i)
+          if (j0 + i * ss_slices < a.ss_n) ss_part += v[i];
+      }
+    }
     s_ss[tid] = ss_part;
   }
   __syncthreads();
