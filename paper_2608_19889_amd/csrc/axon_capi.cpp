@@ -159,6 +159,7 @@ struct axon_model {
   float* gu_f32 = nullptr;
   float* logits_int = nullptr;
   float* attn_part = nullptr;
+  float* gemv_part = nullptr;  // split-K partial sums of the decode projections
   float* ss = nullptr;       // per-workgroup sums of squares of x rows
   void* xg = nullptr;        // bf16(x * g) for the next normalized projection
   int ss_n = 0;              // number of partials currently in ss
@@ -406,7 +407,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
     qa.W = (const bf16*)w.wqkv; qa.N = nq; qa.K = D; qa.M = B;
     qa.X = xg; qa.ss_in = m->ss; qa.ss_n = ss_n; qa.eps = eps;
     qa.bias = (const bf16*)w.bqkv; qa.cos_t = m->rope_cos; qa.sin_t = m->rope_sin; qa.q_out = (bf16*)m->q;
-    qa.kv = kv; qa.len = m->d_len; qa.H = H;
+    qa.kv = kv; qa.len = m->d_len; qa.H = H; qa.part = m->gemv_part;
     gemv(qa, GV_ROPE);
     int ctx_sum = 0;
     for (int b = 0; b < B; ++b) ctx_sum += m->h_len[b] + 1;
@@ -416,6 +417,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
     GemvArgs oa{};
     oa.W = (const bf16*)w.wo; oa.N = D; oa.K = H * hd; oa.M = B; oa.X = (const bf16*)m->o;
     oa.out_f32 = m->x; oa.ldo = D; oa.ss_out = m->ss; oa.xg_out = xg; oa.gain_next = (const bf16*)w.gpost;
+    oa.part = m->gemv_part;
     gemv(oa, GV_RESID);
     ss_n = ss_count(H * hd);
     GemvArgs ga{};
@@ -425,7 +427,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
     gemv(ga, GV_SILU);
     GemvArgs da{};
     da.W = (const bf16*)w.wd; da.N = D; da.K = I; da.M = B; da.X = (const bf16*)m->a;
-    da.out_f32 = m->x; da.ldo = D; da.ss_out = m->ss; da.xg_out = xg;
+    da.out_f32 = m->x; da.ldo = D; da.ss_out = m->ss; da.xg_out = xg; da.part = m->gemv_part;
     da.gain_next = (const bf16*)(last ? m->gfinal : m->layers[l + 1].gin);
     gemv(da, GV_RESID);
     ss_n = ss_count(I);
@@ -695,6 +697,14 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     for (int b = 1; b <= c.max_batch; ++b)
       bsplits = std::max<int64_t>(bsplits, (int64_t)b * plan_decode_splits(b, c.n_kv_heads, c.max_seq));
     TRY(dev_alloc(m, (void**)&m->attn_part, bsplits * H * (hd + 2) * 4));
+    if (m->bf) {
+      int64_t wsf = 0;
+      for (int b = 1; b <= std::min<int>(c.max_batch, GEMV_MAX_M); ++b)
+        wsf = std::max({wsf, gemv_workspace_floats((int)nq, (int)D, b, GV_ROPE),
+                        gemv_workspace_floats((int)D, (int)(H * hd), b, GV_RESID),
+                        gemv_workspace_floats((int)D, (int)I, b, GV_RESID)});
+      if (wsf > 0) TRY(dev_alloc(m, (void**)&m->gemv_part, (size_t)wsf * 4));
+    }
     TRY(dev_alloc(m, (void**)&m->ss, (int64_t)std::max<int64_t>(D / 8, 1) * c.max_batch * 4));
     TRY(dev_alloc(m, &m->xg, (int64_t)c.max_batch * D * 2));
     const int64_t nam = (V + 15) / 16;

@@ -34,6 +34,106 @@ AXON_DEV float silu_g(float z) { return z / (1.f + __expf(-z)); }
 
 constexpr int GV_U = 4;  // k-steps of 32 per pipeline stage
 
+// The epilogues of a tile of ROWS output features x COLS token columns
+// starting at feature n0; total(row, col) is the finished (normalized) dot
+// product.  wg / nwg index the per-tile partials (sums of squares, argmax).
+// aux: LDS of at least max(ROWS, 16) x (COLS + 1) floats.
+template <int ROWS, int COLS, int NT, int EPI, typename Total>
+AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg, int nwg, const Total& total) {
+  const int M = a.M, lane = tid & 63, wave = tid >> 6;
+  auto s_aux = [&](int row, int col) -> float& { return aux[row * (COLS + 1) + col]; };
+  if constexpr (EPI == GV_RESID) {
+    for (int it = tid; it < ROWS * COLS; it += NT) {
+      const int row = it / COLS, col = it % COLS, n = n0 + row;
+      float sq = 0.f;
+      if (col < M && n < a.N) {
+        float* p = a.out_f32 + (int64_t)col * a.ldo + n;
+        const float v = *p + total(row, col);
+        *p = v;
+        sq = v * v;
+        a.xg_out[(int64_t)col * a.ldo + n] = (bf16)(v * (float)a.gain_next[n]);
+      }
+      s_aux(row, col) = sq;
+    }
+    __syncthreads();
+    if (tid < M) {
+      float sq = 0.f;
+      for (int row = 0; row < ROWS; ++row) sq += s_aux(row, tid);
+      a.ss_out[(int64_t)wg * M + tid] = sq;
+    }
+  } else if constexpr (EPI == GV_SILU) {
+    // each 32-row block: rows 0..15 gate, 16..31 the matching up rows
+    for (int it = tid; it < (ROWS / 2) * COLS; it += NT) {
+      const int fl = it / COLS, col = it % COLS;
+      if (col >= M) continue;
+      const int blk = fl / 16, f = fl % 16;
+      const float g = total(blk * 32 + f, col), u = total(blk * 32 + 16 + f, col);
+      a.out_t[(int64_t)col * a.ldo + n0 / 2 + fl] = (bf16)(silu_g(g) * u);
+    }
+  } else if constexpr (EPI == GV_ROPE) {
+    // an 8-row group of a head = first halves i = 4g..4g+3 and their partners
+    const int hd = a.kv.hd, half = hd / 2;
+    const int head = n0 / hd, g0 = (n0 % hd) / 8;
+    const int KVh = a.kv.kv_heads;
+    for (int it = tid; it < (ROWS / 2) * COLS; it += NT) {
+      const int pr = it / COLS, t = it % COLS;
+      if (t >= M) continue;
+      const int gl = pr / 4, i4 = pr % 4;
+      const int i = (g0 + gl) * 4 + i4;  // rotation pair (i, i + hd/2) of this head
+      float x1 = total(gl * 8 + i4, t), x2 = total(gl * 8 + 4 + i4, t);
+      if (a.bias) {
+        x1 += (float)a.bias[head * hd + i];
+        x2 += (float)a.bias[head * hd + half + i];
+      }
+      const int pos = a.len[t];
+      if (head < a.H + KVh) {
+        const float cs = a.cos_t[(int64_t)pos * half + i], sn = a.sin_t[(int64_t)pos * half + i];
+        const float y1 = x1 * cs - x2 * sn, y2 = x2 * cs + x1 * sn;
+        bf16* dst = head < a.H ? a.q_out + ((int64_t)t * a.H + head) * hd
+                               : (bf16*)a.kv.k + k_off(a.kv, t, head - a.H, pos);
+        dst[i] = (bf16)y1;
+        dst[i + half] = (bf16)y2;
+      } else {
+        const int kvh = head - a.H - KVh;
+        bf16* vt = (bf16*)a.kv.v;
+        vt[vt_off(a.kv, t, kvh, i, pos)] = (bf16)x1;
+        vt[vt_off(a.kv, t, kvh, i + half, pos)] = (bf16)x2;
+      }
+    }
+  } else {  // GV_HEAD
+    for (int it = tid; it < ROWS * COLS; it += NT) {
+      const int row = it / COLS, col = it % COLS, n = n0 + row;
+      float v = -INFINITY;
+      if (col < M && n < a.N) {
+        v = total(row, col);
+        if (a.out_f32) a.out_f32[(int64_t)col * a.ldo + n] = v;
+      }
+      s_aux(row, col) = v;
+    }
+    __syncthreads();
+    // per token, the largest logit of the tile and its lowest index (a
+    // wavefront per token)
+    for (int t = wave; t < M; t += NT / 64) {
+      float best = -INFINITY;
+      int bi = 0x7fffffff;
+      for (int row = lane; row < ROWS; row += 64) {
+        const float v = s_aux(row, t);
+        if (v > best) { best = v; bi = n0 + row; }
+      }
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const float ov = __shfl_xor(best, m, 64);
+        const int oi = __shfl_xor(bi, m, 64);
+        if (ov > best || (ov == best && oi < bi)) { best = ov; bi = oi; }
+      }
+      if (lane == 0) {
+        a.am_val[(int64_t)t * nwg + wg] = best;
+        a.am_idx[(int64_t)t * nwg + wg] = bi;
+      }
+    }
+  }
+}
+
 template <int ROWS, int KS, int NB, bool NORM, int EPI, int U = GV_U>
 __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
   constexpr int RB = ROWS < 16 ? 1 : ROWS / 16;  // 16-row MFMA blocks (an 8-row tile leaves 8 rows idle)
@@ -42,13 +142,18 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
   __shared__ float red[KS][RB * 16][COLS + 1];
   __shared__ float s_ss[NT];
   __shared__ float s_inv[64];
-  __shared__ float s_aux[RB * 16][COLS + 1];
+  __shared__ float s_aux[EPI == GV_PART ? 1 : RB * 16][COLS + 1];  // epilogue scratch (unused for partials)
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = blockIdx.x * ROWS;
   const int K = a.K, M = a.M;
-  const int kc = ((K + KS - 1) / KS + 32 * U - 1) / (32 * U) * (32 * U);
-  const int k0 = min(K, wave * kc), k1 = min(K, k0 + kc);
+  // K range of the workgroup (split K: split blockIdx.y of gridDim.y, each a
+  // multiple of 32), divided among the KS wavefronts in whole stages
+  const int klen = EPI == GV_PART ? ((K + gridDim.y - 1) / gridDim.y + 31) / 32 * 32 : K;
+  const int kbase = EPI == GV_PART ? min(K, (int)blockIdx.y * klen) : 0;
+  const int kloc = min(K - kbase, klen);
+  const int kc = ((kloc + KS - 1) / KS + 32 * U - 1) / (32 * U) * (32 * U);
+  const int k0 = kbase + min(kloc, wave * kc), k1 = kbase + min(kloc, wave * kc + kc);
   const int r16 = lane & 15;
 
   // Every load below is unconditional (a load under a lane condition makes
@@ -193,96 +298,60 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
     return s;
   };
 
-  if constexpr (EPI == GV_RESID) {
+  if constexpr (EPI == GV_PART) {
+    // raw tile sums of this K split: part[split][col][n0 + row]
     for (int it = tid; it < ROWS * COLS; it += NT) {
-      const int row = it / COLS, col = it % COLS, n = n0 + row;
-      float sq = 0.f;
-      if (col < M && n < a.N) {
-        float* p = a.out_f32 + (int64_t)col * a.ldo + n;
-        const float v = *p + total(row, col);
-        *p = v;
-        sq = v * v;
-        a.xg_out[(int64_t)col * a.ldo + n] = (bf16)(v * (float)a.gain_next[n]);
-      }
-      s_aux[row][col] = sq;
+      const int row = it % ROWS, col = it / ROWS, n = n0 + row;
+      if (col < M && n < a.N) a.part[((int64_t)blockIdx.y * M + col) * a.N + n] = total(row, col);
     }
+  } else {
+    gv_epilogue<ROWS, COLS, NT, EPI>(a, n0, tid, (float*)s_aux, blockIdx.x, gridDim.x, total);
+  }
+}
+
+// Epilogue of a split-K projection: total = the K splits' partial sums in
+// split order (deterministic), times the RMSNorm factor of the token, then
+// the projection's epilogue on tiles of EROWS features.
+template <int EROWS, int NB, bool NORM, int EPI>
+__global__ void __launch_bounds__(256) gemv_split_epilogue_kernel(GemvArgs a, int nsplit) {
+  constexpr int COLS = NB * 16, NT = 256, SSR = 16;
+  __shared__ float s_ss[NT];
+  __shared__ float s_inv[64];
+  __shared__ float s_aux[(EROWS > 16 ? EROWS : 16) * (COLS + 1)];
+  const int tid = threadIdx.x, M = a.M;
+  const int n0 = blockIdx.x * EROWS;
+  if constexpr (NORM) {
+    // token t = tid % M, slice tid / M: partials j = slice (mod slices), 16
+    // independent loads per round
+    const int slices = NT / M, t = tid % M, sl = tid / M;
+    float v = 0.f;
+    if (sl < slices) {
+      for (int j0 = sl; j0 < a.ss_n; j0 += SSR * slices) {
+        float r[SSR];
+#pragma unroll
+        for (int i = 0; i < SSR; ++i) r[i] = a.ss_in[(int64_t)min(j0 + i * slices, a.ss_n - 1) * M + t];
+#pragma unroll
+        for (int i = 0; i < SSR; ++i)
+          if (j0 + i * slices < a.ss_n) v += r[i];
+      }
+    }
+    s_ss[tid] = v;
     __syncthreads();
     if (tid < M) {
-      float sq = 0.f;
-      for (int row = 0; row < ROWS; ++row) sq += s_aux[row][tid];
-      a.ss_out[(int64_t)blockIdx.x * M + tid] = sq;
-    }
-  } else if constexpr (EPI == GV_SILU) {
-    // each 32-row block: rows 0..15 gate, 16..31 the matching up rows
-    for (int it = tid; it < (ROWS / 2) * COLS; it += NT) {
-      const int fl = it / COLS, col = it % COLS;
-      if (col >= M) continue;
-      const int blk = fl / 16, f = fl % 16;
-      const float g = total(blk * 32 + f, col), u = total(blk * 32 + 16 + f, col);
-      a.out_t[(int64_t)col * a.ldo + n0 / 2 + fl] = (bf16)(silu_g(g) * u);
-    }
-  } else if constexpr (EPI == GV_ROPE) {
-    // an 8-row group of a head = first halves i = 4g..4g+3 and their partners
-    const int hd = a.kv.hd, half = hd / 2;
-    const int head = n0 / hd, g0 = (n0 % hd) / 8;
-    const int KVh = a.kv.kv_heads;
-    for (int it = tid; it < (ROWS / 2) * COLS; it += NT) {
-      const int pr = it / COLS, t = it % COLS;
-      if (t >= M) continue;
-      const int gl = pr / 4, i4 = pr % 4;
-      const int i = (g0 + gl) * 4 + i4;  // rotation pair (i, i + hd/2) of this head
-      float x1 = total(gl * 8 + i4, t), x2 = total(gl * 8 + 4 + i4, t);
-      if (a.bias) {
-        x1 += (float)a.bias[head * hd + i];
-        x2 += (float)a.bias[head * hd + half + i];
-      }
-      const int pos = a.len[t];
-      if (head < a.H + KVh) {
-        const float cs = a.cos_t[(int64_t)pos * half + i], sn = a.sin_t[(int64_t)pos * half + i];
-        const float y1 = x1 * cs - x2 * sn, y2 = x2 * cs + x1 * sn;
-        bf16* dst = head < a.H ? a.q_out + ((int64_t)t * a.H + head) * hd
-                               : (bf16*)a.kv.k + k_off(a.kv, t, head - a.H, pos);
-        dst[i] = (bf16)y1;
-        dst[i + half] = (bf16)y2;
-      } else {
-        const int kvh = head - a.H - KVh;
-        bf16* vt = (bf16*)a.kv.v;
-        vt[vt_off(a.kv, t, kvh, i, pos)] = (bf16)x1;
-        vt[vt_off(a.kv, t, kvh, i + half, pos)] = (bf16)x2;
-      }
-    }
-  } else {  // GV_HEAD
-    for (int it = tid; it < ROWS * COLS; it += NT) {
-      const int row = it / COLS, col = it % COLS, n = n0 + row;
-      float v = -INFINITY;
-      if (col < M && n < a.N) {
-        v = total(row, col);
-        if (a.out_f32) a.out_f32[(int64_t)col * a.ldo + n] = v;
-      }
-      s_aux[row][col] = v;
+      float tot = 0.f;
+      for (int j = 0; j < slices; ++j) tot += s_ss[j * M + tid];
+      s_inv[tid] = rsqrtf(tot / (float)a.K + a.eps);
     }
     __syncthreads();
-    // per token, the largest logit of the tile and its lowest index (a
-    // wavefront per token)
-    for (int t = wave; t < M; t += KS) {
-      float best = -INFINITY;
-      int bi = 0x7fffffff;
-      for (int row = lane; row < ROWS; row += 64) {
-        const float v = s_aux[row][t];
-        if (v > best) { best = v; bi = n0 + row; }
-      }
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        const float ov = __shfl_xor(best, m, 64);
-        const int oi = __shfl_xor(bi, m, 64);
-        if (ov > best || (ov == best && oi < bi)) { best = ov; bi = oi; }
-      }
-      if (lane == 0) {
-        a.am_val[(int64_t)t * gridDim.x + blockIdx.x] = best;
-        a.am_idx[(int64_t)t * gridDim.x + blockIdx.x] = bi;
-      }
-    }
   }
+  auto total = [&](int row, int col) {
+    const int n = min(n0 + row, a.N - 1), c = min(col, M - 1);
+    float sum = 0.f;
+    for (int sp = 0; sp < nsplit; ++sp) sum += a.part[((int64_t)sp * M + c) * a.N + n];
+    if constexpr (NORM) sum *= s_inv[c];
+    return sum;
+  };
+  gv_epilogue<EROWS, COLS, NT, EPI>(a, n0, tid, s_aux, blockIdx.x, gridDim.x, total);
 }
 
 // next[t] = index of the largest partial maximum (lowest index on ties);
@@ -360,21 +429,35 @@ __global__ void __launch_bounds__(256) embed_ss_kernel(const int32_t* __restrict
 GvShape gemv_shape(int N, int K, int M, int epi) {
   const int nb = (M + 15) / 16;
   if (nb == 1) {
-    if (epi == GV_SILU) return {32, 4, 4};
-    if (epi == GV_HEAD) return {K <= 2048 ? 32 : 64, 8, 2};
-    if (N / 16 < 192) return {8, 16, 2};
-    return K >= 8192 ? GvShape{16, 8, 4} : GvShape{16, 16, 2};
+    if (epi == GV_SILU) return {32, 4, 4, 1, 0};
+    if (epi == GV_HEAD) return {K <= 2048 ? 32 : 64, 8, 2, 1, 0};
+    if (N / 16 < 192) return {8, 16, 2, 1, 0};
+    return K >= 8192 ? GvShape{16, 8, 4, 1, 0} : GvShape{16, 16, 2, 1, 0};
   }
-  if (nb == 2) {
-    if (epi == GV_SILU || epi == GV_HEAD) return {64, 2, 2};
-    return epi == GV_ROPE ? GvShape{16, 4, 2} : GvShape{32, 8, 2};
+  if (epi == GV_RESID || epi == GV_ROPE) {
+    // 17..64 tokens, narrow projections: 64-row tiles, so that each token
+    // fragment is reused by 4 row blocks (16-row tiles re-read the token
+    // operand, 4x the weight bytes at 64 tokens, from L2), and K split over
+    // workgroups towards >= 224 of them; a second kernel sums the splits and
+    // runs the epilogue on 16-row tiles.
+    const int blocks = (N + 63) / 64;
+    const int ksplit = std::max(1, std::min(8, (224 + blocks - 1) / blocks));
+    return {64, 4, 2, ksplit, 16};
   }
-  if (epi == GV_SILU) return {64, 4, 2};
-  if (epi == GV_HEAD) return {32, 4, 2};
-  return epi == GV_ROPE ? GvShape{16, 4, 2} : GvShape{16, 4, 4};
+  if (nb == 2) return {64, 2, 2, 1, 0};  // gate/up, head
+  if (epi == GV_SILU) return {64, 4, 2, 1, 0};
+  return {32, 4, 2, 1, 0};  // head
 }
 
-int gemv_rows(int N, int K, int M, int epi) { return gemv_shape(N, K, M, epi).rows; }
+int gemv_rows(int N, int K, int M, int epi) {
+  const GvShape sh = gemv_shape(N, K, M, epi);
+  return sh.ksplit > 1 ? sh.erows : sh.rows;
+}
+
+int64_t gemv_workspace_floats(int N, int K, int M, int epi) {
+  const GvShape sh = gemv_shape(N, K, M, epi);
+  return sh.ksplit > 1 ? (int64_t)sh.ksplit * M * N : 0;
+}
 
 template <int ROWS, int KS, int U, int NB, bool NORM, int EPI>
 static bool gv(const GemvArgs& a, hipStream_t s) {
@@ -392,14 +475,43 @@ static bool gv_dispatch(const GemvArgs& a, const GvShape& sh, int nb, hipStream_
   } else if constexpr (EPI == GV_HEAD) {
     AXON_GV(32, 8, 2, 1) AXON_GV(64, 8, 2, 1) AXON_GV(64, 2, 2, 2) AXON_GV(32, 4, 2, 3) AXON_GV(32, 4, 2, 4)
   } else if constexpr (EPI == GV_ROPE) {
-    AXON_GV(8, 16, 2, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 2, 1) AXON_GV(16, 4, 2, 2) AXON_GV(16, 4, 2, 3)
-    AXON_GV(16, 4, 2, 4)
+    AXON_GV(8, 16, 2, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 2, 1)
   } else {
-    AXON_GV(8, 16, 2, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 2, 1) AXON_GV(32, 8, 2, 2) AXON_GV(16, 4, 4, 3)
-    AXON_GV(16, 4, 4, 4)
+    AXON_GV(8, 16, 2, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 2, 1)
   }
 #undef AXON_GV
   return false;
+}
+
+// split K: partial sums (grid N/rows x ksplit) then the epilogue kernel; a
+// timed launch starts its events with the first kernel and stops with the
+// second
+template <int NB, bool NORM, int EPI>
+static bool gv_split(const GemvArgs& a, const GvShape& sh, hipStream_t s) {
+  if (sh.rows != 64 || sh.ks != 4 || sh.u != 2 || sh.erows != 16 || !a.part) return false;
+  auto k1 = gemv_fused_kernel<64, 4, NB, false, GV_PART, 2>;
+  auto k2 = gemv_split_epilogue_kernel<16, NB, NORM, EPI>;
+  const dim3 g1((a.N + 63) / 64, sh.ksplit), g2((a.N + 15) / 16);
+  const TimingSlot t = g_timing_slot;
+  g_timing_slot = TimingSlot{};
+  if (t.start) {
+    hipExtLaunchKernelGGL(k1, g1, dim3(256), 0, s, t.start, nullptr, 0, a);
+    hipExtLaunchKernelGGL(k2, g2, dim3(256), 0, s, nullptr, t.stop, 0, a, sh.ksplit);
+  } else {
+    k1<<<g1, 256, 0, s>>>(a);
+    k2<<<g2, 256, 0, s>>>(a, sh.ksplit);
+  }
+  return true;
+}
+
+template <int EPI, bool NORM>
+static bool gv_split_nb(const GemvArgs& a, const GvShape& sh, int nb, hipStream_t s) {
+  switch (nb) {
+    case 2: return gv_split<2, NORM, EPI>(a, sh, s);
+    case 3: return gv_split<3, NORM, EPI>(a, sh, s);
+    case 4: return gv_split<4, NORM, EPI>(a, sh, s);
+    default: return false;
+  }
 }
 
 bool launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s) {
@@ -408,6 +520,11 @@ bool launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s) {
   const GvShape sh = gemv_shape(a.N, a.K, a.M, epi);
   const int nb = (a.M + 15) / 16;
   const bool norm = a.ss_in != nullptr;
+  if (sh.ksplit > 1) {
+    if (epi == GV_RESID) return !norm && gv_split_nb<GV_RESID, false>(a, sh, nb, s);
+    if (epi == GV_ROPE) return norm && gv_split_nb<GV_ROPE, true>(a, sh, nb, s);
+    return false;
+  }
   switch (epi) {
     case GV_SILU: return norm && gv_dispatch<GV_SILU, true>(a, sh, nb, s);
     case GV_ROPE: return norm && gv_dispatch<GV_ROPE, true>(a, sh, nb, s);

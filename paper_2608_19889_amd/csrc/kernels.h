@@ -73,7 +73,7 @@ template <typename T>
 void launch_silu_reduce(const float* parts, int nparts, int64_t part_stride, T* a, int M, int I,
                         hipStream_t s);
 // ---- fused decode projections (k_gemv.hip)
-enum GvEpi : int { GV_HEAD = 0, GV_RESID = 1, GV_SILU = 2, GV_ROPE = 3 };
+enum GvEpi : int { GV_HEAD = 0, GV_RESID = 1, GV_SILU = 2, GV_ROPE = 3, GV_PART = 4 /* internal: split-K partials */ };
 
 struct GemvArgs {
   const bf16* W;  // [N][K]
@@ -101,11 +101,18 @@ struct GemvArgs {
   KVView kv;
   const int32_t* len;
   int H;
+  // split K (projections of 17..64 tokens): workspace of ksplit * M * N floats
+  // (gemv_workspace_floats), owned by the caller
+  float* part;
 };
 constexpr int GEMV_MAX_M = 64;  // token columns one fused projection handles
 struct GvShape {
   int rows, ks, u;  // output rows per workgroup, wavefronts splitting K, k-steps of 32 per stage
+  int ksplit;       // workgroups splitting K (1: fused epilogue; else partials + an epilogue kernel)
+  int erows;        // rows per workgroup of the epilogue kernel (ksplit > 1)
 };
+// floats of GemvArgs::part a launch of this shape needs (0 when unsplit)
+int64_t gemv_workspace_floats(int N, int K, int M, int epi);
 GvShape gemv_shape(int N, int K, int M, int epi);
 int gemv_rows(int N, int K, int M, int epi);  // output rows per workgroup (ss partial count = N / rows)
 // false (nothing launched) when M > GEMV_MAX_M or the normalization does not

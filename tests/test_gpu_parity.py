@@ -42,6 +42,12 @@ BF16_CASES = {
     "qwen_hd128_g7_bias": ("7b", dict(layers=2, vocab=2048, hidden=896, intermediate=1792), [5, 129, 300], 6),
     "qwen32_hd128_g5_bias": ("32b", dict(layers=2, vocab=1500, hidden=640, intermediate=1280), [64, 257], 5),
     "smollm_hd64_g3": ("135m", dict(layers=3, vocab=1000, dtype="bf16"), [1, 31, 66, 90], 5),
+    # 17..64 sequences: decode projections split K over workgroups (partials
+    # + an epilogue kernel), with 2 and 3 token blocks
+    "llama_hd64_batch40": ("1b", dict(layers=2, vocab=3000, hidden=512, intermediate=1024),
+                           [2 + (i * 29) % 61 for i in range(40)], 4),
+    "qwen_hd128_bias_batch24": ("7b", dict(layers=2, vocab=2048, hidden=896, intermediate=1792),
+                                [3 + (i * 53) % 97 for i in range(24)], 4),
     # more sequences than one fused decode projection takes (64): the decode
     # step and the prefill head run as GEMMs
     "llama_hd64_batch80": ("1b", dict(layers=2, vocab=3000, hidden=512, intermediate=1024),
