@@ -142,7 +142,9 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
   __shared__ float red[KS][RB * 16][COLS + 1];
   __shared__ float s_ss[NT];
   __shared__ float s_inv[64];
-  __shared__ float s_aux[EPI == GV_PART ? 1 : RB * 16][COLS + 1];  // epilogue scratch (unused for partials)
+  // epilogue scratch: only the residual (sums of squares) and head (argmax)
+  // epilogues use it; its size limits how many workgroups share a CU
+  __shared__ float s_aux[(EPI == GV_RESID || EPI == GV_HEAD) ? RB * 16 : 1][COLS + 1];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = blockIdx.x * ROWS;
