@@ -465,17 +465,19 @@ __global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restric
 }
 
 // ============================================================================
-// float32 check mode: one thread per (query token, head), online softmax over
-// the keys of its sequence read from the cache.  Serves prefill (cu) and
-// decode (len).
+// float32 check mode: a wavefront per (query token, head).  Keys in chunks of
+// 64, one per lane for the score; online softmax across the wavefront; lane d
+// accumulates output dimensions d (and d + 64) over the chunk from the V^T
+// rows.  Serves prefill (cu) and decode (len).
 // ============================================================================
 template <int HD>
 __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ q, KVView kv, float* __restrict__ o,
                                                       int T_tokens, int nseq, const int32_t* __restrict__ cu,
                                                       const int32_t* __restrict__ len, int H) {
-  const int t = blockIdx.x * 64 + threadIdx.x;
-  const int head = blockIdx.y;
-  if (t >= T_tokens) return;
+  constexpr int DL = HD / 64;  // output dimensions per lane
+  __shared__ float qs[HD];
+  __shared__ float ps[64];
+  const int t = blockIdx.x, head = blockIdx.y, lane = threadIdx.x;
   int slot, pos;
   if (len) {
     slot = t;
@@ -485,26 +487,49 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ 
     pos = t - cu[slot];
   }
   const int kvh = head / (H / kv.kv_heads);
-  float qv[HD], acc[HD];
   const float* qp = q + ((int64_t)t * H + head) * HD;
-  for (int d = 0; d < HD; ++d) { qv[d] = qp[d]; acc[d] = 0.f; }
+  for (int d = lane; d < HD; d += 64) qs[d] = qp[d];
+  __syncthreads();
   const float sc = LOG2E / sqrtf((float)HD);
-  float m = -INFINITY, l = 0.f;
   const float* kb = (const float*)kv.k;
   const float* vb = (const float*)kv.v;
-  for (int j = 0; j <= pos; ++j) {
-    const float* kp = kb + k_off(kv, slot, kvh, j);
-    float s = 0.f;
-    for (int d = 0; d < HD; ++d) s = fmaf(qv[d], kp[d], s);
-    s *= sc;
-    const float m_new = fmaxf(m, s);
-    const float alpha = exp2f(m - m_new), p = exp2f(s - m_new);
-    l = l * alpha + p;
-    for (int d = 0; d < HD; ++d) acc[d] = acc[d] * alpha + p * vb[vt_off(kv, slot, kvh, d, j)];
+  float m = -INFINITY, l = 0.f, acc[DL] = {};
+  for (int j0 = 0; j0 <= pos; j0 += 64) {
+    // score of key j0 + lane
+    const int j = j0 + lane;
+    float sj = -INFINITY;
+    if (j <= pos) {
+      const float* kp = kb + k_off(kv, slot, kvh, j);
+      float dot = 0.f;
+      for (int d = 0; d < HD; d += 4) {
+        const f32x4 kv4 = *(const f32x4*)(kp + d);
+        dot = fmaf(qs[d], kv4[0], dot);
+        dot = fmaf(qs[d + 1], kv4[1], dot);
+        dot = fmaf(qs[d + 2], kv4[2], dot);
+        dot = fmaf(qs[d + 3], kv4[3], dot);
+      }
+      sj = dot * sc;
+    }
+    const float m_new = fmaxf(m, wave_max(sj));  // finite: key j0 <= pos
+    const float alpha = exp2f(m - m_new);
+    const float p = j <= pos ? exp2f(sj - m_new) : 0.f;
+    l = l * alpha + wave_sum(p);
     m = m_new;
+    ps[lane] = p;
+    __syncthreads();
+    const int nj = min(64, pos + 1 - j0);
+#pragma unroll
+    for (int i = 0; i < DL; ++i) {
+      const int d = lane + i * 64;
+      float a = acc[i] * alpha;
+      for (int jj = 0; jj < nj; ++jj) a = fmaf(ps[jj], vb[vt_off(kv, slot, kvh, d, j0 + jj)], a);
+      acc[i] = a;
+    }
+    __syncthreads();
   }
   float* op = o + ((int64_t)t * H + head) * HD;
-  for (int d = 0; d < HD; ++d) op[d] = acc[d] / l;
+#pragma unroll
+  for (int i = 0; i < DL; ++i) op[lane + i * 64] = acc[i] / l;
 }
 
 // ---------------------------------------------------------------- launchers
@@ -514,7 +539,7 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
                          const int32_t* h_cu, int H, hipStream_t s) {
   if (T_tokens <= 0) return;
   if constexpr (sizeof(T) == 4) {
-    dim3 grid((T_tokens + 63) / 64, H);
+    dim3 grid(T_tokens, H);
     if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H);
     else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H);
   } else {
@@ -558,7 +583,7 @@ void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, 
                         hipStream_t s) {
   if (B <= 0) return;
   if constexpr (sizeof(T) == 4) {
-    dim3 grid((B + 63) / 64, H);
+    dim3 grid(B, H);
     if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H);
     else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H);
   } else {

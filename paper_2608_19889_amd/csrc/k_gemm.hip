@@ -422,9 +422,64 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
   }
 }
 
+// ============================================================================
+// float32 check mode, up to 32 tokens (M <= MT): a wavefront per weight row, lanes
+// along K with 16-byte loads, compensated (Kahan) per-lane sums reduced across
+// the wavefront by shuffles.  K % 4 == 0.
+// ============================================================================
+template <int EPI, int MT>
+__global__ void __launch_bounds__(256) gemv_f32_kernel(const float* __restrict__ W, const float* __restrict__ X,
+                                                       int N, int M, int K, EpiArgs ep) {
+  const int lane = threadIdx.x & 63;
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;  // whole wavefronts only: no barrier follows
+  float acc[MT], comp[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc[t] = comp[t] = 0.f;
+  const float* wr = W + (int64_t)n * K;
+  for (int k = lane * 4; k < K; k += 256) {
+    const f32x4 w = *(const f32x4*)(wr + k);
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      if (t >= M) break;
+      const f32x4 x = *(const f32x4*)(X + (int64_t)t * K + k);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float y = fmaf(w[j], x[j], -comp[t]);
+        const float u = acc[t] + y;
+        comp[t] = (u - acc[t]) - y;
+        acc[t] = u;
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    if (t >= M) break;
+    const float v = wave_sum(acc[t]);
+    if (lane == 0) {
+      float* p = ep.out_f32 + (int64_t)t * ep.ldo + n;
+      if constexpr (EPI == EPI_RESID) *p += v;
+      else *p = v;
+    }
+  }
+}
+
 void launch_gemm_f32(const float* W, const float* X, int N, int M, int K, int epi, const EpiArgs& ep,
                      hipStream_t s) {
   if (M <= 0) return;
+  if (M <= 32 && K % 4 == 0) {
+    const dim3 g((N + 3) / 4);
+    const bool r = epi == EPI_RESID;
+    if (M <= 1) r ? klaunch(gemv_f32_kernel<EPI_RESID, 1>, g, dim3(256), 0, s, W, X, N, M, K, ep)
+                  : klaunch(gemv_f32_kernel<EPI_F32, 1>, g, dim3(256), 0, s, W, X, N, M, K, ep);
+    else if (M <= 4) r ? klaunch(gemv_f32_kernel<EPI_RESID, 4>, g, dim3(256), 0, s, W, X, N, M, K, ep)
+                       : klaunch(gemv_f32_kernel<EPI_F32, 4>, g, dim3(256), 0, s, W, X, N, M, K, ep);
+    else if (M <= 16) r ? klaunch(gemv_f32_kernel<EPI_RESID, 16>, g, dim3(256), 0, s, W, X, N, M, K, ep)
+                        : klaunch(gemv_f32_kernel<EPI_F32, 16>, g, dim3(256), 0, s, W, X, N, M, K, ep);
+    else r ? klaunch(gemv_f32_kernel<EPI_RESID, 32>, g, dim3(256), 0, s, W, X, N, M, K, ep)
+           : klaunch(gemv_f32_kernel<EPI_F32, 32>, g, dim3(256), 0, s, W, X, N, M, K, ep);
+    return;
+  }
   dim3 grid((N + 63) / 64, (M + 63) / 64);
   if (epi == EPI_RESID) klaunch(gemm_f32_kernel<EPI_RESID>, grid, dim3(256), 0, s, W, X, N, M, K, ep);
   else klaunch(gemm_f32_kernel<EPI_F32>, grid, dim3(256), 0, s, W, X, N, M, K, ep);
