@@ -245,6 +245,18 @@ def roofline_pass(m, generate, shape, esz, lens):
             a["flops"] += 4.0 * H * hd * ctx
         else:
             a["flops"] += 4.0 * H * hd * sq
+    # per-shape breakdown of the decode projections (stderr): (N, K) -> time, bandwidth
+    shapes = {}
+    for c, (d0, d1, d2), ms in recs:
+        if c != ax.T_GEMV:
+            continue
+        b = shapes.setdefault((d0, d2), {"ms": 0.0, "n": 0, "bytes": 0.0})
+        b["ms"] += ms
+        b["n"] += 1
+        b["bytes"] += d0 * d2 * esz + d1 * d2 * esz + d1 * d0 * 4
+    for (N, K), b in sorted(shapes.items(), key=lambda kv: -kv[1]["ms"]):
+        log(f"decode projection N={N} K={K}: {b['n']} launches, avg {1e3 * b['ms'] / b['n']:.2f} us, "
+            f"{b['bytes'] / (b['ms'] / 1e3) / 1e9:.0f} GB/s")
     kernels = {}
     for c, a in agg.items():
         hbm = c in (ax.T_GEMV, ax.T_ATTN_DECODE)
