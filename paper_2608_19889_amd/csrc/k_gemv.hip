@@ -43,10 +43,11 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
   const int M = a.M, lane = tid & 63, wave = tid >> 6;
   auto s_aux = [&](int row, int col) -> float& { return aux[row * (COLS + 1) + col]; };
   if constexpr (EPI == GV_RESID) {
-    for (int it = tid; it < ROWS * COLS; it += NT) {
-      const int row = it / COLS, col = it % COLS, n = n0 + row;
+    // features fastest: each token's outputs are contiguous in memory
+    for (int it = tid; it < ROWS * M; it += NT) {
+      const int row = it % ROWS, col = it / ROWS, n = n0 + row;
       float sq = 0.f;
-      if (col < M && n < a.N) {
+      if (n < a.N) {
         float* p = a.out_f32 + (int64_t)col * a.ldo + n;
         const float v = *p + total(row, col);
         *p = v;
@@ -63,10 +64,10 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
     }
   } else if constexpr (EPI == GV_SILU) {
     // each 32-row block: rows 0..15 gate, 16..31 the matching up rows
-    for (int it = tid; it < (ROWS / 2) * COLS; it += NT) {
-      const int fl = it / COLS, col = it % COLS;
-      if (col >= M) continue;
+    for (int it = tid; it < (ROWS / 2) * M; it += NT) {
+      const int fl = it % (ROWS / 2), col = it / (ROWS / 2);
       const int blk = fl / 16, f = fl % 16;
+      if (n0 + blk * 32 >= a.N) continue;  // N is a multiple of 32 (16 gate + 16 up rows)
       const float g = total(blk * 32 + f, col), u = total(blk * 32 + 16 + f, col);
       a.out_t[(int64_t)col * a.ldo + n0 / 2 + fl] = (bf16)(silu_g(g) * u);
     }
@@ -75,9 +76,8 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
     const int hd = a.kv.hd, half = hd / 2;
     const int head = n0 / hd, g0 = (n0 % hd) / 8;
     const int KVh = a.kv.kv_heads;
-    for (int it = tid; it < (ROWS / 2) * COLS; it += NT) {
-      const int pr = it / COLS, t = it % COLS;
-      if (t >= M) continue;
+    for (int it = tid; it < (ROWS / 2) * M; it += NT) {
+      const int pr = it % (ROWS / 2), t = it / (ROWS / 2);
       const int gl = pr / 4, i4 = pr % 4;
       const int i = (g0 + gl) * 4 + i4;  // rotation pair (i, i + hd/2) of this head
       float x1 = total(gl * 8 + i4, t), x2 = total(gl * 8 + 4 + i4, t);
@@ -101,10 +101,10 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
       }
     }
   } else {  // GV_HEAD
-    for (int it = tid; it < ROWS * COLS; it += NT) {
-      const int row = it / COLS, col = it % COLS, n = n0 + row;
+    for (int it = tid; it < ROWS * M; it += NT) {
+      const int row = it % ROWS, col = it / ROWS, n = n0 + row;
       float v = -INFINITY;
-      if (col < M && n < a.N) {
+      if (n < a.N) {
         v = total(row, col);
         if (a.out_f32) a.out_f32[(int64_t)col * a.ldo + n] = v;
       }
@@ -142,9 +142,6 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
   __shared__ float red[KS][RB * 16][COLS + 1];
   __shared__ float s_ss[NT];
   __shared__ float s_inv[64];
-  // epilogue scratch: only the residual (sums of squares) and head (argmax)
-  // epilogues use it; its size limits how many workgroups share a CU
-  __shared__ float s_aux[(EPI == GV_RESID || EPI == GV_HEAD) ? RB * 16 : 1][COLS + 1];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = blockIdx.x * ROWS;
@@ -307,53 +304,289 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
       if (col < M && n < a.N) a.part[((int64_t)blockIdx.y * M + col) * a.N + n] = total(row, col);
     }
   } else {
-    gv_epilogue<ROWS, COLS, NT, EPI>(a, n0, tid, (float*)s_aux, blockIdx.x, gridDim.x, total);
+    // the residual and head epilogues overwrite element (row, col) of their
+    // scratch only after the same thread has read total(row, col): the first
+    // wavefront's tile serves as that scratch
+    gv_epilogue<ROWS, COLS, NT, EPI>(a, n0, tid, &red[0][0][0], blockIdx.x, gridDim.x, total);
   }
 }
 
-// Epilogue of a split-K projection: total = the K splits' partial sums in
-// split order (deterministic), times the RMSNorm factor of the token, then
-// the projection's epilogue on tiles of EROWS features.
-template <int EROWS, int NB, bool NORM, int EPI>
-__global__ void __launch_bounds__(256) gemv_split_epilogue_kernel(GemvArgs a, int nsplit) {
-  constexpr int COLS = NB * 16, NT = 256, SSR = 16;
+// Projections of 17..64 tokens: the 4 wavefronts of a workgroup split the
+// output rows (16 * RB each) over the workgroup's whole K range and share the
+// token operand, which is staged through LDS in B-fragment lane order (a
+// wavefront reads 1 KB per fragment with consecutive 16-byte lanes, no bank
+// conflicts), double-buffered with one barrier per stage of U k-steps.  There
+// is no cross-wavefront reduction, so registers and LDS stay small enough for
+// several workgroups per CU (the weight stream needs many bytes in flight).
+// Same operands, K splitting (EPI == GV_PART) and epilogues as
+// gemv_fused_kernel.
+template <int RB, int NB, bool NORM, int EPI, int U>
+__global__ void __launch_bounds__(256) gemv_wide_kernel(GemvArgs a) {
+  constexpr int NT = 256, ROWS = 64 * RB, COLS = NB * 16;
+  constexpr int XCH = U * NB * 64;  // 16-byte token chunks per stage
+  static_assert(XCH % NT == 0, "stage must split evenly over the threads");
+  constexpr int XPT = XCH / NT;
+  constexpr int XS_FLOATS = 2 * XCH * 4, TOT_FLOATS = ROWS * (COLS + 1);
+  // token stages while streaming, then the finished tile for the epilogue
+  __shared__ float smem[XS_FLOATS > TOT_FLOATS ? XS_FLOATS : TOT_FLOATS];
   __shared__ float s_ss[NT];
   __shared__ float s_inv[64];
-  __shared__ float s_aux[(EROWS > 16 ? EROWS : 16) * (COLS + 1)];
-  const int tid = threadIdx.x, M = a.M;
-  const int n0 = blockIdx.x * EROWS;
+  bf16x8* xs = (bf16x8*)smem;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n0 = blockIdx.x * ROWS;
+  const int K = a.K, M = a.M;
+  const int klen = EPI == GV_PART ? ((K + gridDim.y - 1) / gridDim.y + 31) / 32 * 32 : K;
+  const int kb = EPI == GV_PART ? min(K, (int)blockIdx.y * klen) : 0;
+  const int nsteps = (min(K, kb + klen) - kb) / 32;  // k-steps of 32 (K is a multiple of 32)
+  const int nst = (nsteps + U - 1) / U;               // stages; the last may be partial
+  const int r16 = lane & 15;
+
+  // weights: this wavefront's row blocks (rows past N read row N-1, never stored)
+  const bf16* wrow[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    const int n = n0 + (wave * RB + r) * 16 + r16;
+    wrow[r] = a.W + wt_chunk(min(n, a.N - 1), lane >> 4, K);
+  }
+  // token chunks this thread stages: chunk q = (u * NB + c) * 64 + l holds
+  // lane l's B fragment of token block c at k-step u (token columns past M
+  // read token M-1)
+  const bf16* xsrc[XPT];
+  int xu[XPT];
+#pragma unroll
+  for (int i = 0; i < XPT; ++i) {
+    const int q = tid + i * NT, l = q & 63, c = (q >> 6) % NB;
+    xu[i] = (q >> 6) / NB;
+    xsrc[i] = a.X + (int64_t)min(c * 16 + (l & 15), M - 1) * K + (l >> 4) * 8;
+  }
+  auto kstep = [&](int j) { return kb + min(j, nsteps - 1) * 32; };  // clamped: every load is unconditional
+
+  constexpr int SSR = 16;
+  float ss_reg[SSR];
+  const int ss_slices = NORM ? min(NT / M, max(1, (a.ss_n + SSR - 1) / SSR)) : 1;
+  const int ss_t = tid % M, ss_sl = tid / M;
   if constexpr (NORM) {
-    // token t = tid % M, slice tid / M: partials j = slice (mod slices), 16
-    // independent loads per round
-    const int slices = NT / M, t = tid % M, sl = tid / M;
-    float v = 0.f;
-    if (sl < slices) {
-      for (int j0 = sl; j0 < a.ss_n; j0 += SSR * slices) {
-        float r[SSR];
+    if (wave * 64 < ss_slices * M) {
 #pragma unroll
-        for (int i = 0; i < SSR; ++i) r[i] = a.ss_in[(int64_t)min(j0 + i * slices, a.ss_n - 1) * M + t];
+      for (int i = 0; i < SSR; ++i) {
+        const int j = min(ss_sl + i * ss_slices, a.ss_n - 1);
+        ss_reg[i] = a.ss_in[(int64_t)j * M + ss_t];
+      }
+    } else {
 #pragma unroll
-        for (int i = 0; i < SSR; ++i)
-          if (j0 + i * slices < a.ss_n) v += r[i];
+      for (int i = 0; i < SSR; ++i) ss_reg[i] = 0.f;
+    }
+  }
+
+  f32x4 acc[RB][NB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int c = 0; c < NB; ++c) acc[r][c] = f32x4{};
+
+  bf16x8 xr[XPT];
+  bf16x8 wA[U][RB], wB[U][RB];
+  auto load_x = [&](int st) {
+#pragma unroll
+    for (int i = 0; i < XPT; ++i) xr[i] = *(const bf16x8*)(xsrc[i] + kstep(st * U + xu[i]));
+  };
+  auto store_x = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < XPT; ++i) xs[buf * XCH + tid + i * NT] = xr[i];
+  };
+  auto load_w = [&](bf16x8 (&w)[U][RB], int st) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int r = 0; r < RB; ++r) w[u][r] = *(const bf16x8*)(wrow[r] + (int64_t)(kstep(st * U + u) >> 5) * 512);
+  };
+  auto compute = [&](const bf16x8 (&w)[U][RB], int st) {
+    const bf16x8* xb = xs + (st & 1) * XCH + lane;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (st * U + u < nsteps) {  // workgroup-uniform: the last stage may be partial
+        bf16x8 xv[NB];
+#pragma unroll
+        for (int c = 0; c < NB; ++c) xv[c] = xb[(u * NB + c) * 64];
+#pragma unroll
+        for (int r = 0; r < RB; ++r)
+#pragma unroll
+          for (int c = 0; c < NB; ++c)
+            acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[u][r], xv[c], acc[r][c], 0, 0, 0);
       }
     }
-    s_ss[tid] = v;
+  };
+  // stage st: barrier (its tokens landed for every wavefront; the other
+  // buffer is no longer read), MFMAs, stage the tokens of st + 1, issue the
+  // loads of st + 2 into the weight registers just consumed
+  auto stage = [&](bf16x8 (&w)[U][RB], int st) {
     __syncthreads();
+    compute(w, st);
+    if (st + 1 < nst) store_x((st + 1) & 1);
+    if (st + 2 < nst) {
+      load_x(st + 2);
+      load_w(w, st + 2);
+    }
+  };
+  if (nst > 0) {
+    load_x(0);
+    load_w(wA, 0);
+    store_x(0);
+    if (nst > 1) {
+      load_x(1);
+      load_w(wB, 1);
+    }
+    for (int st = 0; st < nst; st += 2) {
+      stage(wA, st);
+      if (st + 1 < nst) stage(wB, st + 1);
+    }
+  }
+
+  // finished tile -> LDS (over the token stages): tot[row][col]
+  __syncthreads();
+  float* tot = smem;
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        tot[((wave * RB + r) * 16 + (lane >> 4) * 4 + i) * (COLS + 1) + c * 16 + r16] = acc[r][c][i];
+  if constexpr (NORM) {
+    float ss_part = 0.f;
+#pragma unroll
+    for (int i = 0; i < SSR; ++i)
+      if (ss_sl < ss_slices && ss_sl + i * ss_slices < a.ss_n) ss_part += ss_reg[i];
+    if (ss_sl < ss_slices) {
+      for (int j0 = ss_sl + SSR * ss_slices; j0 < a.ss_n; j0 += SSR * ss_slices) {
+        float v[SSR];
+#pragma unroll
+        for (int i = 0; i < SSR; ++i) v[i] = a.ss_in[(int64_t)min(j0 + i * ss_slices, a.ss_n - 1) * M + ss_t];
+#pragma unroll
+        for (int i = 0; i < SSR; ++i)
+          if (j0 + i * ss_slices < a.ss_n) ss_part += v[i];
+      }
+    }
+    s_ss[tid] = ss_part;
+  }
+  __syncthreads();
+  if constexpr (NORM) {
     if (tid < M) {
-      float tot = 0.f;
-      for (int j = 0; j < slices; ++j) tot += s_ss[j * M + tid];
-      s_inv[tid] = rsqrtf(tot / (float)a.K + a.eps);
+      float t = 0.f;
+      for (int sl = 0; sl < ss_slices; ++sl) t += s_ss[sl * M + tid];
+      s_inv[tid] = rsqrtf(t / (float)K + a.eps);
     }
     __syncthreads();
   }
   auto total = [&](int row, int col) {
-    const int n = min(n0 + row, a.N - 1), c = min(col, M - 1);
-    float sum = 0.f;
-    for (int sp = 0; sp < nsplit; ++sp) sum += a.part[((int64_t)sp * M + c) * a.N + n];
-    if constexpr (NORM) sum *= s_inv[c];
-    return sum;
+    float s = tot[row * (COLS + 1) + col];
+    if constexpr (NORM) s *= s_inv[col];
+    return s;
   };
-  gv_epilogue<EROWS, COLS, NT, EPI>(a, n0, tid, s_aux, blockIdx.x, gridDim.x, total);
+  if constexpr (EPI == GV_PART) {
+    // partial sums of this K split (already scaled by the token's RMSNorm
+    // factor when NORM): part[split][col][n0 + row]
+    for (int it = tid; it < ROWS * M; it += NT) {
+      const int row = it % ROWS, col = it / ROWS, n = n0 + row;
+      if (n < a.N) a.part[((int64_t)blockIdx.y * M + col) * a.N + n] = total(row, col);
+    }
+  } else {
+    // the residual and head epilogues overwrite element (row, col) of their
+    // scratch only after the same thread has read total(row, col): the tile
+    // itself serves as that scratch
+    gv_epilogue<ROWS, COLS, NT, EPI>(a, n0, tid, tot, blockIdx.x, gridDim.x, total);
+  }
+}
+
+// Epilogue of a split-K projection: total = the K splits' partial sums in
+// split order (deterministic; a normalized projection's partials already
+// carry the token's RMSNorm factor), then the projection's epilogue on tiles
+// of EROWS features.
+template <int EROWS, int NB, int EPI>
+__global__ void __launch_bounds__(256) gemv_split_epilogue_kernel(GemvArgs a, int nsplit) {
+  constexpr int COLS = NB * 16, NT = 256;
+  static_assert(EROWS >= 16, "the tile doubles as the epilogue scratch");
+  // the tile's totals; the residual and head epilogues overwrite element
+  // (row, col) only after the same thread has read it, so it is also their
+  // scratch
+  __shared__ float s_tot[EROWS * (COLS + 1)];
+  const int tid = threadIdx.x, M = a.M;
+  const int n0 = blockIdx.x * EROWS;
+  // staged rows-fastest (the partials are [split][token][n]: coalesced), the
+  // splits in order; 4 splits' loads in flight per round
+  constexpr int IT = (EROWS * COLS + NT - 1) / NT;
+  const int items = EROWS * M;
+  float sum[IT];
+#pragma unroll
+  for (int j = 0; j < IT; ++j) sum[j] = 0.f;
+  for (int sp0 = 0; sp0 < nsplit; sp0 += 4) {
+    float v[IT][4];
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const int it = min(tid + j * NT, items - 1);
+      const int n = min(n0 + it % EROWS, a.N - 1), c = it / EROWS;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[j][q] = a.part[((int64_t)min(sp0 + q, nsplit - 1) * M + c) * a.N + n];
+    }
+#pragma unroll
+    for (int j = 0; j < IT; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (sp0 + q < nsplit) sum[j] += v[j][q];
+  }
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const int it = tid + j * NT;
+    if (it < items) s_tot[(it % EROWS) * (COLS + 1) + it / EROWS] = sum[j];
+  }
+  __syncthreads();
+  auto total = [&](int row, int col) { return s_tot[row * (COLS + 1) + col]; };
+  gv_epilogue<EROWS, COLS, NT, EPI>(a, n0, tid, s_tot, blockIdx.x, gridDim.x, total);
+}
+
+// Residual epilogue of a split-K projection by token rows: workgroup
+// (chunk, t) owns features [1024 chunk, 1024 chunk + 1024) of token t, 4 per
+// thread: x[t][n] += the splits' partials (split order), xg = bf16(x *
+// g_next), and one sum of squares of the new x per (chunk, token).  Few
+// partials per token keep the next normalized projection's prologue short.
+// N must be a multiple of 4 (float4 / 4 x bf16 accesses).
+__global__ void __launch_bounds__(256) gemv_split_resid_kernel(GemvArgs a, int nsplit) {
+  const int t = blockIdx.y, tid = threadIdx.x, M = a.M;
+  const int n = min(blockIdx.x * GV_RESID_ROWS + tid * 4, a.N - 4);  // clamped: loads are unconditional
+  const bool own = blockIdx.x * GV_RESID_ROWS + tid * 4 < a.N;
+  float4 s = {0.f, 0.f, 0.f, 0.f};
+  for (int sp0 = 0; sp0 < nsplit; sp0 += 4) {
+    float4 v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = *(const float4*)(a.part + ((int64_t)min(sp0 + q, nsplit - 1) * M + t) * a.N + n);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (sp0 + q < nsplit) {
+        s.x += v[q].x; s.y += v[q].y; s.z += v[q].z; s.w += v[q].w;
+      }
+  }
+  float* xp = a.out_f32 + (int64_t)t * a.ldo + n;
+  const float4 x0 = *(const float4*)xp;
+  const bf16x4 g = *(const bf16x4*)(a.gain_next + n);
+  const float4 x = {x0.x + s.x, x0.y + s.y, x0.z + s.z, x0.w + s.w};
+  float sq = 0.f;
+  if (own) {
+    *(float4*)xp = x;
+    bf16x4 o;
+    o[0] = (bf16)(x.x * (float)g[0]);
+    o[1] = (bf16)(x.y * (float)g[1]);
+    o[2] = (bf16)(x.z * (float)g[2]);
+    o[3] = (bf16)(x.w * (float)g[3]);
+    *(bf16x4*)(a.xg_out + (int64_t)t * a.ldo + n) = o;
+    sq = x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) sq += __shfl_xor(sq, m, 64);
+  __shared__ float s_w[4];
+  if ((tid & 63) == 0) s_w[tid >> 6] = sq;
+  __syncthreads();
+  if (tid == 0) a.ss_out[(int64_t)blockIdx.x * M + t] = (s_w[0] + s_w[1]) + (s_w[2] + s_w[3]);
 }
 
 // next[t] = index of the largest partial maximum (lowest index on ties);
@@ -436,19 +669,30 @@ GvShape gemv_shape(int N, int K, int M, int epi) {
     if (N / 16 < 192) return {8, 16, 2, 1, 0};
     return K >= 8192 ? GvShape{16, 8, 4, 1, 0} : GvShape{16, 16, 2, 1, 0};
   }
+  // 17..64 tokens: the row-splitting kernel (gemv_wide_kernel), whose token
+  // fragments are reused by 4 or 8 row blocks per workgroup.  3 token blocks
+  // need 4 k-steps per stage (the stage is split evenly over 256 threads).
+  // Shapes and split counts from timing the candidates on weights streamed
+  // from HBM (7B- and 32B-shaped layers at 32 and 64 tokens).
   if (epi == GV_RESID || epi == GV_ROPE) {
-    // 17..64 tokens, narrow projections: 64-row tiles, so that each token
-    // fragment is reused by 4 row blocks (16-row tiles re-read the token
-    // operand, 4x the weight bytes at 64 tokens, from L2), and K split over
-    // workgroups towards >= 224 of them; a second kernel sums the splits and
-    // runs the epilogue on 16-row tiles.
-    const int blocks = (N + 63) / 64;
-    const int ksplit = std::max(1, std::min(8, (224 + blocks - 1) / blocks));
-    return {64, 4, 2, ksplit, 16};
+    // narrow projections: K split over workgroups, then a second kernel sums
+    // the splits and runs the epilogue (the residual one by token rows of
+    // 1024 features, the others on 16-row tiles).  Long K: 128-row tiles
+    // towards ~252 workgroups; short K: 64-row tiles towards ~504 (33..64
+    // tokens) or ~1008 (17..32 tokens) workgroups, which keeps enough weight
+    // bytes in flight per CU
+    const int erows = epi == GV_RESID && N % 4 == 0 ? GV_RESID_ROWS : 16;
+    const int rb = K >= 8192 ? 2 : 1;
+    const int blocks = (N + 64 * rb - 1) / (64 * rb);
+    const int target = rb == 2 ? 252 : nb >= 3 ? 504 : 1008;
+    const int ksplit = std::max(2, std::min(12, (target + blocks / 2) / blocks));
+    return {64 * rb, 4, rb == 2 || nb >= 3 ? 4 : 2, ksplit, erows, 1};
   }
-  if (nb == 2) return {64, 2, 2, 1, 0};  // gate/up, head
-  if (epi == GV_SILU) return {64, 4, 2, 1, 0};
-  return {32, 4, 2, 1, 0};  // head
+  if (epi == GV_SILU) {
+    if (nb == 2) return {128, 4, 2, 1, 0, 1};
+    return {64, 4, nb == 3 ? 4 : 2, 1, 0, 1};
+  }
+  return {128, 4, nb == 4 ? 2 : 4, 1, 0, 1};  // head
 }
 
 int gemv_rows(int N, int K, int M, int epi) {
@@ -467,33 +711,43 @@ static bool gv(const GemvArgs& a, hipStream_t s) {
   return true;
 }
 
-// every shape gemv_shape can return, per (epilogue, normalization, token blocks)
+template <int RB, int U, int NB, bool NORM, int EPI>
+static bool gvw(const GemvArgs& a, hipStream_t s) {
+  klaunch(gemv_wide_kernel<RB, NB, NORM, EPI, U>, dim3((a.N + 64 * RB - 1) / (64 * RB)), dim3(256), 0, s, a);
+  return true;
+}
+
+// every unsplit shape gemv_shape can return, per (epilogue, normalization,
+// token blocks)
 template <int EPI, bool NORM>
 static bool gv_dispatch(const GemvArgs& a, const GvShape& sh, int nb, hipStream_t s) {
 #define AXON_GV(R, KS_, U_, NB_) \
-  if (sh.rows == R && sh.ks == KS_ && sh.u == U_ && nb == NB_) return gv<R, KS_, U_, NB_, NORM, EPI>(a, s);
+  if (!sh.wide && sh.rows == R && sh.ks == KS_ && sh.u == U_ && nb == NB_) return gv<R, KS_, U_, NB_, NORM, EPI>(a, s);
+#define AXON_GVW(R, U_, NB_) \
+  if (sh.wide && sh.rows == R && sh.u == U_ && nb == NB_) return gvw<R / 64, U_, NB_, NORM, EPI>(a, s);
   if constexpr (EPI == GV_SILU) {
-    AXON_GV(32, 4, 4, 1) AXON_GV(64, 2, 2, 2) AXON_GV(64, 4, 2, 3) AXON_GV(64, 4, 2, 4)
+    AXON_GV(32, 4, 4, 1) AXON_GVW(128, 2, 2) AXON_GVW(64, 4, 3) AXON_GVW(64, 2, 4)
   } else if constexpr (EPI == GV_HEAD) {
-    AXON_GV(32, 8, 2, 1) AXON_GV(64, 8, 2, 1) AXON_GV(64, 2, 2, 2) AXON_GV(32, 4, 2, 3) AXON_GV(32, 4, 2, 4)
-  } else if constexpr (EPI == GV_ROPE) {
-    AXON_GV(8, 16, 2, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 2, 1)
+    AXON_GV(32, 8, 2, 1) AXON_GV(64, 8, 2, 1) AXON_GVW(128, 4, 2) AXON_GVW(128, 4, 3) AXON_GVW(128, 2, 4)
   } else {
     AXON_GV(8, 16, 2, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 2, 1)
   }
+#undef AXON_GVW
 #undef AXON_GV
   return false;
 }
 
-// split K: partial sums (grid N/rows x ksplit) then the epilogue kernel; a
-// timed launch starts its events with the first kernel and stops with the
-// second
-template <int NB, bool NORM, int EPI>
+// split K: partial sums (grid N/rows x ksplit, normalized when NORM) then the
+// epilogue kernel; a timed launch starts its events with the first kernel
+// and stops with the second
+template <int RB, int U, int NB, bool NORM, int EPI>
 static bool gv_split(const GemvArgs& a, const GvShape& sh, hipStream_t s) {
-  if (sh.rows != 64 || sh.ks != 4 || sh.u != 2 || sh.erows != 16 || !a.part) return false;
-  auto k1 = gemv_fused_kernel<64, 4, NB, false, GV_PART, 2>;
-  auto k2 = gemv_split_epilogue_kernel<16, NB, NORM, EPI>;
-  const dim3 g1((a.N + 63) / 64, sh.ksplit), g2((a.N + 15) / 16);
+  auto k1 = gemv_wide_kernel<RB, NB, NORM, GV_PART, U>;
+  const bool rows = EPI == GV_RESID && sh.erows == GV_RESID_ROWS;
+  if (!rows && sh.erows != 16) return false;
+  auto k2 = rows ? gemv_split_resid_kernel : gemv_split_epilogue_kernel<16, NB, EPI>;
+  const dim3 g1((a.N + 64 * RB - 1) / (64 * RB), sh.ksplit);
+  const dim3 g2 = rows ? dim3((a.N + GV_RESID_ROWS - 1) / GV_RESID_ROWS, a.M) : dim3((a.N + 15) / 16);
   const TimingSlot t = g_timing_slot;
   g_timing_slot = TimingSlot{};
   if (t.start) {
@@ -508,12 +762,13 @@ static bool gv_split(const GemvArgs& a, const GvShape& sh, hipStream_t s) {
 
 template <int EPI, bool NORM>
 static bool gv_split_nb(const GemvArgs& a, const GvShape& sh, int nb, hipStream_t s) {
-  switch (nb) {
-    case 2: return gv_split<2, NORM, EPI>(a, sh, s);
-    case 3: return gv_split<3, NORM, EPI>(a, sh, s);
-    case 4: return gv_split<4, NORM, EPI>(a, sh, s);
-    default: return false;
-  }
+  if (!sh.wide || !a.part) return false;
+#define AXON_GVS(R, U_, NB_) \
+  if (sh.rows == R && sh.u == U_ && nb == NB_) return gv_split<R / 64, U_, NB_, NORM, EPI>(a, sh, s);
+  AXON_GVS(64, 2, 2) AXON_GVS(64, 4, 3) AXON_GVS(64, 4, 4)
+  AXON_GVS(128, 4, 2) AXON_GVS(128, 4, 3) AXON_GVS(128, 4, 4)
+#undef AXON_GVS
+  return false;
 }
 
 bool launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s) {

@@ -105,11 +105,13 @@ struct GemvArgs {
   // (gemv_workspace_floats), owned by the caller
   float* part;
 };
-constexpr int GEMV_MAX_M = 64;  // token columns one fused projection handles
+constexpr int GEMV_MAX_M = 64;      // token columns one fused projection handles
+constexpr int GV_RESID_ROWS = 1024;  // features per workgroup of the split-K residual epilogue
 struct GvShape {
   int rows, ks, u;  // output rows per workgroup, wavefronts splitting K, k-steps of 32 per stage
   int ksplit;       // workgroups splitting K (1: fused epilogue; else partials + an epilogue kernel)
   int erows;        // rows per workgroup of the epilogue kernel (ksplit > 1)
+  int wide = 0;     // 1: gemv_wide_kernel (4 wavefronts splitting the rows, ks unused)
 };
 // floats of GemvArgs::part a launch of this shape needs (0 when unsplit)
 int64_t gemv_workspace_floats(int N, int K, int M, int epi);
