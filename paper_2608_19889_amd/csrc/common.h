@@ -71,13 +71,24 @@ struct KVView {
 AXON_DEV int64_t kv_page(const KVView& c, int slot, int pos) {
   return c.bt ? (int64_t)c.bt[(int64_t)slot * c.bt_stride + pos / c.ps] : (int64_t)slot;
 }
-// element offset of K[pos][d=0] for (slot, kv head)
-AXON_DEV int64_t k_off(const KVView& c, int slot, int kvh, int pos) {
-  return ((kv_page(c, slot, pos) * c.kv_heads + kvh) * c.ps + pos % c.ps) * (int64_t)c.hd;
+// Within a page, each kv head owns a slab of ps x hd elements, cut into
+// blocks of 16 positions (16 hd contiguous elements each; ps is a multiple of
+// 16).  K block: [hd / 8][16 positions][8 dims]: the 8-dim chunk of a
+// position is 16 contiguous bytes and a chunk's 16 positions 256 bytes, so
+// the 16-position x 32-dim MFMA fragment of a key block is one contiguous
+// 1 KB read in lane order.  V block: [hd][16 positions], V^T of the block:
+// 4 consecutive positions of a dimension are 8 contiguous bytes, 16 dims x 16
+// positions one contiguous 512-byte read.
+AXON_DEV int64_t kv_block(const KVView& c, int slot, int kvh, int pos) {  // first element of pos's block
+  return ((kv_page(c, slot, pos) * c.kv_heads + kvh) * c.ps + (pos % c.ps & ~15)) * (int64_t)c.hd;
 }
-// element offset of V^T[d][pos] for (slot, kv head)
-AXON_DEV int64_t vt_off(const KVView& c, int slot, int kvh, int d, int pos) {
-  return ((kv_page(c, slot, pos) * c.kv_heads + kvh) * (int64_t)c.hd + d) * c.ps + pos % c.ps;
+// element offset of K[pos][d] for (slot, kv head)
+AXON_DEV int64_t k_el(const KVView& c, int slot, int kvh, int pos, int d) {
+  return kv_block(c, slot, kvh, pos) + (d >> 3) * 128 + (pos & 15) * 8 + (d & 7);
+}
+// element offset of V[pos][d] for (slot, kv head)
+AXON_DEV int64_t v_el(const KVView& c, int slot, int kvh, int pos, int d) {
+  return kv_block(c, slot, kvh, pos) + d * 16 + (pos & 15);
 }
 
 // Fragment-tiled storage of a bf16 weight matrix W [N][K] (K % 32 == 0).  Rows

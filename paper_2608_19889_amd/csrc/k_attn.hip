@@ -113,7 +113,8 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
       const int r = p / KCH, c = pswz<KCH>(r, p % KCH);  // pswz is its own inverse
       const int key = min(j0 + r, S - 1);                 // in [j0, j0 + 64): j0 < S
       const int64_t page = pg[(key - j0) >> 4];
-      const bf16* src = kb + ((page * kv.kv_heads + kvh) * kv.ps + key % kv.ps) * HD + c * 8;
+      const int kp = key % kv.ps;
+      const bf16* src = kb + ((page * kv.kv_heads + kvh) * kv.ps + (kp & ~15)) * HD + c * 128 + (kp & 15) * 8;
       __builtin_amdgcn_global_load_lds((const void*)src,
                                        (__attribute__((address_space(3))) void*)(lds + b * BUF + (i * 4 + wave) * 64),
                                        16, 0, 0);
@@ -124,7 +125,8 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
       const int d = p / VCH, c = pswz<VCH>(d, p % VCH);
       const int key = min(j0 + c * 8, (S - 1) & ~7);  // 8 keys of one 16-key group, in [j0, j0 + 64)
       const int64_t page = pg[(key - j0) >> 4];
-      const bf16* src = vb + ((page * kv.kv_heads + kvh) * HD + d) * (int64_t)kv.ps + key % kv.ps;
+      const int kp = key % kv.ps;
+      const bf16* src = vb + ((page * kv.kv_heads + kvh) * kv.ps + (kp & ~15)) * HD + d * 16 + (kp & 15);
       __builtin_amdgcn_global_load_lds(
           (const void*)src, (__attribute__((address_space(3))) void*)(lds + b * BUF + KT + (i * 4 + wave) * 64), 16,
           0, 0);
@@ -314,30 +316,31 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
   // (a per-lane load of the page table, on which the K/V addresses depend,
   // would wait for every load in flight).  Keys past the context may have no
   // page: never dereferenced.
-  const int64_t vrow = kv.ps;  // V^T row stride (positions per page)
   auto load = [&](Frag& f, int j0) {
-    int64_t kbase[2], vbase[2];
+    int64_t kbase[2];
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
       const int hs = min(j0 + blk * 16, (s1 - 1) & ~15);  // a valid 16-key group
       const int64_t pg = kv_page_uniform(kv, b, hs);
       const int off = (j0 + blk * 16) - hs + hs % kv.ps;  // in-page position of key j0 + blk*16
-      kbase[blk] = ((pg * kv.kv_heads + kvh) * kv.ps + off) * HD;
-      vbase[blk] = (pg * kv.kv_heads + kvh) * (int64_t)HD * kv.ps + off;
+      kbase[blk] = ((pg * kv.kv_heads + kvh) * kv.ps + off) * HD;  // the key block (off % 16 == 0)
     }
+    // K fragment (key col, dims 32k + 8gq ..): 16 bytes at lane * 16 of the
+    // block's 1 KB run k; V^T fragment (dim 16d + col, keys 4gq ..): 8 bytes
+    // of the block's 512-byte run d
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
       const bool ok = j0 + blk * 16 + col < s1;
-      const bf16* kp = kb + kbase[blk] + col * HD + gq * 8;
+      const bf16* kp = kb + kbase[blk] + lane * 8;
 #pragma unroll
-      for (int k = 0; k < HD / 32; ++k) f.k[blk][k] = ok ? *(const bf16x8*)(kp + k * 32) : z8;
+      for (int k = 0; k < HD / 32; ++k) f.k[blk][k] = ok ? *(const bf16x8*)(kp + k * 512) : z8;
     }
     const bool oka = j0 + gq * 4 < s1, okb = j0 + 16 + gq * 4 < s1;
 #pragma unroll
     for (int d = 0; d < HD / 16; ++d) {
-      const int dd = d * 16 + col;
-      f.vlo[d] = oka ? *(const bf16x4*)(vb + vbase[0] + gq * 4 + dd * vrow) : z4;
-      f.vhi[d] = okb ? *(const bf16x4*)(vb + vbase[1] + gq * 4 + dd * vrow) : z4;
+      const int64_t vo = (d * 16 + col) * 16 + gq * 4;
+      f.vlo[d] = oka ? *(const bf16x4*)(vb + kbase[0] + vo) : z4;
+      f.vhi[d] = okb ? *(const bf16x4*)(vb + kbase[1] + vo) : z4;
     }
   };
   // scores, online softmax update and P V for the 32 keys starting at j0
@@ -499,10 +502,10 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ 
     const int j = j0 + lane;
     float sj = -INFINITY;
     if (j <= pos) {
-      const float* kp = kb + k_off(kv, slot, kvh, j);
+      const float* kp = kb + k_el(kv, slot, kvh, j, 0);  // 8-dim chunks 128 elements apart
       float dot = 0.f;
       for (int d = 0; d < HD; d += 4) {
-        const f32x4 kv4 = *(const f32x4*)(kp + d);
+        const f32x4 kv4 = *(const f32x4*)(kp + (d >> 3) * 128 + (d & 7));
         dot = fmaf(qs[d], kv4[0], dot);
         dot = fmaf(qs[d + 1], kv4[1], dot);
         dot = fmaf(qs[d + 2], kv4[2], dot);
@@ -522,7 +525,7 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ 
     for (int i = 0; i < DL; ++i) {
       const int d = lane + i * 64;
       float a = acc[i] * alpha;
-      for (int jj = 0; jj < nj; ++jj) a = fmaf(ps[jj], vb[vt_off(kv, slot, kvh, d, j0 + jj)], a);
+      for (int jj = 0; jj < nj; ++jj) a = fmaf(ps[jj], vb[v_el(kv, slot, kvh, j0 + jj, d)], a);
       acc[i] = a;
     }
     __syncthreads();

@@ -89,15 +89,20 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
       if (head < a.H + KVh) {
         const float cs = a.cos_t[(int64_t)pos * half + i], sn = a.sin_t[(int64_t)pos * half + i];
         const float y1 = x1 * cs - x2 * sn, y2 = x2 * cs + x1 * sn;
-        bf16* dst = head < a.H ? a.q_out + ((int64_t)t * a.H + head) * hd
-                               : (bf16*)a.kv.k + k_off(a.kv, t, head - a.H, pos);
-        dst[i] = (bf16)y1;
-        dst[i + half] = (bf16)y2;
+        if (head < a.H) {
+          bf16* dst = a.q_out + ((int64_t)t * a.H + head) * hd;
+          dst[i] = (bf16)y1;
+          dst[i + half] = (bf16)y2;
+        } else {
+          bf16* kc = (bf16*)a.kv.k;
+          kc[k_el(a.kv, t, head - a.H, pos, i)] = (bf16)y1;
+          kc[k_el(a.kv, t, head - a.H, pos, i + half)] = (bf16)y2;
+        }
       } else {
         const int kvh = head - a.H - KVh;
-        bf16* vt = (bf16*)a.kv.v;
-        vt[vt_off(a.kv, t, kvh, i, pos)] = (bf16)x1;
-        vt[vt_off(a.kv, t, kvh, i + half, pos)] = (bf16)x2;
+        bf16* vc = (bf16*)a.kv.v;
+        vc[v_el(a.kv, t, kvh, pos, i)] = (bf16)x1;
+        vc[v_el(a.kv, t, kvh, pos, i + half)] = (bf16)x2;
       }
     }
   } else {  // GV_HEAD

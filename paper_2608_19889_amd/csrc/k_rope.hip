@@ -65,13 +65,15 @@ __global__ void __launch_bounds__(256) rope_kv_kernel(const float* __restrict__ 
       const float x1 = val(t, i), x2 = val(t, i + HALF);
       const float c = cos_t[(int64_t)pos * HALF + i], s = sin_t[(int64_t)pos * HALF + i];
       const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
-      T* dst;
-      if (head < H)
-        dst = q_out + ((int64_t)t * H + head) * HD;
-      else
-        dst = (T*)kv.k + k_off(kv, slot, head - H, pos);
-      dst[i] = from_f32<T>(y1);
-      dst[i + HALF] = from_f32<T>(y2);
+      if (head < H) {
+        T* dst = q_out + ((int64_t)t * H + head) * HD;
+        dst[i] = from_f32<T>(y1);
+        dst[i + HALF] = from_f32<T>(y2);
+      } else {
+        T* kc = (T*)kv.k;
+        kc[k_el(kv, slot, head - H, pos, i)] = from_f32<T>(y1);
+        kc[k_el(kv, slot, head - H, pos, i + HALF)] = from_f32<T>(y2);
+      }
     }
   } else {
     const int kvh = head - H - KVh;
@@ -86,7 +88,7 @@ __global__ void __launch_bounds__(256) rope_kv_kernel(const float* __restrict__ 
       if (t >= T_tokens) continue;
       int slot, pos;
       token_slot_pos(t, nseq, cu, len, slot, pos);
-      ((T*)kv.v)[vt_off(kv, slot, kvh, d, pos)] = from_f32<T>(vt[tt][d]);
+      ((T*)kv.v)[v_el(kv, slot, kvh, pos, d)] = from_f32<T>(vt[tt][d]);
     }
   }
 }
