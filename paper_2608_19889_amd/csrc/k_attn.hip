@@ -29,6 +29,17 @@ AXON_DEV int64_t kv_page_uniform(const KVView& c, int slot, int pos) {
   const cptr bt = (cptr)(uintptr_t)c.bt;
   return bt[__builtin_amdgcn_readfirstlane(slot * c.bt_stride + pos / c.ps)];
 }
+// The same with the cache kind fixed at compile time (no branch on bt).
+template <bool PAGED>
+AXON_DEV int64_t kv_page_of(const KVView& c, int slot, int pos) {
+  if constexpr (!PAGED) {
+    return slot;
+  } else {
+    typedef const __attribute__((address_space(4))) int32_t* cptr;
+    const cptr bt = (cptr)(uintptr_t)c.bt;
+    return bt[__builtin_amdgcn_readfirstlane(slot * c.bt_stride + pos / c.ps)];
+  }
+}
 
 // ============================================================================
 // Prefill (bf16): a workgroup = 4 wavefronts x QB blocks of 32 queries of one
@@ -271,7 +282,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
 // partial and the combine kernel merges them.
 // ============================================================================
 
-template <int HD, int DNW>
+template <int HD, int DNW, bool PAGED>
 __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* __restrict__ q, KVView kv,
                                                                     bf16* __restrict__ o, float* __restrict__ part,
                                                                     int H, const int32_t* __restrict__ len,
@@ -291,12 +302,14 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
   float* sl = dyn + DNW * 16;      // [DNW][16]
   float* so = dyn + 2 * DNW * 16;  // [DNW][group][HD]
 
+  // every load below is unconditional (a load under a lane condition makes
+  // the compiler wait for all loads in flight where the branches join):
+  // head columns past the group read the group's last head (never stored)
   bf16x8 qf[HD / 32];
   {
-    const bf16x8 z = {};
-    const bf16* qp = q + ((int64_t)b * H + kvh * group + col) * HD + gq * 8;
+    const bf16* qp = q + ((int64_t)b * H + kvh * group + min(col, group - 1)) * HD + gq * 8;
 #pragma unroll
-    for (int k = 0; k < HD / 32; ++k) qf[k] = col < group ? *(const bf16x8*)(qp + k * 32) : z;
+    for (int k = 0; k < HD / 32; ++k) qf[k] = *(const bf16x8*)(qp + k * 32);
   }
   f32x4 acc[HD / 16];
 #pragma unroll
@@ -304,43 +317,38 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
   float m_run = -INFINITY, l_run = 0.f;
   const bf16* kb = (const bf16*)kv.k;
   const bf16* vb = (const bf16*)kv.v;
-  const bf16x8 z8 = {};
-  const bf16x4 z4 = {};
   struct Frag {
     bf16x8 k[2][HD / 32];
     bf16x4 vlo[HD / 16], vhi[HD / 16];
   };
-  // issue the K and V^T loads of the 32 keys starting at j0
-  // A 16-key half lies in one page (page sizes are multiples of 16, chunks
-  // start at multiples of 32): its page is looked up once, with a scalar load
-  // (a per-lane load of the page table, on which the K/V addresses depend,
-  // would wait for every load in flight).  Keys past the context may have no
-  // page: never dereferenced.
+  // issue the K and V^T loads of the 32 keys starting at j0, as two 16-key
+  // blocks.  A block's page is looked up once, with a scalar load (a per-lane
+  // load of the page table, on which the K/V addresses depend, would wait for
+  // every load in flight).  A block at or past the context end reads the last
+  // block of the context instead: keys past the context get probability 0
+  // (their scores are masked), and the cached values they read are finite.
   auto load = [&](Frag& f, int j0) {
     int64_t kbase[2];
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
-      const int hs = min(j0 + blk * 16, (s1 - 1) & ~15);  // a valid 16-key group
-      const int64_t pg = kv_page_uniform(kv, b, hs);
-      const int off = (j0 + blk * 16) - hs + hs % kv.ps;  // in-page position of key j0 + blk*16
-      kbase[blk] = ((pg * kv.kv_heads + kvh) * kv.ps + off) * HD;  // the key block (off % 16 == 0)
+      const int hs = min(j0 + blk * 16, (s1 - 1) & ~15);  // a 16-key block of the context
+      const int64_t pg = kv_page_of<PAGED>(kv, b, hs);
+      kbase[blk] = ((pg * kv.kv_heads + kvh) * kv.ps + hs % kv.ps) * HD;
     }
     // K fragment (key col, dims 32k + 8gq ..): 16 bytes at lane * 16 of the
     // block's 1 KB run k; V^T fragment (dim 16d + col, keys 4gq ..): 8 bytes
     // of the block's 512-byte run d
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
-      const bool ok = j0 + blk * 16 + col < s1;
       const bf16* kp = kb + kbase[blk] + lane * 8;
 #pragma unroll
-      for (int k = 0; k < HD / 32; ++k) f.k[blk][k] = ok ? *(const bf16x8*)(kp + k * 512) : z8;
+      for (int k = 0; k < HD / 32; ++k) f.k[blk][k] = *(const bf16x8*)(kp + k * 512);
     }
-    const bool oka = j0 + gq * 4 < s1, okb = j0 + 16 + gq * 4 < s1;
 #pragma unroll
     for (int d = 0; d < HD / 16; ++d) {
       const int64_t vo = (d * 16 + col) * 16 + gq * 4;
-      f.vlo[d] = oka ? *(const bf16x4*)(vb + kbase[0] + vo) : z4;
-      f.vhi[d] = okb ? *(const bf16x4*)(vb + kbase[1] + vo) : z4;
+      f.vlo[d] = *(const bf16x4*)(vb + kbase[0] + vo);
+      f.vhi[d] = *(const bf16x4*)(vb + kbase[1] + vo);
     }
   };
   // scores, online softmax update and P V for the 32 keys starting at j0
@@ -392,19 +400,24 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
   // DNW)*64, ...; two chunks are in flight: the next but one is loaded into
   // a chunk's registers as soon as that chunk has been consumed
   auto chunk = [&](int i) { return s0 + wave * 64 + (i >> 1) * (DNW * 64) + (i & 1) * 32; };
-  {
+  // The loop body is one basic block: a load under a branch would be waited
+  // for where the branch joins, or moved next to its use.  A chunk at or past
+  // the context end is computed anyway: its keys are masked (probability 0;
+  // the running maximum is already finite from the chunk before it) and its
+  // loads read the clamped block.
+  if (chunk(0) < s1) {  // wave-uniform
     Frag fa, fb;
+    load(fa, chunk(0));
+    load(fb, chunk(1));
     int i = 0;
-    if (chunk(0) < s1) load(fa, chunk(0));
-    if (chunk(1) < s1) load(fb, chunk(1));
-    while (chunk(i) < s1) {
+    for (; chunk(i + 2) < s1; i += 2) {  // a chunk pair follows this one
       step(fa, chunk(i));
-      if (chunk(i + 2) < s1) load(fa, chunk(i + 2));
-      if (chunk(i + 1) >= s1) break;
+      load(fa, chunk(i + 2));
       step(fb, chunk(i + 1));
-      if (chunk(i + 3) < s1) load(fb, chunk(i + 3));
-      i += 2;
+      load(fb, chunk(i + 3));
     }
+    step(fa, chunk(i));  // the last pair: chunk(i) < s1
+    step(fb, chunk(i + 1));
   }
   // per-wave statistics: m uniform over the 4 lane groups of a column; l summed
   l_run += __shfl_xor(l_run, 16, 64);
@@ -576,8 +589,11 @@ static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int B,
                           int nsplit, int split_len, hipStream_t s) {
   const int group = H / kv.kv_heads;
   const size_t lds = (size_t)(2 * NW * 16 + NW * group * HD) * sizeof(float);
-  attn_decode_bf16_kernel<HD, NW><<<dim3(nsplit, kv.kv_heads, B), NW * 64, lds, s>>>(q, kv, o, part, H, len,
-                                                                                      split_len);
+  const dim3 grid(nsplit, kv.kv_heads, B);
+  if (kv.bt)
+    attn_decode_bf16_kernel<HD, NW, true><<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len);
+  else
+    attn_decode_bf16_kernel<HD, NW, false><<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len);
   if (nsplit > 1) attn_combine_kernel<HD><<<dim3(H, B), HD, 0, s>>>(part, o, H, len, nsplit, split_len);
 }
 
