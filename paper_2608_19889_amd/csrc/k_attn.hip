@@ -274,15 +274,15 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
 // ============================================================================
 // Decode (bf16): one query per slot.  Workgroup = (key split, kv head, slot)
 // with DNW wavefronts; the group's query heads are the columns of
-// v_mfma_f32_16x16x32_bf16 (up to 16 heads per group); each wavefront takes 64
-// keys per iteration as two 32-key chunks whose K and V^T loads go straight
-// from HBM to registers, one chunk ahead of the one being computed.  The
+// v_mfma_f32_16x16x32_bf16 (up to 16 heads per group); the wavefronts take
+// the split's 32-key chunks in turn, with K and V^T loaded straight from HBM
+// into registers, several chunks in flight per wavefront.  The
 // wavefronts' (max, sum, o) are merged in LDS; with one split the normalized
 // output is written directly, otherwise every split stores an unnormalized
 // partial and the combine kernel merges them.
 // ============================================================================
 
-template <int HD, int DNW, bool PAGED>
+template <int HD, int DNW, bool PAGED, int NBUF>
 __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* __restrict__ q, KVView kv,
                                                                     bf16* __restrict__ o, float* __restrict__ part,
                                                                     int H, const int32_t* __restrict__ len,
@@ -396,28 +396,29 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
       acc[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vv, pb, acc[d], 0, 0, 0);
     }
   };
-  // wavefront w takes the 32-key chunks of the 64 keys at s0 + w*64, s0 + (w +
-  // DNW)*64, ...; two chunks are in flight: the next but one is loaded into
-  // a chunk's registers as soon as that chunk has been consumed
-  auto chunk = [&](int i) { return s0 + wave * 64 + (i >> 1) * (DNW * 64) + (i & 1) * 32; };
-  // The loop body is one basic block: a load under a branch would be waited
-  // for where the branch joins, or moved next to its use.  A chunk at or past
-  // the context end is computed anyway: its keys are masked (probability 0;
-  // the running maximum is already finite from the chunk before it) and its
-  // loads read the clamped block.
+  // Wavefront w takes the 32-key chunks w, w + DNW, w + 2 DNW, ... of the
+  // split, NBUF of them in flight (a chunk's registers are reloaded with the
+  // chunk NBUF later as soon as it has been consumed).  The loop body is one
+  // basic block: a load under a branch would be waited for where the branch
+  // joins, or moved next to its use.  Chunks of the last round at or past the
+  // context end are computed anyway: their keys are masked (probability 0;
+  // the running maximum is already finite from the round's first chunk) and
+  // their loads read the clamped block.
+  auto chunk = [&](int i) { return s0 + (wave + i * DNW) * 32; };
   if (chunk(0) < s1) {  // wave-uniform
-    Frag fa, fb;
-    load(fa, chunk(0));
-    load(fb, chunk(1));
+    Frag f[NBUF];
+#pragma unroll
+    for (int j = 0; j < NBUF; ++j) load(f[j], chunk(j));
     int i = 0;
-    for (; chunk(i + 2) < s1; i += 2) {  // a chunk pair follows this one
-      step(fa, chunk(i));
-      load(fa, chunk(i + 2));
-      step(fb, chunk(i + 1));
-      load(fb, chunk(i + 3));
+    for (; chunk(i + NBUF) < s1; i += NBUF) {  // another round follows this one
+#pragma unroll
+      for (int j = 0; j < NBUF; ++j) {
+        step(f[j], chunk(i + j));
+        load(f[j], chunk(i + NBUF + j));
+      }
     }
-    step(fa, chunk(i));  // the last pair: chunk(i) < s1
-    step(fb, chunk(i + 1));
+#pragma unroll
+    for (int j = 0; j < NBUF; ++j) step(f[j], chunk(i + j));  // the last round: chunk(i) < s1
   }
   // per-wave statistics: m uniform over the 4 lane groups of a column; l summed
   l_run += __shfl_xor(l_run, 16, 64);
@@ -590,10 +591,11 @@ static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int B,
   const int group = H / kv.kv_heads;
   const size_t lds = (size_t)(2 * NW * 16 + NW * group * HD) * sizeof(float);
   const dim3 grid(nsplit, kv.kv_heads, B);
+  constexpr int NBUF = 2;  // chunks in flight per wavefront (3-4 measured slower: clamped duplicate loads, registers)
   if (kv.bt)
-    attn_decode_bf16_kernel<HD, NW, true><<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len);
+    attn_decode_bf16_kernel<HD, NW, true, NBUF><<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len);
   else
-    attn_decode_bf16_kernel<HD, NW, false><<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len);
+    attn_decode_bf16_kernel<HD, NW, false, NBUF><<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len);
   if (nsplit > 1) attn_combine_kernel<HD><<<dim3(H, B), HD, 0, s>>>(part, o, H, len, nsplit, split_len);
 }
 
