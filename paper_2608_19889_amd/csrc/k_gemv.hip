@@ -34,12 +34,48 @@ AXON_DEV float silu_g(float z) { return z / (1.f + __expf(-z)); }
 
 constexpr int GV_U = 4;  // k-steps of 32 per pipeline stage
 
+// v(0) + v(1) + ... + v(n - 1) in that order, 8 independent (LDS) reads per
+// round instead of a chain of dependent ones
+template <typename V>
+AXON_DEV float ordered_sum(int n, const V& v) {
+  float s = 0.f;
+  for (int j0 = 0; j0 < n; j0 += 8) {
+    float r[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) r[q] = v(min(j0 + q, n - 1));
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      if (j0 + q < n) s += r[q];
+  }
+  return s;
+}
+
+// Epilogue operands that do not depend on the projection's result, loaded by
+// the fused kernel before its weight stream (one epilogue item per thread).
+// bf16 values are kept as their raw bits and every field is pinned (an empty
+// asm that "modifies" it) after the stream: otherwise the compiler converts
+// or combines a value next to its load and waits for that load before the
+// stream starts.
+struct GvPre {
+  float x;         // residual: x[t][n]
+  uint32_t g;      // residual: bits of the next gain at n
+  int pos;         // rope: the token's position
+  uint32_t b1, b2; // rope: bits of the pair's biases
+};
+AXON_DEV float bf16_bits(uint32_t b) { return __uint_as_float(b << 16); }
+AXON_DEV void pin(float& v) { asm volatile("" : "+v"(v)); }
+AXON_DEV void pin(uint32_t& v) { asm volatile("" : "+v"(v)); }
+AXON_DEV void pin(int& v) { asm volatile("" : "+v"(v)); }
+
 // The epilogues of a tile of ROWS output features x COLS token columns
 // starting at feature n0; total(row, col) is the finished (normalized) dot
 // product.  wg / nwg index the per-tile partials (sums of squares, argmax).
 // aux: LDS of at least max(ROWS, 16) x (COLS + 1) floats.
-template <int ROWS, int COLS, int NT, int EPI, typename Total>
-AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg, int nwg, const Total& total) {
+// PRE: ``pre`` holds the operands of item ``tid`` (the tile has at most one
+// item per thread).
+template <int ROWS, int COLS, int NT, int EPI, bool PRE = false, typename Total>
+AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg, int nwg, const Total& total,
+                          const GvPre& pre = GvPre{}) {
   const int M = a.M, lane = tid & 63, wave = tid >> 6;
   auto s_aux = [&](int row, int col) -> float& { return aux[row * (COLS + 1) + col]; };
   if constexpr (EPI == GV_RESID) {
@@ -49,19 +85,15 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
       float sq = 0.f;
       if (n < a.N) {
         float* p = a.out_f32 + (int64_t)col * a.ldo + n;
-        const float v = *p + total(row, col);
+        const float v = (PRE ? pre.x : *p) + total(row, col);
         *p = v;
         sq = v * v;
-        a.xg_out[(int64_t)col * a.ldo + n] = (bf16)(v * (float)a.gain_next[n]);
+        a.xg_out[(int64_t)col * a.ldo + n] = (bf16)(v * (PRE ? bf16_bits(pre.g) : (float)a.gain_next[n]));
       }
       s_aux(row, col) = sq;
     }
     __syncthreads();
-    if (tid < M) {
-      float sq = 0.f;
-      for (int row = 0; row < ROWS; ++row) sq += s_aux(row, tid);
-      a.ss_out[(int64_t)wg * M + tid] = sq;
-    }
+    if (tid < M) a.ss_out[(int64_t)wg * M + tid] = ordered_sum(ROWS, [&](int row) { return s_aux(row, tid); });
   } else if constexpr (EPI == GV_SILU) {
     // each 32-row block: rows 0..15 gate, 16..31 the matching up rows
     for (int it = tid; it < (ROWS / 2) * M; it += NT) {
@@ -82,10 +114,10 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
       const int i = (g0 + gl) * 4 + i4;  // rotation pair (i, i + hd/2) of this head
       float x1 = total(gl * 8 + i4, t), x2 = total(gl * 8 + 4 + i4, t);
       if (a.bias) {
-        x1 += (float)a.bias[head * hd + i];
-        x2 += (float)a.bias[head * hd + half + i];
+        x1 += PRE ? bf16_bits(pre.b1) : (float)a.bias[head * hd + i];
+        x2 += PRE ? bf16_bits(pre.b2) : (float)a.bias[head * hd + half + i];
       }
-      const int pos = a.len[t];
+      const int pos = PRE ? pre.pos : a.len[t];
       if (head < a.H + KVh) {
         const float cs = a.cos_t[(int64_t)pos * half + i], sn = a.sin_t[(int64_t)pos * half + i];
         const float y1 = x1 * cs - x2 * sn, y2 = x2 * cs + x1 * sn;
@@ -230,9 +262,41 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
         for (int c = 0; c < NB; ++c)
           acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wv[u][r], xv[u][c], acc[r][c], 0, 0, 0);
   };
+  // epilogue operands (one item per thread), loaded behind the first stage
+  constexpr bool PRE = (EPI == GV_RESID && ROWS * COLS <= NT) || (EPI == GV_ROPE && (ROWS / 2) * COLS <= NT);
+  GvPre pre{};
+  auto prefetch = [&] {
+    if constexpr (PRE && EPI == GV_RESID) {
+      const int it = min(tid, ROWS * M - 1);
+      const int n = min(n0 + it % ROWS, a.N - 1), col = it / ROWS;
+      pre.x = a.out_f32[(int64_t)col * a.ldo + n];
+      pre.g = *(const unsigned short*)(a.gain_next + n);
+    } else if constexpr (PRE && EPI == GV_ROPE) {
+      const int it = min(tid, (ROWS / 2) * M - 1);
+      const int pr = it % (ROWS / 2), t = it / (ROWS / 2);
+      const int hd = a.kv.hd, half = hd / 2, head = n0 / hd;
+      const int i = ((n0 % hd) / 8 + pr / 4) * 4 + pr % 4;
+      pre.pos = a.len[t];
+      // no bias: read the weights instead (any valid address; not used)
+      const bf16* bp = a.bias ? a.bias : a.W;
+      pre.b1 = *(const unsigned short*)(bp + head * hd + i);
+      pre.b2 = *(const unsigned short*)(bp + head * hd + half + i);
+    }
+  };
+  auto pin_pre = [&] {
+    if constexpr (PRE && EPI == GV_RESID) {
+      pin(pre.x);
+      pin(pre.g);
+    } else if constexpr (PRE && EPI == GV_ROPE) {
+      pin(pre.pos);
+      pin(pre.b1);
+      pin(pre.b2);
+    }
+  };
   const int nst = (k1 - k0) / (32 * U);
+  if (nst > 0) load_stage(k0);
+  prefetch();
   if (nst > 0) {
-    load_stage(k0);
     for (int st = 1; st < nst; ++st) {
       bf16x8 ca[U][RB], cb[U][NB];
 #pragma unroll
@@ -259,6 +323,12 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
       for (int c = 0; c < NB; ++c) acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1[r], x1[c], acc[r][c], 0, 0, 0);
   }
 
+  // the prefetched values are used from here on (see GvPre)
+  pin_pre();
+  if constexpr (NORM) {
+#pragma unroll
+    for (int i = 0; i < SSR; ++i) pin(ss_reg[i]);
+  }
   // ---- cross-wavefront reduction: acc[r][c][i] = C[n0 + r*16 + (lane/16)*4 + i][c*16 + lane%16]
 #pragma unroll
   for (int r = 0; r < RB; ++r)
@@ -268,9 +338,11 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
       for (int i = 0; i < 4; ++i) red[wave][r * 16 + (lane >> 4) * 4 + i][c * 16 + r16] = acc[r][c][i];
   if constexpr (NORM) {
     float ss_part = 0.f;
+    // selects, not branches: a lane-divergent branch per term costs more
+    // than the adds
+    const bool ss_own = ss_sl < ss_slices;
 #pragma unroll
-    for (int i = 0; i < SSR; ++i)
-      if (ss_sl < ss_slices && ss_sl + i * ss_slices < a.ss_n) ss_part += ss_reg[i];
+    for (int i = 0; i < SSR; ++i) ss_part += ss_own && ss_sl + i * ss_slices < a.ss_n ? ss_reg[i] : 0.f;
     // partials beyond the prefetched ones: 16 independent loads per round
     // (a load-add loop would wait for every load in turn)
     if (ss_sl < ss_slices) {
@@ -288,8 +360,7 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
   __syncthreads();
   if constexpr (NORM) {
     if (tid < M) {
-      float tot = 0.f;
-      for (int sl = 0; sl < ss_slices; ++sl) tot += s_ss[sl * M + tid];
+      const float tot = ordered_sum(ss_slices, [&](int sl) { return s_ss[sl * M + tid]; });
       s_inv[tid] = rsqrtf(tot / (float)K + a.eps);
     }
     __syncthreads();
@@ -312,7 +383,7 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
     // the residual and head epilogues overwrite element (row, col) of their
     // scratch only after the same thread has read total(row, col): the first
     // wavefront's tile serves as that scratch
-    gv_epilogue<ROWS, COLS, NT, EPI>(a, n0, tid, &red[0][0][0], blockIdx.x, gridDim.x, total);
+    gv_epilogue<ROWS, COLS, NT, EPI, PRE>(a, n0, tid, &red[0][0][0], blockIdx.x, gridDim.x, total, pre);
   }
 }
 
@@ -448,6 +519,11 @@ __global__ void __launch_bounds__(256) gemv_wide_kernel(GemvArgs a) {
     }
   }
 
+  // the prefetched sums of squares are used from here on (see GvPre)
+  if constexpr (NORM) {
+#pragma unroll
+    for (int i = 0; i < SSR; ++i) pin(ss_reg[i]);
+  }
   // finished tile -> LDS (over the token stages): tot[row][col]
   __syncthreads();
   float* tot = smem;
@@ -460,9 +536,11 @@ __global__ void __launch_bounds__(256) gemv_wide_kernel(GemvArgs a) {
         tot[((wave * RB + r) * 16 + (lane >> 4) * 4 + i) * (COLS + 1) + c * 16 + r16] = acc[r][c][i];
   if constexpr (NORM) {
     float ss_part = 0.f;
+    // selects, not branches: a lane-divergent branch per term costs more
+    // than the adds
+    const bool ss_own = ss_sl < ss_slices;
 #pragma unroll
-    for (int i = 0; i < SSR; ++i)
-      if (ss_sl < ss_slices && ss_sl + i * ss_slices < a.ss_n) ss_part += ss_reg[i];
+    for (int i = 0; i < SSR; ++i) ss_part += ss_own && ss_sl + i * ss_slices < a.ss_n ? ss_reg[i] : 0.f;
     if (ss_sl < ss_slices) {
       for (int j0 = ss_sl + SSR * ss_slices; j0 < a.ss_n; j0 += SSR * ss_slices) {
         float v[SSR];
@@ -478,9 +556,8 @@ __global__ void __launch_bounds__(256) gemv_wide_kernel(GemvArgs a) {
   __syncthreads();
   if constexpr (NORM) {
     if (tid < M) {
-      float t = 0.f;
-      for (int sl = 0; sl < ss_slices; ++sl) t += s_ss[sl * M + tid];
-      s_inv[tid] = rsqrtf(t / (float)K + a.eps);
+      const float tot = ordered_sum(ss_slices, [&](int sl) { return s_ss[sl * M + tid]; });
+      s_inv[tid] = rsqrtf(tot / (float)K + a.eps);
     }
     __syncthreads();
   }
