@@ -42,12 +42,18 @@ BF16_CASES = {
     "qwen_hd128_g7_bias": ("7b", dict(layers=2, vocab=2048, hidden=896, intermediate=1792), [5, 129, 300], 6),
     "qwen32_hd128_g5_bias": ("32b", dict(layers=2, vocab=1500, hidden=640, intermediate=1280), [64, 257], 5),
     "smollm_hd64_g3": ("135m", dict(layers=3, vocab=1000, dtype="bf16"), [1, 31, 66, 90], 5),
-    # 17..64 sequences: decode projections split K over workgroups (partials
-    # + an epilogue kernel), with 2 and 3 token blocks
+    # 17..64 sequences: the row-splitting decode projections (gate/up, head)
+    # and, for the narrow ones, K split over workgroups (partials + an
+    # epilogue kernel), with 2, 3 and 4 token blocks; the long-K cases
+    # (down with K >= 8192) take the 128-row split
     "llama_hd64_batch40": ("1b", dict(layers=2, vocab=3000, hidden=512, intermediate=1024),
                            [2 + (i * 29) % 61 for i in range(40)], 4),
     "qwen_hd128_bias_batch24": ("7b", dict(layers=2, vocab=2048, hidden=896, intermediate=1792),
                                 [3 + (i * 53) % 97 for i in range(24)], 4),
+    "llama_hd64_batch56_longK": ("1b", dict(layers=2, vocab=3000, hidden=512, intermediate=8192),
+                                 [2 + (i * 23) % 50 for i in range(56)], 3),
+    "qwen32_hd128_bias_batch20_longK": ("32b", dict(layers=2, vocab=1500, hidden=640, intermediate=8192),
+                                        [3 + (i * 41) % 70 for i in range(20)], 3),
     # more sequences than one fused decode projection takes (64): the decode
     # step and the prefill head run as GEMMs
     "llama_hd64_batch80": ("1b", dict(layers=2, vocab=3000, hidden=512, intermediate=1024),
