@@ -147,19 +147,33 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
 }
 
 // ============================================================================
-// Large prefill GEMM: 256 (W rows) x 256 (tokens) tiles, k-tiles of BK, 8
-// wavefronts in a 2 x 4 arrangement, each owning 128 x 64 = 4 x 2 blocks of
-// v_mfma_f32_32x32x16_bf16.  Operands go straight from global memory to LDS
-// (global_load_lds_dwordx4: lane L of an instruction writes 16 bytes at LDS
-// offset 16 L) into a ring of STAGES k-tiles in 128 KB of LDS, loads running
-// STAGES-1 k-tiles ahead; the bank swizzle of the panels is produced by
-// choosing which global chunk each lane loads.
+// Large prefill GEMM: 256 (W rows) x 256 (tokens) tiles, k-tiles of 32, 8
+// wavefronts run as two groups that take turns on the matrix cores
+// ("ping-pong").  Group g = wave / 4 owns W rows g*128 .. g*128+127 of the
+// tile; wave (g, c) owns tokens c*64 .. c*64+63: 4 x 2 blocks of
+// v_mfma_f32_32x32x16_bf16.  Waves w and w + 4 share a SIMD, and the groups
+// run one phase apart: while one group issues a k-tile's 16 MFMAs, the other
+// reads its next fragments from LDS and issues its share of the global->LDS
+// loads, then a barrier swaps the roles.  The matrix core of every SIMD thus
+// always has one wavefront's uninterrupted MFMA run in flight, and LDS
+// latency and load issue are hidden behind it.
+// Operands go straight from global memory to LDS (global_load_lds_dwordx4:
+// lane L of an instruction writes 16 bytes at LDS offset 16 L) into a ring of
+// STAGES k-tiles (32 KB each), issued STAGES-1 tiles ahead; the bank swizzle
+// of the 64-byte panel rows is produced by choosing which global chunk each
+// lane loads.
 // Workgroups are renumbered so that each XCD (workgroup id mod 8) receives a
 // contiguous range of tiles, walked in groups of 8 token tiles so that
 // neighbouring tiles share operand panels in that XCD's L2.
 // ============================================================================
 namespace pf2 {
-constexpr int BN = 256, BM = 256;
+constexpr int BN = 256, BM = 256, BK = 32, STAGES = 4;
+constexpr int CH = BK / 8;            // 16-byte chunks per panel row
+constexpr int PANEL = BN * CH;        // chunks per operand panel
+constexpr int STAGE = 2 * PANEL;      // W panel + X panel
+constexpr int LPT = PANEL / 512;      // load instructions per operand per wave per k-tile
+constexpr int ROWSTEP = 512 / CH;     // panel rows between a lane's consecutive chunks
+constexpr int LDS_BYTES = STAGES * STAGE * 16;
 }
 
 AXON_DEV void tile_order(int bid, int gx, int gy, int& pn, int& pm) {
@@ -176,128 +190,126 @@ AXON_DEV void tile_order(int bid, int gx, int gy, int& pn, int& pm) {
   pn = (logical % per_group) / gsize;
 }
 
-
-template <int STAGES>
-AXON_DEV void wait_stage(int after) {
-  // allow the loads of ``after`` later stages (4 per stage per thread at BK 32,
-  // 8 at BK 64) to stay in flight
-  if constexpr (STAGES == 2) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  } else {
-    if (after >= 2) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else if (after == 1) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
+// Wait until at most ``after`` k-tiles' loads of this wavefront are in flight
+// (2 * LPT load instructions per k-tile).
+AXON_DEV void wait_tiles(int after) {
+  using namespace pf2;
+  static_assert(2 * 2 * LPT <= 63, "vmcnt range");
+  if (after >= 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * 2 * LPT) : "memory");
+  else if (after == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LPT) : "memory");
+  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-template <int EPI, int BK, int STAGES, int NWV>
-__global__ void __launch_bounds__(NWV * 64, 1) gemm_bf16_256_kernel(const bf16* __restrict__ W,
-                                                                    const bf16* __restrict__ X, int N, int M, int K,
-                                                                    EpiArgs ep) {
+// a workgroup barrier the compiler schedules nothing across
+AXON_DEV void phase_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int EPI>
+__global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __restrict__ W,
+                                                               const bf16* __restrict__ X, int N, int M, int K,
+                                                               EpiArgs ep) {
   using namespace pf2;
-  constexpr int CH = BK / 8;                 // 16-byte chunks per panel row
-  constexpr int PANEL = BN * CH;             // chunks per operand panel
-  constexpr int STAGE = 2 * PANEL;           // W panel + X panel
-  constexpr int NT = NWV * 64;
-  constexpr int LPT = PANEL / NT;            // chunks per thread per operand per stage
-  constexpr int WCOLS = NWV / 2;             // wavefront columns (token direction)
-  constexpr int TB = 256 / WCOLS / 32;       // 32-token blocks per wavefront
+  static_assert(STAGES >= 3 && STAGES - 2 <= 2, "wait_tiles covers up to 2 later tiles");
+  static_assert(CH == 4, "the W chunk address below assumes one 32-wide tile per k-tile");
   extern __shared__ bf16x8 lds2[];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave / WCOLS, wc = wave % WCOLS;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar branches only
+  const int grp = wave >> 2, wc = wave & 3;
   const int gx = (N + BN - 1) / BN, gy = (M + BM - 1) / BM;
   int pn, pm;
   tile_order(blockIdx.x, gx, gy, pn, pm);
   const int n0 = pn * BN, m0 = pm * BM;
 
-  // this thread's chunks of each operand per stage: q = (i*NWV + wave)*64 + lane
-  const bf16* wsrc[LPT];
-  const bf16* xsrc[LPT];
-#pragma unroll
-  for (int i = 0; i < LPT; ++i) {
-    const int q = (i * NWV + wave) * 64 + lane;
-    const int row = q / CH, c = swz<CH>(row, q % CH);  // swz is its own inverse
-    const int n = min(n0 + row, N - 1), m = min(m0 + row, M - 1);  // rows past the edge: any valid row
-    wsrc[i] = W + wt_chunk(n, c, K);
-    xsrc[i] = X + (int64_t)m * K + c * 8;
-  }
-  // k-tile k0 (a multiple of 32) of a fragment-tiled row block starts k0 / 32
-  // tiles of 512 elements further on
+  // this lane's chunks of a stage: q = (i * 8 + wave) * 64 + lane, i < LPT,
+  // row q / CH, logical chunk swz(row, q % CH) (swz is its own inverse)
+  const int lrow0 = (wave * 64 + lane) / CH, lch = lane % CH;
+  const int64_t rowblk = (int64_t)(K >> 5) * 512;  // elements per 16-row block of tiled W
   auto issue = [&](int stage, int k0) {
 #pragma unroll
     for (int i = 0; i < LPT; ++i) {
-      bf16x8* base = lds2 + stage * STAGE + (i * NWV + wave) * 64;
-      __builtin_amdgcn_global_load_lds((const void*)(wsrc[i] + (int64_t)k0 * 16),
-                                       (__attribute__((address_space(3))) void*)base, 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((const void*)(xsrc[i] + k0),
-                                       (__attribute__((address_space(3))) void*)(base + PANEL), 16, 0, 0);
+      const int row = lrow0 + i * ROWSTEP;
+      const int c = swz<CH>(row, lch);
+      const int n = min(n0 + row, N - 1), m = min(m0 + row, M - 1);  // rows past the edge: any valid row
+      // wt_chunk(n, k0 / 8 + c, K) with k0 a multiple of 32
+      const bf16* ws = W + ((int64_t)(n >> 4) * rowblk + (int64_t)k0 * 16 + ((n & 15) + 16 * c) * 8);
+      const bf16* xs = X + (int64_t)m * K + k0 + c * 8;
+      bf16x8* base = lds2 + stage * STAGE + (i * 8 + wave) * 64;
+      __builtin_amdgcn_global_load_lds((const void*)ws, (__attribute__((address_space(3))) void*)base, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)xs, (__attribute__((address_space(3))) void*)(base + PANEL),
+                                       16, 0, 0);
     }
   };
 
-  f32x16 acc[4][TB];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < TB; ++b) acc[a][b] = f32x16{};
+    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
 
   const int nk = K / BK;
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
     if (st < nk) issue(st, st * BK);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (grp == 1) phase_barrier();  // group 1 runs one phase behind group 0
+
+  bf16x8 fa[2][4], fb[2][2];
   for (int kt = 0; kt < nk; ++kt) {
-    wait_stage<STAGES>(min(STAGES - 2, nk - 1 - kt));
-    __syncthreads();  // stage kt landed for every wavefront; stage kt-1 is free
-    if (kt + STAGES - 1 < nk) issue((kt + STAGES - 1) % STAGES, (kt + STAGES - 1) * BK);
+    // ---- memory phase: fragments of k-tile kt, loads of k-tile kt+STAGES-1
+    // into the buffer of k-tile kt-1, which both groups have read (group 1
+    // in the phase that just ended)
     const bf16x8* la = lds2 + (kt % STAGES) * STAGE;
     const bf16x8* lb = la + PANEL;
-    // operand fragments double-buffered in registers: the LDS reads of k-step
-    // ks+1 are issued before the MFMAs of k-step ks
-    bf16x8 fa[2][4], fb[2][TB];
-    auto frags = [&](int ks, int f) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
       const int ch = ks * 2 + (lane >> 5);
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
-        const int r = wr * 128 + a * 32 + (lane & 31);
-        fa[f][a] = la[r * CH + swz<CH>(r, ch)];
+        const int r = grp * 128 + a * 32 + (lane & 31);
+        fa[ks][a] = la[r * CH + swz<CH>(r, ch)];
       }
 #pragma unroll
-      for (int b = 0; b < TB; ++b) {
-        const int r = wc * (32 * TB) + b * 32 + (lane & 31);
-        fb[f][b] = lb[r * CH + swz<CH>(r, ch)];
+      for (int b = 0; b < 2; ++b) {
+        const int r = wc * 64 + b * 32 + (lane & 31);
+        fb[ks][b] = lb[r * CH + swz<CH>(r, ch)];
       }
-    };
-    frags(0, 0);
+    }
+    const int kn = kt + STAGES - 1;
+    if (kn < nk) issue(kn % STAGES, kn * BK);
+    // group 1's share of k-tile kt+1 must land before group 0 reads it in
+    // the phase after the coming barrier; group 0 waits for its own share at
+    // the end of its compute phase
+    if (grp == 1) wait_tiles(min(STAGES - 2, nk - 2 - kt));
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    phase_barrier();
+    // ---- compute phase
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      if (ks + 1 < BK / 16) frags(ks + 1, (ks + 1) & 1);
+    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int b = 0; b < TB; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks & 1][a], fb[ks & 1][b], acc[a][b], 0, 0, 0);
-#if AXON_G256_SCHED == 1
-      // interleave: one LDS read after each of the first 4 + TB MFMAs
-#pragma unroll
-      for (int i = 0; i < 4 + TB; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 4 * TB - (4 + TB), 0);
-#endif
-    }
-#if AXON_G256_SCHED == 2
-    __builtin_amdgcn_iglp_opt(0);
-#endif
+        for (int b = 0; b < 2; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][a], fb[ks][b], acc[a][b], 0, 0, 0);
+    __builtin_amdgcn_s_setprio(0);
+    if (grp == 0) wait_tiles(min(STAGES - 2, nk - 2 - kt));
+    phase_barrier();
   }
+  if (grp == 0) phase_barrier();  // same barrier count in both groups
+
   // epilogue: acc[a][b][i] = C[n][t],
-  //   n = n0 + wr*128 + a*32 + (i/4)*8 + (lane/32)*4 + i%4,  t = m0 + wc*32*TB + b*32 + lane%32
+  //   n = n0 + grp*128 + a*32 + (i/4)*8 + (lane/32)*4 + i%4,  t = m0 + wc*64 + b*32 + lane%32
 #pragma unroll
-  for (int b = 0; b < TB; ++b) {
-    const int t = m0 + wc * (32 * TB) + b * 32 + (lane & 31);
+  for (int b = 0; b < 2; ++b) {
+    const int t = m0 + wc * 64 + b * 32 + (lane & 31);
     if (t >= M) continue;
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
-      const int nb = n0 + wr * 128 + a * 32;
+      const int nb = n0 + grp * 128 + a * 32;
       if (nb >= N) continue;
       if constexpr (EPI == EPI_SILU) {
         bf16* out = (bf16*)ep.out_t + (int64_t)t * ep.ldo + (nb / 32) * 16;
@@ -323,27 +335,16 @@ __global__ void __launch_bounds__(NWV * 64, 1) gemm_bf16_256_kernel(const bf16* 
   }
 }
 
-#ifndef AXON_G256_SCHED
-#define AXON_G256_SCHED 0
-#endif
-#ifndef AXON_G256_BK
-#define AXON_G256_BK 64
-#define AXON_G256_STAGES 2
-#define AXON_G256_WAVES 8
-#endif
-constexpr int G256_BK = AXON_G256_BK, G256_STAGES = AXON_G256_STAGES, G256_WAVES = AXON_G256_WAVES;
-constexpr int G256_LDS = G256_STAGES * 2 * pf2::BN * (G256_BK / 8) * 16;
-
 template <int EPI>
 static void launch_256(const bf16* W, const bf16* X, int N, int M, int K, const EpiArgs& ep, hipStream_t s) {
   static bool attr = false;
-  auto kern = gemm_bf16_256_kernel<EPI, G256_BK, G256_STAGES, G256_WAVES>;
+  auto kern = gemm_bf16_256_kernel<EPI>;
   if (!attr) {
-    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, G256_LDS);
+    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, pf2::LDS_BYTES);
     attr = true;
   }
   const int tiles = ((N + pf2::BN - 1) / pf2::BN) * ((M + pf2::BM - 1) / pf2::BM);
-  klaunch(kern, dim3(tiles), dim3(G256_WAVES * 64), G256_LDS, s, W, X, N, M, K, ep);
+  klaunch(kern, dim3(tiles), dim3(512), pf2::LDS_BYTES, s, W, X, N, M, K, ep);
 }
 
 void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi, const EpiArgs& ep,
