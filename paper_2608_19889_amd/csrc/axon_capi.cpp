@@ -266,8 +266,11 @@ void release(axon_model* m) {
 // ------------------------------------------------------------------ forward
 template <typename T>
 void gemm_many(axon_model* m, const void* W, const void* X, int N, int M, int K, int epi, float* out_f32,
-               void* out_t, int ldo, hipStream_t s) {
-  EpiArgs ep{out_f32, out_t, ldo, 0};
+               void* out_t, int ldo, hipStream_t s, const EpiArgs* rope = nullptr) {
+  EpiArgs ep = rope ? *rope : EpiArgs{};
+  ep.out_f32 = out_f32;
+  ep.out_t = out_t;
+  ep.ldo = ldo;
   m->timed(1, N, M, K, s, [&] {
     if constexpr (sizeof(T) == 2)
       launch_gemm_bf16((const bf16*)W, (const bf16*)X, N, M, K, epi, ep, s);
@@ -293,6 +296,22 @@ void gemv_step(axon_model* m, const GemvArgs& a, int epi, hipStream_t s) {
                      " M=" + std::to_string(a.M) + " epilogue " + std::to_string(epi);
 }
 
+// Epilogue arguments of the bf16 QKV GEMM with bias + RoPE + KV write fused:
+// prefill positions from cu (nseq sequences), decode positions from len.
+EpiArgs rope_epi(axon_model* m, const LayerW& w, const KVView& kv, const int32_t* cu, int nseq, const int32_t* len) {
+  EpiArgs e{};
+  e.bias = (const bf16*)w.bqkv;
+  e.cos_t = m->rope_cos;
+  e.sin_t = m->rope_sin;
+  e.q_out = (bf16*)m->q;
+  e.kv = kv;
+  e.cu = cu;
+  e.nseq = nseq;
+  e.len = len;
+  e.H = m->H();
+  return e;
+}
+
 template <typename T>
 void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, const int32_t* d_cu,
                      const int32_t* h_cu, int all_logits, float* d_logits, int32_t* d_next, hipStream_t s) {
@@ -304,9 +323,15 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const LayerW& w = m->layers[l];
     KVView kv = m->kv(l, m->paged());
-    gemm_many<T>(m, w.wqkv, h, nq, Ttok, D, EPI_F32, m->qkv, nullptr, nq, s);
-    launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, Ttok, B, d_cu,
-                      nullptr, H, s);
+    if constexpr (sizeof(T) == 2) {
+      // bias, RoPE and the KV-cache write in the QKV GEMM's epilogue
+      const EpiArgs re = rope_epi(m, w, kv, d_cu, B, nullptr);
+      gemm_many<T>(m, w.wqkv, h, nq, Ttok, D, EPI_ROPE, nullptr, nullptr, nq, s, &re);
+    } else {
+      gemm_many<T>(m, w.wqkv, h, nq, Ttok, D, EPI_F32, m->qkv, nullptr, nq, s);
+      launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, Ttok, B, d_cu,
+                        nullptr, H, s);
+    }
     m->timed(3, H, B, Ttok, s, [&] { launch_attn_prefill<T>((const T*)m->q, kv, (T*)m->o, Ttok, B, d_cu, h_cu, H, s); });
     gemm_many<T>(m, w.wo, m->o, D, Ttok, H * hd, EPI_RESID, m->x, nullptr, D, s);
     launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, Ttok, D, eps, nullptr, s);
@@ -359,9 +384,14 @@ void enqueue_decode_many(axon_model* m, int B, const int32_t* d_tokens, float* d
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const LayerW& w = m->layers[l];
     KVView kv = m->kv(l, m->paged());
-    proj(w.wqkv, h, nq, D, EPI_F32, m->qkv, nullptr, nq);
-    launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, B, 0, nullptr,
-                      m->d_len, H, s);
+    if constexpr (sizeof(T) == 2) {
+      const EpiArgs re = rope_epi(m, w, kv, nullptr, 0, m->d_len);
+      gemm_many<T>(m, w.wqkv, h, nq, B, D, EPI_ROPE, nullptr, nullptr, nq, s, &re);
+    } else {
+      proj(w.wqkv, h, nq, D, EPI_F32, m->qkv, nullptr, nq);
+      launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, B, 0, nullptr,
+                        m->d_len, H, s);
+    }
     launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
     proj(w.wo, m->o, D, H * hd, EPI_RESID, m->x, nullptr, D);
     launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, B, D, eps, nullptr, s);
@@ -686,7 +716,7 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     m->rows = (int)tmax;
     TRY(dev_alloc(m, (void**)&m->x, tmax * D * 4));
     TRY(dev_alloc(m, &m->h, tmax * D * esz));
-    TRY(dev_alloc(m, (void**)&m->qkv, tmax * nq * 4));
+    if (!m->bf) TRY(dev_alloc(m, (void**)&m->qkv, tmax * nq * 4));  // bf16: RoPE is the QKV GEMM's epilogue
     TRY(dev_alloc(m, &m->q, tmax * H * hd * esz));
     TRY(dev_alloc(m, &m->o, tmax * H * hd * esz));
     TRY(dev_alloc(m, &m->a, tmax * I * esz));

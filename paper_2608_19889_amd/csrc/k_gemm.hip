@@ -25,6 +25,55 @@ AXON_DEV void store_cols(float* p, f32x4 v, int left) {
   }
 }
 
+// EPI_ROPE epilogue of one 32 x 32 accumulator block of the fused QKV
+// projection: rows nb .. nb+31 (32-aligned, so inside one head), token t;
+// v[i] = C[nb + (i/4)*8 + (lane/32)*4 + i%4][t].  Within a head the rows come
+// in groups of 8: rotation-pair first halves i0 .. i0+3, then their partners
+// i0+hd/2 .. i0+hd/2+3, so lane L < 32 holds first halves and lane L + 32 the
+// partners for the same token, and one exchange across the half-wavefronts
+// pairs them (both lanes of a pair share t, so they are active together).
+// Bias first, then rotate-half RoPE at the token's position; q -> q_out, k ->
+// its K page block, v (unrotated) -> its transposed V page block.
+AXON_DEV void rope_block(const EpiArgs& ep, int nb, int t, const f32x16& v, int lane) {
+  const int hd = ep.kv.hd, half = hd / 2, KVh = ep.kv.kv_heads;
+  const int head = nb / hd;
+  const bool first = lane < 32;
+  int slot, pos;
+  if (ep.len) {
+    slot = t;
+    pos = ep.len[t];
+  } else {
+    slot = seq_of_token(ep.cu, ep.nseq, t);
+    pos = t - ep.cu[slot];
+  }
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int i0 = ((nb % hd + g * 8) / 8) * 4;  // first rotation pair of the 8-row group
+    const int e0 = first ? i0 : i0 + half;       // element index of this lane's first value
+    float x[4], xp[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[j] = v[g * 4 + j];
+      if (ep.bias) x[j] += (float)ep.bias[head * hd + e0 + j];
+      xp[j] = __shfl_xor(x[j], 32, 64);
+    }
+    if (head < ep.H + KVh) {
+      const f32x4 cs = *(const f32x4*)(ep.cos_t + (int64_t)pos * half + i0);
+      const f32x4 sn = *(const f32x4*)(ep.sin_t + (int64_t)pos * half + i0);
+      bf16x4 y;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        y[j] = (bf16)(first ? x[j] * cs[j] - xp[j] * sn[j] : x[j] * cs[j] + xp[j] * sn[j]);
+      if (head < ep.H) *(bf16x4*)(ep.q_out + ((int64_t)t * ep.H + head) * hd + e0) = y;
+      else *(bf16x4*)((bf16*)ep.kv.k + k_el(ep.kv, slot, head - ep.H, pos, e0)) = y;  // 4 dims contiguous
+    } else {
+      bf16* vc = (bf16*)ep.kv.v;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) vc[v_el(ep.kv, slot, head - ep.H - KVh, pos, e0 + j)] = (bf16)x[j];
+    }
+  }
+}
+
 // physical 16-byte chunk of logical chunk c in row r of an LDS panel with CH
 // chunks per row.  The LDS serves 256 bytes (64 banks) per cycle, so the 16
 // lanes of a ds_read_b128 phase (16 consecutive rows, one logical chunk) must
@@ -121,7 +170,9 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
     for (int a = 0; a < 2; ++a) {
       const int nb = n0 + wr * 64 + a * 32;  // 32-aligned row block
       if (nb >= N) continue;
-      if constexpr (EPI == EPI_SILU) {
+      if constexpr (EPI == EPI_ROPE) {
+        rope_block(ep, nb, t, acc[a][b], lane);
+      } else if constexpr (EPI == EPI_SILU) {
         // rows nb..nb+15 are gate rows, nb+16..nb+31 the matching up rows
         bf16* out = (bf16*)ep.out_t + (int64_t)t * ep.ldo + (nb / 32) * 16;
 #pragma unroll
@@ -311,7 +362,9 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
     for (int a = 0; a < 4; ++a) {
       const int nb = n0 + grp * 128 + a * 32;
       if (nb >= N) continue;
-      if constexpr (EPI == EPI_SILU) {
+      if constexpr (EPI == EPI_ROPE) {
+        rope_block(ep, nb, t, acc[a][b], lane);
+      } else if constexpr (EPI == EPI_SILU) {
         bf16* out = (bf16*)ep.out_t + (int64_t)t * ep.ldo + (nb / 32) * 16;
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
@@ -357,6 +410,7 @@ void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi
       case EPI_F32: launch_256<EPI_F32>(W, X, N, M, K, ep, s); return;
       case EPI_RESID: launch_256<EPI_RESID>(W, X, N, M, K, ep, s); return;
       case EPI_SILU: launch_256<EPI_SILU>(W, X, N, M, K, ep, s); return;
+      case EPI_ROPE: launch_256<EPI_ROPE>(W, X, N, M, K, ep, s); return;
       default: break;
     }
   }
@@ -365,6 +419,7 @@ void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi
     case EPI_F32: klaunch(gemm_bf16_kernel<EPI_F32>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
     case EPI_RESID: klaunch(gemm_bf16_kernel<EPI_RESID>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
     case EPI_SILU: klaunch(gemm_bf16_kernel<EPI_SILU>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
+    case EPI_ROPE: klaunch(gemm_bf16_kernel<EPI_ROPE>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
     default: break;
   }
 }

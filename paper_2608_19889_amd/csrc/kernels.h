@@ -34,7 +34,10 @@ enum Epi : int {
   EPI_RESID = 1,  // out_f32[t * ldo + n] += acc   (residual stream, float)
   EPI_SILU = 2,   // W rows interleaved in blocks of 16 gate rows then 16 up rows;
                   // out_t[t * ldo + f] = silu(gate_f) * up_f
-  EPI_PART = 3    // (reserved)
+  EPI_PART = 3,   // (reserved)
+  EPI_ROPE = 4    // bf16 fused QKV projection (rows in the rotation-pair order of
+                  // the decode projections): bias + rotary embedding, then q ->
+                  // q_out, k -> K pages, v -> transposed V pages
 };
 
 struct EpiArgs {
@@ -42,6 +45,17 @@ struct EpiArgs {
   void* out_t;
   int ldo;
   int64_t part_stride;
+  // EPI_ROPE.  Token t is at position t - cu[seq] of sequence seq (prefill,
+  // len == nullptr) or at position len[t] of slot t (decode).
+  const bf16* bias;  // [(H+2KV)hd] in the original head order, or null
+  const float* cos_t;
+  const float* sin_t;
+  bf16* q_out;       // [T][H][hd]
+  KVView kv;
+  const int32_t* cu;
+  int nseq;
+  const int32_t* len;
+  int H;
 };
 
 // ---- weight layout (k_layout.hip): fragment-tiled copy of row-major bf16
@@ -61,7 +75,8 @@ void launch_argmax_rows(const float* logits, int nseq, int V, int32_t* next, con
 void launch_set_lengths(const int32_t* cu, int32_t* len, int n, hipStream_t s);
 
 // ---- projections (k_gemm.hip)
-// Many-token GEMM (prefill): bf16 MFMA tiles.  Requires K % 64 == 0, N % 32 == 0.
+// Many-token GEMM (prefill): bf16 MFMA tiles.  Requires K % 64 == 0, N % 32 == 0
+// (EPI_ROPE: the head dimension a multiple of 32).
 void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi, const EpiArgs& ep,
                       hipStream_t s);
 // float32 check-mode GEMM (any M): EPI_F32 / EPI_RESID / EPI_PART(split 0 only).
