@@ -144,6 +144,44 @@ int axon_prefill(axon_model* m, int32_t batch, const int32_t* d_tokens,
 int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_tokens, float* d_logits,
                      int32_t* d_next_tokens, void* stream);
 
+/* Continuous batching (the serving loop of a paged-attention engine: prompt
+ * chunks of newly admitted sequences and decode tokens of running ones share
+ * one forward pass; Results, vLLM-native comparison; Introduction, vLLM
+ * backend).  Entry i of the step appends n_i = h_cu_seqlens[i+1] -
+ * h_cu_seqlens[i] >= 1 tokens to slot h_slots[i], at positions len .. len+n_i-1
+ * where len is the slot's current length, or 0 when h_fresh[i] == 1 (the slot
+ * starts a new sequence; what it held is dropped).  n_i > 1 is a prompt chunk,
+ * n_i == 1 a decode token.  Each entry's tokens attend to every earlier
+ * position of its slot (causally within the chunk), so feeding a prompt in
+ * chunks over several calls gives the same result as one prefill.
+ *   n             entries, 1..max_batch;
+ *   h_slots       host int32 [n], distinct slots in [0, max_batch);
+ *   h_fresh       host int32 [n] of 0/1, or NULL (no entry starts a sequence);
+ *   d_tokens      device int32 [sum n_i], the entries' tokens back to back;
+ *   d_cu_seqlens  device int32 [n+1], prefix sums of the n_i; h_cu_seqlens is
+ *                 its host copy;
+ *   h_block_table paged cache: host int32 [n, block_table_stride], the page row
+ *                 of each entry's slot after the call (copied; it must keep the
+ *                 pages that hold the slot's cached positions), or NULL to
+ *                 keep the rows set earlier; must be NULL for a contiguous
+ *                 cache.  Page ids are unique across all slots;
+ *   d_logits      device float [n, V]: logits of each entry's last token, or
+ *                 NULL; d_next_tokens: device int32 [n], their greedy argmax.
+ * Afterwards slot h_slots[i] has length len + n_i; other slots are unchanged.
+ * Fails with AXON_E_CAPACITY when len + n_i > max_seq, sum n_i > max_tokens
+ * or a needed page is missing, and with AXON_E_INVALID for a repeated slot or
+ * page, or a row that moves cached positions; nothing is enqueued then. */
+int axon_step(axon_model* m, int32_t n, const int32_t* h_slots, const int32_t* h_fresh,
+              const int32_t* d_tokens, const int32_t* d_cu_seqlens, const int32_t* h_cu_seqlens,
+              const int32_t* h_block_table, int32_t block_table_stride, float* d_logits,
+              int32_t* d_next_tokens, void* stream);
+
+/* Evict the sequence of ``slot``: its length becomes 0 and, for a paged cache,
+ * its page row is emptied, so its pages may be given to other slots by later
+ * calls.  Host bookkeeping only (nothing is enqueued).  A slot of length 0 is
+ * refused by axon_decode_step until axon_step or axon_prefill fills it. */
+int axon_reset_slot(axon_model* m, int32_t slot);
+
 /* Current length of every slot (host copy kept by the library, no device
  * access).  Writes min(n, max_batch) entries to ``lens``; returns the number of
  * active slots (the batch of the last prefill), or a negative status. */

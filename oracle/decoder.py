@@ -228,9 +228,20 @@ class OracleDecoder:
         return out
 
     def extend(self, b: int, ids, all_logits: bool = True) -> np.ndarray:
-        """Feed more tokens to slot b (positions continue after its cache)."""
+        """Feed more tokens to slot b (positions continue after its cache; a
+        slot never used before starts empty)."""
+        while len(self.caches) <= b:
+            self.caches.append(self._empty_cache())
         lg = self._forward_seq(b, np.asarray(ids), all_logits)
         return lg if all_logits else lg[0]
+
+    def reset(self, b: int):
+        """Drop the sequence of slot b: its cache becomes empty, so the next
+        tokens fed to it start at position 0 (admission of a new sequence in
+        continuous batching)."""
+        while len(self.caches) <= b:
+            self.caches.append(self._empty_cache())
+        self.caches[b] = self._empty_cache()
 
     def decode(self, tokens) -> np.ndarray:
         """One token per active slot; returns logits [B, V]."""

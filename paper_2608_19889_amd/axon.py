@@ -28,8 +28,8 @@ AXON_F32 = 2
 STATUS_NAMES = {0: "AXON_OK", -1: "AXON_E_INVALID", -2: "AXON_E_SHAPE", -3: "AXON_E_MISSING",
                 -4: "AXON_E_DTYPE", -5: "AXON_E_CAPACITY", -6: "AXON_E_OOM", -7: "AXON_E_HIP"}
 
-EXPORTED = ["axon_init_model", "axon_prefill", "axon_decode_step", "axon_slot_lengths",
-            "axon_timing_enable", "axon_timing_records", "axon_free", "axon_last_error"]
+EXPORTED = ["axon_init_model", "axon_prefill", "axon_decode_step", "axon_step", "axon_reset_slot",
+            "axon_slot_lengths", "axon_timing_enable", "axon_timing_records", "axon_free", "axon_last_error"]
 
 # kernel classes of the timing records
 T_GEMV, T_GEMM, T_ATTN_DECODE, T_ATTN_PREFILL = 0, 1, 2, 3
@@ -80,6 +80,13 @@ def lib():
         L.axon_decode_step.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p, ctypes.c_void_p]
         L.axon_decode_step.restype = ctypes.c_int
+        L.axon_step.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
+                                ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p, ctypes.c_void_p,
+                                ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        L.axon_step.restype = ctypes.c_int
+        L.axon_reset_slot.argtypes = [ctypes.c_void_p, ctypes.c_int32]
+        L.axon_reset_slot.restype = ctypes.c_int
         L.axon_slot_lengths.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]
         L.axon_slot_lengths.restype = ctypes.c_int
         L.axon_timing_enable.argtypes = [ctypes.c_void_p, ctypes.c_int32]
@@ -199,6 +206,38 @@ class Model:
                                       logits.data_ptr() if logits is not None else None,
                                       next_tokens.data_ptr(), ctypes.c_void_p(_stream(stream))))
         return logits, next_tokens
+
+    def step(self, tokens: torch.Tensor, cu_seqlens: list, slots: list, fresh: list | None = None,
+             block_rows: torch.Tensor | None = None, logits: torch.Tensor | None = None,
+             next_tokens: torch.Tensor | None = None, want_logits: bool = True, stream=None):
+        """One continuous-batching step (axon_step).  tokens: device int32
+        [sum n_i]; cu_seqlens: host list of n+1 ints; slots / fresh: host lists
+        of n ints; block_rows: host int32 [n, stride] page rows (paged cache) or
+        None.  Returns (logits [n, V] or None, next_tokens [n])."""
+        dev = tokens.device
+        n = len(slots)
+        cu_h = (ctypes.c_int32 * (n + 1))(*[int(c) for c in cu_seqlens])
+        cu_d = torch.tensor([int(c) for c in cu_seqlens], dtype=torch.int32, device=dev)
+        sl_h = (ctypes.c_int32 * n)(*[int(x) for x in slots])
+        fr_h = (ctypes.c_int32 * n)(*[int(x) for x in fresh]) if fresh is not None else None
+        if logits is None and want_logits:
+            logits = torch.empty((n, self.vocab), dtype=torch.float32, device=dev)
+        if next_tokens is None:
+            next_tokens = torch.empty((n,), dtype=torch.int32, device=dev)
+        bt_ptr, stride = None, 0
+        if block_rows is not None:
+            bt = block_rows.to("cpu", torch.int32).contiguous()
+            stride = bt.shape[1]
+            bt_ptr = ctypes.cast(bt.data_ptr(), ctypes.POINTER(ctypes.c_int32))
+        _check(lib().axon_step(self._h, n, sl_h, fr_h, tokens.data_ptr(), cu_d.data_ptr(), cu_h, bt_ptr, stride,
+                               logits.data_ptr() if logits is not None else None, next_tokens.data_ptr(),
+                               ctypes.c_void_p(_stream(stream))))
+        self._keep = (cu_d, tokens)
+        return logits, next_tokens
+
+    def reset_slot(self, slot: int):
+        """Evict the sequence of ``slot`` (axon_reset_slot)."""
+        _check(lib().axon_reset_slot(self._h, int(slot)))
 
     def lengths(self) -> list[int]:
         buf = (ctypes.c_int32 * self.max_batch)()

@@ -167,6 +167,11 @@ struct axon_model {
   int32_t* am_idx = nullptr;
   int32_t* d_len = nullptr;
   std::vector<int> h_len;
+  // per-entry arrays of a continuous-batching step (6 x max_batch int32):
+  // slot, base position, chunk entries, single-token rows / slots / positions
+  int32_t* d_step = nullptr;
+  int32_t* h_step = nullptr;  // pinned staging copy
+  hipEvent_t step_copied = nullptr;
   int active = 0;
   hipStream_t cap_stream = nullptr;
   std::map<GraphKey, hipGraphExec_t> graphs;
@@ -259,6 +264,8 @@ void release(axon_model* m) {
   m->dev_allocs.clear();
   if (m->h_bt) (void)hipHostFree(m->h_bt);
   if (m->bt_copied) (void)hipEventDestroy(m->bt_copied);
+  if (m->h_step) (void)hipHostFree(m->h_step);
+  if (m->step_copied) (void)hipEventDestroy(m->step_copied);
   if (m->cap_stream) (void)hipStreamDestroy(m->cap_stream);
   delete m;
 }
@@ -296,6 +303,25 @@ void gemv_step(axon_model* m, const GemvArgs& a, int epi, hipStream_t s) {
                      " M=" + std::to_string(a.M) + " epilogue " + std::to_string(epi);
 }
 
+// A continuous-batching step: entry e appends tokens cu[e] .. cu[e+1]-1 to
+// slot slot[e] from position base[e].  Entries of >= 2 tokens (prompt chunks)
+// go through the prefill attention kernel, single tokens through the decode
+// attention kernel (one workgroup per (item, kv head) reads the slot's keys
+// once for the head group).
+struct StepPlan {
+  int n = 0;
+  const int32_t* d_slot = nullptr;
+  const int32_t* d_base = nullptr;
+  int nc = 0;                          // chunk entries
+  const int32_t* d_chunks = nullptr;
+  const int32_t* h_chunks = nullptr;
+  int nd = 0;                          // single-token entries
+  const int32_t* d_drow = nullptr;     // token row
+  const int32_t* d_dslot = nullptr;
+  const int32_t* d_dpos = nullptr;
+  int dctx = 0;                        // summed context of the single-token entries
+};
+
 // Epilogue arguments of the bf16 QKV GEMM with bias + RoPE + KV write fused:
 // prefill positions from cu (nseq sequences), decode positions from len.
 EpiArgs rope_epi(axon_model* m, const LayerW& w, const KVView& kv, const int32_t* cu, int nseq, const int32_t* len) {
@@ -312,27 +338,52 @@ EpiArgs rope_epi(axon_model* m, const LayerW& w, const KVView& kv, const int32_t
   return e;
 }
 
+// Prefill of B fresh sequences in slots 0..B-1, or (plan != nullptr) a
+// continuous-batching step of B entries.
 template <typename T>
 void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, const int32_t* d_cu,
-                     const int32_t* h_cu, int all_logits, float* d_logits, int32_t* d_next, hipStream_t s) {
+                     const int32_t* h_cu, int all_logits, float* d_logits, int32_t* d_next, hipStream_t s,
+                     const StepPlan* plan = nullptr) {
   const int D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V(), nq = m->nqkv();
   const float eps = m->cfg.rms_eps;
   T* h = (T*)m->h;
-  launch_set_lengths(d_cu, m->d_len, B, s);
+  const int32_t* ent_slot = plan ? plan->d_slot : nullptr;
+  const int32_t* ent_base = plan ? plan->d_base : nullptr;
+  if (plan) launch_set_step_lengths(d_cu, ent_slot, ent_base, m->d_len, B, s);
+  else launch_set_lengths(d_cu, m->d_len, B, s);
   launch_embed_rmsnorm<T>(d_tokens, (const T*)m->embed, (const T*)m->layers[0].gin, m->x, h, Ttok, D, V, eps, s);
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const LayerW& w = m->layers[l];
     KVView kv = m->kv(l, m->paged());
     if constexpr (sizeof(T) == 2) {
       // bias, RoPE and the KV-cache write in the QKV GEMM's epilogue
-      const EpiArgs re = rope_epi(m, w, kv, d_cu, B, nullptr);
+      EpiArgs re = rope_epi(m, w, kv, d_cu, B, nullptr);
+      re.ent_slot = ent_slot;
+      re.ent_base = ent_base;
       gemm_many<T>(m, w.wqkv, h, nq, Ttok, D, EPI_ROPE, nullptr, nullptr, nq, s, &re);
     } else {
       gemm_many<T>(m, w.wqkv, h, nq, Ttok, D, EPI_F32, m->qkv, nullptr, nq, s);
       launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, Ttok, B, d_cu,
-                        nullptr, H, s);
+                        nullptr, H, s, ent_slot, ent_base);
     }
-    m->timed(3, H, B, Ttok, s, [&] { launch_attn_prefill<T>((const T*)m->q, kv, (T*)m->o, Ttok, B, d_cu, h_cu, H, s); });
+    if (plan && sizeof(T) == 2) {
+      if (plan->nc > 0)
+        m->timed(3, H, plan->nc, Ttok, s, [&] {
+          launch_attn_prefill<T>((const T*)m->q, kv, (T*)m->o, Ttok, plan->nc, d_cu, h_cu, H, s, plan->d_chunks,
+                                 plan->h_chunks, ent_slot, ent_base);
+        });
+      if (plan->nd > 0)
+        m->timed(2, H, plan->nd, plan->dctx, s, [&] {
+          launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, plan->nd, H, plan->d_dpos,
+                                m->cfg.max_seq, s, plan->d_drow, plan->d_dslot);
+        });
+    } else {
+      // prefill, and every entry of a float32 step (its kernel is per token)
+      m->timed(3, H, B, Ttok, s, [&] {
+        launch_attn_prefill<T>((const T*)m->q, kv, (T*)m->o, Ttok, B, d_cu, h_cu, H, s, nullptr, nullptr, ent_slot,
+                               ent_base);
+      });
+    }
     gemm_many<T>(m, w.wo, m->o, D, Ttok, H * hd, EPI_RESID, m->x, nullptr, D, s);
     launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, Ttok, D, eps, nullptr, s);
     if constexpr (sizeof(T) == 2) {
@@ -742,6 +793,9 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     TRY(dev_alloc(m, (void**)&m->am_idx, nam * c.max_batch * 4));
     TRY(dev_alloc(m, (void**)&m->d_len, (size_t)c.max_batch * sizeof(int32_t)));
     HTRY(hipMemsetAsync(m->d_len, 0, (size_t)c.max_batch * sizeof(int32_t), s));
+    TRY(dev_alloc(m, (void**)&m->d_step, (size_t)6 * c.max_batch * sizeof(int32_t)));
+    HTRY(hipHostMalloc((void**)&m->h_step, (size_t)6 * c.max_batch * sizeof(int32_t), hipHostMallocDefault));
+    HTRY(hipEventCreateWithFlags(&m->step_copied, hipEventDisableTiming));
   }
   m->h_len.assign(c.max_batch, 0);
   HTRY(hipStreamCreateWithFlags(&m->cap_stream, hipStreamNonBlocking));
@@ -839,6 +893,7 @@ extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_t
                                      " active slots of the last prefill");
   for (int b = 0; b < batch; ++b) {
     const int pos = m->h_len[b];
+    if (pos < 1) return fail(AXON_E_INVALID, "slot " + std::to_string(b) + " holds no sequence");
     if (pos + 1 > m->cfg.max_seq)
       return fail(AXON_E_CAPACITY, "slot " + std::to_string(b) + " is full (max_seq " + std::to_string(m->cfg.max_seq) + ")");
     if (m->paged() && m->h_bt[(int64_t)b * m->bt_stride + pos / m->ps] < 0)
@@ -878,6 +933,158 @@ extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_t
     if (rc) return rc;
   }
   for (int b = 0; b < batch; ++b) m->h_len[b] += 1;
+  return AXON_OK;
+}
+
+extern "C" int axon_step(axon_model* m, int32_t n, const int32_t* h_slots, const int32_t* h_fresh,
+                         const int32_t* d_tokens, const int32_t* d_cu_seqlens, const int32_t* h_cu_seqlens,
+                         const int32_t* h_block_table, int32_t block_table_stride, float* d_logits,
+                         int32_t* d_next_tokens, void* stream) {
+  g_err.clear();
+  if (!m) return fail(AXON_E_INVALID, "model is NULL");
+  const axon_config& c = m->cfg;
+  if (n < 1) return fail(AXON_E_INVALID, "n must be >= 1");
+  if (n > c.max_batch)
+    return fail(AXON_E_CAPACITY, "n " + std::to_string(n) + " exceeds max_batch " + std::to_string(c.max_batch));
+  if (!h_slots || !d_tokens || !d_cu_seqlens || !h_cu_seqlens || !d_next_tokens)
+    return fail(AXON_E_INVALID, "h_slots, d_tokens, d_cu_seqlens, h_cu_seqlens and d_next_tokens must be non-NULL");
+  if (h_cu_seqlens[0] != 0) return fail(AXON_E_INVALID, "cu_seqlens[0] must be 0");
+  std::vector<char> seen(c.max_batch, 0);
+  std::vector<int> base(n), cnt(n);
+  int64_t total = 0;
+  for (int i = 0; i < n; ++i) {
+    const int sl = h_slots[i];
+    if (sl < 0 || sl >= c.max_batch)
+      return fail(AXON_E_INVALID, "entry " + std::to_string(i) + ": slot " + std::to_string(sl) + " out of range [0, " +
+                                      std::to_string(c.max_batch) + ")");
+    if (seen[sl]) return fail(AXON_E_INVALID, "slot " + std::to_string(sl) + " appears twice");
+    seen[sl] = 1;
+    const int fr = h_fresh ? h_fresh[i] : 0;
+    if (fr != 0 && fr != 1) return fail(AXON_E_INVALID, "h_fresh entries must be 0 or 1");
+    const int64_t ni = (int64_t)h_cu_seqlens[i + 1] - h_cu_seqlens[i];
+    if (ni < 1) return fail(AXON_E_INVALID, "entry " + std::to_string(i) + " has " + std::to_string(ni) + " tokens (must be >= 1)");
+    base[i] = fr ? 0 : m->h_len[sl];
+    cnt[i] = (int)ni;
+    if (base[i] + ni > c.max_seq)
+      return fail(AXON_E_CAPACITY, "slot " + std::to_string(sl) + ": " + std::to_string(base[i]) + " + " +
+                                       std::to_string(ni) + " tokens exceed max_seq " + std::to_string(c.max_seq));
+    total += ni;
+  }
+  if (total > m->rows)
+    return fail(AXON_E_CAPACITY, "step of " + std::to_string(total) + " tokens exceeds max_tokens " + std::to_string(m->rows));
+  hipStream_t s = (hipStream_t)stream;
+  if (m->paged()) {
+    const int cols = h_block_table ? std::min(block_table_stride, m->bt_stride) : m->bt_stride;
+    if (h_block_table && block_table_stride < 1) return fail(AXON_E_INVALID, "block_table_stride must be >= 1");
+    // the rows each entry's slot will have after the call
+    auto row_of = [&](int i, int j) -> int {
+      if (h_block_table) return j < cols ? h_block_table[(int64_t)i * block_table_stride + j] : -1;
+      return m->h_bt[(int64_t)h_slots[i] * m->bt_stride + j];
+    };
+    std::vector<char> used(c.kv_num_pages, 0);
+    // pages of the slots this call leaves alone
+    for (int sl = 0; sl < c.max_batch; ++sl) {
+      if (seen[sl]) continue;
+      for (int j = 0; j < m->bt_stride; ++j) {
+        const int p = m->h_bt[(int64_t)sl * m->bt_stride + j];
+        if (p >= 0) used[p] = 1;
+      }
+    }
+    for (int i = 0; i < n; ++i) {
+      const int sl = h_slots[i];
+      const int need = (base[i] + cnt[i] + m->ps - 1) / m->ps;
+      const int kept = (base[i] + m->ps - 1) / m->ps;  // pages holding the slot's cached positions
+      if (need > cols)
+        return fail(AXON_E_CAPACITY, "entry " + std::to_string(i) + " needs " + std::to_string(need) +
+                                         " pages, the page table has " + std::to_string(cols) + " columns");
+      for (int j = 0; j < m->bt_stride; ++j) {
+        const int p = row_of(i, j);
+        if (j < kept && p != m->h_bt[(int64_t)sl * m->bt_stride + j])
+          return fail(AXON_E_INVALID, "entry " + std::to_string(i) + " changes page " + std::to_string(j) +
+                                          " that holds cached positions of slot " + std::to_string(sl));
+        if (p < 0) {
+          if (j < need)
+            return fail(AXON_E_CAPACITY, "slot " + std::to_string(sl) + " has no page for block " + std::to_string(j));
+          continue;
+        }
+        if (p >= c.kv_num_pages)
+          return fail(AXON_E_CAPACITY, "page id " + std::to_string(p) + " out of range [0, " + std::to_string(c.kv_num_pages) + ")");
+        if (used[p]) return fail(AXON_E_INVALID, "page id " + std::to_string(p) + " appears twice");
+        used[p] = 1;
+      }
+    }
+    if (h_block_table) {
+      HIP_TRY(hipEventSynchronize(m->bt_copied));
+      for (int i = 0; i < n; ++i)
+        for (int j = 0; j < m->bt_stride; ++j) m->h_bt[(int64_t)h_slots[i] * m->bt_stride + j] = row_of(i, j);
+      HIP_TRY(hipMemcpyAsync(m->d_bt, m->h_bt, (size_t)c.max_batch * m->bt_stride * sizeof(int32_t),
+                             hipMemcpyHostToDevice, s));
+      HIP_TRY(hipEventRecord(m->bt_copied, s));
+    }
+  } else if (h_block_table) {
+    return fail(AXON_E_INVALID, "h_block_table given for a contiguous cache");
+  }
+  // per-entry arrays: staged in pinned memory (after the previous step's copy
+  // has left it), copied in one transfer
+  HIP_TRY(hipEventSynchronize(m->step_copied));
+  StepPlan plan;
+  const int MB = c.max_batch;
+  int32_t* hs = m->h_step;
+  int nc = 0, nd = 0;
+  for (int i = 0; i < n; ++i) {
+    hs[i] = h_slots[i];
+    hs[MB + i] = base[i];
+    if (cnt[i] > 1 || !m->bf) {
+      hs[2 * MB + nc++] = i;
+    } else {
+      hs[3 * MB + nd] = h_cu_seqlens[i];
+      hs[4 * MB + nd] = h_slots[i];
+      hs[5 * MB + nd] = base[i];
+      ++nd;
+      plan.dctx += base[i] + 1;
+    }
+  }
+  HIP_TRY(hipMemcpyAsync(m->d_step, hs, (size_t)6 * MB * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  HIP_TRY(hipEventRecord(m->step_copied, s));
+  plan.n = n;
+  plan.d_slot = m->d_step;
+  plan.d_base = m->d_step + MB;
+  plan.nc = nc;
+  plan.d_chunks = m->d_step + 2 * MB;
+  plan.h_chunks = hs + 2 * MB;
+  plan.nd = nd;
+  plan.d_drow = m->d_step + 3 * MB;
+  plan.d_dslot = m->d_step + 4 * MB;
+  plan.d_dpos = m->d_step + 5 * MB;
+  if (m->bf)
+    enqueue_prefill<bf16>(m, n, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, 0, d_logits, d_next_tokens, s,
+                          &plan);
+  else
+    enqueue_prefill<float>(m, n, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, 0, d_logits, d_next_tokens, s,
+                           &plan);
+  int rc = check_launch("step");
+  if (!rc) rc = take_enqueue_err(m, "step");
+  if (rc) return rc;
+  int top = 0;
+  for (int i = 0; i < n; ++i) {
+    m->h_len[h_slots[i]] = base[i] + cnt[i];
+    top = std::max(top, h_slots[i] + 1);
+  }
+  m->active = std::max(m->active, top);
+  return AXON_OK;
+}
+
+extern "C" int axon_reset_slot(axon_model* m, int32_t slot) {
+  g_err.clear();
+  if (!m) return fail(AXON_E_INVALID, "model is NULL");
+  if (slot < 0 || slot >= m->cfg.max_batch)
+    return fail(AXON_E_INVALID, "slot " + std::to_string(slot) + " out of range [0, " + std::to_string(m->cfg.max_batch) + ")");
+  m->h_len[slot] = 0;
+  if (m->paged()) {
+    // host view only: the device row is rewritten when the slot is next given pages
+    HIP_TRY(hipEventSynchronize(m->bt_copied));
+    for (int j = 0; j < m->bt_stride; ++j) m->h_bt[(int64_t)slot * m->bt_stride + j] = -1;
+  }
   return AXON_OK;
 }
 

@@ -68,10 +68,18 @@ AXON_DEV int pswz(int r, int c) {
   else return c ^ ((r >> 1) & 7);  // 8 chunks: rows r and r+1 share a 256-byte bank line
 }
 
+// Entries: the workgroups cover the entries listed in ``ents`` (all nseq
+// entries in order when null).  Entry e holds tokens cu[e] .. cu[e+1]-1 of
+// slot ent_slot[e] (e when null) at positions ent_base[e] .. (0 when null):
+// queries attend to keys 0 .. their own position of that slot, the keys
+// before ent_base[e] written by earlier calls (a chunked prefill).
 template <int HD, int QB>
 __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel(const bf16* __restrict__ q, KVView kv,
                                                                    bf16* __restrict__ o, int nseq,
-                                                                   const int32_t* __restrict__ cu, int H) {
+                                                                   const int32_t* __restrict__ cu, int H,
+                                                                   const int32_t* __restrict__ ents,
+                                                                   const int32_t* __restrict__ ent_slot,
+                                                                   const int32_t* __restrict__ ent_base) {
   constexpr int KCH = HD / 8;            // 16-byte chunks per K row
   constexpr int VCH = PK / 8;            // chunks per V^T row (8)
   constexpr int KT = PK * KCH;           // chunks per K tile
@@ -81,18 +89,22 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
   constexpr int TQ = 4 * WQ;             // queries per workgroup
   __shared__ bf16x8 lds[2 * BUF];
 
-  // locate (sequence, query tile) of this workgroup
-  int seq = 0, tile = blockIdx.x;
-  for (; seq < nseq; ++seq) {
-    const int nt = (cu[seq + 1] - cu[seq] + TQ - 1) / TQ;
+  // locate (entry, query tile) of this workgroup
+  int li = 0, tile = blockIdx.x, ent = 0;
+  for (; li < nseq; ++li) {
+    ent = ents ? ents[li] : li;
+    const int nt = (cu[ent + 1] - cu[ent] + TQ - 1) / TQ;
     if (tile < nt) break;
     tile -= nt;
   }
   const int head = blockIdx.y;
   const int group = H / kv.kv_heads;
   const int kvh = head / group;
-  const int S = cu[seq + 1] - cu[seq];
-  const int tok0 = cu[seq];
+  const int S = cu[ent + 1] - cu[ent];         // this call's queries of the entry
+  const int tok0 = cu[ent];
+  const int seq = ent_slot ? ent_slot[ent] : ent;  // cache slot
+  const int base = ent_base ? ent_base[ent] : 0;   // position of the entry's first query
+  const int KL = base + S;                         // keys of the slot after this call
   const int q0 = tile * TQ;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qw0 = q0 + wave * WQ;  // this wavefront's queries: QB blocks of 32
@@ -117,12 +129,12 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
     const int j0 = kt * PK;
     int64_t pg[4];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) pg[g] = kv_page_uniform(kv, seq, min(j0 + g * 16, S - 1) & ~15);
+    for (int g = 0; g < 4; ++g) pg[g] = kv_page_uniform(kv, seq, min(j0 + g * 16, KL - 1) & ~15);
 #pragma unroll
     for (int i = 0; i < KT / 256; ++i) {
       const int p = (i * 4 + wave) * 64 + lane;
       const int r = p / KCH, c = pswz<KCH>(r, p % KCH);  // pswz is its own inverse
-      const int key = min(j0 + r, S - 1);                 // in [j0, j0 + 64): j0 < S
+      const int key = min(j0 + r, KL - 1);                // in [j0, j0 + 64): j0 < KL
       const int64_t page = pg[(key - j0) >> 4];
       const int kp = key % kv.ps;
       const bf16* src = kb + ((page * kv.kv_heads + kvh) * kv.ps + (kp & ~15)) * HD + c * 128 + (kp & 15) * 8;
@@ -134,7 +146,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
     for (int i = 0; i < VT / 256; ++i) {
       const int p = (i * 4 + wave) * 64 + lane;
       const int d = p / VCH, c = pswz<VCH>(d, p % VCH);
-      const int key = min(j0 + c * 8, (S - 1) & ~7);  // 8 keys of one 16-key group, in [j0, j0 + 64)
+      const int key = min(j0 + c * 8, (KL - 1) & ~7);  // 8 keys of one 16-key group, in [j0, j0 + 64)
       const int64_t page = pg[(key - j0) >> 4];
       const int kp = key % kv.ps;
       const bf16* src = vb + ((page * kv.kv_heads + kvh) * kv.ps + (kp & ~15)) * HD + d * 16 + (kp & 15);
@@ -155,7 +167,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
   }
   const float sc = LOG2E / sqrtf((float)HD);
 
-  const int kend = min(S, q0 + TQ);  // keys needed by the workgroup
+  const int kend = base + min(S, q0 + TQ);  // keys needed by the workgroup
   const int ntiles = (kend + PK - 1) / PK;
   issue(0, 0);
   for (int kt = 0; kt < ntiles; ++kt) {
@@ -165,7 +177,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
     if (kt + 1 < ntiles) issue(kt + 1, b ^ 1);
     const bf16x8* ks = lds + b * BUF;
     const bf16* vsb = (const bf16*)(ks + KT);
-    if (j0 > qw0 + WQ - 1 || qw0 >= S) continue;  // every key of the tile is after this wavefront's queries
+    if (j0 > base + qw0 + WQ - 1 || qw0 >= S) continue;  // every key of the tile is after this wavefront's queries
     // ---- S^T = K Q^T: each K fragment serves the QB query blocks
     f32x16 s[QB][2];
 #pragma unroll
@@ -188,7 +200,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
     //      exceeds it by more than 8 (in log2 units): probabilities stay <= 2^8
     //      and the accumulator is rescaled rarely, not every tile (the sum and
     //      the accumulator always share the reference, so the result is exact).
-    const bool masked = j0 + PK - 1 > qw0 || j0 + PK > S;
+    const bool masked = j0 + PK - 1 > base + qw0 || j0 + PK > KL;
     bf16x8 pb[QB][2][2];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -200,7 +212,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const int key = j0 + r * 32 + (i / 4) * 8 + hl * 4 + (i % 4);
-            const float v = (key <= myq && key < S) ? s[qb][r][i] : -INFINITY;
+            const float v = (key <= base + myq && key < KL) ? s[qb][r][i] : -INFINITY;
             s[qb][r][i] = v;
             mloc = fmaxf(mloc, v);
           }
@@ -282,13 +294,17 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
 // partial and the combine kernel merges them.
 // ============================================================================
 
+// Item b: query row rows[b] (b when null) of q / o, cache slot slots[b] (b
+// when null), position len[b].
 template <int HD, int DNW, bool PAGED, int NBUF>
 __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* __restrict__ q, KVView kv,
                                                                     bf16* __restrict__ o, float* __restrict__ part,
                                                                     int H, const int32_t* __restrict__ len,
-                                                                    int split_len) {
+                                                                    int split_len, const int32_t* __restrict__ rows,
+                                                                    const int32_t* __restrict__ slots) {
   extern __shared__ float dyn[];
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int row = rows ? rows[b] : b, slot = slots ? slots[b] : b;
   const int nsplit = gridDim.x;
   const int ctx = len[b] + 1;
   const int s0 = split * split_len;
@@ -307,7 +323,7 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
   // head columns past the group read the group's last head (never stored)
   bf16x8 qf[HD / 32];
   {
-    const bf16* qp = q + ((int64_t)b * H + kvh * group + min(col, group - 1)) * HD + gq * 8;
+    const bf16* qp = q + ((int64_t)row * H + kvh * group + min(col, group - 1)) * HD + gq * 8;
 #pragma unroll
     for (int k = 0; k < HD / 32; ++k) qf[k] = *(const bf16x8*)(qp + k * 32);
   }
@@ -332,7 +348,7 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
       const int hs = min(j0 + blk * 16, (s1 - 1) & ~15);  // a 16-key block of the context
-      const int64_t pg = kv_page_of<PAGED>(kv, b, hs);
+      const int64_t pg = kv_page_of<PAGED>(kv, slot, hs);
       kbase[blk] = ((pg * kv.kv_heads + kvh) * kv.ps + hs % kv.ps) * HD;
     }
     // K fragment (key col, dims 32k + 8gq ..): 16 bytes at lane * 16 of the
@@ -448,7 +464,7 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
     }
     const int h = kvh * group + c;
     if (nsplit == 1) {
-      o[((int64_t)b * H + h) * HD + d] = (bf16)(O / L);
+      o[((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
     } else {
       float* pp = part + (((int64_t)b * H + h) * nsplit + split) * (HD + 2);
       pp[d] = O;
@@ -465,8 +481,9 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
 template <int HD>
 __global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restrict__ part, bf16* __restrict__ o, int H,
                                                           const int32_t* __restrict__ len, int nsplit,
-                                                          int split_len) {
+                                                          int split_len, const int32_t* __restrict__ rows) {
   const int b = blockIdx.y, h = blockIdx.x, d = threadIdx.x;
+  const int row = rows ? rows[b] : b;
   const int ctx = len[b] + 1;
   const int nact = min(nsplit, (ctx + split_len - 1) / split_len);
   const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
@@ -478,7 +495,7 @@ __global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restric
     L += f * pp[sp * (HD + 2) + HD + 1];
     O += f * pp[sp * (HD + 2) + d];
   }
-  o[((int64_t)b * H + h) * HD + d] = (bf16)(O / L);
+  o[((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
 }
 
 // ============================================================================
@@ -490,7 +507,9 @@ __global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restric
 template <int HD>
 __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ q, KVView kv, float* __restrict__ o,
                                                       int T_tokens, int nseq, const int32_t* __restrict__ cu,
-                                                      const int32_t* __restrict__ len, int H) {
+                                                      const int32_t* __restrict__ len, int H,
+                                                      const int32_t* __restrict__ ent_slot,
+                                                      const int32_t* __restrict__ ent_base) {
   constexpr int DL = HD / 64;  // output dimensions per lane
   __shared__ float qs[HD];
   __shared__ float ps[64];
@@ -500,8 +519,9 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ 
     slot = t;
     pos = len[t];
   } else {
-    slot = seq_of_token(cu, nseq, t);
-    pos = t - cu[slot];
+    const int e = seq_of_token(cu, nseq, t);
+    slot = ent_slot ? ent_slot[e] : e;
+    pos = (ent_base ? ent_base[e] : 0) + t - cu[e];
   }
   const int kvh = head / (H / kv.kv_heads);
   const float* qp = q + ((int64_t)t * H + head) * HD;
@@ -553,19 +573,27 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ 
 
 template <typename T>
 void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, const int32_t* cu,
-                         const int32_t* h_cu, int H, hipStream_t s) {
-  if (T_tokens <= 0) return;
+                         const int32_t* h_cu, int H, hipStream_t s, const int32_t* ents, const int32_t* h_ents,
+                         const int32_t* ent_slot, const int32_t* ent_base) {
+  if (T_tokens <= 0 || nseq <= 0) return;
   if constexpr (sizeof(T) == 4) {
     dim3 grid(T_tokens, H);
-    if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H);
-    else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H);
+    if (kv.hd == 64)
+      attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H, ent_slot, ent_base);
+    else
+      attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H, ent_slot, ent_base);
   } else {
     constexpr int QB = PREFILL_QB, TQ = 4 * 32 * QB;
     int tiles = 0;
-    for (int b = 0; b < nseq; ++b) tiles += (h_cu[b + 1] - h_cu[b] + TQ - 1) / TQ;
+    for (int i = 0; i < nseq; ++i) {
+      const int e = h_ents ? h_ents[i] : i;
+      tiles += (h_cu[e + 1] - h_cu[e] + TQ - 1) / TQ;
+    }
     dim3 grid(tiles, H);
-    if (kv.hd == 64) attn_prefill_bf16_kernel<64, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H);
-    else attn_prefill_bf16_kernel<128, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H);
+    if (kv.hd == 64)
+      attn_prefill_bf16_kernel<64, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base);
+    else
+      attn_prefill_bf16_kernel<128, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base);
   }
 }
 
@@ -587,41 +615,43 @@ int plan_decode_splits(int B, int kv_heads, int max_ctx) {
 
 template <int HD, int NW>
 static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int B, int H, const int32_t* len,
-                          int nsplit, int split_len, hipStream_t s) {
+                          int nsplit, int split_len, hipStream_t s, const int32_t* rows, const int32_t* slots) {
   const int group = H / kv.kv_heads;
   const size_t lds = (size_t)(2 * NW * 16 + NW * group * HD) * sizeof(float);
   const dim3 grid(nsplit, kv.kv_heads, B);
   constexpr int NBUF = 2;  // chunks in flight per wavefront (3-4 measured slower: clamped duplicate loads, registers)
   if (kv.bt)
-    attn_decode_bf16_kernel<HD, NW, true, NBUF><<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len);
+    attn_decode_bf16_kernel<HD, NW, true, NBUF>
+        <<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len, rows, slots);
   else
-    attn_decode_bf16_kernel<HD, NW, false, NBUF><<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len);
-  if (nsplit > 1) attn_combine_kernel<HD><<<dim3(H, B), HD, 0, s>>>(part, o, H, len, nsplit, split_len);
+    attn_decode_bf16_kernel<HD, NW, false, NBUF>
+        <<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len, rows, slots);
+  if (nsplit > 1) attn_combine_kernel<HD><<<dim3(H, B), HD, 0, s>>>(part, o, H, len, nsplit, split_len, rows);
 }
 
 template <typename T>
 void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len, int max_ctx,
-                        hipStream_t s) {
+                        hipStream_t s, const int32_t* rows, const int32_t* slots) {
   if (B <= 0) return;
   if constexpr (sizeof(T) == 4) {
-    dim3 grid(B, H);
-    if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H);
-    else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H);
+    dim3 grid(B, H);  // the float32 path takes rows / slots through launch_attn_prefill
+    if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H, nullptr, nullptr);
+    else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H, nullptr, nullptr);
   } else {
     const int nsplit = plan_decode_splits(B, kv.kv_heads, max_ctx);
     const int split_len = ((max_ctx + nsplit - 1) / nsplit + 63) / 64 * 64;
-    if (kv.hd == 64) decode_launch<64, DECODE_WAVES>(q, kv, o, part, B, H, len, nsplit, split_len, s);
-    else decode_launch<128, DECODE_WAVES>(q, kv, o, part, B, H, len, nsplit, split_len, s);
+    if (kv.hd == 64) decode_launch<64, DECODE_WAVES>(q, kv, o, part, B, H, len, nsplit, split_len, s, rows, slots);
+    else decode_launch<128, DECODE_WAVES>(q, kv, o, part, B, H, len, nsplit, split_len, s, rows, slots);
   }
 }
 
 template void launch_attn_prefill<float>(const float*, KVView, float*, int, int, const int32_t*, const int32_t*, int,
-                                         hipStream_t);
+                                         hipStream_t, const int32_t*, const int32_t*, const int32_t*, const int32_t*);
 template void launch_attn_prefill<bf16>(const bf16*, KVView, bf16*, int, int, const int32_t*, const int32_t*, int,
-                                        hipStream_t);
+                                        hipStream_t, const int32_t*, const int32_t*, const int32_t*, const int32_t*);
 template void launch_attn_decode<float>(const float*, KVView, float*, float*, int, int, const int32_t*, int,
-                                        hipStream_t);
+                                        hipStream_t, const int32_t*, const int32_t*);
 template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int, int, const int32_t*, int,
-                                       hipStream_t);
+                                       hipStream_t, const int32_t*, const int32_t*);
 
 }  // namespace axon

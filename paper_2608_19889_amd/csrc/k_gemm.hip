@@ -43,8 +43,9 @@ AXON_DEV void rope_block(const EpiArgs& ep, int nb, int t, const f32x16& v, int 
     slot = t;
     pos = ep.len[t];
   } else {
-    slot = seq_of_token(ep.cu, ep.nseq, t);
-    pos = t - ep.cu[slot];
+    const int e = seq_of_token(ep.cu, ep.nseq, t);
+    slot = ep.ent_slot ? ep.ent_slot[e] : e;
+    pos = (ep.ent_base ? ep.ent_base[e] : 0) + t - ep.cu[e];
   }
 #pragma unroll
   for (int g = 0; g < 4; ++g) {

@@ -124,6 +124,12 @@ __global__ void set_lengths_kernel(const int32_t* __restrict__ cu, int32_t* __re
   if (b < n) len[b] = cu[b + 1] - cu[b];
 }
 
+__global__ void set_step_lengths_kernel(const int32_t* __restrict__ cu, const int32_t* __restrict__ ent_slot,
+                                        const int32_t* __restrict__ ent_base, int32_t* __restrict__ len, int n) {
+  int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < n) len[ent_slot[e]] = ent_base[e] + cu[e + 1] - cu[e];
+}
+
 // ---------------------------------------------------------------- launchers
 
 template <typename T>
@@ -153,6 +159,12 @@ void launch_argmax_rows(const float* logits, int nseq, int V, int32_t* next, con
 void launch_set_lengths(const int32_t* cu, int32_t* len, int n, hipStream_t s) {
   if (n <= 0) return;
   set_lengths_kernel<<<(n + 255) / 256, 256, 0, s>>>(cu, len, n);
+}
+
+void launch_set_step_lengths(const int32_t* cu, const int32_t* ent_slot, const int32_t* ent_base, int32_t* len,
+                             int n, hipStream_t s) {
+  if (n <= 0) return;
+  set_step_lengths_kernel<<<(n + 255) / 256, 256, 0, s>>>(cu, ent_slot, ent_base, len, n);
 }
 
 template void launch_embed_rmsnorm<float>(const int32_t*, const float*, const float*, float*, float*, int, int,

@@ -16,13 +16,15 @@ namespace axon {
 constexpr int ROPE_TT = 16;  // tokens per workgroup
 
 AXON_DEV void token_slot_pos(int t, int nseq, const int32_t* __restrict__ cu, const int32_t* __restrict__ len,
-                             int& slot, int& pos) {
+                             const int32_t* __restrict__ ent_slot, const int32_t* __restrict__ ent_base, int& slot,
+                             int& pos) {
   if (len) {
     slot = t;
     pos = len[t];
   } else {
-    slot = seq_of_token(cu, nseq, t);
-    pos = t - cu[slot];
+    const int e = seq_of_token(cu, nseq, t);
+    slot = ent_slot ? ent_slot[e] : e;
+    pos = (ent_base ? ent_base[e] : 0) + t - cu[e];
   }
 }
 
@@ -40,7 +42,9 @@ __global__ void __launch_bounds__(256) rope_kv_kernel(const float* __restrict__ 
                                                       const float* __restrict__ sin_t, T* __restrict__ q_out,
                                                       KVView kv, int T_tokens, int nseq,
                                                       const int32_t* __restrict__ cu,
-                                                      const int32_t* __restrict__ len, int H) {
+                                                      const int32_t* __restrict__ len, int H,
+                                                      const int32_t* __restrict__ ent_slot,
+                                                      const int32_t* __restrict__ ent_base) {
   __shared__ float vt[ROPE_TT][HD + 1];
   const int KVh = kv.kv_heads;
   const int nqkv = (H + 2 * KVh) * HD;
@@ -61,7 +65,7 @@ __global__ void __launch_bounds__(256) rope_kv_kernel(const float* __restrict__ 
       const int t = t0 + idx / HALF, i = idx % HALF;
       if (t >= T_tokens) continue;
       int slot, pos;
-      token_slot_pos(t, nseq, cu, len, slot, pos);
+      token_slot_pos(t, nseq, cu, len, ent_slot, ent_base, slot, pos);
       const float x1 = val(t, i), x2 = val(t, i + HALF);
       const float c = cos_t[(int64_t)pos * HALF + i], s = sin_t[(int64_t)pos * HALF + i];
       const float y1 = x1 * c - x2 * s, y2 = x2 * c + x1 * s;
@@ -87,7 +91,7 @@ __global__ void __launch_bounds__(256) rope_kv_kernel(const float* __restrict__ 
       const int t = t0 + tt;
       if (t >= T_tokens) continue;
       int slot, pos;
-      token_slot_pos(t, nseq, cu, len, slot, pos);
+      token_slot_pos(t, nseq, cu, len, ent_slot, ent_base, slot, pos);
       ((T*)kv.v)[v_el(kv, slot, kvh, pos, d)] = from_f32<T>(vt[tt][d]);
     }
   }
@@ -96,20 +100,22 @@ __global__ void __launch_bounds__(256) rope_kv_kernel(const float* __restrict__ 
 template <typename T>
 void launch_rope_kv(const float* parts, int nparts, int64_t part_stride, const T* bias, const float* cos_t,
                     const float* sin_t, T* q_out, KVView kv, int T_tokens, int nseq, const int32_t* cu,
-                    const int32_t* len, int H, hipStream_t s) {
+                    const int32_t* len, int H, hipStream_t s, const int32_t* ent_slot, const int32_t* ent_base) {
   if (T_tokens <= 0) return;
   dim3 grid((T_tokens + ROPE_TT - 1) / ROPE_TT, H + 2 * kv.kv_heads);
   if (kv.hd == 64)
     rope_kv_kernel<T, 64><<<grid, 256, 0, s>>>(parts, nparts, part_stride, bias, cos_t, sin_t, q_out, kv,
-                                               T_tokens, nseq, cu, len, H);
+                                               T_tokens, nseq, cu, len, H, ent_slot, ent_base);
   else
     rope_kv_kernel<T, 128><<<grid, 256, 0, s>>>(parts, nparts, part_stride, bias, cos_t, sin_t, q_out, kv,
-                                                T_tokens, nseq, cu, len, H);
+                                                T_tokens, nseq, cu, len, H, ent_slot, ent_base);
 }
 
 template void launch_rope_kv<float>(const float*, int, int64_t, const float*, const float*, const float*, float*,
-                                    KVView, int, int, const int32_t*, const int32_t*, int, hipStream_t);
+                                    KVView, int, int, const int32_t*, const int32_t*, int, hipStream_t,
+                                    const int32_t*, const int32_t*);
 template void launch_rope_kv<bf16>(const float*, int, int64_t, const bf16*, const float*, const float*, bf16*,
-                                   KVView, int, int, const int32_t*, const int32_t*, int, hipStream_t);
+                                   KVView, int, int, const int32_t*, const int32_t*, int, hipStream_t,
+                                   const int32_t*, const int32_t*);
 
 }  // namespace axon

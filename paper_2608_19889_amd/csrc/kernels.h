@@ -56,6 +56,10 @@ struct EpiArgs {
   int nseq;
   const int32_t* len;
   int H;
+  // prefill entry e (tokens cu[e] .. cu[e+1]-1): cache slot ent_slot[e] and
+  // position of its first token ent_base[e]; null: slot e, position 0
+  const int32_t* ent_slot;
+  const int32_t* ent_base;
 };
 
 // ---- weight layout (k_layout.hip): fragment-tiled copy of row-major bf16
@@ -73,6 +77,9 @@ void launch_argmax(const float* logits, int rows, int V, int32_t* next, int32_t*
 // argmax of row cu[i+1]-1 for each sequence i
 void launch_argmax_rows(const float* logits, int nseq, int V, int32_t* next, const int32_t* cu, hipStream_t s);
 void launch_set_lengths(const int32_t* cu, int32_t* len, int n, hipStream_t s);
+// len[ent_slot[e]] = ent_base[e] + cu[e+1] - cu[e] for the n entries of a step
+void launch_set_step_lengths(const int32_t* cu, const int32_t* ent_slot, const int32_t* ent_base, int32_t* len,
+                             int n, hipStream_t s);
 
 // ---- projections (k_gemm.hip)
 // Many-token GEMM (prefill): bf16 MFMA tiles.  Requires K % 64 == 0, N % 32 == 0
@@ -142,26 +149,37 @@ void launch_embed_ss(const int32_t* tok, const bf16* emb, const bf16* g, float* 
 
 // ---- bias + rotary + KV-cache write (k_rope.hip)
 // qkv rows are sum_s parts[s][t][:] (+ bias): q heads, then k heads, then v heads.
-// Token t belongs to sequence seq(t) at position pos(t): prefill uses cu
-// (positions restart at 0 per sequence), decode (len != nullptr) uses slot t at
-// position len[t].
+// Token t belongs to entry e(t) of cu: prefill puts it in slot ent_slot[e] at
+// position ent_base[e] + t - cu[e] (slot e, position t - cu[e] when the arrays
+// are null); decode (len != nullptr) uses slot t at position len[t].
 template <typename T>
 void launch_rope_kv(const float* parts, int nparts, int64_t part_stride, const T* bias, const float* cos_t,
                     const float* sin_t, T* q_out, KVView kv, int T_tokens, int nseq, const int32_t* cu,
-                    const int32_t* len, int H, hipStream_t s);
+                    const int32_t* len, int H, hipStream_t s, const int32_t* ent_slot = nullptr,
+                    const int32_t* ent_base = nullptr);
 
 // ---- attention (k_attn.hip)
-// Causal prefill attention over the cache; o [T][H*hd].
+// Causal prefill attention over the cache; o [T][H*hd].  The workgroups cover
+// the nseq entries listed in ents (device) / h_ents (host copy), or entries
+// 0..nseq-1 when both are null; entry e's tokens cu[e] .. cu[e+1]-1 are at
+// positions ent_base[e] + 0, 1, ... of slot ent_slot[e] and attend to every
+// earlier key of that slot (null arrays: slot e from position 0).
 template <typename T>
 void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, const int32_t* cu,
-                         const int32_t* h_cu, int H, hipStream_t s);
+                         const int32_t* h_cu, int H, hipStream_t s, const int32_t* ents = nullptr,
+                         const int32_t* h_ents = nullptr, const int32_t* ent_slot = nullptr,
+                         const int32_t* ent_base = nullptr);
 // Decode attention: one query per slot at position len[b] (after the step's
 // key/value were written), context len[b] + 1; keys split over
 // plan_decode_splits() workgroups per (slot, kv head).  ``part`` holds
 // B * H * splits * (hd + 2) floats.
 int plan_decode_splits(int B, int kv_heads, int max_ctx);
+// Item b reads query row rows[b] and writes output row rows[b] (b when null),
+// in cache slot slots[b] (b when null), at position len[b]; bf16 only for the
+// indirection (the float32 path reaches such items through launch_attn_prefill).
 template <typename T>
 void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len,
-                        int max_ctx, hipStream_t s);
+                        int max_ctx, hipStream_t s, const int32_t* rows = nullptr,
+                        const int32_t* slots = nullptr);
 
 }  // namespace axon

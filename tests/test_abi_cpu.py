@@ -163,3 +163,13 @@ def test_no_cpu_fallback_in_binding():
     src = open(os.path.join(ROOT, "paper_2608_19889_amd", "axon.py")).read()
     for forbidden in ("oracle", "torch.matmul", "softmax", "F.linear", "@ "):
         assert forbidden not in src, forbidden
+
+
+def test_step_and_reset_reject_a_null_model():
+    """The continuous-batching calls validate on the host before touching a GPU."""
+    lib = axon.lib()
+    cu = (ctypes.c_int32 * 2)(0, 1)
+    sl = (ctypes.c_int32 * 1)(0)
+    rc = lib.axon_step(None, 1, sl, None, None, None, cu, None, 0, None, None, None)
+    assert rc == axon.AXON_E_INVALID and "NULL" in axon.last_error()
+    assert lib.axon_reset_slot(None, 0) == axon.AXON_E_INVALID

@@ -223,6 +223,31 @@ def test_incremental_decode_equals_full_recompute(kind):
     np.testing.assert_allclose(m2.extend(0, seq[3:]), full[3:], atol=1e-10)
 
 
+def test_slot_reset_and_admission_equal_fresh_sequences():
+    """Continuous batching on the oracle: a slot that is reset and fed a new
+    prompt in chunks gives the logits of a fresh prefill of that prompt, and
+    the other slots are unaffected by it."""
+    shp = _tiny("qwen")
+    w = _np_weights(shp)
+    a = RNG.integers(0, shp["vocab_size"], 10)
+    b = RNG.integers(0, shp["vocab_size"], 7)
+    c = RNG.integers(0, shp["vocab_size"], 9)
+    fresh_b = OracleDecoder(shp, w).prefill([b], all_logits=True)[0]
+    fresh_c = OracleDecoder(shp, w).prefill([c], all_logits=True)[0]
+    full_a = OracleDecoder(shp, w).prefill([a], all_logits=True)[0]
+    m = OracleDecoder(shp, w)
+    m.prefill([a[:4], b])
+    m.reset(1)                       # evict b
+    got_c1 = m.extend(1, c[:5])      # admit c in its slot, in two chunks
+    got_a = m.extend(0, a[4:])       # slot 0 continues meanwhile
+    got_c2 = m.extend(1, c[5:])
+    np.testing.assert_allclose(np.concatenate([got_c1, got_c2]), fresh_c, atol=1e-12)
+    np.testing.assert_allclose(got_a, full_a[4:], atol=1e-12)
+    got_b = m.extend(3, b)           # a slot never used before starts empty
+    np.testing.assert_allclose(got_b, fresh_b, atol=1e-12)
+    assert m.lengths() == [len(a), len(c), 0, len(b)]
+
+
 @pytest.mark.parametrize("kind", ["llama", "qwen"])
 def test_causal_prefix_invariance_and_batch_independence(kind):
     shp = _tiny(kind)
