@@ -120,8 +120,9 @@ struct GraphKey {
   const void* tok;
   const void* logits;
   const void* next;
+  const void* cu = nullptr;  // decode-only continuous-batching step: its cu_seqlens
   bool operator<(const GraphKey& o) const {
-    return std::tie(batch, tok, logits, next) < std::tie(o.batch, o.tok, o.logits, o.next);
+    return std::tie(batch, tok, logits, next, cu) < std::tie(o.batch, o.tok, o.logits, o.next, o.cu);
   }
 };
 
@@ -468,9 +469,13 @@ void enqueue_decode_many(axon_model* m, int B, const int32_t* d_tokens, float* d
 //              O (x += ; sums of squares) -> gate/up (RMSNorm on load; SiLU) ->
 //              down (x += ; sums of squares)
 //   head (RMSNorm on load; logits + argmax partials) -> argmax
+//   plan != nullptr: a step of single-token entries: item b is at position
+//   plan->d_dpos[b] of slot plan->d_dslot[b]; lengths are set at the end.
 void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
-                         hipStream_t s) {
+                         hipStream_t s, const StepPlan* plan = nullptr, const int32_t* d_cu = nullptr) {
   const int D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V(), nq = m->nqkv();
+  const int32_t* pos = plan ? plan->d_dpos : m->d_len;
+  const int32_t* slot = plan ? plan->d_dslot : nullptr;
   const float eps = m->cfg.rms_eps;
   bf16* xg = (bf16*)m->xg;
   launch_embed_ss(d_tokens, (const bf16*)m->embed, (const bf16*)m->layers[0].gin, m->x, xg, m->ss, B, D, V, s);
@@ -488,12 +493,14 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
     qa.W = (const bf16*)w.wqkv; qa.N = nq; qa.K = D; qa.M = B;
     qa.X = xg; qa.ss_in = m->ss; qa.ss_n = ss_n; qa.eps = eps;
     qa.bias = (const bf16*)w.bqkv; qa.cos_t = m->rope_cos; qa.sin_t = m->rope_sin; qa.q_out = (bf16*)m->q;
-    qa.kv = kv; qa.len = m->d_len; qa.H = H; qa.part = m->gemv_part;
+    qa.kv = kv; qa.len = pos; qa.slot = slot; qa.H = H; qa.part = m->gemv_part;
     gemv(qa, GV_ROPE);
     int ctx_sum = 0;
-    for (int b = 0; b < B; ++b) ctx_sum += m->h_len[b] + 1;
+    if (plan) ctx_sum = plan->dctx;
+    else for (int b = 0; b < B; ++b) ctx_sum += m->h_len[b] + 1;
     m->timed(2, H, B, ctx_sum, s, [&] {
-      launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
+      launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, B, H, pos, m->cfg.max_seq, s,
+                               nullptr, slot);
     });
     GemvArgs oa{};
     oa.W = (const bf16*)w.wo; oa.N = D; oa.K = H * hd; oa.M = B; oa.X = (const bf16*)m->o;
@@ -519,7 +526,8 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
   ha.out_f32 = d_logits; ha.ldo = V; ha.am_val = m->am_val; ha.am_idx = m->am_idx;
   gemv(ha, GV_HEAD);
   const int hr = gemv_rows(V, D, B, GV_HEAD);
-  launch_argmax_final(m->am_val, m->am_idx, (V + hr - 1) / hr, B, d_next, m->d_len, s);
+  launch_argmax_final(m->am_val, m->am_idx, (V + hr - 1) / hr, B, d_next, plan ? nullptr : m->d_len, s);
+  if (plan) launch_set_step_lengths(d_cu, plan->d_slot, plan->d_base, m->d_len, B, s);
 }
 
 void enqueue_decode(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next, hipStream_t s) {
@@ -882,6 +890,45 @@ extern "C" int axon_prefill(axon_model* m, int32_t batch, const int32_t* d_token
   return AXON_OK;
 }
 
+// Record ``enqueue`` (launching onto the stream it is given) once per key as a
+// HIP graph and replay it on s; run it eagerly when graphs are off or kernel
+// timing is on.  The graph reads every per-call input through pointers that
+// are part of the key or owned by the model.
+template <typename F>
+int replay_or_run(axon_model* m, const GraphKey& key, hipStream_t s, const char* what, F&& enqueue) {
+  if (m->use_graphs && !m->timing) {
+    auto it = m->graphs.find(key);
+    if (it == m->graphs.end()) {
+      hipGraph_t g = nullptr;
+      HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
+      enqueue(m->cap_stream);
+      hipError_t le = hipGetLastError();
+      hipError_t ce = hipStreamEndCapture(m->cap_stream, &g);
+      if (le != hipSuccess || ce != hipSuccess) {
+        if (g) (void)hipGraphDestroy(g);
+        m->enqueue_err.clear();
+        return fail(AXON_E_HIP, std::string(what) + " graph capture failed: " +
+                                    hipGetErrorString(le != hipSuccess ? le : ce));
+      }
+      if (int rc = take_enqueue_err(m, what)) {
+        (void)hipGraphDestroy(g);
+        return rc;
+      }
+      hipGraphExec_t ex = nullptr;
+      hipError_t ie = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(g);
+      if (ie != hipSuccess) return fail(AXON_E_HIP, std::string(what) + " graph instantiate: " + hipGetErrorString(ie));
+      it = m->graphs.emplace(key, ex).first;
+    }
+    HIP_TRY(hipGraphLaunch(it->second, s));
+    return AXON_OK;
+  }
+  enqueue(s);
+  int rc = check_launch(what);
+  if (!rc) rc = take_enqueue_err(m, what);
+  return rc;
+}
+
 extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_tokens, float* d_logits,
                                 int32_t* d_next_tokens, void* stream) {
   g_err.clear();
@@ -900,38 +947,9 @@ extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_t
       return fail(AXON_E_CAPACITY, "slot " + std::to_string(b) + " has no page for position " + std::to_string(pos));
   }
   hipStream_t s = (hipStream_t)stream;
-  if (m->use_graphs && !m->timing) {
-    GraphKey key{batch, d_tokens, d_logits, d_next_tokens};
-    auto it = m->graphs.find(key);
-    if (it == m->graphs.end()) {
-      hipGraph_t g = nullptr;
-      HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
-      enqueue_decode(m, batch, d_tokens, d_logits, d_next_tokens, m->cap_stream);
-      hipError_t le = hipGetLastError();
-      hipError_t ce = hipStreamEndCapture(m->cap_stream, &g);
-      if (le != hipSuccess || ce != hipSuccess) {
-        if (g) (void)hipGraphDestroy(g);
-        m->enqueue_err.clear();
-        return fail(AXON_E_HIP, std::string("decode graph capture failed: ") +
-                                    hipGetErrorString(le != hipSuccess ? le : ce));
-      }
-      if (int rc = take_enqueue_err(m, "decode")) {
-        (void)hipGraphDestroy(g);
-        return rc;
-      }
-      hipGraphExec_t ex = nullptr;
-      hipError_t ie = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
-      (void)hipGraphDestroy(g);
-      if (ie != hipSuccess) return fail(AXON_E_HIP, std::string("decode graph instantiate: ") + hipGetErrorString(ie));
-      it = m->graphs.emplace(key, ex).first;
-    }
-    HIP_TRY(hipGraphLaunch(it->second, s));
-  } else {
-    enqueue_decode(m, batch, d_tokens, d_logits, d_next_tokens, s);
-    int rc = check_launch("decode");
-    if (!rc) rc = take_enqueue_err(m, "decode");
-    if (rc) return rc;
-  }
+  if (int rc = replay_or_run(m, GraphKey{batch, d_tokens, d_logits, d_next_tokens}, s, "decode",
+                             [&](hipStream_t st) { enqueue_decode(m, batch, d_tokens, d_logits, d_next_tokens, st); }))
+    return rc;
   for (int b = 0; b < batch; ++b) m->h_len[b] += 1;
   return AXON_OK;
 }
@@ -1056,15 +1074,25 @@ extern "C" int axon_step(axon_model* m, int32_t n, const int32_t* h_slots, const
   plan.d_drow = m->d_step + 3 * MB;
   plan.d_dslot = m->d_step + 4 * MB;
   plan.d_dpos = m->d_step + 5 * MB;
-  if (m->bf)
-    enqueue_prefill<bf16>(m, n, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, 0, d_logits, d_next_tokens, s,
-                          &plan);
-  else
-    enqueue_prefill<float>(m, n, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, 0, d_logits, d_next_tokens, s,
-                           &plan);
-  int rc = check_launch("step");
-  if (!rc) rc = take_enqueue_err(m, "step");
-  if (rc) return rc;
+  if (m->bf && nd == n && n <= GEMV_MAX_M) {
+    // decode tokens only: the fused weight-streaming decode step, recorded as
+    // a graph per (n, buffers); the per-entry arrays are read from d_step
+    if (int rc = replay_or_run(m, GraphKey{n, d_tokens, d_logits, d_next_tokens, d_cu_seqlens}, s, "step",
+                               [&](hipStream_t st) {
+                                 enqueue_decode_bf16(m, n, d_tokens, d_logits, d_next_tokens, st, &plan, d_cu_seqlens);
+                               }))
+      return rc;
+  } else {
+    if (m->bf)
+      enqueue_prefill<bf16>(m, n, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, 0, d_logits, d_next_tokens, s,
+                            &plan);
+    else
+      enqueue_prefill<float>(m, n, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, 0, d_logits, d_next_tokens, s,
+                             &plan);
+    int rc = check_launch("step");
+    if (!rc) rc = take_enqueue_err(m, "step");
+    if (rc) return rc;
+  }
   int top = 0;
   for (int i = 0; i < n; ++i) {
     m->h_len[h_slots[i]] = base[i] + cnt[i];

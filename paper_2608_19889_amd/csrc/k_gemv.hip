@@ -118,6 +118,7 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
         x2 += PRE ? bf16_bits(pre.b2) : (float)a.bias[head * hd + half + i];
       }
       const int pos = PRE ? pre.pos : a.len[t];
+      const int sl = a.slot ? a.slot[t] : t;
       if (head < a.H + KVh) {
         const float cs = a.cos_t[(int64_t)pos * half + i], sn = a.sin_t[(int64_t)pos * half + i];
         const float y1 = x1 * cs - x2 * sn, y2 = x2 * cs + x1 * sn;
@@ -127,14 +128,14 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
           dst[i + half] = (bf16)y2;
         } else {
           bf16* kc = (bf16*)a.kv.k;
-          kc[k_el(a.kv, t, head - a.H, pos, i)] = (bf16)y1;
-          kc[k_el(a.kv, t, head - a.H, pos, i + half)] = (bf16)y2;
+          kc[k_el(a.kv, sl, head - a.H, pos, i)] = (bf16)y1;
+          kc[k_el(a.kv, sl, head - a.H, pos, i + half)] = (bf16)y2;
         }
       } else {
         const int kvh = head - a.H - KVh;
         bf16* vc = (bf16*)a.kv.v;
-        vc[v_el(a.kv, t, kvh, pos, i)] = (bf16)x1;
-        vc[v_el(a.kv, t, kvh, pos, i + half)] = (bf16)x2;
+        vc[v_el(a.kv, sl, kvh, pos, i)] = (bf16)x1;
+        vc[v_el(a.kv, sl, kvh, pos, i + half)] = (bf16)x2;
       }
     }
   } else {  // GV_HEAD

@@ -121,7 +121,8 @@ struct GemvArgs {
   const float* sin_t;
   bf16* q_out;  // [M][H][hd]
   KVView kv;
-  const int32_t* len;
+  const int32_t* len;   // token t is at position len[t] ...
+  const int32_t* slot;  // ... of cache slot slot[t] (t when null)
   int H;
   // split K (projections of 17..64 tokens): workspace of ksplit * M * N floats
   // (gemv_workspace_floats), owned by the caller

@@ -56,8 +56,13 @@ SCHEDULE = [
     {"reset": [2], "entries": [(2, 1, 50), (0, 0, "d"), (5, 0, "d")]},
     {"entries": [(0, 0, "d"), (5, 0, "d"), (2, 0, "d"), (1, 1, 1)]},
     {"entries": [(1, 0, "d"), (0, 0, "d"), (2, 0, "d"), (5, 0, "d")]},
+    # decode-only steps of the same size replay one recorded graph with other
+    # slot assignments; then a smaller one
+    {"entries": [(2, 0, "d"), (5, 0, "d"), (1, 0, "d"), (0, 0, "d")]},
+    {"entries": [(5, 0, "d"), (0, 0, "d"), (1, 0, "d")]},
+    {"entries": [(0, 0, "d"), (1, 0, "d"), (2, 0, "d"), (5, 0, "d")]},
 ]
-BUDGET = 8  # decode tokens reserved per admitted sequence (pages)
+BUDGET = 12  # decode tokens reserved per admitted sequence (pages)
 
 
 def run_schedule(shape, w, paged, with_b16=True):
