@@ -49,7 +49,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="1b", choices=["1b", "7b", "135m", "7b_paged", "32b"])
+    ap.add_argument("--workload", default="1b", choices=["1b", "7b", "135m", "7b_paged", "32b", "7b_serve"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=None,
@@ -94,6 +94,7 @@ def main():
                                            wl["page_size"], seed=0)
         lens = [len(s) for s in seqs]
         flat = torch.cat(seqs).to(dev)
+        seqs = [x.to(dev) for x in seqs]
         max_seq = max(lens) + steps
         page_kw = dict(page_size=wl["page_size"], num_pages=pool)
     else:
@@ -107,14 +108,21 @@ def main():
     cu = [0]
     for n in lens:
         cu.append(cu[-1] + n)
-    m = ax.Model(shape, w, max_batch=B, max_seq=max_seq, max_tokens=cu[-1], **page_kw)
+    max_tokens = cu[-1] if not wl.get("serve") else wl["step_tokens"] + B
+    m = ax.Model(shape, w, max_batch=B, max_seq=max_seq, max_tokens=max_tokens, **page_kw)
     log(f"[bench] model + inputs ready in {time.time() - t0:.1f}s "
         f"(weights {weight_bytes(shape, esz) / 1e9:.2f} GB, prompt tokens {cu[-1]})")
 
     nt = [torch.empty(B, dtype=torch.int32, device=dev) for _ in range(2)]
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    serve_plan = make_serve_plan(lens, steps, wl["step_tokens"]) if wl.get("serve") else None
+
+    serve_ev = []
+    serve_state = {}
 
     def generate(record=False):
+        if serve_plan is not None:
+            return serve(m, serve_plan, seqs, table, B, serve_ev if record else None, serve_state)
         if record:
             ev[0].record()
         m.prefill(flat, cu, block_table=table, want_logits=False, next_tokens=nt[0])
@@ -136,9 +144,16 @@ def main():
     for i in range(args.steps):
         generate(record=True)
         torch.cuda.synchronize()
-        pre_ms.append(ev[0].elapsed_time(ev[1]))
-        dec_ms.append(ev[1].elapsed_time(ev[2]))
-        log(f"[bench] step {i + 1}/{args.steps}: prefill {pre_ms[-1]:.2f} ms, decode {dec_ms[-1]:.2f} ms")
+        if serve_plan is not None:
+            p, d = serve_split_ms(serve_plan, serve_ev)
+            pre_ms.append(p)
+            dec_ms.append(d)
+            log(f"[bench] step {i + 1}/{args.steps}: steps with prompt chunks {p:.2f} ms, decode-only steps "
+                f"{d:.2f} ms ({len(serve_plan)} scheduler steps)")
+        else:
+            pre_ms.append(ev[0].elapsed_time(ev[1]))
+            dec_ms.append(ev[1].elapsed_time(ev[2]))
+            log(f"[bench] step {i + 1}/{args.steps}: prefill {pre_ms[-1]:.2f} ms, decode {dec_ms[-1]:.2f} ms")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     ms_per_step = wall * 1e3 / args.steps
@@ -152,13 +167,15 @@ def main():
     # only B rows of the table and the separate head matrix)
     wb = weight_bytes(shape, esz)
     emb = V * D * esz
-    kv_read = 0
-    for s in range(steps):
-        for n in lens:
-            kv_read += 2 * L * KV * hd * (n + s + 1) * esz
-    kv_write = steps * B * 2 * L * KV * hd * esz
-    per_step_weights = wb - (0 if shape["tie_word_embeddings"] else emb) + B * D * esz
-    decode_bytes = steps * per_step_weights + kv_read + kv_write
+    # (decode steps, decode tokens, KV positions read) of the timed decode phase:
+    # every step of a static generate; the decode-only steps of a served run
+    dsteps = [[n + s for n in lens] for s in range(steps)] if serve_plan is None else \
+        [[lens[b] + start for b, start, c in st] for st in serve_plan if all(c == 0 for _, _, c in st)]
+    kv_read = sum(2 * L * KV * hd * (pos + 1) * esz for st in dsteps for pos in st)
+    dtok = sum(len(st) for st in dsteps)
+    kv_write = dtok * 2 * L * KV * hd * esz
+    decode_bytes = sum(wb - (0 if shape["tie_word_embeddings"] else emb) + len(st) * D * esz for st in dsteps) \
+        + kv_read + kv_write
     decode_gbs = decode_bytes / (decode_ms / 1e3) / 1e9
 
     out = {
@@ -178,13 +195,15 @@ def main():
                                + (f"prompts {wl['prompt_len']}" if not wl["paged"] else
                                   f"prompts U[{wl['len_range'][0]},{wl['len_range'][1]}] (sum {cu[-1]})")
                                + f", {steps} greedy decode steps, "
-                               + ("paged KV (16-token pages)" if wl["paged"] else "contiguous KV"),
+                               + ("paged KV (16-token pages)" if wl["paged"] else "contiguous KV")
+                               + (f", continuous batching: {wl['step_tokens']}-token steps of decode tokens and "
+                                  f"prompt chunks, {len(serve_plan)} steps" if serve_plan is not None else ""),
                    "batch": B, "prompt_tokens": cu[-1], "decode_steps": steps,
                    "layers": L, "hidden": D, "vocab": V},
         "prefill_tok_s": round(cu[-1] / (prefill_ms / 1e3), 1),
         "prefill_ms": round(prefill_ms, 3),
-        "decode_tok_s": round(B * steps / (decode_ms / 1e3), 1),
-        "decode_ms_per_token_step": round(decode_ms / steps, 4),
+        "decode_tok_s": round(dtok / (decode_ms / 1e3), 1),
+        "decode_ms_per_token_step": round(decode_ms / max(1, len(dsteps)), 4),
         "decode_hbm_gbs": round(decode_gbs, 1),
         "decode_hbm_frac": round(decode_gbs / HBM_PEAK_GBS, 4),
     }
@@ -207,6 +226,90 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, wl, lens, steps, B)
     print(json.dumps(out), flush=True)
+
+
+def make_serve_plan(lens, steps, budget):
+    """First-come-first-served continuous-batching schedule, host only (the
+    tokens themselves are produced on the device).  Every sequence needs its
+    prompt, fed in chunks, then ``steps`` decode tokens.  A step first gives
+    each running sequence (prompt complete, decode tokens left) one decode
+    token, then fills the rest of the token budget with prompt chunks in
+    arrival order.  Returns the steps as lists of (sequence, start, count):
+    count > 0 prompt tokens from ``start``; count == 0 a decode token, with
+    ``start`` the number of decode tokens the sequence has already fed."""
+    B = len(lens)
+    fed, dec = [0] * B, [0] * B
+    plan = []
+    while True:
+        entries, used = [], 0
+        for b in range(B):
+            if fed[b] == lens[b] and dec[b] < steps:
+                entries.append((b, dec[b], 0))
+                used += 1
+        for b in range(B):
+            if fed[b] < lens[b] and used < budget:
+                c = min(lens[b] - fed[b], budget - used)
+                entries.append((b, fed[b], c))
+                used += c
+        if not entries:
+            return plan
+        for b, _, c in entries:
+            if c == 0:
+                dec[b] += 1
+            else:
+                fed[b] += c
+        plan.append(entries)
+
+
+def serve(m, plan, seqs, table, B, events, state):
+    """Run a continuous-batching schedule through axon_step.  Sequence b lives
+    in slot b; a sequence's decode token is its own previous greedy output,
+    gathered on the device (no host synchronization inside the run).  Token,
+    cu_seqlens and output buffers keep their addresses from step to step, so
+    decode-only steps replay one recorded graph per entry count."""
+    import torch
+    dev = seqs[0].device
+    if not state:
+        cap = max(sum(c if c else 1 for _, _, c in st) for st in plan)
+        state.update(tok=torch.empty(cap, dtype=torch.int32, device=dev),
+                     cu=torch.empty(B + 1, dtype=torch.int32, device=dev),
+                     nxt=torch.empty(B, dtype=torch.int32, device=dev),
+                     last=torch.zeros(B, dtype=torch.int32, device=dev))
+    tok, nxt, last = state["tok"], state["nxt"], state["last"]
+    if events is not None:
+        events.clear()
+    for st in plan:
+        slots = [b for b, _, _ in st]
+        fresh = [1 if c > 0 and start == 0 else 0 for _, start, c in st]
+        dec = [b for b, _, c in st if c == 0]
+        parts = [last.index_select(0, torch.tensor(dec, dtype=torch.int64).to(dev, non_blocking=True))] if dec else []
+        parts += [seqs[b][start:start + c] for b, start, c in st if c > 0]
+        cu = [0]
+        for _, _, c in st:
+            cu.append(cu[-1] + (c if c else 1))
+        torch.cat(parts, out=tok[:cu[-1]])
+        rows = table[slots] if any(fresh) else None
+        if events is not None:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+        m.step(tok[:cu[-1]], cu, slots, fresh, block_rows=rows, next_tokens=nxt[:len(st)], want_logits=False,
+               cu_device=state["cu"])
+        if events is not None:
+            e1.record()
+            events.append((e0, e1))
+        last.index_copy_(0, torch.tensor(slots, dtype=torch.int64).to(dev, non_blocking=True), nxt[:len(st)])
+
+
+def serve_split_ms(plan, events):
+    """(ms of the steps that carry prompt chunks, ms of the decode-only steps)."""
+    mixed = dec = 0.0
+    for st, (e0, e1) in zip(plan, events):
+        t = e0.elapsed_time(e1)
+        if all(c == 0 for _, _, c in st):
+            dec += t
+        else:
+            mixed += t
+    return mixed, dec
 
 
 def roofline_pass(m, generate, shape, esz, lens):
@@ -243,8 +346,10 @@ def roofline_pass(m, generate, shape, esz, lens):
             ctx = d2
             a["bytes"] += 2 * KV * hd * esz * ctx + 2 * d1 * H * hd * esz
             a["flops"] += 4.0 * H * hd * ctx
-        else:
-            a["flops"] += 4.0 * H * hd * sq
+        # prefill attention: the workload's causal total is added below (one
+        # launch per layer for a prefill, several for chunked prompts)
+    if ax.T_ATTN_PREFILL in agg:
+        agg[ax.T_ATTN_PREFILL]["flops"] = 4.0 * H * hd * sq * shape["num_hidden_layers"]
     # per-shape breakdown of the decode projections (stderr): (N, K) -> time, bandwidth
     shapes = {}
     for c, (d0, d1, d2), ms in recs:

@@ -209,15 +209,22 @@ class Model:
 
     def step(self, tokens: torch.Tensor, cu_seqlens: list, slots: list, fresh: list | None = None,
              block_rows: torch.Tensor | None = None, logits: torch.Tensor | None = None,
-             next_tokens: torch.Tensor | None = None, want_logits: bool = True, stream=None):
+             next_tokens: torch.Tensor | None = None, want_logits: bool = True, stream=None,
+             cu_device: torch.Tensor | None = None):
         """One continuous-batching step (axon_step).  tokens: device int32
         [sum n_i]; cu_seqlens: host list of n+1 ints; slots / fresh: host lists
         of n ints; block_rows: host int32 [n, stride] page rows (paged cache) or
-        None.  Returns (logits [n, V] or None, next_tokens [n])."""
+        None; cu_device: optional device int32 buffer (>= n+1 entries) that
+        receives cu_seqlens, so that its address stays fixed across calls.
+        Returns (logits [n, V] or None, next_tokens [n])."""
         dev = tokens.device
         n = len(slots)
         cu_h = (ctypes.c_int32 * (n + 1))(*[int(c) for c in cu_seqlens])
-        cu_d = torch.tensor([int(c) for c in cu_seqlens], dtype=torch.int32, device=dev)
+        if cu_device is not None:
+            cu_d = cu_device
+            cu_d[:n + 1].copy_(torch.tensor([int(c) for c in cu_seqlens], dtype=torch.int32), non_blocking=True)
+        else:
+            cu_d = torch.tensor([int(c) for c in cu_seqlens], dtype=torch.int32, device=dev)
         sl_h = (ctypes.c_int32 * n)(*[int(x) for x in slots])
         fr_h = (ctypes.c_int32 * n)(*[int(x) for x in fresh]) if fresh is not None else None
         if logits is None and want_logits:
