@@ -59,6 +59,14 @@ constexpr int PK = 64;
 #endif
 constexpr int PREFILL_QB = AXON_PREFILL_QB;  // 32-query blocks per wavefront
 
+// LDS row rho of a K tile holds key kappa(rho): bits 2 and 3 of the row index
+// swapped.  The S^T = K Q^T accumulator puts rows {8a + 4 hl + 0..3} of a
+// 16-row group in the half-wavefront hl (a = 0, 1), so with this order a
+// lane's 8 probabilities of a k-step are 8 consecutive keys, and its V^T
+// operand of the P V product is one 16-byte chunk (a single conflict-free LDS
+// read instead of two 8-byte reads that share banks).  An involution.
+AXON_DEV int kappa(int rho) { return (rho & ~12) | ((rho & 4) << 1) | ((rho & 8) >> 1); }
+
 // physical 16-byte chunk of logical chunk c in row r of an LDS tile whose
 // rows hold CH chunks: the 16 lanes of a read phase (16 consecutive rows,
 // one logical chunk) hit distinct banks
@@ -134,7 +142,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
     for (int i = 0; i < KT / 256; ++i) {
       const int p = (i * 4 + wave) * 64 + lane;
       const int r = p / KCH, c = pswz<KCH>(r, p % KCH);  // pswz is its own inverse
-      const int key = min(j0 + r, KL - 1);                // in [j0, j0 + 64): j0 < KL
+      const int key = min(j0 + kappa(r), KL - 1);         // in [j0, j0 + 64): j0 < KL
       const int64_t page = pg[(key - j0) >> 4];
       const int kp = key % kv.ps;
       const bf16* src = kb + ((page * kv.kv_heads + kvh) * kv.ps + (kp & ~15)) * HD + c * 128 + (kp & 15) * 8;
@@ -211,7 +219,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
         for (int r = 0; r < 2; ++r)
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
-            const int key = j0 + r * 32 + (i / 4) * 8 + hl * 4 + (i % 4);
+            const int key = j0 + r * 32 + (i / 8) * 16 + hl * 8 + ((i / 4) & 1) * 4 + (i % 4);  // kappa of the row
             const float v = (key <= base + myq && key < KL) ? s[qb][r][i] : -INFINITY;
             s[qb][r][i] = v;
             mloc = fmaxf(mloc, v);
@@ -243,21 +251,18 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
           pb[qb][r][i / 8][i % 8] = (bf16)p;
         }
     }
-    // ---- O^T += V^T P^T; the k index of block (r, h) covers keys
-    //      r*32 + h*16 + {hl*4 + 0..3, 8 + hl*4 + 0..3}; each V fragment
-    //      serves the QB query blocks
+    // ---- O^T += V^T P^T; the k index of block (r, h) in half-wavefront hl
+    //      covers keys r*32 + h*16 + hl*8 + 0..7 (logical chunk r*4 + 2h + hl
+    //      of the V^T row); each V fragment serves the QB query blocks
 #pragma unroll
     for (int d = 0; d < HD / 32; ++d) {
       const int dd = d * 32 + (lane & 31);
-      const bf16* vr = vsb + dd * PK + hl * 4;
+      const bf16x8* vr = (const bf16x8*)(vsb + dd * PK);
 #pragma unroll
       for (int r = 0; r < 2; ++r)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const int c0 = r * 4 + h * 2;  // logical chunks c0, c0 + 1 of the row
-          const bf16x4 lo = *(const bf16x4*)(vr + pswz<VCH>(dd, c0) * 8);
-          const bf16x4 hi = *(const bf16x4*)(vr + pswz<VCH>(dd, c0 + 1) * 8);
-          const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          const bf16x8 va = vr[pswz<VCH>(dd, r * 4 + h * 2 + hl)];
 #pragma unroll
           for (int qb = 0; qb < QB; ++qb)
             acc_o[qb][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[qb][r][h], acc_o[qb][d], 0, 0, 0);
