@@ -132,6 +132,31 @@ def swiglu_mlp(h: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray, w_down: np.n
     return a @ w_down.T
 
 
+def moe_mlp(h: np.ndarray, w_router: np.ndarray, experts: list, shared, top_k: int, norm_topk: bool,
+            rnd=None) -> np.ndarray:
+    """Mixture-of-experts MLP (the MoE built-in's softmax top-k router followed
+    by the routed experts; Built-In Libraries, "Activations and specialized
+    modules").  Per token: router probabilities = softmax over the experts of
+    h W_router^T; the top_k experts by probability (ties to the lowest expert
+    index); their probabilities are the mixing weights (divided by their sum
+    when ``norm_topk``); each chosen expert is a SwiGLU MLP; ``shared`` (a
+    (gate, up, down) triple or None) is an always-active SwiGLU MLP added
+    without a weight.  ``experts`` is a list of (gate, up, down) triples."""
+    p = softmax(h @ w_router.T)
+    idx = np.argsort(-p, axis=-1, kind="stable")[:, :top_k]
+    wts = np.take_along_axis(p, idx, axis=-1)
+    if norm_topk:
+        wts = wts / np.sum(wts, axis=-1, keepdims=True)
+    out = np.zeros_like(h)
+    for e, (wg, wu, wd) in enumerate(experts):
+        rows, slots = np.nonzero(idx == e)
+        if rows.size:
+            out[rows] += wts[rows, slots][:, None] * swiglu_mlp(h[rows], wg, wu, wd, rnd=rnd)
+    if shared is not None:
+        out = out + swiglu_mlp(h, *shared, rnd=rnd)
+    return out
+
+
 # --------------------------------------------------------------------------
 # the model
 # --------------------------------------------------------------------------
@@ -143,7 +168,12 @@ class OracleDecoder:
     num_attention_heads, num_key_value_heads, head_dim, intermediate_size,
     vocab_size, rms_norm_eps, rope_theta, attention_bias, tie_word_embeddings).
     ``weights`` maps the flat checkpoint names to arrays (any float dtype, or
-    torch tensors); they are held as float64.
+    torch tensors); they are held as float64.  Mixture-of-experts models add
+    n_routed_experts, num_experts_per_tok, moe_intermediate_size,
+    n_shared_experts, first_k_dense_replace (leading layers with a dense MLP)
+    and norm_topk_prob (DeepSeek-MoE-style keys); their MoE layers read
+    ``mlp.gate.weight`` (the router), ``mlp.experts.{e}.*`` and
+    ``mlp.shared_experts.*``.
     """
 
     def __init__(self, cfg: dict, weights: dict, io_round: str | None = None):
@@ -168,6 +198,8 @@ class OracleDecoder:
         else:
             raise ValueError(io_round)
         self.caches: list[list[tuple[np.ndarray, np.ndarray]]] = []
+        self.n_experts = int(cfg.get("n_routed_experts") or 0)
+        self.first_moe = int(cfg.get("first_k_dense_replace") or 0)
 
     # ---- one layer over the new tokens of one sequence ----
     def _layer(self, i: int, x: np.ndarray, pos: np.ndarray, cache: list) -> np.ndarray:
@@ -196,8 +228,17 @@ class OracleDecoder:
         o = self._r(causal_gqa_attention(q, kc, vc, pos)).reshape(s, self.H * self.hd)
         x = self._rx(x + o @ w[p + "self_attn.o_proj.weight"].T)
         h2 = self._r(rms_norm(x, w[p + "post_attention_layernorm.weight"], self.eps))
-        mlp = swiglu_mlp(h2, w[p + "mlp.gate_proj.weight"], w[p + "mlp.up_proj.weight"],
-                         w[p + "mlp.down_proj.weight"], rnd=self._r)
+        if self.n_experts and i >= self.first_moe:
+            c = self.cfg
+            ex = [tuple(w[p + f"mlp.experts.{e}.{n}_proj.weight"] for n in ("gate", "up", "down"))
+                  for e in range(self.n_experts)]
+            sh = tuple(w[p + f"mlp.shared_experts.{n}_proj.weight"] for n in ("gate", "up", "down")) \
+                if c.get("n_shared_experts") else None
+            mlp = moe_mlp(h2, w[p + "mlp.gate.weight"], ex, sh, int(c["num_experts_per_tok"]),
+                          bool(c.get("norm_topk_prob")), rnd=self._r)
+        else:
+            mlp = swiglu_mlp(h2, w[p + "mlp.gate_proj.weight"], w[p + "mlp.up_proj.weight"],
+                             w[p + "mlp.down_proj.weight"], rnd=self._r)
         return self._rx(x + mlp)
 
     def _forward_seq(self, b: int, ids: np.ndarray, all_logits: bool) -> np.ndarray:

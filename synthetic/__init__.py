@@ -5,7 +5,7 @@ of the forward pass's arithmetic.  Both sides receive the tensors it returns as
 plain inputs, so nothing here is computed by either implementation.
 """
 from .models import (MODEL_SHAPES, WORKLOADS, small_shape, model_weights,
-                     weight_names, weight_shapes, prompts, paged_workload)
+                     weight_names, weight_shapes, prompts, paged_workload, is_moe_layer)
 
 __all__ = ["MODEL_SHAPES", "WORKLOADS", "small_shape", "model_weights",
-           "weight_names", "weight_shapes", "prompts", "paged_workload"]
+           "weight_names", "weight_shapes", "prompts", "paged_workload", "is_moe_layer"]

@@ -43,7 +43,20 @@ MODEL_SHAPES = {
                 num_key_value_heads=8, head_dim=128, intermediate_size=27648,
                 vocab_size=152064, tie_word_embeddings=False, attention_bias=True,
                 rms_norm_eps=1e-6, rope_theta=1000000.0, dtype="bf16"),
+    # DeepSeek-MoE-16B-shaped (the MoE model of the paper's 4-32B benchmark):
+    # layer 0 dense (intermediate 10944), layers 1..27 with 64 routed experts
+    # (top 6, intermediate 1408, no renormalization) + 2 shared experts
+    "moe16b": dict(hidden_size=2048, num_hidden_layers=28, num_attention_heads=16,
+                   num_key_value_heads=16, head_dim=128, intermediate_size=10944,
+                   vocab_size=102400, tie_word_embeddings=False, attention_bias=False,
+                   rms_norm_eps=1e-6, rope_theta=10000.0, dtype="bf16",
+                   n_routed_experts=64, num_experts_per_tok=6, moe_intermediate_size=1408,
+                   n_shared_experts=2, first_k_dense_replace=1, norm_topk_prob=False),
 }
+
+
+def is_moe_layer(shape: dict, i: int) -> bool:
+    return bool(shape.get("n_routed_experts")) and i >= int(shape.get("first_k_dense_replace") or 0)
 
 # The five workloads: model shape, batch, prompt length, greedy decode steps,
 # KV-cache kind.  "7b_paged" has per-sequence prompt lengths drawn uniformly in
@@ -90,8 +103,15 @@ def weight_names(shape: dict) -> list[str]:
             names.append(p + f"self_attn.{x}_proj.weight")
             if shape["attention_bias"]:
                 names.append(p + f"self_attn.{x}_proj.bias")
-        names += [p + "self_attn.o_proj.weight", p + "post_attention_layernorm.weight",
-                  p + "mlp.gate_proj.weight", p + "mlp.up_proj.weight", p + "mlp.down_proj.weight"]
+        names += [p + "self_attn.o_proj.weight", p + "post_attention_layernorm.weight"]
+        if is_moe_layer(shape, i):
+            names.append(p + "mlp.gate.weight")
+            for e in range(shape["n_routed_experts"]):
+                names += [p + f"mlp.experts.{e}.{x}_proj.weight" for x in ("gate", "up", "down")]
+            if shape.get("n_shared_experts"):
+                names += [p + f"mlp.shared_experts.{x}_proj.weight" for x in ("gate", "up", "down")]
+        else:
+            names += [p + "mlp.gate_proj.weight", p + "mlp.up_proj.weight", p + "mlp.down_proj.weight"]
     names.append("model.norm.weight")
     if not shape["tie_word_embeddings"]:
         names.append("lm_head.weight")
@@ -117,10 +137,15 @@ def weight_shapes(shape: dict) -> dict[str, tuple]:
             out[n] = (KV * hd,)
         elif n.endswith("o_proj.weight"):
             out[n] = (D, H * hd)
-        elif n.endswith("gate_proj.weight") or n.endswith("up_proj.weight"):
-            out[n] = (I, D)
-        elif n.endswith("down_proj.weight"):
-            out[n] = (D, I)
+        elif n.endswith("mlp.gate.weight"):
+            out[n] = (shape["n_routed_experts"], D)
+        elif n.endswith("gate_proj.weight") or n.endswith("up_proj.weight") or n.endswith("down_proj.weight"):
+            ii = I
+            if ".mlp.experts." in n:
+                ii = shape["moe_intermediate_size"]
+            elif ".mlp.shared_experts." in n:
+                ii = shape["moe_intermediate_size"] * shape["n_shared_experts"]
+            out[n] = (D, ii) if n.endswith("down_proj.weight") else (ii, D)
         else:  # pragma: no cover
             raise KeyError(n)
     return out

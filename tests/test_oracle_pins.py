@@ -353,3 +353,99 @@ def test_io_round_mode_stays_close_to_exact():
     a = OracleDecoder(shp, w).prefill([seq], all_logits=True)[0]
     b = OracleDecoder(shp, w, io_round="bf16").prefill([seq], all_logits=True)[0]
     assert 0 < np.max(np.abs(a - b)) < 2e-2
+
+
+# ----------------------------------------------------------- mixture of experts
+
+def _moe_weights(D, E, I, shared_I, seed):
+    r = np.random.default_rng(seed)
+    router = r.standard_normal((E, D)) * 0.3
+    ex = [tuple(r.standard_normal(shp) * 0.2 for shp in ((I, D), (I, D), (D, I))) for _ in range(E)]
+    sh = tuple(r.standard_normal(shp) * 0.2 for shp in ((shared_I, D), (shared_I, D), (D, shared_I))) \
+        if shared_I else None
+    return router, ex, sh
+
+
+def test_moe_block_matches_transformers_deepseek_v2():
+    """DeepSeek-MoE semantics (the paper's MoE benchmark model): softmax router,
+    greedy top-k without renormalization, ungated shared experts.  Pinned to
+    transformers' DeepseekV2Moe block in float64 (its router runs in float32,
+    so agreement is ~1e-7; a wrong selection, weight or sum differs by ~0.1)."""
+    from transformers import DeepseekV2Config
+    from transformers.models.deepseek_v2.modeling_deepseek_v2 import DeepseekV2Moe
+    D, E, I, K, S = 32, 8, 16, 3, 11
+    cfg = DeepseekV2Config(hidden_size=D, moe_intermediate_size=I, n_routed_experts=E, num_experts_per_tok=K,
+                           n_shared_experts=2, topk_method="greedy", routed_scaling_factor=1.0, n_group=1,
+                           topk_group=1, hidden_act="silu")
+    blk = DeepseekV2Moe(cfg).double()
+    router, ex, sh = _moe_weights(D, E, I, 2 * I, seed=5)
+    with torch.no_grad():
+        blk.gate.weight.copy_(torch.from_numpy(router))
+        blk.experts.gate_up_proj.copy_(torch.from_numpy(np.stack([np.concatenate([g, u]) for g, u, _ in ex])))
+        blk.experts.down_proj.copy_(torch.from_numpy(np.stack([d for _, _, d in ex])))
+        blk.shared_experts.gate_proj.weight.copy_(torch.from_numpy(sh[0]))
+        blk.shared_experts.up_proj.weight.copy_(torch.from_numpy(sh[1]))
+        blk.shared_experts.down_proj.weight.copy_(torch.from_numpy(sh[2]))
+    h = RNG.standard_normal((S, D))
+    with torch.no_grad():
+        ref = blk(torch.from_numpy(h)[None]).numpy()[0]
+    got = oracle.decoder.moe_mlp(h, router, ex, sh, K, False)
+    np.testing.assert_allclose(got, ref, atol=1e-6, rtol=0)
+    # the shared experts matter, and so does the routing
+    assert np.abs(got - oracle.decoder.moe_mlp(h, router, ex, None, K, False)).max() > 1e-2
+    assert np.abs(got - oracle.decoder.moe_mlp(h, router[::-1].copy(), ex, sh, K, False)).max() > 1e-2
+
+
+def test_moe_block_matches_transformers_qwen3_moe_renormalized():
+    """The renormalized variant (weights of the chosen experts divided by their
+    sum), pinned to transformers' Qwen3MoeSparseMoeBlock."""
+    from transformers import Qwen3MoeConfig
+    from transformers.models.qwen3_moe.modeling_qwen3_moe import Qwen3MoeSparseMoeBlock
+    D, E, I, K, S = 32, 8, 16, 2, 9
+    cfg = Qwen3MoeConfig(hidden_size=D, moe_intermediate_size=I, num_experts=E, num_experts_per_tok=K,
+                         norm_topk_prob=True, hidden_act="silu")
+    blk = Qwen3MoeSparseMoeBlock(cfg).double()
+    router, ex, _ = _moe_weights(D, E, I, 0, seed=6)
+    with torch.no_grad():
+        blk.gate.weight.copy_(torch.from_numpy(router))
+        blk.experts.gate_up_proj.copy_(torch.from_numpy(np.stack([np.concatenate([g, u]) for g, u, _ in ex])))
+        blk.experts.down_proj.copy_(torch.from_numpy(np.stack([d for _, _, d in ex])))
+    h = RNG.standard_normal((S, D))
+    with torch.no_grad():
+        ref = blk(torch.from_numpy(h)[None]).numpy()[0]
+    np.testing.assert_allclose(oracle.decoder.moe_mlp(h, router, ex, None, K, True), ref, atol=1e-6, rtol=0)
+
+
+def test_moe_router_ties_go_to_the_lowest_expert():
+    """Experts 2 and 5 tie for the last of 3 places: expert 2 is chosen."""
+    D, E, I = 4, 6, 3
+    v = np.array([1.0, 0.0, 0.0, 0.0])
+    c = np.array([3.0, 0.0, 1.0, 0.0, 2.0, 1.0])
+    router = 0.25 * c[:, None] * v[None, :]
+    _, ex, _ = _moe_weights(D, E, I, 0, seed=7)
+    h = v[None, :] * 2.0  # logits 0.5 c
+    got = oracle.decoder.moe_mlp(h, router, ex, None, 3, False)
+    p = np.exp(0.5 * c) / np.exp(0.5 * c).sum()
+    want = sum(p[e] * oracle.decoder.swiglu_mlp(h, *ex[e]) for e in (0, 4, 2))
+    np.testing.assert_allclose(got, want, atol=1e-14)
+    other = sum(p[e] * oracle.decoder.swiglu_mlp(h, *ex[e]) for e in (0, 4, 5))
+    assert np.abs(got - other).max() > 1e-3
+
+
+def test_moe_model_layers_and_decode_invariants():
+    """A small MoE decoder: layer 0 dense, later layers MoE; incremental decode
+    equals full recompute (routing is per token, so it does not depend on the
+    other tokens of the call)."""
+    shp = _tiny("llama")
+    shp.update(n_routed_experts=6, num_experts_per_tok=2, moe_intermediate_size=16, n_shared_experts=1,
+               first_k_dense_replace=1, norm_topk_prob=False)
+    w = _np_weights(shp)
+    assert "model.layers.0.mlp.gate_proj.weight" in w and "model.layers.1.mlp.experts.5.down_proj.weight" in w
+    seq = RNG.integers(0, shp["vocab_size"], 10)
+    full = OracleDecoder(shp, w).prefill([seq], all_logits=True)[0]
+    m = OracleDecoder(shp, w)
+    m.prefill([seq[:4]])
+    np.testing.assert_allclose(m.extend(0, seq[4:]), full[4:], atol=1e-10)
+    dense = OracleDecoder(dict(shp, n_routed_experts=0), {**w, **{
+        k.replace("mlp.shared_experts.", "mlp."): v for k, v in w.items() if ".mlp.shared_experts." in k}})
+    assert np.abs(dense.prefill([seq], all_logits=True)[0] - full).max() > 1e-3  # the routed experts contribute
