@@ -71,6 +71,22 @@ typedef struct {
   int32_t max_tokens;     /* largest prefill token count per call; 0 = max_batch*max_seq */
   int32_t kv_page_size;   /* 0: contiguous cache; else tokens per page, a multiple of 16 */
   int32_t kv_num_pages;   /* page-pool size when kv_page_size > 0 */
+  /* Mixture of experts (the MoE built-in's softmax top-k router and grouped
+   * experts; Built-In Libraries, "Activations and specialized modules").
+   * n_experts == 0: every layer has the dense MLP and the fields below are
+   * ignored.  Otherwise layers first_moe_layer.. replace it by: probabilities
+   * = softmax of the router logits over the n_experts; the top_k experts by
+   * probability (ties to the lowest index) weighted by their probabilities
+   * (divided by their sum when norm_topk_prob == 1); each expert a SwiGLU MLP
+   * of moe_intermediate; plus, when n_shared_experts > 0, an always-active
+   * SwiGLU MLP of n_shared_experts * moe_intermediate added unweighted.
+   * Requires dtype AXON_BF16. */
+  int32_t n_experts;        /* 0, or 2..256 routed experts */
+  int32_t top_k;            /* experts per token, 1..min(n_experts, 8) */
+  int32_t moe_intermediate; /* multiple of 64 */
+  int32_t n_shared_experts; /* >= 0 */
+  int32_t first_moe_layer;  /* 0..n_layers: the layers before it keep the dense MLP */
+  int32_t norm_topk_prob;   /* 0 or 1 */
 } axon_config;
 
 /* One entry of the flat weight map.  Names follow the HF Llama/Qwen2 layout:
@@ -84,6 +100,12 @@ typedef struct {
  *   model.layers.{i}.mlp.gate_proj.weight     [I, D]
  *   model.layers.{i}.mlp.up_proj.weight       [I, D]
  *   model.layers.{i}.mlp.down_proj.weight     [D, I]
+ * and in a mixture-of-experts layer (i >= first_moe_layer) instead of the mlp.* above:
+ *   model.layers.{i}.mlp.gate.weight          [n_experts, D]  (the router)
+ *   model.layers.{i}.mlp.experts.{e}.gate_proj.weight / up_proj.weight  [moe_intermediate, D]
+ *   model.layers.{i}.mlp.experts.{e}.down_proj.weight                   [D, moe_intermediate]
+ *   model.layers.{i}.mlp.shared_experts.{gate,up,down}_proj.weight      (iff n_shared_experts > 0;
+ *                                          intermediate n_shared_experts * moe_intermediate)
  *   model.norm.weight                         [D]
  *   lm_head.weight                            [V, D]  (present iff tie_embeddings == 0)
  * Linear weights are [out, in] row-major.  Every tensor is contiguous,

@@ -44,7 +44,9 @@ class AxonConfig(ctypes.Structure):
                 ("tie_embeddings", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("max_batch", ctypes.c_int32), ("max_seq", ctypes.c_int32),
                 ("max_tokens", ctypes.c_int32), ("kv_page_size", ctypes.c_int32),
-                ("kv_num_pages", ctypes.c_int32)]
+                ("kv_num_pages", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
+                ("moe_intermediate", ctypes.c_int32), ("n_shared_experts", ctypes.c_int32),
+                ("first_moe_layer", ctypes.c_int32), ("norm_topk_prob", ctypes.c_int32)]
 
 
 class AxonWeight(ctypes.Structure):
@@ -123,7 +125,12 @@ def make_config(shape: dict, max_batch: int, max_seq: int, max_tokens: int = 0, 
         rms_eps=shape["rms_norm_eps"], rope_theta=shape["rope_theta"],
         qkv_bias=int(bool(shape["attention_bias"])), tie_embeddings=int(bool(shape["tie_word_embeddings"])),
         dtype=AXON_BF16 if shape["dtype"] == "bf16" else AXON_F32, max_batch=max_batch, max_seq=max_seq,
-        max_tokens=max_tokens, kv_page_size=page_size, kv_num_pages=num_pages)
+        max_tokens=max_tokens, kv_page_size=page_size, kv_num_pages=num_pages,
+        n_experts=int(shape.get("n_routed_experts") or 0), top_k=int(shape.get("num_experts_per_tok") or 0),
+        moe_intermediate=int(shape.get("moe_intermediate_size") or 0),
+        n_shared_experts=int(shape.get("n_shared_experts") or 0),
+        first_moe_layer=int(shape.get("first_k_dense_replace") or 0),
+        norm_topk_prob=int(bool(shape.get("norm_topk_prob"))))
 
 
 def make_weights(weights: dict) -> tuple[ctypes.Array, list]:

@@ -67,6 +67,22 @@ std::vector<std::pair<std::string, Expected>> expected_weights(const axon_config
     }
     w.push_back({p + "self_attn.o_proj.weight", {2, {D, H * hd}}});
     w.push_back({p + "post_attention_layernorm.weight", {1, {D, 0}}});
+    if (c.n_experts > 0 && i >= c.first_moe_layer) {
+      const int64_t Ie = c.moe_intermediate, Is = (int64_t)c.n_shared_experts * Ie;
+      w.push_back({p + "mlp.gate.weight", {2, {c.n_experts, D}}});
+      for (int e = 0; e < c.n_experts; ++e) {
+        const std::string q = p + "mlp.experts." + std::to_string(e) + ".";
+        w.push_back({q + "gate_proj.weight", {2, {Ie, D}}});
+        w.push_back({q + "up_proj.weight", {2, {Ie, D}}});
+        w.push_back({q + "down_proj.weight", {2, {D, Ie}}});
+      }
+      if (Is > 0) {
+        w.push_back({p + "mlp.shared_experts.gate_proj.weight", {2, {Is, D}}});
+        w.push_back({p + "mlp.shared_experts.up_proj.weight", {2, {Is, D}}});
+        w.push_back({p + "mlp.shared_experts.down_proj.weight", {2, {D, Is}}});
+      }
+      continue;
+    }
     w.push_back({p + "mlp.gate_proj.weight", {2, {I, D}}});
     w.push_back({p + "mlp.up_proj.weight", {2, {I, D}}});
     w.push_back({p + "mlp.down_proj.weight", {2, {D, I}}});
@@ -97,6 +113,15 @@ int validate_config(const axon_config& c) {
   if (c.max_tokens < 0) return bad("max_tokens must be >= 0");
   if (c.kv_page_size < 0 || c.kv_page_size % 16) return bad("kv_page_size must be 0 or a multiple of 16");
   if (c.kv_page_size > 0 && c.kv_num_pages < 1) return bad("kv_num_pages must be >= 1 for a paged cache");
+  if (c.n_experts != 0) {
+    if (c.n_experts < 2 || c.n_experts > 256) return bad("n_experts must be 0 or in [2, 256]");
+    if (c.top_k < 1 || c.top_k > 8 || c.top_k > c.n_experts) return bad("top_k must be in [1, min(n_experts, 8)]");
+    if (c.moe_intermediate <= 0 || c.moe_intermediate % 64) return bad("moe_intermediate must be a positive multiple of 64");
+    if (c.n_shared_experts < 0) return bad("n_shared_experts must be >= 0");
+    if (c.first_moe_layer < 0 || c.first_moe_layer > c.n_layers) return bad("first_moe_layer must be in [0, n_layers]");
+    if (c.norm_topk_prob != 0 && c.norm_topk_prob != 1) return bad("norm_topk_prob must be 0 or 1");
+    if (c.dtype != AXON_BF16) return bad("mixture-of-experts layers need dtype AXON_BF16");
+  }
   return AXON_OK;
 }
 
@@ -108,6 +133,14 @@ struct LayerW {
   void* wd;     // [D, I]
   void* gin;    // [D]
   void* gpost;  // [D]
+  // mixture-of-experts layer: the router [E rounded up to 32, D] (padding rows
+  // zero), every expert's interleaved gate/up [2 Ie, D] and down [D, Ie]
+  // stacked expert after expert; wgu / wd then hold the shared experts (a
+  // dense MLP of n_shared * Ie), or are null
+  bool moe = false;
+  void* wrouter = nullptr;
+  void* wgu_e = nullptr;
+  void* wd_e = nullptr;
 };
 
 struct TimingRec {
@@ -170,6 +203,19 @@ struct axon_model {
   std::vector<int> h_len;
   // per-entry arrays of a continuous-batching step (6 x max_batch int32):
   // slot, base position, chunk entries, single-token rows / slots / positions
+  // mixture-of-experts work buffers (sized for the most tokens of a call)
+  float* moe_logits = nullptr;  // [rows][E rounded up to 32]
+  int32_t* moe_topi = nullptr;  // [rows][k]
+  float* moe_topw = nullptr;
+  int32_t* moe_cnt = nullptr;   // [E], then row / tile offsets [E+1] each
+  int32_t* moe_off = nullptr;
+  int32_t* moe_toff = nullptr;
+  int32_t* moe_xrow = nullptr;  // [rows * k]
+  int32_t* moe_inv = nullptr;
+  void* moe_a = nullptr;        // [rows * k][Ie] bf16 gated expert activations
+  float* moe_y = nullptr;       // [rows * k][D] expert outputs
+  bool moe_model() const { return cfg.n_experts > 0; }
+  int moe_ep() const { return (cfg.n_experts + 31) / 32 * 32; }
   int32_t* d_step = nullptr;
   int32_t* h_step = nullptr;  // pinned staging copy
   hipEvent_t step_copied = nullptr;
@@ -294,6 +340,44 @@ void gemm_few_f32(axon_model* m, const void* W, const void* X, int N, int M, int
   m->timed(0, N, M, K, s, [&] { launch_gemm_f32((const float*)W, (const float*)X, N, M, K, epi, ep, s); });
 }
 
+// Mixture-of-experts MLP of a layer over T rows of normed activations h
+// (bf16), added to the residual stream x: router logits (float) -> top-k
+// routing -> grouped-GEMM plan -> grouped gate/up with the SiLU gate over the
+// gathered token rows -> grouped down -> shared experts (dense, residual
+// epilogue) -> weighted combine of each token's k expert rows into x.
+void enqueue_moe(axon_model* m, const LayerW& w, const bf16* h, int T, hipStream_t s) {
+  const axon_config& c = m->cfg;
+  const int D = m->D(), E = c.n_experts, k = c.top_k, Ie = c.moe_intermediate, Ep = m->moe_ep();
+  const int Is = c.n_shared_experts * Ie;
+  gemm_many<bf16>(m, w.wrouter, h, Ep, T, D, EPI_F32, m->moe_logits, nullptr, Ep, s);
+  launch_moe_route(m->moe_logits, Ep, T, E, k, c.norm_topk_prob, m->moe_topi, m->moe_topw, s);
+  launch_moe_plan(m->moe_topi, T, E, k, m->moe_cnt, m->moe_off, m->moe_toff, m->moe_xrow, m->moe_inv, s);
+  EpiArgs g{};
+  g.g_off = m->moe_off;
+  g.g_toff = m->moe_toff;
+  g.g_E = E;
+  g.g_xrow = m->moe_xrow;
+  g.g_wstride = (int64_t)2 * Ie * D;
+  g.out_t = m->moe_a;
+  g.ldo = Ie;
+  m->timed(1, 2 * Ie, T * k, D, s, [&] {
+    launch_gemm_bf16_grouped((const bf16*)w.wgu_e, h, 2 * Ie, D, T * k, EPI_SILU, g, s);
+  });
+  g.g_xrow = nullptr;
+  g.g_wstride = (int64_t)D * Ie;
+  g.out_t = nullptr;
+  g.out_f32 = m->moe_y;
+  g.ldo = D;
+  m->timed(1, D, T * k, Ie, s, [&] {
+    launch_gemm_bf16_grouped((const bf16*)w.wd_e, (const bf16*)m->moe_a, D, Ie, T * k, EPI_F32, g, s);
+  });
+  if (Is > 0) {
+    gemm_many<bf16>(m, w.wgu, h, 2 * Is, T, D, EPI_SILU, nullptr, m->a, Is, s);
+    gemm_many<bf16>(m, w.wd, m->a, D, T, Is, EPI_RESID, m->x, nullptr, D, s);
+  }
+  launch_moe_combine(m->x, m->moe_y, m->moe_inv, m->moe_topw, T, D, k, s);
+}
+
 // Fused few-token projection; a shape with no kernel is recorded in
 // m->enqueue_err (checked by the caller once the step is enqueued).
 void gemv_step(axon_model* m, const GemvArgs& a, int epi, hipStream_t s) {
@@ -387,13 +471,17 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
     }
     gemm_many<T>(m, w.wo, m->o, D, Ttok, H * hd, EPI_RESID, m->x, nullptr, D, s);
     launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, Ttok, D, eps, nullptr, s);
-    if constexpr (sizeof(T) == 2) {
-      gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_SILU, nullptr, m->a, I, s);
+    if (w.moe) {
+      enqueue_moe(m, w, (const bf16*)h, Ttok, s);  // bf16 only (checked at init)
     } else {
-      gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_F32, m->gu_f32, nullptr, 2 * I, s);
-      launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, Ttok, I, s);
+      if constexpr (sizeof(T) == 2) {
+        gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_SILU, nullptr, m->a, I, s);
+      } else {
+        gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_F32, m->gu_f32, nullptr, 2 * I, s);
+        launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, Ttok, I, s);
+      }
+      gemm_many<T>(m, w.wd, m->a, D, Ttok, I, EPI_RESID, m->x, nullptr, D, s);
     }
-    gemm_many<T>(m, w.wd, m->a, D, Ttok, I, EPI_RESID, m->x, nullptr, D, s);
     const bool last = l + 1 == m->cfg.n_layers;
     const T* gnext = (const T*)(last ? m->gfinal : m->layers[l + 1].gin);
     if (!last || all_logits)
@@ -447,13 +535,17 @@ void enqueue_decode_many(axon_model* m, int B, const int32_t* d_tokens, float* d
     launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
     proj(w.wo, m->o, D, H * hd, EPI_RESID, m->x, nullptr, D);
     launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, B, D, eps, nullptr, s);
-    if constexpr (sizeof(T) == 2) {
-      proj(w.wgu, h, 2 * I, D, EPI_SILU, nullptr, m->a, I);
+    if (w.moe) {
+      enqueue_moe(m, w, (const bf16*)h, B, s);
     } else {
-      proj(w.wgu, h, 2 * I, D, EPI_F32, m->gu_f32, nullptr, 2 * I);
-      launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, B, I, s);
+      if constexpr (sizeof(T) == 2) {
+        proj(w.wgu, h, 2 * I, D, EPI_SILU, nullptr, m->a, I);
+      } else {
+        proj(w.wgu, h, 2 * I, D, EPI_F32, m->gu_f32, nullptr, 2 * I);
+        launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, B, I, s);
+      }
+      proj(w.wd, m->a, D, I, EPI_RESID, m->x, nullptr, D);
     }
-    proj(w.wd, m->a, D, I, EPI_RESID, m->x, nullptr, D);
     const bool last = l + 1 == m->cfg.n_layers;
     const T* gnext = (const T*)(last ? m->gfinal : m->layers[l + 1].gin);
     launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, gnext, h, B, D, eps, nullptr, s);
@@ -531,7 +623,8 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
 }
 
 void enqueue_decode(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next, hipStream_t s) {
-  if (m->bf && B <= GEMV_MAX_M) enqueue_decode_bf16(m, B, d_tokens, d_logits, d_next, s);
+  // mixture-of-experts models decode through the GEMM path (grouped experts)
+  if (m->bf && B <= GEMV_MAX_M && !m->moe_model()) enqueue_decode_bf16(m, B, d_tokens, d_logits, d_next, s);
   else if (m->bf) enqueue_decode_many<bf16>(m, B, d_tokens, d_logits, d_next, s);
   else enqueue_decode_many<float>(m, B, d_tokens, d_logits, d_next, s);
 }
@@ -648,7 +741,9 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     }
   } stage;
   if (m->bf) {
-    const int64_t most = std::max({V * D, nq * D, D * H * hd, 2 * I * D});
+    const int64_t Ie = c.moe_intermediate, Is = (int64_t)c.n_shared_experts * Ie;
+    const int64_t most = std::max({V * D, nq * D, D * H * hd, 2 * I * D, 2 * Ie * D, 2 * Is * D,
+                                   (int64_t)m->moe_ep() * D});
     hipError_t e = hipMalloc(&stage.p, (size_t)most * esz);
     if (e != hipSuccess) {
       stage.p = nullptr;
@@ -670,6 +765,24 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     hipError_t e = hipGetLastError();
     return e == hipSuccess ? AXON_OK : fail(AXON_E_HIP, std::string("weight tiling: ") + hipGetErrorString(e));
   };
+  // fill the staging buffer, tile it into dst (bf16 only)
+  auto tile_into = [&](void* dst, int64_t N, int64_t K, const std::function<int(void*)>& fill) -> int {
+    int r = fill(stage.p);
+    if (r) return r;
+    launch_tile_weight((const bf16*)stage.p, (bf16*)dst, N, (int)K, s);
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? AXON_OK : fail(AXON_E_HIP, std::string("weight tiling: ") + hipGetErrorString(e));
+  };
+  // gate/up of an MLP of intermediate ii interleaved in blocks of 16 rows:
+  // [g0..g15, u0..u15, g16..g31, u16..u31, ...]
+  auto gate_up = [&](const axon_weight* wg, const axon_weight* wu, int64_t ii) {
+    return [&, wg, wu, ii](void* dst) -> int {
+      const size_t blk = 16 * D * esz;
+      hipError_t e = hipMemcpy2DAsync(dst, 2 * blk, wg->data, blk, blk, ii / 16, kind(wg), s);
+      if (e == hipSuccess) e = hipMemcpy2DAsync((char*)dst + blk, 2 * blk, wu->data, blk, blk, ii / 16, kind(wu), s);
+      return e == hipSuccess ? AXON_OK : fail(AXON_E_HIP, std::string("gate/up repack: ") + hipGetErrorString(e));
+    };
+  };
   auto copy_to = [&](const axon_weight* w) {
     return [&, w](void* dst) -> int {
       const size_t bytes = (size_t)w->shape[0] * (size_t)w->shape[1] * esz;
@@ -690,7 +803,8 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     TRY(copy_in(&w.gin, get(p + "input_layernorm.weight")));
     TRY(copy_in(&w.gpost, get(p + "post_attention_layernorm.weight")));
     TRY(matrix(&w.wo, D, H * hd, copy_to(get(p + "self_attn.o_proj.weight"))));
-    TRY(matrix(&w.wd, D, I, copy_to(get(p + "mlp.down_proj.weight"))));
+    w.moe = c.n_experts > 0 && l >= c.first_moe_layer;
+    if (!w.moe) TRY(matrix(&w.wd, D, I, copy_to(get(p + "mlp.down_proj.weight"))));
     // fused QKV: heads q, then k, then v; within each head, rows in groups of
     // 8 = 4 first-half rows i and their rotation partners i + hd/2
     const axon_weight* wq = get(p + "self_attn.q_proj.weight");
@@ -721,15 +835,34 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
       HTRY(hipMemcpyAsync((char*)w.bqkv + H * hd * esz, bk->data, KV * hd * esz, kind(bk), s));
       HTRY(hipMemcpyAsync((char*)w.bqkv + (H + KV) * hd * esz, bv->data, KV * hd * esz, kind(bv), s));
     }
-    // gate/up interleaved in blocks of 16 rows: [g0..g15, u0..u15, g16..g31, u16..u31, ...]
-    const axon_weight* wg = get(p + "mlp.gate_proj.weight");
-    const axon_weight* wu = get(p + "mlp.up_proj.weight");
-    TRY(matrix(&w.wgu, 2 * I, D, [&](void* dst) -> int {
-      const size_t blk = 16 * D * esz;
-      hipError_t e = hipMemcpy2DAsync(dst, 2 * blk, wg->data, blk, blk, I / 16, kind(wg), s);
-      if (e == hipSuccess) e = hipMemcpy2DAsync((char*)dst + blk, 2 * blk, wu->data, blk, blk, I / 16, kind(wu), s);
-      return e == hipSuccess ? AXON_OK : fail(AXON_E_HIP, std::string("gate/up repack: ") + hipGetErrorString(e));
+    if (!w.moe) {
+      TRY(matrix(&w.wgu, 2 * I, D, gate_up(get(p + "mlp.gate_proj.weight"), get(p + "mlp.up_proj.weight"), I)));
+      continue;
+    }
+    // mixture of experts (bf16 only): router rows padded with zeros to a
+    // multiple of 32, experts stacked, shared experts as a dense MLP
+    const int64_t E = c.n_experts, Ep = m->moe_ep(), Ie = c.moe_intermediate;
+    const int64_t Is = (int64_t)c.n_shared_experts * Ie;
+    const axon_weight* wr = get(p + "mlp.gate.weight");
+    TRY(matrix(&w.wrouter, Ep, D, [&](void* dst) -> int {
+      hipError_t e = hipMemcpyAsync(dst, wr->data, (size_t)E * D * esz, kind(wr), s);
+      if (e == hipSuccess && Ep > E) e = hipMemsetAsync((char*)dst + E * D * esz, 0, (size_t)(Ep - E) * D * esz, s);
+      return e == hipSuccess ? AXON_OK : fail(AXON_E_HIP, std::string("router copy: ") + hipGetErrorString(e));
     }));
+    TRY(dev_alloc(m, &w.wgu_e, (size_t)E * 2 * Ie * D * esz));
+    TRY(dev_alloc(m, &w.wd_e, (size_t)E * D * Ie * esz));
+    for (int64_t e = 0; e < E; ++e) {
+      const std::string q = p + "mlp.experts." + std::to_string(e) + ".";
+      TRY(tile_into((char*)w.wgu_e + e * 2 * Ie * D * esz, 2 * Ie, D,
+                    gate_up(get(q + "gate_proj.weight"), get(q + "up_proj.weight"), Ie)));
+      TRY(tile_into((char*)w.wd_e + e * D * Ie * esz, D, Ie, copy_to(get(q + "down_proj.weight"))));
+    }
+    w.wgu = w.wd = nullptr;
+    if (Is > 0) {
+      TRY(matrix(&w.wgu, 2 * Is, D,
+                 gate_up(get(p + "mlp.shared_experts.gate_proj.weight"), get(p + "mlp.shared_experts.up_proj.weight"), Is)));
+      TRY(matrix(&w.wd, D, Is, copy_to(get(p + "mlp.shared_experts.down_proj.weight"))));
+    }
   }
 
   // ---- KV cache
@@ -778,7 +911,21 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     if (!m->bf) TRY(dev_alloc(m, (void**)&m->qkv, tmax * nq * 4));  // bf16: RoPE is the QKV GEMM's epilogue
     TRY(dev_alloc(m, &m->q, tmax * H * hd * esz));
     TRY(dev_alloc(m, &m->o, tmax * H * hd * esz));
-    TRY(dev_alloc(m, &m->a, tmax * I * esz));
+    const int64_t Ishared = (int64_t)c.n_shared_experts * c.moe_intermediate;
+    TRY(dev_alloc(m, &m->a, tmax * std::max<int64_t>(I, Ishared) * esz));
+    if (m->moe_model()) {
+      const int64_t E = c.n_experts, k = c.top_k;
+      TRY(dev_alloc(m, (void**)&m->moe_logits, tmax * m->moe_ep() * 4));
+      TRY(dev_alloc(m, (void**)&m->moe_topi, tmax * k * 4));
+      TRY(dev_alloc(m, (void**)&m->moe_topw, tmax * k * 4));
+      TRY(dev_alloc(m, (void**)&m->moe_cnt, (size_t)(3 * E + 2) * 4));
+      m->moe_off = m->moe_cnt + E;
+      m->moe_toff = m->moe_off + E + 1;
+      TRY(dev_alloc(m, (void**)&m->moe_xrow, tmax * k * 4));
+      TRY(dev_alloc(m, (void**)&m->moe_inv, tmax * k * 4));
+      TRY(dev_alloc(m, &m->moe_a, tmax * k * c.moe_intermediate * esz));
+      TRY(dev_alloc(m, (void**)&m->moe_y, tmax * k * D * 4));
+    }
     TRY(dev_alloc(m, &m->hlast, (int64_t)c.max_batch * D * esz));
     TRY(dev_alloc(m, (void**)&m->logits_int, (int64_t)c.max_batch * V * 4));
     if (!m->bf) TRY(dev_alloc(m, (void**)&m->gu_f32, tmax * 2 * I * 4));
@@ -1074,7 +1221,7 @@ extern "C" int axon_step(axon_model* m, int32_t n, const int32_t* h_slots, const
   plan.d_drow = m->d_step + 3 * MB;
   plan.d_dslot = m->d_step + 4 * MB;
   plan.d_dpos = m->d_step + 5 * MB;
-  if (m->bf && nd == n && n <= GEMV_MAX_M) {
+  if (m->bf && nd == n && n <= GEMV_MAX_M && !m->moe_model()) {
     // decode tokens only: the fused weight-streaming decode step, recorded as
     // a graph per (n, buffers); the per-entry arrays are read from d_step
     if (int rc = replay_or_run(m, GraphKey{n, d_tokens, d_logits, d_next_tokens, d_cu_seqlens}, s, "step",

@@ -259,7 +259,12 @@ AXON_DEV void phase_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int EPI>
+// GROUPED: the mixture-of-experts form (EpiArgs::g_*): workgroup L takes n-tile
+// L % gx of m-tile L / gx in the experts' tile sequence; that m-tile belongs to
+// expert e (g_toff[e] <= L / gx < g_toff[e+1]), covers its local rows
+// m0 .. m0+255 of M = g_off[e+1] - g_off[e], reads X row g_xrow[g_off[e] +
+// row] and writes output row g_off[e] + row.
+template <int EPI, bool GROUPED = false>
 __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __restrict__ W,
                                                                const bf16* __restrict__ X, int N, int M, int K,
                                                                EpiArgs ep) {
@@ -270,10 +275,27 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar branches only
   const int grp = wave >> 2, wc = wave & 3;
-  const int gx = (N + BN - 1) / BN, gy = (M + BM - 1) / BM;
-  int pn, pm;
-  tile_order(blockIdx.x, gx, gy, pn, pm);
-  const int n0 = pn * BN, m0 = pm * BM;
+  const int gx = (N + BN - 1) / BN;
+  int pn, pm, n0, m0, rowbase = 0;
+  if constexpr (GROUPED) {
+    const int mt = blockIdx.x / gx;
+    if (mt >= ep.g_toff[ep.g_E]) return;  // surplus workgroup: exits before any barrier
+    int lo = 0, hi = ep.g_E - 1;          // the expert: largest e with g_toff[e] <= mt
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (ep.g_toff[mid] <= mt) lo = mid; else hi = mid - 1;
+    }
+    const int e = lo;
+    pn = blockIdx.x % gx;
+    pm = mt - ep.g_toff[e];
+    rowbase = ep.g_off[e];
+    M = ep.g_off[e + 1] - rowbase;  // this expert's rows (>= 1: it has an m-tile)
+    W += (int64_t)e * ep.g_wstride;
+  } else {
+    tile_order(blockIdx.x, gx, (M + BM - 1) / BM, pn, pm);
+  }
+  n0 = pn * BN;
+  m0 = pm * BM;
 
   // this lane's chunks of a stage: q = (i * 8 + wave) * 64 + lane, i < LPT,
   // row q / CH, logical chunk swz(row, q % CH) (swz is its own inverse)
@@ -287,7 +309,9 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
       const int n = min(n0 + row, N - 1), m = min(m0 + row, M - 1);  // rows past the edge: any valid row
       // wt_chunk(n, k0 / 8 + c, K) with k0 a multiple of 32
       const bf16* ws = W + ((int64_t)(n >> 4) * rowblk + (int64_t)k0 * 16 + ((n & 15) + 16 * c) * 8);
-      const bf16* xs = X + (int64_t)m * K + k0 + c * 8;
+      int64_t xr = m;
+      if constexpr (GROUPED) xr = ep.g_xrow ? ep.g_xrow[rowbase + m] : rowbase + m;
+      const bf16* xs = X + xr * K + k0 + c * 8;
       bf16x8* base = lds2 + stage * STAGE + (i * 8 + wave) * 64;
       __builtin_amdgcn_global_load_lds((const void*)ws, (__attribute__((address_space(3))) void*)base, 16, 0, 0);
       __builtin_amdgcn_global_load_lds((const void*)xs, (__attribute__((address_space(3))) void*)(base + PANEL),
@@ -355,10 +379,12 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
 
   // epilogue: acc[a][b][i] = C[n][t],
   //   n = n0 + grp*128 + a*32 + (i/4)*8 + (lane/32)*4 + i%4,  t = m0 + wc*64 + b*32 + lane%32
+  // (grouped: output row rowbase + t)
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
-    const int t = m0 + wc * 64 + b * 32 + (lane & 31);
-    if (t >= M) continue;
+    const int tl = m0 + wc * 64 + b * 32 + (lane & 31);
+    if (tl >= M) continue;
+    const int t = rowbase + tl;
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
       const int nb = n0 + grp * 128 + a * 32;
@@ -399,6 +425,28 @@ static void launch_256(const bf16* W, const bf16* X, int N, int M, int K, const 
   }
   const int tiles = ((N + pf2::BN - 1) / pf2::BN) * ((M + pf2::BM - 1) / pf2::BM);
   klaunch(kern, dim3(tiles), dim3(512), pf2::LDS_BYTES, s, W, X, N, M, K, ep);
+}
+
+template <int EPI>
+static void launch_grouped(const bf16* W, const bf16* X, int N, int K, int max_rows, const EpiArgs& ep,
+                           hipStream_t s) {
+  static bool attr = false;
+  auto kern = gemm_bf16_256_kernel<EPI, true>;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, pf2::LDS_BYTES);
+    attr = true;
+  }
+  // sum over experts of ceil(rows_e / 256) <= ceil(max_rows / 256) + E
+  const int64_t mtiles = (max_rows + pf2::BM - 1) / pf2::BM + ep.g_E;
+  const int64_t tiles = mtiles * ((N + pf2::BN - 1) / pf2::BN);
+  klaunch(kern, dim3((unsigned)tiles), dim3(512), pf2::LDS_BYTES, s, W, X, N, 0, K, ep);
+}
+
+void launch_gemm_bf16_grouped(const bf16* W, const bf16* X, int N, int K, int max_rows, int epi, const EpiArgs& ep,
+                              hipStream_t s) {
+  if (max_rows <= 0) return;
+  if (epi == EPI_SILU) launch_grouped<EPI_SILU>(W, X, N, K, max_rows, ep, s);
+  else launch_grouped<EPI_F32>(W, X, N, K, max_rows, ep, s);
 }
 
 void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi, const EpiArgs& ep,

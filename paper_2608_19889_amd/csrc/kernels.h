@@ -60,6 +60,15 @@ struct EpiArgs {
   // position of its first token ent_base[e]; null: slot e, position 0
   const int32_t* ent_slot;
   const int32_t* ent_base;
+  // grouped GEMM (mixture of experts): expert e multiplies its matrix W + e *
+  // g_wstride with rows g_off[e] .. g_off[e+1]-1 of the grouped operand; row a
+  // of it is X row g_xrow[a] (a when null), output row a.  g_toff[e] = sum of
+  // ceil(rows / 256) over the experts before e.
+  const int32_t* g_off;
+  const int32_t* g_toff;
+  const int32_t* g_xrow;
+  int64_t g_wstride;
+  int g_E;
 };
 
 // ---- weight layout (k_layout.hip): fragment-tiled copy of row-major bf16
@@ -86,6 +95,11 @@ void launch_set_step_lengths(const int32_t* cu, const int32_t* ent_slot, const i
 // (EPI_ROPE: the head dimension a multiple of 32).
 void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi, const EpiArgs& ep,
                       hipStream_t s);
+// Grouped GEMM of the experts (ep.g_*): rows of all experts together at most
+// max_rows; launches enough 256 x 256 tiles for any split of them over the
+// experts (surplus workgroups exit at once).  EPI_F32 or EPI_SILU.
+void launch_gemm_bf16_grouped(const bf16* W, const bf16* X, int N, int K, int max_rows, int epi, const EpiArgs& ep,
+                              hipStream_t s);
 // float32 check-mode GEMM (any M): EPI_F32 / EPI_RESID / EPI_PART(split 0 only).
 void launch_gemm_f32(const float* W, const float* X, int N, int M, int K, int epi, const EpiArgs& ep,
                      hipStream_t s);
@@ -182,5 +196,20 @@ template <typename T>
 void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len,
                         int max_ctx, hipStream_t s, const int32_t* rows = nullptr,
                         const int32_t* slots = nullptr);
+
+// ---- mixture of experts (k_moe.hip)
+// topi / topw [T][k]: the top_k experts of each token (E <= 256, k <= 8) from
+// float logits [T][ldl], and their softmax probabilities (over all E),
+// divided by their sum when norm
+void launch_moe_route(const float* logits, int ldl, int T, int E, int k, int norm, int32_t* topi, float* topw,
+                      hipStream_t s);
+// grouped-GEMM plan of the T*k choices: cnt [E], off / toff [E+1] (rows and
+// 256-row tiles before each expert), xrow [T*k] (token of each grouped row),
+// inv [T*k] (grouped row of choice t*k + j)
+void launch_moe_plan(const int32_t* topi, int T, int E, int k, int32_t* cnt, int32_t* off, int32_t* toff,
+                     int32_t* xrow, int32_t* inv, hipStream_t s);
+// x[t] += sum_j w[t][j] * y[inv[t*k+j]] (float rows of D, D % 4 == 0)
+void launch_moe_combine(float* x, const float* y, const int32_t* inv, const float* w, int T, int D, int k,
+                        hipStream_t s);
 
 }  // namespace axon

@@ -38,7 +38,8 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_struct_layout_matches_header():
-    assert ctypes.sizeof(axon.AxonConfig) == 72
+    assert ctypes.sizeof(axon.AxonConfig) == 96
+    assert axon.AxonConfig.n_experts.offset == 72 and axon.AxonConfig.norm_topk_prob.offset == 92
     assert axon.AxonConfig.rope_theta.offset == 32
     assert ctypes.sizeof(axon.AxonWeight) == 48
 
@@ -173,3 +174,39 @@ def test_step_and_reset_reject_a_null_model():
     rc = lib.axon_step(None, 1, sl, None, None, None, cu, None, 0, None, None, None)
     assert rc == axon.AXON_E_INVALID and "NULL" in axon.last_error()
     assert lib.axon_reset_slot(None, 0) == axon.AXON_E_INVALID
+
+
+def _moe_shape(**kw):
+    s = _shape()
+    s.update(n_routed_experts=4, num_experts_per_tok=2, moe_intermediate_size=64, n_shared_experts=1,
+             first_k_dense_replace=1, norm_topk_prob=False)
+    s.update(kw)
+    return s
+
+
+@pytest.mark.parametrize("field,value,fragment", [
+    ("n_experts", 1, "n_experts"), ("n_experts", 300, "n_experts"), ("top_k", 0, "top_k"),
+    ("top_k", 5, "top_k"), ("moe_intermediate", 96, "moe_intermediate"), ("n_shared_experts", -1, "n_shared"),
+    ("first_moe_layer", 3, "first_moe_layer"), ("norm_topk_prob", 2, "norm_topk_prob"), ("dtype", 2, "AXON_BF16")])
+def test_bad_moe_config_is_rejected(field, value, fragment):
+    s = _moe_shape()
+    rc, msg = _status(s, _fake_weights(s), override={field: value})
+    assert rc == axon.AXON_E_INVALID and fragment in msg, (rc, msg)
+
+
+def test_moe_weight_map_is_checked():
+    s = _moe_shape()
+    w = _fake_weights(s)
+    assert "model.layers.1.mlp.experts.3.up_proj.weight" in w and "model.layers.0.mlp.up_proj.weight" in w
+    missing = dict(w)
+    del missing["model.layers.1.mlp.experts.3.up_proj.weight"]
+    rc, msg = _status(s, missing)
+    assert rc == axon.AXON_E_MISSING and "experts.3.up_proj" in msg
+    bad = dict(w)
+    bad["model.layers.1.mlp.shared_experts.down_proj.weight"] = torch.empty((128, 128), dtype=torch.bfloat16)
+    rc, msg = _status(s, bad)
+    assert rc == axon.AXON_E_SHAPE and "shared_experts.down_proj" in msg and "[128, 64]" in msg, msg
+    dense_names = dict(w)
+    dense_names["model.layers.1.mlp.gate_proj.weight"] = torch.empty((128, 128), dtype=torch.bfloat16)
+    rc, msg = _status(s, dense_names)
+    assert rc == axon.AXON_E_MISSING and "unknown" in msg and "layers.1.mlp.gate_proj" in msg

@@ -1,0 +1,121 @@
+"""Mixture-of-experts decoders on the GPU against the float64 oracle.
+
+Small models with the DeepSeek-MoE layout (a dense first layer, routed
+experts without renormalization, shared experts) and the renormalized
+variant, through prefill (grouped expert GEMMs over 256-row tiles, ragged
+per-expert row counts), graph-replayed decode and continuous-batching steps.
+
+Routing is an integer decision taken from floating-point probabilities, and
+near a tie both choices are correct.  The GPU takes it from bf16-stored normed
+activations, as the oracle's bf16-storage mode does, but a bf16 rounding
+boundary can turn an upstream difference of ~1e-9 into one bf16 step of an
+input and move a router probability by ~1e-5, so decisions closer than that
+may go either way.  The tests therefore hold every logits row to the band
+around the exact oracle (which includes such flips), and hold the rows whose
+token has no routing decision within 1e-3 of a tie (most of them) to the
+absolute bf16-storage tolerance.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from parity_util import (BF16_MAX, BF16_MEAN, check_argmax, check_bf16, check_logits, gpu_model, pack,
+                         run_teacher_forced)
+from synthetic import model_weights, prompts, small_shape
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # DeepSeek-MoE layout: layer 0 dense, 8 experts, top 2, 1 shared expert
+    "deepseek_style": ("1b", dict(layers=3, vocab=2000, hidden=512, intermediate=1024),
+                       dict(n_routed_experts=8, num_experts_per_tok=2, moe_intermediate_size=256,
+                            n_shared_experts=1, first_k_dense_replace=1, norm_topk_prob=False)),
+    # renormalized top 4 of 16 experts, every layer MoE, head_dim 128, QKV bias
+    "renormalized_hd128": ("7b", dict(layers=2, vocab=1500, hidden=640, intermediate=1280),
+                           dict(n_routed_experts=16, num_experts_per_tok=4, moe_intermediate_size=128,
+                                n_shared_experts=0, first_k_dense_replace=0, norm_topk_prob=True)),
+}
+
+
+def _shape(case):
+    base, ov, moe = CASES[case]
+    s = small_shape(base, **ov)
+    s.update(moe)
+    return s
+
+
+def _router_gaps(shape, w64, seqs, forced):
+    """[steps+1, B]: for every compared logits row (the last prompt token of
+    each sequence, then each teacher-forced decode token) the smallest gap
+    between the k-th and (k+1)-th router probability of that token over the
+    MoE layers, in the bf16-storage oracle."""
+    record = []
+    orig = oracle.decoder.moe_mlp
+
+    def spy(h, w_router, experts, shared, top_k, norm_topk, rnd=None):
+        p = oracle.decoder.softmax(h @ w_router.T)
+        srt = np.sort(p, axis=-1)[:, ::-1]
+        record.append(srt[:, top_k - 1] - srt[:, top_k])
+        return orig(h, w_router, experts, shared, top_k, norm_topk, rnd)
+
+    oracle.decoder.moe_mlp = spy
+    try:
+        oracle.teacher_forced(oracle.OracleDecoder(shape, w64, io_round="bf16"), seqs, forced)
+    finally:
+        oracle.decoder.moe_mlp = orig
+    n_moe = sum(1 for i in range(shape["num_hidden_layers"]) if i >= shape["first_k_dense_replace"])
+    calls = [record[i:i + n_moe] for i in range(0, len(record), n_moe)]  # one per sequence and call
+    B, steps = len(seqs), forced.shape[1]
+    out = np.empty((steps + 1, B))
+    for b in range(B):
+        out[0, b] = min(g[-1] for g in calls[b])
+        for st in range(steps):
+            out[st + 1, b] = min(g[0] for g in calls[B + st * B + b])
+    return out
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_moe_prefill_and_decode_against_oracle(case):
+    shape = _shape(case)
+    w = model_weights(shape, seed=31)
+    lens = [37, 130, 300, 5]
+    ids = prompts(len(lens), max(lens), shape["vocab_size"], seed=32).numpy()
+    seqs = [ids[i, :n] for i, n in enumerate(lens)]
+    steps = 4
+    w64 = oracle.weights_f64(w)
+    ref_tok, ref_lg = oracle.generate_greedy(oracle.OracleDecoder(shape, w64), seqs, steps)
+    ref_b = oracle.teacher_forced(oracle.OracleDecoder(shape, w64, io_round="bf16"), seqs, ref_tok[:, :steps])
+    gaps = _router_gaps(shape, w64, seqs, ref_tok[:, :steps])
+    clear = gaps >= 1e-3
+    print(f"{case}: smallest router top-k gap of a compared token {gaps.min():.3e}; "
+          f"{int(clear.sum())} of {clear.size} rows clear of routing near-ties")
+    assert clear.mean() >= 0.75
+    m = gpu_model(shape, w, max_batch=len(lens), max_seq=max(lens) + steps + 2)
+    lg, _ = run_teacher_forced(m, seqs, ref_tok[:, :steps])
+    mx = check_bf16(lg, ref_lg, ref_b, f"moe {case}", absolute=False)
+    check_logits(lg[clear], ref_b[clear], BF16_MAX, BF16_MEAN, f"moe {case}, rows clear of near-ties, vs bf16 storage")
+    check_argmax(lg, ref_lg, mx, f"moe {case}")
+    m.close()
+
+
+def test_moe_chunked_prefill_equals_one_shot_bitwise():
+    """Routing, the grouped expert rows and the combine are per token, so a
+    prompt fed in chunks gives the one-shot prefill's logits bit for bit."""
+    shape = _shape("deepseek_style")
+    w = model_weights(shape, seed=33)
+    ids = prompts(2, 120, shape["vocab_size"], seed=34).numpy()
+    a, b = ids[0], ids[1, :45]
+    one = gpu_model(shape, w, max_batch=2, max_seq=128)
+    flat, cu = pack([a, b])
+    ref, _ = one.prefill(flat, cu)
+    ref = ref.cpu().numpy()
+    one.close()
+    m = gpu_model(shape, w, max_batch=2, max_seq=128)
+    m.step(*pack([a[:50], b[:20]]), [0, 1], [1, 1])
+    lg1, _ = m.step(*pack([a[50:100], b[20:]]), [0, 1], [0, 0])
+    lg2, _ = m.step(*pack([a[100:]]), [0], [0])
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(lg2.cpu().numpy()[0], ref[0])
+    np.testing.assert_array_equal(lg1.cpu().numpy()[1], ref[1])
+    m.close()
