@@ -49,7 +49,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="1b", choices=["1b", "7b", "135m", "7b_paged", "32b", "7b_serve"])
+    ap.add_argument("--workload", default="1b", choices=["1b", "7b", "135m", "7b_paged", "32b", "7b_serve", "moe16b"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=None,
@@ -174,8 +174,16 @@ def main():
     kv_read = sum(2 * L * KV * hd * (pos + 1) * esz for st in dsteps for pos in st)
     dtok = sum(len(st) for st in dsteps)
     kv_write = dtok * 2 * L * KV * hd * esz
-    decode_bytes = sum(wb - (0 if shape["tie_word_embeddings"] else emb) + len(st) * D * esz for st in dsteps) \
-        + kv_read + kv_write
+    # a mixture-of-experts step reads the experts its tokens choose: counted as
+    # the expectation under uniform routing, E (1 - (1 - k/E)^tokens) per layer
+    moe_b, moe_frac = 0, (lambda n: 1.0)
+    if shape.get("n_routed_experts"):
+        E, k, Ie = shape["n_routed_experts"], shape["num_experts_per_tok"], shape["moe_intermediate_size"]
+        n_moe = L - shape.get("first_k_dense_replace", 0)
+        moe_b = n_moe * E * 3 * D * Ie * esz
+        moe_frac = lambda n: 1.0 - (1.0 - k / E) ** n  # noqa: E731
+    decode_bytes = sum(wb - moe_b + moe_b * moe_frac(len(st)) - (0 if shape["tie_word_embeddings"] else emb)
+                       + len(st) * D * esz for st in dsteps) + kv_read + kv_write
     decode_gbs = decode_bytes / (decode_ms / 1e3) / 1e9
 
     out = {

@@ -68,6 +68,8 @@ WORKLOADS = {
     "7b_paged": dict(model="7b", batch=64, prompt_len=None, len_range=(64, 4096),
                      steps=128, paged=True, page_size=16),
     "32b": dict(model="32b", batch=32, prompt_len=1024, steps=256, paged=False),
+    # the DeepSeek-MoE-16B shape: routed experts through grouped GEMMs
+    "moe16b": dict(model="moe16b", batch=32, prompt_len=1024, steps=128, paged=False),
     # the 7b_paged requests served by continuous batching: every step carries
     # the running sequences' decode tokens plus prompt chunks of the waiting
     # ones, up to a token budget
