@@ -333,7 +333,11 @@ def roofline_pass(m, generate, shape, esz, lens):
     hd, KV, H = shape["head_dim"], shape["num_key_value_heads"], shape["num_attention_heads"]
     peak_mm = BF16_PEAK_TFLOPS if esz == 2 else F32_PEAK_TFLOPS
     sq = sum(n * (n + 1) / 2 for n in lens)
+    # grouped expert launches stream every expert some token chose: the
+    # expectation under uniform routing, E (1 - (1 - k/E)^tokens) experts
+    E_r, k_r = shape.get("n_routed_experts") or 1, shape.get("num_experts_per_tok") or 1
     cls_name = {ax.T_GEMV: "decode projection GEMM (weight streaming)",
+                ax.T_GEMV_GROUPED: "decode grouped experts (weight streaming)",
                 ax.T_GEMM: "prefill projection GEMM (MFMA)",
                 ax.T_ATTN_DECODE: "decode attention (+ split merge)",
                 ax.T_ATTN_PREFILL: "prefill flash attention"}
@@ -346,6 +350,11 @@ def roofline_pass(m, generate, shape, esz, lens):
             N, M, K = d0, d1, d2
             a["bytes"] += N * K * esz + M * K * esz + M * N * 4
             a["flops"] += 2.0 * N * M * K
+        elif c == ax.T_GEMV_GROUPED:
+            N, M, K = d0, d1, d2
+            active = E_r * (1.0 - (1.0 - k_r / E_r) ** M)
+            a["bytes"] += active * N * K * esz + M * K * esz + M * k_r * N * 4
+            a["flops"] += 2.0 * N * M * k_r * K
         elif c == ax.T_GEMM:
             N, M, K = d0, d1, d2
             a["flops"] += 2.0 * N * M * K
@@ -372,7 +381,7 @@ def roofline_pass(m, generate, shape, esz, lens):
             f"{b['bytes'] / (b['ms'] / 1e3) / 1e9:.0f} GB/s")
     kernels = {}
     for c, a in agg.items():
-        hbm = c in (ax.T_GEMV, ax.T_ATTN_DECODE)
+        hbm = c in (ax.T_GEMV, ax.T_GEMV_GROUPED, ax.T_ATTN_DECODE)
         ach = (a["bytes"] / (a["ms"] / 1e3) / 1e9) if hbm else (a["flops"] / (a["ms"] / 1e3) / 1e12)
         peak = HBM_PEAK_GBS if hbm else peak_mm
         kernels[cls_name[c]] = {"bound": "hbm" if hbm else "mfma", "achieved": round(ach, 1),

@@ -213,7 +213,10 @@ int axon_slot_lengths(const axon_model* m, int32_t* lens, int32_t n);
  *   0 = few-token projection GEMM (decode, weight streaming),
  *   1 = many-token projection GEMM (prefill, MFMA tiles),
  *   2 = decode attention (split over key chunks, with its combine kernel),
- *   3 = prefill attention
+ *   3 = prefill attention,
+ *   4 = grouped expert projection of a mixture-of-experts decode step (dims
+ *       as class 0 with N, K of one expert and M the step's tokens; the
+ *       launch streams the weights of every expert that some token chose)
  * is bracketed by two HIP events recorded on the stream it is launched on, and
  * decode steps run eagerly instead of as a recorded graph (kernel durations
  * are unchanged; only launch gaps differ).  Enabling (1) or disabling (0)

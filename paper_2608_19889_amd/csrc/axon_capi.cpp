@@ -340,18 +340,49 @@ void gemm_few_f32(axon_model* m, const void* W, const void* X, int N, int M, int
   m->timed(0, N, M, K, s, [&] { launch_gemm_f32((const float*)W, (const float*)X, N, M, K, epi, ep, s); });
 }
 
-// Mixture-of-experts MLP of a layer over T rows of normed activations h
-// (bf16), added to the residual stream x: router logits (float) -> top-k
-// routing -> grouped-GEMM plan -> grouped gate/up with the SiLU gate over the
-// gathered token rows -> grouped down -> shared experts (dense, residual
-// epilogue) -> weighted combine of each token's k expert rows into x.
-void enqueue_moe(axon_model* m, const LayerW& w, const bf16* h, int T, hipStream_t s) {
+// Fused few-token projection; a shape with no kernel is recorded in
+// m->enqueue_err (checked by the caller once the step is enqueued).
+void gemv_step(axon_model* m, const GemvArgs& a, int epi, hipStream_t s) {
+  bool ok = true;
+  m->timed(0, a.N, a.M, a.K, s, [&] { ok = launch_gemv_fused(a, epi, s); });
+  if (!ok && m->enqueue_err.empty())
+    m->enqueue_err = "no fused projection kernel for N=" + std::to_string(a.N) + " K=" + std::to_string(a.K) +
+                     " M=" + std::to_string(a.M) + " epilogue " + std::to_string(epi);
+}
+
+// Routed experts of a mixture-of-experts layer over T rows of normed
+// activations h (bf16): router logits (float) -> top-k routing -> grouped plan
+// -> grouped gate/up with the SiLU gate over the gathered token rows ->
+// grouped down, one float row per (token, choice) in m->moe_y.  Up to 64
+// tokens (decode) the experts' weights are streamed once by the grouped
+// few-token projection (a workgroup per 64-row block and expert, the
+// expert's rows gathered from h); wider batches take the grouped GEMM.
+void moe_routed(axon_model* m, const LayerW& w, const bf16* h, int T, hipStream_t s) {
   const axon_config& c = m->cfg;
   const int D = m->D(), E = c.n_experts, k = c.top_k, Ie = c.moe_intermediate, Ep = m->moe_ep();
-  const int Is = c.n_shared_experts * Ie;
-  gemm_many<bf16>(m, w.wrouter, h, Ep, T, D, EPI_F32, m->moe_logits, nullptr, Ep, s);
+  if (T <= GEMV_MAX_M) {
+    GemvArgs ra{};
+    ra.W = (const bf16*)w.wrouter; ra.N = Ep; ra.K = D; ra.M = T; ra.X = h;
+    ra.out_f32 = m->moe_logits; ra.ldo = Ep; ra.part = m->gemv_part;
+    gemv_step(m, ra, GV_F32, s);
+  } else {
+    gemm_many<bf16>(m, w.wrouter, h, Ep, T, D, EPI_F32, m->moe_logits, nullptr, Ep, s);
+  }
   launch_moe_route(m->moe_logits, Ep, T, E, k, c.norm_topk_prob, m->moe_topi, m->moe_topw, s);
   launch_moe_plan(m->moe_topi, T, E, k, m->moe_cnt, m->moe_off, m->moe_toff, m->moe_xrow, m->moe_inv, s);
+  if (T <= GEMV_MAX_M) {
+    GemvArgs ga{};
+    ga.W = (const bf16*)w.wgu_e; ga.N = 2 * Ie; ga.K = D; ga.M = T; ga.X = h;
+    ga.out_t = (bf16*)m->moe_a; ga.ldo = Ie;
+    ga.g_off = m->moe_off; ga.g_xrow = m->moe_xrow; ga.g_wstride = (int64_t)2 * Ie * D;
+    m->timed(4, 2 * Ie, T, D, s, [&] { launch_gemv_grouped(ga, GV_SILU, E, s); });
+    GemvArgs da{};
+    da.W = (const bf16*)w.wd_e; da.N = D; da.K = Ie; da.M = T; da.X = (const bf16*)m->moe_a;
+    da.out_f32 = m->moe_y; da.ldo = D;
+    da.g_off = m->moe_off; da.g_xrow = nullptr; da.g_wstride = (int64_t)D * Ie;
+    m->timed(4, D, T, Ie, s, [&] { launch_gemv_grouped(da, GV_F32, E, s); });
+    return;
+  }
   EpiArgs g{};
   g.g_off = m->moe_off;
   g.g_toff = m->moe_toff;
@@ -371,22 +402,22 @@ void enqueue_moe(axon_model* m, const LayerW& w, const bf16* h, int T, hipStream
   m->timed(1, D, T * k, Ie, s, [&] {
     launch_gemm_bf16_grouped((const bf16*)w.wd_e, (const bf16*)m->moe_a, D, Ie, T * k, EPI_F32, g, s);
   });
+}
+
+// Mixture-of-experts MLP of a layer over T rows of normed activations h,
+// added to the residual stream x: routed experts, shared experts (dense,
+// residual epilogue), then the weighted combine of each token's k expert
+// rows into x.
+void enqueue_moe(axon_model* m, const LayerW& w, const bf16* h, int T, hipStream_t s) {
+  const int D = m->D(), Is = m->cfg.n_shared_experts * m->cfg.moe_intermediate;
+  moe_routed(m, w, h, T, s);
   if (Is > 0) {
     gemm_many<bf16>(m, w.wgu, h, 2 * Is, T, D, EPI_SILU, nullptr, m->a, Is, s);
     gemm_many<bf16>(m, w.wd, m->a, D, T, Is, EPI_RESID, m->x, nullptr, D, s);
   }
-  launch_moe_combine(m->x, m->moe_y, m->moe_inv, m->moe_topw, T, D, k, s);
+  launch_moe_combine(m->x, m->moe_y, m->moe_inv, m->moe_topw, T, D, m->cfg.top_k, s);
 }
 
-// Fused few-token projection; a shape with no kernel is recorded in
-// m->enqueue_err (checked by the caller once the step is enqueued).
-void gemv_step(axon_model* m, const GemvArgs& a, int epi, hipStream_t s) {
-  bool ok = true;
-  m->timed(0, a.N, a.M, a.K, s, [&] { ok = launch_gemv_fused(a, epi, s); });
-  if (!ok && m->enqueue_err.empty())
-    m->enqueue_err = "no fused projection kernel for N=" + std::to_string(a.N) + " K=" + std::to_string(a.K) +
-                     " M=" + std::to_string(a.M) + " epilogue " + std::to_string(epi);
-}
 
 // A continuous-batching step: entry e appends tokens cu[e] .. cu[e+1]-1 to
 // slot slot[e] from position base[e].  Entries of >= 2 tokens (prompt chunks)
@@ -600,17 +631,38 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
     oa.part = m->gemv_part;
     gemv(oa, GV_RESID);
     ss_n = ss_count(H * hd);
-    GemvArgs ga{};
-    ga.W = (const bf16*)w.wgu; ga.N = 2 * I; ga.K = D; ga.M = B;
-    ga.X = xg; ga.ss_in = m->ss; ga.ss_n = ss_n; ga.eps = eps;
-    ga.out_t = (bf16*)m->a; ga.ldo = I;
-    gemv(ga, GV_SILU);
-    GemvArgs da{};
-    da.W = (const bf16*)w.wd; da.N = D; da.K = I; da.M = B; da.X = (const bf16*)m->a;
-    da.out_f32 = m->x; da.ldo = D; da.ss_out = m->ss; da.xg_out = xg; da.part = m->gemv_part;
-    da.gain_next = (const bf16*)(last ? m->gfinal : m->layers[l + 1].gin);
-    gemv(da, GV_RESID);
-    ss_n = ss_count(I);
+    const bf16* gnext = (const bf16*)(last ? m->gfinal : m->layers[l + 1].gin);
+    // dense MLP, or the shared experts of a mixture-of-experts layer
+    const int Id = w.moe ? m->cfg.n_shared_experts * m->cfg.moe_intermediate : I;
+    if (w.moe) {
+      // the router and the routed experts read normed rows h; x gains the
+      // routed rows before the shared experts' down projection (which then
+      // leaves the next layer's xg and sums of squares), or, without shared
+      // experts, the combine leaves them
+      launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, (const bf16*)w.gpost, (bf16*)m->h, B, D, eps, nullptr, s);
+      moe_routed(m, w, (const bf16*)m->h, B, s);
+    }
+    if (Id > 0) {
+      GemvArgs ga{};
+      ga.W = (const bf16*)w.wgu; ga.N = 2 * Id; ga.K = D; ga.M = B;
+      ga.X = xg; ga.ss_in = m->ss; ga.ss_n = ss_n; ga.eps = eps;
+      ga.out_t = (bf16*)m->a; ga.ldo = Id; ga.part = m->gemv_part;
+      gemv(ga, GV_SILU);
+    }
+    if (w.moe) {
+      const bool fold = Id == 0;  // no shared experts: the combine leaves xg
+      launch_moe_combine(m->x, m->moe_y, m->moe_inv, m->moe_topw, B, D, m->cfg.top_k, s, fold ? gnext : nullptr,
+                         fold ? xg : nullptr, fold ? m->ss : nullptr);
+      if (fold) ss_n = moe_combine_blocks(D);
+    }
+    if (Id > 0) {
+      GemvArgs da{};
+      da.W = (const bf16*)w.wd; da.N = D; da.K = Id; da.M = B; da.X = (const bf16*)m->a;
+      da.out_f32 = m->x; da.ldo = D; da.ss_out = m->ss; da.xg_out = xg; da.part = m->gemv_part;
+      da.gain_next = gnext;
+      gemv(da, GV_RESID);
+      ss_n = ss_count(Id);
+    }
   }
   GemvArgs ha{};
   ha.W = (const bf16*)m->lm_head; ha.N = V; ha.K = D; ha.M = B;
@@ -623,8 +675,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
 }
 
 void enqueue_decode(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next, hipStream_t s) {
-  // mixture-of-experts models decode through the GEMM path (grouped experts)
-  if (m->bf && B <= GEMV_MAX_M && !m->moe_model()) enqueue_decode_bf16(m, B, d_tokens, d_logits, d_next, s);
+  if (m->bf && B <= GEMV_MAX_M) enqueue_decode_bf16(m, B, d_tokens, d_logits, d_next, s);
   else if (m->bf) enqueue_decode_many<bf16>(m, B, d_tokens, d_logits, d_next, s);
   else enqueue_decode_many<float>(m, B, d_tokens, d_logits, d_next, s);
 }
@@ -935,10 +986,17 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     TRY(dev_alloc(m, (void**)&m->attn_part, bsplits * H * (hd + 2) * 4));
     if (m->bf) {
       int64_t wsf = 0;
-      for (int b = 1; b <= std::min<int>(c.max_batch, GEMV_MAX_M); ++b)
+      const int Is = c.n_shared_experts * c.moe_intermediate;
+      for (int b = 1; b <= std::min<int>(c.max_batch, GEMV_MAX_M); ++b) {
         wsf = std::max({wsf, gemv_workspace_floats((int)nq, (int)D, b, GV_ROPE),
                         gemv_workspace_floats((int)D, (int)(H * hd), b, GV_RESID),
+                        gemv_workspace_floats(2 * (int)I, (int)D, b, GV_SILU),
                         gemv_workspace_floats((int)D, (int)I, b, GV_RESID)});
+        if (m->moe_model()) wsf = std::max(wsf, gemv_workspace_floats(m->moe_ep(), (int)D, b, GV_F32));
+        if (Is > 0)
+          wsf = std::max({wsf, gemv_workspace_floats(2 * Is, (int)D, b, GV_SILU),
+                          gemv_workspace_floats((int)D, Is, b, GV_RESID)});
+      }
       if (wsf > 0) TRY(dev_alloc(m, (void**)&m->gemv_part, (size_t)wsf * 4));
     }
     TRY(dev_alloc(m, (void**)&m->ss, (int64_t)std::max<int64_t>(D / 8, 1) * c.max_batch * 4));
@@ -1221,7 +1279,7 @@ extern "C" int axon_step(axon_model* m, int32_t n, const int32_t* h_slots, const
   plan.d_drow = m->d_step + 3 * MB;
   plan.d_dslot = m->d_step + 4 * MB;
   plan.d_dpos = m->d_step + 5 * MB;
-  if (m->bf && nd == n && n <= GEMV_MAX_M && !m->moe_model()) {
+  if (m->bf && nd == n && n <= GEMV_MAX_M) {
     // decode tokens only: the fused weight-streaming decode step, recorded as
     // a graph per (n, buffers); the per-entry arrays are read from d_step
     if (int rc = replay_or_run(m, GraphKey{n, d_tokens, d_logits, d_next_tokens, d_cu_seqlens}, s, "step",

@@ -138,6 +138,11 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
         vc[v_el(a.kv, sl, kvh, pos, i + half)] = (bf16)x2;
       }
     }
+  } else if constexpr (EPI == GV_F32) {
+    for (int it = tid; it < ROWS * M; it += NT) {
+      const int row = it % ROWS, col = it / ROWS, n = n0 + row;
+      if (n < a.N) a.out_f32[(int64_t)col * a.ldo + n] = total(row, col);
+    }
   } else {  // GV_HEAD
     for (int it = tid; it < ROWS * M; it += NT) {
       const int row = it % ROWS, col = it / ROWS, n = n0 + row;
@@ -397,7 +402,12 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
 // several workgroups per CU (the weight stream needs many bytes in flight).
 // Same operands, K splitting (EPI == GV_PART) and epilogues as
 // gemv_fused_kernel.
-template <int RB, int NB, bool NORM, int EPI, int U>
+// GROUPED (mixture-of-experts decode, GemvArgs::g_*): expert e = blockIdx.y
+// owns rows g_off[e] .. g_off[e+1]-1 (a workgroup with none leaves at once)
+// and multiplies W + e * g_wstride; its token column c reads X row
+// g_xrow[g_off[e] + c] (row g_off[e] + c without g_xrow) and writes output
+// row g_off[e] + c.
+template <int RB, int NB, bool NORM, int EPI, int U, bool GROUPED = false>
 __global__ void __launch_bounds__(256) gemv_wide_kernel(GemvArgs a) {
   constexpr int NT = 256, ROWS = 64 * RB, COLS = NB * 16;
   constexpr int XCH = U * NB * 64;  // 16-byte token chunks per stage
@@ -412,7 +422,14 @@ __global__ void __launch_bounds__(256) gemv_wide_kernel(GemvArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = blockIdx.x * ROWS;
-  const int K = a.K, M = a.M;
+  const int K = a.K;
+  int M = a.M, r0 = 0;
+  if constexpr (GROUPED) {
+    r0 = a.g_off[blockIdx.y];
+    M = a.g_off[blockIdx.y + 1] - r0;
+    if (M == 0) return;  // no token chose this expert: leave before any barrier
+    a.W += (int64_t)blockIdx.y * a.g_wstride;
+  }
   const int klen = EPI == GV_PART ? ((K + gridDim.y - 1) / gridDim.y + 31) / 32 * 32 : K;
   const int kb = EPI == GV_PART ? min(K, (int)blockIdx.y * klen) : 0;
   const int nsteps = (min(K, kb + klen) - kb) / 32;  // k-steps of 32 (K is a multiple of 32)
@@ -435,7 +452,9 @@ __global__ void __launch_bounds__(256) gemv_wide_kernel(GemvArgs a) {
   for (int i = 0; i < XPT; ++i) {
     const int q = tid + i * NT, l = q & 63, c = (q >> 6) % NB;
     xu[i] = (q >> 6) / NB;
-    xsrc[i] = a.X + (int64_t)min(c * 16 + (l & 15), M - 1) * K + (l >> 4) * 8;
+    int64_t xr = min(c * 16 + (l & 15), M - 1);
+    if constexpr (GROUPED) xr = a.g_xrow ? a.g_xrow[r0 + xr] : r0 + xr;
+    xsrc[i] = a.X + xr * K + (l >> 4) * 8;
   }
   auto kstep = [&](int j) { return kb + min(j, nsteps - 1) * 32; };  // clamped: every load is unconditional
 
@@ -574,10 +593,19 @@ __global__ void __launch_bounds__(256) gemv_wide_kernel(GemvArgs a) {
       const int row = it % ROWS, col = it / ROWS, n = n0 + row;
       if (n < a.N) a.part[((int64_t)blockIdx.y * M + col) * a.N + n] = total(row, col);
     }
+  } else if constexpr (EPI == GV_F32) {
+    for (int it = tid; it < ROWS * M; it += NT) {
+      const int row = it % ROWS, col = it / ROWS, n = n0 + row;
+      if (n < a.N) a.out_f32[(int64_t)(r0 + col) * a.ldo + n] = total(row, col);
+    }
   } else {
     // the residual and head epilogues overwrite element (row, col) of their
     // scratch only after the same thread has read total(row, col): the tile
     // itself serves as that scratch
+    if constexpr (GROUPED) {
+      a.M = M;
+      a.out_t += (int64_t)r0 * a.ldo;
+    }
     gv_epilogue<ROWS, COLS, NT, EPI>(a, n0, tid, tot, blockIdx.x, gridDim.x, total);
   }
 }
@@ -745,7 +773,22 @@ __global__ void __launch_bounds__(256) embed_ss_kernel(const int32_t* __restrict
 // per workgroup (each token fragment is reused across them) and a shallower
 // pipeline (register pressure).
 GvShape gemv_shape(int N, int K, int M, int epi) {
+  N = std::max(N, 1);
   const int nb = (M + 15) / 16;
+  if (epi == GV_F32) {
+    // float rows (a router's tens of logits): K split over up to 32
+    // workgroups per 64-row block, since one CU alone streams slowly
+    const int blocks = (N + 63) / 64;
+    const int ksplit = std::max(1, std::min(K / 64, (32 + blocks - 1) / blocks));
+    return {64, 4, nb == 2 ? 2 : 4, ksplit, 16, 1};
+  }
+  if (epi == GV_SILU && nb >= 2 && (N + 63) / 64 < 256) {
+    // narrow gate/up (shared experts): K split towards ~512 workgroups;
+    // 32-row epilogue tiles hold 16 gate rows and their 16 up rows
+    const int blocks = (N + 63) / 64;
+    const int ksplit = std::max(2, std::min(12, (512 + blocks / 2) / blocks));
+    return {64, 4, nb == 2 ? 2 : 4, ksplit, 32, 1};
+  }
   if (nb == 1) {
     if (epi == GV_SILU) return {32, 4, 4, 1, 0};
     if (epi == GV_HEAD) return {K <= 2048 ? 32 : 64, 8, 2, 1, 0};
@@ -827,10 +870,11 @@ template <int RB, int U, int NB, bool NORM, int EPI>
 static bool gv_split(const GemvArgs& a, const GvShape& sh, hipStream_t s) {
   auto k1 = gemv_wide_kernel<RB, NB, NORM, GV_PART, U>;
   const bool rows = EPI == GV_RESID && sh.erows == GV_RESID_ROWS;
-  if (!rows && sh.erows != 16) return false;
-  auto k2 = rows ? gemv_split_resid_kernel : gemv_split_epilogue_kernel<16, NB, EPI>;
+  constexpr int ER = EPI == GV_SILU ? 32 : 16;  // the SiLU epilogue pairs 16 gate and 16 up rows
+  if (!rows && sh.erows != ER) return false;
+  auto k2 = rows ? gemv_split_resid_kernel : gemv_split_epilogue_kernel<ER, NB, EPI>;
   const dim3 g1((a.N + 64 * RB - 1) / (64 * RB), sh.ksplit);
-  const dim3 g2 = rows ? dim3((a.N + GV_RESID_ROWS - 1) / GV_RESID_ROWS, a.M) : dim3((a.N + 15) / 16);
+  const dim3 g2 = rows ? dim3((a.N + GV_RESID_ROWS - 1) / GV_RESID_ROWS, a.M) : dim3((a.N + ER - 1) / ER);
   const TimingSlot t = g_timing_slot;
   g_timing_slot = TimingSlot{};
   if (t.start) {
@@ -848,8 +892,14 @@ static bool gv_split_nb(const GemvArgs& a, const GvShape& sh, int nb, hipStream_
   if (!sh.wide || !a.part) return false;
 #define AXON_GVS(R, U_, NB_) \
   if (sh.rows == R && sh.u == U_ && nb == NB_) return gv_split<R / 64, U_, NB_, NORM, EPI>(a, sh, s);
-  AXON_GVS(64, 2, 2) AXON_GVS(64, 4, 3) AXON_GVS(64, 4, 4)
-  AXON_GVS(128, 4, 2) AXON_GVS(128, 4, 3) AXON_GVS(128, 4, 4)
+  if constexpr (EPI == GV_F32) {
+    AXON_GVS(64, 4, 1) AXON_GVS(64, 2, 2) AXON_GVS(64, 4, 3) AXON_GVS(64, 4, 4)
+  } else if constexpr (EPI == GV_SILU) {
+    AXON_GVS(64, 2, 2) AXON_GVS(64, 4, 3) AXON_GVS(64, 4, 4)
+  } else {
+    AXON_GVS(64, 2, 2) AXON_GVS(64, 4, 3) AXON_GVS(64, 4, 4)
+    AXON_GVS(128, 4, 2) AXON_GVS(128, 4, 3) AXON_GVS(128, 4, 4)
+  }
 #undef AXON_GVS
   return false;
 }
@@ -863,6 +913,8 @@ bool launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s) {
   if (sh.ksplit > 1) {
     if (epi == GV_RESID) return !norm && gv_split_nb<GV_RESID, false>(a, sh, nb, s);
     if (epi == GV_ROPE) return norm && gv_split_nb<GV_ROPE, true>(a, sh, nb, s);
+    if (epi == GV_SILU) return norm && gv_split_nb<GV_SILU, true>(a, sh, nb, s);
+    if (epi == GV_F32) return !norm && gv_split_nb<GV_F32, false>(a, sh, nb, s);
     return false;
   }
   switch (epi) {
@@ -870,8 +922,38 @@ bool launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s) {
     case GV_ROPE: return norm && gv_dispatch<GV_ROPE, true>(a, sh, nb, s);
     case GV_RESID: return !norm && gv_dispatch<GV_RESID, false>(a, sh, nb, s);
     case GV_HEAD: return norm ? gv_dispatch<GV_HEAD, true>(a, sh, nb, s) : gv_dispatch<GV_HEAD, false>(a, sh, nb, s);
+    case GV_F32:  // float rows out (router logits): 64-row workgroups
+      if (norm) return false;
+      if (nb == 1) return gvw<1, 4, 1, false, GV_F32>(a, s);
+      if (nb == 2) return gvw<1, 2, 2, false, GV_F32>(a, s);
+      if (nb == 3) return gvw<1, 4, 3, false, GV_F32>(a, s);
+      return gvw<1, 2, 4, false, GV_F32>(a, s);
     default: return false;
   }
+}
+
+template <int NB, int EPI>
+static void grouped_launch(const GemvArgs& a, int n_experts, hipStream_t s) {
+  constexpr int U = NB % 2 ? 4 : 2;  // U * NB a multiple of 4: the token stage splits over 256 threads
+  klaunch(gemv_wide_kernel<1, NB, false, EPI, U, true>, dim3((a.N + 63) / 64, n_experts), dim3(256), 0, s, a);
+}
+
+bool launch_gemv_grouped(const GemvArgs& a, int epi, int n_experts, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0 || n_experts <= 0) return true;
+  if (a.M > 64 || (epi != GV_SILU && epi != GV_F32)) return false;
+  const int nb = (a.M + 15) / 16;
+  if (epi == GV_SILU) {
+    if (nb == 1) grouped_launch<1, GV_SILU>(a, n_experts, s);
+    else if (nb == 2) grouped_launch<2, GV_SILU>(a, n_experts, s);
+    else if (nb == 3) grouped_launch<3, GV_SILU>(a, n_experts, s);
+    else grouped_launch<4, GV_SILU>(a, n_experts, s);
+  } else {
+    if (nb == 1) grouped_launch<1, GV_F32>(a, n_experts, s);
+    else if (nb == 2) grouped_launch<2, GV_F32>(a, n_experts, s);
+    else if (nb == 3) grouped_launch<3, GV_F32>(a, n_experts, s);
+    else grouped_launch<4, GV_F32>(a, n_experts, s);
+  }
+  return true;
 }
 
 void launch_argmax_final(const float* val, const int32_t* idx, int nparts, int M, int32_t* next, int32_t* len,

@@ -136,25 +136,46 @@ __global__ void __launch_bounds__(256) moe_scatter_kernel(const int32_t* __restr
   }
 }
 
-// x[t][:] += sum_j w[t][j] * y[inv[t*k + j]][:], 4 features per thread
+// x[t][:] += sum_j w[t][j] * y[inv[t*k + j]][:], 4 features per thread and
+// 1024 per workgroup.  With xg: also xg[t] = bf16(x[t] * g) and the sum of
+// squares of the workgroup's 1024 new x values in ss_out[blockIdx.x * T + t]
+// (the next layer's normalization, applied by the projection that reads xg).
 __global__ void __launch_bounds__(256) moe_combine_kernel(float* __restrict__ x, const float* __restrict__ y,
                                                           const int32_t* __restrict__ inv,
-                                                          const float* __restrict__ w, int D, int k) {
+                                                          const float* __restrict__ w, int D, int k,
+                                                          const bf16* __restrict__ g, bf16* __restrict__ xg,
+                                                          float* __restrict__ ss_out) {
+  __shared__ float red[16];
   const int t = blockIdx.y;
   const int n = (blockIdx.x * 256 + threadIdx.x) * 4;
-  if (n >= D) return;
-  f32x4 acc = *(const f32x4*)(x + (int64_t)t * D + n);
-  f32x4 s = {0.f, 0.f, 0.f, 0.f};
-  for (int j = 0; j < k; ++j) {
-    const float wj = w[(int64_t)t * k + j];
-    const f32x4 v = *(const f32x4*)(y + (int64_t)inv[(int64_t)t * k + j] * D + n);
-    s[0] += wj * v[0];
-    s[1] += wj * v[1];
-    s[2] += wj * v[2];
-    s[3] += wj * v[3];
+  float sq = 0.f;
+  if (n < D) {
+    f32x4 acc = *(const f32x4*)(x + (int64_t)t * D + n);
+    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < k; ++j) {
+      const float wj = w[(int64_t)t * k + j];
+      const f32x4 v = *(const f32x4*)(y + (int64_t)inv[(int64_t)t * k + j] * D + n);
+      s[0] += wj * v[0];
+      s[1] += wj * v[1];
+      s[2] += wj * v[2];
+      s[3] += wj * v[3];
+    }
+    acc += s;
+    *(f32x4*)(x + (int64_t)t * D + n) = acc;
+    if (xg) {
+      bf16x4 o;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        o[j] = (bf16)(acc[j] * (float)g[n + j]);
+        sq += acc[j] * acc[j];
+      }
+      *(bf16x4*)(xg + (int64_t)t * D + n) = o;
+    }
   }
-  acc += s;
-  *(f32x4*)(x + (int64_t)t * D + n) = acc;
+  if (xg) {  // grid-uniform: every thread of the workgroup reaches the barrier
+    sq = block_sum(sq, red);
+    if (threadIdx.x == 0) ss_out[(int64_t)blockIdx.x * gridDim.y + t] = sq;
+  }
 }
 
 void launch_moe_route(const float* logits, int ldl, int T, int E, int k, int norm, int32_t* topi, float* topw,
@@ -172,9 +193,9 @@ void launch_moe_plan(const int32_t* topi, int T, int E, int k, int32_t* cnt, int
 }
 
 void launch_moe_combine(float* x, const float* y, const int32_t* inv, const float* w, int T, int D, int k,
-                        hipStream_t s) {
+                        hipStream_t s, const bf16* g, bf16* xg, float* ss_out) {
   if (T <= 0) return;
-  moe_combine_kernel<<<dim3((D / 4 + 255) / 256, T), 256, 0, s>>>(x, y, inv, w, D, k);
+  moe_combine_kernel<<<dim3(moe_combine_blocks(D), T), 256, 0, s>>>(x, y, inv, w, D, k, g, xg, ss_out);
 }
 
 }  // namespace axon

@@ -109,7 +109,8 @@ template <typename T>
 void launch_silu_reduce(const float* parts, int nparts, int64_t part_stride, T* a, int M, int I,
                         hipStream_t s);
 // ---- fused decode projections (k_gemv.hip)
-enum GvEpi : int { GV_HEAD = 0, GV_RESID = 1, GV_SILU = 2, GV_ROPE = 3, GV_PART = 4 /* internal: split-K partials */ };
+enum GvEpi : int { GV_HEAD = 0, GV_RESID = 1, GV_SILU = 2, GV_ROPE = 3, GV_PART = 4 /* internal: split-K partials */,
+                   GV_F32 = 5 /* grouped experts: float rows out_f32[row][n] */ };
 
 struct GemvArgs {
   const bf16* W;  // [N][K]
@@ -141,6 +142,13 @@ struct GemvArgs {
   // split K (projections of 17..64 tokens): workspace of ksplit * M * N floats
   // (gemv_workspace_floats), owned by the caller
   float* part;
+  // grouped experts (launch_gemv_grouped): expert e multiplies W + e *
+  // g_wstride with its rows g_off[e] .. g_off[e+1]-1; row r reads X row
+  // g_xrow[r] (row r when g_xrow is NULL) and writes output row r (M is an
+  // upper bound of any expert's rows)
+  const int32_t* g_off;
+  const int32_t* g_xrow;
+  int64_t g_wstride;
 };
 constexpr int GEMV_MAX_M = 64;      // token columns one fused projection handles
 constexpr int GV_RESID_ROWS = 1024;  // features per workgroup of the split-K residual epilogue
@@ -159,6 +167,11 @@ int gemv_rows(int N, int K, int M, int epi);  // output rows per workgroup (ss p
 bool launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s);
 void launch_argmax_final(const float* val, const int32_t* idx, int nparts, int M, int32_t* next, int32_t* len,
                          hipStream_t s);
+// Few-token grouped expert projections (mixture-of-experts decode): a
+// workgroup per (64-row block, expert), the expert's rows (at most a.M <= 64)
+// gathered through g_xrow; GV_SILU (out_t rows, interleaved gate/up W) or
+// GV_F32 (out_f32 rows).  false when a.M > 64.
+bool launch_gemv_grouped(const GemvArgs& a, int epi, int n_experts, hipStream_t s);
 void launch_embed_ss(const int32_t* tok, const bf16* emb, const bf16* g, float* x, bf16* xg, float* ss_out, int M,
                      int D, int V, hipStream_t s);
 
@@ -208,8 +221,11 @@ void launch_moe_route(const float* logits, int ldl, int T, int E, int k, int nor
 // inv [T*k] (grouped row of choice t*k + j)
 void launch_moe_plan(const int32_t* topi, int T, int E, int k, int32_t* cnt, int32_t* off, int32_t* toff,
                      int32_t* xrow, int32_t* inv, hipStream_t s);
-// x[t] += sum_j w[t][j] * y[inv[t*k+j]] (float rows of D, D % 4 == 0)
+// x[t] += sum_j w[t][j] * y[inv[t*k+j]] (float rows of D, D % 4 == 0).  With
+// xg: also xg = bf16(x * g) and per-token sums of squares of the new x in
+// moe_combine_blocks(D) partials, ss_out[part * T + t].
+inline int moe_combine_blocks(int D) { return (D / 4 + 255) / 256; }
 void launch_moe_combine(float* x, const float* y, const int32_t* inv, const float* w, int T, int D, int k,
-                        hipStream_t s);
+                        hipStream_t s, const bf16* g = nullptr, bf16* xg = nullptr, float* ss_out = nullptr);
 
 }  // namespace axon

@@ -10,18 +10,18 @@ near a tie both choices are correct.  The GPU takes it from bf16-stored normed
 activations, as the oracle's bf16-storage mode does, but a bf16 rounding
 boundary can turn an upstream difference of ~1e-9 into one bf16 step of an
 input and move a router probability by ~1e-5, so decisions closer than that
-may go either way.  The tests therefore hold every logits row to the band
-around the exact oracle (which includes such flips), and hold the rows whose
-token has no routing decision within 1e-3 of a tie (most of them) to the
-absolute bf16-storage tolerance.
+may go either way, and a flipped choice moves that token's logits by far more
+than rounding does.  The tests therefore hold the rows whose token has no
+routing decision within 1e-3 of a tie (most of them) to the full bf16 bar
+(the band around the exact oracle and the absolute bf16-storage tolerance),
+and every row, near-ties included, to the band on the mean error.
 """
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from parity_util import (BF16_MAX, BF16_MEAN, check_argmax, check_bf16, check_logits, gpu_model, pack,
-                         run_teacher_forced)
+from parity_util import BAND, check_argmax, check_bf16, gpu_model, pack, run_teacher_forced
 from synthetic import model_weights, prompts, small_shape
 
 pytestmark = pytest.mark.gpu
@@ -75,14 +75,11 @@ def _router_gaps(shape, w64, seqs, forced):
     return out
 
 
-@pytest.mark.parametrize("case", list(CASES))
-def test_moe_prefill_and_decode_against_oracle(case):
+def _against_oracle(case, lens, steps, seed):
     shape = _shape(case)
-    w = model_weights(shape, seed=31)
-    lens = [37, 130, 300, 5]
-    ids = prompts(len(lens), max(lens), shape["vocab_size"], seed=32).numpy()
+    w = model_weights(shape, seed=seed)
+    ids = prompts(len(lens), max(lens), shape["vocab_size"], seed=seed + 1).numpy()
     seqs = [ids[i, :n] for i, n in enumerate(lens)]
-    steps = 4
     w64 = oracle.weights_f64(w)
     ref_tok, ref_lg = oracle.generate_greedy(oracle.OracleDecoder(shape, w64), seqs, steps)
     ref_b = oracle.teacher_forced(oracle.OracleDecoder(shape, w64, io_round="bf16"), seqs, ref_tok[:, :steps])
@@ -93,10 +90,31 @@ def test_moe_prefill_and_decode_against_oracle(case):
     assert clear.mean() >= 0.75
     m = gpu_model(shape, w, max_batch=len(lens), max_seq=max(lens) + steps + 2)
     lg, _ = run_teacher_forced(m, seqs, ref_tok[:, :steps])
-    mx = check_bf16(lg, ref_lg, ref_b, f"moe {case}", absolute=False)
-    check_logits(lg[clear], ref_b[clear], BF16_MAX, BF16_MEAN, f"moe {case}, rows clear of near-ties, vs bf16 storage")
-    check_argmax(lg, ref_lg, mx, f"moe {case}")
+    assert np.all(np.isfinite(lg)), "non-finite logits"
+    err = np.abs(lg - ref_lg).max(axis=-1)
+    print(f"largest error of a row clear of near-ties {err[clear].max():.3e}, of a near-tie row "
+          f"{err[~clear].max() if (~clear).any() else 0.0:.3e}")
+    # every row on average (a flipped near-tie moves a few rows only) ...
+    inherent = np.abs(ref_b - ref_lg)
+    assert np.abs(lg - ref_lg).mean() <= BAND * inherent.mean() + 1e-4
+    # ... and each row clear of near-ties to the full bf16 bar
+    check_bf16(lg[clear], ref_lg[clear], ref_b[clear], f"moe {case}, rows clear of near-ties")
+    check_argmax(lg[clear], ref_lg[clear], float(err[clear].max()), f"moe {case}, rows clear of near-ties")
     m.close()
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_moe_prefill_and_decode_against_oracle(case):
+    _against_oracle(case, [37, 130, 300, 5], steps=4, seed=31)
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_moe_wide_decode_batch_against_oracle(case):
+    """17..64 decode tokens: the few-token projections take their row-splitting
+    form (K split for the narrow router and shared-expert gate/up) and every
+    expert sees several tokens."""
+    rng = np.random.default_rng(41)
+    _against_oracle(case, [int(n) for n in rng.integers(3, 48, size=37)], steps=3, seed=43)
 
 
 def test_moe_chunked_prefill_equals_one_shot_bitwise():
