@@ -449,3 +449,32 @@ def test_moe_model_layers_and_decode_invariants():
     dense = OracleDecoder(dict(shp, n_routed_experts=0), {**w, **{
         k.replace("mlp.shared_experts.", "mlp."): v for k, v in w.items() if ".mlp.shared_experts." in k}})
     assert np.abs(dense.prefill([seq], all_logits=True)[0] - full).max() > 1e-3  # the routed experts contribute
+
+
+def test_moe_of_identical_experts_equals_the_dense_model():
+    """Every routed expert a copy of one SwiGLU MLP, renormalized top-k weights
+    and no shared expert: each token's mixture is that MLP times weights that
+    sum to one, so the MoE model equals the dense model with that MLP (a
+    dropped weight, a wrong expert slice or an unnormalized sum breaks it)."""
+    dense_shp = _tiny("qwen", layers=3)
+    w = _np_weights(dense_shp, seed=5)
+    moe_shp = dict(dense_shp, n_routed_experts=5, num_experts_per_tok=3,
+                   moe_intermediate_size=dense_shp["intermediate_size"], n_shared_experts=0,
+                   first_k_dense_replace=1, norm_topk_prob=True)
+    rng = np.random.default_rng(9)
+    mw = {}
+    for k, v in w.items():
+        if ".mlp." in k and not k.startswith("model.layers.0."):
+            p, name = k.split(".mlp.")
+            for e in range(5):
+                mw[f"{p}.mlp.experts.{e}.{name}"] = v
+            mw[f"{p}.mlp.gate.weight"] = rng.standard_normal((5, dense_shp["hidden_size"]))
+        else:
+            mw[k] = v
+    seq = RNG.integers(0, dense_shp["vocab_size"], 9)
+    ref = OracleDecoder(dense_shp, w).prefill([seq], all_logits=True)[0]
+    got = OracleDecoder(moe_shp, mw).prefill([seq], all_logits=True)[0]
+    np.testing.assert_allclose(got, ref, atol=1e-12)
+    # without renormalization the weights sum to less than one: the models differ
+    un = OracleDecoder(dict(moe_shp, norm_topk_prob=False), mw).prefill([seq], all_logits=True)[0]
+    assert np.abs(un - ref).max() > 1e-4
