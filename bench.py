@@ -379,6 +379,19 @@ def roofline_pass(m, generate, shape, esz, lens):
     for (N, K), b in sorted(shapes.items(), key=lambda kv: -kv[1]["ms"]):
         log(f"decode projection N={N} K={K}: {b['n']} launches, avg {1e3 * b['ms'] / b['n']:.2f} us, "
             f"{b['bytes'] / (b['ms'] / 1e3) / 1e9:.0f} GB/s")
+    # and of the prefill GEMMs: (N, K) -> time, TFLOP/s
+    gshapes = {}
+    for c, (d0, d1, d2), ms in recs:
+        if c != ax.T_GEMM:
+            continue
+        b = gshapes.setdefault((d0, d2), {"ms": 0.0, "n": 0, "flops": 0.0, "rows": 0})
+        b["ms"] += ms
+        b["n"] += 1
+        b["flops"] += 2.0 * d0 * d1 * d2
+        b["rows"] += d1
+    for (N, K), b in sorted(gshapes.items(), key=lambda kv: -kv[1]["ms"]):
+        log(f"prefill GEMM N={N} K={K}: {b['n']} launches, {b['rows'] // b['n']} rows each, "
+            f"{b['ms']:.2f} ms, {b['flops'] / (b['ms'] / 1e3) / 1e12:.0f} TFLOP/s")
     kernels = {}
     for c, a in agg.items():
         hbm = c in (ax.T_GEMV, ax.T_GEMV_GROUPED, ax.T_ATTN_DECODE)

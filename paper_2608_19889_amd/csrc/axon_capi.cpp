@@ -383,16 +383,20 @@ void moe_routed(axon_model* m, const LayerW& w, const bf16* h, int T, hipStream_
     m->timed(4, D, T, Ie, s, [&] { launch_gemv_grouped(da, GV_F32, E, s); });
     return;
   }
+  // the token rows in grouped order, contiguous, in moe_y's memory (free
+  // until the down projection writes it, after gate/up has read them)
+  bf16* xg = (bf16*)m->moe_y;
+  launch_moe_gather(h, m->moe_xrow, T * k, D, xg, s);
   EpiArgs g{};
   g.g_off = m->moe_off;
   g.g_toff = m->moe_toff;
   g.g_E = E;
-  g.g_xrow = m->moe_xrow;
+  g.g_xrow = nullptr;
   g.g_wstride = (int64_t)2 * Ie * D;
   g.out_t = m->moe_a;
   g.ldo = Ie;
   m->timed(1, 2 * Ie, T * k, D, s, [&] {
-    launch_gemm_bf16_grouped((const bf16*)w.wgu_e, h, 2 * Ie, D, T * k, EPI_SILU, g, s);
+    launch_gemm_bf16_grouped((const bf16*)w.wgu_e, xg, 2 * Ie, D, T * k, EPI_SILU, g, s);
   });
   g.g_xrow = nullptr;
   g.g_wstride = (int64_t)D * Ie;

@@ -178,6 +178,20 @@ __global__ void __launch_bounds__(256) moe_combine_kernel(float* __restrict__ x,
   }
 }
 
+// out[row] = h[xrow[row]] (bf16 rows of D, 8 elements per thread)
+__global__ void __launch_bounds__(256) moe_gather_kernel(const bf16* __restrict__ h, const int32_t* __restrict__ xrow,
+                                                         int D, bf16* __restrict__ out) {
+  const int row = blockIdx.y;
+  const int i = (blockIdx.x * 256 + threadIdx.x) * 8;
+  if (i >= D) return;
+  *(bf16x8*)(out + (int64_t)row * D + i) = *(const bf16x8*)(h + (int64_t)xrow[row] * D + i);
+}
+
+void launch_moe_gather(const bf16* h, const int32_t* xrow, int rows, int D, bf16* out, hipStream_t s) {
+  if (rows <= 0) return;
+  moe_gather_kernel<<<dim3((D / 8 + 255) / 256, rows), 256, 0, s>>>(h, xrow, D, out);
+}
+
 void launch_moe_route(const float* logits, int ldl, int T, int E, int k, int norm, int32_t* topi, float* topw,
                       hipStream_t s) {
   if (T <= 0) return;

@@ -221,6 +221,8 @@ void launch_moe_route(const float* logits, int ldl, int T, int E, int k, int nor
 // inv [T*k] (grouped row of choice t*k + j)
 void launch_moe_plan(const int32_t* topi, int T, int E, int k, int32_t* cnt, int32_t* off, int32_t* toff,
                      int32_t* xrow, int32_t* inv, hipStream_t s);
+// out[r] = h[xrow[r]] for r < rows (bf16 rows of D, D % 8 == 0)
+void launch_moe_gather(const bf16* h, const int32_t* xrow, int rows, int D, bf16* out, hipStream_t s);
 // x[t] += sum_j w[t][j] * y[inv[t*k+j]] (float rows of D, D % 4 == 0).  With
 // xg: also xg = bf16(x * g) and per-token sums of squares of the new x in
 // moe_combine_blocks(D) partials, ss_out[part * T + t].
