@@ -69,6 +69,21 @@ def rms_norm(x: np.ndarray, gain: np.ndarray, eps: float) -> np.ndarray:
     return x / np.sqrt(ms + eps) * gain
 
 
+def layer_norm(x: np.ndarray, gain: np.ndarray, bias: np.ndarray, eps: float) -> np.ndarray:
+    """Built-in ``NN.layernorm`` (the GPT-2 definition's ln_1 / ln_2 / ln_f):
+    subtract each row's mean, divide by the root of its (biased) variance
+    plus eps, then scale by the gain and add the bias."""
+    mu = np.mean(x, axis=-1, keepdims=True)
+    var = np.mean((x - mu) ** 2, axis=-1, keepdims=True)
+    return (x - mu) / np.sqrt(var + eps) * gain + bias
+
+
+def gelu_tanh(z: np.ndarray) -> np.ndarray:
+    """``gelu_new`` of the GPT-2 definition: the tanh form of GELU,
+    0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3)))."""
+    return 0.5 * z * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (z + 0.044715 * z ** 3)))
+
+
 def rope_inv_freq(head_dim: int, theta: float) -> np.ndarray:
     i = np.arange(head_dim // 2, dtype=np.float64)
     return theta ** (-2.0 * i / head_dim)
@@ -97,12 +112,14 @@ def softmax(s: np.ndarray) -> np.ndarray:
 
 
 def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
-                         q_pos: np.ndarray) -> np.ndarray:
+                         q_pos: np.ndarray, window: int | None = None) -> np.ndarray:
     """Scaled dot-product attention with a causal mask and grouped KV heads.
 
     q: [Sq, H, HD] at absolute positions ``q_pos``; k, v: [Sk, KV, HD] for
-    positions 0..Sk-1.  Query i sees keys j <= q_pos[i].  Head h reads kv head
-    h // (H / KV).  Returns [Sq, H, HD].
+    positions 0..Sk-1.  Query i sees keys j <= q_pos[i], and with a sliding
+    ``window`` W only the last W of them, j > q_pos[i] - W (the masking
+    built-in's ``window`` argument).  Head h reads kv head h // (H / KV).
+    Returns [Sq, H, HD].
     """
     sq, n_heads, hd = q.shape
     n_kv = k.shape[1]
@@ -110,6 +127,8 @@ def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
     scale = 1.0 / np.sqrt(hd)
     keys = np.arange(k.shape[0])
     masked = keys[None, :] > np.asarray(q_pos)[:, None]
+    if window:
+        masked |= keys[None, :] <= np.asarray(q_pos)[:, None] - window
     out = np.empty_like(q)
     for h in range(n_heads):
         kvh = h // group
@@ -130,6 +149,16 @@ def swiglu_mlp(h: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray, w_down: np.n
     if rnd is not None:
         a = rnd(a)
     return a @ w_down.T
+
+
+def gelu_mlp(h: np.ndarray, w_fc: np.ndarray, b_fc: np.ndarray, w_proj: np.ndarray, b_proj: np.ndarray,
+             rnd=None) -> np.ndarray:
+    """The GPT-2 MLP, ``linear@c_fc |> gelu_new |> linear@c_proj`` with biases;
+    the weights are stored [in, out] (the definition's ``transpose=true``)."""
+    a = gelu_tanh(h @ w_fc + b_fc)
+    if rnd is not None:
+        a = rnd(a)
+    return a @ w_proj + b_proj
 
 
 def moe_mlp(h: np.ndarray, w_router: np.ndarray, experts: list, shared, top_k: int, norm_topk: bool,
@@ -174,6 +203,15 @@ class OracleDecoder:
     and norm_topk_prob (DeepSeek-MoE-style keys); their MoE layers read
     ``mlp.gate.weight`` (the router), ``mlp.experts.{e}.*`` and
     ``mlp.shared_experts.*``.
+
+    ``model_type == "gpt2"`` selects the GPT-2 definition of the Technical
+    Supplement ("A Complete Model Definition"): LayerNorm with bias
+    (layer_norm_epsilon), learned positions added to the token embedding
+    (max_position_embeddings rows), one fused ``c_attn`` projection with bias
+    giving q, k, v, multi-head attention without rotation, ``c_proj`` with
+    bias, the GELU MLP with biases, and the head tied to the token embedding;
+    weights under ``transformer.*`` in the [in, out] layout.  ``sliding_window``
+    (any model) limits each query to its last W keys.
     """
 
     def __init__(self, cfg: dict, weights: dict, io_round: str | None = None):
@@ -183,12 +221,17 @@ class OracleDecoder:
         self.H = cfg["num_attention_heads"]
         self.KV = cfg["num_key_value_heads"]
         self.hd = cfg["head_dim"]
-        self.eps = float(cfg["rms_norm_eps"])
-        self.theta = float(cfg["rope_theta"])
+        self.gpt2 = cfg.get("model_type") == "gpt2"
+        self.eps = float(cfg["layer_norm_epsilon"] if self.gpt2 else cfg["rms_norm_eps"])
+        self.theta = None if self.gpt2 else float(cfg["rope_theta"])
         self.bias = bool(cfg["attention_bias"])
+        self.window = int(cfg.get("sliding_window") or 0) or None
         self.w = {k: _to_f64(v) for k, v in weights.items()}
-        self.lm_head = self.w["model.embed_tokens.weight"] if cfg["tie_word_embeddings"] \
-            else self.w["lm_head.weight"]
+        if self.gpt2:
+            self.lm_head = self.w["transformer.wte.weight"]
+        else:
+            self.lm_head = self.w["model.embed_tokens.weight"] if cfg["tie_word_embeddings"] \
+                else self.w["lm_head.weight"]
         if io_round is None:
             self._r = lambda a: a
             self._rx = lambda a: a
@@ -225,7 +268,7 @@ class OracleDecoder:
         kc = np.concatenate([kc, k], axis=0)
         vc = np.concatenate([vc, v], axis=0)
         cache[i] = (kc, vc)
-        o = self._r(causal_gqa_attention(q, kc, vc, pos)).reshape(s, self.H * self.hd)
+        o = self._r(causal_gqa_attention(q, kc, vc, pos, self.window)).reshape(s, self.H * self.hd)
         x = self._rx(x + o @ w[p + "self_attn.o_proj.weight"].T)
         h2 = self._r(rms_norm(x, w[p + "post_attention_layernorm.weight"], self.eps))
         if self.n_experts and i >= self.first_moe:
@@ -241,16 +284,46 @@ class OracleDecoder:
                              w[p + "mlp.down_proj.weight"], rnd=self._r)
         return self._rx(x + mlp)
 
+    def _layer_gpt2(self, i: int, x: np.ndarray, pos: np.ndarray, cache: list) -> np.ndarray:
+        p = f"transformer.h.{i}."
+        w = self.w
+        s, D = x.shape
+        h = self._r(layer_norm(x, w[p + "ln_1.weight"], w[p + "ln_1.bias"], self.eps))
+        qkv = h @ w[p + "attn.c_attn.weight"] + w[p + "attn.c_attn.bias"]
+        q = self._r(qkv[:, :D].reshape(s, self.H, self.hd))
+        k = self._r(qkv[:, D:2 * D].reshape(s, self.KV, self.hd))
+        v = self._r(qkv[:, 2 * D:].reshape(s, self.KV, self.hd))
+        kc, vc = cache[i]
+        kc = np.concatenate([kc, k], axis=0)
+        vc = np.concatenate([vc, v], axis=0)
+        cache[i] = (kc, vc)
+        o = self._r(causal_gqa_attention(q, kc, vc, pos, self.window)).reshape(s, D)
+        x = self._rx(x + o @ w[p + "attn.c_proj.weight"] + w[p + "attn.c_proj.bias"])
+        h2 = self._r(layer_norm(x, w[p + "ln_2.weight"], w[p + "ln_2.bias"], self.eps))
+        mlp = gelu_mlp(h2, w[p + "mlp.c_fc.weight"], w[p + "mlp.c_fc.bias"], w[p + "mlp.c_proj.weight"],
+                       w[p + "mlp.c_proj.bias"], rnd=self._r)
+        return self._rx(x + mlp)
+
     def _forward_seq(self, b: int, ids: np.ndarray, all_logits: bool) -> np.ndarray:
         cache = self.caches[b]
         past = cache[0][0].shape[0]
         pos = past + np.arange(len(ids))
-        x = self._rx(self.w["model.embed_tokens.weight"][np.asarray(ids, dtype=np.int64)])
-        for i in range(self.L):
-            x = self._layer(i, x, pos, cache)
+        ids = np.asarray(ids, dtype=np.int64)
+        if self.gpt2:
+            assert pos[-1] < self.cfg["max_position_embeddings"], "position past the learned table"
+            x = self._rx(self.w["transformer.wte.weight"][ids] + self.w["transformer.wpe.weight"][pos])
+            for i in range(self.L):
+                x = self._layer_gpt2(i, x, pos, cache)
+        else:
+            x = self._rx(self.w["model.embed_tokens.weight"][ids])
+            for i in range(self.L):
+                x = self._layer(i, x, pos, cache)
         if not all_logits:
             x = x[-1:]
-        hf = self._r(rms_norm(x, self.w["model.norm.weight"], self.eps))
+        if self.gpt2:
+            hf = self._r(layer_norm(x, self.w["transformer.ln_f.weight"], self.w["transformer.ln_f.bias"], self.eps))
+        else:
+            hf = self._r(rms_norm(x, self.w["model.norm.weight"], self.eps))
         return hf @ self.lm_head.T
 
     def _empty_cache(self):

@@ -8,7 +8,7 @@ no checkpoints here: every tensor is drawn from a per-tensor seeded generator.
 Recipe (also stated in the design notes):
   * a tensor named ``name`` uses the seed ``crc32(name) ^ (seed << 32)``;
   * linear, embedding and bias tensors are 0.02 * N(0, 1);
-  * RMSNorm gains are 1 + 0.02 * N(0, 1) (a literal N(0, 0.02) gain would
+  * RMSNorm and LayerNorm gains are 1 + 0.02 * N(0, 1) (a literal N(0, 0.02) gain would
     shrink every activation fifty-fold and make the logits nearly constant);
   * values are drawn in float32 with ``torch.randn`` on the requested device
     and rounded to bfloat16 (round-to-nearest-even) for the bf16 models; that
@@ -52,7 +52,26 @@ MODEL_SHAPES = {
                    rms_norm_eps=1e-6, rope_theta=10000.0, dtype="bf16",
                    n_routed_experts=64, num_experts_per_tok=6, moe_intermediate_size=1408,
                    n_shared_experts=2, first_k_dense_replace=1, norm_topk_prob=False),
+    # the GPT-2 definition of the paper's complete-model listing (LayerNorm,
+    # learned positions, fused c_attn, GELU MLP, biases, tied head), XL size
+    "gpt2xl": dict(model_type="gpt2", hidden_size=1600, num_hidden_layers=48, num_attention_heads=25,
+                   num_key_value_heads=25, head_dim=64, intermediate_size=6400, vocab_size=50257,
+                   max_position_embeddings=1024, tie_word_embeddings=True, attention_bias=True,
+                   layer_norm_epsilon=1e-5, dtype="bf16"),
+    "gpt2": dict(model_type="gpt2", hidden_size=768, num_hidden_layers=12, num_attention_heads=12,
+                 num_key_value_heads=12, head_dim=64, intermediate_size=3072, vocab_size=50257,
+                 max_position_embeddings=1024, tie_word_embeddings=True, attention_bias=True,
+                 layer_norm_epsilon=1e-5, dtype="bf16"),
+    # Mistral-7B-shaped: sliding-window attention over the last 4096 keys
+    "mistral7b": dict(hidden_size=4096, num_hidden_layers=32, num_attention_heads=32,
+                      num_key_value_heads=8, head_dim=128, intermediate_size=14336,
+                      vocab_size=32000, tie_word_embeddings=False, attention_bias=False,
+                      rms_norm_eps=1e-5, rope_theta=10000.0, dtype="bf16", sliding_window=4096),
 }
+
+
+def is_gpt2(shape: dict) -> bool:
+    return shape.get("model_type") == "gpt2"
 
 
 def is_moe_layer(shape: dict, i: int) -> bool:
@@ -96,7 +115,14 @@ def small_shape(base: str, layers: int, vocab: int, intermediate: int | None = N
 
 def weight_names(shape: dict) -> list[str]:
     """Flat, path-keyed weight names (the ``_param("layers.0.self_attn...")``
-    convention of the generated code), HF Llama/Qwen2 layout."""
+    convention of the generated code), HF Llama/Qwen2 layout, or HF GPT-2's."""
+    if is_gpt2(shape):
+        names = ["transformer.wte.weight", "transformer.wpe.weight"]
+        for i in range(shape["num_hidden_layers"]):
+            p = f"transformer.h.{i}."
+            for part in ("ln_1", "attn.c_attn", "attn.c_proj", "ln_2", "mlp.c_fc", "mlp.c_proj"):
+                names += [p + part + ".weight", p + part + ".bias"]
+        return names + ["transformer.ln_f.weight", "transformer.ln_f.bias"]
     names = ["model.embed_tokens.weight"]
     for i in range(shape["num_hidden_layers"]):
         p = f"model.layers.{i}."
@@ -120,9 +146,29 @@ def weight_names(shape: dict) -> list[str]:
     return names
 
 
+def _gpt2_shape(n: str, D: int, I: int, V: int, P: int) -> tuple:
+    # Conv1D weights are stored [in, out]
+    if n == "transformer.wte.weight":
+        return (V, D)
+    if n == "transformer.wpe.weight":
+        return (P, D)
+    part = n.rsplit(".", 2)[-2] if n.endswith(".weight") or n.endswith(".bias") else ""
+    full = n.rsplit(".", 1)[0]
+    ins, outs = {"c_attn": (D, 3 * D), "c_fc": (D, I)}.get(part, (None, None))
+    if full.endswith("mlp.c_proj"):
+        ins, outs = I, D
+    elif full.endswith("attn.c_proj"):
+        ins, outs = D, D
+    if ins is None:  # ln_1, ln_2, ln_f
+        return (D,)
+    return (ins, outs) if n.endswith(".weight") else (outs,)
+
+
 def weight_shapes(shape: dict) -> dict[str, tuple]:
     D, H, KV = shape["hidden_size"], shape["num_attention_heads"], shape["num_key_value_heads"]
     hd, I, V = shape["head_dim"], shape["intermediate_size"], shape["vocab_size"]
+    if is_gpt2(shape):
+        return {n: _gpt2_shape(n, D, I, V, shape["max_position_embeddings"]) for n in weight_names(shape)}
     out = {}
     for n in weight_names(shape):
         if n.endswith("embed_tokens.weight") or n == "lm_head.weight":
@@ -153,6 +199,13 @@ def weight_shapes(shape: dict) -> dict[str, tuple]:
     return out
 
 
+def _is_gain(name: str) -> bool:
+    """Norm gains (1 + 0.02 N): RMSNorm weights and LayerNorm weights (the
+    LayerNorm biases are drawn like any bias)."""
+    return (name.endswith("layernorm.weight") or name == "model.norm.weight"
+            or (".ln_" in name and name.endswith(".weight")))
+
+
 def _seed(name: str, seed: int) -> int:
     return (zlib.crc32(name.encode()) ^ (seed << 32)) & ((1 << 63) - 1)
 
@@ -167,7 +220,7 @@ def model_weights(shape: dict, seed: int = 0, device: str = "cpu") -> dict[str, 
         g.manual_seed(_seed(name, seed))
         w = torch.randn(shp, generator=g, device=device, dtype=torch.float32)
         w.mul_(0.02)
-        if name.endswith("layernorm.weight") or name == "model.norm.weight":
+        if _is_gain(name):
             w.add_(1.0)
         out[name] = w.to(dt)
     return out

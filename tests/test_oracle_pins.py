@@ -478,3 +478,142 @@ def test_moe_of_identical_experts_equals_the_dense_model():
     # without renormalization the weights sum to less than one: the models differ
     un = OracleDecoder(dict(moe_shp, norm_topk_prob=False), mw).prefill([seq], all_logits=True)[0]
     assert np.abs(un - ref).max() > 1e-4
+
+
+# ------------------------------------------------- GPT-2 family and sliding windows
+
+def test_layernorm_closed_forms_and_torch():
+    eps = 1e-5
+    g, b = RNG.standard_normal(6), RNG.standard_normal(6)
+    # a constant row has no deviation: the output is the bias
+    np.testing.assert_allclose(oracle.layer_norm(np.full((2, 6), 3.7), g, b, eps), np.broadcast_to(b, (2, 6)),
+                               atol=1e-12)
+    # mean 0, variance 1: x / sqrt(1 + eps) * g + b
+    x = np.array([[1.0, -1.0, 1.0, -1.0, 1.0, -1.0]])
+    np.testing.assert_allclose(oracle.layer_norm(x, g, b, eps), x / math.sqrt(1 + eps) * g + b, rtol=1e-14)
+    # invariant to shifting a row; torch's layer_norm (biased variance)
+    x = RNG.standard_normal((4, 6)) * 3
+    np.testing.assert_allclose(oracle.layer_norm(x + 5.0, g, b, eps), oracle.layer_norm(x, g, b, eps), atol=1e-12)
+    ref = torch.nn.functional.layer_norm(torch.from_numpy(x), (6,), torch.from_numpy(g), torch.from_numpy(b), eps)
+    np.testing.assert_allclose(oracle.layer_norm(x, g, b, eps), ref.numpy(), atol=1e-13)
+
+
+def test_gelu_tanh_against_torch_and_identities():
+    z = np.linspace(-8, 8, 401)
+    ref = torch.nn.functional.gelu(torch.from_numpy(z), approximate="tanh").numpy()
+    np.testing.assert_allclose(oracle.gelu_tanh(z), ref, atol=1e-14)
+    # gelu(z) - gelu(-z) = z (the tanh form keeps this property of z Phi(z))
+    np.testing.assert_allclose(oracle.gelu_tanh(z) - oracle.gelu_tanh(-z), z, atol=1e-13)
+    # within 1e-3 of the exact z Phi(z)
+    exact = 0.5 * z * (1 + np.vectorize(math.erf)(z / math.sqrt(2)))
+    assert np.max(np.abs(oracle.gelu_tanh(z) - exact)) < 1e-3
+
+
+def _tiny_gpt2(layers=2, **kw):
+    s = dict(model_type="gpt2", hidden_size=48, num_hidden_layers=layers, num_attention_heads=6,
+             num_key_value_heads=6, head_dim=8, intermediate_size=192, vocab_size=97,
+             max_position_embeddings=40, tie_word_embeddings=True, attention_bias=True,
+             layer_norm_epsilon=1e-5, dtype="f32")
+    s.update(kw)
+    return s
+
+
+def test_gpt2_matches_transformers_fp64():
+    """The complete GPT-2 definition against transformers' GPT2LMHeadModel in
+    float64 with the same state dict: logits at every position, then greedy
+    generation through its KV cache."""
+    import transformers
+    shp = _tiny_gpt2(layers=3)
+    w = _np_weights(shp, seed=11)
+    cfg = transformers.GPT2Config(n_embd=48, n_layer=3, n_head=6, n_inner=192, vocab_size=97, n_positions=40,
+                                  activation_function="gelu_new", layer_norm_epsilon=1e-5, resid_pdrop=0.0,
+                                  embd_pdrop=0.0, attn_pdrop=0.0)
+    model = transformers.GPT2LMHeadModel(cfg).to(torch.float64).eval()
+    sd = {k: torch.from_numpy(v) for k, v in w.items()}
+    sd["lm_head.weight"] = sd["transformer.wte.weight"]
+    missing, unexpected = model.load_state_dict(sd, strict=False)
+    assert not unexpected and not missing, (missing, unexpected)
+    ids = RNG.integers(0, 97, (2, 13))
+    with torch.no_grad():
+        ref = model(torch.from_numpy(ids)).logits.numpy()
+    orc = OracleDecoder(shp, w).prefill(list(ids), all_logits=True)
+    for b in range(2):
+        np.testing.assert_allclose(orc[b], ref[b], atol=1e-10, rtol=0)
+    steps = 6
+    toks, _ = generate_greedy(OracleDecoder(shp, w), list(ids), steps)
+    with torch.no_grad():
+        # an explicit mask: generate() otherwise takes every prompt token equal
+        # to pad_token_id for padding and shifts the learned positions
+        out = model.generate(torch.from_numpy(ids), attention_mask=torch.ones(ids.shape, dtype=torch.long),
+                             max_new_tokens=steps + 1, do_sample=False, pad_token_id=0, eos_token_id=None)
+    np.testing.assert_array_equal(toks, out[:, ids.shape[1]:].numpy())
+
+
+def test_gpt2_incremental_decode_and_positions():
+    shp = _tiny_gpt2()
+    w = _np_weights(shp, seed=12)
+    seq = RNG.integers(0, 97, 11)
+    full = OracleDecoder(shp, w).prefill([seq], all_logits=True)[0]
+    m = OracleDecoder(shp, w)
+    m.prefill([seq[:4]])
+    np.testing.assert_allclose(m.extend(0, seq[4:7]), full[4:7], atol=1e-10)
+    np.testing.assert_allclose(np.stack([m.decode([t])[0] for t in seq[7:]]), full[7:], atol=1e-10)
+    # the learned positions matter: the same token at two positions differs
+    a = OracleDecoder(shp, w).prefill([[5, 5]], all_logits=True)[0]
+    assert np.abs(a[0] - a[1]).max() > 1e-3
+    # the table ends at max_position_embeddings
+    with pytest.raises(AssertionError):
+        OracleDecoder(shp, w).prefill([RNG.integers(0, 97, 41)])
+
+
+def test_sliding_window_attention_special_cases():
+    S, H, KV, hd = 9, 4, 2, 8
+    q = RNG.standard_normal((S, H, hd))
+    k = RNG.standard_normal((S, KV, hd))
+    v = RNG.standard_normal((S, KV, hd))
+    pos = np.arange(S)
+    full = oracle.causal_gqa_attention(q, k, v, pos)
+    # a window at least as long as the context changes nothing
+    np.testing.assert_array_equal(oracle.causal_gqa_attention(q, k, v, pos, window=S), full)
+    # a window of one key: each query sees only its own key, so the output is v
+    one = oracle.causal_gqa_attention(q, k, v, pos, window=1)
+    np.testing.assert_allclose(one, np.repeat(v, H // KV, axis=1), atol=1e-14)
+    # brute force for W = 3: keys pos-2 .. pos
+    W = 3
+    got = oracle.causal_gqa_attention(q, k, v, pos, window=W)
+    for i in range(S):
+        keys = np.arange(max(0, i - W + 1), i + 1)
+        for h in range(H):
+            s = q[i, h] @ k[keys, h * KV // H].T / math.sqrt(hd)
+            p = np.exp(s - s.max())
+            np.testing.assert_allclose(got[i, h], (p / p.sum()) @ v[keys, h * KV // H], atol=1e-13)
+
+
+def test_sliding_window_matches_transformers_mistral_fp64():
+    """A Mistral-style model (window shorter than the sequence) against
+    transformers' MistralForCausalLM in float64 with eager attention; decode
+    past the window through the cache equals full recompute."""
+    import transformers
+    shp = dict(_tiny("llama", layers=2), sliding_window=4, tie_word_embeddings=False)
+    w = _np_weights(shp, seed=13)
+    cfg = transformers.MistralConfig(hidden_size=48, num_hidden_layers=2, num_attention_heads=6,
+                                     num_key_value_heads=2, head_dim=8, intermediate_size=48, vocab_size=97,
+                                     rms_norm_eps=shp["rms_norm_eps"], max_position_embeddings=64,
+                                     tie_word_embeddings=False, sliding_window=4,
+                                     rope_parameters={"rope_type": "default", "rope_theta": shp["rope_theta"]},
+                                     attn_implementation="eager")
+    model = transformers.MistralForCausalLM(cfg).to(torch.float64).eval()
+    missing, unexpected = model.load_state_dict({k: torch.from_numpy(v) for k, v in w.items()}, strict=False)
+    assert not unexpected and all("rotary" in m for m in missing), (missing, unexpected)
+    ids = RNG.integers(0, 97, (2, 12))
+    with torch.no_grad():
+        ref = model(torch.from_numpy(ids)).logits.numpy()
+    orc = OracleDecoder(shp, w).prefill(list(ids), all_logits=True)
+    for b in range(2):
+        np.testing.assert_allclose(orc[b], ref[b], atol=1e-6, rtol=0)
+    # the window matters here
+    nowin = OracleDecoder(dict(shp, sliding_window=None), w).prefill(list(ids), all_logits=True)
+    assert np.abs(nowin[0] - orc[0]).max() > 1e-3
+    m = OracleDecoder(shp, w)
+    m.prefill([ids[0, :3]])
+    np.testing.assert_allclose(np.stack([m.decode([t])[0] for t in ids[0, 3:]]), orc[0][3:], atol=1e-10)
