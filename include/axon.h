@@ -50,6 +50,14 @@ enum axon_status {
 };
 
 enum axon_dtype { AXON_BF16 = 1, AXON_F32 = 2 };
+/* Model family.  AXON_ARCH_LLAMA: RMSNorm, rotary positions, SwiGLU MLP
+ * (Llama / Qwen / Mistral / DeepSeek-MoE layouts).  AXON_ARCH_GPT2: the GPT-2
+ * definition of the Technical Supplement ("A Complete Model Definition"):
+ * LayerNorm with bias, learned positions added to the token embedding, one
+ * fused c_attn projection with bias, multi-head attention without rotation,
+ * c_proj with bias, GELU (tanh form) MLP with biases, head tied to the token
+ * embedding. */
+enum axon_arch { AXON_ARCH_LLAMA = 0, AXON_ARCH_GPT2 = 1 };
 
 /* Model definition and capacities.  Field meanings follow the HF config keys
  * that the generated code reads (hidden_size, num_hidden_layers, ...). */
@@ -87,6 +95,16 @@ typedef struct {
   int32_t n_shared_experts; /* >= 0 */
   int32_t first_moe_layer;  /* 0..n_layers: the layers before it keep the dense MLP */
   int32_t norm_topk_prob;   /* 0 or 1 */
+  /* Sliding-window attention (the masking built-in's window; Mistral-style):
+   * a query at position p attends to keys max(0, p - W + 1) .. p.  The cache
+   * still holds every position.  0: full causal attention. */
+  int32_t sliding_window;   /* 0 or >= 1 */
+  /* AXON_ARCH_LLAMA or AXON_ARCH_GPT2.  For GPT-2: n_kv_heads == n_heads,
+   * qkv_bias == 1 and tie_embeddings == 1 (the definition's fixed choices),
+   * rms_eps is the LayerNorm epsilon, rope_theta is ignored, dtype must be
+   * AXON_BF16 and n_experts 0. */
+  int32_t arch;
+  int32_t max_positions;    /* GPT-2: rows of the learned position table; max_seq <= max_positions */
 } axon_config;
 
 /* One entry of the flat weight map.  Names follow the HF Llama/Qwen2 layout:

@@ -24,6 +24,8 @@ AXON_E_OOM = -6
 AXON_E_HIP = -7
 AXON_BF16 = 1
 AXON_F32 = 2
+AXON_ARCH_LLAMA = 0
+AXON_ARCH_GPT2 = 1
 
 STATUS_NAMES = {0: "AXON_OK", -1: "AXON_E_INVALID", -2: "AXON_E_SHAPE", -3: "AXON_E_MISSING",
                 -4: "AXON_E_DTYPE", -5: "AXON_E_CAPACITY", -6: "AXON_E_OOM", -7: "AXON_E_HIP"}
@@ -46,7 +48,8 @@ class AxonConfig(ctypes.Structure):
                 ("max_tokens", ctypes.c_int32), ("kv_page_size", ctypes.c_int32),
                 ("kv_num_pages", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
                 ("moe_intermediate", ctypes.c_int32), ("n_shared_experts", ctypes.c_int32),
-                ("first_moe_layer", ctypes.c_int32), ("norm_topk_prob", ctypes.c_int32)]
+                ("first_moe_layer", ctypes.c_int32), ("norm_topk_prob", ctypes.c_int32),
+                ("sliding_window", ctypes.c_int32), ("arch", ctypes.c_int32), ("max_positions", ctypes.c_int32)]
 
 
 class AxonWeight(ctypes.Structure):
@@ -117,12 +120,16 @@ def _check(rc: int):
 
 def make_config(shape: dict, max_batch: int, max_seq: int, max_tokens: int = 0, page_size: int = 0,
                 num_pages: int = 0) -> AxonConfig:
-    """``shape`` uses HF-style keys (hidden_size, num_hidden_layers, ...)."""
+    """``shape`` uses HF-style keys (hidden_size, num_hidden_layers, ...);
+    ``model_type == "gpt2"`` selects the GPT-2 family (layer_norm_epsilon,
+    max_position_embeddings)."""
+    gpt2 = shape.get("model_type") == "gpt2"
     return AxonConfig(
         hidden=shape["hidden_size"], n_layers=shape["num_hidden_layers"],
         n_heads=shape["num_attention_heads"], n_kv_heads=shape["num_key_value_heads"],
         head_dim=shape["head_dim"], intermediate=shape["intermediate_size"], vocab=shape["vocab_size"],
-        rms_eps=shape["rms_norm_eps"], rope_theta=shape["rope_theta"],
+        rms_eps=shape["layer_norm_epsilon"] if gpt2 else shape["rms_norm_eps"],
+        rope_theta=0.0 if gpt2 else shape["rope_theta"],
         qkv_bias=int(bool(shape["attention_bias"])), tie_embeddings=int(bool(shape["tie_word_embeddings"])),
         dtype=AXON_BF16 if shape["dtype"] == "bf16" else AXON_F32, max_batch=max_batch, max_seq=max_seq,
         max_tokens=max_tokens, kv_page_size=page_size, kv_num_pages=num_pages,
@@ -130,7 +137,9 @@ def make_config(shape: dict, max_batch: int, max_seq: int, max_tokens: int = 0, 
         moe_intermediate=int(shape.get("moe_intermediate_size") or 0),
         n_shared_experts=int(shape.get("n_shared_experts") or 0),
         first_moe_layer=int(shape.get("first_k_dense_replace") or 0),
-        norm_topk_prob=int(bool(shape.get("norm_topk_prob"))))
+        norm_topk_prob=int(bool(shape.get("norm_topk_prob"))),
+        sliding_window=int(shape.get("sliding_window") or 0), arch=AXON_ARCH_GPT2 if gpt2 else AXON_ARCH_LLAMA,
+        max_positions=int(shape.get("max_position_embeddings") or 0) if gpt2 else 0)
 
 
 def make_weights(weights: dict) -> tuple[ctypes.Array, list]:

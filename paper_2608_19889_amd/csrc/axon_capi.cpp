@@ -104,7 +104,10 @@ int validate_config(const axon_config& c) {
   if (c.intermediate <= 0 || c.intermediate % 64) return bad("intermediate must be a positive multiple of 64");
   if (c.vocab <= 0) return bad("vocab must be >= 1");
   if (!(c.rms_eps > 0.f) || !std::isfinite(c.rms_eps)) return bad("rms_eps must be finite and > 0");
-  if (!(c.rope_theta > 1.0) || !std::isfinite(c.rope_theta)) return bad("rope_theta must be finite and > 1");
+  if (c.arch != AXON_ARCH_LLAMA && c.arch != AXON_ARCH_GPT2) return bad("arch must be AXON_ARCH_LLAMA or AXON_ARCH_GPT2");
+  const bool gpt2 = c.arch == AXON_ARCH_GPT2;
+  if (!gpt2 && (!(c.rope_theta > 1.0) || !std::isfinite(c.rope_theta))) return bad("rope_theta must be finite and > 1");
+  if (c.sliding_window < 0) return bad("sliding_window must be >= 0");
   if (c.qkv_bias != 0 && c.qkv_bias != 1) return bad("qkv_bias must be 0 or 1");
   if (c.tie_embeddings != 0 && c.tie_embeddings != 1) return bad("tie_embeddings must be 0 or 1");
   if (c.dtype != AXON_BF16 && c.dtype != AXON_F32) return bad("dtype must be AXON_BF16 or AXON_F32");
@@ -121,6 +124,13 @@ int validate_config(const axon_config& c) {
     if (c.first_moe_layer < 0 || c.first_moe_layer > c.n_layers) return bad("first_moe_layer must be in [0, n_layers]");
     if (c.norm_topk_prob != 0 && c.norm_topk_prob != 1) return bad("norm_topk_prob must be 0 or 1");
     if (c.dtype != AXON_BF16) return bad("mixture-of-experts layers need dtype AXON_BF16");
+  }
+  if (gpt2) {
+    if (c.n_kv_heads != c.n_heads) return bad("GPT-2 attention has n_kv_heads == n_heads");
+    if (c.qkv_bias != 1 || c.tie_embeddings != 1) return bad("GPT-2 has qkv_bias == 1 and tie_embeddings == 1");
+    if (c.dtype != AXON_BF16) return bad("the GPT-2 family needs dtype AXON_BF16");
+    if (c.n_experts != 0) return bad("the GPT-2 family has no mixture-of-experts layers (n_experts 0)");
+    if (c.max_positions < 1 || c.max_seq > c.max_positions) return bad("GPT-2 needs 1 <= max_seq <= max_positions");
   }
   return AXON_OK;
 }
@@ -283,6 +293,7 @@ struct axon_model {
     v.ps = ps;
     v.kv_heads = cfg.n_kv_heads;
     v.hd = cfg.head_dim;
+    v.window = cfg.sliding_window;
     return v;
   }
   bool paged() const { return cfg.kv_page_size > 0; }

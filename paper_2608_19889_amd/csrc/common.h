@@ -66,6 +66,7 @@ struct KVView {
   int ps;             // positions per page
   int kv_heads;
   int hd;
+  int window = 0;     // sliding window W: a query at position p sees keys (p - W, p]; 0 = all
 };
 
 AXON_DEV int64_t kv_page(const KVView& c, int slot, int pos) {

@@ -175,10 +175,13 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
   }
   const float sc = LOG2E / sqrtf((float)HD);
 
+  const int W = kv.window;
   const int kend = base + min(S, q0 + TQ);  // keys needed by the workgroup
   const int ntiles = (kend + PK - 1) / PK;
-  issue(0, 0);
-  for (int kt = 0; kt < ntiles; ++kt) {
+  // with a window, the first tile holding a key of the workgroup's first query
+  const int kt0 = W ? max(0, base + q0 - W + 1) / PK : 0;
+  issue(kt0, kt0 & 1);
+  for (int kt = kt0; kt < ntiles; ++kt) {
     const int j0 = kt * PK, b = kt & 1;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();  // tile kt landed for every wavefront; buffer b^1 is free
@@ -186,6 +189,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
     const bf16x8* ks = lds + b * BUF;
     const bf16* vsb = (const bf16*)(ks + KT);
     if (j0 > base + qw0 + WQ - 1 || qw0 >= S) continue;  // every key of the tile is after this wavefront's queries
+    if (W && j0 + PK - 1 <= base + qw0 - W) continue;    // every key of the tile is before their windows
     // ---- S^T = K Q^T: each K fragment serves the QB query blocks
     f32x16 s[QB][2];
 #pragma unroll
@@ -208,7 +212,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
     //      exceeds it by more than 8 (in log2 units): probabilities stay <= 2^8
     //      and the accumulator is rescaled rarely, not every tile (the sum and
     //      the accumulator always share the reference, so the result is exact).
-    const bool masked = j0 + PK - 1 > base + qw0 || j0 + PK > KL;
+    const bool masked = j0 + PK - 1 > base + qw0 || j0 + PK > KL || (W && j0 + W <= base + qw0 + WQ - 1);
     bf16x8 pb[QB][2][2];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -220,7 +224,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const int key = j0 + r * 32 + (i / 8) * 16 + hl * 8 + ((i / 4) & 1) * 4 + (i % 4);  // kappa of the row
-            const float v = (key <= base + myq && key < KL) ? s[qb][r][i] : -INFINITY;
+            const float v = (key <= base + myq && key < KL && (!W || key > base + myq - W)) ? s[qb][r][i] : -INFINITY;
             s[qb][r][i] = v;
             mloc = fmaxf(mloc, v);
           }
@@ -312,7 +316,10 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
   const int row = rows ? rows[b] : b, slot = slots ? slots[b] : b;
   const int nsplit = gridDim.x;
   const int ctx = len[b] + 1;
-  const int s0 = split * split_len;
+  // keys lo .. ctx-1 (a sliding window keeps the last W); the splits start at
+  // lo rounded down to a 32-key chunk, and keys below lo are masked
+  const int lo = kv.window ? max(0, ctx - kv.window) : 0;
+  const int s0 = (lo & ~31) + split * split_len;
   const int s1 = min(ctx, s0 + split_len);
   if (s0 >= ctx) return;
   const int group = H / kv.kv_heads;
@@ -388,13 +395,13 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int key = j0 + blk * 16 + gq * 4 + i;
-        const float v = key < s1 ? s[blk][i] * sc : -INFINITY;
+        const float v = key < s1 && key >= lo ? s[blk][i] * sc : -INFINITY;
         s[blk][i] = v;
         mloc = fmaxf(mloc, v);
       }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_run, mloc);  // finite: key j0 < s1 is in this step
+    const float m_new = fmaxf(m_run, mloc);  // finite: the first chunk holds a key in [lo, s1)
     const float alpha = exp2f(m_run - m_new);
     m_run = m_new;
     l_run *= alpha;
@@ -486,11 +493,13 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
 template <int HD>
 __global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restrict__ part, bf16* __restrict__ o, int H,
                                                           const int32_t* __restrict__ len, int nsplit,
-                                                          int split_len, const int32_t* __restrict__ rows) {
+                                                          int split_len, const int32_t* __restrict__ rows,
+                                                          int window) {
   const int b = blockIdx.y, h = blockIdx.x, d = threadIdx.x;
   const int row = rows ? rows[b] : b;
   const int ctx = len[b] + 1;
-  const int nact = min(nsplit, (ctx + split_len - 1) / split_len);
+  const int lo = (window ? max(0, ctx - window) : 0) & ~31;  // as the attention kernel's first split
+  const int nact = min(nsplit, (ctx - lo + split_len - 1) / split_len);
   const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
   float M = -INFINITY;
   for (int sp = 0; sp < nact; ++sp) M = fmaxf(M, pp[sp * (HD + 2) + HD]);
@@ -536,7 +545,8 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ 
   const float* kb = (const float*)kv.k;
   const float* vb = (const float*)kv.v;
   float m = -INFINITY, l = 0.f, acc[DL] = {};
-  for (int j0 = 0; j0 <= pos; j0 += 64) {
+  const int lo = kv.window ? max(0, pos - kv.window + 1) : 0;  // keys lo .. pos
+  for (int j0 = lo; j0 <= pos; j0 += 64) {
     // score of key j0 + lane
     const int j = j0 + lane;
     float sj = -INFINITY;
@@ -552,7 +562,7 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ 
       }
       sj = dot * sc;
     }
-    const float m_new = fmaxf(m, wave_max(sj));  // finite: key j0 <= pos
+    const float m_new = fmaxf(m, wave_max(sj));  // finite: key j0 <= pos is valid
     const float alpha = exp2f(m - m_new);
     const float p = j <= pos ? exp2f(sj - m_new) : 0.f;
     l = l * alpha + wave_sum(p);
@@ -631,7 +641,8 @@ static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int B,
   else
     attn_decode_bf16_kernel<HD, NW, false, NBUF>
         <<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len, rows, slots);
-  if (nsplit > 1) attn_combine_kernel<HD><<<dim3(H, B), HD, 0, s>>>(part, o, H, len, nsplit, split_len, rows);
+  if (nsplit > 1)
+    attn_combine_kernel<HD><<<dim3(H, B), HD, 0, s>>>(part, o, H, len, nsplit, split_len, rows, kv.window);
 }
 
 template <typename T>
@@ -643,6 +654,7 @@ void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, 
     if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H, nullptr, nullptr);
     else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H, nullptr, nullptr);
   } else {
+    if (kv.window) max_ctx = std::min(max_ctx, kv.window + 31);  // keys from the window's 32-key chunk
     const int nsplit = plan_decode_splits(B, kv.kv_heads, max_ctx);
     const int split_len = ((max_ctx + nsplit - 1) / nsplit + 63) / 64 * 64;
     if (kv.hd == 64) decode_launch<64, DECODE_WAVES>(q, kv, o, part, B, H, len, nsplit, split_len, s, rows, slots);

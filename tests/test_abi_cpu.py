@@ -38,10 +38,33 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_struct_layout_matches_header():
-    assert ctypes.sizeof(axon.AxonConfig) == 96
+    assert ctypes.sizeof(axon.AxonConfig) == 112
     assert axon.AxonConfig.n_experts.offset == 72 and axon.AxonConfig.norm_topk_prob.offset == 92
+    assert axon.AxonConfig.sliding_window.offset == 96 and axon.AxonConfig.max_positions.offset == 104
     assert axon.AxonConfig.rope_theta.offset == 32
     assert ctypes.sizeof(axon.AxonWeight) == 48
+
+
+def test_struct_layout_matches_the_c_compiler(tmp_path):
+    """Offsets of every axon_config / axon_weight field as gcc lays out the
+    header, against the ctypes mirror."""
+    fields = {"axon_config": [f for f, _ in axon.AxonConfig._fields_],
+              "axon_weight": [f for f, _ in axon.AxonWeight._fields_]}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "axon.h"', "int main(void) {"]
+    for st, names in fields.items():
+        lines.append(f'  printf("{st} size %zu\\n", sizeof({st}));')
+        lines += [f'  printf("{st} {n} %zu\\n", offsetof({st}, {n}));' for n in names]
+    lines.append("  return 0;\n}")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    got = {tuple(line.split()[:2]): int(line.split()[2]) for line in out if line}
+    for st, cls in (("axon_config", axon.AxonConfig), ("axon_weight", axon.AxonWeight)):
+        assert got[(st, "size")] == ctypes.sizeof(cls)
+        for n in fields[st]:
+            assert got[(st, n)] == getattr(cls, n).offset, (st, n)
 
 
 def _shape():
