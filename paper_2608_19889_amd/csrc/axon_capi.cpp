@@ -53,6 +53,29 @@ std::vector<std::pair<std::string, Expected>> expected_weights(const axon_config
   const int64_t D = c.hidden, H = c.n_heads, KV = c.n_kv_heads, hd = c.head_dim, I = c.intermediate,
                 V = c.vocab;
   std::vector<std::pair<std::string, Expected>> w;
+  if (c.arch == AXON_ARCH_GPT2) {
+    // the GPT-2 checkpoint layout: Conv1D weights stored [in, out]
+    w.push_back({"transformer.wte.weight", {2, {V, D}}});
+    w.push_back({"transformer.wpe.weight", {2, {c.max_positions, D}}});
+    for (int i = 0; i < c.n_layers; ++i) {
+      const std::string p = "transformer.h." + std::to_string(i) + ".";
+      w.push_back({p + "ln_1.weight", {1, {D, 0}}});
+      w.push_back({p + "ln_1.bias", {1, {D, 0}}});
+      w.push_back({p + "attn.c_attn.weight", {2, {D, 3 * D}}});
+      w.push_back({p + "attn.c_attn.bias", {1, {3 * D, 0}}});
+      w.push_back({p + "attn.c_proj.weight", {2, {D, D}}});
+      w.push_back({p + "attn.c_proj.bias", {1, {D, 0}}});
+      w.push_back({p + "ln_2.weight", {1, {D, 0}}});
+      w.push_back({p + "ln_2.bias", {1, {D, 0}}});
+      w.push_back({p + "mlp.c_fc.weight", {2, {D, I}}});
+      w.push_back({p + "mlp.c_fc.bias", {1, {I, 0}}});
+      w.push_back({p + "mlp.c_proj.weight", {2, {I, D}}});
+      w.push_back({p + "mlp.c_proj.bias", {1, {D, 0}}});
+    }
+    w.push_back({"transformer.ln_f.weight", {1, {D, 0}}});
+    w.push_back({"transformer.ln_f.bias", {1, {D, 0}}});
+    return w;
+  }
   w.push_back({"model.embed_tokens.weight", {2, {V, D}}});
   for (int i = 0; i < c.n_layers; ++i) {
     const std::string p = "model.layers." + std::to_string(i) + ".";
@@ -131,6 +154,7 @@ int validate_config(const axon_config& c) {
     if (c.dtype != AXON_BF16) return bad("the GPT-2 family needs dtype AXON_BF16");
     if (c.n_experts != 0) return bad("the GPT-2 family has no mixture-of-experts layers (n_experts 0)");
     if (c.max_positions < 1 || c.max_seq > c.max_positions) return bad("GPT-2 needs 1 <= max_seq <= max_positions");
+    if (c.hidden > 8192) return bad("GPT-2 hidden must be <= 8192");
   }
   return AXON_OK;
 }
@@ -147,6 +171,13 @@ struct LayerW {
   // zero), every expert's interleaved gate/up [2 Ie, D] and down [D, Ie]
   // stacked expert after expert; wgu / wd then hold the shared experts (a
   // dense MLP of n_shared * Ie), or are null
+  // GPT-2: LayerNorm biases, O and MLP biases (wgu then holds c_fc [I, D]
+  // and wd c_proj [D, I]; bqkv the c_attn bias)
+  void* gin_b = nullptr;
+  void* gpost_b = nullptr;
+  void* bo = nullptr;
+  void* bfc = nullptr;
+  void* bd = nullptr;
   bool moe = false;
   void* wrouter = nullptr;
   void* wgu_e = nullptr;
@@ -179,6 +210,8 @@ struct axon_model {
   void* embed = nullptr;
   void* lm_head = nullptr;
   void* gfinal = nullptr;
+  void* gfinal_b = nullptr;  // GPT-2: final LayerNorm bias
+  void* wpe = nullptr;       // GPT-2: learned positions [max_positions][D], row-major
   std::vector<LayerW> layers;
   // KV cache
   void* kcache = nullptr;
@@ -225,6 +258,7 @@ struct axon_model {
   void* moe_a = nullptr;        // [rows * k][Ie] bf16 gated expert activations
   float* moe_y = nullptr;       // [rows * k][D] expert outputs
   bool moe_model() const { return cfg.n_experts > 0; }
+  bool gpt2() const { return cfg.arch == AXON_ARCH_GPT2; }
   int moe_ep() const { return (cfg.n_experts + 31) / 32 * 32; }
   int32_t* d_step = nullptr;
   int32_t* h_step = nullptr;  // pinned staging copy
@@ -331,8 +365,9 @@ void release(axon_model* m) {
 // ------------------------------------------------------------------ forward
 template <typename T>
 void gemm_many(axon_model* m, const void* W, const void* X, int N, int M, int K, int epi, float* out_f32,
-               void* out_t, int ldo, hipStream_t s, const EpiArgs* rope = nullptr) {
+               void* out_t, int ldo, hipStream_t s, const EpiArgs* rope = nullptr, const void* bias = nullptr) {
   EpiArgs ep = rope ? *rope : EpiArgs{};
+  if (bias) ep.bias = (const bf16*)bias;
   ep.out_f32 = out_f32;
   ep.out_t = out_t;
   ep.ldo = ldo;
@@ -482,12 +517,19 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
   const int32_t* ent_base = plan ? plan->d_base : nullptr;
   if (plan) launch_set_step_lengths(d_cu, ent_slot, ent_base, m->d_len, B, s);
   else launch_set_lengths(d_cu, m->d_len, B, s);
-  launch_embed_rmsnorm<T>(d_tokens, (const T*)m->embed, (const T*)m->layers[0].gin, m->x, h, Ttok, D, V, eps, s);
+  const bool gpt2 = m->gpt2();  // bf16 only (checked at init)
+  if (gpt2)
+    launch_embed_pos_ln(d_tokens, (const bf16*)m->embed, (const bf16*)m->wpe, (const bf16*)m->layers[0].gin,
+                        (const bf16*)m->layers[0].gin_b, m->x, (bf16*)h, Ttok, D, V, m->cfg.max_positions, eps, d_cu,
+                        B, ent_base, nullptr, s);
+  else
+    launch_embed_rmsnorm<T>(d_tokens, (const T*)m->embed, (const T*)m->layers[0].gin, m->x, h, Ttok, D, V, eps, s);
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const LayerW& w = m->layers[l];
     KVView kv = m->kv(l, m->paged());
     if constexpr (sizeof(T) == 2) {
-      // bias, RoPE and the KV-cache write in the QKV GEMM's epilogue
+      // bias, RoPE (GPT-2: the identity) and the KV-cache write in the QKV
+      // GEMM's epilogue
       EpiArgs re = rope_epi(m, w, kv, d_cu, B, nullptr);
       re.ent_slot = ent_slot;
       re.ent_base = ent_base;
@@ -515,9 +557,15 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
                                ent_base);
       });
     }
-    gemm_many<T>(m, w.wo, m->o, D, Ttok, H * hd, EPI_RESID, m->x, nullptr, D, s);
-    launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, Ttok, D, eps, nullptr, s);
-    if (w.moe) {
+    gemm_many<T>(m, w.wo, m->o, D, Ttok, H * hd, EPI_RESID, m->x, nullptr, D, s, nullptr, w.bo);
+    if (gpt2)
+      launch_layernorm(m->x, (const bf16*)w.gpost, (const bf16*)w.gpost_b, (bf16*)h, Ttok, D, eps, nullptr, s);
+    else
+      launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, Ttok, D, eps, nullptr, s);
+    if (gpt2) {
+      gemm_many<T>(m, w.wgu, h, I, Ttok, D, EPI_GELU, nullptr, m->a, I, s, nullptr, w.bfc);
+      gemm_many<T>(m, w.wd, m->a, D, Ttok, I, EPI_RESID, m->x, nullptr, D, s, nullptr, w.bd);
+    } else if (w.moe) {
       enqueue_moe(m, w, (const bf16*)h, Ttok, s);  // bf16 only (checked at init)
     } else {
       if constexpr (sizeof(T) == 2) {
@@ -530,10 +578,17 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
     }
     const bool last = l + 1 == m->cfg.n_layers;
     const T* gnext = (const T*)(last ? m->gfinal : m->layers[l + 1].gin);
-    if (!last || all_logits)
+    if (gpt2) {
+      const bf16* bnext = (const bf16*)(last ? m->gfinal_b : m->layers[l + 1].gin_b);
+      if (!last || all_logits)
+        launch_layernorm(m->x, (const bf16*)gnext, bnext, (bf16*)h, Ttok, D, eps, nullptr, s);
+      else
+        launch_layernorm(m->x, (const bf16*)gnext, bnext, (bf16*)m->hlast, B, D, eps, d_cu, s);
+    } else if (!last || all_logits) {
       launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, gnext, h, Ttok, D, eps, nullptr, s);
-    else
+    } else {
       launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, gnext, (T*)m->hlast, B, D, eps, d_cu, s);
+    }
   }
   if (all_logits) {
     gemm_many<T>(m, m->lm_head, h, V, Ttok, D, EPI_F32, d_logits, nullptr, V, s);
@@ -689,8 +744,84 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
   if (plan) launch_set_step_lengths(d_cu, plan->d_slot, plan->d_base, m->d_len, B, s);
 }
 
+// Decode step of the GPT-2 family: embedding + learned position + the first
+// LayerNorm, then per layer QKV (bias, identity rotation, KV write) ->
+// attention -> c_proj (+ bias, residual) -> LayerNorm -> c_fc (+ bias, GELU)
+// -> c_proj (+ bias, residual) -> the next LayerNorm; the tied head + argmax.
+// Up to 64 tokens the projections are the fused weight-streaming kernels,
+// else the GEMMs.  plan: as enqueue_decode_bf16.
+void enqueue_decode_gpt2(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
+                         hipStream_t s, const StepPlan* plan = nullptr, const int32_t* d_cu = nullptr) {
+  const int D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V(), nq = m->nqkv();
+  const int32_t* pos = plan ? plan->d_dpos : m->d_len;
+  const int32_t* slot = plan ? plan->d_dslot : nullptr;
+  const float eps = m->cfg.rms_eps;
+  const bool few = B <= GEMV_MAX_M;  // plan implies few
+  bf16* h = (bf16*)m->h;
+  launch_embed_pos_ln(d_tokens, (const bf16*)m->embed, (const bf16*)m->wpe, (const bf16*)m->layers[0].gin,
+                      (const bf16*)m->layers[0].gin_b, m->x, h, B, D, V, m->cfg.max_positions, eps, nullptr, 0,
+                      nullptr, pos, s);
+  // x += X W^T + bias, or a = gelu(X W^T + bias)
+  auto proj = [&](const void* W, const bf16* X, int N, int K, int epi, const void* bias) {
+    if (few) {
+      GemvArgs a{};
+      a.W = (const bf16*)W; a.N = N; a.K = K; a.M = B; a.X = X; a.bias = (const bf16*)bias;
+      a.part = m->gemv_part;
+      if (epi == GV_GELU) { a.out_t = (bf16*)m->a; a.ldo = I; }
+      else { a.out_f32 = m->x; a.ldo = D; }
+      gemv_step(m, a, epi, s);
+    } else if (epi == GV_GELU) {
+      gemm_many<bf16>(m, W, X, N, B, K, EPI_GELU, nullptr, m->a, I, s, nullptr, bias);
+    } else {
+      gemm_many<bf16>(m, W, X, N, B, K, EPI_RESID, m->x, nullptr, D, s, nullptr, bias);
+    }
+  };
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    const LayerW& w = m->layers[l];
+    KVView kv = m->kv(l, m->paged());
+    if (few) {
+      GemvArgs qa{};
+      qa.W = (const bf16*)w.wqkv; qa.N = nq; qa.K = D; qa.M = B; qa.X = h;
+      qa.bias = (const bf16*)w.bqkv; qa.cos_t = m->rope_cos; qa.sin_t = m->rope_sin; qa.q_out = (bf16*)m->q;
+      qa.kv = kv; qa.len = pos; qa.slot = slot; qa.H = H; qa.part = m->gemv_part;
+      gemv_step(m, qa, GV_ROPE, s);
+    } else {
+      const EpiArgs re = rope_epi(m, w, kv, nullptr, 0, pos);
+      gemm_many<bf16>(m, w.wqkv, h, nq, B, D, EPI_ROPE, nullptr, nullptr, nq, s, &re);
+    }
+    int ctx_sum = 0;
+    if (plan) ctx_sum = plan->dctx;
+    else for (int b = 0; b < B; ++b) ctx_sum += m->h_len[b] + 1;
+    m->timed(2, H, B, ctx_sum, s, [&] {
+      launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, B, H, pos, m->cfg.max_seq, s,
+                               nullptr, slot);
+    });
+    proj(w.wo, (const bf16*)m->o, D, H * hd, GV_RESID, w.bo);
+    launch_layernorm(m->x, (const bf16*)w.gpost, (const bf16*)w.gpost_b, h, B, D, eps, nullptr, s);
+    proj(w.wgu, h, I, D, GV_GELU, w.bfc);
+    proj(w.wd, (const bf16*)m->a, D, I, GV_RESID, w.bd);
+    const bool last = l + 1 == m->cfg.n_layers;
+    launch_layernorm(m->x, (const bf16*)(last ? m->gfinal : m->layers[l + 1].gin),
+                     (const bf16*)(last ? m->gfinal_b : m->layers[l + 1].gin_b), h, B, D, eps, nullptr, s);
+  }
+  if (few) {
+    GemvArgs ha{};
+    ha.W = (const bf16*)m->lm_head; ha.N = V; ha.K = D; ha.M = B; ha.X = h;
+    ha.out_f32 = d_logits; ha.ldo = V; ha.am_val = m->am_val; ha.am_idx = m->am_idx;
+    gemv_step(m, ha, GV_HEAD, s);
+    const int hr = gemv_rows(V, D, B, GV_HEAD);
+    launch_argmax_final(m->am_val, m->am_idx, (V + hr - 1) / hr, B, d_next, plan ? nullptr : m->d_len, s);
+  } else {
+    float* dst = d_logits ? d_logits : m->logits_int;
+    gemm_many<bf16>(m, m->lm_head, h, V, B, D, EPI_F32, dst, nullptr, V, s);
+    launch_argmax(dst, B, V, d_next, m->d_len, s);
+  }
+  if (plan) launch_set_step_lengths(d_cu, plan->d_slot, plan->d_base, m->d_len, B, s);
+}
+
 void enqueue_decode(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next, hipStream_t s) {
-  if (m->bf && B <= GEMV_MAX_M) enqueue_decode_bf16(m, B, d_tokens, d_logits, d_next, s);
+  if (m->gpt2()) enqueue_decode_gpt2(m, B, d_tokens, d_logits, d_next, s);
+  else if (m->bf && B <= GEMV_MAX_M) enqueue_decode_bf16(m, B, d_tokens, d_logits, d_next, s);
   else if (m->bf) enqueue_decode_many<bf16>(m, B, d_tokens, d_logits, d_next, s);
   else enqueue_decode_many<float>(m, B, d_tokens, d_logits, d_next, s);
 }
@@ -858,78 +989,135 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     };
   };
 
-  TRY(matrix(&m->embed, V, D, copy_to(get("model.embed_tokens.weight"))));
-  TRY(copy_in(&m->gfinal, get("model.norm.weight")));
-  if (c.tie_embeddings) m->lm_head = m->embed;
-  else TRY(matrix(&m->lm_head, V, D, copy_to(get("lm_head.weight"))));
-  m->layers.resize(c.n_layers);
-  for (int l = 0; l < c.n_layers; ++l) {
-    const std::string p = "model.layers." + std::to_string(l) + ".";
-    LayerW& w = m->layers[l];
-    TRY(copy_in(&w.gin, get(p + "input_layernorm.weight")));
-    TRY(copy_in(&w.gpost, get(p + "post_attention_layernorm.weight")));
-    TRY(matrix(&w.wo, D, H * hd, copy_to(get(p + "self_attn.o_proj.weight"))));
-    w.moe = c.n_experts > 0 && l >= c.first_moe_layer;
-    if (!w.moe) TRY(matrix(&w.wd, D, I, copy_to(get(p + "mlp.down_proj.weight"))));
-    // fused QKV: heads q, then k, then v; within each head, rows in groups of
-    // 8 = 4 first-half rows i and their rotation partners i + hd/2
-    const axon_weight* wq = get(p + "self_attn.q_proj.weight");
-    const axon_weight* wk = get(p + "self_attn.k_proj.weight");
-    const axon_weight* wv = get(p + "self_attn.v_proj.weight");
-    TRY(matrix(&w.wqkv, nq, D, [&](void* dst) -> int {
-      const size_t row = (size_t)D * esz;
-      for (int64_t hh = 0; hh < H + 2 * KV; ++hh) {
-        const axon_weight* src = hh < H ? wq : (hh < H + KV ? wk : wv);
-        const int64_t hs = hh < H ? hh : (hh < H + KV ? hh - H : hh - H - KV);
-        const char* sbase = (const char*)src->data + hs * hd * row;
-        char* dbase = (char*)dst + hh * hd * row;
-        hipError_t e = hipMemcpy2DAsync(dbase, 8 * row, sbase, 4 * row, 4 * row, hd / 8, kind(src), s);
-        if (e == hipSuccess)
-          e = hipMemcpy2DAsync(dbase + 4 * row, 8 * row, sbase + (hd / 2) * row, 4 * row, 4 * row, hd / 8,
-                               kind(src), s);
-        if (e != hipSuccess) return fail(AXON_E_HIP, std::string("QKV repack: ") + hipGetErrorString(e));
+  if (m->gpt2()) {
+    // Conv1D weights arrive [in][out]: copied to a second staging buffer, then
+    // transposed into the first (the fused QKV rows also permuted into the
+    // rotation-pair grouping every QKV kernel expects; GPT-2 rotates by the
+    // identity), then tiled
+    struct Stage2 {
+      void* p = nullptr;
+      ~Stage2() {
+        if (p) (void)hipFree(p);
       }
-      return AXON_OK;
-    }));
-    w.bqkv = nullptr;
-    if (c.qkv_bias) {
-      TRY(dev_alloc(m, &w.bqkv, (size_t)nq * esz));
-      const axon_weight* bq = get(p + "self_attn.q_proj.bias");
-      const axon_weight* bk = get(p + "self_attn.k_proj.bias");
-      const axon_weight* bv = get(p + "self_attn.v_proj.bias");
-      HTRY(hipMemcpyAsync(w.bqkv, bq->data, H * hd * esz, kind(bq), s));
-      HTRY(hipMemcpyAsync((char*)w.bqkv + H * hd * esz, bk->data, KV * hd * esz, kind(bk), s));
-      HTRY(hipMemcpyAsync((char*)w.bqkv + (H + KV) * hd * esz, bv->data, KV * hd * esz, kind(bv), s));
+    } st2;
+    HTRY(hipMalloc(&st2.p, (size_t)std::max(3 * D * D, I * D) * esz));
+    std::vector<int32_t> perm(nq);
+    for (int64_t hh = 0; hh < 3 * H; ++hh)
+      for (int64_t r = 0; r < hd; ++r) {
+        const int64_t g = r / 8, j = r % 8;
+        perm[hh * hd + r] = (int32_t)(hh * hd + (j < 4 ? 4 * g + j : hd / 2 + 4 * g + j - 4));
+      }
+    int32_t* d_perm = nullptr;
+    TRY(dev_alloc(m, (void**)&d_perm, perm.size() * sizeof(int32_t)));
+    HTRY(hipMemcpy(d_perm, perm.data(), perm.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+    auto tposed = [&](const axon_weight* w, int64_t K, int64_t N, const int32_t* pm) {
+      return [&, w, K, N, pm](void* dst) -> int {
+        hipError_t e = hipMemcpyAsync(st2.p, w->data, (size_t)K * N * esz, kind(w), s);
+        if (e == hipSuccess) {
+          launch_transpose_rows((const bf16*)st2.p, (bf16*)dst, (int)K, (int)N, pm, s);
+          e = hipGetLastError();
+        }
+        return e == hipSuccess ? AXON_OK
+                               : fail(AXON_E_HIP, std::string("transpose of '") + w->name + "': " + hipGetErrorString(e));
+      };
+    };
+    TRY(matrix(&m->embed, V, D, copy_to(get("transformer.wte.weight"))));
+    m->lm_head = m->embed;
+    TRY(copy_in(&m->wpe, get("transformer.wpe.weight")));
+    TRY(copy_in(&m->gfinal, get("transformer.ln_f.weight")));
+    TRY(copy_in(&m->gfinal_b, get("transformer.ln_f.bias")));
+    m->layers.resize(c.n_layers);
+    for (int l = 0; l < c.n_layers; ++l) {
+      const std::string p = "transformer.h." + std::to_string(l) + ".";
+      LayerW& w = m->layers[l];
+      TRY(copy_in(&w.gin, get(p + "ln_1.weight")));
+      TRY(copy_in(&w.gin_b, get(p + "ln_1.bias")));
+      TRY(copy_in(&w.gpost, get(p + "ln_2.weight")));
+      TRY(copy_in(&w.gpost_b, get(p + "ln_2.bias")));
+      TRY(matrix(&w.wqkv, nq, D, tposed(get(p + "attn.c_attn.weight"), D, 3 * D, d_perm)));
+      TRY(copy_in(&w.bqkv, get(p + "attn.c_attn.bias")));
+      TRY(matrix(&w.wo, D, D, tposed(get(p + "attn.c_proj.weight"), D, D, nullptr)));
+      TRY(copy_in(&w.bo, get(p + "attn.c_proj.bias")));
+      TRY(matrix(&w.wgu, I, D, tposed(get(p + "mlp.c_fc.weight"), D, I, nullptr)));
+      TRY(copy_in(&w.bfc, get(p + "mlp.c_fc.bias")));
+      TRY(matrix(&w.wd, D, I, tposed(get(p + "mlp.c_proj.weight"), I, D, nullptr)));
+      TRY(copy_in(&w.bd, get(p + "mlp.c_proj.bias")));
     }
-    if (!w.moe) {
-      TRY(matrix(&w.wgu, 2 * I, D, gate_up(get(p + "mlp.gate_proj.weight"), get(p + "mlp.up_proj.weight"), I)));
-      continue;
+    HTRY(hipStreamSynchronize(s));  // the transposes read the second staging buffer
+  } else {
+    TRY(matrix(&m->embed, V, D, copy_to(get("model.embed_tokens.weight"))));
+    TRY(copy_in(&m->gfinal, get("model.norm.weight")));
+    if (c.tie_embeddings) m->lm_head = m->embed;
+    else TRY(matrix(&m->lm_head, V, D, copy_to(get("lm_head.weight"))));
+    m->layers.resize(c.n_layers);
+    for (int l = 0; l < c.n_layers; ++l) {
+      const std::string p = "model.layers." + std::to_string(l) + ".";
+      LayerW& w = m->layers[l];
+      TRY(copy_in(&w.gin, get(p + "input_layernorm.weight")));
+      TRY(copy_in(&w.gpost, get(p + "post_attention_layernorm.weight")));
+      TRY(matrix(&w.wo, D, H * hd, copy_to(get(p + "self_attn.o_proj.weight"))));
+      w.moe = c.n_experts > 0 && l >= c.first_moe_layer;
+      if (!w.moe) TRY(matrix(&w.wd, D, I, copy_to(get(p + "mlp.down_proj.weight"))));
+      // fused QKV: heads q, then k, then v; within each head, rows in groups of
+      // 8 = 4 first-half rows i and their rotation partners i + hd/2
+      const axon_weight* wq = get(p + "self_attn.q_proj.weight");
+      const axon_weight* wk = get(p + "self_attn.k_proj.weight");
+      const axon_weight* wv = get(p + "self_attn.v_proj.weight");
+      TRY(matrix(&w.wqkv, nq, D, [&](void* dst) -> int {
+        const size_t row = (size_t)D * esz;
+        for (int64_t hh = 0; hh < H + 2 * KV; ++hh) {
+          const axon_weight* src = hh < H ? wq : (hh < H + KV ? wk : wv);
+          const int64_t hs = hh < H ? hh : (hh < H + KV ? hh - H : hh - H - KV);
+          const char* sbase = (const char*)src->data + hs * hd * row;
+          char* dbase = (char*)dst + hh * hd * row;
+          hipError_t e = hipMemcpy2DAsync(dbase, 8 * row, sbase, 4 * row, 4 * row, hd / 8, kind(src), s);
+          if (e == hipSuccess)
+            e = hipMemcpy2DAsync(dbase + 4 * row, 8 * row, sbase + (hd / 2) * row, 4 * row, 4 * row, hd / 8,
+                                 kind(src), s);
+          if (e != hipSuccess) return fail(AXON_E_HIP, std::string("QKV repack: ") + hipGetErrorString(e));
+        }
+        return AXON_OK;
+      }));
+      w.bqkv = nullptr;
+      if (c.qkv_bias) {
+        TRY(dev_alloc(m, &w.bqkv, (size_t)nq * esz));
+        const axon_weight* bq = get(p + "self_attn.q_proj.bias");
+        const axon_weight* bk = get(p + "self_attn.k_proj.bias");
+        const axon_weight* bv = get(p + "self_attn.v_proj.bias");
+        HTRY(hipMemcpyAsync(w.bqkv, bq->data, H * hd * esz, kind(bq), s));
+        HTRY(hipMemcpyAsync((char*)w.bqkv + H * hd * esz, bk->data, KV * hd * esz, kind(bk), s));
+        HTRY(hipMemcpyAsync((char*)w.bqkv + (H + KV) * hd * esz, bv->data, KV * hd * esz, kind(bv), s));
+      }
+      if (!w.moe) {
+        TRY(matrix(&w.wgu, 2 * I, D, gate_up(get(p + "mlp.gate_proj.weight"), get(p + "mlp.up_proj.weight"), I)));
+        continue;
+      }
+      // mixture of experts (bf16 only): router rows padded with zeros to a
+      // multiple of 32, experts stacked, shared experts as a dense MLP
+      const int64_t E = c.n_experts, Ep = m->moe_ep(), Ie = c.moe_intermediate;
+      const int64_t Is = (int64_t)c.n_shared_experts * Ie;
+      const axon_weight* wr = get(p + "mlp.gate.weight");
+      TRY(matrix(&w.wrouter, Ep, D, [&](void* dst) -> int {
+        hipError_t e = hipMemcpyAsync(dst, wr->data, (size_t)E * D * esz, kind(wr), s);
+        if (e == hipSuccess && Ep > E) e = hipMemsetAsync((char*)dst + E * D * esz, 0, (size_t)(Ep - E) * D * esz, s);
+        return e == hipSuccess ? AXON_OK : fail(AXON_E_HIP, std::string("router copy: ") + hipGetErrorString(e));
+      }));
+      TRY(dev_alloc(m, &w.wgu_e, (size_t)E * 2 * Ie * D * esz));
+      TRY(dev_alloc(m, &w.wd_e, (size_t)E * D * Ie * esz));
+      for (int64_t e = 0; e < E; ++e) {
+        const std::string q = p + "mlp.experts." + std::to_string(e) + ".";
+        TRY(tile_into((char*)w.wgu_e + e * 2 * Ie * D * esz, 2 * Ie, D,
+                      gate_up(get(q + "gate_proj.weight"), get(q + "up_proj.weight"), Ie)));
+        TRY(tile_into((char*)w.wd_e + e * D * Ie * esz, D, Ie, copy_to(get(q + "down_proj.weight"))));
+      }
+      w.wgu = w.wd = nullptr;
+      if (Is > 0) {
+        TRY(matrix(&w.wgu, 2 * Is, D,
+                   gate_up(get(p + "mlp.shared_experts.gate_proj.weight"), get(p + "mlp.shared_experts.up_proj.weight"), Is)));
+        TRY(matrix(&w.wd, D, Is, copy_to(get(p + "mlp.shared_experts.down_proj.weight"))));
+      }
     }
-    // mixture of experts (bf16 only): router rows padded with zeros to a
-    // multiple of 32, experts stacked, shared experts as a dense MLP
-    const int64_t E = c.n_experts, Ep = m->moe_ep(), Ie = c.moe_intermediate;
-    const int64_t Is = (int64_t)c.n_shared_experts * Ie;
-    const axon_weight* wr = get(p + "mlp.gate.weight");
-    TRY(matrix(&w.wrouter, Ep, D, [&](void* dst) -> int {
-      hipError_t e = hipMemcpyAsync(dst, wr->data, (size_t)E * D * esz, kind(wr), s);
-      if (e == hipSuccess && Ep > E) e = hipMemsetAsync((char*)dst + E * D * esz, 0, (size_t)(Ep - E) * D * esz, s);
-      return e == hipSuccess ? AXON_OK : fail(AXON_E_HIP, std::string("router copy: ") + hipGetErrorString(e));
-    }));
-    TRY(dev_alloc(m, &w.wgu_e, (size_t)E * 2 * Ie * D * esz));
-    TRY(dev_alloc(m, &w.wd_e, (size_t)E * D * Ie * esz));
-    for (int64_t e = 0; e < E; ++e) {
-      const std::string q = p + "mlp.experts." + std::to_string(e) + ".";
-      TRY(tile_into((char*)w.wgu_e + e * 2 * Ie * D * esz, 2 * Ie, D,
-                    gate_up(get(q + "gate_proj.weight"), get(q + "up_proj.weight"), Ie)));
-      TRY(tile_into((char*)w.wd_e + e * D * Ie * esz, D, Ie, copy_to(get(q + "down_proj.weight"))));
-    }
-    w.wgu = w.wd = nullptr;
-    if (Is > 0) {
-      TRY(matrix(&w.wgu, 2 * Is, D,
-                 gate_up(get(p + "mlp.shared_experts.gate_proj.weight"), get(p + "mlp.shared_experts.up_proj.weight"), Is)));
-      TRY(matrix(&w.wd, D, Is, copy_to(get(p + "mlp.shared_experts.down_proj.weight"))));
-    }
-  }
+  }  // Llama-family weights
 
   // ---- KV cache
   if (m->paged()) {
@@ -957,7 +1145,8 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     std::vector<float> cs((size_t)c.max_seq * half), sn((size_t)c.max_seq * half);
     for (int p = 0; p < c.max_seq; ++p)
       for (int i = 0; i < half; ++i) {
-        const double ang = (double)p * std::pow(c.rope_theta, -2.0 * i / (double)hd);
+        // GPT-2 has learned positions instead: the QKV epilogue rotates by 0
+        const double ang = m->gpt2() ? 0.0 : (double)p * std::pow(c.rope_theta, -2.0 * i / (double)hd);
         cs[(size_t)p * half + i] = (float)std::cos(ang);
         sn[(size_t)p * half + i] = (float)std::sin(ang);
       }
@@ -1006,6 +1195,7 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
         wsf = std::max({wsf, gemv_workspace_floats((int)nq, (int)D, b, GV_ROPE),
                         gemv_workspace_floats((int)D, (int)(H * hd), b, GV_RESID),
                         gemv_workspace_floats(2 * (int)I, (int)D, b, GV_SILU),
+                        gemv_workspace_floats((int)I, (int)D, b, GV_GELU),
                         gemv_workspace_floats((int)D, (int)I, b, GV_RESID)});
         if (m->moe_model()) wsf = std::max(wsf, gemv_workspace_floats(m->moe_ep(), (int)D, b, GV_F32));
         if (Is > 0)
@@ -1299,7 +1489,10 @@ extern "C" int axon_step(axon_model* m, int32_t n, const int32_t* h_slots, const
     // a graph per (n, buffers); the per-entry arrays are read from d_step
     if (int rc = replay_or_run(m, GraphKey{n, d_tokens, d_logits, d_next_tokens, d_cu_seqlens}, s, "step",
                                [&](hipStream_t st) {
-                                 enqueue_decode_bf16(m, n, d_tokens, d_logits, d_next_tokens, st, &plan, d_cu_seqlens);
+                                 if (m->gpt2())
+                                   enqueue_decode_gpt2(m, n, d_tokens, d_logits, d_next_tokens, st, &plan, d_cu_seqlens);
+                                 else
+                                   enqueue_decode_bf16(m, n, d_tokens, d_logits, d_next_tokens, st, &plan, d_cu_seqlens);
                                }))
       return rc;
   } else {

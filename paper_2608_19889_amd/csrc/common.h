@@ -17,6 +17,14 @@ template <typename T> AXON_DEV T from_f32(float v);
 template <> AXON_DEV float from_f32<float>(float v) { return v; }
 template <> AXON_DEV bf16 from_f32<bf16>(float v) { return (bf16)v; }  // round to nearest even
 
+// GELU, tanh form (GPT-2's gelu_new): 0.5 z (1 + tanh(u)), u = sqrt(2/pi) (z +
+// 0.044715 z^3), with tanh(u) = 1 - 2 / (e^{2u} + 1) (an overflowing e^{2u}
+// gives 1, an underflowing one -1).
+AXON_DEV float gelu_tanh_f(float z) {
+  const float u = 0.7978845608028654f * (z + 0.044715f * z * z * z);
+  return 0.5f * z * (2.f - 2.f / (__expf(2.f * u) + 1.f));
+}
+
 // Sum over the 64 lanes of a wavefront.
 AXON_DEV float wave_sum(float v) {
 #pragma unroll

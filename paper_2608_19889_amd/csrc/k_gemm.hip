@@ -184,6 +184,16 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
           for (int j = 0; j < 4; ++j) v[j] = (bf16)(silu_f(acc[a][b][g * 4 + j]) * acc[a][b][8 + g * 4 + j]);
           *(bf16x4*)(out + f) = v;
         }
+      } else if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = nb + g * 8 + (lane >> 5) * 4;  // N % 32 == 0: all 4 rows exist
+          const bf16x4 bb = *(const bf16x4*)(ep.bias + n);
+          bf16x4 v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = (bf16)gelu_tanh_f(acc[a][b][g * 4 + j] + (float)bb[j]);
+          *(bf16x4*)((bf16*)ep.out_t + (int64_t)t * ep.ldo + n) = v;
+        }
       } else {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
@@ -191,6 +201,10 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
           if (n >= N) continue;
           float* p = ep.out_f32 + (int64_t)t * ep.ldo + n;
           f32x4 v = {acc[a][b][g * 4 + 0], acc[a][b][g * 4 + 1], acc[a][b][g * 4 + 2], acc[a][b][g * 4 + 3]};
+          if (ep.bias) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] += (float)ep.bias[min(n + j, N - 1)];
+          }
           store_cols<EPI == EPI_RESID>(p, v, N - n);
         }
       }
@@ -401,6 +415,16 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
           for (int j = 0; j < 4; ++j) v[j] = (bf16)(silu_f(acc[a][b][g * 4 + j]) * acc[a][b][8 + g * 4 + j]);
           *(bf16x4*)(out + f) = v;
         }
+      } else if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = nb + g * 8 + (lane >> 5) * 4;  // N % 32 == 0: all 4 rows exist
+          const bf16x4 bb = *(const bf16x4*)(ep.bias + n);
+          bf16x4 v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = (bf16)gelu_tanh_f(acc[a][b][g * 4 + j] + (float)bb[j]);
+          *(bf16x4*)((bf16*)ep.out_t + (int64_t)t * ep.ldo + n) = v;
+        }
       } else {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
@@ -408,6 +432,10 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
           if (n >= N) continue;
           float* p = ep.out_f32 + (int64_t)t * ep.ldo + n;
           f32x4 v = {acc[a][b][g * 4 + 0], acc[a][b][g * 4 + 1], acc[a][b][g * 4 + 2], acc[a][b][g * 4 + 3]};
+          if (ep.bias) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] += (float)ep.bias[min(n + j, N - 1)];
+          }
           store_cols<EPI == EPI_RESID>(p, v, N - n);
         }
       }
@@ -460,6 +488,7 @@ void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi
       case EPI_RESID: launch_256<EPI_RESID>(W, X, N, M, K, ep, s); return;
       case EPI_SILU: launch_256<EPI_SILU>(W, X, N, M, K, ep, s); return;
       case EPI_ROPE: launch_256<EPI_ROPE>(W, X, N, M, K, ep, s); return;
+      case EPI_GELU: launch_256<EPI_GELU>(W, X, N, M, K, ep, s); return;
       default: break;
     }
   }
@@ -469,6 +498,7 @@ void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi
     case EPI_RESID: klaunch(gemm_bf16_kernel<EPI_RESID>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
     case EPI_SILU: klaunch(gemm_bf16_kernel<EPI_SILU>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
     case EPI_ROPE: klaunch(gemm_bf16_kernel<EPI_ROPE>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
+    case EPI_GELU: klaunch(gemm_bf16_kernel<EPI_GELU>, grid, dim3(256), 0, s, W, X, N, M, K, ep); break;
     default: break;
   }
 }

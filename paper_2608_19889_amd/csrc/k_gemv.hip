@@ -15,8 +15,10 @@
 //
 // Epilogues:
 //   GV_HEAD  logits (optional) + per-workgroup (max, first index) per token
-//   GV_RESID x[t][n] += acc; writes bf16(x * g_next) for the next normalized
-//            projection and per-workgroup sums of squares of the new x
+//   GV_RESID x[t][n] += acc (+ bias[n]); writes bf16(x * g_next) for the
+//            next normalized projection and per-workgroup sums of squares of
+//            the new x (unless xg_out is null: GPT-2's LayerNorm is a kernel)
+//   GV_GELU  a[t][n] = bf16(gelu_tanh(acc + bias[n])) (GPT-2 MLP)
 //   GV_SILU  rows come in blocks of 16 gate rows + the 16 matching up rows:
 //            a[t][f] = bf16(silu(gate) * up)
 //   GV_ROPE  rows of the fused QKV projection are permuted so that an 8-row
@@ -80,20 +82,25 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
   auto s_aux = [&](int row, int col) -> float& { return aux[row * (COLS + 1) + col]; };
   if constexpr (EPI == GV_RESID) {
     // features fastest: each token's outputs are contiguous in memory
+    // with a bias (GPT-2) the next normalization is a separate LayerNorm: no
+    // xg / sums of squares (xg_out and ss_out null)
     for (int it = tid; it < ROWS * M; it += NT) {
       const int row = it % ROWS, col = it / ROWS, n = n0 + row;
       float sq = 0.f;
       if (n < a.N) {
         float* p = a.out_f32 + (int64_t)col * a.ldo + n;
-        const float v = (PRE ? pre.x : *p) + total(row, col);
+        float v = (PRE ? pre.x : *p) + total(row, col);
+        if (a.bias) v += (float)a.bias[n];
         *p = v;
         sq = v * v;
-        a.xg_out[(int64_t)col * a.ldo + n] = (bf16)(v * (PRE ? bf16_bits(pre.g) : (float)a.gain_next[n]));
+        if (a.xg_out)
+          a.xg_out[(int64_t)col * a.ldo + n] = (bf16)(v * (PRE ? bf16_bits(pre.g) : (float)a.gain_next[n]));
       }
       s_aux(row, col) = sq;
     }
     __syncthreads();
-    if (tid < M) a.ss_out[(int64_t)wg * M + tid] = ordered_sum(ROWS, [&](int row) { return s_aux(row, tid); });
+    if (tid < M && a.ss_out)
+      a.ss_out[(int64_t)wg * M + tid] = ordered_sum(ROWS, [&](int row) { return s_aux(row, tid); });
   } else if constexpr (EPI == GV_SILU) {
     // each 32-row block: rows 0..15 gate, 16..31 the matching up rows
     for (int it = tid; it < (ROWS / 2) * M; it += NT) {
@@ -102,6 +109,11 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
       if (n0 + blk * 32 >= a.N) continue;  // N is a multiple of 32 (16 gate + 16 up rows)
       const float g = total(blk * 32 + f, col), u = total(blk * 32 + 16 + f, col);
       a.out_t[(int64_t)col * a.ldo + n0 / 2 + fl] = (bf16)(silu_g(g) * u);
+    }
+  } else if constexpr (EPI == GV_GELU) {
+    for (int it = tid; it < ROWS * M; it += NT) {
+      const int row = it % ROWS, col = it / ROWS, n = n0 + row;
+      if (n < a.N) a.out_t[(int64_t)col * a.ldo + n] = (bf16)gelu_tanh_f(total(row, col) + (float)a.bias[n]);
     }
   } else if constexpr (EPI == GV_ROPE) {
     // an 8-row group of a head = first halves i = 4g..4g+3 and their partners
@@ -276,7 +288,7 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
       const int it = min(tid, ROWS * M - 1);
       const int n = min(n0 + it % ROWS, a.N - 1), col = it / ROWS;
       pre.x = a.out_f32[(int64_t)col * a.ldo + n];
-      pre.g = *(const unsigned short*)(a.gain_next + n);
+      pre.g = a.gain_next ? *(const unsigned short*)(a.gain_next + n) : 0u;
     } else if constexpr (PRE && EPI == GV_ROPE) {
       const int it = min(tid, (ROWS / 2) * M - 1);
       const int pr = it % (ROWS / 2), t = it / (ROWS / 2);
@@ -679,17 +691,23 @@ __global__ void __launch_bounds__(256) gemv_split_resid_kernel(GemvArgs a, int n
   }
   float* xp = a.out_f32 + (int64_t)t * a.ldo + n;
   const float4 x0 = *(const float4*)xp;
-  const bf16x4 g = *(const bf16x4*)(a.gain_next + n);
-  const float4 x = {x0.x + s.x, x0.y + s.y, x0.z + s.z, x0.w + s.w};
+  float4 x = {x0.x + s.x, x0.y + s.y, x0.z + s.z, x0.w + s.w};
+  if (a.bias) {
+    const bf16x4 bb = *(const bf16x4*)(a.bias + n);
+    x.x += (float)bb[0]; x.y += (float)bb[1]; x.z += (float)bb[2]; x.w += (float)bb[3];
+  }
   float sq = 0.f;
   if (own) {
     *(float4*)xp = x;
-    bf16x4 o;
-    o[0] = (bf16)(x.x * (float)g[0]);
-    o[1] = (bf16)(x.y * (float)g[1]);
-    o[2] = (bf16)(x.z * (float)g[2]);
-    o[3] = (bf16)(x.w * (float)g[3]);
-    *(bf16x4*)(a.xg_out + (int64_t)t * a.ldo + n) = o;
+    if (a.xg_out) {
+      const bf16x4 g = *(const bf16x4*)(a.gain_next + n);
+      bf16x4 o;
+      o[0] = (bf16)(x.x * (float)g[0]);
+      o[1] = (bf16)(x.y * (float)g[1]);
+      o[2] = (bf16)(x.z * (float)g[2]);
+      o[3] = (bf16)(x.w * (float)g[3]);
+      *(bf16x4*)(a.xg_out + (int64_t)t * a.ldo + n) = o;
+    }
     sq = x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
   }
 #pragma unroll
@@ -697,7 +715,7 @@ __global__ void __launch_bounds__(256) gemv_split_resid_kernel(GemvArgs a, int n
   __shared__ float s_w[4];
   if ((tid & 63) == 0) s_w[tid >> 6] = sq;
   __syncthreads();
-  if (tid == 0) a.ss_out[(int64_t)blockIdx.x * M + t] = (s_w[0] + s_w[1]) + (s_w[2] + s_w[3]);
+  if (tid == 0 && a.ss_out) a.ss_out[(int64_t)blockIdx.x * M + t] = (s_w[0] + s_w[1]) + (s_w[2] + s_w[3]);
 }
 
 // next[t] = index of the largest partial maximum (lowest index on ties);
@@ -782,15 +800,16 @@ GvShape gemv_shape(int N, int K, int M, int epi) {
     const int ksplit = std::max(1, std::min(K / 64, (32 + blocks - 1) / blocks));
     return {64, 4, nb == 2 ? 2 : 4, ksplit, 16, 1};
   }
-  if (epi == GV_SILU && nb >= 2 && (N + 63) / 64 < 256) {
-    // narrow gate/up (shared experts): K split towards ~512 workgroups;
-    // 32-row epilogue tiles hold 16 gate rows and their 16 up rows
+  if ((epi == GV_SILU || epi == GV_GELU) && nb >= 2 && (N + 63) / 64 < 256) {
+    // narrow gate/up (shared experts) or GELU up projection: K split towards
+    // ~512 workgroups; 32-row SiLU epilogue tiles hold 16 gate rows and their
+    // 16 up rows
     const int blocks = (N + 63) / 64;
     const int ksplit = std::max(2, std::min(12, (512 + blocks / 2) / blocks));
-    return {64, 4, nb == 2 ? 2 : 4, ksplit, 32, 1};
+    return {64, 4, nb == 2 ? 2 : 4, ksplit, epi == GV_SILU ? 32 : 16, 1};
   }
   if (nb == 1) {
-    if (epi == GV_SILU) return {32, 4, 4, 1, 0};
+    if (epi == GV_SILU || epi == GV_GELU) return {32, 4, 4, 1, 0};
     if (epi == GV_HEAD) return {K <= 2048 ? 32 : 64, 8, 2, 1, 0};
     if (N / 16 < 192) return {8, 16, 2, 1, 0};
     return K >= 8192 ? GvShape{16, 8, 4, 1, 0} : GvShape{16, 16, 2, 1, 0};
@@ -814,7 +833,7 @@ GvShape gemv_shape(int N, int K, int M, int epi) {
     const int ksplit = std::max(2, std::min(12, (target + blocks / 2) / blocks));
     return {64 * rb, 4, rb == 2 || nb >= 3 ? 4 : 2, ksplit, erows, 1};
   }
-  if (epi == GV_SILU) {
+  if (epi == GV_SILU || epi == GV_GELU) {
     if (nb == 2) return {128, 4, 2, 1, 0, 1};
     return {64, 4, nb == 3 ? 4 : 2, 1, 0, 1};
   }
@@ -851,7 +870,7 @@ static bool gv_dispatch(const GemvArgs& a, const GvShape& sh, int nb, hipStream_
   if (!sh.wide && sh.rows == R && sh.ks == KS_ && sh.u == U_ && nb == NB_) return gv<R, KS_, U_, NB_, NORM, EPI>(a, s);
 #define AXON_GVW(R, U_, NB_) \
   if (sh.wide && sh.rows == R && sh.u == U_ && nb == NB_) return gvw<R / 64, U_, NB_, NORM, EPI>(a, s);
-  if constexpr (EPI == GV_SILU) {
+  if constexpr (EPI == GV_SILU || EPI == GV_GELU) {
     AXON_GV(32, 4, 4, 1) AXON_GVW(128, 2, 2) AXON_GVW(64, 4, 3) AXON_GVW(64, 2, 4)
   } else if constexpr (EPI == GV_HEAD) {
     AXON_GV(32, 8, 2, 1) AXON_GV(64, 8, 2, 1) AXON_GVW(128, 4, 2) AXON_GVW(128, 4, 3) AXON_GVW(128, 2, 4)
@@ -894,7 +913,7 @@ static bool gv_split_nb(const GemvArgs& a, const GvShape& sh, int nb, hipStream_
   if (sh.rows == R && sh.u == U_ && nb == NB_) return gv_split<R / 64, U_, NB_, NORM, EPI>(a, sh, s);
   if constexpr (EPI == GV_F32) {
     AXON_GVS(64, 4, 1) AXON_GVS(64, 2, 2) AXON_GVS(64, 4, 3) AXON_GVS(64, 4, 4)
-  } else if constexpr (EPI == GV_SILU) {
+  } else if constexpr (EPI == GV_SILU || EPI == GV_GELU) {
     AXON_GVS(64, 2, 2) AXON_GVS(64, 4, 3) AXON_GVS(64, 4, 4)
   } else {
     AXON_GVS(64, 2, 2) AXON_GVS(64, 4, 3) AXON_GVS(64, 4, 4)
@@ -912,14 +931,16 @@ bool launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s) {
   const bool norm = a.ss_in != nullptr;
   if (sh.ksplit > 1) {
     if (epi == GV_RESID) return !norm && gv_split_nb<GV_RESID, false>(a, sh, nb, s);
-    if (epi == GV_ROPE) return norm && gv_split_nb<GV_ROPE, true>(a, sh, nb, s);
+    if (epi == GV_ROPE) return norm ? gv_split_nb<GV_ROPE, true>(a, sh, nb, s) : gv_split_nb<GV_ROPE, false>(a, sh, nb, s);
     if (epi == GV_SILU) return norm && gv_split_nb<GV_SILU, true>(a, sh, nb, s);
+    if (epi == GV_GELU) return !norm && a.bias && gv_split_nb<GV_GELU, false>(a, sh, nb, s);
     if (epi == GV_F32) return !norm && gv_split_nb<GV_F32, false>(a, sh, nb, s);
     return false;
   }
   switch (epi) {
     case GV_SILU: return norm && gv_dispatch<GV_SILU, true>(a, sh, nb, s);
-    case GV_ROPE: return norm && gv_dispatch<GV_ROPE, true>(a, sh, nb, s);
+    case GV_ROPE: return norm ? gv_dispatch<GV_ROPE, true>(a, sh, nb, s) : gv_dispatch<GV_ROPE, false>(a, sh, nb, s);
+    case GV_GELU: return !norm && a.bias && gv_dispatch<GV_GELU, false>(a, sh, nb, s);
     case GV_RESID: return !norm && gv_dispatch<GV_RESID, false>(a, sh, nb, s);
     case GV_HEAD: return norm ? gv_dispatch<GV_HEAD, true>(a, sh, nb, s) : gv_dispatch<GV_HEAD, false>(a, sh, nb, s);
     case GV_F32:  // float rows out (router logits): 64-row workgroups

@@ -35,10 +35,12 @@ enum Epi : int {
   EPI_SILU = 2,   // W rows interleaved in blocks of 16 gate rows then 16 up rows;
                   // out_t[t * ldo + f] = silu(gate_f) * up_f
   EPI_PART = 3,   // (reserved)
-  EPI_ROPE = 4    // bf16 fused QKV projection (rows in the rotation-pair order of
+  EPI_ROPE = 4,   // bf16 fused QKV projection (rows in the rotation-pair order of
                   // the decode projections): bias + rotary embedding, then q ->
                   // q_out, k -> K pages, v -> transposed V pages
+  EPI_GELU = 5    // out_t[t * ldo + n] = gelu_tanh(acc + bias[n])  (GPT-2 MLP, bf16)
 };
+// EPI_F32 / EPI_RESID add EpiArgs::bias[n] to acc when it is set.
 
 struct EpiArgs {
   float* out_f32;
@@ -70,6 +72,22 @@ struct EpiArgs {
   int64_t g_wstride;
   int g_E;
 };
+
+// ---- GPT-2 rows (k_layernorm.hip).  Token t is at position len[t] (decode)
+// or, with len null, ent_base[e] + t - cu[e] of its entry e (0-based when
+// ent_base is null).
+// x[t] = wte[tok[t]] + wpe[pos] (float; wte fragment-tiled, wpe row-major
+// [P][D]); h[t] = LayerNorm(x[t]) * g + beta (bf16)
+void launch_embed_pos_ln(const int32_t* tok, const bf16* wte, const bf16* wpe, const bf16* g, const bf16* beta,
+                         float* x, bf16* h, int T, int D, int V, int P, float eps, const int32_t* cu, int nseq,
+                         const int32_t* ent_base, const int32_t* len, hipStream_t s);
+// h[i] = LayerNorm(x[r]) * g + beta with r = i, or r = cu_last[i+1]-1 (the
+// last position of sequence i) when cu_last is set
+void launch_layernorm(const float* x, const bf16* g, const bf16* beta, bf16* h, int rows, int D, float eps,
+                      const int32_t* cu_last, hipStream_t s);
+// dst[r][k] = src[k][perm ? perm[r] : r] (bf16): a [K][N] matrix stored
+// [in][out] transposed to [N][K], rows optionally permuted
+void launch_transpose_rows(const bf16* src, bf16* dst, int K, int N, const int32_t* perm, hipStream_t s);
 
 // ---- weight layout (k_layout.hip): fragment-tiled copy of row-major bf16
 // W [N][K] (K % 32 == 0) into dst of round_up(N, 16) * K elements
@@ -110,7 +128,8 @@ void launch_silu_reduce(const float* parts, int nparts, int64_t part_stride, T* 
                         hipStream_t s);
 // ---- fused decode projections (k_gemv.hip)
 enum GvEpi : int { GV_HEAD = 0, GV_RESID = 1, GV_SILU = 2, GV_ROPE = 3, GV_PART = 4 /* internal: split-K partials */,
-                   GV_F32 = 5 /* grouped experts: float rows out_f32[row][n] */ };
+                   GV_F32 = 5 /* grouped experts: float rows out_f32[row][n] */,
+                   GV_GELU = 6 /* out_t[t][n] = bf16(gelu_tanh(acc + bias[n])) */ };
 
 struct GemvArgs {
   const bf16* W;  // [N][K]
@@ -125,13 +144,14 @@ struct GemvArgs {
   float* out_f32;  // GV_HEAD logits [M][ldo] (may be null) / GV_RESID x [M][ldo]
   int ldo;
   bf16* out_t;     // GV_SILU a [M][ldo]
-  float* ss_out;   // GV_RESID: [N / gemv_rows][M]
-  bf16* xg_out;    // GV_RESID: bf16(x * gain_next) [M][ldo]
+  float* ss_out;   // GV_RESID: [N / gemv_rows][M], or null
+  bf16* xg_out;    // GV_RESID: bf16(x * gain_next) [M][ldo], or null (then ss_out too)
   const bf16* gain_next;
   float* am_val;   // GV_HEAD: [M][N / gemv_rows] partial maxima
   int32_t* am_idx;
-  // GV_ROPE
-  const bf16* bias;  // [(H+2KV)hd] in the original (unpermuted) order, or null
+  // GV_ROPE: [(H+2KV)hd] in the original (unpermuted) order; GV_RESID /
+  // GV_GELU: [N] added to acc; or null
+  const bf16* bias;
   const float* cos_t;
   const float* sin_t;
   bf16* q_out;  // [M][H][hd]

@@ -233,3 +233,43 @@ def test_moe_weight_map_is_checked():
     dense_names["model.layers.1.mlp.gate_proj.weight"] = torch.empty((128, 128), dtype=torch.bfloat16)
     rc, msg = _status(s, dense_names)
     assert rc == axon.AXON_E_MISSING and "unknown" in msg and "layers.1.mlp.gate_proj" in msg
+
+
+def _gpt2_shape(**kw):
+    s = dict(model_type="gpt2", hidden_size=128, num_hidden_layers=2, num_attention_heads=2, num_key_value_heads=2,
+             head_dim=64, intermediate_size=512, vocab_size=256, max_position_embeddings=64,
+             tie_word_embeddings=True, attention_bias=True, layer_norm_epsilon=1e-5, dtype="bf16")
+    s.update(kw)
+    return s
+
+
+@pytest.mark.parametrize("field,value,fragment", [
+    ("n_kv_heads", 1, "n_kv_heads == n_heads"), ("qkv_bias", 0, "qkv_bias == 1"),
+    ("tie_embeddings", 0, "tie_embeddings == 1"), ("dtype", 2, "AXON_BF16"), ("max_positions", 32, "max_positions"),
+    ("arch", 5, "arch"), ("sliding_window", -1, "sliding_window")])
+def test_bad_gpt2_config_is_rejected(field, value, fragment):
+    s = _gpt2_shape()
+    rc, msg = _status(s, _fake_weights(s), override={field: value})
+    assert rc == axon.AXON_E_INVALID and fragment in msg, (rc, msg)
+
+
+def test_gpt2_weight_map_is_checked():
+    s = _gpt2_shape()
+    w = _fake_weights(s)
+    assert w["transformer.h.1.attn.c_attn.weight"].shape == (128, 384)  # Conv1D [in, out]
+    missing = dict(w)
+    del missing["transformer.h.1.mlp.c_fc.bias"]
+    rc, msg = _status(s, missing)
+    assert rc == axon.AXON_E_MISSING and "mlp.c_fc.bias" in msg
+    bad = dict(w)
+    bad["transformer.h.0.attn.c_attn.weight"] = torch.empty((384, 128), dtype=torch.bfloat16)  # [out, in]
+    rc, msg = _status(s, bad)
+    assert rc == axon.AXON_E_SHAPE and "c_attn.weight" in msg and "[128, 384]" in msg, msg
+    extra = dict(w)
+    extra["lm_head.weight"] = torch.empty((256, 128), dtype=torch.bfloat16)  # the head is tied
+    rc, msg = _status(s, extra)
+    assert rc == axon.AXON_E_MISSING and "lm_head.weight" in msg
+    llama_names = dict(w)
+    llama_names["model.norm.weight"] = torch.empty(128, dtype=torch.bfloat16)
+    rc, msg = _status(s, llama_names)
+    assert rc == axon.AXON_E_MISSING and "unknown" in msg
