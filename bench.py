@@ -49,7 +49,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="1b", choices=["1b", "7b", "135m", "7b_paged", "32b", "7b_serve", "moe16b"])
+    ap.add_argument("--workload", default="1b", choices=["1b", "7b", "135m", "7b_paged", "32b", "7b_serve", "moe16b",
+                                                         "gpt2xl", "mistral7b"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=None,
@@ -171,7 +172,10 @@ def main():
     # every step of a static generate; the decode-only steps of a served run
     dsteps = [[n + s for n in lens] for s in range(steps)] if serve_plan is None else \
         [[lens[b] + start for b, start, c in st] for st in serve_plan if all(c == 0 for _, _, c in st)]
-    kv_read = sum(2 * L * KV * hd * (pos + 1) * esz for st in dsteps for pos in st)
+    # keys a query at position pos attends to (a sliding window keeps the last W)
+    W = shape.get("sliding_window") or 0
+    keys = (lambda pos: min(pos + 1, W)) if W else (lambda pos: pos + 1)  # noqa: E731
+    kv_read = sum(2 * L * KV * hd * keys(pos) * esz for st in dsteps for pos in st)
     dtok = sum(len(st) for st in dsteps)
     kv_write = dtok * 2 * L * KV * hd * esz
     # a mixture-of-experts step reads the experts its tokens choose: counted as
@@ -182,8 +186,11 @@ def main():
         n_moe = L - shape.get("first_k_dense_replace", 0)
         moe_b = n_moe * E * 3 * D * Ie * esz
         moe_frac = lambda n: 1.0 - (1.0 - k / E) ** n  # noqa: E731
+    # GPT-2's learned-position table: only the step's rows are read
+    wpe = shape.get("max_position_embeddings", 0) * D * esz if shape.get("model_type") == "gpt2" else 0
+    rows_per_token = 2 if wpe else 1  # embedding rows gathered per token (token, and position)
     decode_bytes = sum(wb - moe_b + moe_b * moe_frac(len(st)) - (0 if shape["tie_word_embeddings"] else emb)
-                       + len(st) * D * esz for st in dsteps) + kv_read + kv_write
+                       - wpe + rows_per_token * len(st) * D * esz for st in dsteps) + kv_read + kv_write
     decode_gbs = decode_bytes / (decode_ms / 1e3) / 1e9
 
     out = {
@@ -332,7 +339,9 @@ def roofline_pass(m, generate, shape, esz, lens):
     m.timing(False)
     hd, KV, H = shape["head_dim"], shape["num_key_value_heads"], shape["num_attention_heads"]
     peak_mm = BF16_PEAK_TFLOPS if esz == 2 else F32_PEAK_TFLOPS
-    sq = sum(n * (n + 1) / 2 for n in lens)
+    W = shape.get("sliding_window") or 0
+    # causal (query, key) pairs; a sliding window keeps min(i + 1, W) keys of query i
+    sq = sum(n * (n + 1) / 2 if not W or n <= W else W * (W + 1) / 2 + (n - W) * W for n in lens)
     # grouped expert launches stream every expert some token chose: the
     # expectation under uniform routing, E (1 - (1 - k/E)^tokens) experts
     E_r, k_r = shape.get("n_routed_experts") or 1, shape.get("num_experts_per_tok") or 1

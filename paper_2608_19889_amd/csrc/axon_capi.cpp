@@ -259,6 +259,8 @@ struct axon_model {
   float* moe_y = nullptr;       // [rows * k][D] expert outputs
   bool moe_model() const { return cfg.n_experts > 0; }
   bool gpt2() const { return cfg.arch == AXON_ARCH_GPT2; }
+  // keys a query at context length ctx attends to (timing records)
+  int keys_read(int ctx) const { return cfg.sliding_window > 0 ? std::min(ctx, cfg.sliding_window) : ctx; }
   int moe_ep() const { return (cfg.n_experts + 31) / 32 * 32; }
   int32_t* d_step = nullptr;
   int32_t* h_step = nullptr;  // pinned staging copy
@@ -485,7 +487,7 @@ struct StepPlan {
   const int32_t* d_drow = nullptr;     // token row
   const int32_t* d_dslot = nullptr;
   const int32_t* d_dpos = nullptr;
-  int dctx = 0;                        // summed context of the single-token entries
+  int dctx = 0;                        // summed keys attended by the single-token entries
 };
 
 // Epilogue arguments of the bf16 QKV GEMM with bias + RoPE + KV write fused:
@@ -690,7 +692,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
     gemv(qa, GV_ROPE);
     int ctx_sum = 0;
     if (plan) ctx_sum = plan->dctx;
-    else for (int b = 0; b < B; ++b) ctx_sum += m->h_len[b] + 1;
+    else for (int b = 0; b < B; ++b) ctx_sum += m->keys_read(m->h_len[b] + 1);
     m->timed(2, H, B, ctx_sum, s, [&] {
       launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, B, H, pos, m->cfg.max_seq, s,
                                nullptr, slot);
@@ -791,7 +793,7 @@ void enqueue_decode_gpt2(axon_model* m, int B, const int32_t* d_tokens, float* d
     }
     int ctx_sum = 0;
     if (plan) ctx_sum = plan->dctx;
-    else for (int b = 0; b < B; ++b) ctx_sum += m->h_len[b] + 1;
+    else for (int b = 0; b < B; ++b) ctx_sum += m->keys_read(m->h_len[b] + 1);
     m->timed(2, H, B, ctx_sum, s, [&] {
       launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, B, H, pos, m->cfg.max_seq, s,
                                nullptr, slot);
@@ -1469,7 +1471,7 @@ extern "C" int axon_step(axon_model* m, int32_t n, const int32_t* h_slots, const
       hs[4 * MB + nd] = h_slots[i];
       hs[5 * MB + nd] = base[i];
       ++nd;
-      plan.dctx += base[i] + 1;
+      plan.dctx += m->keys_read(base[i] + 1);
     }
   }
   HIP_TRY(hipMemcpyAsync(m->d_step, hs, (size_t)6 * MB * sizeof(int32_t), hipMemcpyHostToDevice, s));

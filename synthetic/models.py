@@ -89,6 +89,12 @@ WORKLOADS = {
     "32b": dict(model="32b", batch=32, prompt_len=1024, steps=256, paged=False),
     # the DeepSeek-MoE-16B shape: routed experts through grouped GEMMs
     "moe16b": dict(model="moe16b", batch=32, prompt_len=1024, steps=128, paged=False),
+    # GPT-2 XL (the largest checkpoint of the paper's GPT-2 listing), the 1B
+    # workload's batch, prompt and decode lengths
+    "gpt2xl": dict(model="gpt2xl", batch=8, prompt_len=512, steps=128, paged=False),
+    # Mistral-7B shape with its 4096-key sliding window: prompts twice the
+    # window, so prefill attention and every decode step see the window
+    "mistral7b": dict(model="mistral7b", batch=16, prompt_len=8192, steps=128, paged=False),
     # the 7b_paged requests served by continuous batching: every step carries
     # the running sequences' decode tokens plus prompt chunks of the waiting
     # ones, up to a token budget
