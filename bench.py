@@ -418,10 +418,18 @@ def roofline_pass(m, generate, shape, esz, lens):
 
 
 def kernel_source_digest():
+    """Digest of the decode projection kernels' sources: k_gemv.hip, common.h
+    and, of kernels.h, the part from the projection epilogue enum through the
+    argument struct (declarations elsewhere in that header do not change the
+    kernels)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("k_gemv.hip", "kernels.h", "common.h"):
-        h.update(open(os.path.join(ROOT, "paper_2608_19889_amd", "csrc", f), "rb").read())
+    csrc = os.path.join(ROOT, "paper_2608_19889_amd", "csrc")
+    for f in ("k_gemv.hip", "common.h"):
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    hdr = open(os.path.join(csrc, "kernels.h")).read()
+    a = hdr.index("enum GvEpi")
+    h.update(hdr[a:hdr.index("};", hdr.index("struct GemvArgs", a)) + 2].encode())
     return h.hexdigest()[:16]
 
 
