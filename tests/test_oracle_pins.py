@@ -617,3 +617,72 @@ def test_sliding_window_matches_transformers_mistral_fp64():
     m = OracleDecoder(shp, w)
     m.prefill([ids[0, :3]])
     np.testing.assert_allclose(np.stack([m.decode([t])[0] for t in ids[0, 3:]]), orc[0][3:], atol=1e-10)
+
+
+# ----------------------------------------------------------------- backward pass
+
+def test_rmsnorm_backward_against_torch_autograd():
+    x = RNG.standard_normal((5, 12))
+    g = 1 + 0.1 * RNG.standard_normal(12)
+    dy = RNG.standard_normal((5, 12))
+    xt = torch.from_numpy(x).requires_grad_()
+    gt = torch.from_numpy(g).requires_grad_()
+    y = xt / torch.sqrt(torch.mean(xt * xt, -1, keepdim=True) + 1e-5) * gt
+    y.backward(torch.from_numpy(dy))
+    dx, dg = oracle.rms_norm_backward(x, g, 1e-5, dy)
+    np.testing.assert_allclose(dx, xt.grad.numpy(), atol=1e-13)
+    np.testing.assert_allclose(dg, gt.grad.numpy(), atol=1e-13)
+
+
+@pytest.mark.parametrize("kind", ["llama", "qwen"])
+def test_loss_and_grads_match_transformers_autograd_fp64(kind):
+    """The paper trains through the framework's autograd: transformers' model
+    in float64 with labels = the tokens (its loss shifts them by one) gives
+    the same mean cross-entropy and the same gradient for every weight (HF
+    evaluates the rotary angles in float32, hence the 1e-6 scale)."""
+    shp = _tiny(kind, layers=2)
+    w = _np_weights(shp, seed=21)
+    model = _hf_model(kind, shp, w)
+    ids = RNG.integers(0, shp["vocab_size"], (2, 10))
+    out = model(torch.from_numpy(ids), labels=torch.from_numpy(ids))
+    out.loss.backward()
+    targets = [np.append(s[1:], -1) for s in ids]
+    loss, grads = oracle.loss_and_grads(shp, w, list(ids), targets)
+    assert abs(loss - out.loss.item()) < 1e-6
+    params = dict(model.named_parameters())
+    for name, g in grads.items():
+        ref = params[name].grad.numpy()
+        np.testing.assert_allclose(g, ref, atol=1e-6 * max(1.0, np.abs(ref).max()), rtol=0, err_msg=name)
+        assert np.abs(ref).max() > 0, name  # every weight matters here
+
+
+def test_loss_and_grads_against_finite_differences():
+    """Central differences of the oracle's own loss, for entries of every
+    kind of weight (independent of any library): a dropped term, wrong sign
+    or transposed operand in the reverse pass shows up as a mismatch."""
+    shp = _tiny("qwen", layers=2)
+    w = _np_weights(shp, seed=22)
+    seqs = [RNG.integers(0, shp["vocab_size"], 7), RNG.integers(0, shp["vocab_size"], 4)]
+    targets = [RNG.integers(0, shp["vocab_size"], 7), np.array([3, -1, 5, 9])]
+    _, grads = oracle.loss_and_grads(shp, w, seqs, targets)
+    r = np.random.default_rng(5)
+    h = 1e-5
+    for name in ["model.embed_tokens.weight", "lm_head.weight", "model.norm.weight",
+                 "model.layers.0.input_layernorm.weight", "model.layers.0.self_attn.q_proj.weight",
+                 "model.layers.1.self_attn.k_proj.weight", "model.layers.0.self_attn.v_proj.weight",
+                 "model.layers.1.self_attn.q_proj.bias", "model.layers.0.self_attn.k_proj.bias",
+                 "model.layers.1.self_attn.o_proj.weight", "model.layers.0.post_attention_layernorm.weight",
+                 "model.layers.1.mlp.gate_proj.weight", "model.layers.0.mlp.up_proj.weight",
+                 "model.layers.1.mlp.down_proj.weight"]:
+        for _ in range(3):
+            idx = tuple(r.integers(0, n) for n in w[name].shape)
+            if name == "model.embed_tokens.weight":  # a row some token uses
+                idx = (int(seqs[0][r.integers(0, 7)]),) + idx[1:]
+            wp = dict(w)
+            wp[name] = w[name].copy()
+            wp[name][idx] += h
+            lp, _ = oracle.loss_and_grads(shp, wp, seqs, targets)
+            wp[name][idx] -= 2 * h
+            lm, _ = oracle.loss_and_grads(shp, wp, seqs, targets)
+            fd = (lp - lm) / (2 * h)
+            assert abs(fd - grads[name][idx]) < 1e-7 + 1e-5 * abs(fd), (name, idx, fd, grads[name][idx])
