@@ -222,6 +222,35 @@ int axon_step(axon_model* m, int32_t n, const int32_t* h_slots, const int32_t* h
  * refused by axon_decode_step until axon_step or axon_prefill fills it. */
 int axon_reset_slot(axon_model* m, int32_t slot);
 
+/* Backward pass (training; the paper trains its generated models through
+ * automatic differentiation: Results, "Training with Axon Derived Models").
+ * Runs the forward pass over ``batch`` fresh sequences in slots 0..batch-1 (as
+ * axon_prefill: the KV cache and the slot lengths are overwritten), the mean
+ * next-token cross-entropy
+ *   loss = (1/N) sum over positions t with 0 <= targets[t] < V of
+ *          logsumexp(logits[t]) - logits[t][targets[t]]
+ * (N such positions over all sequences; loss 0 and all gradients 0 when
+ * N == 0), and the gradient of that loss with respect to every weight.
+ *   d_tokens, d_cu_seqlens, h_cu_seqlens: as axon_prefill;
+ *   d_targets  device int32 [sum S_b]: the token position t should predict
+ *              (any value outside [0, V), e.g. -1, is not counted);
+ *   d_loss     device float [1];
+ *   grads      one descriptor per weight of the model: the weight map's names
+ *              and shapes, dtype AXON_F32, device buffers (on_device 1),
+ *              owned by the caller and overwritten with the gradients.
+ * Activations and gradients are stored in bf16 between the kernels, with
+ * float32 accumulation, the residual stream and its gradient in float32.
+ * Dense Llama-family models only (AXON_ARCH_LLAMA, AXON_BF16, n_experts 0,
+ * sliding_window 0, contiguous cache).  The first call allocates a
+ * transposed copy of the weights and, for max_tokens positions, the saved
+ * activations (per token and layer 12 hidden + 4 heads * head_dim + 10
+ * intermediate + 4 heads bytes) and the gradient work buffers (including
+ * float32 and bf16 logits, 6 vocab bytes per token).  Returns AXON_OK, AXON_E_INVALID, AXON_E_CAPACITY, AXON_E_MISSING /
+ * AXON_E_SHAPE / AXON_E_DTYPE (gradient map), AXON_E_OOM or AXON_E_HIP. */
+int axon_loss_and_grads(axon_model* m, int32_t batch, const int32_t* d_tokens, const int32_t* d_cu_seqlens,
+                        const int32_t* h_cu_seqlens, const int32_t* d_targets, float* d_loss,
+                        const axon_weight* grads, int32_t n_grads, void* stream);
+
 /* Current length of every slot (host copy kept by the library, no device
  * access).  Writes min(n, max_batch) entries to ``lens``; returns the number of
  * active slots (the batch of the last prefill), or a negative status. */

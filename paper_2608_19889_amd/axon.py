@@ -30,7 +30,7 @@ AXON_ARCH_GPT2 = 1
 STATUS_NAMES = {0: "AXON_OK", -1: "AXON_E_INVALID", -2: "AXON_E_SHAPE", -3: "AXON_E_MISSING",
                 -4: "AXON_E_DTYPE", -5: "AXON_E_CAPACITY", -6: "AXON_E_OOM", -7: "AXON_E_HIP"}
 
-EXPORTED = ["axon_init_model", "axon_prefill", "axon_decode_step", "axon_step", "axon_reset_slot",
+EXPORTED = ["axon_init_model", "axon_prefill", "axon_decode_step", "axon_step", "axon_reset_slot", "axon_loss_and_grads",
             "axon_slot_lengths", "axon_timing_enable", "axon_timing_records", "axon_free", "axon_last_error"]
 
 # kernel classes of the timing records
@@ -91,6 +91,10 @@ def lib():
                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         L.axon_step.restype = ctypes.c_int
         L.axon_reset_slot.argtypes = [ctypes.c_void_p, ctypes.c_int32]
+        L.axon_loss_and_grads.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.POINTER(AxonWeight), ctypes.c_int32, ctypes.c_void_p]
+        L.axon_loss_and_grads.restype = ctypes.c_int
         L.axon_reset_slot.restype = ctypes.c_int
         L.axon_slot_lengths.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32]
         L.axon_slot_lengths.restype = ctypes.c_int
@@ -211,6 +215,25 @@ class Model:
                                   next_tokens.data_ptr(), ctypes.c_void_p(_stream(stream))))
         self._keep = (cu_d, tokens)
         return logits, next_tokens
+
+    def loss_and_grads(self, tokens: torch.Tensor, cu_seqlens: list, targets: torch.Tensor, grads: dict,
+                       loss: torch.Tensor | None = None, stream=None):
+        """Backward pass (axon_loss_and_grads): tokens / targets device int32
+        [sum S_b] (targets -1 or outside [0, V) are not counted); grads: {weight
+        name: device float32 tensor of that weight's shape}, overwritten with
+        the gradient of the mean cross-entropy.  Returns the loss (device
+        float32 [1])."""
+        dev = tokens.device
+        B = len(cu_seqlens) - 1
+        cu_h = (ctypes.c_int32 * (B + 1))(*[int(c) for c in cu_seqlens])
+        cu_d = torch.tensor([int(c) for c in cu_seqlens], dtype=torch.int32, device=dev)
+        if loss is None:
+            loss = torch.empty((1,), dtype=torch.float32, device=dev)
+        arr, keep = make_weights(grads)
+        _check(lib().axon_loss_and_grads(self._h, B, tokens.data_ptr(), cu_d.data_ptr(), cu_h, targets.data_ptr(),
+                                         loss.data_ptr(), arr, len(grads), ctypes.c_void_p(_stream(stream))))
+        self._keep = (cu_d, tokens, targets, keep)
+        return loss
 
     def decode_step(self, tokens: torch.Tensor, logits: torch.Tensor | None = None,
                     next_tokens: torch.Tensor | None = None, stream=None):

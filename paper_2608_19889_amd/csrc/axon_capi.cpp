@@ -200,6 +200,23 @@ struct GraphKey {
   }
 };
 
+// Backward-pass state, allocated by the first axon_loss_and_grads call: the
+// activations the forward pass keeps per layer, the weights transposed and
+// tiled (the B operand of dX = dY W), and the gradient work buffers.
+struct TrainLayer {
+  float *xin, *xmid, *lse, *gu;  // layer input, residual after attention, log2-sum-exp [T][H], gate/up [T][2I]
+  bf16 *h1, *h2, *q, *o, *a;     // normed inputs, rotated q, attention output, gated activation
+  bf16 *wqkvT, *woT, *wguT, *wdT;
+};
+struct TrainBufs {
+  bool ready = false;
+  int Tc = 0, Tp = 0, Vp = 0;
+  std::vector<TrainLayer> L;
+  float *xfin, *logits, *rowloss, *valid, *lserow, *scal, *dx, *dtmp, *dgrow, *dqf, *dkf, *dvf, *dsum, *dqkvf,
+      *colpart, *gtmp;
+  bf16 *hf, *dlog, *dxb, *dgu, *dob, *dqkv, *tra, *trs, *trb, *headT;
+};
+
 }  // namespace
 
 struct axon_model {
@@ -213,6 +230,7 @@ struct axon_model {
   void* gfinal_b = nullptr;  // GPT-2: final LayerNorm bias
   void* wpe = nullptr;       // GPT-2: learned positions [max_positions][D], row-major
   std::vector<LayerW> layers;
+  TrainBufs train;
   // KV cache
   void* kcache = nullptr;
   void* vcache = nullptr;
@@ -1514,6 +1532,262 @@ extern "C" int axon_step(axon_model* m, int32_t n, const int32_t* h_slots, const
     top = std::max(top, h_slots[i] + 1);
   }
   m->active = std::max(m->active, top);
+  return AXON_OK;
+}
+
+// ------------------------------------------------------------------ training
+
+namespace {
+
+// Allocate the backward-pass state for up to m->rows tokens and build the
+// transposed weight tiles (once per model).
+int train_setup(axon_model* m, hipStream_t s) {
+  TrainBufs& tb = m->train;
+  if (tb.ready) return AXON_OK;
+  const axon_config& c = m->cfg;
+  const int64_t D = c.hidden, H = c.n_heads, KV = c.n_kv_heads, hd = c.head_dim, I = c.intermediate, V = c.vocab;
+  const int64_t nq = (H + 2 * KV) * hd, Hhd = H * hd;
+  tb.Tc = m->rows;
+  tb.Tp = (tb.Tc + 31) / 32 * 32;
+  tb.Vp = (int)((V + 31) / 32 * 32);
+  const int64_t T = tb.Tc, Tp = tb.Tp, Vp = tb.Vp;
+  auto tiled = [](int64_t rows, int64_t cols) { return (rows + 15) / 16 * 16 * cols; };
+  auto fa = [&](float** p, int64_t n) { return dev_alloc(m, (void**)p, (size_t)n * 4); };
+  auto ba = [&](bf16** p, int64_t n) { return dev_alloc(m, (void**)p, (size_t)n * 2); };
+  int r = 0;
+  tb.L.resize(c.n_layers);
+  for (auto& l : tb.L) {
+    if (!r) r = fa(&l.xin, T * D);
+    if (!r) r = fa(&l.xmid, T * D);
+    if (!r) r = fa(&l.lse, T * H);
+    if (!r) r = fa(&l.gu, T * 2 * I);
+    if (!r) r = ba(&l.h1, T * D);
+    if (!r) r = ba(&l.h2, T * D);
+    if (!r) r = ba(&l.q, T * Hhd);
+    if (!r) r = ba(&l.o, T * Hhd);
+    if (!r) r = ba(&l.a, T * I);
+    if (!r) r = ba(&l.wqkvT, tiled(D, nq));
+    if (!r) r = ba(&l.woT, tiled(Hhd, D));
+    if (!r) r = ba(&l.wguT, tiled(D, 2 * I));
+    if (!r) r = ba(&l.wdT, tiled(I, D));
+  }
+  const int64_t maxN = std::max({Vp, 2 * I, nq, D}), maxK = std::max({D, I, Hhd});
+  if (!r) r = fa(&tb.xfin, T * D);
+  if (!r) r = fa(&tb.logits, T * Vp);
+  if (!r) r = fa(&tb.rowloss, T);
+  if (!r) r = fa(&tb.valid, T);
+  if (!r) r = fa(&tb.lserow, T);
+  if (!r) r = fa(&tb.scal, 4);
+  if (!r) r = fa(&tb.dx, T * D);
+  if (!r) r = fa(&tb.dtmp, T * std::max({D, I, Hhd}));
+  if (!r) r = fa(&tb.dgrow, T * D);
+  if (!r) r = fa(&tb.dqf, T * Hhd);
+  if (!r) r = fa(&tb.dkf, T * KV * hd);
+  if (!r) r = fa(&tb.dvf, T * KV * hd);
+  if (!r) r = fa(&tb.dsum, T * H);
+  if (!r) r = fa(&tb.dqkvf, T * nq);
+  if (!r) r = fa(&tb.colpart, (int64_t)colsum_chunks((int)T) * std::max(nq, D));
+  if (!r) r = fa(&tb.gtmp, std::max(nq, 2 * I) * D);
+  if (!r) r = ba(&tb.hf, T * D);
+  if (!r) r = ba(&tb.dlog, T * Vp);
+  if (!r) r = ba(&tb.dxb, T * D);
+  if (!r) r = ba(&tb.dgu, T * 2 * I);
+  if (!r) r = ba(&tb.dob, T * Hhd);
+  if (!r) r = ba(&tb.dqkv, T * nq);
+  if (!r) r = ba(&tb.tra, maxN * Tp);
+  if (!r) r = ba(&tb.trs, maxK * Tp);
+  if (!r) r = ba(&tb.trb, tiled(maxK, Tp));
+  if (!r) r = ba(&tb.headT, tiled(D, Vp));
+  if (r) return r;
+  // W [N][K] (tiled) -> W^T [K][Np] tiled, through a row-major staging copy
+  // whose columns N .. Np-1 are zero
+  bf16* stage = nullptr;
+  const int64_t most = std::max({D * nq, Hhd * D, D * 2 * I, I * D, D * Vp});
+  hipError_t e = hipMalloc((void**)&stage, (size_t)most * 2);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(e == hipErrorOutOfMemory ? AXON_E_OOM : AXON_E_HIP,
+                std::string("training staging allocation: ") + hipGetErrorString(e));
+  }
+  auto wt = [&](const void* W, int64_t N, int64_t K, int64_t Np, bf16* dst) {
+    if (Np > N) (void)hipMemsetAsync(stage, 0, (size_t)K * Np * 2, s);
+    launch_untile_transpose((const bf16*)W, N, (int)K, stage, Np, s);
+    launch_tile_weight(stage, dst, K, (int)Np, s);
+  };
+  for (int l = 0; l < c.n_layers; ++l) {
+    const LayerW& w = m->layers[l];
+    TrainLayer& t = tb.L[l];
+    wt(w.wqkv, nq, D, nq, t.wqkvT);
+    wt(w.wo, D, Hhd, D, t.woT);
+    wt(w.wgu, 2 * I, D, 2 * I, t.wguT);
+    wt(w.wd, D, I, D, t.wdT);
+  }
+  wt(m->lm_head, V, D, Vp, tb.headT);
+  e = hipGetLastError();
+  const hipError_t e2 = hipStreamSynchronize(s);
+  (void)hipFree(stage);
+  if (e != hipSuccess || e2 != hipSuccess)
+    return fail(AXON_E_HIP, std::string("weight transposes: ") + hipGetErrorString(e != hipSuccess ? e : e2));
+  tb.ready = true;
+  return AXON_OK;
+}
+
+// Forward over B fresh sequences keeping every activation the backward pass
+// reads, the loss, and the reverse pass into the caller's gradient buffers
+// (g: one float pointer per expected weight, in expected_weights order).
+void enqueue_train(axon_model* m, int B, int T, const int32_t* d_tokens, const int32_t* d_cu, const int32_t* h_cu,
+                   const int32_t* d_targets, float* d_loss, const std::vector<float*>& g,
+                   const std::unordered_map<std::string, size_t>& gi, hipStream_t s) {
+  const axon_config& c = m->cfg;
+  TrainBufs& tb = m->train;
+  const int D = c.hidden, H = c.n_heads, KV = c.n_kv_heads, hd = c.head_dim, I = c.intermediate, V = c.vocab;
+  const int nq = (H + 2 * KV) * hd, Hhd = H * hd, Tp = tb.Tp, Vp = tb.Vp, L = c.n_layers;
+  const float eps = c.rms_eps;
+  auto G = [&](const std::string& n) { return g[gi.at(n)]; };
+  // ---- forward, keeping activations
+  launch_set_lengths(d_cu, m->d_len, B, s);
+  launch_embed_rmsnorm<bf16>(d_tokens, (const bf16*)m->embed, (const bf16*)m->layers[0].gin, m->x, tb.L[0].h1, T, D,
+                             V, eps, s);
+  for (int l = 0; l < L; ++l) {
+    const LayerW& w = m->layers[l];
+    TrainLayer& t = tb.L[l];
+    KVView kv = m->kv(l, false);
+    (void)hipMemcpyAsync(t.xin, m->x, (size_t)T * D * 4, hipMemcpyDeviceToDevice, s);
+    EpiArgs re = rope_epi(m, w, kv, d_cu, B, nullptr);
+    re.q_out = t.q;
+    gemm_many<bf16>(m, w.wqkv, t.h1, nq, T, D, EPI_ROPE, nullptr, nullptr, nq, s, &re);
+    launch_attn_prefill<bf16>(t.q, kv, t.o, T, B, d_cu, h_cu, H, s, nullptr, nullptr, nullptr, nullptr, t.lse);
+    gemm_many<bf16>(m, w.wo, t.o, D, T, Hhd, EPI_RESID, m->x, nullptr, D, s);
+    (void)hipMemcpyAsync(t.xmid, m->x, (size_t)T * D * 4, hipMemcpyDeviceToDevice, s);
+    launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, (const bf16*)w.gpost, t.h2, T, D, eps, nullptr, s);
+    gemm_many<bf16>(m, w.wgu, t.h2, 2 * I, T, D, EPI_F32, t.gu, nullptr, 2 * I, s);
+    launch_silu_reduce<bf16>(t.gu, 1, 0, t.a, T, I, s);
+    gemm_many<bf16>(m, w.wd, t.a, D, T, I, EPI_RESID, m->x, nullptr, D, s);
+    if (l + 1 < L)
+      launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, (const bf16*)m->layers[l + 1].gin, tb.L[l + 1].h1, T, D, eps,
+                                 nullptr, s);
+  }
+  (void)hipMemcpyAsync(tb.xfin, m->x, (size_t)T * D * 4, hipMemcpyDeviceToDevice, s);
+  launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, (const bf16*)m->gfinal, tb.hf, T, D, eps, nullptr, s);
+  gemm_many<bf16>(m, m->lm_head, tb.hf, V, T, D, EPI_F32, tb.logits, nullptr, Vp, s);
+  // ---- loss and its gradient at the logits
+  launch_ce_loss(tb.logits, Vp, V, d_targets, T, tb.rowloss, tb.valid, tb.lserow, d_loss, tb.scal, tb.dlog, s);
+  // ---- backward
+  // dX = dY W: [T][K] float from dY [T][N] and the tiled W^T [K][N]
+  auto dX = [&](const bf16* WT, const bf16* dY, int N, int K, float* out) {
+    gemm_many<bf16>(m, WT, dY, K, T, N, EPI_F32, out, nullptr, K, s);
+  };
+  // dW = dY^T X: [N][K] float from dY [T][N] (rows ldy apart) and X [T][K]
+  auto dW = [&](const bf16* dY, int ldy, int N, const bf16* X, int K, float* out) {
+    launch_transpose_pad(dY, ldy, T, N, tb.tra, Tp, s);
+    launch_transpose_pad(X, K, T, K, tb.trs, Tp, s);
+    launch_tile_weight(tb.trs, tb.trb, K, Tp, s);
+    gemm_many<bf16>(m, tb.trb, tb.tra, K, N, Tp, EPI_F32, out, nullptr, K, s);
+  };
+  const bool tied = c.tie_embeddings;
+  float* g_embed = G("model.embed_tokens.weight");
+  dW(tb.dlog, Vp, V, tb.hf, D, tied ? g_embed : G("lm_head.weight"));
+  dX(tb.headT, tb.dlog, Vp, D, tb.dtmp);
+  launch_rmsnorm_bwd(tb.xfin, (const bf16*)m->gfinal, tb.dtmp, D, T, D, eps, tb.dx, 0, tb.dgrow, s);
+  launch_colsum(tb.dgrow, D, T, D, tb.colpart, G("model.norm.weight"), s);
+  for (int l = L - 1; l >= 0; --l) {
+    const LayerW& w = m->layers[l];
+    TrainLayer& t = tb.L[l];
+    KVView kv = m->kv(l, false);
+    const std::string p = "model.layers." + std::to_string(l) + ".";
+    // MLP
+    launch_to_bf16(tb.dx, tb.dxb, (int64_t)T * D, s);
+    dW(tb.dxb, D, D, t.a, I, G(p + "mlp.down_proj.weight"));
+    dX(t.wdT, tb.dxb, D, I, tb.dtmp);
+    launch_swiglu_bwd(t.gu, tb.dtmp, tb.dgu, T, I, s);
+    dW(tb.dgu, 2 * I, 2 * I, t.h2, D, tb.gtmp);
+    launch_scatter_rows(tb.gtmp, 2 * I, D, 1, hd, H, KV, G(p + "mlp.gate_proj.weight"), G(p + "mlp.up_proj.weight"),
+                        nullptr, s);
+    dX(t.wguT, tb.dgu, 2 * I, D, tb.dtmp);
+    launch_rmsnorm_bwd(t.xmid, (const bf16*)w.gpost, tb.dtmp, D, T, D, eps, tb.dx, 1, tb.dgrow, s);
+    launch_colsum(tb.dgrow, D, T, D, tb.colpart, G(p + "post_attention_layernorm.weight"), s);
+    // attention
+    launch_to_bf16(tb.dx, tb.dxb, (int64_t)T * D, s);
+    dW(tb.dxb, D, D, t.o, Hhd, G(p + "self_attn.o_proj.weight"));
+    dX(t.woT, tb.dxb, D, Hhd, tb.dtmp);
+    launch_to_bf16(tb.dtmp, tb.dob, (int64_t)T * Hhd, s);
+    launch_attn_bwd(t.q, kv, t.o, tb.dob, t.lse, tb.dsum, d_cu, B, T, H, tb.dqf, tb.dkf, tb.dvf, s);
+    launch_rope_bwd(tb.dqf, tb.dkf, tb.dvf, m->rope_cos, m->rope_sin, d_cu, B, T, H, KV, hd, tb.dqkv,
+                    c.qkv_bias ? tb.dqkvf : nullptr, s);
+    dW(tb.dqkv, nq, nq, t.h1, D, tb.gtmp);
+    launch_scatter_rows(tb.gtmp, nq, D, 0, hd, H, KV, G(p + "self_attn.q_proj.weight"),
+                        G(p + "self_attn.k_proj.weight"), G(p + "self_attn.v_proj.weight"), s);
+    if (c.qkv_bias) {
+      launch_colsum(tb.dqkvf, nq, T, Hhd, tb.colpart, G(p + "self_attn.q_proj.bias"), s);
+      launch_colsum(tb.dqkvf + Hhd, nq, T, KV * hd, tb.colpart, G(p + "self_attn.k_proj.bias"), s);
+      launch_colsum(tb.dqkvf + Hhd + KV * hd, nq, T, KV * hd, tb.colpart, G(p + "self_attn.v_proj.bias"), s);
+    }
+    dX(t.wqkvT, tb.dqkv, nq, D, tb.dtmp);
+    launch_rmsnorm_bwd(t.xin, (const bf16*)w.gin, tb.dtmp, D, T, D, eps, tb.dx, 1, tb.dgrow, s);
+    launch_colsum(tb.dgrow, D, T, D, tb.colpart, G(p + "input_layernorm.weight"), s);
+  }
+  if (!tied) (void)hipMemsetAsync(g_embed, 0, (size_t)V * D * 4, s);
+  launch_embed_bwd(d_tokens, tb.dx, T, D, V, g_embed, s);
+}
+
+}  // namespace
+
+extern "C" int axon_loss_and_grads(axon_model* m, int32_t batch, const int32_t* d_tokens,
+                                   const int32_t* d_cu_seqlens, const int32_t* h_cu_seqlens,
+                                   const int32_t* d_targets, float* d_loss, const axon_weight* grads,
+                                   int32_t n_grads, void* stream) {
+  g_err.clear();
+  if (!m) return fail(AXON_E_INVALID, "model is NULL");
+  const axon_config& c = m->cfg;
+  if (!m->bf || m->gpt2() || m->moe_model() || c.sliding_window > 0 || m->paged())
+    return fail(AXON_E_INVALID, "the backward pass covers dense Llama-family bf16 models with a contiguous cache "
+                                "and no sliding window");
+  if (batch < 1) return fail(AXON_E_INVALID, "batch must be >= 1");
+  if (batch > c.max_batch)
+    return fail(AXON_E_CAPACITY, "batch " + std::to_string(batch) + " exceeds max_batch " + std::to_string(c.max_batch));
+  if (!d_tokens || !d_cu_seqlens || !h_cu_seqlens || !d_targets || !d_loss || !grads)
+    return fail(AXON_E_INVALID, "d_tokens, d_cu_seqlens, h_cu_seqlens, d_targets, d_loss and grads must be non-NULL");
+  if (h_cu_seqlens[0] != 0) return fail(AXON_E_INVALID, "cu_seqlens[0] must be 0");
+  int64_t total = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int64_t sb = (int64_t)h_cu_seqlens[b + 1] - h_cu_seqlens[b];
+    if (sb < 1) return fail(AXON_E_INVALID, "sequence " + std::to_string(b) + " has length " + std::to_string(sb) + " (must be >= 1)");
+    if (sb > c.max_seq)
+      return fail(AXON_E_CAPACITY, "sequence " + std::to_string(b) + " has length " + std::to_string(sb) +
+                                       " > max_seq " + std::to_string(c.max_seq));
+    total += sb;
+  }
+  if (total > m->rows)
+    return fail(AXON_E_CAPACITY, std::to_string(total) + " tokens exceed max_tokens " + std::to_string(m->rows));
+  // the gradient map: exactly the weight map's names and shapes, float32, on the device
+  const auto expected = expected_weights(c);
+  std::unordered_map<std::string, size_t> index;
+  for (size_t i = 0; i < expected.size(); ++i) index[expected[i].first] = i;
+  std::vector<float*> g(expected.size(), nullptr);
+  if (n_grads < 0) return fail(AXON_E_INVALID, "n_grads must be >= 0");
+  for (int i = 0; i < n_grads; ++i) {
+    const axon_weight& w = grads[i];
+    if (!w.name) return fail(AXON_E_INVALID, "gradient " + std::to_string(i) + " has a NULL name");
+    auto it = index.find(w.name);
+    if (it == index.end()) return fail(AXON_E_MISSING, std::string("unknown gradient '") + w.name + "'");
+    if (g[it->second]) return fail(AXON_E_MISSING, std::string("duplicate gradient '") + w.name + "'");
+    const Expected& ex = expected[it->second].second;
+    if (w.dtype != AXON_F32) return fail(AXON_E_DTYPE, std::string("gradient '") + w.name + "' must be AXON_F32");
+    if (w.ndim != ex.ndim || w.shape[0] != ex.shape[0] || (ex.ndim == 2 && w.shape[1] != ex.shape[1]))
+      return fail(AXON_E_SHAPE, std::string("gradient '") + w.name + "' has shape " + shape_str(w.ndim, w.shape) +
+                                    ", expected " + shape_str(ex.ndim, ex.shape));
+    if (!w.data || !w.on_device)
+      return fail(AXON_E_INVALID, std::string("gradient '") + w.name + "' needs a device buffer");
+    g[it->second] = (float*)w.data;
+  }
+  for (size_t i = 0; i < g.size(); ++i)
+    if (!g[i]) return fail(AXON_E_MISSING, "missing gradient '" + expected[i].first + "'");
+  hipStream_t s = (hipStream_t)stream;
+  if (int r = train_setup(m, s)) return r;
+  enqueue_train(m, batch, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, d_targets, d_loss, g, index, s);
+  if (int r = check_launch("backward pass")) return r;
+  for (int b = 0; b < c.max_batch; ++b) m->h_len[b] = b < batch ? h_cu_seqlens[b + 1] - h_cu_seqlens[b] : 0;
+  m->active = batch;
   return AXON_OK;
 }
 

@@ -87,7 +87,8 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
                                                                    const int32_t* __restrict__ cu, int H,
                                                                    const int32_t* __restrict__ ents,
                                                                    const int32_t* __restrict__ ent_slot,
-                                                                   const int32_t* __restrict__ ent_base) {
+                                                                   const int32_t* __restrict__ ent_base,
+                                                                   float* __restrict__ lse) {
   constexpr int KCH = HD / 8;            // 16-byte chunks per K row
   constexpr int VCH = PK / 8;            // chunks per V^T row (8)
   constexpr int KT = PK * KCH;           // chunks per K tile
@@ -279,6 +280,9 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
     if (myq >= S) continue;
     const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32, 64);
     const float inv = 1.f / l_tot;
+    // log2 of sum_k exp2(score_k * sc): what the backward pass recomputes
+    // its probabilities from
+    if (lse && hl == 0) lse[(int64_t)(tok0 + myq) * H + head] = (m_run[qb] == -INFINITY ? 0.f : m_run[qb]) + __log2f(l_tot);
     bf16* op = o + ((int64_t)(tok0 + myq) * H + head) * HD;
 #pragma unroll
     for (int d = 0; d < HD / 32; ++d)
@@ -589,7 +593,7 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ 
 template <typename T>
 void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, const int32_t* cu,
                          const int32_t* h_cu, int H, hipStream_t s, const int32_t* ents, const int32_t* h_ents,
-                         const int32_t* ent_slot, const int32_t* ent_base) {
+                         const int32_t* ent_slot, const int32_t* ent_base, float* lse) {
   if (T_tokens <= 0 || nseq <= 0) return;
   if constexpr (sizeof(T) == 4) {
     dim3 grid(T_tokens, H);
@@ -606,9 +610,9 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
     }
     dim3 grid(tiles, H);
     if (kv.hd == 64)
-      attn_prefill_bf16_kernel<64, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base);
+      attn_prefill_bf16_kernel<64, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base, lse);
     else
-      attn_prefill_bf16_kernel<128, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base);
+      attn_prefill_bf16_kernel<128, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base, lse);
   }
 }
 
@@ -663,9 +667,11 @@ void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, 
 }
 
 template void launch_attn_prefill<float>(const float*, KVView, float*, int, int, const int32_t*, const int32_t*, int,
-                                         hipStream_t, const int32_t*, const int32_t*, const int32_t*, const int32_t*);
+                                         hipStream_t, const int32_t*, const int32_t*, const int32_t*, const int32_t*,
+                                         float*);
 template void launch_attn_prefill<bf16>(const bf16*, KVView, bf16*, int, int, const int32_t*, const int32_t*, int,
-                                        hipStream_t, const int32_t*, const int32_t*, const int32_t*, const int32_t*);
+                                        hipStream_t, const int32_t*, const int32_t*, const int32_t*, const int32_t*,
+                                        float*);
 template void launch_attn_decode<float>(const float*, KVView, float*, float*, int, int, const int32_t*, int,
                                         hipStream_t, const int32_t*, const int32_t*);
 template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int, int, const int32_t*, int,

@@ -1,0 +1,505 @@
+// Backward pass of the Llama-family decoder (training): the loss, the
+// reverse of each forward step that is not a projection, and the layout
+// helpers that let the projection gradients run on the prefill GEMM.
+//
+// Every projection Y = X W^T (X [T][K], W [N][K]) has two gradients, both run
+// by gemm_bf16 (out[r][c] = sum_k A[r][k] B[c][k], B fragment-tiled):
+//   dX = dY W       : A = dY [T][N],   B = W^T tiled [K][N]  (contraction N)
+//   dW = dY^T X     : A = dY^T [N][Tp], B = X^T tiled [K][Tp] (contraction Tp,
+//                     the token count padded to 32 with zero columns)
+// so the weights get a transposed tiled copy once, and the activations and
+// their gradients are transposed per use (transpose_pad_kernel).
+//
+// Attention backward recomputes the probabilities from the forward pass's
+// per-(query, head) log2-sum-exp: P = 2^(s sc - lse) with sc = log2(e) /
+// sqrt(hd); dP = dO V^T; dS = P (dP - D) with D = rowsum(dO O); dQ = dS K /
+// sqrt(hd); dK = dS^T Q / sqrt(hd); dV = P^T dO.  One wavefront per (query,
+// head) accumulates dQ over the query's keys; one per (key, kv head)
+// accumulates dK and dV over the later queries of every head of its group.
+// No atomics, so every gradient but the embedding's is deterministic.
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace axon {
+
+constexpr float LOG2E = 1.4426950408889634f;
+
+AXON_DEV float block_max(float v, float* red) {
+  v = wave_max(v);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float m = -INFINITY;
+  for (int i = 0; i < nw; ++i) m = fmaxf(m, red[i]);
+  return m;
+}
+
+// ---------------------------------------------------------------- the loss
+
+// Row t of logits [T][ldl]: lse = log sum_v exp(logit_v) over v < V; a target
+// in [0, V) counts (rowloss = lse - logit_target, valid = 1), any other value
+// does not (0, 0).
+__global__ void __launch_bounds__(256) ce_rows_kernel(const float* __restrict__ logits, int ldl, int V,
+                                                      const int32_t* __restrict__ targets,
+                                                      float* __restrict__ rowloss, float* __restrict__ valid,
+                                                      float* __restrict__ lse_out) {
+  __shared__ float red[16];
+  const int t = blockIdx.x;
+  const float* row = logits + (int64_t)t * ldl;
+  float mx = -INFINITY;
+  for (int v = threadIdx.x; v < V; v += 256) mx = fmaxf(mx, row[v]);
+  mx = block_max(mx, red);
+  float sum = 0.f;
+  for (int v = threadIdx.x; v < V; v += 256) sum += __expf(row[v] - mx);
+  sum = block_sum(sum, red);
+  if (threadIdx.x == 0) {
+    const float lse = mx + __logf(sum);
+    const int tg = targets[t];
+    const bool ok = tg >= 0 && tg < V;
+    rowloss[t] = ok ? lse - row[tg] : 0.f;
+    valid[t] = ok ? 1.f : 0.f;
+    lse_out[t] = lse;
+  }
+}
+
+// loss = sum(rowloss) / N over the N counted rows (0 when none); scal[0] = 1/N
+// (0 when none).  One workgroup, fixed summation order.
+__global__ void __launch_bounds__(256) ce_reduce_kernel(const float* __restrict__ rowloss,
+                                                        const float* __restrict__ valid, int T,
+                                                        float* __restrict__ loss, float* __restrict__ scal) {
+  __shared__ float red[16];
+  float s = 0.f, n = 0.f;
+  for (int t = threadIdx.x; t < T; t += 256) {
+    s += rowloss[t];
+    n += valid[t];
+  }
+  s = block_sum(s, red);
+  n = block_sum(n, red);
+  if (threadIdx.x == 0) {
+    loss[0] = n > 0.f ? s / n : 0.f;
+    scal[0] = n > 0.f ? 1.f / n : 0.f;
+  }
+}
+
+// dlogits[t][v] = (softmax_v - [v == target]) / N for counted rows, else 0;
+// columns V .. ldl-1 are zero.  4 columns per thread (ldl % 4 == 0).
+__global__ void __launch_bounds__(256) ce_grad_kernel(const float* __restrict__ logits, int ldl, int V,
+                                                      const int32_t* __restrict__ targets,
+                                                      const float* __restrict__ valid,
+                                                      const float* __restrict__ lse, const float* __restrict__ scal,
+                                                      bf16* __restrict__ dlog) {
+  const int t = blockIdx.y;
+  const int v0 = (blockIdx.x * 256 + threadIdx.x) * 4;
+  if (v0 >= ldl) return;
+  const bool ok = valid[t] > 0.f;
+  const float l = lse[t], inv = scal[0];
+  const int tg = targets[t];
+  bf16x4 o;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int v = v0 + j;
+    float g = 0.f;
+    if (ok && v < V) g = (__expf(logits[(int64_t)t * ldl + v] - l) - (v == tg ? 1.f : 0.f)) * inv;
+    o[j] = (bf16)g;
+  }
+  *(bf16x4*)(dlog + (int64_t)t * ldl + v0) = o;
+}
+
+// ---------------------------------------------------------------- layouts
+
+// dst[c][t] = src[t][c] for t < T, 0 for T <= t < Tp (bf16; src rows ld apart)
+__global__ void __launch_bounds__(256) transpose_pad_kernel(const bf16* __restrict__ src, int ld, int T, int C,
+                                                            bf16* __restrict__ dst, int Tp) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int t0 = blockIdx.y * 8;
+  if (c >= C) return;
+  bf16x8 v;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] = t0 + j < T ? src[(int64_t)(t0 + j) * ld + c] : (bf16)0.f;
+  *(bf16x8*)(dst + (int64_t)c * Tp + t0) = v;
+}
+
+// dst[k][n] = W[n][k] from the fragment-tiled W [N][K]; dst rows are Np
+// apart (the caller zeroes columns N .. Np-1)
+__global__ void __launch_bounds__(256) untile_transpose_kernel(const bf16* __restrict__ W, int64_t N, int K,
+                                                               bf16* __restrict__ dst, int64_t Np) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (n, k-chunk)
+  const int kc = K / 8;
+  if (q >= N * kc) return;
+  const int64_t n = q / kc;
+  const int c = (int)(q % kc);
+  const bf16x8 v = *(const bf16x8*)(W + wt_chunk(n, c, K));
+#pragma unroll
+  for (int j = 0; j < 8; ++j) dst[(int64_t)(c * 8 + j) * Np + n] = v[j];
+}
+
+__global__ void __launch_bounds__(256) to_bf16_kernel(const float* __restrict__ src, bf16* __restrict__ dst,
+                                                      int64_t n4) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n4) return;
+  const f32x4 v = *(const f32x4*)(src + i * 4);
+  *(bf16x4*)(dst + i * 4) = bf16x4{(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+}
+
+// ---------------------------------------------------------------- norms, MLP
+
+// RMSNorm y = x r g, r = rsqrt(mean(x^2) + eps): dx (= or +=) r g dy - x r^3
+// mean(g dy x); dgrow = dy x r (summed over rows by the column sum)
+__global__ void __launch_bounds__(256) rmsnorm_bwd_kernel(const float* __restrict__ x, const bf16* __restrict__ g,
+                                                          const float* __restrict__ dy, int ldy, int D, float eps,
+                                                          float* __restrict__ dx, int accumulate,
+                                                          float* __restrict__ dgrow) {
+  __shared__ float red[16];
+  const int t = blockIdx.x;
+  const float* xr = x + (int64_t)t * D;
+  const float* dyr = dy + (int64_t)t * ldy;
+  float ss = 0.f, sgd = 0.f;
+  for (int i = threadIdx.x; i < D; i += 256) {
+    const float xv = xr[i];
+    ss += xv * xv;
+    sgd += (float)g[i] * dyr[i] * xv;
+  }
+  ss = block_sum(ss, red);
+  sgd = block_sum(sgd, red);
+  const float r = rsqrtf(ss / (float)D + eps);
+  const float c = r * r * r * sgd / (float)D;
+  float* dxr = dx + (int64_t)t * D;
+  for (int i = threadIdx.x; i < D; i += 256) {
+    const float xv = xr[i], d = dyr[i];
+    const float v = r * (float)g[i] * d - xv * c;
+    dxr[i] = accumulate ? dxr[i] + v : v;
+    dgrow[(int64_t)t * D + i] = d * xv * r;
+  }
+}
+
+// gate/up pre-activations gu [T][2I] in the interleaved row order (16 gate
+// rows, then the 16 matching up rows); da [T][I]: dgu = (da u silu'(g),
+// da silu(g)) in the same order, silu'(g) = s (1 + g (1 - s)), s = sigmoid(g)
+__global__ void __launch_bounds__(256) swiglu_bwd_kernel(const float* __restrict__ gu, const float* __restrict__ da,
+                                                         bf16* __restrict__ dgu, int T, int I) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)T * I) return;
+  const int t = (int)(idx / I), f = (int)(idx % I);
+  const int64_t rg = (int64_t)t * 2 * I + (f / 16) * 32 + (f % 16);
+  const float g = gu[rg], u = gu[rg + 16], d = da[idx];
+  const float s = 1.f / (1.f + __expf(-g));
+  dgu[rg] = (bf16)(d * u * s * (1.f + g * (1.f - s)));
+  dgu[rg + 16] = (bf16)(d * g * s);
+}
+
+// column sums of src [T][C] (rows ld apart) in two deterministic passes:
+// part[chunk][c] over rows chunk*rpc .., then dst[c] = sum over chunks
+__global__ void __launch_bounds__(256) colsum_part_kernel(const float* __restrict__ src, int64_t ld, int T, int C,
+                                                          int rpc, float* __restrict__ part) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= C) return;
+  const int t0 = blockIdx.y * rpc, t1 = min(T, t0 + rpc);
+  float s = 0.f;
+  for (int t = t0; t < t1; ++t) s += src[(int64_t)t * ld + c];
+  part[(int64_t)blockIdx.y * C + c] = s;
+}
+__global__ void __launch_bounds__(256) colsum_final_kernel(const float* __restrict__ part, int nchunks, int C,
+                                                           float* __restrict__ dst) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= C) return;
+  float s = 0.f;
+  for (int i = 0; i < nchunks; ++i) s += part[(int64_t)i * C + c];
+  dst[c] = s;
+}
+
+// ---------------------------------------------------------------- attention
+
+// D[t][h] = sum_d dO[t][h][d] O[t][h][d]
+__global__ void __launch_bounds__(256) attn_bwd_d_kernel(const bf16* __restrict__ dob, const bf16* __restrict__ o,
+                                                         int TH, int hd, float* __restrict__ dsum) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= TH) return;
+  const bf16* a = dob + (int64_t)i * hd;
+  const bf16* b = o + (int64_t)i * hd;
+  float s = 0.f;
+  for (int d = 0; d < hd; d += 8) {
+    const bf16x8 x = *(const bf16x8*)(a + d), y = *(const bf16x8*)(b + d);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s += (float)x[j] * (float)y[j];
+  }
+  dsum[i] = s;
+}
+
+// dQ of query token t (sequence e = slot e, position t - cu[e]) and head:
+// lane = key for the scores, lane = head dimension for the accumulation
+template <int HD>
+__global__ void __launch_bounds__(64) attn_bwd_dq_kernel(const bf16* __restrict__ q, KVView kv,
+                                                         const bf16* __restrict__ dob, const float* __restrict__ lse,
+                                                         const float* __restrict__ dsum,
+                                                         const int32_t* __restrict__ cu, int nseq, int H,
+                                                         float* __restrict__ dq) {
+  constexpr int DL = HD / 64;
+  __shared__ float qs[HD], dos[HD], ps[64];
+  const int t = blockIdx.x, head = blockIdx.y, lane = threadIdx.x;
+  const int e = seq_of_token(cu, nseq, t);
+  const int pos = t - cu[e];
+  const int kvh = head / (H / kv.kv_heads);
+  const int64_t row = ((int64_t)t * H + head) * HD;
+  for (int d = lane; d < HD; d += 64) {
+    qs[d] = (float)q[row + d];
+    dos[d] = (float)dob[row + d];
+  }
+  __syncthreads();
+  const float sc = LOG2E / sqrtf((float)HD);
+  const float l2 = lse[(int64_t)t * H + head], Di = dsum[(int64_t)t * H + head];
+  const bf16* kb = (const bf16*)kv.k;
+  const bf16* vb = (const bf16*)kv.v;
+  float acc[DL] = {};
+  for (int j0 = 0; j0 <= pos; j0 += 64) {
+    const int j = j0 + lane;
+    float ds = 0.f;
+    if (j <= pos) {
+      const int64_t kbase = k_el(kv, e, kvh, j, 0), vbase = v_el(kv, e, kvh, j, 0);
+      float s = 0.f, dp = 0.f;
+      for (int d = 0; d < HD; d += 8) {
+        const bf16x8 k8 = *(const bf16x8*)(kb + kbase + (d >> 3) * 128);
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          s = fmaf(qs[d + c], (float)k8[c], s);
+          dp = fmaf(dos[d + c], (float)vb[vbase + (d + c) * 16], dp);
+        }
+      }
+      ds = exp2f(s * sc - l2) * (dp - Di);
+    }
+    ps[lane] = ds;
+    __syncthreads();
+    const int nj = min(64, pos + 1 - j0);
+    for (int jj = 0; jj < nj; ++jj) {
+      const int64_t kbase = k_el(kv, e, kvh, j0 + jj, 0);
+#pragma unroll
+      for (int i = 0; i < DL; ++i) {
+        const int d = lane + i * 64;
+        acc[i] = fmaf(ps[jj], (float)kb[kbase + (d >> 3) * 128 + (d & 7)], acc[i]);
+      }
+    }
+    __syncthreads();
+  }
+  const float rs = 1.f / sqrtf((float)HD);
+#pragma unroll
+  for (int i = 0; i < DL; ++i) dq[row + lane + i * 64] = acc[i] * rs;
+}
+
+// dK and dV of key token j (sequence e, position j - cu[e]) and kv head: over
+// the queries of the sequence at positions >= the key's, for every query head
+// of the group (lane = query for the scores, lane = head dimension for the
+// accumulation)
+template <int HD>
+__global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict__ q, KVView kv,
+                                                          const bf16* __restrict__ dob,
+                                                          const float* __restrict__ lse,
+                                                          const float* __restrict__ dsum,
+                                                          const int32_t* __restrict__ cu, int nseq, int H,
+                                                          float* __restrict__ dk, float* __restrict__ dv) {
+  constexpr int DL = HD / 64;
+  __shared__ float ks[HD], vs[HD], ps[64], dss[64];
+  const int j = blockIdx.x, kvh = blockIdx.y, lane = threadIdx.x;
+  const int e = seq_of_token(cu, nseq, j);
+  const int tok0 = cu[e], S = cu[e + 1] - tok0, posj = j - tok0;
+  const int group = H / kv.kv_heads;
+  const bf16* kb = (const bf16*)kv.k;
+  const bf16* vb = (const bf16*)kv.v;
+  for (int d = lane; d < HD; d += 64) {
+    ks[d] = (float)kb[k_el(kv, e, kvh, posj, d)];
+    vs[d] = (float)vb[v_el(kv, e, kvh, posj, d)];
+  }
+  __syncthreads();
+  const float sc = LOG2E / sqrtf((float)HD);
+  float akk[DL] = {}, avv[DL] = {};
+  for (int hh = 0; hh < group; ++hh) {
+    const int head = kvh * group + hh;
+    for (int i0 = posj; i0 < S; i0 += 64) {
+      const int i = i0 + lane;
+      float p = 0.f, ds = 0.f;
+      if (i < S) {
+        const int64_t row = ((int64_t)(tok0 + i) * H + head) * HD;
+        float s = 0.f, dp = 0.f;
+        for (int d = 0; d < HD; d += 8) {
+          const bf16x8 q8 = *(const bf16x8*)(q + row + d), o8 = *(const bf16x8*)(dob + row + d);
+#pragma unroll
+          for (int c = 0; c < 8; ++c) {
+            s = fmaf((float)q8[c], ks[d + c], s);
+            dp = fmaf((float)o8[c], vs[d + c], dp);
+          }
+        }
+        const int64_t th = (int64_t)(tok0 + i) * H + head;
+        p = exp2f(s * sc - lse[th]);
+        ds = p * (dp - dsum[th]);
+      }
+      ps[lane] = p;
+      dss[lane] = ds;
+      __syncthreads();
+      const int ni = min(64, S - i0);
+      for (int ii = 0; ii < ni; ++ii) {
+        const int64_t row = ((int64_t)(tok0 + i0 + ii) * H + head) * HD;
+#pragma unroll
+        for (int c = 0; c < DL; ++c) {
+          const int d = lane + c * 64;
+          avv[c] = fmaf(ps[ii], (float)dob[row + d], avv[c]);
+          akk[c] = fmaf(dss[ii], (float)q[row + d], akk[c]);
+        }
+      }
+      __syncthreads();
+    }
+  }
+  const float rs = 1.f / sqrtf((float)HD);
+  const int64_t orow = ((int64_t)j * kv.kv_heads + kvh) * HD;
+#pragma unroll
+  for (int c = 0; c < DL; ++c) {
+    dk[orow + lane + c * 64] = akk[c] * rs;
+    dv[orow + lane + c * 64] = avv[c];
+  }
+}
+
+// Gradients at the rotated q / k and at v back through RoPE (the transpose of
+// a rotation rotates by the opposite angle) into the fused QKV layout: dqkv
+// [T][nq] bf16 in the projection's row order (within a head, groups of 8 =
+// 4 first halves and their partners), dqkv_f [T][nq] float in the original
+// order (for the bias gradient; may be null).  One thread per (token, head,
+// pair i < hd/2).
+__global__ void __launch_bounds__(256) rope_bwd_kernel(const float* __restrict__ dq, const float* __restrict__ dk,
+                                                       const float* __restrict__ dv, const float* __restrict__ cos_t,
+                                                       const float* __restrict__ sin_t,
+                                                       const int32_t* __restrict__ cu, int nseq, int T, int H,
+                                                       int KVh, int hd, bf16* __restrict__ dqkv,
+                                                       float* __restrict__ dqkv_f) {
+  const int half = hd / 2, NH = H + 2 * KVh;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)T * NH * half) return;
+  const int i = (int)(idx % half);
+  const int hh = (int)((idx / half) % NH);
+  const int t = (int)(idx / ((int64_t)half * NH));
+  const float* src = hh < H ? dq + ((int64_t)t * H + hh) * hd
+                            : (hh < H + KVh ? dk + ((int64_t)t * KVh + hh - H) * hd
+                                            : dv + ((int64_t)t * KVh + hh - H - KVh) * hd);
+  float y1 = src[i], y2 = src[i + half];
+  if (hh < H + KVh) {
+    const int pos = t - cu[seq_of_token(cu, nseq, t)];
+    const float c = cos_t[(int64_t)pos * half + i], s = sin_t[(int64_t)pos * half + i];
+    const float x1 = y1 * c + y2 * s, x2 = y2 * c - y1 * s;
+    y1 = x1;
+    y2 = x2;
+  }
+  const int64_t nq = (int64_t)NH * hd;
+  const int r1 = 8 * (i / 4) + (i % 4);  // row of element i in the grouped order; its partner is 4 later
+  dqkv[(int64_t)t * nq + hh * hd + r1] = (bf16)y1;
+  dqkv[(int64_t)t * nq + hh * hd + r1 + 4] = (bf16)y2;
+  if (dqkv_f) {
+    dqkv_f[(int64_t)t * nq + hh * hd + i] = y1;
+    dqkv_f[(int64_t)t * nq + hh * hd + i + half] = y2;
+  }
+}
+
+// Rows of a projection gradient [R][D] in the kernel layout, back to the
+// weight map's tensors: mode 0 (fused QKV, heads q then k then v, grouped rows)
+// into dst0 / dst1 / dst2 = q / k / v; mode 1 (gate/up interleaved in blocks
+// of 16) into dst0 / dst1 = gate / up.  4 columns per thread.
+__global__ void __launch_bounds__(256) scatter_rows_kernel(const float* __restrict__ src, int D, int mode, int hd,
+                                                           int H, int KVh, float* __restrict__ dst0,
+                                                           float* __restrict__ dst1, float* __restrict__ dst2) {
+  const int r = blockIdx.x;
+  const int c = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (c >= D) return;
+  float* dst;
+  if (mode == 0) {
+    const int hh = r / hd, rr = r % hd, g = rr / 8, j = rr % 8;
+    const int L = hh * hd + (j < 4 ? 4 * g + j : hd / 2 + 4 * g + j - 4);
+    dst = hh < H ? dst0 + (int64_t)L * D
+                 : (hh < H + KVh ? dst1 + (int64_t)(L - H * hd) * D : dst2 + (int64_t)(L - (H + KVh) * hd) * D);
+  } else {
+    const int b = r / 32, j = r % 32;
+    dst = j < 16 ? dst0 + (int64_t)(b * 16 + j) * D : dst1 + (int64_t)(b * 16 + j - 16) * D;
+  }
+  *(f32x4*)(dst + c) = *(const f32x4*)(src + (int64_t)r * D + c);
+}
+
+// dE[tok[t]] += dx[t] (tokens repeat, hence atomic additions)
+__global__ void __launch_bounds__(256) embed_bwd_kernel(const int32_t* __restrict__ tok, const float* __restrict__ dx,
+                                                        int D, int V, float* __restrict__ dE) {
+  const int t = blockIdx.x;
+  const int id = min(max(tok[t], 0), V - 1);
+  for (int d = threadIdx.x; d < D; d += 256) atomicAdd(dE + (int64_t)id * D + d, dx[(int64_t)t * D + d]);
+}
+
+// ---------------------------------------------------------------- launchers
+
+void launch_ce_loss(const float* logits, int ldl, int V, const int32_t* targets, int T, float* rowloss, float* valid,
+                    float* lse, float* loss, float* scal, bf16* dlog, hipStream_t s) {
+  ce_rows_kernel<<<T, 256, 0, s>>>(logits, ldl, V, targets, rowloss, valid, lse);
+  ce_reduce_kernel<<<1, 256, 0, s>>>(rowloss, valid, T, loss, scal);
+  ce_grad_kernel<<<dim3((ldl / 4 + 255) / 256, T), 256, 0, s>>>(logits, ldl, V, targets, valid, lse, scal, dlog);
+}
+
+void launch_transpose_pad(const bf16* src, int ld, int T, int C, bf16* dst, int Tp, hipStream_t s) {
+  if (C <= 0 || Tp <= 0) return;
+  transpose_pad_kernel<<<dim3((C + 255) / 256, Tp / 8), 256, 0, s>>>(src, ld, T, C, dst, Tp);
+}
+
+void launch_untile_transpose(const bf16* W, int64_t N, int K, bf16* dst, int64_t Np, hipStream_t s) {
+  const int64_t n = N * (K / 8);
+  if (n > 0) untile_transpose_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(W, N, K, dst, Np);
+}
+
+void launch_to_bf16(const float* src, bf16* dst, int64_t n, hipStream_t s) {
+  const int64_t n4 = n / 4;
+  if (n4 > 0) to_bf16_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(src, dst, n4);
+}
+
+void launch_rmsnorm_bwd(const float* x, const bf16* g, const float* dy, int ldy, int T, int D, float eps, float* dx,
+                        int accumulate, float* dgrow, hipStream_t s) {
+  if (T > 0) rmsnorm_bwd_kernel<<<T, 256, 0, s>>>(x, g, dy, ldy, D, eps, dx, accumulate, dgrow);
+}
+
+void launch_swiglu_bwd(const float* gu, const float* da, bf16* dgu, int T, int I, hipStream_t s) {
+  const int64_t n = (int64_t)T * I;
+  if (n > 0) swiglu_bwd_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(gu, da, dgu, T, I);
+}
+
+int colsum_chunks(int T) { return std::max(1, std::min(256, (T + 63) / 64)); }
+
+void launch_colsum(const float* src, int64_t ld, int T, int C, float* part, float* dst, hipStream_t s) {
+  if (T <= 0 || C <= 0) return;
+  const int nch = colsum_chunks(T), rpc = (T + nch - 1) / nch;
+  colsum_part_kernel<<<dim3((C + 255) / 256, nch), 256, 0, s>>>(src, ld, T, C, rpc, part);
+  colsum_final_kernel<<<(C + 255) / 256, 256, 0, s>>>(part, nch, C, dst);
+}
+
+void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
+                     const int32_t* cu, int nseq, int T, int H, float* dq, float* dk, float* dv, hipStream_t s) {
+  if (T <= 0) return;
+  attn_bwd_d_kernel<<<(T * H + 255) / 256, 256, 0, s>>>(dob, o, T * H, kv.hd, dsum);
+  if (kv.hd == 64) {
+    attn_bwd_dq_kernel<64><<<dim3(T, H), 64, 0, s>>>(q, kv, dob, lse, dsum, cu, nseq, H, dq);
+    attn_bwd_dkv_kernel<64><<<dim3(T, kv.kv_heads), 64, 0, s>>>(q, kv, dob, lse, dsum, cu, nseq, H, dk, dv);
+  } else {
+    attn_bwd_dq_kernel<128><<<dim3(T, H), 64, 0, s>>>(q, kv, dob, lse, dsum, cu, nseq, H, dq);
+    attn_bwd_dkv_kernel<128><<<dim3(T, kv.kv_heads), 64, 0, s>>>(q, kv, dob, lse, dsum, cu, nseq, H, dk, dv);
+  }
+}
+
+void launch_rope_bwd(const float* dq, const float* dk, const float* dv, const float* cos_t, const float* sin_t,
+                     const int32_t* cu, int nseq, int T, int H, int KVh, int hd, bf16* dqkv, float* dqkv_f,
+                     hipStream_t s) {
+  const int64_t n = (int64_t)T * (H + 2 * KVh) * (hd / 2);
+  if (n > 0)
+    rope_bwd_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(dq, dk, dv, cos_t, sin_t, cu, nseq, T, H, KVh, hd,
+                                                                dqkv, dqkv_f);
+}
+
+void launch_scatter_rows(const float* src, int R, int D, int mode, int hd, int H, int KVh, float* dst0, float* dst1,
+                         float* dst2, hipStream_t s) {
+  if (R > 0) scatter_rows_kernel<<<dim3(R, (D / 4 + 255) / 256), 256, 0, s>>>(src, D, mode, hd, H, KVh, dst0, dst1, dst2);
+}
+
+void launch_embed_bwd(const int32_t* tok, const float* dx, int T, int D, int V, float* dE, hipStream_t s) {
+  if (T > 0) embed_bwd_kernel<<<T, 256, 0, s>>>(tok, dx, D, V, dE);
+}
+
+}  // namespace axon

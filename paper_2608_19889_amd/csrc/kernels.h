@@ -89,6 +89,40 @@ void launch_layernorm(const float* x, const bf16* g, const bf16* beta, bf16* h, 
 // [in][out] transposed to [N][K], rows optionally permuted
 void launch_transpose_rows(const bf16* src, bf16* dst, int K, int N, const int32_t* perm, hipStream_t s);
 
+// ---- backward pass (k_train.hip)
+// loss over logits [T][ldl] (V real columns, ldl % 4 == 0) and targets
+// (counted when in [0, V)): loss[0] = mean cross-entropy, dlog [T][ldl] bf16 =
+// its gradient (zero padding); rowloss / valid / lse [T] and scal [1] scratch
+void launch_ce_loss(const float* logits, int ldl, int V, const int32_t* targets, int T, float* rowloss, float* valid,
+                    float* lse, float* loss, float* scal, bf16* dlog, hipStream_t s);
+// dst [C][Tp] = src [T][C]^T (rows ld apart), zero columns T .. Tp-1 (Tp % 8 == 0)
+void launch_transpose_pad(const bf16* src, int ld, int T, int C, bf16* dst, int Tp, hipStream_t s);
+// dst [K][Np] (row-major) = W^T for the fragment-tiled W [N][K]
+void launch_untile_transpose(const bf16* W, int64_t N, int K, bf16* dst, int64_t Np, hipStream_t s);
+void launch_to_bf16(const float* src, bf16* dst, int64_t n, hipStream_t s);  // n % 4 == 0
+// RMSNorm backward: dx (accumulate ? += : =) and per-row gain terms dgrow [T][D]
+void launch_rmsnorm_bwd(const float* x, const bf16* g, const float* dy, int ldy, int T, int D, float eps, float* dx,
+                        int accumulate, float* dgrow, hipStream_t s);
+void launch_swiglu_bwd(const float* gu, const float* da, bf16* dgu, int T, int I, hipStream_t s);
+// dst[c] = sum_t src[t][c], deterministic; part holds colsum_chunks(T) * C floats
+int colsum_chunks(int T);
+void launch_colsum(const float* src, int64_t ld, int T, int C, float* part, float* dst, hipStream_t s);
+// attention backward over nseq fresh sequences in slots 0.. (contiguous cache):
+// dq [T][H][hd], dk / dv [T][KV][hd] (float), from q / o / dO [T][H][hd] bf16,
+// the forward's log2-sum-exp lse [T][H]; dsum [T][H] scratch
+void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
+                     const int32_t* cu, int nseq, int T, int H, float* dq, float* dk, float* dv, hipStream_t s);
+// back through RoPE into the fused QKV row order (bf16) and the original order
+// (float, may be null)
+void launch_rope_bwd(const float* dq, const float* dk, const float* dv, const float* cos_t, const float* sin_t,
+                     const int32_t* cu, int nseq, int T, int H, int KVh, int hd, bf16* dqkv, float* dqkv_f,
+                     hipStream_t s);
+// projection gradient rows back to the weight map's tensors (mode 0: QKV into
+// q / k / v; mode 1: gate/up into gate / up)
+void launch_scatter_rows(const float* src, int R, int D, int mode, int hd, int H, int KVh, float* dst0, float* dst1,
+                         float* dst2, hipStream_t s);
+void launch_embed_bwd(const int32_t* tok, const float* dx, int T, int D, int V, float* dE, hipStream_t s);
+
 // ---- weight layout (k_layout.hip): fragment-tiled copy of row-major bf16
 // W [N][K] (K % 32 == 0) into dst of round_up(N, 16) * K elements
 void launch_tile_weight(const bf16* src, bf16* dst, int64_t N, int K, hipStream_t s);
@@ -216,7 +250,7 @@ template <typename T>
 void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, const int32_t* cu,
                          const int32_t* h_cu, int H, hipStream_t s, const int32_t* ents = nullptr,
                          const int32_t* h_ents = nullptr, const int32_t* ent_slot = nullptr,
-                         const int32_t* ent_base = nullptr);
+                         const int32_t* ent_base = nullptr, float* lse = nullptr);
 // Decode attention: one query per slot at position len[b] (after the step's
 // key/value were written), context len[b] + 1; keys split over
 // plan_decode_splits() workgroups per (slot, kv head).  ``part`` holds

@@ -1,0 +1,89 @@
+"""The backward pass on the GPU against the float64 oracle.
+
+Loss and the gradient of every weight (embedding with the tied head, norm
+gains, q/k/v weights and biases back through RoPE and the grouped-row layout,
+O, the interleaved gate/up, down) for ragged batches with uncounted
+positions.  The GPU stores activations and gradients in bf16 between kernels
+(float32 accumulation, float32 residual stream and residual gradient): each
+such rounding has relative error 2^-9 ~ 2e-3, and a gradient passes through a
+handful of them (the head, two per layer), so its relative L2 error is a few
+1e-3; the bar is 3e-2 per tensor with cosine similarity >= 0.999, and 2e-3 on
+the loss (about 8 here).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from parity_util import gpu_model, pack
+from synthetic import model_weights, prompts, small_shape
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # tied head, head_dim 64, group 4
+    "llama_hd64_tied": ("1b", dict(layers=2, vocab=3000, hidden=512, intermediate=1024), [37, 130, 65, 5]),
+    # untied head, q/k/v biases, head_dim 128, group 7
+    "qwen_hd128_bias": ("7b", dict(layers=2, vocab=2048, hidden=896, intermediate=1792), [100, 33, 71]),
+}
+
+
+def _targets(seqs, vocab, seed):
+    r = np.random.default_rng(seed)
+    out = []
+    for s in seqs:
+        t = np.append(s[1:], -1).astype(np.int64)
+        t[r.random(len(t)) < 0.1] = -1  # some positions are not counted
+        out.append(t)
+    return out
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_loss_and_grads_against_oracle(case):
+    base, ov, lens = CASES[case]
+    shape = small_shape(base, **ov)
+    w = model_weights(shape, seed=71)
+    ids = prompts(len(lens), max(lens), shape["vocab_size"], seed=72).numpy()
+    seqs = [ids[i, :n] for i, n in enumerate(lens)]
+    tg = _targets(seqs, shape["vocab_size"], seed=73)
+    ref_loss, ref = oracle.loss_and_grads(shape, oracle.weights_f64(w), seqs, tg)
+    m = gpu_model(shape, w, max_batch=len(lens), max_seq=max(lens))
+    flat, cu = pack(seqs)
+    targets = torch.as_tensor(np.concatenate(tg).astype(np.int32)).to("cuda")
+    grads = {k: torch.full(tuple(v.shape), float("nan"), dtype=torch.float32, device="cuda") for k, v in w.items()}
+    loss = m.loss_and_grads(flat, cu, targets, grads)
+    torch.cuda.synchronize()
+    got = float(loss.item())
+    print(f"{case}: loss {got:.6f} vs oracle {ref_loss:.6f}")
+    assert abs(got - ref_loss) < 2e-3
+    worst, worst_name = 0.0, ""
+    for name, r in ref.items():
+        g = grads[name].cpu().double().numpy()
+        assert np.all(np.isfinite(g)), name
+        rel = np.linalg.norm(g - r) / np.linalg.norm(r)
+        cos = float(np.sum(g * r) / (np.linalg.norm(g) * np.linalg.norm(r)))
+        if rel > worst:
+            worst, worst_name = rel, name
+        assert rel < 3e-2 and cos > 0.999, (name, rel, cos)
+    print(f"{case}: largest relative L2 gradient error {worst:.3e} ({worst_name})")
+    # a second call on another batch overwrites every gradient
+    loss2 = m.loss_and_grads(*pack(seqs[:2]), targets[:sum(lens[:2])], grads)
+    ref_loss2, ref2 = oracle.loss_and_grads(shape, oracle.weights_f64(w), seqs[:2], tg[:2])
+    torch.cuda.synchronize()
+    assert abs(float(loss2.item()) - ref_loss2) < 2e-3
+    n = "model.layers.1.mlp.down_proj.weight"
+    r2 = ref2[n]
+    assert np.linalg.norm(grads[n].cpu().double().numpy() - r2) / np.linalg.norm(r2) < 3e-2
+    m.close()
+
+
+def test_backward_rejects_other_model_kinds():
+    from paper_2608_19889_amd import axon as ax
+    shape = dict(small_shape("1b", layers=1, vocab=500, hidden=256, intermediate=512), sliding_window=16)
+    w = model_weights(shape, seed=74)
+    m = gpu_model(shape, w, max_batch=1, max_seq=32)
+    flat, cu = pack([np.arange(8)])
+    grads = {k: torch.zeros(tuple(v.shape), dtype=torch.float32, device="cuda") for k, v in w.items()}
+    with pytest.raises(ax.AxonError, match="backward pass covers"):
+        m.loss_and_grads(flat, cu, flat.clone(), grads)
+    m.close()
