@@ -50,7 +50,7 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="1b", choices=["1b", "7b", "135m", "7b_paged", "32b", "7b_serve", "moe16b",
-                                                         "gpt2xl", "mistral7b"])
+                                                         "gpt2xl", "mistral7b", "1b_train"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=None,
@@ -80,6 +80,8 @@ def main():
 
     wl = dict(WORKLOADS[args.workload])
     shape = MODEL_SHAPES[wl["model"]]
+    if wl.get("train"):
+        return train_bench(args, wl, shape)
     esz = 2 if shape["dtype"] == "bf16" else 4
     B, steps = wl["batch"], wl["steps"] if args.decode_steps is None else args.decode_steps
     L, D, V = shape["num_hidden_layers"], shape["hidden_size"], shape["vocab_size"]
@@ -240,6 +242,120 @@ def main():
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, wl, lens, steps, B)
+    print(json.dumps(out), flush=True)
+
+
+def train_bench(args, wl, shape):
+    """One training step per timed step: the forward pass keeping its
+    activations, the mean next-token cross-entropy and every weight's
+    gradient (axon_loss_and_grads) over batch x prompt_len synthetic tokens."""
+    import numpy as np
+    import torch
+
+    from paper_2608_19889_amd import axon as ax
+    from synthetic import model_weights, prompts
+    dev = "cuda"
+    torch.cuda.set_device(0)
+    B, P = wl["batch"], wl["prompt_len"]
+    V, D, L = shape["vocab_size"], shape["hidden_size"], shape["num_hidden_layers"]
+    H, hd = shape["num_attention_heads"], shape["head_dim"]
+    t0 = time.time()
+    w = model_weights(shape, seed=0, device=dev)
+    ids = prompts(B, P, V, seed=0)
+    flat = ids.reshape(-1).to(dev)
+    tg = torch.cat([ids[:, 1:], torch.full((B, 1), -1, dtype=ids.dtype)], 1).reshape(-1).to(dev)
+    cu = [b * P for b in range(B + 1)]
+    T = B * P
+    m = ax.Model(shape, w, max_batch=B, max_seq=P, max_tokens=T)
+    grads = {k: torch.empty(tuple(v.shape), dtype=torch.float32, device=dev) for k, v in w.items()}
+    loss = torch.empty((1,), dtype=torch.float32, device=dev)
+    log(f"[bench] model + inputs ready in {time.time() - t0:.1f}s (weights {weight_bytes(shape, 2) / 1e9:.2f} GB, "
+        f"{T} training tokens)")
+
+    def step():
+        m.loss_and_grads(flat, cu, tg, grads, loss=loss)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done (loss {loss.item():.4f})")
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_start = time.perf_counter()
+    e0.record()
+    for i in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms = wall * 1e3 / args.steps
+    log(f"[bench] {args.steps} steps: {ms:.2f} ms per step (events {e0.elapsed_time(e1) / args.steps:.2f} ms), "
+        f"loss {loss.item():.4f}")
+    # algorithmic FLOPs of a step: 6 x (matmul parameters) per token (forward
+    # 2, backward 4), attention 4 hd per (query, key, head) forward and 10 hd
+    # backward (probabilities recomputed)
+    mm = 0
+    for n, shp in w.items():
+        if len(shp) == 2 and n != "model.embed_tokens.weight":
+            mm += shp[0] * shp[1]
+    if shape["tie_word_embeddings"]:
+        mm += V * D
+    pairs = B * P * (P + 1) / 2
+    flops = 6.0 * mm * T + 14.0 * hd * H * pairs * L
+    out = {
+        "metric": "training tokens/s (forward + next-token cross-entropy + every weight's gradient)",
+        "value": round(T / (ms / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (random-init N(0,0.02) weights, uniform random token ids, next-token targets)",
+        "config": {"workload": f"{wl['model']}-shaped decoder training step: batch {B} x {P} tokens",
+                   "batch": B, "seq_len": P, "tokens": T, "layers": L, "hidden": D, "vocab": V},
+        "loss": round(float(loss.item()), 5),
+        "step_tflops": round(flops / (ms / 1e3) / 1e12, 1),
+    }
+    if not args.no_roofline:
+        m.timing(True)
+        step()
+        torch.cuda.synchronize()
+        recs = m.timing_records()
+        m.timing(False)
+        agg = {}
+        for c, (d0, d1, d2), t_ms in recs:
+            a = agg.setdefault(c, {"ms": 0.0, "n": 0, "flops": 0.0})
+            a["ms"] += t_ms
+            a["n"] += 1
+            if c == ax.T_GEMM:
+                a["flops"] += 2.0 * d0 * d1 * d2
+        if ax.T_ATTN_PREFILL in agg:
+            agg[ax.T_ATTN_PREFILL]["flops"] = 4.0 * H * hd * pairs * L
+        if ax.T_ATTN_BWD in agg:
+            agg[ax.T_ATTN_BWD]["flops"] = 10.0 * H * hd * pairs * L
+        names = {ax.T_GEMM: ("forward and backward projection GEMMs (MFMA)", "mfma", BF16_PEAK_TFLOPS),
+                 ax.T_ATTN_PREFILL: ("forward flash attention (MFMA)", "mfma", BF16_PEAK_TFLOPS),
+                 ax.T_ATTN_BWD: ("attention backward (MFMA)", "mfma", BF16_PEAK_TFLOPS)}
+        kernels = {}
+        for c, a in agg.items():
+            if c not in names:
+                continue
+            nm, bound, peak = names[c]
+            ach = a["flops"] / (a["ms"] / 1e3) / 1e12
+            kernels[nm] = {"bound": bound, "achieved": round(ach, 1), "peak": peak, "unit": "TFLOP/s",
+                           "frac": round(ach / peak, 4), "launches": a["n"], "total_ms": round(a["ms"], 3),
+                           "avg_us": round(1e3 * a["ms"] / a["n"], 2)}
+        dom = max((c for c in agg if c in names), key=lambda c: agg[c]["ms"])
+        r = dict(kernels[names[dom][0]])
+        r["kernel"] = names[dom][0]
+        r["traffic"] = None
+        out["roofline"] = r
+        out["kernels"] = kernels
+    m.close()
     print(json.dumps(out), flush=True)
 
 

@@ -263,7 +263,8 @@ int axon_slot_lengths(const axon_model* m, int32_t* lens, int32_t n);
  *   3 = prefill attention,
  *   4 = grouped expert projection of a mixture-of-experts decode step (dims
  *       as class 0 with N, K of one expert and M the step's tokens; the
- *       launch streams the weights of every expert that some token chose)
+ *       launch streams the weights of every expert that some token chose),
+ *   5 = attention backward of a training step (dims: heads, sequences, tokens)
  * is bracketed by two HIP events recorded on the stream it is launched on, and
  * decode steps run eagerly instead of as a recorded graph (kernel durations
  * are unchanged; only launch gaps differ).  Enabling (1) or disabling (0)

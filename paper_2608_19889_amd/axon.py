@@ -34,7 +34,7 @@ EXPORTED = ["axon_init_model", "axon_prefill", "axon_decode_step", "axon_step", 
             "axon_slot_lengths", "axon_timing_enable", "axon_timing_records", "axon_free", "axon_last_error"]
 
 # kernel classes of the timing records
-T_GEMV, T_GEMM, T_ATTN_DECODE, T_ATTN_PREFILL, T_GEMV_GROUPED = 0, 1, 2, 3, 4
+T_GEMV, T_GEMM, T_ATTN_DECODE, T_ATTN_PREFILL, T_GEMV_GROUPED, T_ATTN_BWD = 0, 1, 2, 3, 4, 5
 
 
 class AxonConfig(ctypes.Structure):

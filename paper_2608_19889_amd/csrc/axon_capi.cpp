@@ -211,6 +211,9 @@ struct TrainLayer {
 struct TrainBufs {
   bool ready = false;
   int Tc = 0, Tp = 0, Vp = 0;
+  int SP = 0;       // positions per sequence in the attention backward's packed copies
+  int64_t W = 0;    // max_batch * SP
+  bf16 *kr, *vr, *kt, *qt, *dot;
   std::vector<TrainLayer> L;
   float *xfin, *logits, *rowloss, *valid, *lserow, *scal, *dx, *dtmp, *dgrow, *dqf, *dkf, *dvf, *dsum, *dqkvf,
       *colpart, *gtmp;
@@ -1598,7 +1601,17 @@ int train_setup(axon_model* m, hipStream_t s) {
   if (!r) r = ba(&tb.trs, maxK * Tp);
   if (!r) r = ba(&tb.trb, tiled(maxK, Tp));
   if (!r) r = ba(&tb.headT, tiled(D, Vp));
+  tb.SP = (c.max_seq + 31) / 32 * 32 + 32;
+  tb.W = (int64_t)c.max_batch * tb.SP;
+  if (!r) r = ba(&tb.kr, tb.W * KV * hd);
+  if (!r) r = ba(&tb.vr, tb.W * KV * hd);
+  if (!r) r = ba(&tb.kt, tb.W * KV * hd);
+  if (!r) r = ba(&tb.qt, tb.W * Hhd);
+  if (!r) r = ba(&tb.dot, tb.W * Hhd);
   if (r) return r;
+  // the packed copies' padding is read (masked) past each sequence's end: finite from the start
+  for (bf16* p : {tb.kr, tb.vr, tb.kt}) (void)hipMemsetAsync(p, 0, (size_t)tb.W * KV * hd * 2, s);
+  for (bf16* p : {tb.qt, tb.dot}) (void)hipMemsetAsync(p, 0, (size_t)tb.W * Hhd * 2, s);
   // W [N][K] (tiled) -> W^T [K][Np] tiled, through a row-major staging copy
   // whose columns N .. Np-1 are zero
   bf16* stage = nullptr;
@@ -1656,7 +1669,9 @@ void enqueue_train(axon_model* m, int B, int T, const int32_t* d_tokens, const i
     EpiArgs re = rope_epi(m, w, kv, d_cu, B, nullptr);
     re.q_out = t.q;
     gemm_many<bf16>(m, w.wqkv, t.h1, nq, T, D, EPI_ROPE, nullptr, nullptr, nq, s, &re);
-    launch_attn_prefill<bf16>(t.q, kv, t.o, T, B, d_cu, h_cu, H, s, nullptr, nullptr, nullptr, nullptr, t.lse);
+    m->timed(3, H, B, T, s, [&] {
+      launch_attn_prefill<bf16>(t.q, kv, t.o, T, B, d_cu, h_cu, H, s, nullptr, nullptr, nullptr, nullptr, t.lse);
+    });
     gemm_many<bf16>(m, w.wo, t.o, D, T, Hhd, EPI_RESID, m->x, nullptr, D, s);
     (void)hipMemcpyAsync(t.xmid, m->x, (size_t)T * D * 4, hipMemcpyDeviceToDevice, s);
     launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, (const bf16*)w.gpost, t.h2, T, D, eps, nullptr, s);
@@ -1711,7 +1726,10 @@ void enqueue_train(axon_model* m, int B, int T, const int32_t* d_tokens, const i
     dW(tb.dxb, D, D, t.o, Hhd, G(p + "self_attn.o_proj.weight"));
     dX(t.woT, tb.dxb, D, Hhd, tb.dtmp);
     launch_to_bf16(tb.dtmp, tb.dob, (int64_t)T * Hhd, s);
-    launch_attn_bwd(t.q, kv, t.o, tb.dob, t.lse, tb.dsum, d_cu, B, T, H, tb.dqf, tb.dkf, tb.dvf, s);
+    m->timed(5, H, B, T, s, [&] {
+      launch_attn_bwd(t.q, kv, t.o, tb.dob, t.lse, tb.dsum, d_cu, h_cu, B, T, H, tb.SP, tb.W, tb.kr, tb.vr, tb.kt,
+                      tb.qt, tb.dot, tb.dqf, tb.dkf, tb.dvf, s);
+    });
     launch_rope_bwd(tb.dqf, tb.dkf, tb.dvf, m->rope_cos, m->rope_sin, d_cu, B, T, H, KV, hd, tb.dqkv,
                     c.qkv_bias ? tb.dqkvf : nullptr, s);
     dW(tb.dqkv, nq, nq, t.h1, D, tb.gtmp);

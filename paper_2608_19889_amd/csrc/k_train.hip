@@ -13,10 +13,11 @@
 // Attention backward recomputes the probabilities from the forward pass's
 // per-(query, head) log2-sum-exp: P = 2^(s sc - lse) with sc = log2(e) /
 // sqrt(hd); dP = dO V^T; dS = P (dP - D) with D = rowsum(dO O); dQ = dS K /
-// sqrt(hd); dK = dS^T Q / sqrt(hd); dV = P^T dO.  One wavefront per (query,
-// head) accumulates dQ over the query's keys; one per (key, kv head)
-// accumulates dK and dV over the later queries of every head of its group.
-// No atomics, so every gradient but the embedding's is deterministic.
+// sqrt(hd); dK = dS^T Q / sqrt(hd); dV = P^T dO, all on the matrix cores.
+// One wavefront per 32-query block and head accumulates dQ over the keys; one
+// per 32-key block and kv head accumulates dK and dV over the later queries of
+// every head of its group.  No atomics, so every gradient but the
+// embedding's is deterministic.
 #include <algorithm>
 
 #include "common.h"
@@ -228,134 +229,205 @@ __global__ void __launch_bounds__(256) attn_bwd_d_kernel(const bf16* __restrict_
   dsum[i] = s;
 }
 
-// dQ of query token t (sequence e = slot e, position t - cu[e]) and head:
-// lane = key for the scores, lane = head dimension for the accumulation
-template <int HD>
-__global__ void __launch_bounds__(64) attn_bwd_dq_kernel(const bf16* __restrict__ q, KVView kv,
-                                                         const bf16* __restrict__ dob, const float* __restrict__ lse,
-                                                         const float* __restrict__ dsum,
-                                                         const int32_t* __restrict__ cu, int nseq, int H,
-                                                         float* __restrict__ dq) {
-  constexpr int DL = HD / 64;
-  __shared__ float qs[HD], dos[HD], ps[64];
-  const int t = blockIdx.x, head = blockIdx.y, lane = threadIdx.x;
+// ---- MFMA attention backward.  v_mfma_f32_32x32x16_bf16 with lane L, half
+// hl = L / 32, column c = L % 32: A operand = row c, k = 8 hl .. 8 hl + 7;
+// B operand = column c, the same k; accumulator element i = row (i/4)*8 +
+// 4 hl + i%4, column c.  The accumulator of a 32 x 32 block therefore holds,
+// per lane, 16 rows of one column: taken 8 at a time (k-steps kk = 0, 1) it
+// is directly a B operand whose k slot (hl, j) stands for row kk*16 +
+// kap(hl, j), kap(hl, j) = (j/4)*8 + 4 hl + j%4, and the A operand of that
+// product reads its rows in the same order: two runs of 4 consecutive
+// positions, which the transposed copies (positions contiguous) serve as two
+// 8-byte reads.
+//
+// Packed copies, per sequence e at columns / rows e*SP + position (SP = the
+// longest sequence rounded up to 32, plus 32 positions of finite padding, so
+// a block's reads past its sequence end stay inside the sequence's range):
+//   kr, vr [B*SP][KV][hd]  K and V rows      qt, dot [H*hd][B*SP]  Q^T, dO^T
+//   kt [KV*hd][B*SP]       K^T
+
+// pack the layer's K / V (from the cache) and Q / dO into the copies above;
+// grid (token, head), one thread per head dimension
+__global__ void __launch_bounds__(128) attn_bwd_pack_kernel(const bf16* __restrict__ q, const bf16* __restrict__ dob,
+                                                            KVView kv, const int32_t* __restrict__ cu, int nseq,
+                                                            int H, int SP, int64_t W, bf16* __restrict__ kr,
+                                                            bf16* __restrict__ vr, bf16* __restrict__ kt,
+                                                            bf16* __restrict__ qt, bf16* __restrict__ dot) {
+  const int t = blockIdx.x, h = blockIdx.y, d = threadIdx.x, hd = kv.hd, KVh = kv.kv_heads;
+  if (d >= hd) return;
   const int e = seq_of_token(cu, nseq, t);
-  const int pos = t - cu[e];
-  const int kvh = head / (H / kv.kv_heads);
-  const int64_t row = ((int64_t)t * H + head) * HD;
-  for (int d = lane; d < HD; d += 64) {
-    qs[d] = (float)q[row + d];
-    dos[d] = (float)dob[row + d];
+  const int p = t - cu[e];
+  const int64_t col = (int64_t)e * SP + p;
+  qt[((int64_t)h * hd + d) * W + col] = q[((int64_t)t * H + h) * hd + d];
+  dot[((int64_t)h * hd + d) * W + col] = dob[((int64_t)t * H + h) * hd + d];
+  if (h < KVh) {
+    const bf16 kv_k = ((const bf16*)kv.k)[k_el(kv, e, h, p, d)];
+    kr[(col * KVh + h) * hd + d] = kv_k;
+    vr[(col * KVh + h) * hd + d] = ((const bf16*)kv.v)[v_el(kv, e, h, p, d)];
+    kt[((int64_t)h * hd + d) * W + col] = kv_k;
   }
-  __syncthreads();
-  const float sc = LOG2E / sqrtf((float)HD);
-  const float l2 = lse[(int64_t)t * H + head], Di = dsum[(int64_t)t * H + head];
-  const bf16* kb = (const bf16*)kv.k;
-  const bf16* vb = (const bf16*)kv.v;
-  float acc[DL] = {};
-  for (int j0 = 0; j0 <= pos; j0 += 64) {
-    const int j = j0 + lane;
-    float ds = 0.f;
-    if (j <= pos) {
-      const int64_t kbase = k_el(kv, e, kvh, j, 0), vbase = v_el(kv, e, kvh, j, 0);
-      float s = 0.f, dp = 0.f;
-      for (int d = 0; d < HD; d += 8) {
-        const bf16x8 k8 = *(const bf16x8*)(kb + kbase + (d >> 3) * 128);
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          s = fmaf(qs[d + c], (float)k8[c], s);
-          dp = fmaf(dos[d + c], (float)vb[vbase + (d + c) * 16], dp);
-        }
-      }
-      ds = exp2f(s * sc - l2) * (dp - Di);
-    }
-    ps[lane] = ds;
-    __syncthreads();
-    const int nj = min(64, pos + 1 - j0);
-    for (int jj = 0; jj < nj; ++jj) {
-      const int64_t kbase = k_el(kv, e, kvh, j0 + jj, 0);
-#pragma unroll
-      for (int i = 0; i < DL; ++i) {
-        const int d = lane + i * 64;
-        acc[i] = fmaf(ps[jj], (float)kb[kbase + (d >> 3) * 128 + (d & 7)], acc[i]);
-      }
-    }
-    __syncthreads();
-  }
-  const float rs = 1.f / sqrtf((float)HD);
-#pragma unroll
-  for (int i = 0; i < DL; ++i) dq[row + lane + i * 64] = acc[i] * rs;
 }
 
-// dK and dV of key token j (sequence e, position j - cu[e]) and kv head: over
-// the queries of the sequence at positions >= the key's, for every query head
-// of the group (lane = query for the scores, lane = head dimension for the
-// accumulation)
+AXON_DEV int kap(int hl, int j) { return (j >> 2) * 8 + hl * 4 + (j & 3); }
+
+// the 32-position block blockIdx.x of the sequences in order: (sequence, first position)
+AXON_DEV void locate_block(const int32_t* __restrict__ cu, int nseq, int& e, int& p0) {
+  int blk = blockIdx.x;
+  for (e = 0; e < nseq - 1; ++e) {
+    const int nb = (cu[e + 1] - cu[e] + 31) / 32;
+    if (blk < nb) break;
+    blk -= nb;
+  }
+  p0 = blk * 32;
+}
+
+// dQ of 32 queries (one head): over the key blocks up to the last query,
+// S^T = K Q^T and dP^T = V dO^T (k = head dim), then dQ^T += K^T dS^T (k =
+// the block's 32 keys).  One wavefront per workgroup; no LDS.
 template <int HD>
-__global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict__ q, KVView kv,
-                                                          const bf16* __restrict__ dob,
+__global__ void __launch_bounds__(64) attn_bwd_dq_kernel(const bf16* __restrict__ q, const bf16* __restrict__ dob,
+                                                         const bf16* __restrict__ kr, const bf16* __restrict__ vr,
+                                                         const bf16* __restrict__ kt, const float* __restrict__ lse,
+                                                         const float* __restrict__ dsum,
+                                                         const int32_t* __restrict__ cu, int nseq, int H, int KVh,
+                                                         int SP, int64_t W, float* __restrict__ dq) {
+  int e, q0;
+  locate_block(cu, nseq, e, q0);
+  const int h = blockIdx.y, kvh = h / (H / KVh);
+  const int tok0 = cu[e], S = cu[e + 1] - tok0;
+  const int lane = threadIdx.x, hl = lane >> 5, c = lane & 31;
+  const int myq = q0 + c;
+  const int64_t tq = tok0 + min(myq, S - 1);  // columns past the sequence read its last query (not stored)
+  bf16x8 qf[HD / 16], df[HD / 16];
+#pragma unroll
+  for (int s = 0; s < HD / 16; ++s) {
+    qf[s] = *(const bf16x8*)(q + (tq * H + h) * HD + s * 16 + hl * 8);
+    df[s] = *(const bf16x8*)(dob + (tq * H + h) * HD + s * 16 + hl * 8);
+  }
+  const float sc = LOG2E / sqrtf((float)HD);
+  const float l2 = lse[tq * H + h], Dq = dsum[tq * H + h];
+  f32x16 acc[HD / 32];
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b) acc[b] = f32x16{};
+  const int kend = min(S, q0 + 32);
+  for (int kb0 = 0; kb0 < kend; kb0 += 32) {
+    f32x16 st = {}, dpt = {};
+    const int64_t krow = (((int64_t)e * SP + kb0 + c) * KVh + kvh) * HD + hl * 8;
+#pragma unroll
+    for (int s = 0; s < HD / 16; ++s) {
+      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(kr + krow + s * 16), qf[s], st, 0, 0, 0);
+      dpt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(vr + krow + s * 16), df[s], dpt, 0, 0, 0);
+    }
+    bf16x8 dsb[2];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int key = kb0 + (i >> 2) * 8 + hl * 4 + (i & 3);
+      const float p = (key <= myq && myq < S) ? exp2f(st[i] * sc - l2) : 0.f;
+      dsb[i >> 3][i & 7] = (bf16)(p * (dpt[i] - Dq));
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int b = 0; b < HD / 32; ++b) {
+        const bf16* ktr = kt + ((int64_t)kvh * HD + b * 32 + c) * W + (int64_t)e * SP + kb0 + kk * 16 + hl * 4;
+        const bf16x4 lo = *(const bf16x4*)ktr, hi = *(const bf16x4*)(ktr + 8);
+        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[kk], acc[b], 0, 0, 0);
+      }
+  }
+  if (myq >= S) return;
+  const float rs = 1.f / sqrtf((float)HD);
+  float* out = dq + ((int64_t)(tok0 + myq) * H + h) * HD;
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int d = b * 32 + g * 8 + hl * 4;
+      *(f32x4*)(out + d) = f32x4{acc[b][g * 4] * rs, acc[b][g * 4 + 1] * rs, acc[b][g * 4 + 2] * rs,
+                                 acc[b][g * 4 + 3] * rs};
+    }
+}
+
+// dK and dV of 32 keys (one kv head): over the group's heads and the query
+// blocks from the key block on, S = Q K^T and dP = dO V^T (k = head dim),
+// then dV^T += dO^T P and dK^T += Q^T dS (k = the block's 32 queries).
+template <int HD>
+__global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict__ q, const bf16* __restrict__ dob,
+                                                          const bf16* __restrict__ kr, const bf16* __restrict__ vr,
+                                                          const bf16* __restrict__ qt, const bf16* __restrict__ dot,
                                                           const float* __restrict__ lse,
                                                           const float* __restrict__ dsum,
-                                                          const int32_t* __restrict__ cu, int nseq, int H,
-                                                          float* __restrict__ dk, float* __restrict__ dv) {
-  constexpr int DL = HD / 64;
-  __shared__ float ks[HD], vs[HD], ps[64], dss[64];
-  const int j = blockIdx.x, kvh = blockIdx.y, lane = threadIdx.x;
-  const int e = seq_of_token(cu, nseq, j);
-  const int tok0 = cu[e], S = cu[e + 1] - tok0, posj = j - tok0;
-  const int group = H / kv.kv_heads;
-  const bf16* kb = (const bf16*)kv.k;
-  const bf16* vb = (const bf16*)kv.v;
-  for (int d = lane; d < HD; d += 64) {
-    ks[d] = (float)kb[k_el(kv, e, kvh, posj, d)];
-    vs[d] = (float)vb[v_el(kv, e, kvh, posj, d)];
+                                                          const int32_t* __restrict__ cu, int nseq, int H, int KVh,
+                                                          int SP, int64_t W, float* __restrict__ dk,
+                                                          float* __restrict__ dv) {
+  int e, kb0;
+  locate_block(cu, nseq, e, kb0);
+  const int kvh = blockIdx.y, group = H / KVh;
+  const int tok0 = cu[e], S = cu[e + 1] - tok0;
+  const int lane = threadIdx.x, hl = lane >> 5, c = lane & 31;
+  const int mykey = kb0 + c;
+  bf16x8 kf[HD / 16], vf[HD / 16];
+  const int64_t krow = (((int64_t)e * SP + mykey) * KVh + kvh) * HD + hl * 8;  // padded rows past the sequence
+#pragma unroll
+  for (int s = 0; s < HD / 16; ++s) {
+    kf[s] = *(const bf16x8*)(kr + krow + s * 16);
+    vf[s] = *(const bf16x8*)(vr + krow + s * 16);
   }
-  __syncthreads();
   const float sc = LOG2E / sqrtf((float)HD);
-  float akk[DL] = {}, avv[DL] = {};
+  f32x16 akk[HD / 32], avv[HD / 32];
+#pragma unroll
+  for (int b = 0; b < HD / 32; ++b) {
+    akk[b] = f32x16{};
+    avv[b] = f32x16{};
+  }
   for (int hh = 0; hh < group; ++hh) {
-    const int head = kvh * group + hh;
-    for (int i0 = posj; i0 < S; i0 += 64) {
-      const int i = i0 + lane;
-      float p = 0.f, ds = 0.f;
-      if (i < S) {
-        const int64_t row = ((int64_t)(tok0 + i) * H + head) * HD;
-        float s = 0.f, dp = 0.f;
-        for (int d = 0; d < HD; d += 8) {
-          const bf16x8 q8 = *(const bf16x8*)(q + row + d), o8 = *(const bf16x8*)(dob + row + d);
+    const int h = kvh * group + hh;
+    for (int qb0 = kb0; qb0 < S; qb0 += 32) {
+      const int64_t tq = tok0 + min(qb0 + c, S - 1);  // rows past the sequence read its last query
+      f32x16 sq = {}, dpq = {};
 #pragma unroll
-          for (int c = 0; c < 8; ++c) {
-            s = fmaf((float)q8[c], ks[d + c], s);
-            dp = fmaf((float)o8[c], vs[d + c], dp);
-          }
-        }
-        const int64_t th = (int64_t)(tok0 + i) * H + head;
-        p = exp2f(s * sc - lse[th]);
-        ds = p * (dp - dsum[th]);
+      for (int s = 0; s < HD / 16; ++s) {
+        sq = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(q + (tq * H + h) * HD + s * 16 + hl * 8), kf[s],
+                                                     sq, 0, 0, 0);
+        dpq = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(dob + (tq * H + h) * HD + s * 16 + hl * 8),
+                                                      vf[s], dpq, 0, 0, 0);
       }
-      ps[lane] = p;
-      dss[lane] = ds;
-      __syncthreads();
-      const int ni = min(64, S - i0);
-      for (int ii = 0; ii < ni; ++ii) {
-        const int64_t row = ((int64_t)(tok0 + i0 + ii) * H + head) * HD;
+      bf16x8 pb[2], dsb[2];
 #pragma unroll
-        for (int c = 0; c < DL; ++c) {
-          const int d = lane + c * 64;
-          avv[c] = fmaf(ps[ii], (float)dob[row + d], avv[c]);
-          akk[c] = fmaf(dss[ii], (float)q[row + d], akk[c]);
-        }
+      for (int i = 0; i < 16; ++i) {
+        const int qi = qb0 + (i >> 2) * 8 + hl * 4 + (i & 3);
+        const int64_t ti = tok0 + min(qi, S - 1);
+        const bool ok = qi < S && mykey <= qi;
+        const float p = ok ? exp2f(sq[i] * sc - lse[ti * H + h]) : 0.f;
+        pb[i >> 3][i & 7] = (bf16)p;
+        dsb[i >> 3][i & 7] = (bf16)(p * (dpq[i] - dsum[ti * H + h]));
       }
-      __syncthreads();
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int b = 0; b < HD / 32; ++b) {
+          const int64_t off = ((int64_t)h * HD + b * 32 + c) * W + (int64_t)e * SP + qb0 + kk * 16 + hl * 4;
+          const bf16x4 olo = *(const bf16x4*)(dot + off), ohi = *(const bf16x4*)(dot + off + 8);
+          const bf16x4 qlo = *(const bf16x4*)(qt + off), qhi = *(const bf16x4*)(qt + off + 8);
+          const bf16x8 ao = {olo[0], olo[1], olo[2], olo[3], ohi[0], ohi[1], ohi[2], ohi[3]};
+          const bf16x8 aq = {qlo[0], qlo[1], qlo[2], qlo[3], qhi[0], qhi[1], qhi[2], qhi[3]};
+          avv[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ao, pb[kk], avv[b], 0, 0, 0);
+          akk[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, dsb[kk], akk[b], 0, 0, 0);
+        }
     }
   }
+  if (mykey >= S) return;
   const float rs = 1.f / sqrtf((float)HD);
-  const int64_t orow = ((int64_t)j * kv.kv_heads + kvh) * HD;
+  const int64_t orow = ((int64_t)(tok0 + mykey) * KVh + kvh) * HD;
 #pragma unroll
-  for (int c = 0; c < DL; ++c) {
-    dk[orow + lane + c * 64] = akk[c] * rs;
-    dv[orow + lane + c * 64] = avv[c];
-  }
+  for (int b = 0; b < HD / 32; ++b)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int d = b * 32 + g * 8 + hl * 4;
+      *(f32x4*)(dk + orow + d) = f32x4{akk[b][g * 4] * rs, akk[b][g * 4 + 1] * rs, akk[b][g * 4 + 2] * rs,
+                                       akk[b][g * 4 + 3] * rs};
+      *(f32x4*)(dv + orow + d) = f32x4{avv[b][g * 4], avv[b][g * 4 + 1], avv[b][g * 4 + 2], avv[b][g * 4 + 3]};
+    }
 }
 
 // Gradients at the rotated q / k and at v back through RoPE (the transpose of
@@ -472,15 +544,23 @@ void launch_colsum(const float* src, int64_t ld, int T, int C, float* part, floa
 }
 
 void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
-                     const int32_t* cu, int nseq, int T, int H, float* dq, float* dk, float* dv, hipStream_t s) {
+                     const int32_t* cu, const int32_t* h_cu, int nseq, int T, int H, int SP, int64_t W,
+                     bf16* kr, bf16* vr, bf16* kt, bf16* qt, bf16* dot, float* dq, float* dk, float* dv,
+                     hipStream_t s) {
   if (T <= 0) return;
   attn_bwd_d_kernel<<<(T * H + 255) / 256, 256, 0, s>>>(dob, o, T * H, kv.hd, dsum);
+  attn_bwd_pack_kernel<<<dim3(T, H), 128, 0, s>>>(q, dob, kv, cu, nseq, H, SP, W, kr, vr, kt, qt, dot);
+  int blocks = 0;
+  for (int e = 0; e < nseq; ++e) blocks += (h_cu[e + 1] - h_cu[e] + 31) / 32;
+  const int KVh = kv.kv_heads;
   if (kv.hd == 64) {
-    attn_bwd_dq_kernel<64><<<dim3(T, H), 64, 0, s>>>(q, kv, dob, lse, dsum, cu, nseq, H, dq);
-    attn_bwd_dkv_kernel<64><<<dim3(T, kv.kv_heads), 64, 0, s>>>(q, kv, dob, lse, dsum, cu, nseq, H, dk, dv);
+    attn_bwd_dq_kernel<64><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, kt, lse, dsum, cu, nseq, H, KVh, SP, W, dq);
+    attn_bwd_dkv_kernel<64><<<dim3(blocks, KVh), 64, 0, s>>>(q, dob, kr, vr, qt, dot, lse, dsum, cu, nseq, H, KVh,
+                                                             SP, W, dk, dv);
   } else {
-    attn_bwd_dq_kernel<128><<<dim3(T, H), 64, 0, s>>>(q, kv, dob, lse, dsum, cu, nseq, H, dq);
-    attn_bwd_dkv_kernel<128><<<dim3(T, kv.kv_heads), 64, 0, s>>>(q, kv, dob, lse, dsum, cu, nseq, H, dk, dv);
+    attn_bwd_dq_kernel<128><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, kt, lse, dsum, cu, nseq, H, KVh, SP, W, dq);
+    attn_bwd_dkv_kernel<128><<<dim3(blocks, KVh), 64, 0, s>>>(q, dob, kr, vr, qt, dot, lse, dsum, cu, nseq, H, KVh,
+                                                              SP, W, dk, dv);
   }
 }
 

@@ -109,9 +109,14 @@ int colsum_chunks(int T);
 void launch_colsum(const float* src, int64_t ld, int T, int C, float* part, float* dst, hipStream_t s);
 // attention backward over nseq fresh sequences in slots 0.. (contiguous cache):
 // dq [T][H][hd], dk / dv [T][KV][hd] (float), from q / o / dO [T][H][hd] bf16,
-// the forward's log2-sum-exp lse [T][H]; dsum [T][H] scratch
+// the forward's log2-sum-exp lse [T][H]; dsum [T][H] scratch.  Packed copies
+// (scratch, finite at allocation): kr / vr [nseq*SP][KV][hd], kt [KV*hd][W],
+// qt / dot [H*hd][W], W >= nseq*SP, SP >= the longest sequence rounded up to
+// 32, plus 32
 void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
-                     const int32_t* cu, int nseq, int T, int H, float* dq, float* dk, float* dv, hipStream_t s);
+                     const int32_t* cu, const int32_t* h_cu, int nseq, int T, int H, int SP, int64_t W,
+                     bf16* kr, bf16* vr, bf16* kt, bf16* qt, bf16* dot, float* dq, float* dk, float* dv,
+                     hipStream_t s);
 // back through RoPE into the fused QKV row order (bf16) and the original order
 // (float, may be null)
 void launch_rope_bwd(const float* dq, const float* dk, const float* dv, const float* cos_t, const float* sin_t,

@@ -89,6 +89,9 @@ WORKLOADS = {
     "32b": dict(model="32b", batch=32, prompt_len=1024, steps=256, paged=False),
     # the DeepSeek-MoE-16B shape: routed experts through grouped GEMMs
     "moe16b": dict(model="moe16b", batch=32, prompt_len=1024, steps=128, paged=False),
+    # a training step (forward, mean next-token cross-entropy, every weight's
+    # gradient) over the 1B workload's 8 x 512 prompts
+    "1b_train": dict(model="1b", batch=8, prompt_len=512, steps=0, paged=False, train=True),
     # GPT-2 XL (the largest checkpoint of the paper's GPT-2 listing), the 1B
     # workload's batch, prompt and decode lengths
     "gpt2xl": dict(model="gpt2xl", batch=8, prompt_len=512, steps=128, paged=False),
