@@ -216,7 +216,7 @@ struct TrainBufs {
   bf16 *kr, *vr, *kt, *qt, *dot;
   std::vector<TrainLayer> L;
   float *xfin, *logits, *rowloss, *valid, *lserow, *scal, *dx, *dtmp, *dgrow, *dqf, *dkf, *dvf, *dsum, *dqkvf,
-      *colpart, *gtmp;
+      *colpart, *gtmp, *dkh, *dvh;
   bf16 *hf, *dlog, *dxb, *dgu, *dob, *dqkv, *tra, *trs, *trb, *headT;
 };
 
@@ -1587,6 +1587,8 @@ int train_setup(axon_model* m, hipStream_t s) {
   if (!r) r = fa(&tb.dqf, T * Hhd);
   if (!r) r = fa(&tb.dkf, T * KV * hd);
   if (!r) r = fa(&tb.dvf, T * KV * hd);
+  if (!r) r = fa(&tb.dkh, T * Hhd);
+  if (!r) r = fa(&tb.dvh, T * Hhd);
   if (!r) r = fa(&tb.dsum, T * H);
   if (!r) r = fa(&tb.dqkvf, T * nq);
   if (!r) r = fa(&tb.colpart, (int64_t)colsum_chunks((int)T) * std::max(nq, D));
@@ -1728,7 +1730,7 @@ void enqueue_train(axon_model* m, int B, int T, const int32_t* d_tokens, const i
     launch_to_bf16(tb.dtmp, tb.dob, (int64_t)T * Hhd, s);
     m->timed(5, H, B, T, s, [&] {
       launch_attn_bwd(t.q, kv, t.o, tb.dob, t.lse, tb.dsum, d_cu, h_cu, B, T, H, tb.SP, tb.W, tb.kr, tb.vr, tb.kt,
-                      tb.qt, tb.dot, tb.dqf, tb.dkf, tb.dvf, s);
+                      tb.qt, tb.dot, tb.dqf, tb.dkh, tb.dvh, tb.dkf, tb.dvf, s);
     });
     launch_rope_bwd(tb.dqf, tb.dkf, tb.dvf, m->rope_cos, m->rope_sin, d_cu, B, T, H, KV, hd, tb.dqkv,
                     c.qkv_bias ? tb.dqkvf : nullptr, s);

@@ -15,9 +15,10 @@
 // sqrt(hd); dP = dO V^T; dS = P (dP - D) with D = rowsum(dO O); dQ = dS K /
 // sqrt(hd); dK = dS^T Q / sqrt(hd); dV = P^T dO, all on the matrix cores.
 // One wavefront per 32-query block and head accumulates dQ over the keys; one
-// per 32-key block and kv head accumulates dK and dV over the later queries of
-// every head of its group.  No atomics, so every gradient but the
-// embedding's is deterministic.
+// per 32-key block and query head accumulates that head's share of dK and dV
+// over the later queries, and the shares of a group's heads are summed in
+// order.  No atomics, so every gradient but the embedding's is
+// deterministic.
 #include <algorithm>
 
 #include "common.h"
@@ -111,16 +112,41 @@ __global__ void __launch_bounds__(256) ce_grad_kernel(const float* __restrict__ 
 
 // ---------------------------------------------------------------- layouts
 
-// dst[c][t] = src[t][c] for t < T, 0 for T <= t < Tp (bf16; src rows ld apart)
-__global__ void __launch_bounds__(256) transpose_pad_kernel(const bf16* __restrict__ src, int ld, int T, int C,
-                                                            bf16* __restrict__ dst, int Tp) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  const int t0 = blockIdx.y * 8;
-  if (c >= C) return;
-  bf16x8 v;
+// dst[c][col(t)] = src[t][c] through a 64 x 64 LDS tile, both sides
+// coalesced: rows t < T are read (rows T .. Tmax-1 give zeros), col(t) = t,
+// or with cu: e * SP + (t - cu[e]) for t's sequence e (t < T only).  C % 4
+// == 0, ld % 4 == 0.
+__global__ void __launch_bounds__(256) transpose_tile_kernel(const bf16* __restrict__ src, int64_t ld, int T, int Tmax,
+                                                             int C, bf16* __restrict__ dst, int64_t dld,
+                                                             const int32_t* __restrict__ cu, int nseq, int SP) {
+  __shared__ bf16 tile[64][66];
+  const int t0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) v[j] = t0 + j < T ? src[(int64_t)(t0 + j) * ld + c] : (bf16)0.f;
-  *(bf16x8*)(dst + (int64_t)c * Tp + t0) = v;
+  for (int r = 0; r < 4; ++r) {
+    const int t = t0 + ty + 16 * r, c = c0 + tx * 4;
+    bf16x4 v = {(bf16)0.f, (bf16)0.f, (bf16)0.f, (bf16)0.f};
+    if (t < T && c < C) v = *(const bf16x4*)(src + (int64_t)t * ld + c);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) tile[ty + 16 * r][tx * 4 + j] = v[j];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int c = c0 + ty + 16 * r;
+    if (c >= C) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = t0 + tx * 4 + j;
+      if (t >= (cu ? T : Tmax)) continue;
+      int64_t col = t;
+      if (cu) {
+        const int e = seq_of_token(cu, nseq, t);
+        col = (int64_t)e * SP + (t - cu[e]);
+      }
+      dst[(int64_t)c * dld + col] = tile[tx * 4 + j][ty + 16 * r];
+    }
+  }
 }
 
 // dst[k][n] = W[n][k] from the fragment-tiled W [N][K]; dst rows are Np
@@ -246,26 +272,17 @@ __global__ void __launch_bounds__(256) attn_bwd_d_kernel(const bf16* __restrict_
 //   kr, vr [B*SP][KV][hd]  K and V rows      qt, dot [H*hd][B*SP]  Q^T, dO^T
 //   kt [KV*hd][B*SP]       K^T
 
-// pack the layer's K / V (from the cache) and Q / dO into the copies above;
-// grid (token, head), one thread per head dimension
-__global__ void __launch_bounds__(128) attn_bwd_pack_kernel(const bf16* __restrict__ q, const bf16* __restrict__ dob,
-                                                            KVView kv, const int32_t* __restrict__ cu, int nseq,
-                                                            int H, int SP, int64_t W, bf16* __restrict__ kr,
-                                                            bf16* __restrict__ vr, bf16* __restrict__ kt,
-                                                            bf16* __restrict__ qt, bf16* __restrict__ dot) {
+// the layer's K / V rows from the cache into kr / vr (row e*SP + position);
+// grid (token, kv head), one thread per head dimension
+__global__ void __launch_bounds__(128) attn_bwd_pack_kernel(KVView kv, const int32_t* __restrict__ cu, int nseq,
+                                                            int SP, bf16* __restrict__ kr, bf16* __restrict__ vr) {
   const int t = blockIdx.x, h = blockIdx.y, d = threadIdx.x, hd = kv.hd, KVh = kv.kv_heads;
   if (d >= hd) return;
   const int e = seq_of_token(cu, nseq, t);
   const int p = t - cu[e];
   const int64_t col = (int64_t)e * SP + p;
-  qt[((int64_t)h * hd + d) * W + col] = q[((int64_t)t * H + h) * hd + d];
-  dot[((int64_t)h * hd + d) * W + col] = dob[((int64_t)t * H + h) * hd + d];
-  if (h < KVh) {
-    const bf16 kv_k = ((const bf16*)kv.k)[k_el(kv, e, h, p, d)];
-    kr[(col * KVh + h) * hd + d] = kv_k;
-    vr[(col * KVh + h) * hd + d] = ((const bf16*)kv.v)[v_el(kv, e, h, p, d)];
-    kt[((int64_t)h * hd + d) * W + col] = kv_k;
-  }
+  kr[(col * KVh + h) * hd + d] = ((const bf16*)kv.k)[k_el(kv, e, h, p, d)];
+  vr[(col * KVh + h) * hd + d] = ((const bf16*)kv.v)[v_el(kv, e, h, p, d)];
 }
 
 AXON_DEV int kap(int hl, int j) { return (j >> 2) * 8 + hl * 4 + (j & 3); }
@@ -348,9 +365,12 @@ __global__ void __launch_bounds__(64) attn_bwd_dq_kernel(const bf16* __restrict_
     }
 }
 
-// dK and dV of 32 keys (one kv head): over the group's heads and the query
-// blocks from the key block on, S = Q K^T and dP = dO V^T (k = head dim),
-// then dV^T += dO^T P and dK^T += Q^T dS (k = the block's 32 queries).
+// dK and dV of 32 keys from one query head h = blockIdx.y (kv head h / group):
+// over the query blocks from the key block on, S = Q K^T and dP = dO V^T (k =
+// head dim), then dV^T += dO^T P and dK^T += Q^T dS (k = the block's 32
+// queries).  Writes the head's share into dk / dv [T][H][hd] (the heads of a
+// group are summed by attn_bwd_group_sum_kernel; with one head per group they
+// are the result).
 template <int HD>
 __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict__ q, const bf16* __restrict__ dob,
                                                           const bf16* __restrict__ kr, const bf16* __restrict__ vr,
@@ -362,7 +382,7 @@ __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict
                                                           float* __restrict__ dv) {
   int e, kb0;
   locate_block(cu, nseq, e, kb0);
-  const int kvh = blockIdx.y, group = H / KVh;
+  const int h = blockIdx.y, kvh = h / (H / KVh);
   const int tok0 = cu[e], S = cu[e + 1] - tok0;
   const int lane = threadIdx.x, hl = lane >> 5, c = lane & 31;
   const int mykey = kb0 + c;
@@ -380,8 +400,7 @@ __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict
     akk[b] = f32x16{};
     avv[b] = f32x16{};
   }
-  for (int hh = 0; hh < group; ++hh) {
-    const int h = kvh * group + hh;
+  {
     for (int qb0 = kb0; qb0 < S; qb0 += 32) {
       const int64_t tq = tok0 + min(qb0 + c, S - 1);  // rows past the sequence read its last query
       f32x16 sq = {}, dpq = {};
@@ -418,7 +437,7 @@ __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict
   }
   if (mykey >= S) return;
   const float rs = 1.f / sqrtf((float)HD);
-  const int64_t orow = ((int64_t)(tok0 + mykey) * KVh + kvh) * HD;
+  const int64_t orow = ((int64_t)(tok0 + mykey) * H + h) * HD;
 #pragma unroll
   for (int b = 0; b < HD / 32; ++b)
 #pragma unroll
@@ -428,6 +447,24 @@ __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict
                                        akk[b][g * 4 + 3] * rs};
       *(f32x4*)(dv + orow + d) = f32x4{avv[b][g * 4], avv[b][g * 4 + 1], avv[b][g * 4 + 2], avv[b][g * 4 + 3]};
     }
+}
+
+// dk[t][kvh] = sum over the group's heads (in order) of dkh[t][head], same for v
+__global__ void __launch_bounds__(256) attn_bwd_group_sum_kernel(const float* __restrict__ dkh,
+                                                                 const float* __restrict__ dvh, int64_t n, int group,
+                                                                 int hd, float* __restrict__ dk,
+                                                                 float* __restrict__ dv) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;  // over T * KV * hd
+  if (i >= n) return;
+  const int64_t row = i / hd, d = i % hd;  // row = t * KV + kvh
+  const int64_t base = row * group * hd + d;
+  float a = 0.f, b = 0.f;
+  for (int g = 0; g < group; ++g) {
+    a += dkh[base + (int64_t)g * hd];
+    b += dvh[base + (int64_t)g * hd];
+  }
+  dk[i] = a;
+  dv[i] = b;
 }
 
 // Gradients at the rotated q / k and at v back through RoPE (the transpose of
@@ -511,7 +548,7 @@ void launch_ce_loss(const float* logits, int ldl, int V, const int32_t* targets,
 
 void launch_transpose_pad(const bf16* src, int ld, int T, int C, bf16* dst, int Tp, hipStream_t s) {
   if (C <= 0 || Tp <= 0) return;
-  transpose_pad_kernel<<<dim3((C + 255) / 256, Tp / 8), 256, 0, s>>>(src, ld, T, C, dst, Tp);
+  transpose_tile_kernel<<<dim3((Tp + 63) / 64, (C + 63) / 64), 256, 0, s>>>(src, ld, T, Tp, C, dst, Tp, nullptr, 0, 0);
 }
 
 void launch_untile_transpose(const bf16* W, int64_t N, int K, bf16* dst, int64_t Np, hipStream_t s) {
@@ -545,22 +582,35 @@ void launch_colsum(const float* src, int64_t ld, int T, int C, float* part, floa
 
 void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
                      const int32_t* cu, const int32_t* h_cu, int nseq, int T, int H, int SP, int64_t W,
-                     bf16* kr, bf16* vr, bf16* kt, bf16* qt, bf16* dot, float* dq, float* dk, float* dv,
-                     hipStream_t s) {
+                     bf16* kr, bf16* vr, bf16* kt, bf16* qt, bf16* dot, float* dq, float* dkh, float* dvh, float* dk,
+                     float* dv, hipStream_t s) {
   if (T <= 0) return;
-  attn_bwd_d_kernel<<<(T * H + 255) / 256, 256, 0, s>>>(dob, o, T * H, kv.hd, dsum);
-  attn_bwd_pack_kernel<<<dim3(T, H), 128, 0, s>>>(q, dob, kv, cu, nseq, H, SP, W, kr, vr, kt, qt, dot);
+  const int KVh = kv.kv_heads, hd = kv.hd, group = H / KVh;
+  attn_bwd_d_kernel<<<(T * H + 255) / 256, 256, 0, s>>>(dob, o, T * H, hd, dsum);
+  attn_bwd_pack_kernel<<<dim3(T, KVh), 128, 0, s>>>(kv, cu, nseq, SP, kr, vr);
+  const int64_t nrows = (int64_t)nseq * SP;  // packed K rows (padding included) -> K^T
+  transpose_tile_kernel<<<dim3((unsigned)((nrows + 63) / 64), (KVh * hd + 63) / 64), 256, 0, s>>>(
+      kr, (int64_t)KVh * hd, (int)nrows, (int)nrows, KVh * hd, kt, W, nullptr, 0, 0);
+  transpose_tile_kernel<<<dim3((T + 63) / 64, (H * hd + 63) / 64), 256, 0, s>>>(q, (int64_t)H * hd, T, T, H * hd, qt,
+                                                                                 W, cu, nseq, SP);
+  transpose_tile_kernel<<<dim3((T + 63) / 64, (H * hd + 63) / 64), 256, 0, s>>>(dob, (int64_t)H * hd, T, T, H * hd,
+                                                                                 dot, W, cu, nseq, SP);
   int blocks = 0;
   for (int e = 0; e < nseq; ++e) blocks += (h_cu[e + 1] - h_cu[e] + 31) / 32;
-  const int KVh = kv.kv_heads;
-  if (kv.hd == 64) {
+  float* dkt = group > 1 ? dkh : dk;  // per-head shares, summed below when a group has several heads
+  float* dvt = group > 1 ? dvh : dv;
+  if (hd == 64) {
     attn_bwd_dq_kernel<64><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, kt, lse, dsum, cu, nseq, H, KVh, SP, W, dq);
-    attn_bwd_dkv_kernel<64><<<dim3(blocks, KVh), 64, 0, s>>>(q, dob, kr, vr, qt, dot, lse, dsum, cu, nseq, H, KVh,
-                                                             SP, W, dk, dv);
+    attn_bwd_dkv_kernel<64><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, qt, dot, lse, dsum, cu, nseq, H, KVh, SP,
+                                                           W, dkt, dvt);
   } else {
     attn_bwd_dq_kernel<128><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, kt, lse, dsum, cu, nseq, H, KVh, SP, W, dq);
-    attn_bwd_dkv_kernel<128><<<dim3(blocks, KVh), 64, 0, s>>>(q, dob, kr, vr, qt, dot, lse, dsum, cu, nseq, H, KVh,
-                                                              SP, W, dk, dv);
+    attn_bwd_dkv_kernel<128><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, qt, dot, lse, dsum, cu, nseq, H, KVh, SP,
+                                                            W, dkt, dvt);
+  }
+  if (group > 1) {
+    const int64_t n = (int64_t)T * KVh * hd;
+    attn_bwd_group_sum_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(dkh, dvh, n, group, hd, dk, dv);
   }
 }
 

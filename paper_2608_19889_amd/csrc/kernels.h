@@ -113,10 +113,11 @@ void launch_colsum(const float* src, int64_t ld, int T, int C, float* part, floa
 // (scratch, finite at allocation): kr / vr [nseq*SP][KV][hd], kt [KV*hd][W],
 // qt / dot [H*hd][W], W >= nseq*SP, SP >= the longest sequence rounded up to
 // 32, plus 32
+// dkh / dvh [T][H][hd] scratch (the per-head shares of dk / dv)
 void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
                      const int32_t* cu, const int32_t* h_cu, int nseq, int T, int H, int SP, int64_t W,
-                     bf16* kr, bf16* vr, bf16* kt, bf16* qt, bf16* dot, float* dq, float* dk, float* dv,
-                     hipStream_t s);
+                     bf16* kr, bf16* vr, bf16* kt, bf16* qt, bf16* dot, float* dq, float* dkh, float* dvh, float* dk,
+                     float* dv, hipStream_t s);
 // back through RoPE into the fused QKV row order (bf16) and the original order
 // (float, may be null)
 void launch_rope_bwd(const float* dq, const float* dk, const float* dv, const float* cos_t, const float* sin_t,
