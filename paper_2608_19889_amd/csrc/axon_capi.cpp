@@ -258,6 +258,8 @@ struct axon_model {
   float* logits_int = nullptr;
   float* attn_part = nullptr;
   float* gemv_part = nullptr;  // split-K partial sums of the decode projections
+  float* gemm_part = nullptr;  // split-K partial sums of the narrow prefill / training GEMMs
+  int64_t gemm_part_floats = 0;
   float* ss = nullptr;       // per-workgroup sums of squares of x rows
   void* xg = nullptr;        // bf16(x * g) for the next normalized projection
   int ss_n = 0;              // number of partials currently in ss
@@ -400,6 +402,45 @@ void gemm_many(axon_model* m, const void* W, const void* X, int N, int M, int K,
     else
       launch_gemm_f32((const float*)W, (const float*)X, N, M, K, epi, ep, s);
   });
+}
+
+// Split-K choice for a bf16 GEMM with a float32 result: the split
+// gemm_ksplit takes when its partials fit m->gemm_part, else 1.
+int split_for(axon_model* m, int N, int M, int K) {
+  const int ks = gemm_ksplit(N, M, K);
+  return ks > 1 && (int64_t)ks * M * N <= m->gemm_part_floats ? ks : 1;
+}
+
+// out (accumulate ? += : =) X W^T (float32 [M][N], rows N apart), split over
+// K when the output has few 256-tiles (partials summed in order)
+void gemm_f32_out(axon_model* m, const void* W, const void* X, int N, int M, int K, float* out, bool accumulate,
+                  hipStream_t s) {
+  const int ks = split_for(m, N, M, K);
+  if (ks > 1) {
+    m->timed(1, N, M, K, s, [&] {
+      launch_gemm_bf16_split((const bf16*)W, (const bf16*)X, N, M, K, ks, m->gemm_part, (int64_t)M * N, s);
+    });
+    launch_sum_parts(out, m->gemm_part, ks, (int64_t)M * N, (int64_t)M * N, accumulate ? 1 : 0, s);
+  } else {
+    gemm_many<bf16>(m, W, X, N, M, K, accumulate ? EPI_RESID : EPI_F32, out, nullptr, N, s);
+  }
+}
+
+// x += X W^T, then h = RMSNorm(x) g for ``rows`` rows (the last row of each
+// sequence when cu_last is set): a split-K GEMM's partials are summed into x
+// by the normalization kernel itself
+void gemm_resid_norm(axon_model* m, const void* W, const bf16* X, int T, int K, const bf16* g, bf16* h, int rows,
+                     const int32_t* cu_last, hipStream_t s) {
+  const int D = m->D(), ks = split_for(m, D, T, K);
+  if (ks > 1) {
+    m->timed(1, D, T, K, s, [&] {
+      launch_gemm_bf16_split((const bf16*)W, X, D, T, K, ks, m->gemm_part, (int64_t)T * D, s);
+    });
+    launch_resid_rmsnorm<bf16>(m->x, m->gemm_part, ks, (int64_t)T * D, g, h, rows, D, m->cfg.rms_eps, cu_last, s);
+  } else {
+    gemm_many<bf16>(m, W, X, D, T, K, EPI_RESID, m->x, nullptr, D, s);
+    launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, g, h, rows, D, m->cfg.rms_eps, cu_last, s);
+  }
 }
 
 // Few-token projection in float32 check mode.
@@ -1603,6 +1644,13 @@ int train_setup(axon_model* m, hipStream_t s) {
   if (!r) r = ba(&tb.trs, maxK * Tp);
   if (!r) r = ba(&tb.trb, tiled(maxK, Tp));
   if (!r) r = ba(&tb.headT, tiled(D, Vp));
+  // split-K partials of the narrow training GEMMs: up to 4 splits of an
+  // output as large as T x max(D, I) or one weight's gradient
+  if (!m->gemm_part) {
+    m->gemm_part_floats = 4 * std::max({T * D, T * I, T * Hhd, nq * D, 2 * I * D});
+    if (!r) r = fa(&m->gemm_part, m->gemm_part_floats);
+    if (r) m->gemm_part_floats = 0;
+  }
   tb.SP = (c.max_seq + 31) / 32 * 32 + 32;
   tb.W = (int64_t)c.max_batch * tb.SP;
   if (!r) r = ba(&tb.kr, tb.W * KV * hd);
@@ -1674,32 +1722,31 @@ void enqueue_train(axon_model* m, int B, int T, const int32_t* d_tokens, const i
     m->timed(3, H, B, T, s, [&] {
       launch_attn_prefill<bf16>(t.q, kv, t.o, T, B, d_cu, h_cu, H, s, nullptr, nullptr, nullptr, nullptr, t.lse);
     });
-    gemm_many<bf16>(m, w.wo, t.o, D, T, Hhd, EPI_RESID, m->x, nullptr, D, s);
+    gemm_resid_norm(m, w.wo, t.o, T, Hhd, (const bf16*)w.gpost, t.h2, T, nullptr, s);
     (void)hipMemcpyAsync(t.xmid, m->x, (size_t)T * D * 4, hipMemcpyDeviceToDevice, s);
-    launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, (const bf16*)w.gpost, t.h2, T, D, eps, nullptr, s);
     gemm_many<bf16>(m, w.wgu, t.h2, 2 * I, T, D, EPI_F32, t.gu, nullptr, 2 * I, s);
     launch_silu_reduce<bf16>(t.gu, 1, 0, t.a, T, I, s);
-    gemm_many<bf16>(m, w.wd, t.a, D, T, I, EPI_RESID, m->x, nullptr, D, s);
-    if (l + 1 < L)
-      launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, (const bf16*)m->layers[l + 1].gin, tb.L[l + 1].h1, T, D, eps,
-                                 nullptr, s);
+    if (l + 1 < L) {
+      gemm_resid_norm(m, w.wd, t.a, T, I, (const bf16*)m->layers[l + 1].gin, tb.L[l + 1].h1, T, nullptr, s);
+    } else {
+      gemm_resid_norm(m, w.wd, t.a, T, I, (const bf16*)m->gfinal, tb.hf, T, nullptr, s);
+      (void)hipMemcpyAsync(tb.xfin, m->x, (size_t)T * D * 4, hipMemcpyDeviceToDevice, s);
+    }
   }
-  (void)hipMemcpyAsync(tb.xfin, m->x, (size_t)T * D * 4, hipMemcpyDeviceToDevice, s);
-  launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, (const bf16*)m->gfinal, tb.hf, T, D, eps, nullptr, s);
   gemm_many<bf16>(m, m->lm_head, tb.hf, V, T, D, EPI_F32, tb.logits, nullptr, Vp, s);
   // ---- loss and its gradient at the logits
   launch_ce_loss(tb.logits, Vp, V, d_targets, T, tb.rowloss, tb.valid, tb.lserow, d_loss, tb.scal, tb.dlog, s);
   // ---- backward
   // dX = dY W: [T][K] float from dY [T][N] and the tiled W^T [K][N]
   auto dX = [&](const bf16* WT, const bf16* dY, int N, int K, float* out) {
-    gemm_many<bf16>(m, WT, dY, K, T, N, EPI_F32, out, nullptr, K, s);
+    gemm_f32_out(m, WT, dY, K, T, N, out, false, s);
   };
   // dW = dY^T X: [N][K] float from dY [T][N] (rows ldy apart) and X [T][K]
   auto dW = [&](const bf16* dY, int ldy, int N, const bf16* X, int K, float* out) {
     launch_transpose_pad(dY, ldy, T, N, tb.tra, Tp, s);
     launch_transpose_pad(X, K, T, K, tb.trs, Tp, s);
     launch_tile_weight(tb.trs, tb.trb, K, Tp, s);
-    gemm_many<bf16>(m, tb.trb, tb.tra, K, N, Tp, EPI_F32, out, nullptr, K, s);
+    gemm_f32_out(m, tb.trb, tb.tra, K, N, Tp, out, false, s);
   };
   const bool tied = c.tie_embeddings;
   float* g_embed = G("model.embed_tokens.weight");

@@ -339,10 +339,13 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
 
-  const int nk = K / BK;
+  // split K (gridDim.y > 1, float32 partials): this workgroup's share of
+  // the k-tiles (gridDim.y divides K / BK)
+  const int nk = K / BK / (int)gridDim.y;
+  const int kbase = (int)blockIdx.y * nk * BK;
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
-    if (st < nk) issue(st, st * BK);
+    if (st < nk) issue(st, kbase + st * BK);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (grp == 1) phase_barrier();  // group 1 runs one phase behind group 0
@@ -369,7 +372,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
       }
     }
     const int kn = kt + STAGES - 1;
-    if (kn < nk) issue(kn % STAGES, kn * BK);
+    if (kn < nk) issue(kn % STAGES, kbase + kn * BK);
     // group 1's share of k-tile kt+1 must land before group 0 reads it in
     // the phase after the coming barrier; group 0 waits for its own share at
     // the end of its compute phase
@@ -430,7 +433,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
         for (int g = 0; g < 4; ++g) {
           const int n = nb + g * 8 + (lane >> 5) * 4;
           if (n >= N) continue;
-          float* p = ep.out_f32 + (int64_t)t * ep.ldo + n;
+          float* p = ep.out_f32 + (int64_t)blockIdx.y * ep.part_stride + (int64_t)t * ep.ldo + n;
           f32x4 v = {acc[a][b][g * 4 + 0], acc[a][b][g * 4 + 1], acc[a][b][g * 4 + 2], acc[a][b][g * 4 + 3]};
           if (ep.bias) {
 #pragma unroll
@@ -468,6 +471,33 @@ static void launch_grouped(const bf16* W, const bf16* X, int N, int K, int max_r
   const int64_t mtiles = (max_rows + pf2::BM - 1) / pf2::BM + ep.g_E;
   const int64_t tiles = mtiles * ((N + pf2::BN - 1) / pf2::BN);
   klaunch(kern, dim3((unsigned)tiles), dim3(512), pf2::LDS_BYTES, s, W, X, N, 0, K, ep);
+}
+
+void launch_gemm_bf16_split(const bf16* W, const bf16* X, int N, int M, int K, int ksplit, float* part,
+                            int64_t part_stride, hipStream_t s) {
+  if (M <= 0) return;
+  static bool attr = false;
+  auto kern = gemm_bf16_256_kernel<EPI_F32>;
+  if (!attr) {
+    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, pf2::LDS_BYTES);
+    attr = true;
+  }
+  EpiArgs ep{};
+  ep.out_f32 = part;
+  ep.ldo = N;
+  ep.part_stride = part_stride;
+  const int tiles = ((N + pf2::BN - 1) / pf2::BN) * ((M + pf2::BM - 1) / pf2::BM);
+  klaunch(kern, dim3(tiles, ksplit), dim3(512), pf2::LDS_BYTES, s, W, X, N, M, K, ep);
+}
+
+int gemm_ksplit(int N, int M, int K) {
+  if (M < 256 || N < 256) return 1;
+  const int tiles = ((N + 255) / 256) * ((M + 255) / 256);
+  if (tiles >= 160) return 1;
+  const int nk = K / 32;
+  for (int ks : {2, 4})
+    if (tiles * ks >= 200 && nk % ks == 0 && nk / ks >= 8) return ks;
+  return nk % 2 == 0 && nk / 2 >= 8 ? 2 : 1;
 }
 
 void launch_gemm_bf16_grouped(const bf16* W, const bf16* X, int N, int K, int max_rows, int epi, const EpiArgs& ep,
@@ -623,6 +653,21 @@ void launch_gemm_f32(const float* W, const float* X, int N, int M, int K, int ep
 // ============================================================================
 // split-K reductions
 // ============================================================================
+// out[i] (accumulate ? += : =) sum over s of parts[s * stride + i], in order
+__global__ void __launch_bounds__(256) sum_parts_kernel(float* __restrict__ out, const float* __restrict__ parts,
+                                                        int nparts, int64_t stride, int64_t n4, int accumulate) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n4) return;
+  f32x4 v = accumulate ? *(const f32x4*)(out + i * 4) : f32x4{};
+  for (int p = 0; p < nparts; ++p) v += *(const f32x4*)(parts + p * stride + i * 4);
+  *(f32x4*)(out + i * 4) = v;
+}
+
+void launch_sum_parts(float* out, const float* parts, int nparts, int64_t stride, int64_t n, int accumulate,
+                      hipStream_t s) {
+  const int64_t n4 = n / 4;
+  if (n4 > 0) sum_parts_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(out, parts, nparts, stride, n4, accumulate);
+}
 template <typename T>
 __global__ void silu_reduce_kernel(const float* __restrict__ parts, int nparts, int64_t part_stride,
                                    T* __restrict__ a, int M, int I) {

@@ -158,6 +158,16 @@ void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi
 // experts (surplus workgroups exit at once).  EPI_F32 or EPI_SILU.
 void launch_gemm_bf16_grouped(const bf16* W, const bf16* X, int N, int K, int max_rows, int epi, const EpiArgs& ep,
                               hipStream_t s);
+// split K over gridDim.y = ksplit workgroup rows: float32 partials
+// part[s * part_stride + m * N + n] (the 256 x 256 kernel; ksplit divides K /
+// 32).  gemm_ksplit: the split worth taking for an output of few 256-tiles
+// (1: none).
+void launch_gemm_bf16_split(const bf16* W, const bf16* X, int N, int M, int K, int ksplit, float* part,
+                            int64_t part_stride, hipStream_t s);
+int gemm_ksplit(int N, int M, int K);
+// out[i] (accumulate ? += : =) sum of parts[s * stride + i] over s in order (n % 4 == 0)
+void launch_sum_parts(float* out, const float* parts, int nparts, int64_t stride, int64_t n, int accumulate,
+                      hipStream_t s);
 // float32 check-mode GEMM (any M): EPI_F32 / EPI_RESID / EPI_PART(split 0 only).
 void launch_gemm_f32(const float* W, const float* X, int N, int M, int K, int epi, const EpiArgs& ep,
                      hipStream_t s);

@@ -27,6 +27,9 @@ CASES = {
     "llama_hd64_tied": ("1b", dict(layers=2, vocab=3000, hidden=512, intermediate=1024), [37, 130, 65, 5]),
     # untied head, q/k/v biases, head_dim 128, group 7
     "qwen_hd128_bias": ("7b", dict(layers=2, vocab=2048, hidden=896, intermediate=1792), [100, 33, 71]),
+    # 600 tokens: the narrow projections (hidden 512) have fewer than 160
+    # output tiles of 256 and split K (float32 partials summed in order)
+    "llama_hd64_split_k": ("1b", dict(layers=2, vocab=3000, hidden=512, intermediate=1024), [200, 310, 90]),
 }
 
 
