@@ -426,12 +426,23 @@ void gemm_f32_out(axon_model* m, const void* W, const void* X, int N, int M, int
   }
 }
 
+// Split of an inference prefill's residual projection (O, dense down): by
+// its shape alone, never by the token count, so that a prompt fed in chunks
+// takes the same k-order as the whole prompt and gives the same bits.  Narrow
+// outputs (hidden <= 2048: too few 256-tiles at any prompt length) split K in
+// two.
+int prefill_split(axon_model* m, int N, int M, int K) {
+  const int nk = K / 32;
+  if (N > 2048 || K < 1024 || nk % 2 || (int64_t)2 * M * N > m->gemm_part_floats) return 1;
+  return 2;
+}
+
 // x += X W^T, then h = RMSNorm(x) g for ``rows`` rows (the last row of each
 // sequence when cu_last is set): a split-K GEMM's partials are summed into x
 // by the normalization kernel itself
 void gemm_resid_norm(axon_model* m, const void* W, const bf16* X, int T, int K, const bf16* g, bf16* h, int rows,
-                     const int32_t* cu_last, hipStream_t s) {
-  const int D = m->D(), ks = split_for(m, D, T, K);
+                     const int32_t* cu_last, hipStream_t s, bool by_shape = false) {
+  const int D = m->D(), ks = by_shape ? prefill_split(m, D, T, K) : split_for(m, D, T, K);
   if (ks > 1) {
     m->timed(1, D, T, K, s, [&] {
       launch_gemm_bf16_split((const bf16*)W, X, D, T, K, ks, m->gemm_part, (int64_t)T * D, s);
@@ -621,11 +632,19 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
                                ent_base);
       });
     }
-    gemm_many<T>(m, w.wo, m->o, D, Ttok, H * hd, EPI_RESID, m->x, nullptr, D, s, nullptr, w.bo);
-    if (gpt2)
-      launch_layernorm(m->x, (const bf16*)w.gpost, (const bf16*)w.gpost_b, (bf16*)h, Ttok, D, eps, nullptr, s);
-    else
-      launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, Ttok, D, eps, nullptr, s);
+    const bool llama_bf16 = sizeof(T) == 2 && !gpt2;
+    if (llama_bf16) {
+      gemm_resid_norm(m, w.wo, (const bf16*)m->o, Ttok, H * hd, (const bf16*)w.gpost, (bf16*)h, Ttok, nullptr, s, true);
+    } else {
+      gemm_many<T>(m, w.wo, m->o, D, Ttok, H * hd, EPI_RESID, m->x, nullptr, D, s, nullptr, w.bo);
+      if (gpt2)
+        launch_layernorm(m->x, (const bf16*)w.gpost, (const bf16*)w.gpost_b, (bf16*)h, Ttok, D, eps, nullptr, s);
+      else
+        launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, Ttok, D, eps, nullptr, s);
+    }
+    const bool last = l + 1 == m->cfg.n_layers;
+    const T* gnext = (const T*)(last ? m->gfinal : m->layers[l + 1].gin);
+    bool normed = false;  // the dense down projection also ran the next normalization
     if (gpt2) {
       gemm_many<T>(m, w.wgu, h, I, Ttok, D, EPI_GELU, nullptr, m->a, I, s, nullptr, w.bfc);
       gemm_many<T>(m, w.wd, m->a, D, Ttok, I, EPI_RESID, m->x, nullptr, D, s, nullptr, w.bd);
@@ -634,14 +653,17 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
     } else {
       if constexpr (sizeof(T) == 2) {
         gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_SILU, nullptr, m->a, I, s);
+        const bool to_last = last && !all_logits;
+        gemm_resid_norm(m, w.wd, (const bf16*)m->a, Ttok, I, (const bf16*)gnext, (bf16*)(to_last ? m->hlast : h),
+                        to_last ? B : Ttok, to_last ? d_cu : nullptr, s, true);
+        normed = true;
       } else {
         gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_F32, m->gu_f32, nullptr, 2 * I, s);
         launch_silu_reduce<T>(m->gu_f32, 1, 0, (T*)m->a, Ttok, I, s);
+        gemm_many<T>(m, w.wd, m->a, D, Ttok, I, EPI_RESID, m->x, nullptr, D, s);
       }
-      gemm_many<T>(m, w.wd, m->a, D, Ttok, I, EPI_RESID, m->x, nullptr, D, s);
     }
-    const bool last = l + 1 == m->cfg.n_layers;
-    const T* gnext = (const T*)(last ? m->gfinal : m->layers[l + 1].gin);
+    if (normed) continue;
     if (gpt2) {
       const bf16* bnext = (const bf16*)(last ? m->gfinal_b : m->layers[l + 1].gin_b);
       if (!last || all_logits)
@@ -1267,6 +1289,11 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
                           gemv_workspace_floats((int)D, Is, b, GV_RESID)});
       }
       if (wsf > 0) TRY(dev_alloc(m, (void**)&m->gemv_part, (size_t)wsf * 4));
+      // two K halves of the narrow prefill residual projections (hidden <= 2048)
+      if (!m->gpt2() && D <= 2048) {
+        m->gemm_part_floats = 2 * tmax * D;
+        TRY(dev_alloc(m, (void**)&m->gemm_part, (size_t)m->gemm_part_floats * 4));
+      }
     }
     TRY(dev_alloc(m, (void**)&m->ss, (int64_t)std::max<int64_t>(D / 8, 1) * c.max_batch * 4));
     TRY(dev_alloc(m, &m->xg, (int64_t)c.max_batch * D * 2));
@@ -1646,10 +1673,14 @@ int train_setup(axon_model* m, hipStream_t s) {
   if (!r) r = ba(&tb.headT, tiled(D, Vp));
   // split-K partials of the narrow training GEMMs: up to 4 splits of an
   // output as large as T x max(D, I) or one weight's gradient
-  if (!m->gemm_part) {
-    m->gemm_part_floats = 4 * std::max({T * D, T * I, T * Hhd, nq * D, 2 * I * D});
-    if (!r) r = fa(&m->gemm_part, m->gemm_part_floats);
-    if (r) m->gemm_part_floats = 0;
+  const int64_t want = 4 * std::max({T * D, T * I, T * Hhd, nq * D, 2 * I * D});
+  if (m->gemm_part_floats < want) {  // the inference buffer (if any) stays allocated until axon_free
+    float* p = nullptr;
+    if (!r) r = fa(&p, want);
+    if (!r) {
+      m->gemm_part = p;
+      m->gemm_part_floats = want;
+    }
   }
   tb.SP = (c.max_seq + 31) / 32 * 32 + 32;
   tb.W = (int64_t)c.max_batch * tb.SP;
