@@ -273,3 +273,11 @@ def test_gpt2_weight_map_is_checked():
     llama_names["model.norm.weight"] = torch.empty(128, dtype=torch.bfloat16)
     rc, msg = _status(s, llama_names)
     assert rc == axon.AXON_E_MISSING and "unknown" in msg
+
+
+def test_loss_and_grads_rejects_null_arguments():
+    """The backward entry point validates on the host before any GPU work."""
+    lib = axon.lib()
+    cu = (ctypes.c_int32 * 2)(0, 4)
+    rc = lib.axon_loss_and_grads(None, 1, None, None, cu, None, None, None, 0, None)
+    assert rc == axon.AXON_E_INVALID and "NULL" in axon.last_error()

@@ -92,3 +92,37 @@ def test_backward_rejects_other_model_kinds():
     with pytest.raises(ax.AxonError, match="backward pass covers"):
         m.loss_and_grads(flat, cu, flat.clone(), grads)
     m.close()
+
+
+def test_gradient_map_is_validated_and_uncounted_batches_give_zero():
+    from paper_2608_19889_amd import axon as ax
+    shape = small_shape("1b", layers=1, vocab=500, hidden=256, intermediate=512)
+    w = model_weights(shape, seed=75)
+    m = gpu_model(shape, w, max_batch=2, max_seq=32)
+    flat, cu = pack([np.arange(9), np.arange(5)])
+    grads = {k: torch.full(tuple(v.shape), 7.0, dtype=torch.float32, device="cuda") for k, v in w.items()}
+    # no position counted: loss 0 and every gradient 0 (overwritten, not left as 7)
+    none = torch.full((14,), -1, dtype=torch.int32, device="cuda")
+    loss = m.loss_and_grads(flat, cu, none, grads)
+    torch.cuda.synchronize()
+    assert float(loss.item()) == 0.0
+    for name, g in grads.items():
+        assert float(g.abs().max().item()) == 0.0, name
+    # the map must match the weights exactly: dtype, names, shapes, device buffers
+    bad = dict(grads)
+    bad["model.norm.weight"] = torch.zeros(256, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ax.AxonError, match="AXON_F32"):
+        m.loss_and_grads(flat, cu, none, bad)
+    bad = dict(grads)
+    del bad["model.layers.0.mlp.up_proj.weight"]
+    with pytest.raises(ax.AxonError, match="missing gradient"):
+        m.loss_and_grads(flat, cu, none, bad)
+    bad = dict(grads)
+    bad["model.layers.0.self_attn.o_proj.weight"] = torch.zeros((256, 128), dtype=torch.float32, device="cuda")
+    with pytest.raises(ax.AxonError, match="o_proj"):
+        m.loss_and_grads(flat, cu, none, bad)
+    bad = dict(grads)
+    bad["model.norm.weight"] = torch.zeros(256, dtype=torch.float32)  # host memory
+    with pytest.raises(ax.AxonError, match="device buffer"):
+        m.loss_and_grads(flat, cu, none, bad)
+    m.close()
