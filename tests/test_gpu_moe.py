@@ -108,6 +108,13 @@ def test_moe_prefill_and_decode_against_oracle(case):
     _against_oracle(case, [37, 130, 300, 5], steps=4, seed=31)
 
 
+def test_moe_decode_beyond_64_sequences_against_oracle():
+    """More sequences than one fused decode projection takes: the decode step
+    runs as separate kernels and the experts through the grouped GEMM."""
+    rng = np.random.default_rng(44)
+    _against_oracle("deepseek_style", [int(n) for n in rng.integers(2, 20, size=70)], steps=2, seed=45)
+
+
 @pytest.mark.parametrize("case", list(CASES))
 def test_moe_wide_decode_batch_against_oracle(case):
     """17..64 decode tokens: the few-token projections take their row-splitting
