@@ -809,10 +809,16 @@ GvShape gemv_shape(int N, int K, int M, int epi) {
     return {64, 4, nb == 2 ? 2 : 4, ksplit, epi == GV_SILU ? 32 : 16, 1};
   }
   if (nb == 1) {
-    if (epi == GV_SILU || epi == GV_GELU) return {32, 4, 4, 1, 0};
+    // from timing every (rows, wavefronts, k-steps) candidate on weights
+    // streamed from HBM, 1B- and 7B-shaped layers at 8 and 16 tokens
+    if (epi == GV_SILU) return {32, 8, 4, 1, 0};
+    if (epi == GV_GELU) return {32, 4, 4, 1, 0};
     if (epi == GV_HEAD) return {K <= 2048 ? 32 : 64, 8, 2, 1, 0};
-    if (N / 16 < 192) return {8, 16, 2, 1, 0};
-    return K >= 8192 ? GvShape{16, 8, 4, 1, 0} : GvShape{16, 16, 2, 1, 0};
+    // QKV + RoPE: with a long K, 32-row tiles halve the token-operand reads
+    // per weight byte (10.7 against 14.4 us on the 7B shape)
+    if (epi == GV_ROPE) return K >= 3072 ? GvShape{32, 8, 4, 1, 0} : GvShape{16, 16, 4, 1, 0};
+    if (N / 16 < 192) return K >= 8192 ? GvShape{8, 8, 8, 1, 0} : GvShape{8, 16, 2, 1, 0};
+    return {16, 8, 4, 1, 0};
   }
   // 17..64 tokens: the row-splitting kernel (gemv_wide_kernel), whose token
   // fragments are reused by 4 or 8 row blocks per workgroup.  3 token blocks
@@ -871,11 +877,11 @@ static bool gv_dispatch(const GemvArgs& a, const GvShape& sh, int nb, hipStream_
 #define AXON_GVW(R, U_, NB_) \
   if (sh.wide && sh.rows == R && sh.u == U_ && nb == NB_) return gvw<R / 64, U_, NB_, NORM, EPI>(a, s);
   if constexpr (EPI == GV_SILU || EPI == GV_GELU) {
-    AXON_GV(32, 4, 4, 1) AXON_GVW(128, 2, 2) AXON_GVW(64, 4, 3) AXON_GVW(64, 2, 4)
+    AXON_GV(32, 4, 4, 1) AXON_GV(32, 8, 4, 1) AXON_GVW(128, 2, 2) AXON_GVW(64, 4, 3) AXON_GVW(64, 2, 4)
   } else if constexpr (EPI == GV_HEAD) {
     AXON_GV(32, 8, 2, 1) AXON_GV(64, 8, 2, 1) AXON_GVW(128, 4, 2) AXON_GVW(128, 4, 3) AXON_GVW(128, 2, 4)
   } else {
-    AXON_GV(8, 16, 2, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 2, 1)
+    AXON_GV(8, 16, 2, 1) AXON_GV(8, 8, 8, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 4, 1) AXON_GV(32, 8, 4, 1)
   }
 #undef AXON_GVW
 #undef AXON_GV
