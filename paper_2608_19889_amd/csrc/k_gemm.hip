@@ -34,43 +34,60 @@ AXON_DEV void store_cols(float* p, f32x4 v, int left) {
 // pairs them (both lanes of a pair share t, so they are active together).
 // Bias first, then rotate-half RoPE at the token's position; q -> q_out, k ->
 // its K page block, v (unrotated) -> its transposed V page block.
-AXON_DEV void rope_block(const EpiArgs& ep, int nb, int t, const f32x16& v, int lane) {
+// The token's cache slot and position (rope_token) are looked up before the
+// k-loop: the lookup is a chain of dependent loads (a binary search over the
+// sequence offsets) whose latency the k-loop hides.
+struct RopeTok {
+  int slot, pos;
+};
+AXON_DEV RopeTok rope_token(const EpiArgs& ep, int t) {
+  if (ep.len) return {t, ep.len[t]};
+  const int e = seq_of_token(ep.cu, ep.nseq, t);
+  return {ep.ent_slot ? ep.ent_slot[e] : e, (ep.ent_base ? ep.ent_base[e] : 0) + t - ep.cu[e]};
+}
+AXON_DEV void rope_block(const EpiArgs& ep, int nb, int t, RopeTok tok, const f32x16& v, int lane) {
   const int hd = ep.kv.hd, half = hd / 2, KVh = ep.kv.kv_heads;
   const int head = nb / hd;
   const bool first = lane < 32;
-  int slot, pos;
-  if (ep.len) {
-    slot = t;
-    pos = ep.len[t];
-  } else {
-    const int e = seq_of_token(ep.cu, ep.nseq, t);
-    slot = ep.ent_slot ? ep.ent_slot[e] : e;
-    pos = (ep.ent_base ? ep.ent_base[e] : 0) + t - ep.cu[e];
-  }
+  const bool rotate = head < ep.H + KVh;  // q and k heads (v is stored unrotated)
+  // every operand of the block is loaded before its first store: the stores
+  // may alias the tables as far as the compiler knows, so loads issued
+  // between them would cost one memory round trip per 8-row group
+  bf16x4 bb[4];
+  f32x4 cs[4], sn[4];
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
     const int i0 = ((nb % hd + g * 8) / 8) * 4;  // first rotation pair of the 8-row group
     const int e0 = first ? i0 : i0 + half;       // element index of this lane's first value
+    bb[g] = ep.bias ? *(const bf16x4*)(ep.bias + head * hd + e0) : bf16x4{};
+    cs[g] = f32x4{};
+    sn[g] = f32x4{};
+    if (rotate) {
+      cs[g] = *(const f32x4*)(ep.cos_t + (int64_t)tok.pos * half + i0);
+      sn[g] = *(const f32x4*)(ep.sin_t + (int64_t)tok.pos * half + i0);
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int i0 = ((nb % hd + g * 8) / 8) * 4;
+    const int e0 = first ? i0 : i0 + half;
     float x[4], xp[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      x[j] = v[g * 4 + j];
-      if (ep.bias) x[j] += (float)ep.bias[head * hd + e0 + j];
+      x[j] = v[g * 4 + j] + (float)bb[g][j];
       xp[j] = __shfl_xor(x[j], 32, 64);
     }
-    if (head < ep.H + KVh) {
-      const f32x4 cs = *(const f32x4*)(ep.cos_t + (int64_t)pos * half + i0);
-      const f32x4 sn = *(const f32x4*)(ep.sin_t + (int64_t)pos * half + i0);
+    if (rotate) {
       bf16x4 y;
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        y[j] = (bf16)(first ? x[j] * cs[j] - xp[j] * sn[j] : x[j] * cs[j] + xp[j] * sn[j]);
+        y[j] = (bf16)(first ? x[j] * cs[g][j] - xp[j] * sn[g][j] : x[j] * cs[g][j] + xp[j] * sn[g][j]);
       if (head < ep.H) *(bf16x4*)(ep.q_out + ((int64_t)t * ep.H + head) * hd + e0) = y;
-      else *(bf16x4*)((bf16*)ep.kv.k + k_el(ep.kv, slot, head - ep.H, pos, e0)) = y;  // 4 dims contiguous
+      else *(bf16x4*)((bf16*)ep.kv.k + k_el(ep.kv, tok.slot, head - ep.H, tok.pos, e0)) = y;  // 4 dims contiguous
     } else {
       bf16* vc = (bf16*)ep.kv.v;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) vc[v_el(ep.kv, slot, head - ep.H - KVh, pos, e0 + j)] = (bf16)x[j];
+      for (int j = 0; j < 4; ++j) vc[v_el(ep.kv, tok.slot, head - ep.H - KVh, tok.pos, e0 + j)] = (bf16)x[j];
     }
   }
 }
@@ -132,9 +149,14 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
   for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+  RopeTok tok[2] = {};
 
   const int nk = K / BK;
   gload(0);
+  if constexpr (EPI == EPI_ROPE) {  // behind the first tile's loads
+#pragma unroll
+    for (int b = 0; b < 2; ++b) tok[b] = rope_token(ep, min(m0 + wc * 64 + b * 32 + (lane & 31), M - 1));
+  }
   sstore(0);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
@@ -172,7 +194,7 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
       const int nb = n0 + wr * 64 + a * 32;  // 32-aligned row block
       if (nb >= N) continue;
       if constexpr (EPI == EPI_ROPE) {
-        rope_block(ep, nb, t, acc[a][b], lane);
+        rope_block(ep, nb, t, tok[b], acc[a][b], lane);
       } else if constexpr (EPI == EPI_SILU) {
         // rows nb..nb+15 are gate rows, nb+16..nb+31 the matching up rows
         bf16* out = (bf16*)ep.out_t + (int64_t)t * ep.ldo + (nb / 32) * 16;
@@ -338,6 +360,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
   for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+  RopeTok tok[2] = {};
 
   // split K (gridDim.y > 1, float32 partials): this workgroup's share of
   // the k-tiles (gridDim.y divides K / BK)
@@ -346,6 +369,10 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
 #pragma unroll
   for (int st = 0; st < STAGES - 1; ++st)
     if (st < nk) issue(st, kbase + st * BK);
+  if constexpr (EPI == EPI_ROPE) {  // behind the first stages' loads
+#pragma unroll
+    for (int b = 0; b < 2; ++b) tok[b] = rope_token(ep, rowbase + min(m0 + wc * 64 + b * 32 + (lane & 31), M - 1));
+  }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (grp == 1) phase_barrier();  // group 1 runs one phase behind group 0
@@ -407,7 +434,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
       const int nb = n0 + grp * 128 + a * 32;
       if (nb >= N) continue;
       if constexpr (EPI == EPI_ROPE) {
-        rope_block(ep, nb, t, acc[a][b], lane);
+        rope_block(ep, nb, t, tok[b], acc[a][b], lane);
       } else if constexpr (EPI == EPI_SILU) {
         bf16* out = (bf16*)ep.out_t + (int64_t)t * ep.ldo + (nb / 32) * 16;
 #pragma unroll
