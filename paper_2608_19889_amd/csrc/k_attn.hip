@@ -638,7 +638,10 @@ static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int B,
   const int group = H / kv.kv_heads;
   const size_t lds = (size_t)(2 * NW * 16 + NW * group * HD) * sizeof(float);
   const dim3 grid(nsplit, kv.kv_heads, B);
-  constexpr int NBUF = 2;  // chunks in flight per wavefront (3-4 measured slower: clamped duplicate loads, registers)
+  // chunks in flight per wavefront: 1 measured fastest on the 1B-, 7B- and
+  // 32B-shaped batches (5.9 / 21.4 / 29.4 us against 6.5 / 22.3 / 29.8 with
+  // 2; the 8 wavefronts of a workgroup already keep 8 chunks in flight)
+  constexpr int NBUF = 1;
   if (kv.bt)
     attn_decode_bf16_kernel<HD, NW, true, NBUF>
         <<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len, rows, slots);
