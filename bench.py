@@ -60,6 +60,9 @@ def main():
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) of a "
                          "--copy-calibration run into profiles/decode_gemv_<workload>_traffic.json and exit")
+    ap.add_argument("--vendor-gemm", action="store_true",
+                    help="time the vendor library's GEMM (torch.matmul, bf16) on the workload's prefill projection "
+                         "shapes instead of the workload, as a reference for the hand-written kernels, and exit")
     args = ap.parse_args()
     if args.summarize_counters:
         summarize_counters(args.summarize_counters[0], args.summarize_counters[1], args.workload)
@@ -80,6 +83,8 @@ def main():
 
     wl = dict(WORKLOADS[args.workload])
     shape = MODEL_SHAPES[wl["model"]]
+    if args.vendor_gemm:
+        return vendor_gemm(shape, wl)
     if wl.get("train"):
         return train_bench(args, wl, shape)
     esz = 2 if shape["dtype"] == "bf16" else 4
@@ -243,6 +248,40 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, wl, lens, steps, B)
     print(json.dumps(out), flush=True)
+
+
+def vendor_gemm(shape, wl):
+    """Time torch.matmul (the vendor BLAS library) on the prefill projection
+    shapes of the workload's model (QKV, O, gate/up, down; M = the prompt
+    tokens of one prefill), bf16 operands and output, X ~ N(0, 1), W ~ N(0,
+    0.02).  A reference point for the hand-written GEMMs only: nothing of it
+    runs in the measured path."""
+    import torch
+    D, H, KV, hd = shape["hidden_size"], shape["num_attention_heads"], shape["num_key_value_heads"], shape["head_dim"]
+    I = shape["intermediate_size"]
+    M = wl["batch"] * wl["prompt_len"] if wl.get("prompt_len") else wl["batch"] * sum(wl["len_range"]) // 2
+    shapes = {"qkv": ((H + 2 * KV) * hd, D), "o": (D, H * hd), "gate/up": (2 * I, D), "down": (D, I)}
+    torch.cuda.set_device(0)
+    g = torch.Generator(device="cuda").manual_seed(0)
+    out = {}
+    for name, (N, K) in shapes.items():
+        W = (torch.randn(N, K, device="cuda", generator=g) * 0.02).to(torch.bfloat16)
+        X = torch.randn(M, K, device="cuda", generator=g).to(torch.bfloat16)
+        for _ in range(3):
+            Y = X @ W.t()
+        torch.cuda.synchronize()
+        reps = 5
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            Y = X @ W.t()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        out[name] = {"N": N, "K": K, "M": M, "ms": round(ms, 4), "tflops": round(2.0 * M * N * K / ms / 1e9, 1)}
+        log(f"vendor GEMM {name} N={N} K={K} M={M}: {ms:.3f} ms, {out[name]['tflops']} TFLOP/s")
+        del W, X, Y
+    print(json.dumps({"vendor_gemm": out, "workload": wl["model"]}))
 
 
 def train_bench(args, wl, shape):
