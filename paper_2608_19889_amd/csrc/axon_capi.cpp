@@ -217,6 +217,7 @@ struct TrainBufs {
   std::vector<TrainLayer> L;
   float *xfin, *logits, *rowloss, *valid, *lserow, *scal, *dx, *dtmp, *dgrow, *dqf, *dkf, *dvf, *dsum, *dqkvf,
       *colpart, *gtmp, *dkh, *dvh;
+  float* statp;     // attention backward: log2-sum-exp and D in packed per-head rows [2][H][W]
   bf16 *hf, *dlog, *dxb, *dgu, *dob, *dqkv, *tra, *trs, *trb, *headT;
 };
 
@@ -1684,6 +1685,7 @@ int train_setup(axon_model* m, hipStream_t s) {
   }
   tb.SP = (c.max_seq + 31) / 32 * 32 + 32;
   tb.W = (int64_t)c.max_batch * tb.SP;
+  if (!r) r = fa(&tb.statp, 2 * H * tb.W);
   if (!r) r = ba(&tb.kr, tb.W * KV * hd);
   if (!r) r = ba(&tb.vr, tb.W * KV * hd);
   if (!r) r = ba(&tb.kt, tb.W * KV * hd);
@@ -1807,7 +1809,7 @@ void enqueue_train(axon_model* m, int B, int T, const int32_t* d_tokens, const i
     dX(t.woT, tb.dxb, D, Hhd, tb.dtmp);
     launch_to_bf16(tb.dtmp, tb.dob, (int64_t)T * Hhd, s);
     m->timed(5, H, B, T, s, [&] {
-      launch_attn_bwd(t.q, kv, t.o, tb.dob, t.lse, tb.dsum, d_cu, h_cu, B, T, H, tb.SP, tb.W, tb.kr, tb.vr, tb.kt,
+      launch_attn_bwd(t.q, kv, t.o, tb.dob, t.lse, tb.dsum, tb.statp, d_cu, h_cu, B, T, H, tb.SP, tb.W, tb.kr, tb.vr, tb.kt,
                       tb.qt, tb.dot, tb.dqf, tb.dkh, tb.dvh, tb.dkf, tb.dvf, s);
     });
     launch_rope_bwd(tb.dqf, tb.dkf, tb.dvf, m->rope_cos, m->rope_sin, d_cu, B, T, H, KV, hd, tb.dqkv,

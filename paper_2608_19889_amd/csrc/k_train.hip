@@ -239,9 +239,15 @@ __global__ void __launch_bounds__(256) colsum_final_kernel(const float* __restri
 
 // ---------------------------------------------------------------- attention
 
-// D[t][h] = sum_d dO[t][h][d] O[t][h][d]
+// D[t][h] = sum_d dO[t][h][d] O[t][h][d]; D and the forward's log2-sum-exp
+// are also copied into the packed per-head rows lsep / dsump [H][W] (column
+// e*SP + position), where the 4 consecutive queries a lane of the dK / dV
+// kernel needs are one 16-byte load
 __global__ void __launch_bounds__(256) attn_bwd_d_kernel(const bf16* __restrict__ dob, const bf16* __restrict__ o,
-                                                         int TH, int hd, float* __restrict__ dsum) {
+                                                         int TH, int hd, float* __restrict__ dsum,
+                                                         const float* __restrict__ lse, const int32_t* __restrict__ cu,
+                                                         int nseq, int H, int SP, int64_t W,
+                                                         float* __restrict__ lsep, float* __restrict__ dsump) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= TH) return;
   const bf16* a = dob + (int64_t)i * hd;
@@ -253,6 +259,11 @@ __global__ void __launch_bounds__(256) attn_bwd_d_kernel(const bf16* __restrict_
     for (int j = 0; j < 8; ++j) s += (float)x[j] * (float)y[j];
   }
   dsum[i] = s;
+  const int t = i / H, h = i % H;
+  const int e = seq_of_token(cu, nseq, t);
+  const int64_t col = (int64_t)h * W + (int64_t)e * SP + (t - cu[e]);
+  lsep[col] = lse[i];
+  dsump[col] = s;
 }
 
 // ---- MFMA attention backward.  v_mfma_f32_32x32x16_bf16 with lane L, half
@@ -375,8 +386,8 @@ template <int HD>
 __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict__ q, const bf16* __restrict__ dob,
                                                           const bf16* __restrict__ kr, const bf16* __restrict__ vr,
                                                           const bf16* __restrict__ qt, const bf16* __restrict__ dot,
-                                                          const float* __restrict__ lse,
-                                                          const float* __restrict__ dsum,
+                                                          const float* __restrict__ lsep,
+                                                          const float* __restrict__ dsump,
                                                           const int32_t* __restrict__ cu, int nseq, int H, int KVh,
                                                           int SP, int64_t W, float* __restrict__ dk,
                                                           float* __restrict__ dv) {
@@ -411,15 +422,23 @@ __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict
         dpq = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(dob + (tq * H + h) * HD + s * 16 + hl * 8),
                                                       vf[s], dpq, 0, 0, 0);
       }
+      // the statistics of queries qb0 + g*8 + hl*4 .. +3 (packed rows; past
+      // the sequence end they are whatever the padding holds, and unused)
+      const int64_t srow = (int64_t)h * W + (int64_t)e * SP + qb0 + hl * 4;
+      f32x4 lq[4], dq4[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        lq[g] = *(const f32x4*)(lsep + srow + g * 8);
+        dq4[g] = *(const f32x4*)(dsump + srow + g * 8);
+      }
       bf16x8 pb[2], dsb[2];
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int qi = qb0 + (i >> 2) * 8 + hl * 4 + (i & 3);
-        const int64_t ti = tok0 + min(qi, S - 1);
         const bool ok = qi < S && mykey <= qi;
-        const float p = ok ? exp2f(sq[i] * sc - lse[ti * H + h]) : 0.f;
+        const float p = ok ? exp2f(sq[i] * sc - lq[i >> 2][i & 3]) : 0.f;
         pb[i >> 3][i & 7] = (bf16)p;
-        dsb[i >> 3][i & 7] = (bf16)(p * (dpq[i] - dsum[ti * H + h]));
+        dsb[i >> 3][i & 7] = ok ? (bf16)(p * (dpq[i] - dq4[i >> 2][i & 3])) : (bf16)0.f;
       }
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
@@ -581,12 +600,14 @@ void launch_colsum(const float* src, int64_t ld, int T, int C, float* part, floa
 }
 
 void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
-                     const int32_t* cu, const int32_t* h_cu, int nseq, int T, int H, int SP, int64_t W,
+                     float* statp, const int32_t* cu, const int32_t* h_cu, int nseq, int T, int H, int SP, int64_t W,
                      bf16* kr, bf16* vr, bf16* kt, bf16* qt, bf16* dot, float* dq, float* dkh, float* dvh, float* dk,
                      float* dv, hipStream_t s) {
   if (T <= 0) return;
   const int KVh = kv.kv_heads, hd = kv.hd, group = H / KVh;
-  attn_bwd_d_kernel<<<(T * H + 255) / 256, 256, 0, s>>>(dob, o, T * H, hd, dsum);
+  float* lsep = statp;
+  float* dsump = statp + (int64_t)H * W;
+  attn_bwd_d_kernel<<<(T * H + 255) / 256, 256, 0, s>>>(dob, o, T * H, hd, dsum, lse, cu, nseq, H, SP, W, lsep, dsump);
   attn_bwd_pack_kernel<<<dim3(T, KVh), 128, 0, s>>>(kv, cu, nseq, SP, kr, vr);
   const int64_t nrows = (int64_t)nseq * SP;  // packed K rows (padding included) -> K^T
   transpose_tile_kernel<<<dim3((unsigned)((nrows + 63) / 64), (KVh * hd + 63) / 64), 256, 0, s>>>(
@@ -601,11 +622,11 @@ void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, c
   float* dvt = group > 1 ? dvh : dv;
   if (hd == 64) {
     attn_bwd_dq_kernel<64><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, kt, lse, dsum, cu, nseq, H, KVh, SP, W, dq);
-    attn_bwd_dkv_kernel<64><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, qt, dot, lse, dsum, cu, nseq, H, KVh, SP,
+    attn_bwd_dkv_kernel<64><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, qt, dot, lsep, dsump, cu, nseq, H, KVh, SP,
                                                            W, dkt, dvt);
   } else {
     attn_bwd_dq_kernel<128><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, kt, lse, dsum, cu, nseq, H, KVh, SP, W, dq);
-    attn_bwd_dkv_kernel<128><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, qt, dot, lse, dsum, cu, nseq, H, KVh, SP,
+    attn_bwd_dkv_kernel<128><<<dim3(blocks, H), 64, 0, s>>>(q, dob, kr, vr, qt, dot, lsep, dsump, cu, nseq, H, KVh, SP,
                                                             W, dkt, dvt);
   }
   if (group > 1) {

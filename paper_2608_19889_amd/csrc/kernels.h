@@ -115,7 +115,8 @@ void launch_colsum(const float* src, int64_t ld, int T, int C, float* part, floa
 // 32, plus 32
 // dkh / dvh [T][H][hd] scratch (the per-head shares of dk / dv)
 void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
-                     const int32_t* cu, const int32_t* h_cu, int nseq, int T, int H, int SP, int64_t W,
+                     float* statp /* [2][H][W] */, const int32_t* cu, const int32_t* h_cu, int nseq, int T, int H,
+                     int SP, int64_t W,
                      bf16* kr, bf16* vr, bf16* kt, bf16* qt, bf16* dot, float* dq, float* dkh, float* dvh, float* dk,
                      float* dv, hipStream_t s);
 // back through RoPE into the fused QKV row order (bf16) and the original order
