@@ -301,7 +301,7 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
 // with DNW wavefronts; the group's query heads are the columns of
 // v_mfma_f32_16x16x32_bf16 (up to 16 heads per group); the wavefronts take
 // the split's 32-key chunks in turn, with K and V^T loaded straight from HBM
-// into registers, several chunks in flight per wavefront.  The
+// into registers, NBUF chunks in flight per wavefront.  The
 // wavefronts' (max, sum, o) are merged in LDS; with one split the normalized
 // output is written directly, otherwise every split stores an unnormalized
 // partial and the combine kernel merges them.
