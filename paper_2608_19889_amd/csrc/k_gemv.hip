@@ -720,18 +720,31 @@ __global__ void __launch_bounds__(256) gemv_split_resid_kernel(GemvArgs a, int n
 
 // next[t] = index of the largest partial maximum (lowest index on ties);
 // len[t] += 1 when ``len`` is set.
-__global__ void __launch_bounds__(256) argmax_final_kernel(const float* __restrict__ val,
-                                                           const int32_t* __restrict__ idx, int nparts,
-                                                           int32_t* __restrict__ next, int32_t* __restrict__ len) {
-  __shared__ float sv[4];
-  __shared__ int si[4];
+__global__ void __launch_bounds__(1024) argmax_final_kernel(const float* __restrict__ val,
+                                                            const int32_t* __restrict__ idx, int nparts,
+                                                            int32_t* __restrict__ next, int32_t* __restrict__ len) {
+  __shared__ float sv[16];
+  __shared__ int si[16];
   const int t = blockIdx.x;
   float best = -INFINITY;
   int bi = 0x7fffffff;
-  for (int j = threadIdx.x; j < nparts; j += blockDim.x) {
-    const float v = val[(int64_t)t * nparts + j];
-    const int i = idx[(int64_t)t * nparts + j];
-    if (v > best || (v == best && i < bi)) { best = v; bi = i; }
+  // 4 independent partial loads per thread and round (a compare-as-you-load
+  // loop waits for every load in turn); the order of the candidates does
+  // not matter: the largest value wins, ties go to the lowest index
+  const float* vr = val + (int64_t)t * nparts;
+  const int32_t* ir = idx + (int64_t)t * nparts;
+  for (int j0 = threadIdx.x; j0 < nparts; j0 += 4 * 1024) {
+    float v[4];
+    int i[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = min(j0 + u * 1024, nparts - 1);
+      v[u] = vr[j];
+      i[u] = ir[j];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (v[u] > best || (v[u] == best && i[u] < bi)) { best = v[u]; bi = i[u]; }
   }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
@@ -742,7 +755,7 @@ __global__ void __launch_bounds__(256) argmax_final_kernel(const float* __restri
   if ((threadIdx.x & 63) == 0) { sv[threadIdx.x >> 6] = best; si[threadIdx.x >> 6] = bi; }
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int w = 1; w < 4; ++w)
+    for (int w = 1; w < 16; ++w)
       if (sv[w] > best || (sv[w] == best && si[w] < bi)) { best = sv[w]; bi = si[w]; }
     next[t] = bi == 0x7fffffff ? 0 : bi;
     if (len) len[t] += 1;
@@ -988,7 +1001,7 @@ bool launch_gemv_grouped(const GemvArgs& a, int epi, int n_experts, hipStream_t 
 void launch_argmax_final(const float* val, const int32_t* idx, int nparts, int M, int32_t* next, int32_t* len,
                          hipStream_t s) {
   if (M <= 0) return;
-  argmax_final_kernel<<<M, 256, 0, s>>>(val, idx, nparts, next, len);
+  argmax_final_kernel<<<M, 1024, 0, s>>>(val, idx, nparts, next, len);
 }
 
 void launch_embed_ss(const int32_t* tok, const bf16* emb, const bf16* g, float* x, bf16* xg, float* ss_out, int M,
