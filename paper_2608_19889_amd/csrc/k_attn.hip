@@ -505,13 +505,34 @@ __global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restric
   const int lo = (window ? max(0, ctx - window) : 0) & ~31;  // as the attention kernel's first split
   const int nact = min(nsplit, (ctx - lo + split_len - 1) / split_len);
   const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
+  // 8 independent loads per round (a load-then-use loop waits for every
+  // load in turn); the sums still run in split order
   float M = -INFINITY;
-  for (int sp = 0; sp < nact; ++sp) M = fmaxf(M, pp[sp * (HD + 2) + HD]);
+  for (int b0 = 0; b0 < nact; b0 += 8) {
+    float mv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) mv[u] = pp[min(b0 + u, nact - 1) * (HD + 2) + HD];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (b0 + u < nact) M = fmaxf(M, mv[u]);
+  }
   float L = 0.f, O = 0.f;
-  for (int sp = 0; sp < nact; ++sp) {
-    const float f = exp2f(pp[sp * (HD + 2) + HD] - M);
-    L += f * pp[sp * (HD + 2) + HD + 1];
-    O += f * pp[sp * (HD + 2) + d];
+  for (int b0 = 0; b0 < nact; b0 += 8) {
+    float mv[8], lv[8], ov[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float* ps = pp + min(b0 + u, nact - 1) * (HD + 2);
+      mv[u] = ps[HD];
+      lv[u] = ps[HD + 1];
+      ov[u] = ps[d];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (b0 + u < nact) {
+        const float f = exp2f(mv[u] - M);
+        L += f * lv[u];
+        O += f * ov[u];
+      }
   }
   o[((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
 }
