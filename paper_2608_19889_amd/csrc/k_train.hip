@@ -112,13 +112,27 @@ __global__ void __launch_bounds__(256) ce_grad_kernel(const float* __restrict__ 
 
 // ---------------------------------------------------------------- layouts
 
+// Element offset of (row c, column col) of a [C][dld] matrix stored in the
+// A-operand fragments of the attention backward's Q^T / dO^T / K^T products
+// (C and dld multiples of 32): fragment (c / 32, col / 32, kk) is 1 KB of 64
+// lanes x 8 values, lane hl * 32 + c % 32 holding the block's columns kk * 16 +
+// kap(hl, j), j = 0..7, kap(hl, j) = (j / 4) * 8 + 4 hl + j % 4 (the order of
+// the dS / P operand it multiplies), so a wavefront's fragment is one
+// contiguous read.
+AXON_DEV int64_t frag_off(int64_t c, int64_t col, int64_t dld) {
+  const int q = (int)(col & 31), kk = q >> 4, r16 = q & 15;
+  const int hl = (r16 >> 2) & 1, j = (r16 >> 3) * 4 + (r16 & 3);
+  return ((((c >> 5) * (dld >> 5) + (col >> 5)) * 2 + kk) * 64 + hl * 32 + (c & 31)) * 8 + j;
+}
+
 // dst[c][col(t)] = src[t][c] through a 64 x 64 LDS tile, both sides
 // coalesced: rows t < T are read (rows T .. Tmax-1 give zeros), col(t) = t,
 // or with cu: e * SP + (t - cu[e]) for t's sequence e (t < T only).  C % 4
-// == 0, ld % 4 == 0.
+// == 0, ld % 4 == 0.  frag: dst in the fragment order of frag_off.
 __global__ void __launch_bounds__(256) transpose_tile_kernel(const bf16* __restrict__ src, int64_t ld, int T, int Tmax,
                                                              int C, bf16* __restrict__ dst, int64_t dld,
-                                                             const int32_t* __restrict__ cu, int nseq, int SP) {
+                                                             const int32_t* __restrict__ cu, int nseq, int SP,
+                                                             bool frag = false) {
   __shared__ bf16 tile[64][66];
   const int t0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
   const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
@@ -144,7 +158,7 @@ __global__ void __launch_bounds__(256) transpose_tile_kernel(const bf16* __restr
         const int e = seq_of_token(cu, nseq, t);
         col = (int64_t)e * SP + (t - cu[e]);
       }
-      dst[(int64_t)c * dld + col] = tile[tx * 4 + j][ty + 16 * r];
+      dst[frag ? frag_off(c, col, dld) : (int64_t)c * dld + col] = tile[tx * 4 + j][ty + 16 * r];
     }
   }
 }
@@ -357,9 +371,9 @@ __global__ void __launch_bounds__(64) attn_bwd_dq_kernel(const bf16* __restrict_
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int b = 0; b < HD / 32; ++b) {
-        const bf16* ktr = kt + ((int64_t)kvh * HD + b * 32 + c) * W + (int64_t)e * SP + kb0 + kk * 16 + hl * 4;
-        const bf16x4 lo = *(const bf16x4*)ktr, hi = *(const bf16x4*)(ktr + 8);
-        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const bf16x8 a =
+            *(const bf16x8*)(kt + frag_off((int64_t)kvh * HD + b * 32 + c, (int64_t)e * SP + kb0 + kk * 16, W) +
+                             hl * 256);
         acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[kk], acc[b], 0, 0, 0);
       }
   }
@@ -444,11 +458,9 @@ __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict
       for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
         for (int b = 0; b < HD / 32; ++b) {
-          const int64_t off = ((int64_t)h * HD + b * 32 + c) * W + (int64_t)e * SP + qb0 + kk * 16 + hl * 4;
-          const bf16x4 olo = *(const bf16x4*)(dot + off), ohi = *(const bf16x4*)(dot + off + 8);
-          const bf16x4 qlo = *(const bf16x4*)(qt + off), qhi = *(const bf16x4*)(qt + off + 8);
-          const bf16x8 ao = {olo[0], olo[1], olo[2], olo[3], ohi[0], ohi[1], ohi[2], ohi[3]};
-          const bf16x8 aq = {qlo[0], qlo[1], qlo[2], qlo[3], qhi[0], qhi[1], qhi[2], qhi[3]};
+          const int64_t off = frag_off((int64_t)h * HD + b * 32 + c, (int64_t)e * SP + qb0 + kk * 16, W) + hl * 256;
+          const bf16x8 ao = *(const bf16x8*)(dot + off);
+          const bf16x8 aq = *(const bf16x8*)(qt + off);
           avv[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ao, pb[kk], avv[b], 0, 0, 0);
           akk[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, dsb[kk], akk[b], 0, 0, 0);
         }
@@ -611,11 +623,11 @@ void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, c
   attn_bwd_pack_kernel<<<dim3(T, KVh), 128, 0, s>>>(kv, cu, nseq, SP, kr, vr);
   const int64_t nrows = (int64_t)nseq * SP;  // packed K rows (padding included) -> K^T
   transpose_tile_kernel<<<dim3((unsigned)((nrows + 63) / 64), (KVh * hd + 63) / 64), 256, 0, s>>>(
-      kr, (int64_t)KVh * hd, (int)nrows, (int)nrows, KVh * hd, kt, W, nullptr, 0, 0);
+      kr, (int64_t)KVh * hd, (int)nrows, (int)nrows, KVh * hd, kt, W, nullptr, 0, 0, true);
   transpose_tile_kernel<<<dim3((T + 63) / 64, (H * hd + 63) / 64), 256, 0, s>>>(q, (int64_t)H * hd, T, T, H * hd, qt,
-                                                                                 W, cu, nseq, SP);
+                                                                                 W, cu, nseq, SP, true);
   transpose_tile_kernel<<<dim3((T + 63) / 64, (H * hd + 63) / 64), 256, 0, s>>>(dob, (int64_t)H * hd, T, T, H * hd,
-                                                                                 dot, W, cu, nseq, SP);
+                                                                                 dot, W, cu, nseq, SP, true);
   int blocks = 0;
   for (int e = 0; e < nseq; ++e) blocks += (h_cu[e + 1] - h_cu[e] + 31) / 32;
   float* dkt = group > 1 ? dkh : dk;  // per-head shares, summed below when a group has several heads
