@@ -293,21 +293,34 @@ __global__ void __launch_bounds__(256) attn_bwd_d_kernel(const bf16* __restrict_
 //
 // Packed copies, per sequence e at columns / rows e*SP + position (SP = the
 // longest sequence rounded up to 32, plus 32 positions of finite padding, so
-// a block's reads past its sequence end stay inside the sequence's range):
-//   kr, vr [B*SP][KV][hd]  K and V rows      qt, dot [H*hd][B*SP]  Q^T, dO^T
-//   kt [KV*hd][B*SP]       K^T
+// a block's reads past its sequence end stay inside the sequence's range;
+// W = the packed width), every one stored in MFMA fragment order so that a
+// wavefront's operand fragment is one contiguous 1 KB read:
+//   kr, vr  K and V rows (row_frag_off: fragment = 32 positions x 16 dims)
+//   qt, dot, kt  Q^T, dO^T [H*hd][W], K^T [KV*hd][W] (frag_off)
 
-// the layer's K / V rows from the cache into kr / vr (row e*SP + position);
-// grid (token, kv head), one thread per head dimension
+// Element offset of dimension d of packed row col of kv head g in kr / vr:
+// fragment (g, col / 32, d / 16) holds lane (d % 16) / 8 * 32 + col % 32,
+// values d % 8 (the A / B operand lane order of a 32-row x 16-k fragment)
+AXON_DEV int64_t row_frag_off(int64_t g, int64_t col, int d, int hd, int64_t W) {
+  return (((g * (W >> 5) + (col >> 5)) * (hd >> 4) + (d >> 4)) * 64 + ((d & 15) >> 3) * 32 + (col & 31)) * 8 + (d & 7);
+}
+
+// the layer's K / V rows from the cache into kr / vr (row e*SP + position)
+// and K^T into kt; grid (token, kv head), one thread per head dimension
 __global__ void __launch_bounds__(128) attn_bwd_pack_kernel(KVView kv, const int32_t* __restrict__ cu, int nseq,
-                                                            int SP, bf16* __restrict__ kr, bf16* __restrict__ vr) {
+                                                            int SP, int64_t W, bf16* __restrict__ kr,
+                                                            bf16* __restrict__ vr, bf16* __restrict__ kt) {
   const int t = blockIdx.x, h = blockIdx.y, d = threadIdx.x, hd = kv.hd, KVh = kv.kv_heads;
   if (d >= hd) return;
   const int e = seq_of_token(cu, nseq, t);
   const int p = t - cu[e];
   const int64_t col = (int64_t)e * SP + p;
-  kr[(col * KVh + h) * hd + d] = ((const bf16*)kv.k)[k_el(kv, e, h, p, d)];
-  vr[(col * KVh + h) * hd + d] = ((const bf16*)kv.v)[v_el(kv, e, h, p, d)];
+  (void)KVh;
+  const bf16 kval = ((const bf16*)kv.k)[k_el(kv, e, h, p, d)];
+  kr[row_frag_off(h, col, d, hd, W)] = kval;
+  kt[frag_off((int64_t)h * hd + d, col, W)] = kval;
+  vr[row_frag_off(h, col, d, hd, W)] = ((const bf16*)kv.v)[v_el(kv, e, h, p, d)];
 }
 
 AXON_DEV int kap(int hl, int j) { return (j >> 2) * 8 + hl * 4 + (j & 3); }
@@ -354,11 +367,11 @@ __global__ void __launch_bounds__(64) attn_bwd_dq_kernel(const bf16* __restrict_
   const int kend = min(S, q0 + 32);
   for (int kb0 = 0; kb0 < kend; kb0 += 32) {
     f32x16 st = {}, dpt = {};
-    const int64_t krow = (((int64_t)e * SP + kb0 + c) * KVh + kvh) * HD + hl * 8;
+    const int64_t kfr = ((int64_t)kvh * (W >> 5) + (((int64_t)e * SP + kb0) >> 5)) * (HD / 16) * 512 + lane * 8;
 #pragma unroll
     for (int s = 0; s < HD / 16; ++s) {
-      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(kr + krow + s * 16), qf[s], st, 0, 0, 0);
-      dpt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(vr + krow + s * 16), df[s], dpt, 0, 0, 0);
+      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(kr + kfr + s * 512), qf[s], st, 0, 0, 0);
+      dpt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(vr + kfr + s * 512), df[s], dpt, 0, 0, 0);
     }
     bf16x8 dsb[2];
 #pragma unroll
@@ -412,11 +425,12 @@ __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict
   const int lane = threadIdx.x, hl = lane >> 5, c = lane & 31;
   const int mykey = kb0 + c;
   bf16x8 kf[HD / 16], vf[HD / 16];
-  const int64_t krow = (((int64_t)e * SP + mykey) * KVh + kvh) * HD + hl * 8;  // padded rows past the sequence
+  // this lane's key mykey (padded rows past the sequence), fragments of 16 dims
+  const int64_t kfr = ((int64_t)kvh * (W >> 5) + (((int64_t)e * SP + kb0) >> 5)) * (HD / 16) * 512 + lane * 8;
 #pragma unroll
   for (int s = 0; s < HD / 16; ++s) {
-    kf[s] = *(const bf16x8*)(kr + krow + s * 16);
-    vf[s] = *(const bf16x8*)(vr + krow + s * 16);
+    kf[s] = *(const bf16x8*)(kr + kfr + s * 512);
+    vf[s] = *(const bf16x8*)(vr + kfr + s * 512);
   }
   const float sc = LOG2E / sqrtf((float)HD);
   f32x16 akk[HD / 32], avv[HD / 32];
@@ -620,10 +634,7 @@ void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, c
   float* lsep = statp;
   float* dsump = statp + (int64_t)H * W;
   attn_bwd_d_kernel<<<(T * H + 255) / 256, 256, 0, s>>>(dob, o, T * H, hd, dsum, lse, cu, nseq, H, SP, W, lsep, dsump);
-  attn_bwd_pack_kernel<<<dim3(T, KVh), 128, 0, s>>>(kv, cu, nseq, SP, kr, vr);
-  const int64_t nrows = (int64_t)nseq * SP;  // packed K rows (padding included) -> K^T
-  transpose_tile_kernel<<<dim3((unsigned)((nrows + 63) / 64), (KVh * hd + 63) / 64), 256, 0, s>>>(
-      kr, (int64_t)KVh * hd, (int)nrows, (int)nrows, KVh * hd, kt, W, nullptr, 0, 0, true);
+  attn_bwd_pack_kernel<<<dim3(T, KVh), 128, 0, s>>>(kv, cu, nseq, SP, W, kr, vr, kt);
   transpose_tile_kernel<<<dim3((T + 63) / 64, (H * hd + 63) / 64), 256, 0, s>>>(q, (int64_t)H * hd, T, T, H * hd, qt,
                                                                                  W, cu, nseq, SP, true);
   transpose_tile_kernel<<<dim3((T + 63) / 64, (H * hd + 63) / 64), 256, 0, s>>>(dob, (int64_t)H * hd, T, T, H * hd,
