@@ -34,11 +34,24 @@ greedy ties go to the lowest index.
 ``io_round="bf16"`` is a diagnostic mode that rounds to bfloat16 at the points
 where the GPU path stores bf16 (normed activations, rotated q/k, v, attention
 output, gated MLP activation) and keeps the residual stream in float32.  The
-reference mode is ``io_round=None`` (everything float64).
+reference mode is ``io_round=None`` (everything float64).  Each rounding point
+is a named site (``BF16_SITES``, ``F32_SITES``); ``io_skip`` leaves the named
+sites unrounded and ``io_applied`` records the sites a run actually rounded,
+so that the set of rounding points can be checked and each one's share of the
+error measured.
 """
 from __future__ import annotations
 
 import numpy as np
+
+# Rounding sites of the bf16-storage mode: bf16 where the GPU stores an
+# activation in bf16 (the RMSNorm / LayerNorm outputs that feed a projection,
+# the rotated query and key and the value as stored in the KV cache, the
+# attention output, the gated MLP activation, the final norm's output), float32
+# for the residual stream (the embedding row and the stream after each residual
+# add).
+BF16_SITES = ("norm_in", "q", "k", "v", "attn_out", "norm_post", "mlp_act", "final_norm")
+F32_SITES = ("resid",)
 
 
 # --------------------------------------------------------------------------
@@ -214,7 +227,7 @@ class OracleDecoder:
     (any model) limits each query to its last W keys.
     """
 
-    def __init__(self, cfg: dict, weights: dict, io_round: str | None = None):
+    def __init__(self, cfg: dict, weights: dict, io_round: str | None = None, io_skip=()):
         self.cfg = cfg
         self.D = cfg["hidden_size"]
         self.L = cfg["num_hidden_layers"]
@@ -232,24 +245,40 @@ class OracleDecoder:
         else:
             self.lm_head = self.w["model.embed_tokens.weight"] if cfg["tie_word_embeddings"] \
                 else self.w["lm_head.weight"]
-        if io_round is None:
-            self._r = lambda a: a
-            self._rx = lambda a: a
-        elif io_round == "bf16":
-            self._r = round_to_bf16
-            self._rx = round_to_f32
-        else:
+        if io_round not in (None, "bf16"):
             raise ValueError(io_round)
+        unknown = set(io_skip) - set(BF16_SITES) - set(F32_SITES)
+        if unknown:
+            raise ValueError(f"unknown rounding sites {sorted(unknown)}")
+        self.io_round = io_round
+        self.io_skip = frozenset(io_skip)
+        self.io_applied: set[str] = set()
         self.caches: list[list[tuple[np.ndarray, np.ndarray]]] = []
         self.n_experts = int(cfg.get("n_routed_experts") or 0)
         self.first_moe = int(cfg.get("first_k_dense_replace") or 0)
+
+    # ---- rounding at the GPU's storage points (bf16-storage mode only) ----
+    def _r(self, a: np.ndarray, site: str) -> np.ndarray:
+        if self.io_round is None or site in self.io_skip:
+            return a
+        self.io_applied.add(site)
+        return round_to_bf16(a)
+
+    def _rx(self, a: np.ndarray) -> np.ndarray:
+        if self.io_round is None or "resid" in self.io_skip:
+            return a
+        self.io_applied.add("resid")
+        return round_to_f32(a)
+
+    def _r_act(self, a: np.ndarray) -> np.ndarray:
+        return self._r(a, "mlp_act")
 
     # ---- one layer over the new tokens of one sequence ----
     def _layer(self, i: int, x: np.ndarray, pos: np.ndarray, cache: list) -> np.ndarray:
         p = f"model.layers.{i}."
         w = self.w
         s = x.shape[0]
-        h = self._r(rms_norm(x, w[p + "input_layernorm.weight"], self.eps))
+        h = self._r(rms_norm(x, w[p + "input_layernorm.weight"], self.eps), "norm_in")
         q = h @ w[p + "self_attn.q_proj.weight"].T
         k = h @ w[p + "self_attn.k_proj.weight"].T
         v = h @ w[p + "self_attn.v_proj.weight"].T
@@ -261,16 +290,16 @@ class OracleDecoder:
         k = k.reshape(s, self.KV, self.hd)
         v = v.reshape(s, self.KV, self.hd)
         cos, sin = rope_cos_sin(pos, self.hd, self.theta)
-        q = self._r(apply_rope(q, cos, sin))
-        k = self._r(apply_rope(k, cos, sin))
-        v = self._r(v)
+        q = self._r(apply_rope(q, cos, sin), "q")
+        k = self._r(apply_rope(k, cos, sin), "k")
+        v = self._r(v, "v")
         kc, vc = cache[i]
         kc = np.concatenate([kc, k], axis=0)
         vc = np.concatenate([vc, v], axis=0)
         cache[i] = (kc, vc)
-        o = self._r(causal_gqa_attention(q, kc, vc, pos, self.window)).reshape(s, self.H * self.hd)
+        o = self._r(causal_gqa_attention(q, kc, vc, pos, self.window), "attn_out").reshape(s, self.H * self.hd)
         x = self._rx(x + o @ w[p + "self_attn.o_proj.weight"].T)
-        h2 = self._r(rms_norm(x, w[p + "post_attention_layernorm.weight"], self.eps))
+        h2 = self._r(rms_norm(x, w[p + "post_attention_layernorm.weight"], self.eps), "norm_post")
         if self.n_experts and i >= self.first_moe:
             c = self.cfg
             ex = [tuple(w[p + f"mlp.experts.{e}.{n}_proj.weight"] for n in ("gate", "up", "down"))
@@ -278,30 +307,30 @@ class OracleDecoder:
             sh = tuple(w[p + f"mlp.shared_experts.{n}_proj.weight"] for n in ("gate", "up", "down")) \
                 if c.get("n_shared_experts") else None
             mlp = moe_mlp(h2, w[p + "mlp.gate.weight"], ex, sh, int(c["num_experts_per_tok"]),
-                          bool(c.get("norm_topk_prob")), rnd=self._r)
+                          bool(c.get("norm_topk_prob")), rnd=self._r_act)
         else:
             mlp = swiglu_mlp(h2, w[p + "mlp.gate_proj.weight"], w[p + "mlp.up_proj.weight"],
-                             w[p + "mlp.down_proj.weight"], rnd=self._r)
+                             w[p + "mlp.down_proj.weight"], rnd=self._r_act)
         return self._rx(x + mlp)
 
     def _layer_gpt2(self, i: int, x: np.ndarray, pos: np.ndarray, cache: list) -> np.ndarray:
         p = f"transformer.h.{i}."
         w = self.w
         s, D = x.shape
-        h = self._r(layer_norm(x, w[p + "ln_1.weight"], w[p + "ln_1.bias"], self.eps))
+        h = self._r(layer_norm(x, w[p + "ln_1.weight"], w[p + "ln_1.bias"], self.eps), "norm_in")
         qkv = h @ w[p + "attn.c_attn.weight"] + w[p + "attn.c_attn.bias"]
-        q = self._r(qkv[:, :D].reshape(s, self.H, self.hd))
-        k = self._r(qkv[:, D:2 * D].reshape(s, self.KV, self.hd))
-        v = self._r(qkv[:, 2 * D:].reshape(s, self.KV, self.hd))
+        q = self._r(qkv[:, :D].reshape(s, self.H, self.hd), "q")
+        k = self._r(qkv[:, D:2 * D].reshape(s, self.KV, self.hd), "k")
+        v = self._r(qkv[:, 2 * D:].reshape(s, self.KV, self.hd), "v")
         kc, vc = cache[i]
         kc = np.concatenate([kc, k], axis=0)
         vc = np.concatenate([vc, v], axis=0)
         cache[i] = (kc, vc)
-        o = self._r(causal_gqa_attention(q, kc, vc, pos, self.window)).reshape(s, D)
+        o = self._r(causal_gqa_attention(q, kc, vc, pos, self.window), "attn_out").reshape(s, D)
         x = self._rx(x + o @ w[p + "attn.c_proj.weight"] + w[p + "attn.c_proj.bias"])
-        h2 = self._r(layer_norm(x, w[p + "ln_2.weight"], w[p + "ln_2.bias"], self.eps))
+        h2 = self._r(layer_norm(x, w[p + "ln_2.weight"], w[p + "ln_2.bias"], self.eps), "norm_post")
         mlp = gelu_mlp(h2, w[p + "mlp.c_fc.weight"], w[p + "mlp.c_fc.bias"], w[p + "mlp.c_proj.weight"],
-                       w[p + "mlp.c_proj.bias"], rnd=self._r)
+                       w[p + "mlp.c_proj.bias"], rnd=self._r_act)
         return self._rx(x + mlp)
 
     def _forward_seq(self, b: int, ids: np.ndarray, all_logits: bool) -> np.ndarray:
@@ -321,9 +350,9 @@ class OracleDecoder:
         if not all_logits:
             x = x[-1:]
         if self.gpt2:
-            hf = self._r(layer_norm(x, self.w["transformer.ln_f.weight"], self.w["transformer.ln_f.bias"], self.eps))
+            hf = self._r(layer_norm(x, self.w["transformer.ln_f.weight"], self.w["transformer.ln_f.bias"], self.eps), "final_norm")
         else:
-            hf = self._r(rms_norm(x, self.w["model.norm.weight"], self.eps))
+            hf = self._r(rms_norm(x, self.w["model.norm.weight"], self.eps), "final_norm")
         return hf @ self.lm_head.T
 
     def _empty_cache(self):

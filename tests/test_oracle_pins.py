@@ -355,6 +355,44 @@ def test_io_round_mode_stays_close_to_exact():
     assert 0 < np.max(np.abs(a - b)) < 2e-2
 
 
+def test_io_round_sites_are_the_documented_ones_and_each_is_live():
+    """The bf16-storage mode rounds at exactly the documented sites (the GPU's
+    bf16 storage points: normed projection inputs, rotated q and k, v, the
+    attention output, the gated activation, the final norm; float32 residual
+    stream).  Each bf16 site alone moves the logits away from the exact ones,
+    removing any one changes the result, and the error of the full mode is the
+    sum of the single sites' errors (as variances of independent rounding
+    errors, within 25%): nothing outside the listed sites adds error, so the
+    tolerance band that this mode sets is made of these roundings only.  With
+    every site removed the mode is the exact oracle."""
+    from oracle.decoder import BF16_SITES, F32_SITES
+    every = set(BF16_SITES) | set(F32_SITES)
+    shp = _tiny("qwen", dtype="bf16")
+    shp.update(num_attention_heads=8, num_key_value_heads=2, head_dim=16)
+    w = _np_weights(shp)
+    seqs = [np.random.default_rng(5).integers(0, shp["vocab_size"], 24) for _ in range(2)]
+
+    def run(skip):
+        o = OracleDecoder(shp, w, io_round="bf16", io_skip=skip)
+        out = np.concatenate(o.prefill(seqs, all_logits=True))
+        assert o.io_applied == every - set(skip)
+        return out
+
+    exact = np.concatenate(OracleDecoder(shp, w).prefill(seqs, all_logits=True))
+    np.testing.assert_array_equal(run(every), exact)
+    full = run(set())
+    mse_full = np.mean((full - exact) ** 2)
+    parts = 0.0
+    for site in BF16_SITES:
+        assert not np.array_equal(run({site}), full), f"rounding site {site} has no effect"
+        only = np.mean((run(every - {site}) - exact) ** 2)
+        assert only > 0, site
+        parts += only
+    assert 0.75 < parts / mse_full < 1.25, parts / mse_full
+    with pytest.raises(ValueError):
+        OracleDecoder(shp, w, io_round="bf16", io_skip={"residual_bf16"})
+
+
 # ----------------------------------------------------------- mixture of experts
 
 def _moe_weights(D, E, I, shared_I, seed):
