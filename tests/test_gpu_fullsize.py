@@ -1,78 +1,22 @@
-"""GPU parity at the workloads' full sizes.
+"""GPU properties at the workloads' sizes that hold without the oracle.
 
-* The 1B workload in the launch configuration bench.py times (8 sequences of
-  512 prompt tokens, all 16 layers, the full vocabulary): the oracle computes
-  the outputs of sequence 0 only, one by one.
-* The 7B shape at full depth and width with short prompts against the oracle.
-  At full depth the bf16 path's logits are as far from the exact oracle as
-  bf16 storage of the activations alone makes them (error amplified through
-  16-28 layers, up to 0.19 max at 7B): these tests hold it to that band.
-* The float32 check mode (the same bf16-valued weights in float32) at full
-  depth: logits within 1e-4 of the exact oracle and identical greedy tokens
-  over 16 decode steps.
-* Properties that hold at any size, checked bit for bit where the arithmetic is
-  identical: the paged cache equals the contiguous one; a sequence's logits do
-  not depend on the other sequences of its batch; the graph-replayed decode
-  step equals the eager one.  And, across kernels, the decode step's logits
-  agree with the all-positions prefill of the same tokens.
+Checked bit for bit where the arithmetic is identical: the paged cache equals
+the contiguous one (7B shape, ragged prompts, permuted pages); a sequence's
+logits do not depend on the other sequences of its batch; the graph-replayed
+decode step equals the eager one.  Across kernels, the decode step's logits
+agree with the all-positions prefill of the same tokens.  Capacity errors are
+reported without side effects.  (Oracle parity at the workloads' own sizes is
+in test_gpu_atsize.py.)
 """
 import numpy as np
 import pytest
 import torch
 
-import oracle
 from paper_2608_19889_amd.axon import AxonError, Model
-from parity_util import (BF16_MAX, BF16_MEAN, F32_MAX, check_argmax, check_bf16, check_logits, pack, run_free,
-                         run_teacher_forced)
+from parity_util import BF16_MAX, BF16_MEAN, F32_MAX, check_logits, pack
 from synthetic import MODEL_SHAPES, model_weights, paged_workload, prompts, small_shape
 
 pytestmark = pytest.mark.gpu
-
-
-def _oracles(shape, w_cpu):
-    w64 = oracle.weights_f64(w_cpu)
-    return (oracle.OracleDecoder(shape, w64), oracle.OracleDecoder(shape, w64, io_round="bf16"))
-
-
-def test_1b_bench_configuration_sequence0():
-    shape = MODEL_SHAPES["1b"]
-    B, P, steps = 8, 512, 3
-    w = model_weights(shape, seed=0, device="cuda")
-    ids = prompts(B, P, shape["vocab_size"], seed=0).numpy()
-    exact, b16 = _oracles(shape, {k: v.cpu() for k, v in w.items()})
-    ref_tok, ref_lg = oracle.generate_greedy(exact, [ids[0]], steps)
-    ref_b = oracle.teacher_forced(b16, [ids[0]], ref_tok[:, :steps])
-    m = Model(shape, w, max_batch=B, max_seq=P + 128, max_tokens=B * P)
-    flat, cu = pack(list(ids))
-    lg, nxt = m.prefill(flat, cu)
-    got = [lg[0].cpu().double().numpy()]
-    for s in range(steps):
-        tok = nxt.clone()
-        tok[0] = int(ref_tok[0, s])  # sequence 0 follows the oracle; the others their own argmax
-        lg = torch.empty((B, shape["vocab_size"]), dtype=torch.float32, device="cuda")
-        _, nxt = m.decode_step(tok, logits=lg)
-        got.append(lg[0].cpu().double().numpy())
-    torch.cuda.synchronize()
-    got = np.stack(got)[:, None, :]
-    mx = check_bf16(got, ref_lg, ref_b, "1b bench configuration, sequence 0", absolute=False)
-    check_argmax(got, ref_lg, mx, "1b bench configuration, sequence 0")
-    m.close()
-
-
-def test_7b_full_depth_short_prompts():
-    shape = MODEL_SHAPES["7b"]
-    steps = 3
-    w = model_weights(shape, seed=0, device="cuda")
-    ids = prompts(2, 13, shape["vocab_size"], seed=3).numpy()
-    seqs = [ids[0], ids[1, :7]]
-    exact, b16 = _oracles(shape, {k: v.cpu() for k, v in w.items()})
-    ref_tok, ref_lg = oracle.generate_greedy(exact, seqs, steps)
-    ref_b = oracle.teacher_forced(b16, seqs, ref_tok[:, :steps])
-    m = Model(shape, w, max_batch=2, max_seq=64)
-    lg, _ = run_teacher_forced(m, seqs, ref_tok[:, :steps])
-    mx = check_bf16(lg, ref_lg, ref_b, "7b full depth", absolute=False)
-    check_argmax(lg, ref_lg, mx, "7b full depth")
-    m.close()
 
 
 def test_7b_paged_equals_contiguous_bitwise():
@@ -177,26 +121,6 @@ def test_decode_logits_agree_with_all_positions_prefill(mode):
         check_logits(got, want, F32_MAX, None, "decode vs all-positions prefill (f32)")
     else:
         check_logits(got, want, BF16_MAX, BF16_MEAN, "decode vs all-positions prefill (bf16)")
-    m.close()
-
-
-@pytest.mark.parametrize("base", ["1b", "7b"])
-def test_f32_check_mode_full_depth(base):
-    """The paper's fallback precision at full size: the bf16-valued weights held
-    in float32 reproduce the float64 oracle's logits to 1e-4 and its greedy
-    tokens over the first 16 decode steps."""
-    shape = dict(MODEL_SHAPES[base], dtype="f32")
-    steps = 16
-    w = {k: v.float() for k, v in model_weights(MODEL_SHAPES[base], seed=12, device="cuda").items()}
-    ids = prompts(2, 11, shape["vocab_size"], seed=13).numpy()
-    seqs = [ids[0], ids[1, :6]]
-    ref_tok, ref_lg = oracle.generate_greedy(oracle.OracleDecoder(shape, {k: v.cpu() for k, v in w.items()}),
-                                             seqs, steps)
-    m = Model(shape, w, max_batch=2, max_seq=32)
-    lg, _ = run_teacher_forced(m, seqs, ref_tok[:, :steps])
-    mx = check_logits(lg, ref_lg, F32_MAX, None, f"{base} f32 check mode, full depth")
-    check_argmax(lg, ref_lg, mx, f"{base} f32 check mode, full depth")
-    np.testing.assert_array_equal(run_free(m, seqs, steps), ref_tok)
     m.close()
 
 
