@@ -1809,8 +1809,10 @@ void enqueue_train(axon_model* m, int B, int T, const int32_t* d_tokens, const i
     dX(t.woT, tb.dxb, D, Hhd, tb.dtmp);
     launch_to_bf16(tb.dtmp, tb.dob, (int64_t)T * Hhd, s);
     m->timed(5, H, B, T, s, [&] {
-      launch_attn_bwd(t.q, kv, t.o, tb.dob, t.lse, tb.dsum, tb.statp, d_cu, h_cu, B, T, H, tb.SP, tb.W, tb.kr, tb.vr, tb.kt,
-                      tb.qt, tb.dot, tb.dqf, tb.dkh, tb.dvh, tb.dkf, tb.dvf, s);
+      if (!launch_attn_bwd(t.q, kv, t.o, tb.dob, t.lse, tb.dsum, tb.statp, d_cu, h_cu, B, T, H, tb.SP, tb.W, tb.kr, tb.vr, tb.kt,
+                      tb.qt, tb.dot, tb.dqf, tb.dkh, tb.dvh, tb.dkf, tb.dvf, s) &&
+          m->enqueue_err.empty())
+        m->enqueue_err = "attention backward: packed layout does not fit the shape";
     });
     launch_rope_bwd(tb.dqf, tb.dkf, tb.dvf, m->rope_cos, m->rope_sin, d_cu, B, T, H, KV, hd, tb.dqkv,
                     c.qkv_bias ? tb.dqkvf : nullptr, s);
@@ -1884,8 +1886,12 @@ extern "C" int axon_loss_and_grads(axon_model* m, int32_t batch, const int32_t* 
     if (!g[i]) return fail(AXON_E_MISSING, "missing gradient '" + expected[i].first + "'");
   hipStream_t s = (hipStream_t)stream;
   if (int r = train_setup(m, s)) return r;
+  if (!attn_bwd_layout_ok(m->H(), m->KVh(), m->hd(), m->train.SP, m->train.W))
+    return fail(AXON_E_INVALID, "attention backward: the packed layout needs H*hd, KV*hd, the packed width and the "
+                                "per-sequence stride to be multiples of 32 (hd 64 or 128)");
   enqueue_train(m, batch, (int)total, d_tokens, d_cu_seqlens, h_cu_seqlens, d_targets, d_loss, g, index, s);
   if (int r = check_launch("backward pass")) return r;
+  if (int r = take_enqueue_err(m, "backward pass")) return r;
   for (int b = 0; b < c.max_batch; ++b) m->h_len[b] = b < batch ? h_cu_seqlens[b + 1] - h_cu_seqlens[b] : 0;
   m->active = batch;
   return AXON_OK;

@@ -373,12 +373,18 @@ __global__ void __launch_bounds__(64) attn_bwd_dq_kernel(const bf16* __restrict_
       st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(kr + kfr + s * 512), qf[s], st, 0, 0, 0);
       dpt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(vr + kfr + s * 512), df[s], dpt, 0, 0, 0);
     }
-    bf16x8 dsb[2];
+    // dS as a bf16 pair hi + lo: a row of dS sums to zero, so dQ = dS K
+    // cancels, and rounding dS to one bf16 would leave an error of 2^-9 of
+    // the row's absolute sum times the keys' common part
+    bf16x8 dsh[2], dsl[2];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int key = kb0 + (i >> 2) * 8 + hl * 4 + (i & 3);
       const float p = (key <= myq && myq < S) ? exp2f(st[i] * sc - l2) : 0.f;
-      dsb[i >> 3][i & 7] = (bf16)(p * (dpt[i] - Dq));
+      const float ds = p * (dpt[i] - Dq);
+      const bf16 hi = (bf16)ds;
+      dsh[i >> 3][i & 7] = hi;
+      dsl[i >> 3][i & 7] = (bf16)(ds - (float)hi);
     }
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
@@ -387,7 +393,8 @@ __global__ void __launch_bounds__(64) attn_bwd_dq_kernel(const bf16* __restrict_
         const bf16x8 a =
             *(const bf16x8*)(kt + frag_off((int64_t)kvh * HD + b * 32 + c, (int64_t)e * SP + kb0 + kk * 16, W) +
                              hl * 256);
-        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsb[kk], acc[b], 0, 0, 0);
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsh[kk], acc[b], 0, 0, 0);
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, dsl[kk], acc[b], 0, 0, 0);
       }
   }
   if (myq >= S) return;
@@ -459,14 +466,19 @@ __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict
         lq[g] = *(const f32x4*)(lsep + srow + g * 8);
         dq4[g] = *(const f32x4*)(dsump + srow + g * 8);
       }
-      bf16x8 pb[2], dsb[2];
+      // P in bf16; dS as a bf16 pair hi + lo (dK = dS^T Q sums a row of dS,
+      // which sums to zero, against the queries: see the dQ kernel)
+      bf16x8 pb[2], dsh[2], dsl[2];
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int qi = qb0 + (i >> 2) * 8 + hl * 4 + (i & 3);
         const bool ok = qi < S && mykey <= qi;
         const float p = ok ? exp2f(sq[i] * sc - lq[i >> 2][i & 3]) : 0.f;
         pb[i >> 3][i & 7] = (bf16)p;
-        dsb[i >> 3][i & 7] = ok ? (bf16)(p * (dpq[i] - dq4[i >> 2][i & 3])) : (bf16)0.f;
+        const float ds = ok ? p * (dpq[i] - dq4[i >> 2][i & 3]) : 0.f;
+        const bf16 hi = (bf16)ds;
+        dsh[i >> 3][i & 7] = hi;
+        dsl[i >> 3][i & 7] = (bf16)(ds - (float)hi);
       }
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
@@ -476,7 +488,8 @@ __global__ void __launch_bounds__(64) attn_bwd_dkv_kernel(const bf16* __restrict
           const bf16x8 ao = *(const bf16x8*)(dot + off);
           const bf16x8 aq = *(const bf16x8*)(qt + off);
           avv[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ao, pb[kk], avv[b], 0, 0, 0);
-          akk[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, dsb[kk], akk[b], 0, 0, 0);
+          akk[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, dsh[kk], akk[b], 0, 0, 0);
+          akk[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(aq, dsl[kk], akk[b], 0, 0, 0);
         }
     }
   }
@@ -625,11 +638,19 @@ void launch_colsum(const float* src, int64_t ld, int T, int C, float* part, floa
   colsum_final_kernel<<<(C + 255) / 256, 256, 0, s>>>(part, nch, C, dst);
 }
 
-void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
+bool attn_bwd_layout_ok(int H, int KVh, int hd, int SP, int64_t W) {
+  // frag_off / row_frag_off cut rows, columns and packed positions into
+  // 32-wide fragments and head dimensions into 16-wide k-steps
+  return H > 0 && KVh > 0 && H % KVh == 0 && (hd == 64 || hd == 128) && SP > 0 && SP % 32 == 0 && W % 32 == 0 &&
+         ((int64_t)H * hd) % 32 == 0 && ((int64_t)KVh * hd) % 32 == 0;
+}
+
+bool launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
                      float* statp, const int32_t* cu, const int32_t* h_cu, int nseq, int T, int H, int SP, int64_t W,
                      bf16* kr, bf16* vr, bf16* kt, bf16* qt, bf16* dot, float* dq, float* dkh, float* dvh, float* dk,
                      float* dv, hipStream_t s) {
-  if (T <= 0) return;
+  if (!attn_bwd_layout_ok(H, kv.kv_heads, kv.hd, SP, W)) return false;
+  if (T <= 0) return true;
   const int KVh = kv.kv_heads, hd = kv.hd, group = H / KVh;
   float* lsep = statp;
   float* dsump = statp + (int64_t)H * W;
@@ -656,6 +677,7 @@ void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, c
     const int64_t n = (int64_t)T * KVh * hd;
     attn_bwd_group_sum_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(dkh, dvh, n, group, hd, dk, dv);
   }
+  return true;
 }
 
 void launch_rope_bwd(const float* dq, const float* dk, const float* dv, const float* cos_t, const float* sin_t,

@@ -114,7 +114,10 @@ void launch_colsum(const float* src, int64_t ld, int T, int C, float* part, floa
 // qt / dot [H*hd][W], W >= nseq*SP, SP >= the longest sequence rounded up to
 // 32, plus 32
 // dkh / dvh [T][H][hd] scratch (the per-head shares of dk / dv)
-void launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
+// false (nothing launched) unless the packed fragment layouts fit the shape:
+// attn_bwd_layout_ok(H, kv heads, head_dim, SP, W)
+bool attn_bwd_layout_ok(int H, int KVh, int hd, int SP, int64_t W);
+bool launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, const float* lse, float* dsum,
                      float* statp /* [2][H][W] */, const int32_t* cu, const int32_t* h_cu, int nseq, int T, int H,
                      int SP, int64_t W,
                      bf16* kr, bf16* vr, bf16* kt, bf16* qt, bf16* dot, float* dq, float* dkh, float* dvh, float* dk,
