@@ -175,7 +175,7 @@ def gelu_mlp(h: np.ndarray, w_fc: np.ndarray, b_fc: np.ndarray, w_proj: np.ndarr
 
 
 def moe_mlp(h: np.ndarray, w_router: np.ndarray, experts: list, shared, top_k: int, norm_topk: bool,
-            rnd=None) -> np.ndarray:
+            rnd=None, force: dict | None = None) -> np.ndarray:
     """Mixture-of-experts MLP (the MoE built-in's softmax top-k router followed
     by the routed experts; Built-In Libraries, "Activations and specialized
     modules").  Per token: router probabilities = softmax over the experts of
@@ -183,9 +183,15 @@ def moe_mlp(h: np.ndarray, w_router: np.ndarray, experts: list, shared, top_k: i
     index); their probabilities are the mixing weights (divided by their sum
     when ``norm_topk``); each chosen expert is a SwiGLU MLP; ``shared`` (a
     (gate, up, down) triple or None) is an always-active SwiGLU MLP added
-    without a weight.  ``experts`` is a list of (gate, up, down) triples."""
+    without a weight.  ``experts`` is a list of (gate, up, down) triples.
+    ``force`` (row -> top_k expert ids) replaces the chosen set of the given
+    rows (their weights are still their probabilities): where two experts'
+    probabilities lie within rounding of each other either choice is a valid
+    result, and this evaluates the other one."""
     p = softmax(h @ w_router.T)
     idx = np.argsort(-p, axis=-1, kind="stable")[:, :top_k]
+    for row, chosen in (force or {}).items():
+        idx[row] = np.asarray(chosen, dtype=idx.dtype)
     wts = np.take_along_axis(p, idx, axis=-1)
     if norm_topk:
         wts = wts / np.sum(wts, axis=-1, keepdims=True)
@@ -227,7 +233,8 @@ class OracleDecoder:
     (any model) limits each query to its last W keys.
     """
 
-    def __init__(self, cfg: dict, weights: dict, io_round: str | None = None, io_skip=()):
+    def __init__(self, cfg: dict, weights: dict, io_round: str | None = None, io_skip=(),
+                 route_override: dict | None = None):
         self.cfg = cfg
         self.D = cfg["hidden_size"]
         self.L = cfg["num_hidden_layers"]
@@ -254,6 +261,10 @@ class OracleDecoder:
         self.io_skip = frozenset(io_skip)
         self.io_applied: set[str] = set()
         self.caches: list[list[tuple[np.ndarray, np.ndarray]]] = []
+        # (sequence, layer, position) -> the top-k expert set that token takes
+        # in that layer instead of its own choice (mixture-of-experts models)
+        self.route_override = dict(route_override or {})
+        self._seq = 0
         self.n_experts = int(cfg.get("n_routed_experts") or 0)
         self.first_moe = int(cfg.get("first_k_dense_replace") or 0)
 
@@ -306,8 +317,10 @@ class OracleDecoder:
                   for e in range(self.n_experts)]
             sh = tuple(w[p + f"mlp.shared_experts.{n}_proj.weight"] for n in ("gate", "up", "down")) \
                 if c.get("n_shared_experts") else None
+            force = {r: self.route_override[(self._seq, i, int(q))] for r, q in enumerate(pos)
+                     if (self._seq, i, int(q)) in self.route_override}
             mlp = moe_mlp(h2, w[p + "mlp.gate.weight"], ex, sh, int(c["num_experts_per_tok"]),
-                          bool(c.get("norm_topk_prob")), rnd=self._r_act)
+                          bool(c.get("norm_topk_prob")), rnd=self._r_act, force=force)
         else:
             mlp = swiglu_mlp(h2, w[p + "mlp.gate_proj.weight"], w[p + "mlp.up_proj.weight"],
                              w[p + "mlp.down_proj.weight"], rnd=self._r_act)
@@ -334,6 +347,7 @@ class OracleDecoder:
         return self._rx(x + mlp)
 
     def _forward_seq(self, b: int, ids: np.ndarray, all_logits: bool) -> np.ndarray:
+        self._seq = b
         cache = self.caches[b]
         past = cache[0][0].shape[0]
         pos = past + np.arange(len(ids))

@@ -516,6 +516,47 @@ def test_moe_of_identical_experts_equals_the_dense_model():
     # without renormalization the weights sum to less than one: the models differ
     un = OracleDecoder(dict(moe_shp, norm_topk_prob=False), mw).prefill([seq], all_logits=True)[0]
     assert np.abs(un - ref).max() > 1e-4
+    # a routing override (another valid top-k set for some tokens) keeps the
+    # weights summing to one, so it leaves this model equal to the dense one
+    force = {(0, 1, 2): (4, 0, 1), (0, 2, 5): (3, 2, 4), (0, 1, 8): (0, 1, 2)}
+    got = OracleDecoder(moe_shp, mw, route_override=force).prefill([seq], all_logits=True)[0]
+    np.testing.assert_allclose(got, ref, atol=1e-12)
+
+
+def test_moe_route_override():
+    """Forcing each token's own top-k set changes nothing (bit for bit);
+    forcing another set changes that token's logits and, through the KV cache,
+    only the later positions'."""
+    shp = dict(_tiny("llama", layers=2), n_routed_experts=6, num_experts_per_tok=2, moe_intermediate_size=16,
+               n_shared_experts=1, first_k_dense_replace=0, norm_topk_prob=False)
+    w = _np_weights(shp, seed=8)
+    seq = RNG.integers(0, shp["vocab_size"], 7)
+    base = OracleDecoder(shp, w).prefill([seq], all_logits=True)[0]
+    own = {}
+    orig = oracle.decoder.moe_mlp
+    calls = []
+
+    def spy(h, w_router, experts, shared, top_k, norm_topk, rnd=None, force=None):
+        p = oracle.decoder.softmax(h @ w_router.T)
+        calls.append(np.argsort(-p, axis=-1, kind="stable")[:, :top_k])
+        return orig(h, w_router, experts, shared, top_k, norm_topk, rnd, force)
+
+    oracle.decoder.moe_mlp = spy
+    try:
+        OracleDecoder(shp, w).prefill([seq], all_logits=True)
+    finally:
+        oracle.decoder.moe_mlp = orig
+    for layer, idx in enumerate(calls):
+        for pos in range(len(seq)):
+            own[(0, layer, pos)] = tuple(int(e) for e in idx[pos])
+    same = OracleDecoder(shp, w, route_override=own).prefill([seq], all_logits=True)[0]
+    np.testing.assert_array_equal(same, base)
+    alt = dict(own)
+    e0, e1 = own[(0, 1, 4)]
+    alt[(0, 1, 4)] = (e0, next(e for e in range(6) if e not in (e0, e1)))
+    moved = OracleDecoder(shp, w, route_override=alt).prefill([seq], all_logits=True)[0]
+    np.testing.assert_array_equal(moved[:4], base[:4])
+    assert np.abs(moved[4] - base[4]).max() > 1e-6
 
 
 # ------------------------------------------------- GPT-2 family and sliding windows
