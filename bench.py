@@ -53,6 +53,8 @@ def main():
                                                          "gpt2xl", "mistral7b", "1b_train"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--no-7b", action="store_true",
+                    help="with the 1b workload: leave out the 7B workload's object in the JSON line")
     ap.add_argument("--decode-steps", type=int, default=None,
                     help="override the workload's decode step count (hardware-counter runs only)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -72,14 +74,13 @@ def main():
               "(this build has no multi-GPU path)", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     from paper_2608_19889_amd import axon as ax
     if not os.path.exists(ax.LIB_PATH):
         from paper_2608_19889_amd.build import build
         build()
-    from synthetic import MODEL_SHAPES, WORKLOADS, model_weights, paged_workload, prompts
+    from synthetic import MODEL_SHAPES, WORKLOADS
 
     wl = dict(WORKLOADS[args.workload])
     shape = MODEL_SHAPES[wl["model"]]
@@ -87,6 +88,35 @@ def main():
         return vendor_gemm(shape, wl)
     if wl.get("train"):
         return train_bench(args, wl, shape)
+    out, lens, steps = measure_generate(args, args.workload, args.steps, args.warmup)
+    # the metric covers the 1B and the 7B shapes: the 7B workload's figures go
+    # into the same line (1 warmup + up to 2 timed generates)
+    if args.workload == "1b" and not args.no_7b:
+        out["workloads"] = {"7b": workload_summary(measure_generate(args, "7b", min(args.steps, 2), 1)[0])}
+    if args.copy_calibration:
+        src = torch.empty(1 << 29, dtype=torch.int16, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] calibration copy: 1 GiB read + 1 GiB written")
+        del src, dst
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(shape, wl, lens, steps, wl["batch"])
+    print(json.dumps(out), flush=True)
+
+
+def measure_generate(args, workload, n_steps, n_warmup):
+    """Time ``n_steps`` whole greedy generates of ``workload`` after
+    ``n_warmup`` untimed ones; returns (result dict, prompt lengths, decode
+    steps)."""
+    import numpy as np
+    import torch
+
+    from paper_2608_19889_amd import axon as ax
+    from synthetic import MODEL_SHAPES, WORKLOADS, model_weights, paged_workload, prompts
+    wl = dict(WORKLOADS[workload])
+    shape = MODEL_SHAPES[wl["model"]]
     esz = 2 if shape["dtype"] == "bf16" else 4
     B, steps = wl["batch"], wl["steps"] if args.decode_steps is None else args.decode_steps
     L, D, V = shape["num_hidden_layers"], shape["hidden_size"], shape["vocab_size"]
@@ -143,28 +173,28 @@ def main():
         if record:
             ev[2].record()
 
-    for i in range(args.warmup):
+    for i in range(n_warmup):
         generate()
-        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+        log(f"[bench] warmup {i + 1}/{n_warmup} done")
     torch.cuda.synchronize()
     pre_ms, dec_ms = [], []
     t_start = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(n_steps):
         generate(record=True)
         torch.cuda.synchronize()
         if serve_plan is not None:
             p, d = serve_split_ms(serve_plan, serve_ev)
             pre_ms.append(p)
             dec_ms.append(d)
-            log(f"[bench] step {i + 1}/{args.steps}: steps with prompt chunks {p:.2f} ms, decode-only steps "
+            log(f"[bench] step {i + 1}/{n_steps}: steps with prompt chunks {p:.2f} ms, decode-only steps "
                 f"{d:.2f} ms ({len(serve_plan)} scheduler steps)")
         else:
             pre_ms.append(ev[0].elapsed_time(ev[1]))
             dec_ms.append(ev[1].elapsed_time(ev[2]))
-            log(f"[bench] step {i + 1}/{args.steps}: prefill {pre_ms[-1]:.2f} ms, decode {dec_ms[-1]:.2f} ms")
+            log(f"[bench] step {i + 1}/{n_steps}: prefill {pre_ms[-1]:.2f} ms, decode {dec_ms[-1]:.2f} ms")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
-    ms_per_step = wall * 1e3 / args.steps
+    ms_per_step = wall * 1e3 / n_steps
     gen_tokens = B * (steps + 1)
     value = gen_tokens / (ms_per_step / 1e3)
     prefill_ms, decode_ms = float(np.mean(pre_ms)), float(np.mean(dec_ms))
@@ -205,15 +235,15 @@ def main():
         "value": round(value, 2),
         "unit": "generated tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": n_steps,
+        "warmup": n_warmup,
         "ms_per_step": round(ms_per_step, 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": shape["dtype"],
         "data": "synthetic (random-init N(0,0.02) weights, uniform random prompt ids)",
-        "config": {"workload": f"{args.workload}-shaped decoder: batch {B}, "
+        "config": {"workload": f"{workload}-shaped decoder: batch {B}, "
                                + (f"prompts {wl['prompt_len']}" if not wl["paged"] else
                                   f"prompts U[{wl['len_range'][0]},{wl['len_range'][1]}] (sum {cu[-1]})")
                                + f", {steps} greedy decode steps, "
@@ -232,22 +262,31 @@ def main():
 
     if not args.no_roofline:
         out.update(roofline_pass(m, generate, shape, esz, lens))
-        out["roofline"]["traffic"] = measured_traffic(out["roofline"], args.workload)
+        out["roofline"]["traffic"] = measured_traffic(out["roofline"], workload)
     m.close()
-    if args.copy_calibration:
-        src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log("[bench] calibration copy: 1 GiB read + 1 GiB written")
-        del src, dst
     del w
     torch.cuda.empty_cache()
+    return out, lens, steps
 
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(shape, wl, lens, steps, B)
-    print(json.dumps(out), flush=True)
+
+def workload_summary(o):
+    """The figures of a second workload's measurement that go into the main
+    JSON line: throughput, prefill and decode rates, decode HBM fraction and
+    each kernel class's roofline."""
+    keys = ("value", "ms_per_step", "steps", "warmup", "prefill_tok_s", "prefill_ms", "decode_tok_s",
+            "decode_ms_per_token_step", "decode_hbm_gbs", "decode_hbm_frac")
+    r = {"workload": o["config"]["workload"], "unit": o["unit"]}
+    r.update({k: o[k] for k in keys if k in o})
+    r["generated_tok_s"] = r.pop("value")
+    k = o.get("kernels", {})
+    for name, key in (("prefill projection GEMM (MFMA)", "prefill_gemm"), ("prefill flash attention", "prefill_attention"),
+                      ("decode projection GEMM (weight streaming)", "decode_projections"),
+                      ("decode attention (+ split merge)", "decode_attention")):
+        if name in k:
+            r[key] = {f: k[name][f] for f in ("bound", "achieved", "peak", "unit", "frac", "avg_us", "total_ms")}
+    if "roofline" in o:
+        r["roofline"] = o["roofline"]
+    return r
 
 
 def vendor_gemm(shape, wl):
@@ -663,6 +702,25 @@ def summarize_counters(fetch_csv, write_csv, workload):
     print(json.dumps(rec, indent=1))
 
 
+def host_description():
+    """The host the oracle ran on: logical CPUs, CPU model name and RAM, read
+    from /proc."""
+    model, mem_kb = "unknown", 0
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+        for line in open("/proc/meminfo"):
+            if line.startswith("MemTotal:"):
+                mem_kb = int(line.split()[1])
+                break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpu_model": model, "ram_gb": round(mem_kb / 2 ** 20, 1),
+            "blas_threads_env": os.environ.get("OMP_NUM_THREADS")}
+
+
 def cpu_baseline(shape, wl, lens, steps, B, seqs_sample=2):
     """The float64 oracle on the host cores, on a bounded sample of the same
     workload: the first ``seqs_sample`` sequences run in full (prefill of the
@@ -695,6 +753,7 @@ def cpu_baseline(shape, wl, lens, steps, B, seqs_sample=2):
     value = gen / (t2 - t1)
     log(f"[bench] oracle sample: {gen} tokens in {t2 - t1:.1f}s")
     return {"value": round(value, 4), "unit": "generated tokens/s", "cores": threads, "kind": "oracle",
+            "host": host_description(),
             "sample": f"{len(seqs)} of the {B} sequences, complete (prefill of {[len(x) for x in seqs]} prompt "
                       f"tokens + {steps} greedy decode steps each), float64, {t2 - t1:.1f}s"}
 
