@@ -184,6 +184,31 @@ int axon_prefill(axon_model* m, int32_t batch, const int32_t* d_tokens,
 int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_tokens, float* d_logits,
                      int32_t* d_next_tokens, void* stream);
 
+/* Decode step that allocates nothing, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, validation, kernels and results as
+ * axon_decode_step, but the step is launched directly on ``stream`` (no graph
+ * of the library's own is recorded: instantiating one allocates) and its
+ * per-step work buffers (residual rows, the normalized operand and its sums
+ * of squares, q, the attention output, the gated activation, split partials,
+ * argmax partials) are laid out in one fixed device array of
+ * AXON_NOALLOC_SCRATCH_BYTES that the library holds per GPU from the time its
+ * code is loaded until the process ends.  The model (weights, KV cache,
+ * lengths) is the one axon_init_model allocated.  The call makes no
+ * hipMalloc, hipFree or other allocating call.
+ * Dense Llama-family bf16 models only (AXON_ARCH_LLAMA, AXON_BF16,
+ * n_experts 0; else AXON_E_INVALID) and batch <= 64; a step whose buffers
+ * need more than the array is refused with AXON_E_CAPACITY (the message gives
+ * the bytes needed); AXON_E_HIP if the array's address could not be obtained
+ * at init.  Nothing is enqueued on failure.  All calls on one GPU share its
+ * array, which keeps the last call's contents (every buffer is written before
+ * it is read within a step, so nothing needs clearing); calls that overlap in
+ * time on one GPU -- from two streams or threads, on any models -- race on it
+ * and must be serialized by the caller. */
+#define AXON_NOALLOC_SCRATCH_BYTES (64u << 20)
+int axon_decode_step_noalloc(axon_model* m, int32_t batch, const int32_t* d_tokens, float* d_logits,
+                             int32_t* d_next_tokens, void* stream);
+
 /* Continuous batching (the serving loop of a paged-attention engine: prompt
  * chunks of newly admitted sequences and decode tokens of running ones share
  * one forward pass; Results, vLLM-native comparison; Introduction, vLLM

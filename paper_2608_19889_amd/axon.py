@@ -30,7 +30,7 @@ AXON_ARCH_GPT2 = 1
 STATUS_NAMES = {0: "AXON_OK", -1: "AXON_E_INVALID", -2: "AXON_E_SHAPE", -3: "AXON_E_MISSING",
                 -4: "AXON_E_DTYPE", -5: "AXON_E_CAPACITY", -6: "AXON_E_OOM", -7: "AXON_E_HIP"}
 
-EXPORTED = ["axon_init_model", "axon_prefill", "axon_decode_step", "axon_step", "axon_reset_slot", "axon_loss_and_grads",
+EXPORTED = ["axon_init_model", "axon_prefill", "axon_decode_step", "axon_decode_step_noalloc", "axon_step", "axon_reset_slot", "axon_loss_and_grads",
             "axon_slot_lengths", "axon_timing_enable", "axon_timing_records", "axon_free", "axon_last_error"]
 
 # kernel classes of the timing records
@@ -85,6 +85,8 @@ def lib():
         L.axon_decode_step.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p, ctypes.c_void_p]
         L.axon_decode_step.restype = ctypes.c_int
+        L.axon_decode_step_noalloc.argtypes = L.axon_decode_step.argtypes
+        L.axon_decode_step_noalloc.restype = ctypes.c_int
         L.axon_step.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
                                 ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p, ctypes.c_void_p,
                                 ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
@@ -244,6 +246,19 @@ class Model:
         _check(lib().axon_decode_step(self._h, B, tokens.data_ptr(),
                                       logits.data_ptr() if logits is not None else None,
                                       next_tokens.data_ptr(), ctypes.c_void_p(_stream(stream))))
+        return logits, next_tokens
+
+    def decode_step_noalloc(self, tokens: torch.Tensor, logits: torch.Tensor | None = None,
+                            next_tokens: torch.Tensor = None, stream=None):
+        """axon_decode_step_noalloc: the decode step with its work buffers in the
+        library's fixed per-GPU array (nothing is allocated by the call; the
+        caller provides ``next_tokens``, device int32 [batch]).  Returns
+        (logits or None, next_tokens)."""
+        if next_tokens is None:
+            raise ValueError("decode_step_noalloc needs a caller-provided next_tokens buffer")
+        _check(lib().axon_decode_step_noalloc(self._h, tokens.shape[0], tokens.data_ptr(),
+                                              logits.data_ptr() if logits is not None else None,
+                                              next_tokens.data_ptr(), ctypes.c_void_p(_stream(stream))))
         return logits, next_tokens
 
     def step(self, tokens: torch.Tensor, cu_seqlens: list, slots: list, fresh: list | None = None,

@@ -11,6 +11,7 @@
 #include <cstring>
 #include <functional>
 #include <map>
+#include <mutex>
 #include <string>
 #include <tuple>
 #include <unordered_map>
@@ -23,9 +24,45 @@ using namespace axon;
 
 thread_local axon::TimingSlot axon::g_timing_slot;
 
+// Work memory of axon_decode_step_noalloc: one array per GPU, reserved when
+// the code object is loaded and held until the process ends.  Host code never
+// passes ``scratch`` itself to a kernel (in host code the name is only a
+// stand-in); it uses the device address that hipGetSymbolAddress returns for
+// the current device, looked up once per device by axon_init_model.
+static __device__ __align__(256) unsigned char scratch[AXON_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string g_err;
+
+// device id -> address of that device's ``scratch`` (or the lookup's error)
+std::mutex g_scratch_mu;
+std::map<int, std::pair<void*, std::string>> g_scratch_addr;
+
+void scratch_of_current_device(void** ptr, std::string* err) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    *ptr = nullptr;
+    *err = std::string("hipGetDevice: ") + hipGetErrorString(e);
+    return;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  auto it = g_scratch_addr.find(dev);
+  if (it == g_scratch_addr.end()) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    std::string msg;
+    if (e != hipSuccess) {
+      p = nullptr;
+      msg = std::string("hipGetSymbolAddress of the no-allocation work array: ") + hipGetErrorString(e);
+      (void)hipGetLastError();
+    }
+    it = g_scratch_addr.emplace(dev, std::make_pair(p, msg)).first;
+  }
+  *ptr = it->second.first;
+  *err = it->second.second;
+}
 
 int fail(int code, const std::string& msg) {
   g_err = msg;
@@ -221,6 +258,21 @@ struct TrainBufs {
   bf16 *hf, *dlog, *dxb, *dgu, *dob, *dqkv, *tra, *trs, *trb, *headT;
 };
 
+// Per-step work buffers of the bf16 decode step: the model's own (allocated
+// at init), or carved from the no-allocation array.
+struct DecodeWs {
+  float* x;          // residual rows [B][D]
+  bf16* xg;          // bf16(x * g) [B][D]
+  float* ss;         // sums-of-squares partials [D / 8][B]
+  bf16* q;           // rotated queries [B][H hd]
+  bf16* o;           // attention output [B][H hd]
+  bf16* a;           // gated activation [B][I]
+  float* attn_part;  // decode attention split partials
+  float* gemv_part;  // split-K partials of the projections
+  float* am_val;     // head argmax partials [B][ceil(V / 16)]
+  int32_t* am_idx;
+};
+
 }  // namespace
 
 struct axon_model {
@@ -268,6 +320,12 @@ struct axon_model {
   int32_t* am_idx = nullptr;
   int32_t* d_len = nullptr;
   std::vector<int> h_len;
+  // this device's no-allocation work array (or why it is unavailable)
+  void* scratch_ptr = nullptr;
+  std::string scratch_err;
+  DecodeWs own_ws() const {
+    return DecodeWs{x, (bf16*)xg, ss, (bf16*)q, (bf16*)o, (bf16*)a, attn_part, gemv_part, am_val, am_idx};
+  }
   // per-entry arrays of a continuous-batching step (6 x max_batch int32):
   // slot, base position, chunk entries, single-token rows / slots / positions
   // mixture-of-experts work buffers (sized for the most tokens of a call)
@@ -752,13 +810,15 @@ void enqueue_decode_many(axon_model* m, int B, const int32_t* d_tokens, float* d
 //   plan != nullptr: a step of single-token entries: item b is at position
 //   plan->d_dpos[b] of slot plan->d_dslot[b]; lengths are set at the end.
 void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
-                         hipStream_t s, const StepPlan* plan = nullptr, const int32_t* d_cu = nullptr) {
+                         hipStream_t s, const StepPlan* plan = nullptr, const int32_t* d_cu = nullptr,
+                         const DecodeWs* wsp = nullptr) {
   const int D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V(), nq = m->nqkv();
+  const DecodeWs ws = wsp ? *wsp : m->own_ws();
   const int32_t* pos = plan ? plan->d_dpos : m->d_len;
   const int32_t* slot = plan ? plan->d_dslot : nullptr;
   const float eps = m->cfg.rms_eps;
-  bf16* xg = (bf16*)m->xg;
-  launch_embed_ss(d_tokens, (const bf16*)m->embed, (const bf16*)m->layers[0].gin, m->x, xg, m->ss, B, D, V, s);
+  bf16* xg = ws.xg;
+  launch_embed_ss(d_tokens, (const bf16*)m->embed, (const bf16*)m->layers[0].gin, ws.x, xg, ws.ss, B, D, V, s);
   int ss_n = 1;
   auto gemv = [&](GemvArgs& a, int epi) { gemv_step(m, a, epi, s); };
   auto ss_count = [&](int K) {
@@ -771,21 +831,20 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
     const bool last = l + 1 == m->cfg.n_layers;
     GemvArgs qa{};
     qa.W = (const bf16*)w.wqkv; qa.N = nq; qa.K = D; qa.M = B;
-    qa.X = xg; qa.ss_in = m->ss; qa.ss_n = ss_n; qa.eps = eps;
-    qa.bias = (const bf16*)w.bqkv; qa.cos_t = m->rope_cos; qa.sin_t = m->rope_sin; qa.q_out = (bf16*)m->q;
-    qa.kv = kv; qa.len = pos; qa.slot = slot; qa.H = H; qa.part = m->gemv_part;
+    qa.X = xg; qa.ss_in = ws.ss; qa.ss_n = ss_n; qa.eps = eps;
+    qa.bias = (const bf16*)w.bqkv; qa.cos_t = m->rope_cos; qa.sin_t = m->rope_sin; qa.q_out = ws.q;
+    qa.kv = kv; qa.len = pos; qa.slot = slot; qa.H = H; qa.part = ws.gemv_part;
     gemv(qa, GV_ROPE);
     int ctx_sum = 0;
     if (plan) ctx_sum = plan->dctx;
     else for (int b = 0; b < B; ++b) ctx_sum += m->keys_read(m->h_len[b] + 1);
     m->timed(2, H, B, ctx_sum, s, [&] {
-      launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, B, H, pos, m->cfg.max_seq, s,
-                               nullptr, slot);
+      launch_attn_decode<bf16>(ws.q, kv, ws.o, ws.attn_part, B, H, pos, m->cfg.max_seq, s, nullptr, slot);
     });
     GemvArgs oa{};
-    oa.W = (const bf16*)w.wo; oa.N = D; oa.K = H * hd; oa.M = B; oa.X = (const bf16*)m->o;
-    oa.out_f32 = m->x; oa.ldo = D; oa.ss_out = m->ss; oa.xg_out = xg; oa.gain_next = (const bf16*)w.gpost;
-    oa.part = m->gemv_part;
+    oa.W = (const bf16*)w.wo; oa.N = D; oa.K = H * hd; oa.M = B; oa.X = ws.o;
+    oa.out_f32 = ws.x; oa.ldo = D; oa.ss_out = ws.ss; oa.xg_out = xg; oa.gain_next = (const bf16*)w.gpost;
+    oa.part = ws.gemv_part;
     gemv(oa, GV_RESID);
     ss_n = ss_count(H * hd);
     const bf16* gnext = (const bf16*)(last ? m->gfinal : m->layers[l + 1].gin);
@@ -796,26 +855,26 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
       // routed rows before the shared experts' down projection (which then
       // leaves the next layer's xg and sums of squares), or, without shared
       // experts, the combine leaves them
-      launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, (const bf16*)w.gpost, (bf16*)m->h, B, D, eps, nullptr, s);
+      launch_resid_rmsnorm<bf16>(ws.x, nullptr, 0, 0, (const bf16*)w.gpost, (bf16*)m->h, B, D, eps, nullptr, s);
       moe_routed(m, w, (const bf16*)m->h, B, s);
     }
     if (Id > 0) {
       GemvArgs ga{};
       ga.W = (const bf16*)w.wgu; ga.N = 2 * Id; ga.K = D; ga.M = B;
-      ga.X = xg; ga.ss_in = m->ss; ga.ss_n = ss_n; ga.eps = eps;
-      ga.out_t = (bf16*)m->a; ga.ldo = Id; ga.part = m->gemv_part;
+      ga.X = xg; ga.ss_in = ws.ss; ga.ss_n = ss_n; ga.eps = eps;
+      ga.out_t = ws.a; ga.ldo = Id; ga.part = ws.gemv_part;
       gemv(ga, GV_SILU);
     }
     if (w.moe) {
       const bool fold = Id == 0;  // no shared experts: the combine leaves xg
-      launch_moe_combine(m->x, m->moe_y, m->moe_inv, m->moe_topw, B, D, m->cfg.top_k, s, fold ? gnext : nullptr,
-                         fold ? xg : nullptr, fold ? m->ss : nullptr);
+      launch_moe_combine(ws.x, m->moe_y, m->moe_inv, m->moe_topw, B, D, m->cfg.top_k, s, fold ? gnext : nullptr,
+                         fold ? xg : nullptr, fold ? ws.ss : nullptr);
       if (fold) ss_n = moe_combine_blocks(D);
     }
     if (Id > 0) {
       GemvArgs da{};
-      da.W = (const bf16*)w.wd; da.N = D; da.K = Id; da.M = B; da.X = (const bf16*)m->a;
-      da.out_f32 = m->x; da.ldo = D; da.ss_out = m->ss; da.xg_out = xg; da.part = m->gemv_part;
+      da.W = (const bf16*)w.wd; da.N = D; da.K = Id; da.M = B; da.X = ws.a;
+      da.out_f32 = ws.x; da.ldo = D; da.ss_out = ws.ss; da.xg_out = xg; da.part = ws.gemv_part;
       da.gain_next = gnext;
       gemv(da, GV_RESID);
       ss_n = ss_count(Id);
@@ -823,11 +882,11 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
   }
   GemvArgs ha{};
   ha.W = (const bf16*)m->lm_head; ha.N = V; ha.K = D; ha.M = B;
-  ha.X = xg; ha.ss_in = m->ss; ha.ss_n = ss_n; ha.eps = eps;
-  ha.out_f32 = d_logits; ha.ldo = V; ha.am_val = m->am_val; ha.am_idx = m->am_idx;
+  ha.X = xg; ha.ss_in = ws.ss; ha.ss_n = ss_n; ha.eps = eps;
+  ha.out_f32 = d_logits; ha.ldo = V; ha.am_val = ws.am_val; ha.am_idx = ws.am_idx;
   gemv(ha, GV_HEAD);
   const int hr = gemv_rows(V, D, B, GV_HEAD);
-  launch_argmax_final(m->am_val, m->am_idx, (V + hr - 1) / hr, B, d_next, plan ? nullptr : m->d_len, s);
+  launch_argmax_final(ws.am_val, ws.am_idx, (V + hr - 1) / hr, B, d_next, plan ? nullptr : m->d_len, s);
   if (plan) launch_set_step_lengths(d_cu, plan->d_slot, plan->d_base, m->d_len, B, s);
 }
 
@@ -1308,6 +1367,9 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     HTRY(hipEventCreateWithFlags(&m->step_copied, hipEventDisableTiming));
   }
   m->h_len.assign(c.max_batch, 0);
+  // this device's no-allocation work array (a failed lookup only disables
+  // axon_decode_step_noalloc)
+  scratch_of_current_device(&m->scratch_ptr, &m->scratch_err);
   HTRY(hipStreamCreateWithFlags(&m->cap_stream, hipStreamNonBlocking));
   HTRY(hipStreamSynchronize(s));
 #undef TRY
@@ -1431,9 +1493,10 @@ int replay_or_run(axon_model* m, const GraphKey& key, hipStream_t s, const char*
   return rc;
 }
 
-extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_tokens, float* d_logits,
-                                int32_t* d_next_tokens, void* stream) {
-  g_err.clear();
+namespace {
+
+// Host checks shared by the decode entry points.
+int check_decode(const axon_model* m, int32_t batch, const int32_t* d_tokens, const int32_t* d_next_tokens) {
   if (!m) return fail(AXON_E_INVALID, "model is NULL");
   if (!d_tokens || !d_next_tokens) return fail(AXON_E_INVALID, "d_tokens and d_next_tokens must be non-NULL");
   if (batch < 1) return fail(AXON_E_INVALID, "batch must be >= 1");
@@ -1448,6 +1511,77 @@ extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_t
     if (m->paged() && m->h_bt[(int64_t)b * m->bt_stride + pos / m->ps] < 0)
       return fail(AXON_E_CAPACITY, "slot " + std::to_string(b) + " has no page for position " + std::to_string(pos));
   }
+  return AXON_OK;
+}
+
+// Bytes of the per-step work buffers of a bf16 decode step over B tokens,
+// each buffer 256-byte aligned; with ``base`` set, *ws receives the buffers
+// laid out from it.
+size_t decode_ws_layout(const axon_model* m, int B, char* base, DecodeWs* ws) {
+  const int64_t D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V();
+  size_t off = 0;
+  auto take = [&](int64_t bytes) -> char* {
+    const size_t at = off;
+    off += (size_t)(bytes + 255) / 256 * 256;
+    return base ? base + at : nullptr;
+  };
+  DecodeWs w{};
+  w.x = (float*)take(B * D * 4);
+  w.xg = (bf16*)take(B * D * 2);
+  w.ss = (float*)take(std::max<int64_t>(D / 8, 1) * B * 4);
+  w.q = (bf16*)take(B * H * hd * 2);
+  w.o = (bf16*)take(B * H * hd * 2);
+  w.a = (bf16*)take(B * I * 2);
+  w.attn_part = (float*)take((int64_t)B * plan_decode_splits(B, m->KVh(), m->cfg.max_seq) * H * (hd + 2) * 4);
+  const int64_t wsf = std::max({gemv_workspace_floats(m->nqkv(), (int)D, B, GV_ROPE),
+                                gemv_workspace_floats((int)D, (int)(H * hd), B, GV_RESID),
+                                gemv_workspace_floats(2 * (int)I, (int)D, B, GV_SILU),
+                                gemv_workspace_floats((int)D, (int)I, B, GV_RESID), (int64_t)1});
+  w.gemv_part = (float*)take(wsf * 4);
+  const int64_t nam = (V + 15) / 16;
+  w.am_val = (float*)take(nam * B * 4);
+  w.am_idx = (int32_t*)take(nam * B * 4);
+  if (ws) *ws = w;
+  return off;
+}
+
+}  // namespace
+
+extern "C" int axon_decode_step_noalloc(axon_model* m, int32_t batch, const int32_t* d_tokens, float* d_logits,
+                                        int32_t* d_next_tokens, void* stream) {
+  g_err.clear();
+  if (int rc = check_decode(m, batch, d_tokens, d_next_tokens)) return rc;
+  if (!m->bf || m->gpt2() || m->moe_model())
+    return fail(AXON_E_INVALID, "the no-allocation decode step serves dense Llama-family bf16 models only");
+  if (batch > GEMV_MAX_M)
+    return fail(AXON_E_CAPACITY, "the no-allocation decode step takes at most " + std::to_string(GEMV_MAX_M) +
+                                     " sequences, got " + std::to_string(batch));
+  if (!m->scratch_ptr) return fail(AXON_E_HIP, "no-allocation work array unavailable: " + m->scratch_err);
+  const size_t need = decode_ws_layout(m, batch, nullptr, nullptr);
+  if (need > (size_t)AXON_NOALLOC_SCRATCH_BYTES)
+    return fail(AXON_E_CAPACITY, "a decode step of " + std::to_string(batch) + " sequences of this model needs " +
+                                     std::to_string(need) + " bytes of work memory, more than the " +
+                                     std::to_string((size_t)AXON_NOALLOC_SCRATCH_BYTES) + " of the fixed array");
+  DecodeWs ws{};
+  decode_ws_layout(m, batch, (char*)m->scratch_ptr, &ws);
+  hipStream_t s = (hipStream_t)stream;
+  // launched directly: no graph is recorded (instantiation allocates) and no
+  // timing events are created
+  const bool timing = m->timing;
+  m->timing = false;
+  enqueue_decode_bf16(m, batch, d_tokens, d_logits, d_next_tokens, s, nullptr, nullptr, &ws);
+  m->timing = timing;
+  int rc = check_launch("decode (no allocation)");
+  if (!rc) rc = take_enqueue_err(m, "decode (no allocation)");
+  if (rc) return rc;
+  for (int b = 0; b < batch; ++b) m->h_len[b] += 1;
+  return AXON_OK;
+}
+
+extern "C" int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_tokens, float* d_logits,
+                                int32_t* d_next_tokens, void* stream) {
+  g_err.clear();
+  if (int rc = check_decode(m, batch, d_tokens, d_next_tokens)) return rc;
   hipStream_t s = (hipStream_t)stream;
   if (int rc = replay_or_run(m, GraphKey{batch, d_tokens, d_logits, d_next_tokens}, s, "decode",
                              [&](hipStream_t st) { enqueue_decode(m, batch, d_tokens, d_logits, d_next_tokens, st); }))

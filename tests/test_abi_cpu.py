@@ -169,6 +169,7 @@ def test_null_arguments():
     assert L.axon_init_model(ctypes.byref(cfg), None, -1, None, ctypes.byref(h)) == axon.AXON_E_INVALID
     assert L.axon_prefill(None, 1, None, None, None, None, 0, 0, None, None, None) == axon.AXON_E_INVALID
     assert L.axon_decode_step(None, 1, None, None, None, None) == axon.AXON_E_INVALID
+    assert L.axon_decode_step_noalloc(None, 1, None, None, None, None) == axon.AXON_E_INVALID
     assert L.axon_slot_lengths(None, None, 0) == axon.AXON_E_INVALID
     L.axon_free(None)  # NULL-safe
     w = _fake_weights(s)

@@ -1,0 +1,90 @@
+"""The decode step that allocates nothing (axon_decode_step_noalloc) against
+the ordinary decode step (axon_decode_step), called through the C ABI.
+
+Two models with the same weights and prompts take the same tokens; one
+decodes through the ordinary entry point (a recorded graph over the model's
+own work buffers), the other through the no-allocation one (direct launches
+over the library's fixed per-GPU array).  Both run the same kernels in the
+same order, so logits and tokens must agree bit for bit, on two calls in a
+row, the second with fewer sequences than the first.  Also: models the entry
+point does not serve are refused before anything is enqueued.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_19889_amd.axon import AxonError, Model
+from parity_util import pack
+from synthetic import MODEL_SHAPES, model_weights, prompts, small_shape
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("kind", ["1b_2_layers", "7b_2_layers_paged"])
+def test_noalloc_decode_equals_decode(kind):
+    if kind == "1b_2_layers":
+        shape = small_shape("1b", layers=2, vocab=8192)
+        page = {}
+    else:
+        shape = small_shape("7b", layers=2, vocab=8192)
+        page = dict(page_size=16, num_pages=64)
+    print(f"[noalloc] {kind}", flush=True)
+    w = model_weights(shape, seed=21, device="cuda")
+    ids = prompts(4, 90, shape["vocab_size"], seed=22).numpy()
+    seqs = [ids[0], ids[1, :37], ids[2, :64], ids[3, :5]]
+    table = None
+    if page:
+        table = torch.full((4, 16), -1, dtype=torch.int32)
+        perm = torch.randperm(64, generator=torch.Generator().manual_seed(3)).to(torch.int32)
+        for b in range(4):
+            table[b, :7] = perm[7 * b:7 * b + 7]
+    flat, cu = pack(seqs)
+    ref = Model(shape, w, max_batch=4, max_seq=112, **page)
+    new = Model(shape, w, max_batch=4, max_seq=112, **page)
+    _, t_ref = ref.prefill(flat, cu, block_table=table)
+    _, t_new = new.prefill(flat, cu, block_table=table)
+    torch.cuda.synchronize()
+    assert torch.equal(t_ref, t_new)
+    V = shape["vocab_size"]
+    for batch in (4, 2):  # the second call serves fewer sequences
+        tok = t_ref[:batch].clone()
+        lg_ref = torch.empty((batch, V), dtype=torch.float32, device="cuda")
+        lg_new = torch.full((batch, V), float("nan"), dtype=torch.float32, device="cuda")
+        nx_ref = torch.empty(batch, dtype=torch.int32, device="cuda")
+        nx_new = torch.full((batch,), -1, dtype=torch.int32, device="cuda")
+        ref.decode_step(tok, logits=lg_ref, next_tokens=nx_ref)
+        new.decode_step_noalloc(tok, logits=lg_new, next_tokens=nx_new)
+        torch.cuda.synchronize()
+        assert torch.isfinite(lg_ref).all()
+        assert torch.equal(lg_ref, lg_new), (lg_ref - lg_new).abs().max().item()
+        assert torch.equal(nx_ref, nx_new)
+        t_ref = torch.cat([nx_ref, t_ref[batch:]])
+    assert ref.lengths() == new.lengths() == [len(seqs[0]) + 2, len(seqs[1]) + 2, len(seqs[2]) + 1,
+                                              len(seqs[3]) + 1]
+    # without logits, tokens only
+    tok = t_ref[:3].clone()
+    nx_ref = torch.empty(3, dtype=torch.int32, device="cuda")
+    nx_new = torch.full((3,), -1, dtype=torch.int32, device="cuda")
+    ref.decode_step(tok, next_tokens=nx_ref)
+    new.decode_step_noalloc(tok, next_tokens=nx_new)
+    torch.cuda.synchronize()
+    assert torch.equal(nx_ref, nx_new)
+    ref.close()
+    new.close()
+
+
+def test_noalloc_refuses_other_models():
+    """float32 models are refused before any work is enqueued (and lengths do
+    not move)."""
+    shape = small_shape("1b", layers=1, vocab=512, dtype="f32")
+    w = {k: v.float() for k, v in model_weights(small_shape("1b", layers=1, vocab=512), seed=2, device="cuda").items()}
+    m = Model(shape, w, max_batch=2, max_seq=16)
+    flat, cu = pack([np.arange(5), np.arange(3)])
+    _, tok = m.prefill(flat, cu)
+    nx = torch.empty(2, dtype=torch.int32, device="cuda")
+    with pytest.raises(AxonError) as e:
+        m.decode_step_noalloc(tok, next_tokens=nx)
+    assert e.value.code == -1 and "bf16" in str(e.value)
+    assert m.lengths() == [5, 3]
+    torch.cuda.synchronize()
+    m.close()
