@@ -149,7 +149,17 @@ int axon_init_model(const axon_config* cfg, const axon_weight* weights, int32_t 
                     void* stream, axon_model** out);
 
 /* Prefill: start ``batch`` fresh sequences in slots 0..batch-1 (every earlier
- * sequence is dropped) and run the forward pass over their prompts.
+ * sequence is dropped) and run the forward pass over their prompts.  This is
+ * the model's forward over a whole prompt with an empty cache: positions
+ * start at the past length 0 (Built-In Libraries, "Positions and cache
+ * management"), each layer is the pre-norm attention + gated-MLP block of the
+ * complete model definition (Technical Supplement), attention is causal
+ * grouped-query attention with scale 1/sqrt(head_dim) (Built-In Libraries,
+ * "Attention and masking", "Tensor and math built-ins"), and the greedy token
+ * is the argmax of the final logits that generate() takes (Results,
+ * Measures).  The page table is given here, on the host, and kept by the
+ * library for the decode steps that follow (so it can be validated without a
+ * device-to-host copy); axon_step replaces rows of it later.
  *   d_tokens      device int32 [sum S_b], the prompts packed back to back;
  *   d_cu_seqlens  device int32 [batch+1], prefix sums of the prompt lengths;
  *   h_cu_seqlens  host copy of the same array (checked on the host, so no
@@ -173,7 +183,13 @@ int axon_prefill(axon_model* m, int32_t batch, const int32_t* d_tokens,
                  float* d_logits, int32_t* d_next_tokens, void* stream);
 
 /* One greedy decode step for slots 0..batch-1 (batch <= the batch of the last
- * prefill).  Slot b consumes d_tokens[b] (device int32 [batch]) at position
+ * prefill): the same forward for one new token per sequence against the
+ * cached keys and values, positions continuing from each sequence's past
+ * length (Built-In Libraries, "Positions and cache management": the cache is
+ * updated and positions are past_length + arange), then the greedy argmax
+ * (Results, Measures; the paper's generate() loop, done here without a host
+ * synchronization per step).  The page rows set by axon_prefill / axon_step
+ * are used; no table is passed per step.  Slot b consumes d_tokens[b] (device int32 [batch]) at position
  * len_b (its current length), appends its key/value to the cache, writes the
  * logits (device float [batch, V], or NULL to skip) and the argmax token
  * (device int32 [batch]), and increments len_b.  Fails with AXON_E_CAPACITY if
