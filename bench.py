@@ -27,6 +27,7 @@ BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 F32_PEAK_TFLOPS = 157.3     # MI355X fp32 vector
 
 METRIC = "prefill & decode tokens/s + decode HBM GB/s fraction, 1B and 7B shapes"
+COUNTER_DECODE_STEPS = 4    # decode steps of the hardware-counter runs
 
 
 def log(*a):
@@ -263,6 +264,9 @@ def measure_generate(args, workload, n_steps, n_warmup):
     if not args.no_roofline:
         out.update(roofline_pass(m, generate, shape, esz, lens))
         out["roofline"]["traffic"] = measured_traffic(out["roofline"], workload)
+        att = out["kernels"].get("decode attention (+ split merge)")
+        if att is not None:
+            att["traffic_per_layer"] = measured_attention_traffic(workload)
     m.close()
     del w
     torch.cuda.empty_cache()
@@ -283,7 +287,8 @@ def workload_summary(o):
                       ("decode projection GEMM (weight streaming)", "decode_projections"),
                       ("decode attention (+ split merge)", "decode_attention")):
         if name in k:
-            r[key] = {f: k[name][f] for f in ("bound", "achieved", "peak", "unit", "frac", "avg_us", "total_ms")}
+            r[key] = {f: k[name][f] for f in ("bound", "achieved", "peak", "unit", "frac", "avg_us", "total_ms",
+                                              "traffic_per_layer") if f in k[name]}
     if "roofline" in o:
         r["roofline"] = o["roofline"]
     return r
@@ -627,6 +632,30 @@ def kernel_source_digest():
     return h.hexdigest()[:16]
 
 
+def attention_source_digest():
+    """Digest of the decode attention kernels' source (k_attn.hip, common.h)."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_19889_amd", "csrc")
+    for f in ("k_attn.hip", "common.h"):
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_attention_traffic(workload):
+    """HBM bytes per layer of the decode attention (with its split merge) from
+    the committed counter runs, or None when they were taken on other kernel
+    sources."""
+    path = os.path.join(ROOT, "profiles", f"decode_gemv_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    att = rec.get("decode_attention")
+    if not att or rec.get("attention_source_digest") != attention_source_digest():
+        return None
+    return att.get("hbm_bytes_per_layer")
+
+
 def measured_traffic(roof, workload):
     """HBM bytes per launch of the decode projection kernels from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE runs (scaled by the counters' reading of
@@ -662,6 +691,11 @@ def summarize_counters(fetch_csv, write_csv, workload):
         agg, names, after = {}, {}, None
         for r in rows:
             name = r["Kernel_Name"]
+            if "attn_decode_bf16_kernel" in name or "attn_combine_kernel" in name:
+                a = agg.setdefault("attention" if "attn_decode" in name else "attention merge", [0, 0.0])
+                a[0] += 1
+                a[1] += float(r["Counter_Value"]) * 1024.0 * scale
+                continue
             if "gemv_fused_kernel" not in name:
                 continue
             targs = name[name.index("gemv_fused_kernel<") + 18:name.index(">")].split(",")
@@ -683,18 +717,48 @@ def summarize_counters(fetch_csv, write_csv, workload):
     fs, fetch, names = per_role(fetch_csv)
     ws, write, _ = per_role(write_csv)
     per = {k: fetch[k] + write.get(k, 0.0) for k in fetch}
+    # decode attention: HBM bytes of one layer's launch (with its split merge,
+    # when there is one) against its algorithmic bytes (K and V of every key
+    # each sequence attends to, q read and o written), averaged over the
+    # COUNTER_DECODE_STEPS decode steps of the counter run
+    shape = MODEL_SHAPES[wl["model"]]
+    KV, hd, H = shape["num_key_value_heads"], shape["head_dim"], shape["num_attention_heads"]
+    W = shape.get("sliding_window") or 0
+    if wl["paged"]:
+        from synthetic import paged_workload
+        seqs, _, _ = paged_workload(wl["batch"], wl["len_range"][0], wl["len_range"][1], steps,
+                                    shape["vocab_size"], wl["page_size"], seed=0)
+        lens = [len(x) for x in seqs]
+    else:
+        lens = [wl["prompt_len"]] * wl["batch"]
+    alg = 0.0
+    for st in range(COUNTER_DECODE_STEPS):
+        keys = sum(min(n + st + 1, W) if W else n + st + 1 for n in lens)
+        alg += 2 * KV * hd * 2 * keys + 2 * len(lens) * H * hd * 2
+    alg /= COUNTER_DECODE_STEPS
+    attention = None
+    if "attention" in per:
+        hbm = per["attention"] + per.get("attention merge", 0.0)
+        attention = {"hbm_bytes_per_layer": round(hbm), "algorithmic_bytes_per_layer": round(alg),
+                     "ratio": round(hbm / alg, 4), "kernel_bytes": round(per["attention"]),
+                     "merge_bytes": round(per.get("attention merge", 0.0))}
+    for k in ("attention", "attention merge"):
+        per.pop(k, None)
     step_bytes = L * sum(per[k] for k in ("qkv", "o", "gate/up", "down")) + per["head (decode)"]
     launches = steps * (4 * L + 1) + 1
     total = steps * step_bytes + per["head (prefill)"]
     rec = {"workload": workload, "kernel_source_digest": kernel_source_digest(),
+           "attention_source_digest": attention_source_digest(),
            "fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
            "hbm_bytes_per_launch_by_role": {k: round(v) for k, v in per.items()},
            "kernel_by_role": names,
            "hbm_bytes_per_launch": round(total / launches),
            "launch_mix": f"{steps} decode steps x ({L} layers x 4 projections + head) + prefill head = {launches}",
-           "commands": [f"rocprofv3 --pmc {c} --kernel-include-regex 'gemv_fused|copyBuffer|elementwise_kernel' "
+           "decode_attention": attention,
+           "commands": [f"rocprofv3 --pmc {c} --kernel-include-regex "
+                        f"'gemv_fused|attn_decode|attn_combine|copyBuffer|elementwise_kernel' "
                         f"-f csv -d <dir> -o run -- python3 bench.py --workload {workload} --steps 1 --warmup 0 "
-                        f"--decode-steps 4 --no-cpu-baseline --no-roofline --copy-calibration"
+                        f"--decode-steps {COUNTER_DECODE_STEPS} --no-cpu-baseline --no-roofline --copy-calibration"
                         for c in ("FETCH_SIZE", "WRITE_SIZE")]}
     out = os.path.join(ROOT, "profiles", f"decode_gemv_{workload}_traffic.json")
     with open(out, "w") as f:
