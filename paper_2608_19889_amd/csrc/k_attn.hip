@@ -98,17 +98,32 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
   constexpr int TQ = 4 * WQ;             // queries per workgroup
   __shared__ bf16x8 lds[2 * BUF];
 
-  // locate (entry, query tile) of this workgroup
-  int li = 0, tile = blockIdx.x, ent = 0;
+  // (entry, query tile, head) of this workgroup, in an XCD-aware order: the
+  // workgroup id mod 8 picks the XCD, and each XCD walks a contiguous range
+  // of (kv head, entry, query tile from the longest down, query head of the
+  // group), so the workgroups that read one sequence's keys and values for
+  // one kv head run together on one XCD and find them in its L2, and the
+  // longest tiles start first
+  const int group = H / kv.kv_heads;
+  const int G = gridDim.x, ntl = G / H;  // ntl: query tiles over all entries
+  int logical = blockIdx.x;
+  const int full = G / 8 * 8;
+  if (logical < full) logical = (logical % 8) * (full / 8) + logical / 8;
+  const int hin = logical % group;
+  const int rest = logical / group;
+  int tile = rest % ntl;
+  const int kvh = rest / ntl;
+  const int head = kvh * group + hin;
+  int li = 0, ent = 0;
   for (; li < nseq; ++li) {
     ent = ents ? ents[li] : li;
     const int nt = (cu[ent + 1] - cu[ent] + TQ - 1) / TQ;
-    if (tile < nt) break;
+    if (tile < nt) {
+      tile = nt - 1 - tile;
+      break;
+    }
     tile -= nt;
   }
-  const int head = blockIdx.y;
-  const int group = H / kv.kv_heads;
-  const int kvh = head / group;
   const int S = cu[ent + 1] - cu[ent];         // this call's queries of the entry
   const int tok0 = cu[ent];
   const int seq = ent_slot ? ent_slot[ent] : ent;  // cache slot
@@ -629,7 +644,7 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
       const int e = h_ents ? h_ents[i] : i;
       tiles += (h_cu[e + 1] - h_cu[e] + TQ - 1) / TQ;
     }
-    dim3 grid(tiles, H);
+    const dim3 grid(tiles * H);  // the kernel maps the linear id to (tile, head)
     if (kv.hd == 64)
       attn_prefill_bf16_kernel<64, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base, lse);
     else
