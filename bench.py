@@ -691,7 +691,7 @@ def summarize_counters(fetch_csv, write_csv, workload):
         agg, names, after = {}, {}, None
         for r in rows:
             name = r["Kernel_Name"]
-            if "attn_decode_bf16_kernel" in name or "attn_combine_kernel" in name:
+            if "attn_decode_bf16_kernel" in name or "attn_combine_kernel" in name:  # (older builds: a merge kernel)
                 a = agg.setdefault("attention" if "attn_decode" in name else "attention merge", [0, 0.0])
                 a[0] += 1
                 a[1] += float(r["Counter_Value"]) * 1024.0 * scale

@@ -300,7 +300,7 @@ int axon_slot_lengths(const axon_model* m, int32_t* lens, int32_t n);
 /* Measurement support.  While enabled, every launch of the kernel classes
  *   0 = few-token projection GEMM (decode, weight streaming),
  *   1 = many-token projection GEMM (prefill, MFMA tiles),
- *   2 = decode attention (split over key chunks, with its combine kernel),
+ *   2 = decode attention (split over key chunks; the last split merges),
  *   3 = prefill attention,
  *   4 = grouped expert projection of a mixture-of-experts decode step (dims
  *       as class 0 with N, K of one expert and M the step's tokens; the

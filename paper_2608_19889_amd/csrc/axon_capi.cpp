@@ -268,6 +268,7 @@ struct DecodeWs {
   bf16* o;           // attention output [B][H hd]
   bf16* a;           // gated activation [B][I]
   float* attn_part;  // decode attention split partials
+  int32_t* attn_cnt; // decode attention split arrival counters [B][KV], zero between launches
   float* gemv_part;  // split-K partials of the projections
   float* am_val;     // head argmax partials [B][ceil(V / 16)]
   int32_t* am_idx;
@@ -310,6 +311,7 @@ struct axon_model {
   float* gu_f32 = nullptr;
   float* logits_int = nullptr;
   float* attn_part = nullptr;
+  int32_t* attn_cnt = nullptr;  // [max_batch][KV], zero between decode attention launches
   float* gemv_part = nullptr;  // split-K partial sums of the decode projections
   float* gemm_part = nullptr;  // split-K partial sums of the narrow prefill / training GEMMs
   int64_t gemm_part_floats = 0;
@@ -324,7 +326,7 @@ struct axon_model {
   void* scratch_ptr = nullptr;
   std::string scratch_err;
   DecodeWs own_ws() const {
-    return DecodeWs{x, (bf16*)xg, ss, (bf16*)q, (bf16*)o, (bf16*)a, attn_part, gemv_part, am_val, am_idx};
+    return DecodeWs{x, (bf16*)xg, ss, (bf16*)q, (bf16*)o, (bf16*)a, attn_part, attn_cnt, gemv_part, am_val, am_idx};
   }
   // per-entry arrays of a continuous-batching step (6 x max_batch int32):
   // slot, base position, chunk entries, single-token rows / slots / positions
@@ -681,7 +683,7 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
         });
       if (plan->nd > 0)
         m->timed(2, H, plan->nd, plan->dctx, s, [&] {
-          launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, plan->nd, H, plan->d_dpos,
+          launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, m->attn_cnt, plan->nd, H, plan->d_dpos,
                                 m->cfg.max_seq, s, plan->d_drow, plan->d_dslot);
         });
     } else {
@@ -778,7 +780,7 @@ void enqueue_decode_many(axon_model* m, int B, const int32_t* d_tokens, float* d
       launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, B, 0, nullptr,
                         m->d_len, H, s);
     }
-    launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, B, H, m->d_len, m->cfg.max_seq, s);
+    launch_attn_decode<T>((const T*)m->q, kv, (T*)m->o, m->attn_part, m->attn_cnt, B, H, m->d_len, m->cfg.max_seq, s);
     proj(w.wo, m->o, D, H * hd, EPI_RESID, m->x, nullptr, D);
     launch_resid_rmsnorm<T>(m->x, nullptr, 0, 0, (const T*)w.gpost, h, B, D, eps, nullptr, s);
     if (w.moe) {
@@ -839,7 +841,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
     if (plan) ctx_sum = plan->dctx;
     else for (int b = 0; b < B; ++b) ctx_sum += m->keys_read(m->h_len[b] + 1);
     m->timed(2, H, B, ctx_sum, s, [&] {
-      launch_attn_decode<bf16>(ws.q, kv, ws.o, ws.attn_part, B, H, pos, m->cfg.max_seq, s, nullptr, slot);
+      launch_attn_decode<bf16>(ws.q, kv, ws.o, ws.attn_part, ws.attn_cnt, B, H, pos, m->cfg.max_seq, s, nullptr, slot);
     });
     GemvArgs oa{};
     oa.W = (const bf16*)w.wo; oa.N = D; oa.K = H * hd; oa.M = B; oa.X = ws.o;
@@ -939,7 +941,7 @@ void enqueue_decode_gpt2(axon_model* m, int B, const int32_t* d_tokens, float* d
     if (plan) ctx_sum = plan->dctx;
     else for (int b = 0; b < B; ++b) ctx_sum += m->keys_read(m->h_len[b] + 1);
     m->timed(2, H, B, ctx_sum, s, [&] {
-      launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, B, H, pos, m->cfg.max_seq, s,
+      launch_attn_decode<bf16>((const bf16*)m->q, kv, (bf16*)m->o, m->attn_part, m->attn_cnt, B, H, pos, m->cfg.max_seq, s,
                                nullptr, slot);
     });
     proj(w.wo, (const bf16*)m->o, D, H * hd, GV_RESID, w.bo);
@@ -1334,6 +1336,8 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     for (int b = 1; b <= c.max_batch; ++b)
       bsplits = std::max<int64_t>(bsplits, (int64_t)b * plan_decode_splits(b, c.n_kv_heads, c.max_seq));
     TRY(dev_alloc(m, (void**)&m->attn_part, bsplits * H * (hd + 2) * 4));
+    TRY(dev_alloc(m, (void**)&m->attn_cnt, (size_t)c.max_batch * KV * sizeof(int32_t)));
+    HTRY(hipMemsetAsync(m->attn_cnt, 0, (size_t)c.max_batch * KV * sizeof(int32_t), s));
     if (m->bf) {
       int64_t wsf = 0;
       const int Is = c.n_shared_experts * c.moe_intermediate;
@@ -1526,6 +1530,7 @@ size_t decode_ws_layout(const axon_model* m, int B, char* base, DecodeWs* ws) {
     return base ? base + at : nullptr;
   };
   DecodeWs w{};
+  w.attn_cnt = (int32_t*)take((int64_t)B * m->KVh() * 4);  // first, cleared by every call
   w.x = (float*)take(B * D * 4);
   w.xg = (bf16*)take(B * D * 2);
   w.ss = (float*)take(std::max<int64_t>(D / 8, 1) * B * 4);
@@ -1569,6 +1574,9 @@ extern "C" int axon_decode_step_noalloc(axon_model* m, int32_t batch, const int3
   // timing events are created
   const bool timing = m->timing;
   m->timing = false;
+  // the split counters must start at zero; the array keeps whatever the last
+  // call on this GPU left there
+  launch_zero_i32(ws.attn_cnt, batch * m->KVh(), s);
   enqueue_decode_bf16(m, batch, d_tokens, d_logits, d_next_tokens, s, nullptr, nullptr, &ws);
   m->timing = timing;
   int rc = check_launch("decode (no allocation)");

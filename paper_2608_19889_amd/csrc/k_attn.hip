@@ -319,7 +319,9 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
 // into registers, NBUF chunks in flight per wavefront.  The
 // wavefronts' (max, sum, o) are merged in LDS; with one split the normalized
 // output is written directly, otherwise every split stores an unnormalized
-// partial and the combine kernel merges them.
+// partial and the last split of its (slot, kv head) to finish, found with a
+// counter in ``cnt`` (zero before the launch, left zero after it), merges
+// them.
 // ============================================================================
 
 // Item b: query row rows[b] (b when null) of q / o, cache slot slots[b] (b
@@ -327,7 +329,8 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
 template <int HD, int DNW, bool PAGED, int NBUF>
 __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* __restrict__ q, KVView kv,
                                                                     bf16* __restrict__ o, float* __restrict__ part,
-                                                                    int H, const int32_t* __restrict__ len,
+                                                                    int32_t* __restrict__ cnt, int H,
+                                                                    const int32_t* __restrict__ len,
                                                                     int split_len, const int32_t* __restrict__ rows,
                                                                     const int32_t* __restrict__ slots) {
   extern __shared__ float dyn[];
@@ -497,59 +500,70 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
     if (nsplit == 1) {
       o[((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
     } else {
+      // system-scope stores: written through to memory, so the split that
+      // merges (on any XCD) reads them without an L2 write-back
       float* pp = part + (((int64_t)b * H + h) * nsplit + split) * (HD + 2);
-      pp[d] = O;
+      __hip_atomic_store(pp + d, O, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
       if (d == 0) {
-        pp[HD] = M;
-        pp[HD + 1] = L;
+        __hip_atomic_store(pp + HD, M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        __hip_atomic_store(pp + HD + 1, L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
       }
     }
   }
-}
-
-// Merge the split partials of one (slot, head), in split order:
-// o = sum_c 2^(m_c - M) o_c / sum_c 2^(m_c - M) l_c.
-template <int HD>
-__global__ void __launch_bounds__(HD) attn_combine_kernel(const float* __restrict__ part, bf16* __restrict__ o, int H,
-                                                          const int32_t* __restrict__ len, int nsplit,
-                                                          int split_len, const int32_t* __restrict__ rows,
-                                                          int window) {
-  const int b = blockIdx.y, h = blockIdx.x, d = threadIdx.x;
-  const int row = rows ? rows[b] : b;
-  const int ctx = len[b] + 1;
-  const int lo = (window ? max(0, ctx - window) : 0) & ~31;  // as the attention kernel's first split
-  const int nact = min(nsplit, (ctx - lo + split_len - 1) / split_len);
-  const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
-  // 8 independent loads per round (a load-then-use loop waits for every
-  // load in turn); the sums still run in split order
-  float M = -INFINITY;
-  for (int b0 = 0; b0 < nact; b0 += 8) {
-    float mv[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) mv[u] = pp[min(b0 + u, nact - 1) * (HD + 2) + HD];
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (b0 + u < nact) M = fmaxf(M, mv[u]);
+  if (nsplit == 1) return;
+  // The split that arrives last merges the active splits' partials (in split
+  // order) and resets its (slot, kv head) counter for the next launch: every
+  // thread's partial stores have completed before the workgroup's arrival is
+  // counted.
+  const int lo31 = lo & ~31;
+  const int nact = min(nsplit, (ctx - lo31 + split_len - 1) / split_len);  // splits with s0 < ctx
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  int* flag = (int*)dyn;
+  if (threadIdx.x == 0) {
+    int32_t* cp = cnt + (int64_t)b * kv.kv_heads + kvh;
+    const int arrived = __hip_atomic_fetch_add(cp, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = arrived == nact - 1;
+    if (last) __hip_atomic_exchange(cp, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    flag[0] = last;
   }
-  float L = 0.f, O = 0.f;
-  for (int b0 = 0; b0 < nact; b0 += 8) {
-    float mv[8], lv[8], ov[8];
+  __syncthreads();
+  if (!flag[0]) return;
+  for (int idx = threadIdx.x; idx < group * HD; idx += DNW * 64) {
+    const int c = idx / HD, d = idx % HD, h = kvh * group + c;
+    const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
+    // up to 8 splits' loads in flight per round; sums in split order
+    float M = -INFINITY;
+    for (int b0 = 0; b0 < nact; b0 += 8) {
+      float mv[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const float* ps = pp + min(b0 + u, nact - 1) * (HD + 2);
-      mv[u] = ps[HD];
-      lv[u] = ps[HD + 1];
-      ov[u] = ps[d];
+      for (int u = 0; u < 8; ++u)
+        mv[u] = __hip_atomic_load(pp + min(b0 + u, nact - 1) * (HD + 2) + HD, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_SYSTEM);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (b0 + u < nact) M = fmaxf(M, mv[u]);
     }
+    float L = 0.f, O = 0.f;
+    for (int b0 = 0; b0 < nact; b0 += 8) {
+      float mv[8], lv[8], ov[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (b0 + u < nact) {
-        const float f = exp2f(mv[u] - M);
-        L += f * lv[u];
-        O += f * ov[u];
+      for (int u = 0; u < 8; ++u) {
+        const float* ps = pp + min(b0 + u, nact - 1) * (HD + 2);
+        mv[u] = __hip_atomic_load(ps + HD, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        lv[u] = __hip_atomic_load(ps + HD + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        ov[u] = __hip_atomic_load(ps + d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
       }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (b0 + u < nact) {
+          const float f = exp2f(mv[u] - M);
+          L += f * lv[u];
+          O += f * ov[u];
+        }
+    }
+    o[((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
   }
-  o[((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
 }
 
 // ============================================================================
@@ -624,6 +638,16 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ 
   for (int i = 0; i < DL; ++i) op[lane + i * 64] = acc[i] / l;
 }
 
+// p[0 .. n) = 0 (a kernel, so that it may be recorded into a graph)
+__global__ void __launch_bounds__(256) zero_i32_kernel(int32_t* __restrict__ p, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+void launch_zero_i32(int32_t* p, int n, hipStream_t s) {
+  if (n > 0) zero_i32_kernel<<<(n + 255) / 256, 256, 0, s>>>(p, n);
+}
+
 // ---------------------------------------------------------------- launchers
 
 template <typename T>
@@ -656,9 +680,10 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
 // Few (slot, kv head) pairs leave most CUs idle, so their keys are split
 // towards ~256 workgroups with >= 512 keys per split; many pairs are split
 // only for long contexts (<= 1536 keys per split), which bounds the time of the
-// longest sequences of a ragged batch.  Split partials are merged by a second
-// kernel (merging inside the first would take a device-scope release fence
-// per workgroup, an L2 write-back, which costs more).
+// longest sequences of a ragged batch.  The last split of a (slot, kv head)
+// to finish merges the partials (system-scope stores and loads carry them
+// between XCDs without an L2 write-back).  Splitting short contexts further
+// (128 keys per split on the 1B-shaped batch) measured slower.
 constexpr int DECODE_WAVES = 8;
 
 int plan_decode_splits(int B, int kv_heads, int max_ctx) {
@@ -669,8 +694,9 @@ int plan_decode_splits(int B, int kv_heads, int max_ctx) {
 }
 
 template <int HD, int NW>
-static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int B, int H, const int32_t* len,
-                          int nsplit, int split_len, hipStream_t s, const int32_t* rows, const int32_t* slots) {
+static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int32_t* cnt, int B, int H,
+                          const int32_t* len, int nsplit, int split_len, hipStream_t s, const int32_t* rows,
+                          const int32_t* slots) {
   const int group = H / kv.kv_heads;
   const size_t lds = (size_t)(2 * NW * 16 + NW * group * HD) * sizeof(float);
   const dim3 grid(nsplit, kv.kv_heads, B);
@@ -680,17 +706,15 @@ static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int B,
   constexpr int NBUF = 1;
   if (kv.bt)
     attn_decode_bf16_kernel<HD, NW, true, NBUF>
-        <<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len, rows, slots);
+        <<<grid, NW * 64, lds, s>>>(q, kv, o, part, cnt, H, len, split_len, rows, slots);
   else
     attn_decode_bf16_kernel<HD, NW, false, NBUF>
-        <<<grid, NW * 64, lds, s>>>(q, kv, o, part, H, len, split_len, rows, slots);
-  if (nsplit > 1)
-    attn_combine_kernel<HD><<<dim3(H, B), HD, 0, s>>>(part, o, H, len, nsplit, split_len, rows, kv.window);
+        <<<grid, NW * 64, lds, s>>>(q, kv, o, part, cnt, H, len, split_len, rows, slots);
 }
 
 template <typename T>
-void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len, int max_ctx,
-                        hipStream_t s, const int32_t* rows, const int32_t* slots) {
+void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* cnt, int B, int H, const int32_t* len,
+                        int max_ctx, hipStream_t s, const int32_t* rows, const int32_t* slots) {
   if (B <= 0) return;
   if constexpr (sizeof(T) == 4) {
     dim3 grid(B, H);  // the float32 path takes rows / slots through launch_attn_prefill
@@ -700,8 +724,8 @@ void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, 
     if (kv.window) max_ctx = std::min(max_ctx, kv.window + 31);  // keys from the window's 32-key chunk
     const int nsplit = plan_decode_splits(B, kv.kv_heads, max_ctx);
     const int split_len = ((max_ctx + nsplit - 1) / nsplit + 63) / 64 * 64;
-    if (kv.hd == 64) decode_launch<64, DECODE_WAVES>(q, kv, o, part, B, H, len, nsplit, split_len, s, rows, slots);
-    else decode_launch<128, DECODE_WAVES>(q, kv, o, part, B, H, len, nsplit, split_len, s, rows, slots);
+    if (kv.hd == 64) decode_launch<64, DECODE_WAVES>(q, kv, o, part, cnt, B, H, len, nsplit, split_len, s, rows, slots);
+    else decode_launch<128, DECODE_WAVES>(q, kv, o, part, cnt, B, H, len, nsplit, split_len, s, rows, slots);
   }
 }
 
@@ -711,9 +735,9 @@ template void launch_attn_prefill<float>(const float*, KVView, float*, int, int,
 template void launch_attn_prefill<bf16>(const bf16*, KVView, bf16*, int, int, const int32_t*, const int32_t*, int,
                                         hipStream_t, const int32_t*, const int32_t*, const int32_t*, const int32_t*,
                                         float*);
-template void launch_attn_decode<float>(const float*, KVView, float*, float*, int, int, const int32_t*, int,
-                                        hipStream_t, const int32_t*, const int32_t*);
-template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int, int, const int32_t*, int,
+template void launch_attn_decode<float>(const float*, KVView, float*, float*, int32_t*, int, int, const int32_t*,
+                                        int, hipStream_t, const int32_t*, const int32_t*);
+template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int32_t*, int, int, const int32_t*, int,
                                        hipStream_t, const int32_t*, const int32_t*);
 
 }  // namespace axon

@@ -274,13 +274,18 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
 // Decode attention: one query per slot at position len[b] (after the step's
 // key/value were written), context len[b] + 1; keys split over
 // plan_decode_splits() workgroups per (slot, kv head).  ``part`` holds
-// B * H * splits * (hd + 2) floats.
+// B * H * splits * (hd + 2) floats; the last split of a (slot, kv head)
+// merges them.
 int plan_decode_splits(int B, int kv_heads, int max_ctx);
 // Item b reads query row rows[b] and writes output row rows[b] (b when null),
 // in cache slot slots[b] (b when null), at position len[b]; bf16 only for the
 // indirection (the float32 path reaches such items through launch_attn_prefill).
+// p[0 .. n) = 0, as a kernel (graph-capture safe)
+void launch_zero_i32(int32_t* p, int n, hipStream_t s);
+// cnt: int32 [B][kv heads], zero before the launch and left zero after it
+// (split arrival counters).
 template <typename T>
-void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int B, int H, const int32_t* len,
+void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* cnt, int B, int H, const int32_t* len,
                         int max_ctx, hipStream_t s, const int32_t* rows = nullptr,
                         const int32_t* slots = nullptr);
 
