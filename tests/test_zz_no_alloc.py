@@ -20,18 +20,26 @@ from synthetic import MODEL_SHAPES, model_weights, prompts, small_shape
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("kind", ["1b_2_layers", "7b_2_layers_paged"])
+@pytest.mark.parametrize("kind", ["1b_2_layers", "7b_2_layers_paged", "1b_2_layers_long_split"])
 def test_noalloc_decode_equals_decode(kind):
+    lens, max_seq = [90, 37, 64, 5], 112
     if kind == "1b_2_layers":
         shape = small_shape("1b", layers=2, vocab=8192)
         page = {}
+    elif kind == "1b_2_layers_long_split":
+        # contexts up to 1500 keys in a 2048-token cache: the decode attention
+        # splits each (slot, kv head) in 4 and merges through the counters
+        # kept in the fixed array
+        shape = small_shape("1b", layers=2, vocab=8192)
+        page = {}
+        lens, max_seq = [1500, 700, 1201, 33], 2048
     else:
         shape = small_shape("7b", layers=2, vocab=8192)
         page = dict(page_size=16, num_pages=64)
     print(f"[noalloc] {kind}", flush=True)
     w = model_weights(shape, seed=21, device="cuda")
-    ids = prompts(4, 90, shape["vocab_size"], seed=22).numpy()
-    seqs = [ids[0], ids[1, :37], ids[2, :64], ids[3, :5]]
+    ids = prompts(4, max(lens), shape["vocab_size"], seed=22).numpy()
+    seqs = [ids[b, :n] for b, n in enumerate(lens)]
     table = None
     if page:
         table = torch.full((4, 16), -1, dtype=torch.int32)
@@ -39,8 +47,8 @@ def test_noalloc_decode_equals_decode(kind):
         for b in range(4):
             table[b, :7] = perm[7 * b:7 * b + 7]
     flat, cu = pack(seqs)
-    ref = Model(shape, w, max_batch=4, max_seq=112, **page)
-    new = Model(shape, w, max_batch=4, max_seq=112, **page)
+    ref = Model(shape, w, max_batch=4, max_seq=max_seq, max_tokens=sum(lens), **page)
+    new = Model(shape, w, max_batch=4, max_seq=max_seq, max_tokens=sum(lens), **page)
     _, t_ref = ref.prefill(flat, cu, block_table=table)
     _, t_new = new.prefill(flat, cu, block_table=table)
     torch.cuda.synchronize()
@@ -59,8 +67,7 @@ def test_noalloc_decode_equals_decode(kind):
         assert torch.equal(lg_ref, lg_new), (lg_ref - lg_new).abs().max().item()
         assert torch.equal(nx_ref, nx_new)
         t_ref = torch.cat([nx_ref, t_ref[batch:]])
-    assert ref.lengths() == new.lengths() == [len(seqs[0]) + 2, len(seqs[1]) + 2, len(seqs[2]) + 1,
-                                              len(seqs[3]) + 1]
+    assert ref.lengths() == new.lengths() == [lens[0] + 2, lens[1] + 2, lens[2] + 1, lens[3] + 1]
     # without logits, tokens only
     tok = t_ref[:3].clone()
     nx_ref = torch.empty(3, dtype=torch.int32, device="cuda")
