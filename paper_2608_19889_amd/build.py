@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "libaxon.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["axon_capi.cpp", "k_layout.hip", "k_norm.hip", "k_gemm.hip", "k_gemv.hip", "k_rope.hip", "k_attn.hip",
-           "k_moe.hip", "k_layernorm.hip", "k_train.hip"]
+           "k_moe.hip", "k_layernorm.hip", "k_train.hip", "k_gemv_f32.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC,
          # keep the compiler from emitting packed fp32 arithmetic
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -270,7 +270,7 @@ struct DecodeWs {
   float* attn_part;  // decode attention split partials
   int32_t* attn_cnt; // decode attention split arrival counters [B][KV], zero between launches
   float* gemv_part;  // split-K partials of the projections
-  float* am_val;     // head argmax partials [B][ceil(V / 16)]
+  float* am_val;     // head argmax partials [B][V / rows of the head tile]
   int32_t* am_idx;
 };
 
@@ -892,6 +892,75 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
   if (plan) launch_set_step_lengths(d_cu, plan->d_slot, plan->d_base, m->d_len, B, s);
 }
 
+// Decode step of a float32 model (Llama family) over at most 16 tokens: the
+// float32 fused projections, 5 kernels per layer (4 when the contexts are
+// short enough for every O workgroup to compute the attention itself).
+//   embed: x = E[tok], xg = x * g, sum of squares
+//   per layer: QKV (RMSNorm on load; bias + RoPE + KV write) -> attention ->
+//              O (x += ; xg, sums of squares) -> gate/up (RMSNorm on load;
+//              SiLU) -> down (x += ; xg, sums of squares)
+//   head (RMSNorm on load; logits + argmax partials) -> argmax
+void enqueue_decode_f32(axon_model* m, int B, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
+                        hipStream_t s) {
+  const int D = m->D(), H = m->H(), hd = m->hd(), I = m->I(), V = m->V(), nq = m->nqkv();
+  const float eps = m->cfg.rms_eps;
+  float* xg = (float*)m->xg;
+  // contexts never exceed the capacity max_seq
+  const bool fused_attn = attn_o_f32_fits(B, H, m->KVh(), hd, m->cfg.max_seq);
+  launch_embed_ss_f32(d_tokens, (const float*)m->embed, (const float*)m->layers[0].gin, m->x, xg, m->ss, B, D, V, s);
+  int ss_n = 1;
+  auto proj = [&](GemvF32Args& a, int epi) {
+    bool ok = true;
+    m->timed(0, a.N, a.M, a.K, s, [&] { ok = launch_gemv_f32_fused(a, epi, s); });
+    if (!ok && m->enqueue_err.empty())
+      m->enqueue_err = "no float32 projection kernel for N=" + std::to_string(a.N) + " K=" + std::to_string(a.K) +
+                       " M=" + std::to_string(a.M) + " epilogue " + std::to_string(epi);
+  };
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    const LayerW& w = m->layers[l];
+    KVView kv = m->kv(l, m->paged());
+    const bool last = l + 1 == m->cfg.n_layers;
+    GemvF32Args qa{};
+    qa.W = (const float*)w.wqkv; qa.N = nq; qa.K = D; qa.M = B;
+    qa.X = xg; qa.ss_in = m->ss; qa.ss_n = ss_n; qa.eps = eps;
+    qa.bias = (const float*)w.bqkv; qa.cos_t = m->rope_cos; qa.sin_t = m->rope_sin; qa.q_out = (float*)m->q;
+    qa.kv = kv; qa.len = m->d_len; qa.H = H;
+    proj(qa, GV_ROPE);
+    GemvF32Args oa{};
+    oa.W = (const float*)w.wo; oa.N = D; oa.K = H * hd; oa.M = B; oa.X = (const float*)m->o;
+    oa.out = m->x; oa.ldo = D; oa.xg_out = xg; oa.gain_next = (const float*)w.gpost; oa.ss_out = m->ss;
+    if (fused_attn) {
+      // short contexts: every O workgroup computes the attention itself
+      oa.len = m->d_len; oa.H = H;
+      bool ok = true;
+      m->timed(0, D, B, H * hd, s, [&] { ok = launch_attn_o_f32(oa, (const float*)m->q, kv, s); });
+      if (!ok && m->enqueue_err.empty()) m->enqueue_err = "no fused attention + O projection kernel";
+    } else {
+      m->timed(2, H, B, 0, s, [&] {
+        launch_attn_decode<float>((const float*)m->q, kv, (float*)m->o, m->attn_part, m->attn_cnt, B, H, m->d_len,
+                                  m->cfg.max_seq, s);
+      });
+      proj(oa, GV_RESID);
+    }
+    ss_n = gemv_f32_parts(D, GV_RESID);
+    GemvF32Args ga{};
+    ga.W = (const float*)w.wgu; ga.N = 2 * I; ga.K = D; ga.M = B;
+    ga.X = xg; ga.ss_in = m->ss; ga.ss_n = ss_n; ga.eps = eps; ga.out = (float*)m->a; ga.ldo = I;
+    proj(ga, GV_SILU);
+    GemvF32Args da{};
+    da.W = (const float*)w.wd; da.N = D; da.K = I; da.M = B; da.X = (const float*)m->a;
+    da.out = m->x; da.ldo = D; da.xg_out = xg; da.ss_out = m->ss;
+    da.gain_next = (const float*)(last ? m->gfinal : m->layers[l + 1].gin);
+    proj(da, GV_RESID);
+  }
+  GemvF32Args ha{};
+  ha.W = (const float*)m->lm_head; ha.N = V; ha.K = D; ha.M = B;
+  ha.X = xg; ha.ss_in = m->ss; ha.ss_n = ss_n; ha.eps = eps;
+  ha.out = d_logits; ha.ldo = V; ha.am_val = m->am_val; ha.am_idx = m->am_idx;
+  proj(ha, GV_HEAD);
+  launch_argmax_final(m->am_val, m->am_idx, gemv_f32_parts(V, GV_HEAD), B, d_next, m->d_len, s);
+}
+
 // Decode step of the GPT-2 family: embedding + learned position + the first
 // LayerNorm, then per layer QKV (bias, identity rotation, KV write) ->
 // attention -> c_proj (+ bias, residual) -> LayerNorm -> c_fc (+ bias, GELU)
@@ -971,6 +1040,7 @@ void enqueue_decode(axon_model* m, int B, const int32_t* d_tokens, float* d_logi
   if (m->gpt2()) enqueue_decode_gpt2(m, B, d_tokens, d_logits, d_next, s);
   else if (m->bf && B <= GEMV_MAX_M) enqueue_decode_bf16(m, B, d_tokens, d_logits, d_next, s);
   else if (m->bf) enqueue_decode_many<bf16>(m, B, d_tokens, d_logits, d_next, s);
+  else if (B <= GEMV_F32_MAX_M) enqueue_decode_f32(m, B, d_tokens, d_logits, d_next, s);
   else enqueue_decode_many<float>(m, B, d_tokens, d_logits, d_next, s);
 }
 
@@ -1360,8 +1430,8 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
       }
     }
     TRY(dev_alloc(m, (void**)&m->ss, (int64_t)std::max<int64_t>(D / 8, 1) * c.max_batch * 4));
-    TRY(dev_alloc(m, &m->xg, (int64_t)c.max_batch * D * 2));
-    const int64_t nam = (V + 15) / 16;
+    TRY(dev_alloc(m, &m->xg, (int64_t)c.max_batch * D * esz));
+    const int64_t nam = (V + 7) / 8;  // argmax partials per token (8-row float32 head tiles)
     TRY(dev_alloc(m, (void**)&m->am_val, nam * c.max_batch * 4));
     TRY(dev_alloc(m, (void**)&m->am_idx, nam * c.max_batch * 4));
     TRY(dev_alloc(m, (void**)&m->d_len, (size_t)c.max_batch * sizeof(int32_t)));

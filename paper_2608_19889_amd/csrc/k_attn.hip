@@ -638,6 +638,139 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(const float* __restrict__ 
   for (int i = 0; i < DL; ++i) op[lane + i * 64] = acc[i] / l;
 }
 
+// ============================================================================
+// float32 decode: one workgroup of 4 wavefronts per (query, kv head) serves the
+// kv head's group of query heads (at most 8), so every key and value is read
+// once per group.  Wavefront w takes the 64-key chunks w, w + 4, ...: lane j
+// loads key j of the chunk (independent 16-byte loads) and scores it against
+// each head of the group in turn, the online softmax runs per head across the
+// wavefront, and lane d then accumulates output dimensions d (and d + 64)
+// over the chunk's 64 keys from the V^T blocks (16 consecutive keys of a
+// dimension are 64 contiguous bytes).  The per-head running state (maximum,
+// sum, output accumulator) lives in the wavefront's own LDS rows, so the head
+// loop needs no registers per head.  Keys past the context (or before a
+// sliding window) get probability 0; their loads read the last key's block.
+// The wavefronts' states are merged at the end.
+// ============================================================================
+constexpr int F32_DEC_MAXG = 8;
+
+template <int HD>
+__global__ void __launch_bounds__(256) attn_decode_f32_kernel(const float* __restrict__ q, KVView kv,
+                                                              float* __restrict__ o, int H,
+                                                              const int32_t* __restrict__ len) {
+  constexpr int DL = HD / 64;  // output dimensions per lane
+  __shared__ f32x4 qs[F32_DEC_MAXG][HD / 4];
+  __shared__ f32x4 ps[4][F32_DEC_MAXG][16];  // probabilities of the chunk's 64 keys
+  __shared__ float sm[4][F32_DEC_MAXG], sl[4][F32_DEC_MAXG], sa[4][F32_DEC_MAXG];
+  __shared__ float so[4][F32_DEC_MAXG][HD];
+  const int b = blockIdx.x, kvh = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int G = H / kv.kv_heads;  // <= F32_DEC_MAXG (checked by the launcher)
+  const int pos = len[b], slot = b;
+  const int lo = kv.window ? max(0, pos - kv.window + 1) : 0;  // keys lo .. pos
+  const float sc = LOG2E / sqrtf((float)HD);
+  const float* kb = (const float*)kv.k;
+  const float* vb = (const float*)kv.v;
+  // key j of a chunk (clamped into the context) and, at head_dim 64, the
+  // chunk's V^T blocks of this lane's dimension: the loads of a chunk are
+  // issued before anything waits (for the first chunk, before the query
+  // staging), so they cost one memory round trip
+  f32x4 kr[HD / 4], vr[16];
+  auto load_k = [&](int j0) {
+    const float* kp = kb + k_el(kv, slot, kvh, min(max(j0 + lane, lo), pos), 0);
+#pragma unroll
+    for (int d = 0; d < HD / 4; ++d) kr[d] = *(const f32x4*)(kp + (d >> 1) * 128 + (d & 1) * 4);
+  };
+  auto load_v = [&](int j0, int d) {
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk) {
+      const float* vp = vb + v_el(kv, slot, kvh, min(j0 + blk * 16, pos & ~15), d);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) vr[blk * 4 + c] = *(const f32x4*)(vp + c * 4);
+    }
+  };
+  const int jfirst = (lo & ~63) + wave * 64;
+  if (jfirst <= pos) {  // wave-uniform
+    load_k(jfirst);
+    if constexpr (DL == 1) load_v(jfirst, lane);
+  }
+  for (int i = tid; i < G * (HD / 4); i += 256)
+    qs[i / (HD / 4)][i % (HD / 4)] =
+        *(const f32x4*)(q + ((int64_t)b * H + kvh * G + i / (HD / 4)) * HD + 4 * (i % (HD / 4)));
+  for (int i = lane; i < G * HD; i += 64) so[wave][i / HD][i % HD] = 0.f;
+  if (lane < G) {
+    sm[wave][lane] = -INFINITY;
+    sl[wave][lane] = 0.f;
+  }
+  __syncthreads();
+  for (int j0 = jfirst; j0 <= pos; j0 += 4 * 64) {
+    const int j = j0 + lane;
+    const bool valid = j >= lo && j <= pos;
+    {
+      for (int h = 0; h < G; ++h) {
+        // 4 independent partial sums (a single chain waits on every FMA)
+        float dp[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int d = 0; d < HD / 4; ++d) {
+          const f32x4 qv = qs[h][d];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dp[e] = fmaf(qv[e], kr[d][e], dp[e]);
+        }
+        const float dot = (dp[0] + dp[1]) + (dp[2] + dp[3]);
+        const float s = valid ? dot * sc : -INFINITY;
+        const float m_old = sm[wave][h];
+        const float m_new = fmaxf(m_old, wave_max(s));  // finite: the chunk holds a key in [lo, pos]
+        const float alpha = exp2f(m_old - m_new);
+        const float p = valid ? exp2f(s - m_new) : 0.f;
+        const float lsum = wave_sum(p);
+        ((float*)ps[wave][h])[lane] = p;
+        if (lane == 0) {
+          sl[wave][h] = sl[wave][h] * alpha + lsum;
+          sm[wave][h] = m_new;
+          sa[wave][h] = alpha;
+        }
+      }
+    }
+    // o = alpha o + P V over the chunk: lane d reads the 4 16-key blocks of
+    // dimension d (blocks past the context read the context's last block;
+    // their keys have probability 0).  Only this wavefront touches its rows.
+    const bool more = j0 + 4 * 64 <= pos;  // wave-uniform
+    if (more) load_k(j0 + 4 * 64);
+#pragma unroll
+    for (int i = 0; i < DL; ++i) {
+      const int d = lane + i * 64;
+      if constexpr (DL > 1) load_v(j0, d);
+      for (int h = 0; h < G; ++h) {
+        float pa[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+          const f32x4 pv = ps[wave][h][c];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) pa[e] = fmaf(pv[e], vr[c][e], pa[e]);
+        }
+        so[wave][h][d] = so[wave][h][d] * sa[wave][h] + ((pa[0] + pa[1]) + (pa[2] + pa[3]));
+      }
+    }
+    if constexpr (DL == 1) {
+      if (more) load_v(j0 + 4 * 64, lane);
+    }
+  }
+  __syncthreads();
+  // merge the wavefronts (a wavefront without keys has m = -inf, l = 0)
+  for (int idx = tid; idx < G * HD; idx += 256) {
+    const int h = idx / HD, d = idx % HD;
+    float M = -INFINITY;
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, sm[w][h]);
+    float L = 0.f, O = 0.f;
+    for (int w = 0; w < 4; ++w) {
+      const float f = sm[w][h] == -INFINITY ? 0.f : exp2f(sm[w][h] - M);
+      L += f * sl[w][h];
+      O += f * so[w][h][d];
+    }
+    o[((int64_t)b * H + kvh * G + h) * HD + d] = O / L;
+  }
+}
+
 // p[0 .. n) = 0 (a kernel, so that it may be recorded into a graph)
 __global__ void __launch_bounds__(256) zero_i32_kernel(int32_t* __restrict__ p, int n) {
   const int i = blockIdx.x * 256 + threadIdx.x;
@@ -717,9 +850,16 @@ void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* cnt, 
                         int max_ctx, hipStream_t s, const int32_t* rows, const int32_t* slots) {
   if (B <= 0) return;
   if constexpr (sizeof(T) == 4) {
-    dim3 grid(B, H);  // the float32 path takes rows / slots through launch_attn_prefill
-    if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H, nullptr, nullptr);
-    else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H, nullptr, nullptr);
+    // the float32 path takes rows / slots through launch_attn_prefill
+    if (H / kv.kv_heads <= F32_DEC_MAXG) {
+      const dim3 grid(B, kv.kv_heads);
+      if (kv.hd == 64) attn_decode_f32_kernel<64><<<grid, 256, 0, s>>>(q, kv, o, H, len);
+      else attn_decode_f32_kernel<128><<<grid, 256, 0, s>>>(q, kv, o, H, len);
+    } else {
+      const dim3 grid(B, H);
+      if (kv.hd == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H, nullptr, nullptr);
+      else attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, B, 0, nullptr, len, H, nullptr, nullptr);
+    }
   } else {
     if (kv.window) max_ctx = std::min(max_ctx, kv.window + 31);  // keys from the window's 32-key chunk
     const int nsplit = plan_decode_splits(B, kv.kv_heads, max_ctx);

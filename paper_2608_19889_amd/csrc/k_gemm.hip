@@ -615,7 +615,7 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
 }
 
 // ============================================================================
-// float32 check mode, up to 32 tokens (M <= MT): a wavefront per weight row, lanes
+// float32 check mode, one token (M <= MT): a wavefront per weight row, lanes
 // along K with 16-byte loads, compensated (Kahan) per-lane sums reduced across
 // the wavefront by shuffles.  K % 4 == 0.
 // ============================================================================
@@ -656,20 +656,112 @@ __global__ void __launch_bounds__(256) gemv_f32_kernel(const float* __restrict__
   }
 }
 
+// ============================================================================
+// float32 check mode, 2..32 tokens: the token rows are staged through LDS in
+// k-chunks of 256 (double-buffered; the next chunk's loads are issued before
+// the current chunk is used and stored after it), and each wavefront computes two weight rows for
+// every token, lanes along K with compensated (Kahan) per-lane sums and a
+// butterfly sum across the wavefront: the token operand is read from HBM once
+// per workgroup instead of once per weight row.  Workgroup = 8 rows x MT
+// tokens (token groups along gridDim.y, so that there are enough wavefronts
+// for the compensated sums).  K % 4 == 0.
+// ============================================================================
+template <int EPI, int MT>
+__global__ void __launch_bounds__(256) gemv_f32_lds_kernel(const float* __restrict__ W, const float* __restrict__ X,
+                                                           int N, int M, int K, EpiArgs ep) {
+  constexpr int KC = 256;
+  __shared__ f32x4 xs[2][MT][KC / 4];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // token group blockIdx.y: tokens MT y .. MT y + MT - 1
+  X += (int64_t)blockIdx.y * MT * K;
+  ep.out_f32 += (int64_t)blockIdx.y * MT * ep.ldo;
+  M = min(MT, M - (int)blockIdx.y * MT);
+  const int n0 = blockIdx.x * 8 + 2 * w, n1 = n0 + 1;
+  const float* w0 = W + (int64_t)min(n0, N - 1) * K;
+  const float* w1 = W + (int64_t)min(n1, N - 1) * K;
+  float acc0[MT], cmp0[MT], acc1[MT], cmp1[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc0[t] = cmp0[t] = acc1[t] = cmp1[t] = 0.f;
+  const int nch = (K + KC - 1) / KC;
+  // chunk c of the token rows: loaded into registers (MT * KC / 1024 16-byte
+  // pieces per thread), then written to xs[c & 1] (zeros past K and past M)
+  constexpr int SP = MT * (KC / 4) / 256;
+  f32x4 sv[SP];
+  auto stage_load = [&](int c) {
+#pragma unroll
+    for (int r = 0; r < SP; ++r) {
+      const int i = tid + r * 256, t = i / (KC / 4), k = c * KC + 4 * (i % (KC / 4));
+      sv[r] = *(const f32x4*)(X + (int64_t)min(t, M - 1) * K + min(k, K - 4));
+    }
+  };
+  auto stage_store = [&](int c) {
+#pragma unroll
+    for (int r = 0; r < SP; ++r) {
+      const int i = tid + r * 256, t = i / (KC / 4), q = i % (KC / 4), k = c * KC + 4 * q;
+      xs[c & 1][t][q] = t < M && k < K ? sv[r] : f32x4{};
+    }
+  };
+  stage_load(0);
+  stage_store(0);
+  f32x4 wv0 = *(const f32x4*)(w0 + min(lane * 4, K - 4)), wv1 = *(const f32x4*)(w1 + min(lane * 4, K - 4));
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    if (c + 1 < nch) stage_load(c + 1);
+    const int k = c * KC + lane * 4;
+    const f32x4 a0 = wv0, a1 = wv1;
+    if (c + 1 < nch) {
+      const int kn = min(k + KC, K - 4);
+      wv0 = *(const f32x4*)(w0 + kn);
+      wv1 = *(const f32x4*)(w1 + kn);
+    }
+    if (k < K) {
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        const f32x4 x = xs[c & 1][t][lane];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float y = fmaf(a0[j], x[j], -cmp0[t]);
+          float u = acc0[t] + y;
+          cmp0[t] = (u - acc0[t]) - y;
+          acc0[t] = u;
+          y = fmaf(a1[j], x[j], -cmp1[t]);
+          u = acc1[t] + y;
+          cmp1[t] = (u - acc1[t]) - y;
+          acc1[t] = u;
+        }
+      }
+    }
+    // the buffer of chunk c + 1 was last read in chunk c - 1, before the
+    // barrier that ended it
+    if (c + 1 < nch) stage_store(c + 1);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    if (t >= M) break;
+    const float v0 = wave_sum(acc0[t] - cmp0[t]), v1 = wave_sum(acc1[t] - cmp1[t]);
+    if (lane == 0) {
+      float* p = ep.out_f32 + (int64_t)t * ep.ldo;
+      if (n0 < N) p[n0] = EPI == EPI_RESID ? p[n0] + v0 : v0;
+      if (n1 < N) p[n1] = EPI == EPI_RESID ? p[n1] + v1 : v1;
+    }
+  }
+}
+
 void launch_gemm_f32(const float* W, const float* X, int N, int M, int K, int epi, const EpiArgs& ep,
                      hipStream_t s) {
   if (M <= 0) return;
   if (M <= 32 && K % 4 == 0) {
-    const dim3 g((N + 3) / 4);
     const bool r = epi == EPI_RESID;
-    if (M <= 1) r ? klaunch(gemv_f32_kernel<EPI_RESID, 1>, g, dim3(256), 0, s, W, X, N, M, K, ep)
-                  : klaunch(gemv_f32_kernel<EPI_F32, 1>, g, dim3(256), 0, s, W, X, N, M, K, ep);
-    else if (M <= 4) r ? klaunch(gemv_f32_kernel<EPI_RESID, 4>, g, dim3(256), 0, s, W, X, N, M, K, ep)
-                       : klaunch(gemv_f32_kernel<EPI_F32, 4>, g, dim3(256), 0, s, W, X, N, M, K, ep);
-    else if (M <= 16) r ? klaunch(gemv_f32_kernel<EPI_RESID, 16>, g, dim3(256), 0, s, W, X, N, M, K, ep)
-                        : klaunch(gemv_f32_kernel<EPI_F32, 16>, g, dim3(256), 0, s, W, X, N, M, K, ep);
-    else r ? klaunch(gemv_f32_kernel<EPI_RESID, 32>, g, dim3(256), 0, s, W, X, N, M, K, ep)
-           : klaunch(gemv_f32_kernel<EPI_F32, 32>, g, dim3(256), 0, s, W, X, N, M, K, ep);
+    if (M <= 1) {
+      const dim3 g((N + 3) / 4);
+      r ? klaunch(gemv_f32_kernel<EPI_RESID, 1>, g, dim3(256), 0, s, W, X, N, M, K, ep)
+        : klaunch(gemv_f32_kernel<EPI_F32, 1>, g, dim3(256), 0, s, W, X, N, M, K, ep);
+      return;
+    }
+    const dim3 g((N + 7) / 8, (M + 7) / 8);
+    r ? klaunch(gemv_f32_lds_kernel<EPI_RESID, 8>, g, dim3(256), 0, s, W, X, N, M, K, ep)
+      : klaunch(gemv_f32_lds_kernel<EPI_F32, 8>, g, dim3(256), 0, s, W, X, N, M, K, ep);
     return;
   }
   dim3 grid((N + 63) / 64, (M + 63) / 64);

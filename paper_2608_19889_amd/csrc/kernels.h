@@ -249,6 +249,48 @@ bool launch_gemv_grouped(const GemvArgs& a, int epi, int n_experts, hipStream_t 
 void launch_embed_ss(const int32_t* tok, const bf16* emb, const bf16* g, float* x, bf16* xg, float* ss_out, int M,
                      int D, int V, hipStream_t s);
 
+// ---- float32 few-token projections (k_gemv_f32.hip): float weights [N][K]
+// row-major (QKV rows in the rotation-pair order, gate/up interleaved in
+// blocks of 16 rows), up to GEMV_F32_MAX_M tokens, the epilogues of
+// GV_ROPE / GV_SILU (normalized operand), GV_RESID, GV_HEAD (normalized)
+struct GemvF32Args {
+  const float* W;
+  int N, K, M;
+  const float* X;       // [M][K]: x * g (normalized operand) or the plain operand
+  const float* ss_in;   // [ss_n][M] partial sums of squares of x, or null
+  int ss_n;
+  float eps;
+  float* out;           // GV_RESID x [M][ldo] (+=) / GV_SILU a [M][ldo] / GV_HEAD logits [M][ldo] or null
+  int ldo;
+  float* xg_out;        // GV_RESID: x * gain_next [M][ldo], or null
+  const float* gain_next;
+  float* ss_out;        // GV_RESID: [gemv_f32_parts(N)][M]
+  float* am_val;        // GV_HEAD: [M][gemv_f32_parts(N)] per-workgroup maxima
+  int32_t* am_idx;
+  const float* bias;    // GV_ROPE: [(H+2KV)hd] in the original head order, or null
+  const float* cos_t;
+  const float* sin_t;
+  float* q_out;         // [M][H][hd]
+  KVView kv;
+  const int32_t* len;   // token t at position len[t] of slot slot[t] (t when null)
+  const int32_t* slot;
+  int H;
+};
+constexpr int GEMV_F32_MAX_M = 16;
+// false (nothing launched) for more than GEMV_F32_MAX_M tokens or a shape or
+// normalization the epilogue does not take
+bool launch_gemv_f32_fused(const GemvF32Args& a, int epi, hipStream_t s);
+int gemv_f32_parts(int N, int epi);  // workgroups of a launch (partials per token)
+// Short-context decode (attention recomputed by every workgroup of the O
+// projection): whether a step of M tokens with contexts up to max_ctx keys
+// qualifies, and the fused attention + residual O projection (a: the
+// GV_RESID projection with K = H * hd; q [M][H][hd]; token t at position
+// a.len[t] of slot a.slot[t]).  false (nothing launched) outside those limits.
+bool attn_o_f32_fits(int M, int H, int KVh, int hd, int max_ctx);
+bool launch_attn_o_f32(const GemvF32Args& a, const float* q, KVView kv, hipStream_t s);
+void launch_embed_ss_f32(const int32_t* tok, const float* emb, const float* g, float* x, float* xg, float* ss_out,
+                         int M, int D, int V, hipStream_t s);
+
 // ---- bias + rotary + KV-cache write (k_rope.hip)
 // qkv rows are sum_s parts[s][t][:] (+ bias): q heads, then k heads, then v heads.
 // Token t belongs to entry e(t) of cu: prefill puts it in slot ent_slot[e] at
