@@ -42,22 +42,19 @@ AXON_DEV int64_t kv_page_of(const KVView& c, int slot, int pos) {
 }
 
 // ============================================================================
-// Prefill (bf16): a workgroup = 4 wavefronts x QB blocks of 32 queries of one
-// head of one sequence (each K / V^T fragment read from LDS feeds QB MFMAs:
-// with one block per wavefront the LDS reads alone would need ~128 B/clk
-// per CU at full MFMA rate); key tiles of 64, K [64][hd] and V^T [hd][64]
-// moved straight from global memory into LDS (global_load_lds_dwordx4: lane L
-// writes 16 bytes at offset 16 L) one tile ahead of the tile being computed,
-// in two LDS buffers; v_mfma_f32_32x32x16_bf16 for both products.  The bank
-// swizzle of a tile (16-byte chunk c of row r stored at c ^ swz(r)) is made by
-// choosing which global chunk each lane loads.  Keys past the sequence load
-// its last key (finite; their scores are masked).
+// Prefill (bf16): a workgroup = 8 wavefronts x 32 queries of one head of one
+// sequence (256 queries: each K / V^T tile moved into LDS feeds 8
+// wavefronts; workgroups of several heads of a GQA group x fewer queries, or
+// of 128 queries, measured slower).  Key tiles of 64, K [64][hd] and V^T
+// [hd][64] moved straight from global memory into LDS (global_load_lds_dwordx4:
+// lane L writes 16 bytes at offset 16 L) two tiles ahead of the tile being
+// computed, in a ring of three; v_mfma_f32_32x32x16_bf16 for both products.
+// The bank swizzle of a tile (16-byte chunk c of row r stored at c ^ swz(r))
+// is made by choosing which global chunk each lane loads.  Keys past the
+// sequence load its last key (finite; their scores are masked).
 // ============================================================================
 constexpr int PK = 64;
-#ifndef AXON_PREFILL_QB
-#define AXON_PREFILL_QB 1
-#endif
-constexpr int PREFILL_QB = AXON_PREFILL_QB;  // 32-query blocks per wavefront
+constexpr int PREFILL_WAVES = 8;
 
 // LDS row rho of a K tile holds key kappa(rho): bits 2 and 3 of the row index
 // swapped.  The S^T = K Q^T accumulator puts rows {8a + 4 hl + 0..3} of a
@@ -81,22 +78,21 @@ AXON_DEV int pswz(int r, int c) {
 // slot ent_slot[e] (e when null) at positions ent_base[e] .. (0 when null):
 // queries attend to keys 0 .. their own position of that slot, the keys
 // before ent_base[e] written by earlier calls (a chunked prefill).
-template <int HD, int QB>
-__global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel(const bf16* __restrict__ q, KVView kv,
-                                                                   bf16* __restrict__ o, int nseq,
-                                                                   const int32_t* __restrict__ cu, int H,
-                                                                   const int32_t* __restrict__ ents,
-                                                                   const int32_t* __restrict__ ent_slot,
-                                                                   const int32_t* __restrict__ ent_base,
-                                                                   float* __restrict__ lse) {
+template <int HD>
+__global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
+    const bf16* __restrict__ q, KVView kv, bf16* __restrict__ o, int nseq, const int32_t* __restrict__ cu, int H,
+    const int32_t* __restrict__ ents, const int32_t* __restrict__ ent_slot, const int32_t* __restrict__ ent_base,
+    float* __restrict__ lse) {
+  constexpr int NW = PREFILL_WAVES;      // wavefronts
   constexpr int KCH = HD / 8;            // 16-byte chunks per K row
   constexpr int VCH = PK / 8;            // chunks per V^T row (8)
   constexpr int KT = PK * KCH;           // chunks per K tile
   constexpr int VT = HD * VCH;           // chunks per V^T tile
   constexpr int BUF = KT + VT;           // chunks per buffer
-  constexpr int WQ = 32 * QB;            // queries per wavefront
-  constexpr int TQ = 4 * WQ;             // queries per workgroup
-  __shared__ bf16x8 lds[2 * BUF];
+  constexpr int TQ = 32 * NW;            // queries per workgroup
+  constexpr int STG = 3;                 // tiles in the LDS ring: two in flight while one is used
+  static_assert(KT % 64 == 0 && VT % 64 == 0, "tiles are whole load instructions");
+  __shared__ bf16x8 lds[STG * BUF];
 
   // (entry, query tile, head) of this workgroup, in an XCD-aware order: the
   // workgroup id mod 8 picks the XCD, and each XCD walks a contiguous range
@@ -105,9 +101,9 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
   // one kv head run together on one XCD and find them in its L2, and the
   // longest tiles start first
   const int group = H / kv.kv_heads;
-  const int G = gridDim.x, ntl = G / H;  // ntl: query tiles over all entries
+  const int Gd = gridDim.x, ntl = Gd / H;  // ntl: query tiles over all entries
   int logical = blockIdx.x;
-  const int full = G / 8 * 8;
+  const int full = Gd / 8 * 8;
   if (logical < full) logical = (logical % 8) * (full / 8) + logical / 8;
   const int hin = logical % group;
   const int rest = logical / group;
@@ -131,64 +127,105 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
   const int KL = base + S;                         // keys of the slot after this call
   const int q0 = tile * TQ;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qw0 = q0 + wave * WQ;  // this wavefront's queries: QB blocks of 32
+  const int qw0 = q0 + wave * 32;  // this wavefront's queries
   const int hl = lane >> 5;
 
   // Q^T fragments (B operand): column = query, k = head-dim (queries past S
   // read the last query; their outputs are not stored)
-  bf16x8 qf[QB][HD / 16];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int myq = qw0 + qb * 32 + (lane & 31);
+  bf16x8 qf[HD / 16];
+  {
+    const int myq = qw0 + (lane & 31);
     const bf16* qp = q + ((int64_t)(tok0 + min(myq, S - 1)) * H + head) * HD + hl * 8;
 #pragma unroll
-    for (int k = 0; k < HD / 16; ++k) qf[qb][k] = *(const bf16x8*)(qp + k * 16);
+    for (int k = 0; k < HD / 16; ++k) qf[k] = *(const bf16x8*)(qp + k * 16);
   }
 
-  // issue the loads of key tile kt into buffer b: thread chunk slots
-  // p = (i*4 + wave)*64 + lane of the K tile, then of the V^T tile
+  // issue the loads of key tile kt into buffer b: instruction i of wavefront
+  // w moves chunk slots (i NW + w) 64 + lane of the K tile, then of the V^T
+  // tile.  A tile wholly inside the slot's keys takes the fast form: the
+  // lane's offset inside a 16-key block is fixed per instruction, and the
+  // four blocks' base addresses are wave-uniform (computed once per tile);
+  // the slot's last tile clamps every key to the last one.
   const bf16* kb = (const bf16*)kv.k;
   const bf16* vb = (const bf16*)kv.v;
+  constexpr int NKI = (KT / 64 + NW - 1) / NW, NVI = (VT / 64 + NW - 1) / NW;
+  int koff[NKI], kgrp[NKI], voff[NVI], vgrp[NVI];
+#pragma unroll
+  for (int i = 0; i < NKI; ++i) {
+    const int p = (i * NW + wave) * 64 + lane;
+    const int r = p / KCH, c = pswz<KCH>(r, p % KCH);
+    koff[i] = c * 128 + (kappa(r) & 15) * 8;
+    kgrp[i] = __builtin_amdgcn_readfirstlane(kappa(r) >> 4);  // one 16-key block per instruction
+  }
+#pragma unroll
+  for (int i = 0; i < NVI; ++i) {
+    const int p = (i * NW + wave) * 64 + lane;
+    const int d = p / VCH, c = pswz<VCH>(d, p % VCH);
+    voff[i] = d * 16 + (c & 1) * 8;
+    vgrp[i] = c >> 1;
+  }
   auto issue = [&](int kt, int b) {
     const int j0 = kt * PK;
+    if (j0 + PK <= KL) {
+      int64_t gb[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        gb[g] = ((kv_page_uniform(kv, seq, j0 + g * 16) * kv.kv_heads + kvh) * kv.ps + (j0 + g * 16) % kv.ps) * HD;
+#pragma unroll
+      for (int i = 0; i < NKI; ++i) {
+        if ((i * NW + wave) * 64 >= KT) break;  // wave-uniform
+        const int g = kgrp[i];
+        const int64_t base = g == 0 ? gb[0] : g == 1 ? gb[1] : g == 2 ? gb[2] : gb[3];
+        __builtin_amdgcn_global_load_lds((const void*)(kb + base + koff[i]),
+                                         (__attribute__((address_space(3))) void*)(lds + b * BUF + (i * NW + wave) * 64),
+                                         16, 0, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < NVI; ++i) {
+        if ((i * NW + wave) * 64 >= VT) break;  // wave-uniform
+        const int g = vgrp[i];
+        const int64_t base = g == 0 ? gb[0] : g == 1 ? gb[1] : g == 2 ? gb[2] : gb[3];
+        __builtin_amdgcn_global_load_lds(
+            (const void*)(vb + base + voff[i]),
+            (__attribute__((address_space(3))) void*)(lds + b * BUF + KT + (i * NW + wave) * 64), 16, 0, 0);
+      }
+      return;
+    }
     int64_t pg[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) pg[g] = kv_page_uniform(kv, seq, min(j0 + g * 16, KL - 1) & ~15);
 #pragma unroll
-    for (int i = 0; i < KT / 256; ++i) {
-      const int p = (i * 4 + wave) * 64 + lane;
+    for (int i = 0; i < NKI; ++i) {
+      if ((i * NW + wave) * 64 >= KT) break;  // wave-uniform
+      const int p = (i * NW + wave) * 64 + lane;
       const int r = p / KCH, c = pswz<KCH>(r, p % KCH);  // pswz is its own inverse
       const int key = min(j0 + kappa(r), KL - 1);         // in [j0, j0 + 64): j0 < KL
       const int64_t page = pg[(key - j0) >> 4];
       const int kp = key % kv.ps;
       const bf16* src = kb + ((page * kv.kv_heads + kvh) * kv.ps + (kp & ~15)) * HD + c * 128 + (kp & 15) * 8;
       __builtin_amdgcn_global_load_lds((const void*)src,
-                                       (__attribute__((address_space(3))) void*)(lds + b * BUF + (i * 4 + wave) * 64),
+                                       (__attribute__((address_space(3))) void*)(lds + b * BUF + (i * NW + wave) * 64),
                                        16, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < VT / 256; ++i) {
-      const int p = (i * 4 + wave) * 64 + lane;
+    for (int i = 0; i < NVI; ++i) {
+      if ((i * NW + wave) * 64 >= VT) break;  // wave-uniform
+      const int p = (i * NW + wave) * 64 + lane;
       const int d = p / VCH, c = pswz<VCH>(d, p % VCH);
       const int key = min(j0 + c * 8, (KL - 1) & ~7);  // 8 keys of one 16-key group, in [j0, j0 + 64)
       const int64_t page = pg[(key - j0) >> 4];
       const int kp = key % kv.ps;
       const bf16* src = vb + ((page * kv.kv_heads + kvh) * kv.ps + (kp & ~15)) * HD + d * 16 + (kp & 15);
       __builtin_amdgcn_global_load_lds(
-          (const void*)src, (__attribute__((address_space(3))) void*)(lds + b * BUF + KT + (i * 4 + wave) * 64), 16,
+          (const void*)src, (__attribute__((address_space(3))) void*)(lds + b * BUF + KT + (i * NW + wave) * 64), 16,
           0, 0);
     }
   };
 
-  f32x16 acc_o[QB][HD / 32];
-  float m_run[QB], l_run[QB];
+  f32x16 acc_o[HD / 32];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-#pragma unroll
-    for (int d = 0; d < HD / 32; ++d) acc_o[qb][d] = f32x16{};
-    m_run[qb] = -INFINITY;
-    l_run[qb] = 0.f;
-  }
+  for (int d = 0; d < HD / 32; ++d) acc_o[d] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;
   const float sc = LOG2E / sqrtf((float)HD);
 
   const int W = kv.window;
@@ -196,43 +233,53 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
   const int ntiles = (kend + PK - 1) / PK;
   // with a window, the first tile holding a key of the workgroup's first query
   const int kt0 = W ? max(0, base + q0 - W + 1) / PK : 0;
-  issue(kt0, kt0 & 1);
+  // this wavefront's load instructions per tile (its waits leave one tile in flight)
+  const int nld = (wave < KT / 64 ? (KT / 64 - wave + NW - 1) / NW : 0) + (wave < VT / 64 ? (VT / 64 - wave + NW - 1) / NW : 0);
+  issue(kt0, kt0 % STG);
+  if (kt0 + 1 < ntiles) issue(kt0 + 1, (kt0 + 1) % STG);
   for (int kt = kt0; kt < ntiles; ++kt) {
-    const int j0 = kt * PK, b = kt & 1;
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();  // tile kt landed for every wavefront; buffer b^1 is free
-    if (kt + 1 < ntiles) issue(kt + 1, b ^ 1);
+    const int j0 = kt * PK, b = kt % STG;
+    // tile kt landed for this wavefront (tile kt + 1 may still be in flight)
+    if (kt + 1 < ntiles) {
+      switch (nld) {  // wave-uniform; the counts the shapes produce
+        case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
+        case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+        case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+        case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+      }
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    __syncthreads();  // tile kt landed for every wavefront; the buffer of tile kt - 1 is free
+    if (kt + 2 < ntiles) issue(kt + 2, (kt + 2) % STG);
     const bf16x8* ks = lds + b * BUF;
     const bf16* vsb = (const bf16*)(ks + KT);
-    if (j0 > base + qw0 + WQ - 1 || qw0 >= S) continue;  // every key of the tile is after this wavefront's queries
-    if (W && j0 + PK - 1 <= base + qw0 - W) continue;    // every key of the tile is before their windows
-    // ---- S^T = K Q^T: each K fragment serves the QB query blocks
-    f32x16 s[QB][2];
+    if (j0 > base + qw0 + 31 || qw0 >= S) continue;  // no key of the tile for this wavefront's queries
+    if (W && j0 + PK - 1 <= base + qw0 - W) continue;         // every key of the tile is before their windows
+    // ---- S^T = K Q^T
+    f32x16 s[2];
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) s[qb][r] = f32x16{};
+      s[r] = f32x16{};
       const int row = r * 32 + (lane & 31);
 #pragma unroll
       for (int k = 0; k < HD / 16; ++k) {
         const bf16x8 kf = ks[row * KCH + pswz<KCH>(row, k * 2 + hl)];
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-          s[qb][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][k], s[qb][r], 0, 0, 0);
+        s[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], s[r], 0, 0, 0);
       }
     }
     // ---- online softmax (lane = query column), on unscaled scores: the
     //      1/sqrt(hd) scale (log2 e folded in) enters the exponent's FMA.
     //      Masking only where the tile crosses the diagonal or the sequence
-    //      end.  The reference maximum m_run[qb] is raised only when a score
+    //      end.  The reference maximum m_run is raised only when a score
     //      exceeds it by more than 8 (in log2 units): probabilities stay <= 2^8
     //      and the accumulator is rescaled rarely, not every tile (the sum and
     //      the accumulator always share the reference, so the result is exact).
-    const bool masked = j0 + PK - 1 > base + qw0 || j0 + PK > KL || (W && j0 + W <= base + qw0 + WQ - 1);
-    bf16x8 pb[QB][2][2];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      const int myq = qw0 + qb * 32 + (lane & 31);
+    const bool masked = j0 + PK - 1 > base + qw0 || j0 + PK > KL || (W && j0 + W <= base + qw0 + 31);
+    bf16x8 pb[2][2];
+    {
+      const int myq = qw0 + (lane & 31);
       float mloc = -INFINITY;
       if (masked) {
 #pragma unroll
@@ -240,40 +287,40 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const int key = j0 + r * 32 + (i / 8) * 16 + hl * 8 + ((i / 4) & 1) * 4 + (i % 4);  // kappa of the row
-            const float v = (key <= base + myq && key < KL && (!W || key > base + myq - W)) ? s[qb][r][i] : -INFINITY;
-            s[qb][r][i] = v;
+            const float v = (key <= base + myq && key < KL && (!W || key > base + myq - W)) ? s[r][i] : -INFINITY;
+            s[r][i] = v;
             mloc = fmaxf(mloc, v);
           }
       } else {
 #pragma unroll
         for (int r = 0; r < 2; ++r)
 #pragma unroll
-          for (int i = 0; i < 16; ++i) mloc = fmaxf(mloc, s[qb][r][i]);
+          for (int i = 0; i < 16; ++i) mloc = fmaxf(mloc, s[r][i]);
       }
       mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * sc;  // scaled maximum of the tile
       // raise the reference when the tile's maximum exceeds it by > 8
-      const bool raise = mloc > m_run[qb] + 8.f;
+      const bool raise = mloc > m_run + 8.f;
       if (__builtin_amdgcn_ballot_w64(raise) != 0) {  // wave-uniform: rare after the first tiles
-        const float m_new = raise ? mloc : m_run[qb];
-        const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run[qb] - m_new);
-        m_run[qb] = m_new;
-        l_run[qb] *= alpha;
+        const float m_new = raise ? mloc : m_run;
+        const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
 #pragma unroll
-        for (int d = 0; d < HD / 32; ++d) acc_o[qb][d] *= alpha;
+        for (int d = 0; d < HD / 32; ++d) acc_o[d] *= alpha;
       }
-      const float m_ref = m_run[qb] == -INFINITY ? 0.f : m_run[qb];
+      const float m_ref = m_run == -INFINITY ? 0.f : m_run;
 #pragma unroll
       for (int r = 0; r < 2; ++r)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(s[qb][r][i], sc, -m_ref));
-          l_run[qb] += p;
-          pb[qb][r][i / 8][i % 8] = (bf16)p;
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[r][i], sc, -m_ref));
+          l_run += p;
+          pb[r][i / 8][i % 8] = (bf16)p;
         }
     }
     // ---- O^T += V^T P^T; the k index of block (r, h) in half-wavefront hl
     //      covers keys r*32 + h*16 + hl*8 + 0..7 (logical chunk r*4 + 2h + hl
-    //      of the V^T row); each V fragment serves the QB query blocks
+    //      of the V^T row)
 #pragma unroll
     for (int d = 0; d < HD / 32; ++d) {
       const int dd = d * 32 + (lane & 31);
@@ -283,32 +330,26 @@ __global__ void __launch_bounds__(256, QB == 1 ? 2 : 1) attn_prefill_bf16_kernel
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const bf16x8 va = vr[pswz<VCH>(dd, r * 4 + h * 2 + hl)];
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb)
-            acc_o[qb][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[qb][r][h], acc_o[qb][d], 0, 0, 0);
+          acc_o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[r][h], acc_o[d], 0, 0, 0);
         }
     }
   }
+  const int myq = qw0 + (lane & 31);
+  if (myq >= S) return;
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = 1.f / l_tot;
+  // log2 of sum_k exp2(score_k * sc): what the backward pass recomputes its
+  // probabilities from
+  if (lse && hl == 0) lse[(int64_t)(tok0 + myq) * H + head] = (m_run == -INFINITY ? 0.f : m_run) + __log2f(l_tot);
+  bf16* op = o + ((int64_t)(tok0 + myq) * H + head) * HD;
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int myq = qw0 + qb * 32 + (lane & 31);
-    if (myq >= S) continue;
-    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32, 64);
-    const float inv = 1.f / l_tot;
-    // log2 of sum_k exp2(score_k * sc): what the backward pass recomputes
-    // its probabilities from
-    if (lse && hl == 0) lse[(int64_t)(tok0 + myq) * H + head] = (m_run[qb] == -INFINITY ? 0.f : m_run[qb]) + __log2f(l_tot);
-    bf16* op = o + ((int64_t)(tok0 + myq) * H + head) * HD;
+  for (int d = 0; d < HD / 32; ++d)
 #pragma unroll
-    for (int d = 0; d < HD / 32; ++d)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int dd = d * 32 + g * 8 + hl * 4;
-        *(bf16x4*)(op + dd) =
-            bf16x4{(bf16)(acc_o[qb][d][g * 4 + 0] * inv), (bf16)(acc_o[qb][d][g * 4 + 1] * inv),
-                   (bf16)(acc_o[qb][d][g * 4 + 2] * inv), (bf16)(acc_o[qb][d][g * 4 + 3] * inv)};
-      }
-  }
+    for (int g = 0; g < 4; ++g) {
+      const int dd = d * 32 + g * 8 + hl * 4;
+      *(bf16x4*)(op + dd) = bf16x4{(bf16)(acc_o[d][g * 4 + 0] * inv), (bf16)(acc_o[d][g * 4 + 1] * inv),
+                                   (bf16)(acc_o[d][g * 4 + 2] * inv), (bf16)(acc_o[d][g * 4 + 3] * inv)};
+    }
 }
 
 // ============================================================================
@@ -795,7 +836,7 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
     else
       attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, kv, o, T_tokens, nseq, cu, nullptr, H, ent_slot, ent_base);
   } else {
-    constexpr int QB = PREFILL_QB, TQ = 4 * 32 * QB;
+    constexpr int TQ = 32 * PREFILL_WAVES;
     int tiles = 0;
     for (int i = 0; i < nseq; ++i) {
       const int e = h_ents ? h_ents[i] : i;
@@ -803,9 +844,9 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
     }
     const dim3 grid(tiles * H);  // the kernel maps the linear id to (tile, head)
     if (kv.hd == 64)
-      attn_prefill_bf16_kernel<64, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base, lse);
+      attn_prefill_bf16_kernel<64><<<grid, 64 * PREFILL_WAVES, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base, lse);
     else
-      attn_prefill_bf16_kernel<128, QB><<<grid, 256, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base, lse);
+      attn_prefill_bf16_kernel<128><<<grid, 64 * PREFILL_WAVES, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base, lse);
   }
 }
 
