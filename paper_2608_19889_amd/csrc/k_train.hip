@@ -307,20 +307,60 @@ AXON_DEV int64_t row_frag_off(int64_t g, int64_t col, int d, int hd, int64_t W) 
 }
 
 // the layer's K / V rows from the cache into kr / vr (row e*SP + position)
-// and K^T into kt; grid (token, kv head), one thread per head dimension
-__global__ void __launch_bounds__(128) attn_bwd_pack_kernel(KVView kv, const int32_t* __restrict__ cu, int nseq,
+// and K^T into kt.  Workgroup = 16 positions p0 .. p0+15 of one sequence
+// (p0 % 16 == 0, blockIdx.x counts the sequences' 16-position blocks in
+// order) x one kv head: the cache's K block (positions x 8-dim chunks) and
+// V^T block (dims x 16 positions) are staged in LDS, then every output leaves
+// in 16-byte stores: 8 dims of one position (kr, vr) or 8 positions of one
+// dim (kt, in the kap order of its fragment).  Positions past the sequence
+// end are written as zeros, which is what the zero-filled padding holds.
+template <int HD>
+__global__ void __launch_bounds__(256) attn_bwd_pack_kernel(KVView kv, const int32_t* __restrict__ cu, int nseq,
                                                             int SP, int64_t W, bf16* __restrict__ kr,
                                                             bf16* __restrict__ vr, bf16* __restrict__ kt) {
-  const int t = blockIdx.x, h = blockIdx.y, d = threadIdx.x, hd = kv.hd, KVh = kv.kv_heads;
-  if (d >= hd) return;
-  const int e = seq_of_token(cu, nseq, t);
-  const int p = t - cu[e];
-  const int64_t col = (int64_t)e * SP + p;
-  (void)KVh;
-  const bf16 kval = ((const bf16*)kv.k)[k_el(kv, e, h, p, d)];
-  kr[row_frag_off(h, col, d, hd, W)] = kval;
-  kt[frag_off((int64_t)h * hd + d, col, W)] = kval;
-  vr[row_frag_off(h, col, d, hd, W)] = ((const bf16*)kv.v)[v_el(kv, e, h, p, d)];
+  __shared__ bf16 ks[16][HD + 8];  // K rows (padded: the kt gather reads a column)
+  __shared__ bf16 vs[HD][16 + 8];  // V^T rows
+  const int h = blockIdx.y, tid = threadIdx.x;
+  int e = 0, blk = blockIdx.x;
+  for (; e < nseq - 1; ++e) {
+    const int nb = (cu[e + 1] - cu[e] + 15) / 16;
+    if (blk < nb) break;
+    blk -= nb;
+  }
+  const int p0 = blk * 16, len = cu[e + 1] - cu[e];
+  const bf16 zero = (bf16)0.f;
+  // K: thread -> (position, 8-dim chunk); V^T: thread -> (dim, 8 positions)
+  for (int i = tid; i < 16 * (HD / 8); i += 256) {
+    const int pp = i / (HD / 8), d0 = (i % (HD / 8)) * 8, p = p0 + pp;
+    bf16x8 v = {zero, zero, zero, zero, zero, zero, zero, zero};
+    if (p < len) v = *(const bf16x8*)((const bf16*)kv.k + k_el(kv, e, h, p, d0));
+    *(bf16x8*)&ks[pp][d0] = v;
+  }
+  for (int i = tid; i < HD * 2; i += 256) {
+    const int d = i / 2, half = i % 2;
+    // the block's V^T row of dim d holds positions p0 .. p0+15 contiguously
+    const bf16x8 v = *(const bf16x8*)((const bf16*)kv.v + v_el(kv, e, h, min(p0, len - 1) & ~15, d) + half * 8);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) vs[d][half * 8 + j] = p0 + half * 8 + j < len ? v[j] : zero;
+  }
+  __syncthreads();
+  const int64_t col0 = (int64_t)e * SP + p0;
+  for (int i = tid; i < 16 * (HD / 8); i += 256) {
+    const int pp = i / (HD / 8), d0 = (i % (HD / 8)) * 8;
+    bf16x8 vv;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) vv[j] = vs[d0 + j][pp];
+    *(bf16x8*)(kr + row_frag_off(h, col0 + pp, d0, HD, W)) = *(const bf16x8*)&ks[pp][d0];
+    *(bf16x8*)(vr + row_frag_off(h, col0 + pp, d0, HD, W)) = vv;
+  }
+  // kt: dim d, half hl of the 16 positions (kap(hl, j) = (j/4)*8 + 4 hl + j%4)
+  for (int i = tid; i < HD * 2; i += 256) {
+    const int d = i / 2, hl = i % 2;
+    bf16x8 v;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = ks[(j / 4) * 8 + hl * 4 + j % 4][d];
+    *(bf16x8*)(kt + frag_off((int64_t)h * HD + d, col0 + hl * 4, W)) = v;
+  }
 }
 
 AXON_DEV int kap(int hl, int j) { return (j >> 2) * 8 + hl * 4 + (j & 3); }
@@ -655,7 +695,10 @@ bool launch_attn_bwd(const bf16* q, KVView kv, const bf16* o, const bf16* dob, c
   float* lsep = statp;
   float* dsump = statp + (int64_t)H * W;
   attn_bwd_d_kernel<<<(T * H + 255) / 256, 256, 0, s>>>(dob, o, T * H, hd, dsum, lse, cu, nseq, H, SP, W, lsep, dsump);
-  attn_bwd_pack_kernel<<<dim3(T, KVh), 128, 0, s>>>(kv, cu, nseq, SP, W, kr, vr, kt);
+  int blocks16 = 0;
+  for (int e = 0; e < nseq; ++e) blocks16 += (h_cu[e + 1] - h_cu[e] + 15) / 16;
+  if (hd == 64) attn_bwd_pack_kernel<64><<<dim3(blocks16, KVh), 256, 0, s>>>(kv, cu, nseq, SP, W, kr, vr, kt);
+  else attn_bwd_pack_kernel<128><<<dim3(blocks16, KVh), 256, 0, s>>>(kv, cu, nseq, SP, W, kr, vr, kt);
   transpose_tile_kernel<<<dim3((T + 63) / 64, (H * hd + 63) / 64), 256, 0, s>>>(q, (int64_t)H * hd, T, T, H * hd, qt,
                                                                                  W, cu, nseq, SP, true);
   transpose_tile_kernel<<<dim3((T + 63) / 64, (H * hd + 63) / 64), 256, 0, s>>>(dob, (int64_t)H * hd, T, T, H * hd,
