@@ -820,7 +820,11 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
   const int32_t* slot = plan ? plan->d_dslot : nullptr;
   const float eps = m->cfg.rms_eps;
   bf16* xg = ws.xg;
-  launch_embed_ss(d_tokens, (const bf16*)m->embed, (const bf16*)m->layers[0].gin, ws.x, xg, ws.ss, B, D, V, s);
+  // up to 16 tokens of a dense model: the token operands of every projection
+  // (xg, the attention output, the gated activation) pass in the tile order
+  // of the one-block fused kernel, written so by their producers
+  const int xt = B <= XT_ROWS && !m->moe_model() ? 1 : 0;
+  launch_embed_ss(d_tokens, (const bf16*)m->embed, (const bf16*)m->layers[0].gin, ws.x, xg, ws.ss, B, D, V, s, xt);
   int ss_n = 1;
   auto gemv = [&](GemvArgs& a, int epi) { gemv_step(m, a, epi, s); };
   auto ss_count = [&](int K) {
@@ -836,17 +840,20 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
     qa.X = xg; qa.ss_in = ws.ss; qa.ss_n = ss_n; qa.eps = eps;
     qa.bias = (const bf16*)w.bqkv; qa.cos_t = m->rope_cos; qa.sin_t = m->rope_sin; qa.q_out = ws.q;
     qa.kv = kv; qa.len = pos; qa.slot = slot; qa.H = H; qa.part = ws.gemv_part;
+    qa.x_tiled = xt;
     gemv(qa, GV_ROPE);
     int ctx_sum = 0;
     if (plan) ctx_sum = plan->dctx;
     else for (int b = 0; b < B; ++b) ctx_sum += m->keys_read(m->h_len[b] + 1);
     m->timed(2, H, B, ctx_sum, s, [&] {
-      launch_attn_decode<bf16>(ws.q, kv, ws.o, ws.attn_part, ws.attn_cnt, B, H, pos, m->cfg.max_seq, s, nullptr, slot);
+      launch_attn_decode<bf16>(ws.q, kv, ws.o, ws.attn_part, ws.attn_cnt, B, H, pos, m->cfg.max_seq, s, nullptr, slot,
+                               xt);
     });
     GemvArgs oa{};
     oa.W = (const bf16*)w.wo; oa.N = D; oa.K = H * hd; oa.M = B; oa.X = ws.o;
     oa.out_f32 = ws.x; oa.ldo = D; oa.ss_out = ws.ss; oa.xg_out = xg; oa.gain_next = (const bf16*)w.gpost;
     oa.part = ws.gemv_part;
+    oa.x_tiled = oa.out_tiled = xt;
     gemv(oa, GV_RESID);
     ss_n = ss_count(H * hd);
     const bf16* gnext = (const bf16*)(last ? m->gfinal : m->layers[l + 1].gin);
@@ -865,6 +872,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
       ga.W = (const bf16*)w.wgu; ga.N = 2 * Id; ga.K = D; ga.M = B;
       ga.X = xg; ga.ss_in = ws.ss; ga.ss_n = ss_n; ga.eps = eps;
       ga.out_t = ws.a; ga.ldo = Id; ga.part = ws.gemv_part;
+      ga.x_tiled = ga.out_tiled = xt;
       gemv(ga, GV_SILU);
     }
     if (w.moe) {
@@ -878,6 +886,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
       da.W = (const bf16*)w.wd; da.N = D; da.K = Id; da.M = B; da.X = ws.a;
       da.out_f32 = ws.x; da.ldo = D; da.ss_out = ws.ss; da.xg_out = xg; da.part = ws.gemv_part;
       da.gain_next = gnext;
+      da.x_tiled = da.out_tiled = xt;
       gemv(da, GV_RESID);
       ss_n = ss_count(Id);
     }
@@ -886,6 +895,7 @@ void enqueue_decode_bf16(axon_model* m, int B, const int32_t* d_tokens, float* d
   ha.W = (const bf16*)m->lm_head; ha.N = V; ha.K = D; ha.M = B;
   ha.X = xg; ha.ss_in = ws.ss; ha.ss_n = ss_n; ha.eps = eps;
   ha.out_f32 = d_logits; ha.ldo = V; ha.am_val = ws.am_val; ha.am_idx = ws.am_idx;
+  ha.x_tiled = xt;
   gemv(ha, GV_HEAD);
   const int hr = gemv_rows(V, D, B, GV_HEAD);
   launch_argmax_final(ws.am_val, ws.am_idx, (V + hr - 1) / hr, B, d_next, plan ? nullptr : m->d_len, s);
@@ -1383,9 +1393,11 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     TRY(dev_alloc(m, &m->h, tmax * D * esz));
     if (!m->bf) TRY(dev_alloc(m, (void**)&m->qkv, tmax * nq * 4));  // bf16: RoPE is the QKV GEMM's epilogue
     TRY(dev_alloc(m, &m->q, tmax * H * hd * esz));
-    TRY(dev_alloc(m, &m->o, tmax * H * hd * esz));
+    // o, a and xg hold at least the 16 token rows of the tile order
+    const int64_t trows = std::max<int64_t>(tmax, XT_ROWS);
+    TRY(dev_alloc(m, &m->o, trows * H * hd * esz));
     const int64_t Ishared = (int64_t)c.n_shared_experts * c.moe_intermediate;
-    TRY(dev_alloc(m, &m->a, tmax * std::max<int64_t>(I, Ishared) * esz));
+    TRY(dev_alloc(m, &m->a, trows * std::max<int64_t>(I, Ishared) * esz));
     if (m->moe_model()) {
       const int64_t E = c.n_experts, k = c.top_k;
       TRY(dev_alloc(m, (void**)&m->moe_logits, tmax * m->moe_ep() * 4));
@@ -1430,7 +1442,7 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
       }
     }
     TRY(dev_alloc(m, (void**)&m->ss, (int64_t)std::max<int64_t>(D / 8, 1) * c.max_batch * 4));
-    TRY(dev_alloc(m, &m->xg, (int64_t)c.max_batch * D * esz));
+    TRY(dev_alloc(m, &m->xg, (int64_t)std::max(c.max_batch, XT_ROWS) * D * esz));
     const int64_t nam = (V + 7) / 8;  // argmax partials per token (8-row float32 head tiles)
     TRY(dev_alloc(m, (void**)&m->am_val, nam * c.max_batch * 4));
     TRY(dev_alloc(m, (void**)&m->am_idx, nam * c.max_batch * 4));
@@ -1601,12 +1613,13 @@ size_t decode_ws_layout(const axon_model* m, int B, char* base, DecodeWs* ws) {
   };
   DecodeWs w{};
   w.attn_cnt = (int32_t*)take((int64_t)B * m->KVh() * 4);  // first, cleared by every call
+  const int64_t trows = std::max(B, XT_ROWS);  // the tile order's 16 token rows
   w.x = (float*)take(B * D * 4);
-  w.xg = (bf16*)take(B * D * 2);
+  w.xg = (bf16*)take(trows * D * 2);
   w.ss = (float*)take(std::max<int64_t>(D / 8, 1) * B * 4);
   w.q = (bf16*)take(B * H * hd * 2);
-  w.o = (bf16*)take(B * H * hd * 2);
-  w.a = (bf16*)take(B * I * 2);
+  w.o = (bf16*)take(trows * H * hd * 2);
+  w.a = (bf16*)take(trows * I * 2);
   w.attn_part = (float*)take((int64_t)B * plan_decode_splits(B, m->KVh(), m->cfg.max_seq) * H * (hd + 2) * 4);
   const int64_t wsf = std::max({gemv_workspace_floats(m->nqkv(), (int)D, B, GV_ROPE),
                                 gemv_workspace_floats((int)D, (int)(H * hd), B, GV_RESID),

@@ -107,6 +107,15 @@ AXON_DEV int64_t v_el(const KVView& c, int slot, int kvh, int pos, int d) {
 // (r, s) = row r of the block, k values 8s..8s+7 of the tile, at position
 // r + 16 s.  A wavefront's fragment load is one contiguous 1 KB read, and a
 // row block is one contiguous stream along k.
+// Token operand of the few-token projections in tile order: element (t, k)
+// of a [16][K] bf16 operand (t < 16, K a multiple of 32) sits where the B
+// fragment of v_mfma_f32_16x16x32_bf16 for k-step k / 32 wants it, so a
+// wavefront's fragment is one contiguous 1 KB read (lane L = 16 ((k / 8) % 4)
+// + t holds k values 8 (L / 16) .. +7 of token t).  Rows t >= the token count
+// are neither written nor read (their lanes read token count - 1).
+AXON_DEV int64_t xt_off(int t, int64_t k) { return (k >> 5) * 512 + ((((k >> 3) & 3) << 4) + t) * 8 + (k & 7); }
+constexpr int XT_ROWS = 16;  // tokens of the tile order (one B fragment column block)
+
 // Element offset of W[n][8c .. 8c+7] (c = k-chunk index, k = 8c):
 AXON_DEV int64_t wt_chunk(int64_t n, int c, int K) {
   return (((n >> 4) * (K >> 5) + (c >> 2)) * 64 + (n & 15) + 16 * (c & 3)) * 8;

@@ -373,7 +373,7 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
                                                                     int32_t* __restrict__ cnt, int H,
                                                                     const int32_t* __restrict__ len,
                                                                     int split_len, const int32_t* __restrict__ rows,
-                                                                    const int32_t* __restrict__ slots) {
+                                                                    const int32_t* __restrict__ slots, bool o_tiled) {
   extern __shared__ float dyn[];
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int row = rows ? rows[b] : b, slot = slots ? slots[b] : b;
@@ -539,7 +539,7 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
     }
     const int h = kvh * group + c;
     if (nsplit == 1) {
-      o[((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
+      o[o_tiled ? xt_off(row, h * HD + d) : ((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
     } else {
       // system-scope stores: written through to memory, so the split that
       // merges (on any XCD) reads them without an L2 write-back
@@ -603,7 +603,7 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
           O += f * ov[u];
         }
     }
-    o[((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
+    o[o_tiled ? xt_off(row, h * HD + d) : ((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
   }
 }
 
@@ -870,7 +870,7 @@ int plan_decode_splits(int B, int kv_heads, int max_ctx) {
 template <int HD, int NW>
 static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int32_t* cnt, int B, int H,
                           const int32_t* len, int nsplit, int split_len, hipStream_t s, const int32_t* rows,
-                          const int32_t* slots) {
+                          const int32_t* slots, bool o_tiled) {
   const int group = H / kv.kv_heads;
   const size_t lds = (size_t)(2 * NW * 16 + NW * group * HD) * sizeof(float);
   const dim3 grid(nsplit, kv.kv_heads, B);
@@ -880,15 +880,15 @@ static void decode_launch(const bf16* q, KVView kv, bf16* o, float* part, int32_
   constexpr int NBUF = 1;
   if (kv.bt)
     attn_decode_bf16_kernel<HD, NW, true, NBUF>
-        <<<grid, NW * 64, lds, s>>>(q, kv, o, part, cnt, H, len, split_len, rows, slots);
+        <<<grid, NW * 64, lds, s>>>(q, kv, o, part, cnt, H, len, split_len, rows, slots, o_tiled);
   else
     attn_decode_bf16_kernel<HD, NW, false, NBUF>
-        <<<grid, NW * 64, lds, s>>>(q, kv, o, part, cnt, H, len, split_len, rows, slots);
+        <<<grid, NW * 64, lds, s>>>(q, kv, o, part, cnt, H, len, split_len, rows, slots, o_tiled);
 }
 
 template <typename T>
 void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* cnt, int B, int H, const int32_t* len,
-                        int max_ctx, hipStream_t s, const int32_t* rows, const int32_t* slots) {
+                        int max_ctx, hipStream_t s, const int32_t* rows, const int32_t* slots, bool o_tiled) {
   if (B <= 0) return;
   if constexpr (sizeof(T) == 4) {
     // the float32 path takes rows / slots through launch_attn_prefill
@@ -905,8 +905,10 @@ void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* cnt, 
     if (kv.window) max_ctx = std::min(max_ctx, kv.window + 31);  // keys from the window's 32-key chunk
     const int nsplit = plan_decode_splits(B, kv.kv_heads, max_ctx);
     const int split_len = ((max_ctx + nsplit - 1) / nsplit + 63) / 64 * 64;
-    if (kv.hd == 64) decode_launch<64, DECODE_WAVES>(q, kv, o, part, cnt, B, H, len, nsplit, split_len, s, rows, slots);
-    else decode_launch<128, DECODE_WAVES>(q, kv, o, part, cnt, B, H, len, nsplit, split_len, s, rows, slots);
+    if (kv.hd == 64)
+      decode_launch<64, DECODE_WAVES>(q, kv, o, part, cnt, B, H, len, nsplit, split_len, s, rows, slots, o_tiled);
+    else
+      decode_launch<128, DECODE_WAVES>(q, kv, o, part, cnt, B, H, len, nsplit, split_len, s, rows, slots, o_tiled);
   }
 }
 
@@ -917,8 +919,8 @@ template void launch_attn_prefill<bf16>(const bf16*, KVView, bf16*, int, int, co
                                         hipStream_t, const int32_t*, const int32_t*, const int32_t*, const int32_t*,
                                         float*);
 template void launch_attn_decode<float>(const float*, KVView, float*, float*, int32_t*, int, int, const int32_t*,
-                                        int, hipStream_t, const int32_t*, const int32_t*);
+                                        int, hipStream_t, const int32_t*, const int32_t*, bool);
 template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int32_t*, int, int, const int32_t*, int,
-                                       hipStream_t, const int32_t*, const int32_t*);
+                                       hipStream_t, const int32_t*, const int32_t*, bool);
 
 }  // namespace axon

@@ -94,7 +94,8 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
         *p = v;
         sq = v * v;
         if (a.xg_out)
-          a.xg_out[(int64_t)col * a.ldo + n] = (bf16)(v * (PRE ? bf16_bits(pre.g) : (float)a.gain_next[n]));
+          a.xg_out[a.out_tiled ? xt_off(col, n) : (int64_t)col * a.ldo + n] =
+              (bf16)(v * (PRE ? bf16_bits(pre.g) : (float)a.gain_next[n]));
       }
       s_aux(row, col) = sq;
     }
@@ -108,7 +109,8 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
       const int blk = fl / 16, f = fl % 16;
       if (n0 + blk * 32 >= a.N) continue;  // N is a multiple of 32 (16 gate + 16 up rows)
       const float g = total(blk * 32 + f, col), u = total(blk * 32 + 16 + f, col);
-      a.out_t[(int64_t)col * a.ldo + n0 / 2 + fl] = (bf16)(silu_g(g) * u);
+      const int fo = n0 / 2 + fl;
+      a.out_t[a.out_tiled ? xt_off(col, fo) : (int64_t)col * a.ldo + fo] = (bf16)(silu_g(g) * u);
     }
   } else if constexpr (EPI == GV_GELU) {
     for (int it = tid; it < ROWS * M; it += NT) {
@@ -189,8 +191,10 @@ AXON_DEV void gv_epilogue(const GemvArgs& a, int n0, int tid, float* aux, int wg
   }
 }
 
-template <int ROWS, int KS, int NB, bool NORM, int EPI, int U = GV_U>
+// XT: the token operand is in tile order (xt_off; one token block)
+template <int ROWS, int KS, int NB, bool NORM, int EPI, int U = GV_U, bool XT = false>
 __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
+  static_assert(!XT || NB == 1, "the tile order holds one block of 16 tokens");
   constexpr int RB = ROWS < 16 ? 1 : ROWS / 16;  // 16-row MFMA blocks (an 8-row tile leaves 8 rows idle)
   constexpr int COLS = NB * 16;
   constexpr int NT = KS * 64;
@@ -225,9 +229,16 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
     wrow[r] = a.W + wt_chunk(min(n, a.N - 1), lane >> 4, K);
   }
   auto woff = [](int k) -> int64_t { return (int64_t)(k >> 5) * 512; };
+  // token fragments: lane (r16, lane / 16) reads 16 bytes of token r16
+  // (tokens past M-1 read token M-1: no bytes beyond the tokens' own), from
+  // row r16 (row-major) or, in tile order, from the k-step's 1 KB at 16 k
+  // (xt_off)
   const bf16* xrow[NB];
 #pragma unroll
-  for (int c = 0; c < NB; ++c) xrow[c] = a.X + (int64_t)min(c * 16 + r16, M - 1) * K + (lane >> 4) * 8;
+  for (int c = 0; c < NB; ++c)
+    xrow[c] = XT ? a.X + ((lane >> 4) * 16 + min(r16, M - 1)) * 8
+                 : a.X + (int64_t)min(c * 16 + r16, M - 1) * K + (lane >> 4) * 8;
+  auto xoff = [](int k) -> int64_t { return XT ? (int64_t)k * 16 : (int64_t)k; };
 
   // sums of squares of the normalized rows: the first SSR partials of this
   // thread are loaded into registers now (index clamped, excluded in the sum)
@@ -268,7 +279,7 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
 #pragma unroll
       for (int r = 0; r < RB; ++r) wa[u][r] = *(const bf16x8*)(wrow[r] + woff(k + u * 32));
 #pragma unroll
-      for (int c = 0; c < NB; ++c) xb[u][c] = *(const bf16x8*)(xrow[c] + k + u * 32);
+      for (int c = 0; c < NB; ++c) xb[u][c] = *(const bf16x8*)(xrow[c] + xoff(k + u * 32));
     }
   };
   auto mfma_stage = [&](const bf16x8 (&wv)[U][RB], const bf16x8 (&xv)[U][NB]) {
@@ -334,7 +345,7 @@ __global__ void __launch_bounds__(KS * 64) gemv_fused_kernel(GemvArgs a) {
 #pragma unroll
     for (int r = 0; r < RB; ++r) w1[r] = *(const bf16x8*)(wrow[r] + woff(k));
 #pragma unroll
-    for (int c = 0; c < NB; ++c) x1[c] = *(const bf16x8*)(xrow[c] + k);
+    for (int c = 0; c < NB; ++c) x1[c] = *(const bf16x8*)(xrow[c] + xoff(k));
 #pragma unroll
     for (int r = 0; r < RB; ++r)
 #pragma unroll
@@ -767,7 +778,7 @@ __global__ void __launch_bounds__(1024) argmax_final_kernel(const float* __restr
 __global__ void __launch_bounds__(256) embed_ss_kernel(const int32_t* __restrict__ tok, const bf16* __restrict__ emb,
                                                        const bf16* __restrict__ g, float* __restrict__ x,
                                                        bf16* __restrict__ xg, float* __restrict__ ss_out, int D,
-                                                       int V) {
+                                                       int V, bool xg_tiled) {
   __shared__ float red[16];
   const int t = blockIdx.x;
   const int id = min(max(tok[t], 0), V - 1);
@@ -788,7 +799,7 @@ __global__ void __launch_bounds__(256) embed_ss_kernel(const int32_t* __restrict
     bf16x8 o;
 #pragma unroll
     for (int j = 0; j < 8; ++j) o[j] = (bf16)((float)v[j] * (float)gv[j]);
-    *(bf16x8*)(xg + (int64_t)t * D + i) = o;
+    *(bf16x8*)(xg + (xg_tiled ? xt_off(t, i) : (int64_t)t * D + i)) = o;  // i % 8 == 0: 16 contiguous bytes
   }
   ss = block_sum(ss, red);
   if (threadIdx.x == 0) ss_out[t] = ss;
@@ -871,6 +882,13 @@ int64_t gemv_workspace_floats(int N, int K, int M, int epi) {
 
 template <int ROWS, int KS, int U, int NB, bool NORM, int EPI>
 static bool gv(const GemvArgs& a, hipStream_t s) {
+  if constexpr (NB == 1) {
+    if (a.x_tiled) {
+      klaunch(gemv_fused_kernel<ROWS, KS, NB, NORM, EPI, U, true>, dim3((a.N + ROWS - 1) / ROWS), dim3(KS * 64), 0, s,
+              a);
+      return true;
+    }
+  }
   klaunch(gemv_fused_kernel<ROWS, KS, NB, NORM, EPI, U>, dim3((a.N + ROWS - 1) / ROWS), dim3(KS * 64), 0, s, a);
   return true;
 }
@@ -948,6 +966,9 @@ bool launch_gemv_fused(const GemvArgs& a, int epi, hipStream_t s) {
   const GvShape sh = gemv_shape(a.N, a.K, a.M, epi);
   const int nb = (a.M + 15) / 16;
   const bool norm = a.ss_in != nullptr;
+  // the tile order serves the unsplit one-block kernel only
+  if ((a.x_tiled || a.out_tiled) && (a.M > XT_ROWS || sh.wide || sh.ksplit > 1 || epi == GV_F32)) return false;
+  if (a.out_tiled && epi != GV_RESID && epi != GV_SILU) return false;
   if (sh.ksplit > 1) {
     if (epi == GV_RESID) return !norm && gv_split_nb<GV_RESID, false>(a, sh, nb, s);
     if (epi == GV_ROPE) return norm ? gv_split_nb<GV_ROPE, true>(a, sh, nb, s) : gv_split_nb<GV_ROPE, false>(a, sh, nb, s);
@@ -1005,9 +1026,9 @@ void launch_argmax_final(const float* val, const int32_t* idx, int nparts, int M
 }
 
 void launch_embed_ss(const int32_t* tok, const bf16* emb, const bf16* g, float* x, bf16* xg, float* ss_out, int M,
-                     int D, int V, hipStream_t s) {
+                     int D, int V, hipStream_t s, bool xg_tiled) {
   if (M <= 0) return;
-  embed_ss_kernel<<<M, 256, 0, s>>>(tok, emb, g, x, xg, ss_out, D, V);
+  embed_ss_kernel<<<M, 256, 0, s>>>(tok, emb, g, x, xg, ss_out, D, V, xg_tiled);
 }
 
 }  // namespace axon

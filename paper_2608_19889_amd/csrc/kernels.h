@@ -223,6 +223,11 @@ struct GemvArgs {
   const int32_t* g_off;
   const int32_t* g_xrow;
   int64_t g_wstride;
+  // tile order (xt_off) of the token operands, up to 16 tokens, unsplit
+  // fused projections only: x_tiled -- X is stored in it; out_tiled -- the
+  // epilogue writes xg_out (GV_RESID) or out_t (GV_SILU) in it
+  int x_tiled;
+  int out_tiled;
 };
 constexpr int GEMV_MAX_M = 64;      // token columns one fused projection handles
 constexpr int GV_RESID_ROWS = 1024;  // features per workgroup of the split-K residual epilogue
@@ -246,8 +251,9 @@ void launch_argmax_final(const float* val, const int32_t* idx, int nparts, int M
 // gathered through g_xrow; GV_SILU (out_t rows, interleaved gate/up W) or
 // GV_F32 (out_f32 rows).  false when a.M > 64.
 bool launch_gemv_grouped(const GemvArgs& a, int epi, int n_experts, hipStream_t s);
+// xg_tiled: xg in the tile order of the few-token projections (M <= 16)
 void launch_embed_ss(const int32_t* tok, const bf16* emb, const bf16* g, float* x, bf16* xg, float* ss_out, int M,
-                     int D, int V, hipStream_t s);
+                     int D, int V, hipStream_t s, bool xg_tiled = false);
 
 // ---- float32 few-token projections (k_gemv_f32.hip): float weights [N][K]
 // row-major (QKV rows in the rotation-pair order, gate/up interleaved in
@@ -325,11 +331,12 @@ int plan_decode_splits(int B, int kv_heads, int max_ctx);
 // p[0 .. n) = 0, as a kernel (graph-capture safe)
 void launch_zero_i32(int32_t* p, int n, hipStream_t s);
 // cnt: int32 [B][kv heads], zero before the launch and left zero after it
-// (split arrival counters).
+// (split arrival counters).  o_tiled (bf16, B <= 16, no rows): o [B][H hd]
+// in the tile order of the few-token projections (xt_off).
 template <typename T>
 void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* cnt, int B, int H, const int32_t* len,
                         int max_ctx, hipStream_t s, const int32_t* rows = nullptr,
-                        const int32_t* slots = nullptr);
+                        const int32_t* slots = nullptr, bool o_tiled = false);
 
 // ---- mixture of experts (k_moe.hip)
 // topi / topw [T][k]: the top_k experts of each token (E <= 256, k <= 8) from
