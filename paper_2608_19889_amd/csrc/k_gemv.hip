@@ -834,14 +834,15 @@ GvShape gemv_shape(int N, int K, int M, int epi) {
   }
   if (nb == 1) {
     // from timing every (rows, wavefronts, k-steps) candidate on weights
-    // streamed from HBM, 1B- and 7B-shaped layers at 8 and 16 tokens
+    // streamed from HBM, 1B- and 7B-shaped layers at 8 and 16 tokens (token
+    // operands in tile order)
     if (epi == GV_SILU) return {32, 8, 4, 1, 0};
     if (epi == GV_GELU) return {32, 4, 4, 1, 0};
-    if (epi == GV_HEAD) return {K <= 2048 ? 32 : 64, 8, 2, 1, 0};
+    if (epi == GV_HEAD) return {32, 8, 4, 1, 0};
     // QKV + RoPE: with a long K, 32-row tiles halve the token-operand reads
     // per weight byte (10.7 against 14.4 us on the 7B shape)
     if (epi == GV_ROPE) return K >= 3072 ? GvShape{32, 8, 4, 1, 0} : GvShape{16, 16, 4, 1, 0};
-    if (N / 16 < 192) return K >= 8192 ? GvShape{8, 8, 8, 1, 0} : GvShape{8, 16, 2, 1, 0};
+    if (N / 16 < 192) return K >= 2048 ? GvShape{8, 8, 8, 1, 0} : GvShape{8, 16, 2, 1, 0};
     return {16, 8, 4, 1, 0};
   }
   // 17..64 tokens: the row-splitting kernel (gemv_wide_kernel), whose token
@@ -910,7 +911,7 @@ static bool gv_dispatch(const GemvArgs& a, const GvShape& sh, int nb, hipStream_
   if constexpr (EPI == GV_SILU || EPI == GV_GELU) {
     AXON_GV(32, 4, 4, 1) AXON_GV(32, 8, 4, 1) AXON_GVW(128, 2, 2) AXON_GVW(64, 4, 3) AXON_GVW(64, 2, 4)
   } else if constexpr (EPI == GV_HEAD) {
-    AXON_GV(32, 8, 2, 1) AXON_GV(64, 8, 2, 1) AXON_GVW(128, 4, 2) AXON_GVW(128, 4, 3) AXON_GVW(128, 2, 4)
+    AXON_GV(32, 8, 4, 1) AXON_GVW(128, 4, 2) AXON_GVW(128, 4, 3) AXON_GVW(128, 2, 4)
   } else {
     AXON_GV(8, 16, 2, 1) AXON_GV(8, 8, 8, 1) AXON_GV(16, 8, 4, 1) AXON_GV(16, 16, 4, 1) AXON_GV(32, 8, 4, 1)
   }
