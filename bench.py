@@ -712,6 +712,13 @@ def summarize_counters(fetch_csv, write_csv, workload):
             a[0] += 1
             a[1] += float(r["Counter_Value"]) * 1024.0 * scale
             names.setdefault(role, name[name.index("gemv_fused_kernel"):name.index(">") + 1])
+        # one generate of this workload alone: each projection once per layer
+        # and decode step (a run that also held another model would mix them)
+        want = COUNTER_DECODE_STEPS * L
+        for role in ("qkv", "o", "gate/up", "down"):
+            if agg.get(role, [0])[0] != want:
+                raise SystemExit(f"{path}: {agg.get(role, [0])[0]} '{role}' dispatches, expected {want} "
+                                 f"({COUNTER_DECODE_STEPS} decode steps x {L} layers of the {workload} workload)")
         return scale, {k: v[1] / v[0] for k, v in agg.items()}, names
 
     fs, fetch, names = per_role(fetch_csv)
@@ -759,6 +766,7 @@ def summarize_counters(fetch_csv, write_csv, workload):
                         f"'gemv_fused|attn_decode|attn_combine|copyBuffer|elementwise_kernel' "
                         f"-f csv -d <dir> -o run -- python3 bench.py --workload {workload} --steps 1 --warmup 0 "
                         f"--decode-steps {COUNTER_DECODE_STEPS} --no-cpu-baseline --no-roofline --copy-calibration"
+                        + (" --no-7b" if workload == "1b" else "")
                         for c in ("FETCH_SIZE", "WRITE_SIZE")]}
     out = os.path.join(ROOT, "profiles", f"decode_gemv_{workload}_traffic.json")
     with open(out, "w") as f:
