@@ -42,6 +42,14 @@ BF16_CASES = {
     "qwen_hd128_g7_bias": ("7b", dict(layers=2, vocab=2048, hidden=896, intermediate=1792), [5, 129, 300], 6),
     "qwen32_hd128_g5_bias": ("32b", dict(layers=2, vocab=1500, hidden=640, intermediate=1280), [64, 257], 5),
     "smollm_hd64_g3": ("135m", dict(layers=3, vocab=1000, dtype="bf16"), [1, 31, 66, 90], 5),
+    # the decode projections' token operands in tile order (up to 16
+    # sequences): one sequence, and a full 16-token block; 17 sequences are
+    # the first batch with row-major operands
+    "llama_hd64_single": ("1b", dict(layers=2, vocab=3000, hidden=512, intermediate=1024), [77], 6),
+    "qwen_hd128_bias_batch16": ("7b", dict(layers=2, vocab=2048, hidden=896, intermediate=1792),
+                                [3 + (i * 37) % 90 for i in range(16)], 4),
+    "llama_hd64_batch17": ("1b", dict(layers=2, vocab=3000, hidden=512, intermediate=1024),
+                           [2 + (i * 29) % 61 for i in range(17)], 3),
     # 17..64 sequences: the row-splitting decode projections (gate/up, head)
     # and, for the narrow ones, K split over workgroups (partials + an
     # epilogue kernel), with 2, 3 and 4 token blocks; the long-K cases
