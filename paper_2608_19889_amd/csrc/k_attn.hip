@@ -19,17 +19,11 @@ namespace axon {
 
 constexpr float LOG2E = 1.4426950408889634f;
 
-// Page of position ``pos`` of ``slot`` for a wave-uniform (slot, pos): read
-// through the constant address space, so that it is a scalar load whose
-// wait does not hold up the wavefront's outstanding vector loads.  The page
-// table is not written while a kernel runs.
-AXON_DEV int64_t kv_page_uniform(const KVView& c, int slot, int pos) {
-  if (!c.bt) return slot;
-  typedef const __attribute__((address_space(4))) int32_t* cptr;
-  const cptr bt = (cptr)(uintptr_t)c.bt;
-  return bt[__builtin_amdgcn_readfirstlane(slot * c.bt_stride + pos / c.ps)];
-}
-// The same with the cache kind fixed at compile time (no branch on bt).
+// Page of position ``pos`` of ``slot`` for a wave-uniform (slot, pos), the
+// cache kind fixed at compile time (no branch on bt): read through the
+// constant address space, so that it is a scalar load whose wait does not
+// hold up the wavefront's outstanding vector loads.  The page table is not
+// written while a kernel runs.
 template <bool PAGED>
 AXON_DEV int64_t kv_page_of(const KVView& c, int slot, int pos) {
   if constexpr (!PAGED) {
@@ -192,7 +186,7 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
       int64_t gb[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g)
-        gb[g] = ((kv_page_uniform(kv, seq, j0 + g * 16) * kv.kv_heads + kvh) * kv.ps + (j0 + g * 16) % kv.ps) * HD;
+        gb[g] = ((kv_page_of<PAGED>(kv, seq, j0 + g * 16) * kv.kv_heads + kvh) * kv.ps + (j0 + g * 16) % kv.ps) * HD;
 #pragma unroll
       for (int i = 0; i < NKI; ++i) {
         if ((i * NW + wave) * 64 >= KT) break;  // wave-uniform
@@ -215,7 +209,7 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
     }
     int64_t pg[4];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) pg[g] = kv_page_uniform(kv, seq, min(j0 + g * 16, KL - 1) & ~15);
+    for (int g = 0; g < 4; ++g) pg[g] = kv_page_of<PAGED>(kv, seq, min(j0 + g * 16, KL - 1) & ~15);
 #pragma unroll
     for (int i = 0; i < NKI; ++i) {
       if ((i * NW + wave) * 64 >= KT) break;  // wave-uniform
