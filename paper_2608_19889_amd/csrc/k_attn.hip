@@ -144,7 +144,10 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
   // clamps every key to the last one.
   const bf16* kb = (const bf16*)kv.k;
   const bf16* vb = (const bf16*)kv.v;
-  constexpr int NKI = (KT / 64 + NW - 1) / NW, NVI = (VT / 64 + NW - 1) / NW;
+  // every wavefront issues the same number of load instructions per tile, so
+  // the loads and their waits are free of (scalar) branches
+  static_assert((KT / 64) % NW == 0 && (VT / 64) % NW == 0, "tiles split evenly over the wavefronts");
+  constexpr int NKI = KT / 64 / NW, NVI = VT / 64 / NW;
   int koff[NKI], kgrp[NKI], voff[NVI], vgrp[NVI];
 #pragma unroll
   for (int i = 0; i < NKI; ++i) {
@@ -168,14 +171,12 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
       const int64_t tb = (((int64_t)seq * kv.kv_heads + kvh) * kv.ps + j0) * HD;
 #pragma unroll
       for (int i = 0; i < NKI; ++i) {
-        if ((i * NW + wave) * 64 >= KT) break;  // wave-uniform
         __builtin_amdgcn_global_load_lds((const void*)(kb + tb + kgrp[i] * (16 * HD) + koff[i]),
                                          (__attribute__((address_space(3))) void*)(lds + b * BUF + (i * NW + wave) * 64),
                                          16, 0, 0);
       }
 #pragma unroll
       for (int i = 0; i < NVI; ++i) {
-        if ((i * NW + wave) * 64 >= VT) break;  // wave-uniform
         __builtin_amdgcn_global_load_lds(
             (const void*)(vb + tb + vgrp[i] * (16 * HD) + voff[i]),
             (__attribute__((address_space(3))) void*)(lds + b * BUF + KT + (i * NW + wave) * 64), 16, 0, 0);
@@ -189,7 +190,6 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
         gb[g] = ((kv_page_of<PAGED>(kv, seq, j0 + g * 16) * kv.kv_heads + kvh) * kv.ps + (j0 + g * 16) % kv.ps) * HD;
 #pragma unroll
       for (int i = 0; i < NKI; ++i) {
-        if ((i * NW + wave) * 64 >= KT) break;  // wave-uniform
         const int g = kgrp[i];
         const int64_t base = g == 0 ? gb[0] : g == 1 ? gb[1] : g == 2 ? gb[2] : gb[3];
         __builtin_amdgcn_global_load_lds((const void*)(kb + base + koff[i]),
@@ -198,7 +198,6 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
       }
 #pragma unroll
       for (int i = 0; i < NVI; ++i) {
-        if ((i * NW + wave) * 64 >= VT) break;  // wave-uniform
         const int g = vgrp[i];
         const int64_t base = g == 0 ? gb[0] : g == 1 ? gb[1] : g == 2 ? gb[2] : gb[3];
         __builtin_amdgcn_global_load_lds(
@@ -212,7 +211,6 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
     for (int g = 0; g < 4; ++g) pg[g] = kv_page_of<PAGED>(kv, seq, min(j0 + g * 16, KL - 1) & ~15);
 #pragma unroll
     for (int i = 0; i < NKI; ++i) {
-      if ((i * NW + wave) * 64 >= KT) break;  // wave-uniform
       const int p = (i * NW + wave) * 64 + lane;
       const int r = p / KCH, c = pswz<KCH>(r, p % KCH);  // pswz is its own inverse
       const int key = min(j0 + kappa(r), KL - 1);         // in [j0, j0 + 64): j0 < KL
@@ -225,7 +223,6 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
     }
 #pragma unroll
     for (int i = 0; i < NVI; ++i) {
-      if ((i * NW + wave) * 64 >= VT) break;  // wave-uniform
       const int p = (i * NW + wave) * 64 + lane;
       const int d = p / VCH, c = pswz<VCH>(d, p % VCH);
       const int key = min(j0 + c * 8, (KL - 1) & ~7);  // 8 keys of one 16-key group, in [j0, j0 + 64)
@@ -249,24 +246,14 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
   const int ntiles = (kend + PK - 1) / PK;
   // with a window, the first tile holding a key of the workgroup's first query
   const int kt0 = W ? max(0, base + q0 - W + 1) / PK : 0;
-  // this wavefront's load instructions per tile (its waits leave one tile in flight)
-  const int nld = (wave < KT / 64 ? (KT / 64 - wave + NW - 1) / NW : 0) + (wave < VT / 64 ? (VT / 64 - wave + NW - 1) / NW : 0);
   issue(kt0, kt0 % STG);
   if (kt0 + 1 < ntiles) issue(kt0 + 1, (kt0 + 1) % STG);
   for (int kt = kt0; kt < ntiles; ++kt) {
     const int j0 = kt * PK, b = kt % STG;
-    // tile kt landed for this wavefront (tile kt + 1 may still be in flight)
-    if (kt + 1 < ntiles) {
-      switch (nld) {  // wave-uniform; the counts the shapes produce
-        case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
-        case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
-        case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
-        case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
-        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-      }
-    } else {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    }
+    // tile kt landed for this wavefront (tile kt + 1, this wavefront's
+    // NKI + NVI load instructions, may still be in flight)
+    if (kt + 1 < ntiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NKI + NVI) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();  // tile kt landed for every wavefront; the buffer of tile kt - 1 is free
     if (kt + 2 < ntiles) issue(kt + 2, (kt + 2) % STG);
     const bf16x8* ks = lds + b * BUF;
