@@ -378,7 +378,9 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
   if (grp == 1) phase_barrier();  // group 1 runs one phase behind group 0
 
   bf16x8 fa[2][4], fb[2][2];
-  for (int kt = 0; kt < nk; ++kt) {
+  // one k-tile: do_issue -- issue the loads of k-tile kt + STAGES - 1;
+  // after -- k-tiles of this wavefront's loads left in flight by its wait
+  auto ktile = [&](int kt, bool do_issue, int after) {
     // ---- memory phase: fragments of k-tile kt, loads of k-tile kt+STAGES-1
     // into the buffer of k-tile kt-1, which both groups have read (group 1
     // in the phase that just ended)
@@ -399,11 +401,11 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
       }
     }
     const int kn = kt + STAGES - 1;
-    if (kn < nk) issue(kn % STAGES, kbase + kn * BK);
+    if (do_issue) issue(kn % STAGES, kbase + kn * BK);
     // group 1's share of k-tile kt+1 must land before group 0 reads it in
     // the phase after the coming barrier; group 0 waits for its own share at
     // the end of its compute phase
-    if (grp == 1) wait_tiles(min(STAGES - 2, nk - 2 - kt));
+    if (grp == 1) wait_tiles(after);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     phase_barrier();
     // ---- compute phase
@@ -416,9 +418,21 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
         for (int b = 0; b < 2; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][a], fb[ks][b], acc[a][b], 0, 0, 0);
     __builtin_amdgcn_s_setprio(0);
-    if (grp == 0) wait_tiles(min(STAGES - 2, nk - 2 - kt));
+    if (grp == 0) wait_tiles(after);
     phase_barrier();
-  }
+  };
+  // steady state with constant arguments (no scalar branches around the
+  // loads and waits: 1-3% on the 7B shapes), then the last STAGES - 1
+  // k-tiles, which issue nothing and leave fewer k-tiles in flight
+  static_assert(STAGES == 4, "the tail below peels STAGES - 1 k-tiles");
+  int kt = 0;
+  for (; kt + STAGES - 1 < nk; ++kt) ktile(kt, true, STAGES - 2);
+#pragma unroll
+  for (int j = 0; j < STAGES - 1; ++j)
+    if (kt < nk) {
+      ktile(kt, false, min(STAGES - 2, nk - 2 - kt));
+      ++kt;
+    }
   if (grp == 0) phase_barrier();  // same barrier count in both groups
 
   // SiLU epilogue staged through LDS (the ring is idle: every load has landed
