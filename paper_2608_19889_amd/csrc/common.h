@@ -25,6 +25,19 @@ AXON_DEV float gelu_tanh_f(float z) {
   return 0.5f * z * (2.f - 2.f / (__expf(2.f * u) + 1.f));
 }
 
+// The value that lane l ^ 32 (l ^ 16) of the wavefront holds, by the gfx950
+// permlane swaps: a register exchange between half-wavefronts (16-lane rows),
+// no LDS round trip as with ds_bpermute.  A swap of v with itself leaves
+// lane l the pair (its own value, the partner's) in half order.
+AXON_DEV float lane_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
+AXON_DEV float lane_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float((threadIdx.x & 16) ? r[0] : r[1]);
+}
+
 // Sum over the 64 lanes of a wavefront.
 AXON_DEV float wave_sum(float v) {
 #pragma unroll

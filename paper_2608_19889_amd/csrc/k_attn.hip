@@ -300,7 +300,7 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
 #pragma unroll
           for (int i = 0; i < 16; ++i) mloc = fmaxf(mloc, s[r][i]);
       }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * sc;  // scaled maximum of the tile
+      mloc = fmaxf(mloc, lane_xor32(mloc)) * sc;  // scaled maximum of the tile
       // raise the reference when the tile's maximum exceeds it by > 8
       const bool raise = mloc > m_run + 8.f;
       if (__builtin_amdgcn_ballot_w64(raise) != 0) {  // wave-uniform: rare after the first tiles
@@ -339,7 +339,7 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
   }
   const int myq = qw0 + (lane & 31);
   if (myq >= S) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float l_tot = l_run + lane_xor32(l_run);
   const float inv = 1.f / l_tot;
   // log2 of sum_k exp2(score_k * sc): what the backward pass recomputes its
   // probabilities from
@@ -465,8 +465,8 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
         s[blk][i] = v;
         mloc = fmaxf(mloc, v);
       }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    mloc = fmaxf(mloc, lane_xor16(mloc));
+    mloc = fmaxf(mloc, lane_xor32(mloc));
     const float m_new = fmaxf(m_run, mloc);  // finite: the first chunk holds a key in [lo, s1)
     const float alpha = exp2f(m_run - m_new);
     m_run = m_new;
@@ -515,8 +515,8 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
     for (int j = 0; j < NBUF; ++j) step(f[j], chunk(i + j));  // the last round: chunk(i) < s1
   }
   // per-wave statistics: m uniform over the 4 lane groups of a column; l summed
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
+  l_run += lane_xor16(l_run);
+  l_run += lane_xor32(l_run);
   if (gq == 0) {
     sm[wave * 16 + col] = m_run;
     sl[wave * 16 + col] = l_run;

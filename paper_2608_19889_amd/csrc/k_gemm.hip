@@ -75,7 +75,7 @@ AXON_DEV void rope_block(const EpiArgs& ep, int nb, int t, RopeTok tok, const f3
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       x[j] = v[g * 4 + j] + (float)bb[g][j];
-      xp[j] = __shfl_xor(x[j], 32, 64);
+      xp[j] = lane_xor32(x[j]);
     }
     if (rotate) {
       bf16x4 y;
