@@ -38,15 +38,35 @@ AXON_DEV float lane_xor16(float v) {
   return __uint_as_float((threadIdx.x & 16) ? r[0] : r[1]);
 }
 
-// Sum over the 64 lanes of a wavefront.
+// DPP lane moves within 16-lane rows: CTRL 0xB1 / 0x4E = quad_perm
+// [1,0,3,2] / [2,3,0,1] (lane l ^ 1, l ^ 2), 0x141 = row_half_mirror (lane j
+// of an 8-lane half <- 7 - j), 0x140 = row_mirror (lane j of a row <- 15 - j).
+template <int CTRL>
+AXON_DEV float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+// Sum / maximum over the 64 lanes of a wavefront, every lane the same
+// result: a butterfly of register moves (no LDS round trip).  After the l ^ 1
+// and l ^ 2 steps a value is uniform over its 4-lane group, so the half-row
+// mirror adds the other group of its 8 lanes (as l ^ 4 would) and, the value
+// then uniform over 8 lanes, the row mirror the other half of its row (as
+// l ^ 8 would); both operands of every add are the same pair in either lane.
 AXON_DEV float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  v += dpp_move<0xB1>(v);
+  v += dpp_move<0x4E>(v);
+  v += dpp_move<0x141>(v);
+  v += dpp_move<0x140>(v);
+  v += lane_xor16(v);
+  v += lane_xor32(v);
   return v;
 }
 AXON_DEV float wave_max(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  v = fmaxf(v, dpp_move<0xB1>(v));
+  v = fmaxf(v, dpp_move<0x4E>(v));
+  v = fmaxf(v, dpp_move<0x141>(v));
+  v = fmaxf(v, dpp_move<0x140>(v));
+  v = fmaxf(v, lane_xor16(v));
+  v = fmaxf(v, lane_xor32(v));
   return v;
 }
 
