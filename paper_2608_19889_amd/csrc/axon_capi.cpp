@@ -449,14 +449,18 @@ void release(axon_model* m) {
 }
 
 // ------------------------------------------------------------------ forward
+// xpair / opair: X / the bf16 output out_t in the row-pair layout (bf16 only)
 template <typename T>
 void gemm_many(axon_model* m, const void* W, const void* X, int N, int M, int K, int epi, float* out_f32,
-               void* out_t, int ldo, hipStream_t s, const EpiArgs* rope = nullptr, const void* bias = nullptr) {
+               void* out_t, int ldo, hipStream_t s, const EpiArgs* rope = nullptr, const void* bias = nullptr,
+               bool xpair = false, bool opair = false) {
   EpiArgs ep = rope ? *rope : EpiArgs{};
   if (bias) ep.bias = (const bf16*)bias;
   ep.out_f32 = out_f32;
   ep.out_t = out_t;
   ep.ldo = ldo;
+  ep.xpair = xpair ? 1 : 0;
+  ep.opair = opair ? 1 : 0;
   m->timed(1, N, M, K, s, [&] {
     if constexpr (sizeof(T) == 2)
       launch_gemm_bf16((const bf16*)W, (const bf16*)X, N, M, K, epi, ep, s);
@@ -500,18 +504,21 @@ int prefill_split(axon_model* m, int N, int M, int K) {
 
 // x += X W^T, then h = RMSNorm(x) g for ``rows`` rows (the last row of each
 // sequence when cu_last is set): a split-K GEMM's partials are summed into x
-// by the normalization kernel itself
+// by the normalization kernel itself.  xpair / hpair: X / h in the row-pair
+// layout.
 void gemm_resid_norm(axon_model* m, const void* W, const bf16* X, int T, int K, const bf16* g, bf16* h, int rows,
-                     const int32_t* cu_last, hipStream_t s, bool by_shape = false) {
+                     const int32_t* cu_last, hipStream_t s, bool by_shape = false, bool xpair = false,
+                     bool hpair = false) {
   const int D = m->D(), ks = by_shape ? prefill_split(m, D, T, K) : split_for(m, D, T, K);
   if (ks > 1) {
     m->timed(1, D, T, K, s, [&] {
-      launch_gemm_bf16_split((const bf16*)W, X, D, T, K, ks, m->gemm_part, (int64_t)T * D, s);
+      launch_gemm_bf16_split((const bf16*)W, X, D, T, K, ks, m->gemm_part, (int64_t)T * D, s, xpair);
     });
-    launch_resid_rmsnorm<bf16>(m->x, m->gemm_part, ks, (int64_t)T * D, g, h, rows, D, m->cfg.rms_eps, cu_last, s);
+    launch_resid_rmsnorm<bf16>(m->x, m->gemm_part, ks, (int64_t)T * D, g, h, rows, D, m->cfg.rms_eps, cu_last, s,
+                               hpair);
   } else {
-    gemm_many<bf16>(m, W, X, D, T, K, EPI_RESID, m->x, nullptr, D, s);
-    launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, g, h, rows, D, m->cfg.rms_eps, cu_last, s);
+    gemm_many<bf16>(m, W, X, D, T, K, EPI_RESID, m->x, nullptr, D, s, nullptr, nullptr, xpair);
+    launch_resid_rmsnorm<bf16>(m->x, nullptr, 0, 0, g, h, rows, D, m->cfg.rms_eps, cu_last, s, hpair);
   }
 }
 
@@ -654,12 +661,18 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
   if (plan) launch_set_step_lengths(d_cu, ent_slot, ent_base, m->d_len, B, s);
   else launch_set_lengths(d_cu, m->d_len, B, s);
   const bool gpt2 = m->gpt2();  // bf16 only (checked at init)
+  // dense Llama-family bf16 models pass the GEMMs' token operands (h, o, a) in
+  // the row-pair layout; o only when no single-token entry (decode attention
+  // writes row-major rows) shares the step
+  const bool xp = sizeof(T) == 2 && !gpt2 && !m->moe_model();
+  const bool o_pair = xp && !(plan && plan->nd > 0);
   if (gpt2)
     launch_embed_pos_ln(d_tokens, (const bf16*)m->embed, (const bf16*)m->wpe, (const bf16*)m->layers[0].gin,
                         (const bf16*)m->layers[0].gin_b, m->x, (bf16*)h, Ttok, D, V, m->cfg.max_positions, eps, d_cu,
                         B, ent_base, nullptr, s);
   else
-    launch_embed_rmsnorm<T>(d_tokens, (const T*)m->embed, (const T*)m->layers[0].gin, m->x, h, Ttok, D, V, eps, s);
+    launch_embed_rmsnorm<T>(d_tokens, (const T*)m->embed, (const T*)m->layers[0].gin, m->x, h, Ttok, D, V, eps, s,
+                            xp);
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const LayerW& w = m->layers[l];
     KVView kv = m->kv(l, m->paged());
@@ -669,7 +682,7 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
       EpiArgs re = rope_epi(m, w, kv, d_cu, B, nullptr);
       re.ent_slot = ent_slot;
       re.ent_base = ent_base;
-      gemm_many<T>(m, w.wqkv, h, nq, Ttok, D, EPI_ROPE, nullptr, nullptr, nq, s, &re);
+      gemm_many<T>(m, w.wqkv, h, nq, Ttok, D, EPI_ROPE, nullptr, nullptr, nq, s, &re, nullptr, xp);
     } else {
       gemm_many<T>(m, w.wqkv, h, nq, Ttok, D, EPI_F32, m->qkv, nullptr, nq, s);
       launch_rope_kv<T>(m->qkv, 1, 0, (const T*)w.bqkv, m->rope_cos, m->rope_sin, (T*)m->q, kv, Ttok, B, d_cu,
@@ -679,7 +692,7 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
       if (plan->nc > 0)
         m->timed(3, H, plan->nc, Ttok, s, [&] {
           launch_attn_prefill<T>((const T*)m->q, kv, (T*)m->o, Ttok, plan->nc, d_cu, h_cu, H, s, plan->d_chunks,
-                                 plan->h_chunks, ent_slot, ent_base);
+                                 plan->h_chunks, ent_slot, ent_base, nullptr, o_pair);
         });
       if (plan->nd > 0)
         m->timed(2, H, plan->nd, plan->dctx, s, [&] {
@@ -690,12 +703,13 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
       // prefill, and every entry of a float32 step (its kernel is per token)
       m->timed(3, H, B, Ttok, s, [&] {
         launch_attn_prefill<T>((const T*)m->q, kv, (T*)m->o, Ttok, B, d_cu, h_cu, H, s, nullptr, nullptr, ent_slot,
-                               ent_base);
+                               ent_base, nullptr, o_pair);
       });
     }
     const bool llama_bf16 = sizeof(T) == 2 && !gpt2;
     if (llama_bf16) {
-      gemm_resid_norm(m, w.wo, (const bf16*)m->o, Ttok, H * hd, (const bf16*)w.gpost, (bf16*)h, Ttok, nullptr, s, true);
+      gemm_resid_norm(m, w.wo, (const bf16*)m->o, Ttok, H * hd, (const bf16*)w.gpost, (bf16*)h, Ttok, nullptr, s, true,
+                      o_pair, xp);
     } else {
       gemm_many<T>(m, w.wo, m->o, D, Ttok, H * hd, EPI_RESID, m->x, nullptr, D, s, nullptr, w.bo);
       if (gpt2)
@@ -713,10 +727,10 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
       enqueue_moe(m, w, (const bf16*)h, Ttok, s);  // bf16 only (checked at init)
     } else {
       if constexpr (sizeof(T) == 2) {
-        gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_SILU, nullptr, m->a, I, s);
-        const bool to_last = last && !all_logits;
+        gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_SILU, nullptr, m->a, I, s, nullptr, nullptr, xp, xp);
+        const bool to_last = last && !all_logits;  // hlast: row-major rows for the head projection
         gemm_resid_norm(m, w.wd, (const bf16*)m->a, Ttok, I, (const bf16*)gnext, (bf16*)(to_last ? m->hlast : h),
-                        to_last ? B : Ttok, to_last ? d_cu : nullptr, s, true);
+                        to_last ? B : Ttok, to_last ? d_cu : nullptr, s, true, xp, xp && !to_last);
         normed = true;
       } else {
         gemm_many<T>(m, w.wgu, h, 2 * I, Ttok, D, EPI_F32, m->gu_f32, nullptr, 2 * I, s);
@@ -738,7 +752,7 @@ void enqueue_prefill(axon_model* m, int B, int Ttok, const int32_t* d_tokens, co
     }
   }
   if (all_logits) {
-    gemm_many<T>(m, m->lm_head, h, V, Ttok, D, EPI_F32, d_logits, nullptr, V, s);
+    gemm_many<T>(m, m->lm_head, h, V, Ttok, D, EPI_F32, d_logits, nullptr, V, s, nullptr, nullptr, xp);
     launch_argmax_rows(d_logits, B, V, d_next, d_cu, s);
   } else if (sizeof(T) == 2 && B <= GEMV_MAX_M) {
     GemvArgs ha{};
@@ -1390,11 +1404,13 @@ extern "C" int axon_init_model(const axon_config* cfg, const axon_weight* weight
     tmax = std::max<int64_t>(tmax, c.max_batch);
     m->rows = (int)tmax;
     TRY(dev_alloc(m, (void**)&m->x, tmax * D * 4));
-    TRY(dev_alloc(m, &m->h, tmax * D * esz));
+    // h, o and a may hold the row-pair layout: an even number of rows
+    const int64_t tpair = (tmax + 1) & ~(int64_t)1;
+    TRY(dev_alloc(m, &m->h, tpair * D * esz));
     if (!m->bf) TRY(dev_alloc(m, (void**)&m->qkv, tmax * nq * 4));  // bf16: RoPE is the QKV GEMM's epilogue
     TRY(dev_alloc(m, &m->q, tmax * H * hd * esz));
     // o, a and xg hold at least the 16 token rows of the tile order
-    const int64_t trows = std::max<int64_t>(tmax, XT_ROWS);
+    const int64_t trows = std::max<int64_t>(tpair, XT_ROWS);
     TRY(dev_alloc(m, &m->o, trows * H * hd * esz));
     const int64_t Ishared = (int64_t)c.n_shared_experts * c.moe_intermediate;
     TRY(dev_alloc(m, &m->a, trows * std::max<int64_t>(I, Ishared) * esz));

@@ -149,6 +149,16 @@ AXON_DEV int64_t v_el(const KVView& c, int slot, int kvh, int pos, int d) {
 AXON_DEV int64_t xt_off(int t, int64_t k) { return (k >> 5) * 512 + ((((k >> 3) & 3) << 4) + t) * 8 + (k & 7); }
 constexpr int XT_ROWS = 16;  // tokens of the tile order (one B fragment column block)
 
+// Row-pair layout of a bf16 token operand [T][K] (K a multiple of 32) of the
+// prefill GEMMs: rows 2p and 2p+1 are stored together in slices of 32 k values,
+// row 2p's slice then row 2p+1's, so that the two 64-byte pieces a 32-deep
+// k-tile takes from the pair fill one 128-byte line (row-major rows left every
+// such piece half a line, and the GEMM's tile loads ran 15-20% slower).  A
+// buffer of an odd row count holds one row more.
+AXON_DEV int64_t xp_off(int64_t t, int64_t k, int K) {
+  return ((t >> 1) * (K >> 5) + (k >> 5)) * 64 + (t & 1) * 32 + (k & 31);
+}
+
 // Element offset of W[n][8c .. 8c+7] (c = k-chunk index, k = 8c):
 AXON_DEV int64_t wt_chunk(int64_t n, int c, int K) {
   return (((n >> 4) * (K >> 5) + (c >> 2)) * 64 + (n & 15) + 16 * (c & 3)) * 8;

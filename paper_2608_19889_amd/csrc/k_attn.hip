@@ -76,7 +76,7 @@ template <int HD, bool PAGED>
 __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
     const bf16* __restrict__ q, KVView kv, bf16* __restrict__ o, int nseq, const int32_t* __restrict__ cu, int H,
     const int32_t* __restrict__ ents, const int32_t* __restrict__ ent_slot, const int32_t* __restrict__ ent_base,
-    float* __restrict__ lse) {
+    float* __restrict__ lse, int o_pair) {
   constexpr int NW = PREFILL_WAVES;      // wavefronts
   constexpr int KCH = HD / 8;            // 16-byte chunks per K row
   constexpr int VCH = PK / 8;            // chunks per V^T row (8)
@@ -344,12 +344,14 @@ __global__ void __launch_bounds__(64 * PREFILL_WAVES) attn_prefill_bf16_kernel(
   // log2 of sum_k exp2(score_k * sc): what the backward pass recomputes its
   // probabilities from
   if (lse && hl == 0) lse[(int64_t)(tok0 + myq) * H + head] = (m_run == -INFINITY ? 0.f : m_run) + __log2f(l_tot);
-  bf16* op = o + ((int64_t)(tok0 + myq) * H + head) * HD;
+  // 4 consecutive dims never cross a 32-dim slice of the row-pair layout
+  const int64_t trow = tok0 + myq;
+  bf16* op = o_pair ? o + xp_off(trow, (int64_t)head * HD, H * HD) : o + (trow * H + head) * HD;
 #pragma unroll
   for (int d = 0; d < HD / 32; ++d)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int dd = d * 32 + g * 8 + hl * 4;
+      const int dd = g * 8 + hl * 4 + (o_pair ? d * 64 : d * 32);  // a 32-dim slice every 64 elements in a pair
       *(bf16x4*)(op + dd) = bf16x4{(bf16)(acc_o[d][g * 4 + 0] * inv), (bf16)(acc_o[d][g * 4 + 1] * inv),
                                    (bf16)(acc_o[d][g * 4 + 2] * inv), (bf16)(acc_o[d][g * 4 + 3] * inv)};
     }
@@ -830,7 +832,7 @@ void launch_zero_i32(int32_t* p, int n, hipStream_t s) {
 template <typename T>
 void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, const int32_t* cu,
                          const int32_t* h_cu, int H, hipStream_t s, const int32_t* ents, const int32_t* h_ents,
-                         const int32_t* ent_slot, const int32_t* ent_base, float* lse) {
+                         const int32_t* ent_slot, const int32_t* ent_base, float* lse, bool o_pair) {
   if (T_tokens <= 0 || nseq <= 0) return;
   if constexpr (sizeof(T) == 4) {
     dim3 grid(T_tokens, H);
@@ -846,7 +848,9 @@ void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, co
       tiles += (h_cu[e + 1] - h_cu[e] + TQ - 1) / TQ;
     }
     const dim3 grid(tiles * H);  // the kernel maps the linear id to (tile, head)
-    auto go = [&](auto kern) { kern<<<grid, 64 * PREFILL_WAVES, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base, lse); };
+    auto go = [&](auto kern) {
+      kern<<<grid, 64 * PREFILL_WAVES, 0, s>>>(q, kv, o, nseq, cu, H, ents, ent_slot, ent_base, lse, o_pair ? 1 : 0);
+    };
     if (kv.hd == 64) {
       if (kv.bt) go(attn_prefill_bf16_kernel<64, true>);
       else go(attn_prefill_bf16_kernel<64, false>);
@@ -921,10 +925,10 @@ void launch_attn_decode(const T* q, KVView kv, T* o, float* part, int32_t* cnt, 
 
 template void launch_attn_prefill<float>(const float*, KVView, float*, int, int, const int32_t*, const int32_t*, int,
                                          hipStream_t, const int32_t*, const int32_t*, const int32_t*, const int32_t*,
-                                         float*);
+                                         float*, bool);
 template void launch_attn_prefill<bf16>(const bf16*, KVView, bf16*, int, int, const int32_t*, const int32_t*, int,
                                         hipStream_t, const int32_t*, const int32_t*, const int32_t*, const int32_t*,
-                                        float*);
+                                        float*, bool);
 template void launch_attn_decode<float>(const float*, KVView, float*, float*, int32_t*, int, int, const int32_t*,
                                         int, hipStream_t, const int32_t*, const int32_t*, bool);
 template void launch_attn_decode<bf16>(const bf16*, KVView, bf16*, float*, int32_t*, int, int, const int32_t*, int,

@@ -132,7 +132,8 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
       const int idx = tid + i * 256, row = idx >> 3, ch = idx & 7;
       const int n = n0 + row, m = m0 + row;
       ra[i] = n < N ? *(const bf16x8*)(W + wt_chunk(n, (k0 >> 3) + ch, K)) : zero8;
-      rb[i] = m < M ? *(const bf16x8*)(X + (int64_t)m * K + k0 + ch * 8) : zero8;
+      rb[i] = m < M ? *(const bf16x8*)(X + (ep.xpair ? xp_off(m, k0 + ch * 8, K) : (int64_t)m * K + k0 + ch * 8))
+                    : zero8;
     }
   };
   auto sstore = [&](int buf) {
@@ -197,7 +198,9 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const bf16* __restrict__
         rope_block(ep, nb, t, tok[b], acc[a][b], lane);
       } else if constexpr (EPI == EPI_SILU) {
         // rows nb..nb+15 are gate rows, nb+16..nb+31 the matching up rows
-        bf16* out = (bf16*)ep.out_t + (int64_t)t * ep.ldo + (nb / 32) * 16;
+        // (features (nb / 32) * 16 .. +15: inside one 32-feature slice)
+        const int64_t f0 = (nb / 32) * 16;
+        bf16* out = (bf16*)ep.out_t + (ep.opair ? xp_off(t, f0, ep.ldo) : (int64_t)t * ep.ldo + f0);
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
           const int f = g * 8 + (lane >> 5) * 4;
@@ -300,7 +303,9 @@ AXON_DEV void phase_barrier() {
 // expert e (g_toff[e] <= L / gx < g_toff[e+1]), covers its local rows
 // m0 .. m0+255 of M = g_off[e+1] - g_off[e], reads X row g_xrow[g_off[e] +
 // row] and writes output row g_off[e] + row.
-template <int EPI, bool GROUPED = false>
+// XP: X in the row-pair layout (xp_off), so a k-tile's two 64-byte pieces of a
+// row pair are one 128-byte line.
+template <int EPI, bool GROUPED = false, bool XP = false>
 __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __restrict__ W,
                                                                const bf16* __restrict__ X, int N, int M, int K,
                                                                EpiArgs ep) {
@@ -347,7 +352,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
       const bf16* ws = W + ((int64_t)(n >> 4) * rowblk + (int64_t)k0 * 16 + ((n & 15) + 16 * c) * 8);
       int64_t xr = m;
       if constexpr (GROUPED) xr = ep.g_xrow ? ep.g_xrow[rowbase + m] : rowbase + m;
-      const bf16* xs = X + xr * K + k0 + c * 8;
+      const bf16* xs = XP ? X + xp_off(xr, k0 + c * 8, K) : X + xr * K + k0 + c * 8;
       bf16x8* base = lds2 + stage * STAGE + (i * 8 + wave) * 64;
       __builtin_amdgcn_global_load_lds((const void*)ws, (__attribute__((address_space(3))) void*)base, 16, 0, 0);
       __builtin_amdgcn_global_load_lds((const void*)xs, (__attribute__((address_space(3))) void*)(base + PANEL),
@@ -461,10 +466,16 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
     __syncthreads();
     const int nf = min(128, (N - n0) / 2);  // N % 32 == 0
     for (int idx = tid; idx < 256 * 16; idx += 512) {
-      const int tl = idx >> 4, ch = idx & 15;
-      if (m0 + tl < M && ch * 8 < nf)
-        *(bf16x8*)((bf16*)ep.out_t + (int64_t)(rowbase + m0 + tl) * ep.ldo + n0 / 2 + ch * 8) =
+      // row-major output: 16 chunks of a token row in consecutive lanes; the
+      // row-pair layout: 8 lanes fill one 128-byte line (4 chunks of 32
+      // features of each row of a pair), then the pair's next 32 features
+      const int tl = ep.opair ? ((idx >> 5) << 1) | ((idx >> 2) & 1) : idx >> 4;
+      const int ch = ep.opair ? (((idx >> 3) & 3) << 2) | (idx & 3) : idx & 15;
+      if (m0 + tl < M && ch * 8 < nf) {
+        const int64_t t = rowbase + m0 + tl, f = n0 / 2 + ch * 8;
+        *(bf16x8*)((bf16*)ep.out_t + (ep.opair ? xp_off(t, f, ep.ldo) : t * ep.ldo + f)) =
             *(const bf16x8*)(st + tl * LD + ch * 8);
+      }
     }
     return;
   }
@@ -520,48 +531,50 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_256_kernel(const bf16* __res
   }
 }
 
-template <int EPI>
-static void launch_256(const bf16* W, const bf16* X, int N, int M, int K, const EpiArgs& ep, hipStream_t s) {
+// the 256 x 256 kernel instance, its LDS size raised at first use
+template <int EPI, bool GROUPED, bool XP>
+static auto kern_256() {
   static bool attr = false;
-  auto kern = gemm_bf16_256_kernel<EPI>;
+  auto kern = gemm_bf16_256_kernel<EPI, GROUPED, XP>;
   if (!attr) {
     (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, pf2::LDS_BYTES);
     attr = true;
   }
+  return kern;
+}
+
+template <int EPI, bool XP = false>
+static void launch_256(const bf16* W, const bf16* X, int N, int M, int K, const EpiArgs& ep, hipStream_t s) {
+  if constexpr (!XP) {
+    if (ep.xpair) {
+      if constexpr (EPI != EPI_GELU) launch_256<EPI, true>(W, X, N, M, K, ep, s);  // GELU: GPT-2, row-major only
+      return;
+    }
+  }
   const int tiles = ((N + pf2::BN - 1) / pf2::BN) * ((M + pf2::BM - 1) / pf2::BM);
-  klaunch(kern, dim3(tiles), dim3(512), pf2::LDS_BYTES, s, W, X, N, M, K, ep);
+  klaunch(kern_256<EPI, false, XP>(), dim3(tiles), dim3(512), pf2::LDS_BYTES, s, W, X, N, M, K, ep);
 }
 
 template <int EPI>
 static void launch_grouped(const bf16* W, const bf16* X, int N, int K, int max_rows, const EpiArgs& ep,
                            hipStream_t s) {
-  static bool attr = false;
-  auto kern = gemm_bf16_256_kernel<EPI, true>;
-  if (!attr) {
-    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, pf2::LDS_BYTES);
-    attr = true;
-  }
   // sum over experts of ceil(rows_e / 256) <= ceil(max_rows / 256) + E
   const int64_t mtiles = (max_rows + pf2::BM - 1) / pf2::BM + ep.g_E;
   const int64_t tiles = mtiles * ((N + pf2::BN - 1) / pf2::BN);
-  klaunch(kern, dim3((unsigned)tiles), dim3(512), pf2::LDS_BYTES, s, W, X, N, 0, K, ep);
+  klaunch(kern_256<EPI, true, false>(), dim3((unsigned)tiles), dim3(512), pf2::LDS_BYTES, s, W, X, N, 0, K, ep);
 }
 
 void launch_gemm_bf16_split(const bf16* W, const bf16* X, int N, int M, int K, int ksplit, float* part,
-                            int64_t part_stride, hipStream_t s) {
+                            int64_t part_stride, hipStream_t s, bool xpair) {
   if (M <= 0) return;
-  static bool attr = false;
-  auto kern = gemm_bf16_256_kernel<EPI_F32>;
-  if (!attr) {
-    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, pf2::LDS_BYTES);
-    attr = true;
-  }
   EpiArgs ep{};
   ep.out_f32 = part;
   ep.ldo = N;
   ep.part_stride = part_stride;
   const int tiles = ((N + pf2::BN - 1) / pf2::BN) * ((M + pf2::BM - 1) / pf2::BM);
-  klaunch(kern, dim3(tiles, ksplit), dim3(512), pf2::LDS_BYTES, s, W, X, N, M, K, ep);
+  const dim3 grid(tiles, ksplit);
+  if (xpair) klaunch(kern_256<EPI_F32, false, true>(), grid, dim3(512), pf2::LDS_BYTES, s, W, X, N, M, K, ep);
+  else klaunch(kern_256<EPI_F32, false, false>(), grid, dim3(512), pf2::LDS_BYTES, s, W, X, N, M, K, ep);
 }
 
 int gemm_ksplit(int N, int M, int K) {

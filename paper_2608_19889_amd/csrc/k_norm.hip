@@ -28,7 +28,7 @@ __global__ void __launch_bounds__(256) embed_rmsnorm_kernel(const int32_t* __res
                                                             const T* __restrict__ emb,
                                                             const T* __restrict__ g,
                                                             float* __restrict__ x, T* __restrict__ h,
-                                                            int D, int V, float eps) {
+                                                            int D, int V, float eps, int h_pair) {
   __shared__ float red[16];
   const int r = blockIdx.x;
   const int id = min(max(tok[r], 0), V - 1);  // ids outside [0, V) are clamped, never dereferenced
@@ -41,23 +41,24 @@ __global__ void __launch_bounds__(256) embed_rmsnorm_kernel(const int32_t* __res
   }
   ss = block_sum(ss, red);
   const float inv = rsqrtf(ss / (float)D + eps);
-  T* hr = h + (int64_t)r * D;
   for (int i = threadIdx.x * 4; i < D; i += blockDim.x * 4) {
     f32x4 v = load4(emb_at(emb, id, i, D)), gv = load4(g + i);
-    store4(hr + i, f32x4{v[0] * inv * gv[0], v[1] * inv * gv[1], v[2] * inv * gv[2], v[3] * inv * gv[3]});
+    store4(h + (h_pair ? xp_off(r, i, D) : (int64_t)r * D + i),
+           f32x4{v[0] * inv * gv[0], v[1] * inv * gv[1], v[2] * inv * gv[2], v[3] * inv * gv[3]});
   }
 }
 
 // Optionally x[r,:] += sum_s parts[s][r,:] (split-K partial products of the
 // projection that feeds the residual), then h[i,:] = rmsnorm(x[r,:]) * g with
-// r = i, or r = cu[i+1]-1 (last position of sequence i) when ``cu_last`` is set.
+// r = i, or r = cu[i+1]-1 (last position of sequence i) when ``cu_last`` is set;
+// h rows in the row-pair layout when h_pair is set (both kernels).
 template <typename T>
 __global__ void __launch_bounds__(256) resid_rmsnorm_kernel(float* __restrict__ x,
                                                             const float* __restrict__ parts,
                                                             int nparts, int64_t part_stride,
                                                             const T* __restrict__ g, T* __restrict__ h,
                                                             int D, float eps,
-                                                            const int32_t* __restrict__ cu_last) {
+                                                            const int32_t* __restrict__ cu_last, int h_pair) {
   __shared__ float red[16];
   const int i_out = blockIdx.x;
   const int r = cu_last ? cu_last[i_out + 1] - 1 : i_out;
@@ -76,10 +77,10 @@ __global__ void __launch_bounds__(256) resid_rmsnorm_kernel(float* __restrict__ 
   }
   ss = block_sum(ss, red);
   const float inv = rsqrtf(ss / (float)D + eps);
-  T* hr = h + (int64_t)i_out * D;
   for (int i = threadIdx.x * 4; i < D; i += blockDim.x * 4) {
     f32x4 v = load4(xr + i), gv = load4(g + i);
-    store4(hr + i, f32x4{v[0] * inv * gv[0], v[1] * inv * gv[1], v[2] * inv * gv[2], v[3] * inv * gv[3]});
+    store4(h + (h_pair ? xp_off(i_out, i, D) : (int64_t)i_out * D + i),
+           f32x4{v[0] * inv * gv[0], v[1] * inv * gv[1], v[2] * inv * gv[2], v[3] * inv * gv[3]});
   }
 }
 
@@ -134,16 +135,16 @@ __global__ void set_step_lengths_kernel(const int32_t* __restrict__ cu, const in
 
 template <typename T>
 void launch_embed_rmsnorm(const int32_t* tok, const T* emb, const T* g, float* x, T* h, int rows, int D, int V,
-                          float eps, hipStream_t s) {
+                          float eps, hipStream_t s, bool h_pair) {
   if (rows <= 0) return;
-  embed_rmsnorm_kernel<T><<<rows, 256, 0, s>>>(tok, emb, g, x, h, D, V, eps);
+  embed_rmsnorm_kernel<T><<<rows, 256, 0, s>>>(tok, emb, g, x, h, D, V, eps, h_pair ? 1 : 0);
 }
 
 template <typename T>
 void launch_resid_rmsnorm(float* x, const float* parts, int nparts, int64_t part_stride, const T* g, T* h,
-                          int rows, int D, float eps, const int32_t* cu_last, hipStream_t s) {
+                          int rows, int D, float eps, const int32_t* cu_last, hipStream_t s, bool h_pair) {
   if (rows <= 0) return;
-  resid_rmsnorm_kernel<T><<<rows, 256, 0, s>>>(x, parts, nparts, part_stride, g, h, D, eps, cu_last);
+  resid_rmsnorm_kernel<T><<<rows, 256, 0, s>>>(x, parts, nparts, part_stride, g, h, D, eps, cu_last, h_pair ? 1 : 0);
 }
 
 void launch_argmax(const float* logits, int rows, int V, int32_t* next, int32_t* len, hipStream_t s) {
@@ -168,12 +169,12 @@ void launch_set_step_lengths(const int32_t* cu, const int32_t* ent_slot, const i
 }
 
 template void launch_embed_rmsnorm<float>(const int32_t*, const float*, const float*, float*, float*, int, int,
-                                          int, float, hipStream_t);
+                                          int, float, hipStream_t, bool);
 template void launch_embed_rmsnorm<bf16>(const int32_t*, const bf16*, const bf16*, float*, bf16*, int, int, int,
-                                         float, hipStream_t);
+                                         float, hipStream_t, bool);
 template void launch_resid_rmsnorm<float>(float*, const float*, int, int64_t, const float*, float*, int, int,
-                                          float, const int32_t*, hipStream_t);
+                                          float, const int32_t*, hipStream_t, bool);
 template void launch_resid_rmsnorm<bf16>(float*, const float*, int, int64_t, const bf16*, bf16*, int, int,
-                                         float, const int32_t*, hipStream_t);
+                                         float, const int32_t*, hipStream_t, bool);
 
 }  // namespace axon

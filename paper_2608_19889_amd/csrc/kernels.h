@@ -71,6 +71,10 @@ struct EpiArgs {
   const int32_t* g_xrow;
   int64_t g_wstride;
   int g_E;
+  // row-pair layout (xp_off) of the token operand X, and of the bf16 output
+  // out_t of the SiLU epilogue; 0: row-major
+  int xpair;
+  int opair;
 };
 
 // ---- GPT-2 rows (k_layernorm.hip).  Token t is at position len[t] (decode)
@@ -137,13 +141,14 @@ void launch_embed_bwd(const int32_t* tok, const float* dx, int T, int D, int V, 
 // W [N][K] (K % 32 == 0) into dst of round_up(N, 16) * K elements
 void launch_tile_weight(const bf16* src, bf16* dst, int64_t N, int K, hipStream_t s);
 
-// ---- row kernels (k_norm.hip); a bf16 embedding table is fragment-tiled
+// ---- row kernels (k_norm.hip); a bf16 embedding table is fragment-tiled.
+// h_pair: h in the row-pair layout (xp_off; D % 32 == 0), else row-major.
 template <typename T>
 void launch_embed_rmsnorm(const int32_t* tok, const T* emb, const T* g, float* x, T* h, int rows, int D, int V,
-                          float eps, hipStream_t s);
+                          float eps, hipStream_t s, bool h_pair = false);
 template <typename T>
 void launch_resid_rmsnorm(float* x, const float* parts, int nparts, int64_t part_stride, const T* g, T* h,
-                          int rows, int D, float eps, const int32_t* cu_last, hipStream_t s);
+                          int rows, int D, float eps, const int32_t* cu_last, hipStream_t s, bool h_pair = false);
 void launch_argmax(const float* logits, int rows, int V, int32_t* next, int32_t* len, hipStream_t s);
 // argmax of row cu[i+1]-1 for each sequence i
 void launch_argmax_rows(const float* logits, int nseq, int V, int32_t* next, const int32_t* cu, hipStream_t s);
@@ -154,7 +159,8 @@ void launch_set_step_lengths(const int32_t* cu, const int32_t* ent_slot, const i
 
 // ---- projections (k_gemm.hip)
 // Many-token GEMM (prefill): bf16 MFMA tiles.  Requires K % 64 == 0, N % 32 == 0
-// (EPI_ROPE: the head dimension a multiple of 32).
+// (EPI_ROPE: the head dimension a multiple of 32).  ep.xpair: X in the row-pair
+// layout (xp_off); ep.opair: the SiLU epilogue's output in that layout.
 void launch_gemm_bf16(const bf16* W, const bf16* X, int N, int M, int K, int epi, const EpiArgs& ep,
                       hipStream_t s);
 // Grouped GEMM of the experts (ep.g_*): rows of all experts together at most
@@ -167,7 +173,7 @@ void launch_gemm_bf16_grouped(const bf16* W, const bf16* X, int N, int K, int ma
 // 32).  gemm_ksplit: the split worth taking for an output of few 256-tiles
 // (1: none).
 void launch_gemm_bf16_split(const bf16* W, const bf16* X, int N, int M, int K, int ksplit, float* part,
-                            int64_t part_stride, hipStream_t s);
+                            int64_t part_stride, hipStream_t s, bool xpair = false);
 int gemm_ksplit(int N, int M, int K);
 // out[i] (accumulate ? += : =) sum of parts[s * stride + i] over s in order (n % 4 == 0)
 void launch_sum_parts(float* out, const float* parts, int nparts, int64_t stride, int64_t n, int accumulate,
@@ -309,7 +315,8 @@ void launch_rope_kv(const float* parts, int nparts, int64_t part_stride, const T
                     const int32_t* ent_base = nullptr);
 
 // ---- attention (k_attn.hip)
-// Causal prefill attention over the cache; o [T][H*hd].  The workgroups cover
+// Causal prefill attention over the cache; o [T][H*hd] (bf16 with o_pair: in
+// the row-pair layout, xp_off with K = H*hd).  The workgroups cover
 // the nseq entries listed in ents (device) / h_ents (host copy), or entries
 // 0..nseq-1 when both are null; entry e's tokens cu[e] .. cu[e+1]-1 are at
 // positions ent_base[e] + 0, 1, ... of slot ent_slot[e] and attend to every
@@ -318,7 +325,7 @@ template <typename T>
 void launch_attn_prefill(const T* q, KVView kv, T* o, int T_tokens, int nseq, const int32_t* cu,
                          const int32_t* h_cu, int H, hipStream_t s, const int32_t* ents = nullptr,
                          const int32_t* h_ents = nullptr, const int32_t* ent_slot = nullptr,
-                         const int32_t* ent_base = nullptr, float* lse = nullptr);
+                         const int32_t* ent_base = nullptr, float* lse = nullptr, bool o_pair = false);
 // Decode attention: one query per slot at position len[b] (after the step's
 // key/value were written), context len[b] + 1; keys split over
 // plan_decode_splits() workgroups per (slot, kv head).  ``part`` holds
