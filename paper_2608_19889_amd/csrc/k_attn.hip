@@ -389,7 +389,6 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
   const int lo = kv.window ? max(0, ctx - kv.window) : 0;
   const int s0 = (lo & ~31) + split * split_len;
   const int s1 = min(ctx, s0 + split_len);
-  if (s0 >= ctx) return;
   const int group = H / kv.kv_heads;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, gq = lane >> 4;
@@ -501,10 +500,36 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
   // the running maximum is already finite from the round's first chunk) and
   // their loads read the clamped block.
   auto chunk = [&](int i) { return s0 + (wave + i * DNW) * 32; };
-  if (chunk(0) < s1) {  // wave-uniform
-    Frag f[NBUF];
+  // Contiguous cache without a window: the first chunk's address does not
+  // depend on the context length, so its loads are issued before that length
+  // has arrived (one memory round trip less per workgroup), clamped to the
+  // slot's positions (the cache is zeroed at allocation and holds only
+  // finite values); a chunk that reaches past the context is loaded again
+  // below with the context's clamping, so the result does not change.
+  Frag f[NBUF];
+  const bool spec = !PAGED && kv.window == 0;
+  if (spec) {
+    const int j0 = split * split_len + wave * 32;
 #pragma unroll
-    for (int j = 0; j < NBUF; ++j) load(f[j], chunk(j));
+    for (int blk = 0; blk < 2; ++blk) {
+      const int hs = min(j0 + blk * 16, kv.ps - 16);
+      const int64_t kbase = (((int64_t)slot * kv.kv_heads + kvh) * kv.ps + hs) * HD;
+      const bf16* kp = kb + kbase + lane * 8;
+#pragma unroll
+      for (int k = 0; k < HD / 32; ++k) f[0].k[blk][k] = *(const bf16x8*)(kp + k * 512);
+#pragma unroll
+      for (int d = 0; d < HD / 16; ++d) {
+        const bf16x4 v = *(const bf16x4*)(vb + kbase + (d * 16 + col) * 16 + gq * 4);
+        if (blk == 0) f[0].vlo[d] = v;
+        else f[0].vhi[d] = v;
+      }
+    }
+  }
+  if (s0 >= ctx) return;
+  if (chunk(0) < s1) {  // wave-uniform
+    if (!spec || chunk(0) + 32 > s1) load(f[0], chunk(0));
+#pragma unroll
+    for (int j = 1; j < NBUF; ++j) load(f[j], chunk(j));
     int i = 0;
     for (; chunk(i + NBUF) < s1; i += NBUF) {  // another round follows this one
 #pragma unroll
