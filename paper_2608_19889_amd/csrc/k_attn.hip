@@ -603,35 +603,58 @@ __global__ void __launch_bounds__(DNW * 64) attn_decode_bf16_kernel(const bf16* 
   for (int idx = threadIdx.x; idx < group * HD; idx += DNW * 64) {
     const int c = idx / HD, d = idx % HD, h = kvh * group + c;
     const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
-    // up to 8 splits' loads in flight per round; sums in split order
-    float M = -INFINITY;
-    for (int b0 = 0; b0 < nact; b0 += 8) {
-      float mv[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        mv[u] = __hip_atomic_load(pp + min(b0 + u, nact - 1) * (HD + 2) + HD, __ATOMIC_RELAXED,
-                                  __HIP_MEMORY_SCOPE_SYSTEM);
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (b0 + u < nact) M = fmaxf(M, mv[u]);
-    }
-    float L = 0.f, O = 0.f;
-    for (int b0 = 0; b0 < nact; b0 += 8) {
+    // sums in split order.  Up to 8 splits: every partial's (max, sum, o) in
+    // one round of independent loads, then the maximum and the sums from
+    // registers (7B decode attention 21.6 -> 20.8 us per layer); more
+    // splits: rounds of 8 for the maximum, then again for the sums
+    float M = -INFINITY, L = 0.f, O = 0.f;
+    if (nact <= 8) {
       float mv[8], lv[8], ov[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const float* ps = pp + min(b0 + u, nact - 1) * (HD + 2);
+        const float* ps = pp + min(u, nact - 1) * (HD + 2);
         mv[u] = __hip_atomic_load(ps + HD, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         lv[u] = __hip_atomic_load(ps + HD + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         ov[u] = __hip_atomic_load(ps + d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        if (b0 + u < nact) {
+        if (u < nact) M = fmaxf(M, mv[u]);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (u < nact) {
           const float f = exp2f(mv[u] - M);
           L += f * lv[u];
           O += f * ov[u];
         }
+    } else {
+      for (int b0 = 0; b0 < nact; b0 += 8) {
+        float mv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          mv[u] = __hip_atomic_load(pp + min(b0 + u, nact - 1) * (HD + 2) + HD, __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_SYSTEM);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (b0 + u < nact) M = fmaxf(M, mv[u]);
+      }
+      for (int b0 = 0; b0 < nact; b0 += 8) {
+        float mv[8], lv[8], ov[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float* ps = pp + min(b0 + u, nact - 1) * (HD + 2);
+          mv[u] = __hip_atomic_load(ps + HD, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          lv[u] = __hip_atomic_load(ps + HD + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          ov[u] = __hip_atomic_load(ps + d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (b0 + u < nact) {
+            const float f = exp2f(mv[u] - M);
+            L += f * lv[u];
+            O += f * ov[u];
+          }
+      }
     }
     o[o_tiled ? xt_off(row, h * HD + d) : ((int64_t)row * H + h) * HD + d] = (bf16)(O / L);
   }
