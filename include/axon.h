@@ -217,10 +217,12 @@ int axon_decode_step(axon_model* m, int32_t batch, const int32_t* d_tokens, floa
  * need more than the array is refused with AXON_E_CAPACITY (the message gives
  * the bytes needed); AXON_E_HIP if the array's address could not be obtained
  * at init.  Nothing is enqueued on failure.  All calls on one GPU share its
- * array, which keeps the last call's contents (every buffer is written before
- * it is read within a step, so nothing needs clearing); calls that overlap in
- * time on one GPU -- from two streams or threads, on any models -- race on it
- * and must be serialized by the caller. */
+ * array, which keeps the last call's contents: each call first clears, with a
+ * fill kernel on ``stream``, the counters of the decode attention's split
+ * merge (the only part that must start at zero; every other buffer is written
+ * before it is read within a step); calls that overlap in time on one GPU --
+ * from two streams or threads, on any models -- race on it and must be
+ * serialized by the caller. */
 #define AXON_NOALLOC_SCRATCH_BYTES (64u << 20)
 int axon_decode_step_noalloc(axon_model* m, int32_t batch, const int32_t* d_tokens, float* d_logits,
                              int32_t* d_next_tokens, void* stream);
