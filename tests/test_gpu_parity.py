@@ -107,6 +107,32 @@ def test_long_context_split_merge():
     m.close()
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_sixteen_query_heads_per_kv_head(dtype):
+    """16 query heads share one kv head: the most that one bf16 decode
+    attention workgroup serves (the 16 columns of its MFMA tiles), here with
+    the keys of the 700-token sequence split in two; in float32, more than
+    the grouped float32 decode kernel takes (8), so each head runs on its
+    own.  The width of the query heads (16 x 64) differs from the hidden
+    size (576)."""
+    shape = dict(small_shape("135m", layers=2, vocab=1000, dtype=dtype), num_attention_heads=16,
+                 num_key_value_heads=1)
+    w = model_weights(shape, seed=5)
+    seqs = _ragged(shape["vocab_size"], [9, 150, 700], seed=6)
+    steps = 5
+    ref_tok, ref_lg = oracle_greedy(shape, w, seqs, steps)
+    m = gpu_model(shape, w, max_batch=3, max_seq=1040)
+    lg, _ = run_teacher_forced(m, seqs, ref_tok[:, :steps])
+    if dtype == "bf16":
+        ref_b = oracle_bf16_storage(shape, w, seqs, ref_tok[:, :steps])
+        mx = check_bf16(lg, ref_lg, ref_b, "16 query heads per kv head")
+        check_argmax(lg, ref_lg, mx, "16 query heads per kv head")
+    else:
+        check_logits(lg, ref_lg, F32_MAX, None, "16 query heads per kv head, float32")
+        np.testing.assert_array_equal(run_free(m, seqs, steps), ref_tok)
+    m.close()
+
+
 def test_f32_check_mode_on_bf16_valued_weights():
     """The paper's fallback precision: the same bf16-valued weights held in
     float32 must reproduce the oracle's logits to 1e-4 and its greedy tokens."""
