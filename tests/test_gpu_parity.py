@@ -107,16 +107,19 @@ def test_long_context_split_merge():
     m.close()
 
 
+@pytest.mark.parametrize("base,heads,kv_heads", [("135m", 16, 1), ("7b", 24, 2)], ids=["hd64_g16", "hd128_bias_g12"])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_sixteen_query_heads_per_kv_head(dtype):
-    """16 query heads share one kv head: the most that one bf16 decode
-    attention workgroup serves (the 16 columns of its MFMA tiles), here with
-    the keys of the 700-token sequence split in two; in float32, more than
-    the grouped float32 decode kernel takes (8), so each head runs on its
-    own.  The width of the query heads (16 x 64) differs from the hidden
-    size (576)."""
-    shape = dict(small_shape("135m", layers=2, vocab=1000, dtype=dtype), num_attention_heads=16,
-                 num_key_value_heads=1)
+def test_wide_query_groups(dtype, base, heads, kv_heads):
+    """The widest query groups the library takes: 16 query heads of 64 dims
+    per kv head (the 16 columns of the bf16 decode attention's MFMA tiles)
+    and 12 of 128 (group x head_dim = 1536, the limit), here with the keys
+    of the 700-token sequence split in two; in float32, more than the
+    grouped float32 decode kernel takes (8), so each head runs on its own.
+    The width of the query heads (16 x 64, 24 x 128) differs from the hidden
+    size (576, 896)."""
+    ov = dict(intermediate=1792, hidden=896) if base == "7b" else {}
+    shape = dict(small_shape(base, layers=2, vocab=1000, dtype=dtype, **ov), num_attention_heads=heads,
+                 num_key_value_heads=kv_heads)
     w = model_weights(shape, seed=5)
     seqs = _ragged(shape["vocab_size"], [9, 150, 700], seed=6)
     steps = 5
@@ -125,10 +128,10 @@ def test_sixteen_query_heads_per_kv_head(dtype):
     lg, _ = run_teacher_forced(m, seqs, ref_tok[:, :steps])
     if dtype == "bf16":
         ref_b = oracle_bf16_storage(shape, w, seqs, ref_tok[:, :steps])
-        mx = check_bf16(lg, ref_lg, ref_b, "16 query heads per kv head")
-        check_argmax(lg, ref_lg, mx, "16 query heads per kv head")
+        mx = check_bf16(lg, ref_lg, ref_b, "wide query groups")
+        check_argmax(lg, ref_lg, mx, "wide query groups")
     else:
-        check_logits(lg, ref_lg, F32_MAX, None, "16 query heads per kv head, float32")
+        check_logits(lg, ref_lg, F32_MAX, None, "wide query groups, float32")
         np.testing.assert_array_equal(run_free(m, seqs, steps), ref_tok)
     m.close()
 
