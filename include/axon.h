@@ -65,7 +65,7 @@ typedef struct {
   int32_t hidden;         /* D; multiple of 64 */
   int32_t n_layers;       /* L >= 1 */
   int32_t n_heads;        /* H; a multiple of n_kv_heads */
-  int32_t n_kv_heads;     /* KV; H / KV <= 16 */
+  int32_t n_kv_heads;     /* KV; H / KV <= 16 and (H / KV) * head_dim <= 1536 */
   int32_t head_dim;       /* hd; 64 or 128 */
   int32_t intermediate;   /* I; multiple of 64 */
   int32_t vocab;          /* V >= 1 */

@@ -103,6 +103,9 @@ def test_group_size_limit_and_paged_needs_pages():
     s = _shape()
     rc, msg = _status(s, _fake_weights(s), override={"n_heads": 34, "n_kv_heads": 2})
     assert rc == axon.AXON_E_INVALID and "<= 16" in msg
+    # 13 query heads of 128 dims per kv head: within 16 heads, past 1536 dims
+    rc, msg = _status(s, _fake_weights(s), override={"n_heads": 26, "n_kv_heads": 2, "head_dim": 128})
+    assert rc == axon.AXON_E_INVALID and "1536" in msg
     rc, msg = _status(s, _fake_weights(s), page_size=16, num_pages=0)
     assert rc == axon.AXON_E_INVALID and "kv_num_pages" in msg
 
